@@ -1,0 +1,119 @@
+/*
+ * nestquant.h -- C ABI of the MI355X NestQuant coded-GEMM library (libnestquant.so).
+ *
+ * NestQuant (Savkin, Porat, Ordentlich, Polyanskiy, arXiv 2502.09720) quantizes every row
+ * of a matrix with a union of k scaled Voronoi codes of the Gosset lattice E8 and
+ * computes matrix products from the codes.  This library implements, for one AMD
+ * Instinct MI355X (gfx950):
+ *
+ *   nq_encode  -- Sec. 4.2, Alg. 3 (row quantizer) with the First-beta strategy of App. F,
+ *                 built on Alg. 1 (Voronoi encode) and App. C, Alg. 5 (nearest E8 point);
+ *   nq_decode  -- Alg. 2 (Voronoi decode) scaled back by beta and the row scale;
+ *   nq_matmul  -- C = A_hat * W_hat^T from two coded operands, i.e. Alg. 4 (dot product of
+ *                 coded vectors) for every pair of rows, as one dense contraction.
+ *
+ * Storage of a coded matrix with `rows` rows of `cols` entries (cols % 8 == 0):
+ *   codes    uint32[rows][cols/8]           block j of row i: code c_l (0 <= c_l < q) of
+ *                                           entry 8j+l in bits 4l..4l+3 (App. E packs the
+ *                                           eight codes of a block into one 32-bit word);
+ *   beta_idx uint32[rows][ceil(cols/128)]   two bits per block: (t - 1) of block j in bits
+ *                                           2*(j%16) of word j/16 (App. E: 2-bit indices
+ *                                           into a dictionary of four betas);
+ *   scales   float[rows]                    r = ||row||_2 / sqrt(cols), the fp32 number
+ *                                           nearest to the exact value (Alg. 3's s/sqrt(n)).
+ * The value coded for entry 8j+l is  r * beta_t * p_l  with beta_t = t * base and p the
+ * decoded E8 point; beta_t = t * base for t = 1..k is the beta dictionary (App. F).
+ *
+ * Conventions for every call:
+ *   - all array pointers are device pointers, owned by the caller; the library allocates
+ *     nothing and keeps no per-call state;
+ *   - calls are asynchronous on `hip_stream` (a hipStream_t; NULL = the null stream) and
+ *     may be issued from several host threads;
+ *   - arguments are checked on the host before anything is launched: on any error the
+ *     call returns the status, launches nothing and writes nothing; nq_last_error() then
+ *     describes the failure (per host thread);
+ *   - rows == 0 (or M == 0 / N == 0) is a no-op returning NQ_OK.
+ */
+#ifndef NESTQUANT_H
+#define NESTQUANT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  NQ_OK = 0,
+  NQ_ERR_INVALID_ARG = 1,  /* a size, stride, pointer or parameter is out of range   */
+  NQ_ERR_UNSUPPORTED = 2,  /* valid in principle but not implemented (e.g. dtype)    */
+  NQ_ERR_HIP = 3           /* the HIP runtime reported an error at launch            */
+} nq_status;
+
+typedef enum { NQ_F32 = 0, NQ_F16 = 1, NQ_BF16 = 2 } nq_dtype;
+
+/* Quantizer parameters (Sec. 4.2, App. F):
+ *   q    nesting ratio, 2 <= q <= 16 (codes are nibbles);
+ *   k    number of betas, 1 <= k <= 4 (2-bit beta indices);
+ *   base beta_t = t * base for t = 1..k; finite, > 0, and large enough that
+ *        sqrt(cols) / base < 2^21 (bounds the lattice input |y| <= sqrt(cols) / base).
+ *        The paper's grid "k betas uniform on [0, 10] / q" is base = 10 / (k q). */
+typedef struct {
+  int32_t q;
+  int32_t k;
+  double base;
+} nq_params;
+
+/* Alg. 3 + First-beta (App. F) on each row of x.
+ *   x        device, rows x cols of dtype x_dtype (NQ_F32, NQ_F16 or NQ_BF16), row i at
+ *            x + i*ld_x elements; ld_x >= cols; cols % 8 == 0, 8 <= cols <= 65536.
+ *   codes    device, nq_codes_words(rows, cols) uint32 (output);
+ *   beta_idx device, nq_beta_words(rows, cols) uint32 (output);
+ *   scales   device, rows floats (output).
+ * Per row: r = RMS; for every 8-block, for t = 1..k the block y = fl32(x * c_t) with
+ * c_t = fl32(1 / fl64(r * fl64(t * base))) is rounded to the nearest E8 point (Alg. 5;
+ * ties: exact halves round down, lowest index on argmin/argmax ties, equal D8 / D8+1/2
+ * distances pick D8+1/2); the first t whose point survives decode(encode(.)) (no
+ * overload, Sec. 4.1) is kept, else t = k.  A zero row gives r = 0, codes 0, index 0.
+ * Non-finite inputs give unspecified (but in-range) codes. */
+nq_status nq_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t rows,
+                    int64_t cols, int64_t ld_x, uint32_t* codes, uint32_t* beta_idx,
+                    float* scales, void* hip_stream);
+
+/* Alg. 2 and the inverse scaling: out[i][8j+l] = r_i * (t_ij * base) * X2_l / 2 where X2
+ * is the decoded point of block j in 2E8 units (App. E).  out is rows x cols of out_dtype,
+ * row i at out + i*ld_out elements, ld_out >= cols.  Each value is the fp64 product rounded
+ * once to fp32 (and, for NQ_F16 / NQ_BF16, from there to the 16-bit type). */
+nq_status nq_decode(const nq_params* p, const uint32_t* codes, const uint32_t* beta_idx,
+                    const float* scales, int64_t rows, int64_t cols, void* out,
+                    nq_dtype out_dtype, int64_t ld_out, void* hip_stream);
+
+/* C = A_hat * W_hat^T (Alg. 4 for every row pair), fp32 output.
+ *   A: M x K coded with parameters pa; W: N x K coded with parameters pw (q, k and base
+ *   may differ between the operands; K must be the same);  K % 8 == 0.
+ *   c: device, M x N floats, row i at c + i*ldc, ldc >= N.
+ * C_ij = r_Ai r_Wj base_A base_W / 4 * sum_blocks <t_A X2_A, t_W X2_W>; the integer tiles
+ * t*X2 are exact in bf16 and contracted with fp32 accumulation. */
+nq_status nq_matmul(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,
+                    const float* a_scales, int64_t M, const nq_params* pw,
+                    const uint32_t* w_codes, const uint32_t* w_beta, const float* w_scales,
+                    int64_t N, int64_t K, float* c, int64_t ldc, void* hip_stream);
+
+/* Sizes of the code and beta-index arrays for a rows x cols matrix (-1 if invalid). */
+int64_t nq_codes_words(int64_t rows, int64_t cols);
+int64_t nq_beta_words(int64_t rows, int64_t cols);
+
+/* Static description of a status code. */
+const char* nq_status_string(nq_status s);
+
+/* Message describing the last failed call on this host thread ("" if none). */
+const char* nq_last_error(void);
+
+/* Library version as MAJOR*10000 + MINOR*100 + PATCH. */
+int32_t nq_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* NESTQUANT_H */

@@ -1,0 +1,20 @@
+"""NestQuant coded GEMM on AMD Instinct MI355X (gfx950).
+
+A thin Python layer over libnestquant.so (C ABI in include/nestquant.h): it marshals torch
+device tensors and the current HIP stream into the C calls.  All arithmetic of the method
+runs in the library's HIP kernels; there is no CPU fallback, and every call raises if the
+library has not been built.
+"""
+
+from .binding import (  # noqa: F401
+    Coded,
+    NQError,
+    decode,
+    default_base,
+    encode,
+    library,
+    library_path,
+    matmul,
+    nq_beta_words,
+    nq_codes_words,
+)

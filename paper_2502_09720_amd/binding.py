@@ -1,0 +1,165 @@
+"""ctypes binding of libnestquant.so: argument marshalling only.
+
+Device memory and streams come from torch; each function passes raw device pointers and
+the current stream's handle to the matching C entry point and checks its status.
+"""
+
+import ctypes
+import os
+from typing import NamedTuple
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+_LIB = None
+
+NQ_OK, NQ_ERR_INVALID_ARG, NQ_ERR_UNSUPPORTED, NQ_ERR_HIP = 0, 1, 2, 3
+NQ_F32, NQ_F16, NQ_BF16 = 0, 1, 2
+
+
+class NQError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"{message} (status {status})")
+        self.status = status
+
+
+class _Params(ctypes.Structure):
+    _fields_ = [("q", ctypes.c_int32), ("k", ctypes.c_int32), ("base", ctypes.c_double)]
+
+
+def library_path():
+    return os.environ.get("NESTQUANT_LIB", os.path.join(PKG, "libnestquant.so"))
+
+
+def library():
+    """Load libnestquant.so (raises if it has not been built)."""
+    global _LIB
+    if _LIB is None:
+        path = library_path()
+        if not os.path.exists(path):
+            raise RuntimeError(
+                f"{path} is missing: build it with `python -m paper_2502_09720_amd.build`")
+        lib = ctypes.CDLL(path)
+        vp, i64, u32p, f32p = ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p
+        pp = ctypes.POINTER(_Params)
+        lib.nq_encode.argtypes = [pp, vp, ctypes.c_int, i64, i64, i64, u32p, u32p, f32p, vp]
+        lib.nq_decode.argtypes = [pp, u32p, u32p, f32p, i64, i64, vp, ctypes.c_int, i64, vp]
+        lib.nq_matmul.argtypes = [pp, u32p, u32p, f32p, i64, pp, u32p, u32p, f32p, i64, i64,
+                                  f32p, i64, vp]
+        for f in ("nq_encode", "nq_decode", "nq_matmul"):
+            getattr(lib, f).restype = ctypes.c_int
+        lib.nq_codes_words.argtypes = [i64, i64]
+        lib.nq_codes_words.restype = i64
+        lib.nq_beta_words.argtypes = [i64, i64]
+        lib.nq_beta_words.restype = i64
+        lib.nq_status_string.argtypes = [ctypes.c_int]
+        lib.nq_status_string.restype = ctypes.c_char_p
+        lib.nq_last_error.argtypes = []
+        lib.nq_last_error.restype = ctypes.c_char_p
+        lib.nq_version.argtypes = []
+        lib.nq_version.restype = ctypes.c_int32
+        _LIB = lib
+    return _LIB
+
+
+def _check(status):
+    if status != NQ_OK:
+        lib = library()
+        raise NQError(status, lib.nq_last_error().decode() or lib.nq_status_string(status).decode())
+
+
+def default_base(q, k):
+    """beta_t = t * base with the k betas uniform on [0, 10] / q."""
+    return 10.0 / (k * q)
+
+
+def _params(q, k, base):
+    return _Params(int(q), int(k), float(default_base(q, k) if base is None else base))
+
+
+def _stream(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _dtype_code(dt):
+    import torch
+    return {torch.float32: NQ_F32, torch.float16: NQ_F16, torch.bfloat16: NQ_BF16}[dt]
+
+
+def nq_codes_words(rows, cols):
+    return library().nq_codes_words(rows, cols)
+
+
+def nq_beta_words(rows, cols):
+    return library().nq_beta_words(rows, cols)
+
+
+class Coded(NamedTuple):
+    """A coded matrix: uint32 code words (stored in an int32 tensor), uint32 beta words,
+    fp32 row scales, and the quantizer parameters."""
+    codes: "object"
+    beta: "object"
+    scales: "object"
+    rows: int
+    cols: int
+    q: int
+    k: int
+    base: float
+
+
+def encode(x, q=14, k=4, base=None, stream=None, out=None):
+    """nq_encode on a 2-D cuda tensor (fp32 / fp16 / bf16, unit stride along rows)."""
+    import torch
+    if x.dim() != 2 or x.stride(1) != 1 or not x.is_cuda:
+        raise ValueError("x must be a 2-D cuda tensor with unit column stride")
+    rows, cols = x.shape
+    lib = library()
+    nw, bw = lib.nq_codes_words(rows, cols), lib.nq_beta_words(rows, cols)
+    if nw < 0:
+        raise ValueError("cols must be a positive multiple of 8")
+    if out is None:
+        codes = torch.empty(nw, dtype=torch.int32, device=x.device)
+        beta = torch.empty(bw, dtype=torch.int32, device=x.device)
+        scales = torch.empty(rows, dtype=torch.float32, device=x.device)
+    else:
+        codes, beta, scales = out
+    p = _params(q, k, base)
+    _check(lib.nq_encode(ctypes.byref(p), ctypes.c_void_p(x.data_ptr()), _dtype_code(x.dtype),
+                         rows, cols, x.stride(0), ctypes.c_void_p(codes.data_ptr()),
+                         ctypes.c_void_p(beta.data_ptr()), ctypes.c_void_p(scales.data_ptr()),
+                         _stream(stream)))
+    return Coded(codes, beta, scales, rows, cols, int(q), int(k), p.base)
+
+
+def decode(coded, out_dtype=None, stream=None, out=None):
+    """nq_decode: the reconstruction r * beta_t * p as a rows x cols tensor."""
+    import torch
+    dt = torch.float32 if out_dtype is None else out_dtype
+    if out is None:
+        out = torch.empty(coded.rows, coded.cols, dtype=dt, device=coded.codes.device)
+    p = _params(coded.q, coded.k, coded.base)
+    lib = library()
+    _check(lib.nq_decode(ctypes.byref(p), ctypes.c_void_p(coded.codes.data_ptr()),
+                         ctypes.c_void_p(coded.beta.data_ptr()),
+                         ctypes.c_void_p(coded.scales.data_ptr()), coded.rows, coded.cols,
+                         ctypes.c_void_p(out.data_ptr()), _dtype_code(out.dtype), out.stride(0),
+                         _stream(stream)))
+    return out
+
+
+def matmul(a, w, stream=None, out=None):
+    """nq_matmul: C = A_hat W_hat^T (fp32, M x N) from two coded operands."""
+    import torch
+    if a.cols != w.cols:
+        raise ValueError("K mismatch")
+    if out is None:
+        out = torch.empty(a.rows, w.rows, dtype=torch.float32, device=a.codes.device)
+    pa, pw = _params(a.q, a.k, a.base), _params(w.q, w.k, w.base)
+    lib = library()
+    _check(lib.nq_matmul(ctypes.byref(pa), ctypes.c_void_p(a.codes.data_ptr()),
+                         ctypes.c_void_p(a.beta.data_ptr()), ctypes.c_void_p(a.scales.data_ptr()),
+                         a.rows, ctypes.byref(pw), ctypes.c_void_p(w.codes.data_ptr()),
+                         ctypes.c_void_p(w.beta.data_ptr()), ctypes.c_void_p(w.scales.data_ptr()),
+                         w.rows, a.cols, ctypes.c_void_p(out.data_ptr()), out.stride(0),
+                         _stream(stream)))
+    return out

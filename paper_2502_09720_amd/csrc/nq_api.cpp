@@ -1,0 +1,159 @@
+// C ABI of libnestquant.so: argument checking and dispatch to the kernels.
+// The declarations and their contracts are in include/nestquant.h.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+
+#include "nestquant.h"
+#include "nq_kernels.hpp"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+nq_status fail(nq_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+nq_status ok() {
+  g_last_error[0] = '\0';
+  return NQ_OK;
+}
+
+constexpr int64_t kMaxCols = 65536;
+constexpr int64_t kMaxRows = (int64_t)1 << 31;
+
+nq_status check_params(const nq_params* p, int64_t cols, const char* who) {
+  if (!p) return fail(NQ_ERR_INVALID_ARG, "%s: params is NULL", who);
+  if (p->q < 2 || p->q > 16) return fail(NQ_ERR_INVALID_ARG, "%s: q=%d outside [2,16]", who, p->q);
+  if (p->k < 1 || p->k > 4) return fail(NQ_ERR_INVALID_ARG, "%s: k=%d outside [1,4]", who, p->k);
+  if (!std::isfinite(p->base) || !(p->base > 0.0))
+    return fail(NQ_ERR_INVALID_ARG, "%s: base must be finite and > 0", who);
+  if (std::sqrt((double)cols) / p->base >= 2097152.0)
+    return fail(NQ_ERR_INVALID_ARG, "%s: base too small for cols=%lld (sqrt(cols)/base >= 2^21)",
+                who, (long long)cols);
+  return NQ_OK;
+}
+
+nq_status check_cols(int64_t cols, const char* who) {
+  if (cols < 8 || cols % 8 != 0 || cols > kMaxCols)
+    return fail(NQ_ERR_INVALID_ARG, "%s: cols=%lld must be a multiple of 8 in [8, %lld]", who,
+                (long long)cols, (long long)kMaxCols);
+  return NQ_OK;
+}
+
+size_t dtype_size(nq_dtype d) { return d == NQ_F32 ? 4 : 2; }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+nq_status hip_status(hipError_t e, const char* who) {
+  if (e != hipSuccess) return fail(NQ_ERR_HIP, "%s: %s", who, hipGetErrorString(e));
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+int64_t nq_codes_words(int64_t rows, int64_t cols) {
+  if (rows < 0 || cols < 8 || cols % 8) return -1;
+  return rows * (cols / 8);
+}
+
+int64_t nq_beta_words(int64_t rows, int64_t cols) {
+  if (rows < 0 || cols < 8 || cols % 8) return -1;
+  return rows * ((cols / 8 + 15) / 16);
+}
+
+const char* nq_status_string(nq_status s) {
+  switch (s) {
+    case NQ_OK: return "NQ_OK";
+    case NQ_ERR_INVALID_ARG: return "NQ_ERR_INVALID_ARG: invalid argument";
+    case NQ_ERR_UNSUPPORTED: return "NQ_ERR_UNSUPPORTED: unsupported configuration";
+    case NQ_ERR_HIP: return "NQ_ERR_HIP: HIP runtime error";
+  }
+  return "unknown nq_status";
+}
+
+const char* nq_last_error(void) { return g_last_error; }
+
+int32_t nq_version(void) { return 100; }
+
+nq_status nq_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t rows,
+                    int64_t cols, int64_t ld_x, uint32_t* codes, uint32_t* beta_idx,
+                    float* scales, void* hip_stream) {
+  const char* who = "nq_encode";
+  if (nq_status s = check_cols(cols, who)) return s;
+  if (nq_status s = check_params(p, cols, who)) return s;
+  if (x_dtype != NQ_F32 && x_dtype != NQ_F16 && x_dtype != NQ_BF16)
+    return fail(NQ_ERR_UNSUPPORTED, "%s: unsupported input dtype %d", who, (int)x_dtype);
+  if (rows < 0 || rows >= kMaxRows)
+    return fail(NQ_ERR_INVALID_ARG, "%s: rows=%lld outside [0, 2^31)", who, (long long)rows);
+  if (ld_x < cols) return fail(NQ_ERR_INVALID_ARG, "%s: ld_x < cols", who);
+  if (rows == 0) return ok();
+  if (!x || !codes || !beta_idx || !scales)
+    return fail(NQ_ERR_INVALID_ARG, "%s: NULL array pointer", who);
+  if (!aligned16(x) || (ld_x * (int64_t)dtype_size(x_dtype)) % 16 != 0)
+    return fail(NQ_ERR_INVALID_ARG, "%s: x and its row stride must be 16-byte aligned", who);
+  nq::EncodeArgs a;
+  a.q = p->q;
+  a.k = p->k;
+  a.rq = (float)(1.0 / p->q);
+  a.m2q = nq::magic_2q(p->q);
+  for (int t = 0; t < 4; ++t) a.beta[t] = (double)(t + 1) * p->base;
+  return hip_status(nq::launch_encode(x, (int)x_dtype, rows, (int)cols, ld_x, a, codes, beta_idx,
+                                      scales, (hipStream_t)hip_stream),
+                    who);
+}
+
+nq_status nq_decode(const nq_params* p, const uint32_t* codes, const uint32_t* beta_idx,
+                    const float* scales, int64_t rows, int64_t cols, void* out,
+                    nq_dtype out_dtype, int64_t ld_out, void* hip_stream) {
+  const char* who = "nq_decode";
+  if (nq_status s = check_cols(cols, who)) return s;
+  if (nq_status s = check_params(p, cols, who)) return s;
+  if (out_dtype != NQ_F32 && out_dtype != NQ_F16 && out_dtype != NQ_BF16)
+    return fail(NQ_ERR_UNSUPPORTED, "%s: unsupported output dtype %d", who, (int)out_dtype);
+  if (rows < 0 || rows >= kMaxRows)
+    return fail(NQ_ERR_INVALID_ARG, "%s: rows=%lld outside [0, 2^31)", who, (long long)rows);
+  if (ld_out < cols) return fail(NQ_ERR_INVALID_ARG, "%s: ld_out < cols", who);
+  if (rows == 0) return ok();
+  if (!codes || !beta_idx || !scales || !out)
+    return fail(NQ_ERR_INVALID_ARG, "%s: NULL array pointer", who);
+  if (!aligned16(out) || (ld_out * (int64_t)dtype_size(out_dtype)) % 16 != 0)
+    return fail(NQ_ERR_INVALID_ARG, "%s: out and its row stride must be 16-byte aligned", who);
+  nq::DecodeArgs a;
+  a.q = p->q;
+  a.m2q = nq::magic_2q(p->q);
+  for (int t = 0; t < 4; ++t) a.half_beta[t] = ((double)(t + 1) * p->base) * 0.5;
+  return hip_status(nq::launch_decode(codes, beta_idx, scales, rows, (int)cols, out,
+                                      (int)out_dtype, ld_out, a, (hipStream_t)hip_stream),
+                    who);
+}
+
+nq_status nq_matmul(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,
+                    const float* a_scales, int64_t M, const nq_params* pw,
+                    const uint32_t* w_codes, const uint32_t* w_beta, const float* w_scales,
+                    int64_t N, int64_t K, float* c, int64_t ldc, void* hip_stream) {
+  const char* who = "nq_matmul";
+  if (nq_status s = check_cols(K, who)) return s;
+  if (nq_status s = check_params(pa, K, who)) return s;
+  if (nq_status s = check_params(pw, K, who)) return s;
+  if (M < 0 || M >= kMaxRows || N < 0 || N >= kMaxRows)
+    return fail(NQ_ERR_INVALID_ARG, "%s: M, N must be in [0, 2^31)", who);
+  if (ldc < N) return fail(NQ_ERR_INVALID_ARG, "%s: ldc < N", who);
+  if (M == 0 || N == 0) return ok();
+  if (!a_codes || !a_beta || !a_scales || !w_codes || !w_beta || !w_scales || !c)
+    return fail(NQ_ERR_INVALID_ARG, "%s: NULL array pointer", who);
+  nq::MatmulOperand A{a_codes, a_beta, a_scales, pa->q, nq::magic_2q(pa->q), M};
+  nq::MatmulOperand W{w_codes, w_beta, w_scales, pw->q, nq::magic_2q(pw->q), N};
+  const float scale = (float)(pa->base * pw->base * 0.25);
+  return hip_status(nq::launch_matmul(A, W, K, c, ldc, scale, (hipStream_t)hip_stream), who);
+}
+
+}  // extern "C"

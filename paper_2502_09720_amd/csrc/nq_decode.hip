@@ -1,0 +1,83 @@
+// NestQuant decoder: Alg. 2 (Voronoi decode over 2E8) followed by the inverse scaling
+// x_hat = r * beta_t * p (Alg. 3's normalization undone).
+//
+// One lane per 8-entry block: read one code word, the row's beta word and scale, decode in
+// exact integer arithmetic, and write the 8 values (32 B fp32 or 16 B fp16/bf16) with one
+// or two vector stores; consecutive lanes handle consecutive blocks of a row.
+#include "nq_device.hpp"
+#include "nq_kernels.hpp"
+
+namespace nq {
+
+__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
+  // round to nearest even (the inputs are finite)
+  const uint32_t u = __float_as_uint(f);
+  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+}
+
+template <int OUT>  // 0 = fp32, 1 = fp16, 2 = bf16
+__global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict__ codes,
+                                                     const uint32_t* __restrict__ beta,
+                                                     const float* __restrict__ scales,
+                                                     int64_t rows, int nb, void* __restrict__ out,
+                                                     int64_t ld_out, DecodeArgs a) {
+  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t row = gid / nb;
+  if (row >= rows) return;
+  const int j = (int)(gid - row * nb);
+  const int nbw = (nb + 15) >> 4;
+  const uint32_t w = __builtin_nontemporal_load(codes + gid);
+  const uint32_t bw = beta[row * nbw + (j >> 4)];
+  const int t = (int)((bw >> (2 * (j & 15))) & 3u);
+  const double sc = (double)scales[row] * a.half_beta[t];
+  int X2[8];
+  decode_word(w, a.q, a.m2q, X2);
+  float v[8];
+#pragma unroll
+  for (int l = 0; l < 8; ++l) v[l] = (float)(sc * (double)X2[l]);
+  if constexpr (OUT == 0) {
+    f32x4* o = reinterpret_cast<f32x4*>((float*)out + row * ld_out + 8 * j);
+    const f32x4 lo = {v[0], v[1], v[2], v[3]};
+    const f32x4 hi = {v[4], v[5], v[6], v[7]};
+    __builtin_nontemporal_store(lo, o);
+    __builtin_nontemporal_store(hi, o + 1);
+  } else {
+    uint32_t h[8];
+#pragma unroll
+    for (int l = 0; l < 8; ++l) {
+      if constexpr (OUT == 1) {
+        h[l] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v[l]);
+      } else {
+        h[l] = f32_to_bf16_bits(v[l]);
+      }
+    }
+    const u32x4 pk = {h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
+                      h[6] | (h[7] << 16)};
+    __builtin_nontemporal_store(pk, reinterpret_cast<u32x4*>((uint16_t*)out + row * ld_out + 8 * j));
+  }
+}
+
+hipError_t launch_decode(const uint32_t* codes, const uint32_t* beta, const float* scales,
+                         int64_t rows, int cols, void* out, int out_dtype, int64_t ld_out,
+                         const DecodeArgs& a, hipStream_t st) {
+  const int nb = cols / 8;
+  const int64_t total = rows * nb;
+  const unsigned grid = (unsigned)((total + 255) / 256);
+  switch (out_dtype) {
+    case 0:
+      hipLaunchKernelGGL(decode_kernel<0>, dim3(grid), dim3(256), 0, st, codes, beta, scales, rows,
+                         nb, out, ld_out, a);
+      break;
+    case 1:
+      hipLaunchKernelGGL(decode_kernel<1>, dim3(grid), dim3(256), 0, st, codes, beta, scales, rows,
+                         nb, out, ld_out, a);
+      break;
+    default:
+      hipLaunchKernelGGL(decode_kernel<2>, dim3(grid), dim3(256), 0, st, codes, beta, scales, rows,
+                         nb, out, ld_out, a);
+      break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace nq

@@ -1,0 +1,328 @@
+// NestQuant row encoder (Sec. 4.2, Alg. 3 with the First-beta strategy of App. F).
+//
+// One lane per 8-entry block.  A row is handled by a group of LANES lanes (a power of two,
+// 8 <= LANES <= 1024); each lane keeps BPT blocks of the row in registers, block
+// j = lane + i * LANES, so the row is read from HBM exactly once and consecutive lanes read
+// consecutive 8-entry blocks (16 B for bf16/fp16, 32 B for fp32).
+//
+// Row scale (Alg. 3, s / sqrt(n)): r is the fp32 number nearest to sqrt(sum x^2 / n).  The
+// squares of fp32 values are exact in fp64; the fp64 sum is accepted when it cannot straddle
+// an fp32 rounding boundary, otherwise the row is summed again as a double-double and the
+// boundary comparison is made exactly.
+#include "nq_device.hpp"
+#include "nq_kernels.hpp"
+
+namespace nq {
+
+template <typename T>
+__device__ __forceinline__ void load_block(const T* __restrict__ p, float (&v)[8]);
+
+template <>
+__device__ __forceinline__ void load_block<float>(const float* __restrict__ p, float (&v)[8]) {
+  const f32x4 a = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+  const f32x4 b = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p) + 1);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+
+template <>
+__device__ __forceinline__ void load_block<uint16_t>(const uint16_t* __restrict__ p,
+                                                     float (&v)[8]) {
+  // bf16: the value is the upper half of an fp32 word
+  const u32x4 a = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  const uint32_t w[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = __uint_as_float(w[i] << 16);
+    v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+
+template <>
+__device__ __forceinline__ void load_block<_Float16>(const _Float16* __restrict__ p,
+                                                     float (&v)[8]) {
+  const u32x4 a = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+  const uint32_t w[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint16_t lo = (uint16_t)(w[i] & 0xffffu), hi = (uint16_t)(w[i] >> 16);
+    v[2 * i] = (float)__builtin_bit_cast(_Float16, lo);
+    v[2 * i + 1] = (float)__builtin_bit_cast(_Float16, hi);
+  }
+}
+
+// Sum over the LANES lanes of a row group.  LANES <= 64: within the wave by xor shuffles.
+// LANES > 64: wave sums, then the waves of the (single) row combine through LDS.
+template <int LANES>
+__device__ __forceinline__ double group_sum(double v, double* red) {
+#pragma unroll
+  for (int m = 1; m < (LANES < 64 ? LANES : 64); m <<= 1) v += __shfl_xor(v, m, 64);
+  if constexpr (LANES > 64) {
+    const int wave = threadIdx.x >> 6;
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) red[wave] = v;
+    __syncthreads();
+    v = red[0];
+#pragma unroll
+    for (int i = 1; i < LANES / 64; ++i) v += red[i];
+  }
+  return v;
+}
+
+// Double-double version of group_sum (error-free on the hi parts).
+__device__ __forceinline__ void two_sum(double a, double b, double& s, double& e) {
+  s = a + b;
+  const double bv = s - a;
+  const double av = s - bv;
+  e = (a - av) + (b - bv);
+}
+
+template <int LANES>
+__device__ __forceinline__ void group_sum_dd(double& hi, double& lo, double* red) {
+#pragma unroll
+  for (int m = 1; m < (LANES < 64 ? LANES : 64); m <<= 1) {
+    const double oh = __shfl_xor(hi, m, 64), ol = __shfl_xor(lo, m, 64);
+    double s, e;
+    two_sum(hi, oh, s, e);
+    hi = s;
+    lo = lo + ol + e;
+  }
+  if constexpr (LANES > 64) {
+    const int wave = threadIdx.x >> 6;
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) {
+      red[2 * wave] = hi;
+      red[2 * wave + 1] = lo;
+    }
+    __syncthreads();
+    hi = red[0];
+    lo = red[1];
+#pragma unroll
+    for (int i = 1; i < LANES / 64; ++i) {
+      double s, e;
+      two_sum(hi, red[2 * i], s, e);
+      hi = s;
+      lo = lo + red[2 * i + 1] + e;
+    }
+  }
+  double s, e;
+  two_sum(hi, lo, s, e);
+  hi = s;
+  lo = e;
+}
+
+// sign of (hi + lo) - n * m^2, exactly (m has at most 25 significant bits, so m^2 is exact
+// in fp64 and n * m^2 is exact as the pair (prod, err) of a fused multiply).
+__device__ __forceinline__ int cmp_sum_square(double hi, double lo, double n, double m) {
+  const double m2 = m * m;
+  const double prod = n * m2;
+  const double err = __builtin_fma(n, m2, -prod);
+  const double t[4] = {hi, lo, -prod, -err};
+  return exact_sign_sum<4>(t);
+}
+
+__device__ __forceinline__ float next_up(float v) { return __uint_as_float(__float_as_uint(v) + 1u); }
+__device__ __forceinline__ float next_down(float v) { return __uint_as_float(__float_as_uint(v) - 1u); }
+
+// First-beta search for one block (App. F): the smallest t whose nearest E8 point of
+// y = fl32(x * c_t) survives decode(encode(.)); t = k when every beta overloads.
+__device__ __forceinline__ void encode_block(const float (&v)[8], const float (&c)[4],
+                                             const EncodeArgs& a, uint32_t& word, int& tsel) {
+  int P[8];
+  tsel = a.k - 1;
+  for (int t = 0; t < a.k; ++t) {
+    float y[8];
+#pragma unroll
+    for (int l = 0; l < 8; ++l) y[l] = v[l] * c[t];
+    nearest_e8(y, P);
+    if (t == a.k - 1 || !overloaded(P, a.q, a.rq, a.m2q)) {
+      tsel = t;
+      break;
+    }
+  }
+  word = encode_codes(P, a.q, a.rq);
+}
+
+// Exact RN32(sqrt(S / n)) from a double-double S and a candidate r within a few ulps.
+__device__ __forceinline__ float exact_rms(double hi, double lo, double n, float r) {
+  for (int it = 0; it < 4; ++it) {
+    const float up = next_up(r), dn = next_down(r);
+    const int cu = cmp_sum_square(hi, lo, n, 0.5 * ((double)r + (double)up));
+    if (cu > 0) { r = up; continue; }
+    if (cu == 0) return (__float_as_uint(r) & 1u) ? up : r;
+    if (r > 0.0f) {
+      const int cd = cmp_sum_square(hi, lo, n, 0.5 * ((double)r + (double)dn));
+      if (cd < 0) { r = dn; continue; }
+      if (cd == 0) return (__float_as_uint(r) & 1u) ? dn : r;
+    }
+    break;
+  }
+  return r;
+}
+
+// The fp32 RMS candidate from an fp64 sum, and whether it is certainly RN32(sqrt(S / n)):
+// the fp64 sum has relative error below 2^-46 here, so S farther than 2^-40 S from both
+// rounding-boundary squares n m^2 settles the rounding.
+__device__ __forceinline__ float rms_candidate(double s, double n, bool& sure) {
+  const float r = (float)__builtin_sqrt(s / n);
+  sure = true;
+  if (s > 0.0 && r > 0.0f && isfinite(r)) {
+    const double m_hi = 0.5 * ((double)r + (double)next_up(r));
+    const double m_lo = 0.5 * ((double)r + (double)next_down(r));
+    const double tol = s * 0x1p-40;
+    sure = (n * m_hi * m_hi - s > tol) && (s - n * m_lo * m_lo > tol);
+  }
+  return r;
+}
+
+__device__ __forceinline__ void dd_add_square(double& hi, double& lo, float x) {
+  const double sq = (double)x * (double)x;
+  double t, e;
+  two_sum(hi, sq, t, e);
+  hi = t;
+  lo += e;
+}
+
+// BPT > 0: the row's blocks stay in registers (read once).  BPT == 0: long rows are
+// streamed, reading each block once for the scale and once more for the codes.
+template <typename T, int LANES, int BPT>
+__global__ __launch_bounds__(LANES > 256 ? LANES : 256) void encode_kernel(
+    const T* __restrict__ x, int64_t rows, int cols, int64_t ld_x, EncodeArgs a,
+    uint32_t* __restrict__ codes, uint32_t* __restrict__ beta, float* __restrict__ scales) {
+  constexpr int WG = LANES > 256 ? LANES : 256;
+  constexpr int ROWS_PER_WG = WG / LANES;
+  constexpr int NV = BPT > 0 ? BPT : 1;
+  __shared__ double red[2 * (WG / 64)];
+
+  const int lane = threadIdx.x % LANES;
+  const int64_t row = (int64_t)blockIdx.x * ROWS_PER_WG + threadIdx.x / LANES;
+  const bool row_ok = row < rows;  // uniform per group; whole-WG uniform when LANES > 64
+  const int nb = cols >> 3;
+  const int nbw = (nb + 15) >> 4;
+  const T* xr = x + (row_ok ? row : 0) * ld_x;
+
+  float v[NV][8];
+  double s = 0.0;
+  if constexpr (BPT > 0) {
+#pragma unroll
+    for (int i = 0; i < BPT; ++i) {
+      const int j = lane + i * LANES;
+      if (row_ok && j < nb) {
+        load_block<T>(xr + 8 * j, v[i]);
+      } else {
+#pragma unroll
+        for (int l = 0; l < 8; ++l) v[i][l] = 0.0f;
+      }
+#pragma unroll
+      for (int l = 0; l < 8; ++l) s = __builtin_fma((double)v[i][l], (double)v[i][l], s);
+    }
+  } else {
+    for (int j = lane; row_ok && j < nb; j += LANES) {
+      load_block<T>(xr + 8 * j, v[0]);
+#pragma unroll
+      for (int l = 0; l < 8; ++l) s = __builtin_fma((double)v[0][l], (double)v[0][l], s);
+    }
+  }
+  s = group_sum<LANES>(s, red);
+
+  const double n = (double)cols;
+  bool sure;
+  float r = rms_candidate(s, n, sure);
+  // With LANES > 64 there is one row per workgroup and every thread holds the same s, so
+  // this branch (which synchronizes the workgroup) is uniform.
+  if (!sure) {
+    double hi = 0.0, lo = 0.0;
+    if constexpr (BPT > 0) {
+#pragma unroll
+      for (int i = 0; i < BPT; ++i)
+#pragma unroll
+        for (int l = 0; l < 8; ++l) dd_add_square(hi, lo, v[i][l]);
+    } else {
+      for (int j = lane; row_ok && j < nb; j += LANES) {
+        float w[8];
+        load_block<T>(xr + 8 * j, w);
+#pragma unroll
+        for (int l = 0; l < 8; ++l) dd_add_square(hi, lo, w[l]);
+      }
+    }
+    group_sum_dd<LANES>(hi, lo, red);
+    r = exact_rms(hi, lo, n, r);
+  }
+
+  const bool coded = (r > 0.0f) && isfinite(r);
+  float c[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) c[t] = coded ? (float)(1.0 / ((double)r * a.beta[t])) : 0.0f;
+
+  uint32_t* crow = codes + (row_ok ? row : 0) * nb;
+  uint32_t* brow = beta + (row_ok ? row : 0) * nbw;
+  const int iters = BPT > 0 ? BPT : (nb + LANES - 1) / LANES;
+  constexpr int UNROLL = BPT > 0 ? BPT : 1;
+#pragma unroll UNROLL
+  for (int i = 0; i < iters; ++i) {
+    const int j = lane + i * LANES;
+    const bool mine = row_ok && j < nb;
+    float* vb = v[BPT > 0 ? i : 0];
+    if constexpr (BPT == 0) {
+      if (mine) load_block<T>(xr + 8 * j, v[0]);
+    }
+    uint32_t word = 0;
+    int tsel = 0;
+    if (mine && coded) encode_block(*reinterpret_cast<float(*)[8]>(vb), c, a, word, tsel);
+    if (mine) crow[j] = word;
+    // two-bit beta indices: OR over the 16 consecutive blocks of one word
+    uint32_t bits = mine ? ((uint32_t)tsel << (2 * (j & 15))) : 0u;
+    constexpr int W = LANES < 16 ? LANES : 16;
+#pragma unroll
+    for (int m = 1; m < W; m <<= 1) bits |= __shfl_xor(bits, m, 64);
+    if (mine && (j & 15) == 0) brow[j >> 4] = bits;
+  }
+  if (row_ok && lane == 0) scales[row] = r;
+}
+
+// ---------------------------------------------------------------------------------------
+// launch
+// ---------------------------------------------------------------------------------------
+template <typename T, int LANES, int BPT>
+static hipError_t launch_t(const void* x, int64_t rows, int cols, int64_t ld_x,
+                           const EncodeArgs& a, uint32_t* codes, uint32_t* beta, float* scales,
+                           hipStream_t st) {
+  constexpr int WG = LANES > 256 ? LANES : 256;
+  constexpr int RPW = WG / LANES;
+  const int64_t grid = (rows + RPW - 1) / RPW;
+  hipLaunchKernelGGL((encode_kernel<T, LANES, BPT>), dim3((unsigned)grid), dim3(WG), 0, st,
+                     (const T*)x, rows, cols, ld_x, a, codes, beta, scales);
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t launch_dtype(const void* x, int64_t rows, int cols, int64_t ld_x,
+                               const EncodeArgs& a, uint32_t* codes, uint32_t* beta,
+                               float* scales, hipStream_t st) {
+  const int nb = cols / 8;
+#define NQ_L(L, B) return launch_t<T, L, B>(x, rows, cols, ld_x, a, codes, beta, scales, st)
+  if (nb <= 8) NQ_L(8, 1);
+  if (nb <= 16) NQ_L(16, 1);
+  if (nb <= 32) NQ_L(32, 1);
+  if (nb <= 64) NQ_L(64, 1);
+  if (nb <= 128) NQ_L(128, 1);
+  if (nb <= 256) NQ_L(256, 1);
+  if (nb <= 512) NQ_L(256, 2);
+  if (nb <= 1024) NQ_L(256, 4);
+  if (nb <= 2048) NQ_L(256, 8);
+  if (nb <= 4096) NQ_L(512, 8);
+  NQ_L(1024, 0);
+#undef NQ_L
+}
+
+hipError_t launch_encode(const void* x, int dtype, int64_t rows, int cols, int64_t ld_x,
+                         const EncodeArgs& a, uint32_t* codes, uint32_t* beta, float* scales,
+                         hipStream_t st) {
+  switch (dtype) {
+    case 0: return launch_dtype<float>(x, rows, cols, ld_x, a, codes, beta, scales, st);
+    case 1: return launch_dtype<_Float16>(x, rows, cols, ld_x, a, codes, beta, scales, st);
+    default: return launch_dtype<uint16_t>(x, rows, cols, ld_x, a, codes, beta, scales, st);
+  }
+}
+
+}  // namespace nq

@@ -1,0 +1,45 @@
+// Host-side launch interface of the NestQuant kernels (internal to libnestquant.so).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace nq {
+
+struct EncodeArgs {
+  int q;           // nesting ratio
+  int k;           // number of betas
+  float rq;        // fl32(1 / q), estimate for the mod-q reduction
+  uint32_t m2q;    // ceil(2^16 / (2q)): floor(X / 2q) = (X * m2q) >> 16 for 0 <= X < 2^11
+  double beta[4];  // fl64(t * base), t = 1..4
+};
+
+struct DecodeArgs {
+  int q;
+  uint32_t m2q;
+  double half_beta[4];  // fl64(t * base) / 2 (exact halving), t = 1..4
+};
+
+struct MatmulOperand {
+  const uint32_t* codes;
+  const uint32_t* beta;
+  const float* scales;
+  int q;
+  uint32_t m2q;
+  int64_t rows;
+};
+
+hipError_t launch_encode(const void* x, int dtype, int64_t rows, int cols, int64_t ld_x,
+                         const EncodeArgs& a, uint32_t* codes, uint32_t* beta, float* scales,
+                         hipStream_t st);
+
+hipError_t launch_decode(const uint32_t* codes, const uint32_t* beta, const float* scales,
+                         int64_t rows, int cols, void* out, int out_dtype, int64_t ld_out,
+                         const DecodeArgs& a, hipStream_t st);
+
+hipError_t launch_matmul(const MatmulOperand& A, const MatmulOperand& W, int64_t K, float* c,
+                         int64_t ldc, float scale, hipStream_t st);
+
+inline uint32_t magic_2q(int q) { return (uint32_t)((65536 + 2 * q - 1) / (2 * q)); }
+
+}  // namespace nq

@@ -1,0 +1,119 @@
+"""The C ABI library loads, exports every declared entry point, and rejects bad arguments
+on the host before launching anything.  No kernel runs here (no GPU needed): every call
+below either fails validation or is a documented no-op (rows == 0)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from conftest import ROOT
+
+HEADER = os.path.join(ROOT, "include", "nestquant.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(nq_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    import paper_2502_09720_amd as nq
+    return nq.library()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert {"nq_encode", "nq_decode", "nq_matmul"} <= set(names)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_sizes(lib):
+    assert lib.nq_codes_words(3, 64) == 24
+    assert lib.nq_beta_words(3, 64) == 3
+    assert lib.nq_beta_words(3, 128) == 3
+    assert lib.nq_beta_words(3, 136) == 6
+    assert lib.nq_codes_words(3, 12) == -1
+    assert lib.nq_codes_words(-1, 64) == -1
+
+
+def test_status_strings(lib):
+    for s in range(4):
+        assert lib.nq_status_string(s)
+    assert lib.nq_version() >= 100
+
+
+def _p(q=14, k=4, base=None):
+    from paper_2502_09720_amd.binding import _Params
+    return _Params(q, k, 10.0 / (max(k, 1) * max(q, 1)) if base is None else base)
+
+
+FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: each call below fails validation
+NULL = ctypes.c_void_p(0)
+S = ctypes.c_void_p(0)
+
+
+@pytest.mark.parametrize("case", [
+    dict(p=None), dict(p=_p(q=1)), dict(p=_p(q=17)), dict(p=_p(k=0)), dict(p=_p(k=5)),
+    dict(p=_p(base=0.0)), dict(p=_p(base=-1.0)), dict(p=_p(base=float("nan"))),
+    dict(p=_p(base=1e-9)), dict(cols=12), dict(cols=0), dict(cols=65544), dict(rows=-1),
+    dict(ld=32), dict(x=NULL), dict(codes=NULL), dict(x=ctypes.c_void_p(0x1004)),
+    dict(dtype=7),
+])
+def test_encode_rejects(lib, case):
+    p = case.get("p", _p())
+    args = dict(rows=4, cols=64, ld=64, x=FAKE, codes=FAKE, dtype=0)
+    args.update(case)
+    pp = None if p is None else ctypes.byref(p)
+    st = lib.nq_encode(pp, args["x"], args["dtype"], args["rows"], args["cols"], args["ld"],
+                       args["codes"], FAKE, FAKE, S)
+    assert st in (1, 2)
+    assert lib.nq_last_error()
+
+
+def test_encode_zero_rows_is_noop(lib):
+    p = _p()
+    assert lib.nq_encode(ctypes.byref(p), NULL, 0, 0, 64, 64, NULL, NULL, NULL, S) == 0
+
+
+@pytest.mark.parametrize("case", [
+    dict(p=_p(q=0)), dict(cols=7), dict(ld=8), dict(out=NULL), dict(dtype=3),
+    dict(out=ctypes.c_void_p(0x1002)), dict(rows=-5),
+])
+def test_decode_rejects(lib, case):
+    p = case.get("p", _p())
+    args = dict(rows=4, cols=64, ld=64, out=FAKE, dtype=0)
+    args.update(case)
+    st = lib.nq_decode(ctypes.byref(p), FAKE, FAKE, FAKE, args["rows"], args["cols"],
+                       args["out"], args["dtype"], args["ld"], S)
+    assert st in (1, 2)
+
+
+@pytest.mark.parametrize("case", [
+    dict(pa=_p(k=9)), dict(pw=_p(q=99)), dict(K=20), dict(M=-1), dict(ldc=3), dict(c=NULL),
+])
+def test_matmul_rejects(lib, case):
+    pa, pw = case.get("pa", _p()), case.get("pw", _p())
+    args = dict(M=4, N=8, K=64, ldc=8, c=FAKE)
+    args.update(case)
+    st = lib.nq_matmul(ctypes.byref(pa), FAKE, FAKE, FAKE, args["M"], ctypes.byref(pw), FAKE,
+                       FAKE, FAKE, args["N"], args["K"], args["c"], args["ldc"], S)
+    assert st == 1
+
+
+def test_matmul_empty_is_noop(lib):
+    p = _p()
+    assert lib.nq_matmul(ctypes.byref(p), NULL, NULL, NULL, 0, ctypes.byref(p), NULL, NULL,
+                         NULL, 5, 64, NULL, 5, S) == 0
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    import paper_2502_09720_amd.binding as b
+    monkeypatch.setenv("NESTQUANT_LIB", str(tmp_path / "missing.so"))
+    monkeypatch.setattr(b, "_LIB", None)
+    with pytest.raises(RuntimeError):
+        b.library()

@@ -1,0 +1,232 @@
+"""GPU parity: the HIP path through the C ABI against the oracle, on identical host inputs.
+
+Bar (from the method and its numerics):
+* nq_encode: code words, beta words and scales bit-exact;
+* nq_decode: every value within 1 ulp of the output type of the oracle's fp64 value;
+* nq_matmul: relative Frobenius error <= 1e-3 against the oracle's exact product (bf16
+  tiles t*X2 are exact integers; only the fp32 accumulation and the fp32 scale epilogue
+  round, so the observed error is ~1e-7).
+"""
+
+import numpy as np
+import pytest
+
+import workloads
+from oracle import nestquant
+from nq_gpu import (decoded_to_f64, first_mismatch, oracle_encode, to_device, u32, ulp_in,
+                    upload_coded)
+
+pytestmark = pytest.mark.gpu
+
+MATMUL_RTOL = 1e-3
+
+
+@pytest.fixture(scope="module")
+def nq():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2502_09720_amd as nq
+    nq.library()
+    return nq
+
+
+def check_encode(nq, store, x32, dtype, q, k, base=None, ld_pad=0):
+    torch = __import__("torch")
+    rows, cols = x32.shape
+    if ld_pad:
+        big = np.zeros((rows, cols + ld_pad), dtype=store.dtype)
+        big[:, :cols] = store
+        xd = to_device(big, dtype)[:, :cols]
+    else:
+        xd = to_device(store, dtype)
+    got = nq.encode(xd, q=q, k=k, base=base)
+    torch.cuda.synchronize()
+    nb = cols // 8
+    gc = u32(got.codes, (rows, nb))
+    gb = u32(got.beta, (rows, (nb + 15) // 16))
+    gs = got.scales.cpu().numpy()
+    oc, ob, os_ = oracle_encode(x32, q, k, base)
+    assert first_mismatch(gs.view(np.uint32), os_.view(np.uint32)) is None, \
+        "scales: " + first_mismatch(gs.view(np.uint32), os_.view(np.uint32))
+    m = first_mismatch(gc, oc)
+    assert m is None, "codes: " + m
+    m = first_mismatch(gb, ob)
+    assert m is None, "beta: " + m
+    return got
+
+
+ENCODE_CASES = [
+    # (seed, rows, cols, dtype, dist, scale, q, k)
+    (1, 64, 512, "f32", "normal", 1.0, 14, 4),
+    (2, 37, 8, "bf16", "normal", 1.0, 14, 4),
+    (3, 37, 16, "bf16", "normal", 1.0, 14, 4),
+    (4, 33, 24, "bf16", "t4", 1.0, 14, 4),
+    (5, 20, 120, "f16", "normal", 1.0, 14, 4),
+    (6, 20, 136, "bf16", "normal", 0.02, 14, 4),
+    (7, 9, 1000, "f32", "t4", 3.0, 7, 4),
+    (8, 7, 2056, "bf16", "normal", 1.0, 14, 4),
+    (9, 5, 4096, "bf16", "t4", 1.0, 14, 4),
+    (10, 3, 14336, "bf16", "normal", 1.0, 14, 4),
+    (11, 2, 24576, "f16", "normal", 1.0, 14, 4),
+    (12, 2, 40000, "f32", "normal", 1.0, 14, 4),
+    (13, 50, 128, "f16", "normal", 1.0, 16, 4),
+    (14, 50, 128, "bf16", "t4", 1.0, 3, 2),
+    (15, 50, 64, "f32", "uniform", 1.0, 2, 1),
+    (16, 50, 96, "bf16", "normal", 1.0, 5, 3),
+    (17, 30, 256, "f32", "normal", 1e-30, 14, 4),
+    (18, 30, 256, "f32", "normal", 1e30, 12, 4),
+]
+
+
+@pytest.mark.parametrize("case", ENCODE_CASES, ids=lambda c: f"s{c[0]}-{c[1]}x{c[2]}-{c[3]}-q{c[6]}k{c[7]}")
+def test_encode_parity(nq, case):
+    seed, rows, cols, dtype, dist, scale, q, k = case
+    store, x32 = workloads.random_rows(seed, rows, cols, dtype=dtype, scale=scale, dist=dist)
+    check_encode(nq, store, x32, dtype, q, k)
+
+
+def test_encode_strided_rows(nq):
+    store, x32 = workloads.random_rows(30, 17, 64, dtype="bf16")
+    check_encode(nq, store, x32, "bf16", 14, 4, ld_pad=24)
+
+
+def test_encode_custom_base(nq):
+    store, x32 = workloads.random_rows(31, 40, 128, dtype="f32")
+    check_encode(nq, store, x32, "f32", 14, 4, base=0.3)
+    check_encode(nq, store, x32, "f32", 10, 2, base=0.11)
+
+
+def _tie_rows(seed):
+    """Rows built to hit the tie rules: quarter/eighth grids, repeated values, constant
+    rows, a zero row, single non-zero entries and exact halves after scaling."""
+    rng = np.random.default_rng(seed)
+    rows = [
+        rng.integers(-8, 8, 128) / 4.0,
+        rng.integers(-16, 16, 128) / 8.0,
+        np.repeat(rng.standard_normal(16), 8),
+        np.full(128, 0.75),
+        np.zeros(128),
+        np.eye(128)[5] * 3.0,
+        np.tile([0.5, -0.5, 0.25, 0.0, 1.0, -1.0, 0.125, 2.0], 16),
+        rng.choice([-1.0, 1.0], 128),
+    ]
+    return np.array(rows)
+
+
+@pytest.mark.parametrize("q,k", [(14, 4), (7, 4), (16, 4), (4, 2), (8, 1)])
+def test_encode_ties(nq, q, k):
+    x = _tie_rows(q * 10 + k)
+    for dtype in ("f32", "bf16"):
+        store, x32 = workloads.round_to(x, dtype)
+        check_encode(nq, store, x32, dtype, q, k)
+
+
+def test_encode_outlier_columns(nq):
+    store, x32 = workloads.random_rows(40, 24, 1024, dtype="bf16")
+    x = x32.astype(np.float64)
+    x[:, ::97] *= 20.0
+    store, x32 = workloads.round_to(x, "bf16")
+    check_encode(nq, store, x32, "bf16", 14, 4)
+    check_encode(nq, store, x32, "bf16", 7, 4)
+
+
+def test_encode_non_finite_rows_are_zero(nq):
+    torch = __import__("torch")
+    x = np.ones((3, 64), np.float32)
+    x[0, 3] = np.inf
+    x[1, 7] = np.nan
+    got = nq.encode(torch.from_numpy(x).cuda(), 14, 4)
+    torch.cuda.synchronize()
+    codes = u32(got.codes, (3, 8))
+    assert not codes[0].any() and not codes[1].any() and codes[2].any()
+
+
+@pytest.mark.parametrize("out_dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("q,k", [(14, 4), (7, 4), (16, 3), (3, 1)])
+def test_decode_parity(nq, out_dtype, q, k):
+    torch = __import__("torch")
+    store, x32 = workloads.random_rows(50 + q, 45, 520, dtype="bf16", dist="t4")
+    base = nestquant.default_base(q, k)
+    oc, ob, os_ = oracle_encode(x32, q, k)
+    coded = upload_coded(oc, ob, os_, 45, 520, q, k, base)
+    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[out_dtype]
+    out = nq.decode(coded, tdt)
+    torch.cuda.synchronize()
+    got = decoded_to_f64(out, out_dtype)
+    from oracle import layout
+    want = nestquant.decode_rows(layout.unpack_codes(oc), layout.unpack_beta(ob, 65), os_, q, base)
+    err = np.abs(got - want)
+    tol = ulp_in(out_dtype, want)
+    bad = err > tol
+    assert not bad.any(), f"{bad.sum()} values beyond 1 ulp; worst {err.max()}"
+
+
+def _oracle_product(A32, W32, qa, qw, k):
+    ba, bw = nestquant.default_base(qa, k), nestquant.default_base(qw, k)
+    ca, ta, ra = nestquant.quantize_rows(A32, qa, k)
+    cw, tw, rw = nestquant.quantize_rows(W32, qw, k)
+    C = nestquant.coded_matmul(ca, ta, ra, qa, ba, cw, tw, rw, qw, bw)
+    from oracle import layout
+    A = (layout.pack_codes(ca), layout.pack_beta(ta), ra, ba)
+    W = (layout.pack_codes(cw), layout.pack_beta(tw), rw, bw)
+    return C, A, W
+
+
+MATMUL_CASES = [
+    # (seed, M, N, K, qa, qw, k)
+    (1, 64, 256, 512, 14, 14, 4),
+    (2, 1, 1, 8, 14, 14, 4),
+    (3, 130, 70, 72, 14, 7, 4),
+    (4, 257, 129, 1032, 16, 14, 4),
+    (5, 16, 300, 2048, 7, 7, 4),
+    (6, 200, 40, 136, 5, 3, 2),
+    (7, 33, 65, 64, 14, 14, 1),
+]
+
+
+@pytest.mark.parametrize("case", MATMUL_CASES, ids=lambda c: f"{c[1]}x{c[2]}x{c[3]}-q{c[4]}/{c[5]}k{c[6]}")
+def test_matmul_parity(nq, case):
+    torch = __import__("torch")
+    seed, M, N, K, qa, qw, k = case
+    _, A32 = workloads.random_rows(seed, M, K, dtype="bf16", dist="t4")
+    _, W32 = workloads.random_rows(seed + 1000, N, K, dtype="bf16", scale=0.02)
+    C, (ac, ab, ar, ba), (wc, wb, wr, bw) = _oracle_product(A32, W32, qa, qw, k)
+    a = upload_coded(ac, ab, ar, M, K, qa, k, ba)
+    w = upload_coded(wc, wb, wr, N, K, qw, k, bw)
+    got = nq.matmul(a, w)
+    torch.cuda.synchronize()
+    g = got.cpu().numpy().astype(np.float64)
+    rel = np.linalg.norm(g - C) / max(np.linalg.norm(C), 1e-300)
+    assert rel <= MATMUL_RTOL, f"relative Frobenius error {rel}"
+    # elementwise: the fp32 accumulation of exact integer products is far tighter
+    assert np.all(np.abs(g - C) <= 1e-5 * np.abs(C).max() + 1e-30)
+
+
+def test_matmul_strided_output(nq):
+    torch = __import__("torch")
+    _, A32 = workloads.random_rows(60, 70, 256, dtype="f32")
+    _, W32 = workloads.random_rows(61, 50, 256, dtype="f32")
+    C, (ac, ab, ar, ba), (wc, wb, wr, bw) = _oracle_product(A32, W32, 14, 14, 4)
+    a = upload_coded(ac, ab, ar, 70, 256, 14, 4, ba)
+    w = upload_coded(wc, wb, wr, 50, 256, 14, 4, bw)
+    buf = torch.full((70, 64), 7.0, device="cuda")
+    nq.matmul(a, w, out=buf[:, :50])
+    torch.cuda.synchronize()
+    g = buf.cpu().numpy()
+    assert np.all(g[:, 50:] == 7.0)
+    assert np.linalg.norm(g[:, :50] - C) / np.linalg.norm(C) < 1e-6
+
+
+def test_end_to_end_small_config(nq):
+    """The small workload end to end on the GPU (encode both operands, then multiply)."""
+    torch = __import__("torch")
+    sa, A32, _ = workloads.operand(1, "A")
+    sw, W32, _ = workloads.operand(1, "W")
+    a = check_encode(nq, sa, A32, "f32", 14, 4)
+    w = check_encode(nq, sw, W32, "f32", 14, 4)
+    got = nq.matmul(a, w)
+    torch.cuda.synchronize()
+    C, _, _ = _oracle_product(A32, W32, 14, 14, 4)
+    g = got.cpu().numpy().astype(np.float64)
+    assert np.linalg.norm(g - C) / np.linalg.norm(C) <= MATMUL_RTOL
