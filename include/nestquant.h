@@ -25,8 +25,8 @@
  * decoded E8 point; beta_t = t * base for t = 1..k is the beta dictionary (App. F).
  *
  * Conventions for every call:
- *   - all array pointers are device pointers, owned by the caller; the library allocates
- *     nothing and keeps no per-call state;
+ *   - all array pointers are device pointers, owned by the caller; the library keeps no
+ *     per-call state, and allocates nothing except nq_matmul's stream-ordered workspace;
  *   - calls are asynchronous on `hip_stream` (a hipStream_t; NULL = the null stream) and
  *     may be issued from several host threads;
  *   - arguments are checked on the host before anything is launched: on any error the
@@ -90,14 +90,30 @@ nq_status nq_decode(const nq_params* p, const uint32_t* codes, const uint32_t* b
 
 /* C = A_hat * W_hat^T (Alg. 4 for every row pair), fp32 output.
  *   A: M x K coded with parameters pa; W: N x K coded with parameters pw (q, k and base
- *   may differ between the operands; K must be the same);  K % 8 == 0.
+ *   may differ between the operands; K must be the same);  K % 8 == 0, K <= 65536.
  *   c: device, M x N floats, row i at c + i*ldc, ldc >= N.
  * C_ij = r_Ai r_Wj base_A base_W / 4 * sum_blocks <t_A X2_A, t_W X2_W>; the integer tiles
- * t*X2 are exact in bf16 and contracted with fp32 accumulation. */
+ * t*X2 are exact in bf16 and contracted with fp32 accumulation.
+ * For M > 64 the product decodes every block once into a workspace of
+ * nq_matmul_workspace_size(M, N, K) bytes, which nq_matmul takes from the stream-ordered
+ * allocator of the current device (hipMallocAsync / hipFreeAsync on hip_stream); use
+ * nq_matmul_ex to pass a workspace instead. */
 nq_status nq_matmul(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,
                     const float* a_scales, int64_t M, const nq_params* pw,
                     const uint32_t* w_codes, const uint32_t* w_beta, const float* w_scales,
                     int64_t N, int64_t K, float* c, int64_t ldc, void* hip_stream);
+
+/* nq_matmul with a caller-owned device workspace (16-byte aligned, at least
+ * nq_matmul_workspace_size(M, N, K) bytes; may be NULL when that size is 0).  The workspace
+ * is used as scratch until the call's kernels finish on hip_stream. */
+nq_status nq_matmul_ex(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,
+                       const float* a_scales, int64_t M, const nq_params* pw,
+                       const uint32_t* w_codes, const uint32_t* w_beta, const float* w_scales,
+                       int64_t N, int64_t K, float* c, int64_t ldc, void* workspace,
+                       int64_t workspace_bytes, void* hip_stream);
+
+/* Workspace bytes nq_matmul_ex needs for an M x N x K product (0: none; -1: invalid). */
+int64_t nq_matmul_workspace_size(int64_t M, int64_t N, int64_t K);
 
 /* Sizes of the code and beta-index arrays for a rows x cols matrix (-1 if invalid). */
 int64_t nq_codes_words(int64_t rows, int64_t cols);

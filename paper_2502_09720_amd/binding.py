@@ -44,7 +44,11 @@ def library():
         lib.nq_decode.argtypes = [pp, u32p, u32p, f32p, i64, i64, vp, ctypes.c_int, i64, vp]
         lib.nq_matmul.argtypes = [pp, u32p, u32p, f32p, i64, pp, u32p, u32p, f32p, i64, i64,
                                   f32p, i64, vp]
-        for f in ("nq_encode", "nq_decode", "nq_matmul"):
+        lib.nq_matmul_ex.argtypes = [pp, u32p, u32p, f32p, i64, pp, u32p, u32p, f32p, i64, i64,
+                                     f32p, i64, vp, i64, vp]
+        lib.nq_matmul_workspace_size.argtypes = [i64, i64, i64]
+        lib.nq_matmul_workspace_size.restype = i64
+        for f in ("nq_encode", "nq_decode", "nq_matmul", "nq_matmul_ex"):
             getattr(lib, f).restype = ctypes.c_int
         lib.nq_codes_words.argtypes = [i64, i64]
         lib.nq_codes_words.restype = i64
@@ -147,8 +151,10 @@ def decode(coded, out_dtype=None, stream=None, out=None):
     return out
 
 
-def matmul(a, w, stream=None, out=None):
-    """nq_matmul: C = A_hat W_hat^T (fp32, M x N) from two coded operands."""
+def matmul(a, w, stream=None, out=None, workspace=None):
+    """nq_matmul: C = A_hat W_hat^T (fp32, M x N) from two coded operands.
+
+    The decode-once workspace (large M) is taken from torch's allocator unless given."""
     import torch
     if a.cols != w.cols:
         raise ValueError("K mismatch")
@@ -156,10 +162,22 @@ def matmul(a, w, stream=None, out=None):
         out = torch.empty(a.rows, w.rows, dtype=torch.float32, device=a.codes.device)
     pa, pw = _params(a.q, a.k, a.base), _params(w.q, w.k, w.base)
     lib = library()
-    _check(lib.nq_matmul(ctypes.byref(pa), ctypes.c_void_p(a.codes.data_ptr()),
-                         ctypes.c_void_p(a.beta.data_ptr()), ctypes.c_void_p(a.scales.data_ptr()),
-                         a.rows, ctypes.byref(pw), ctypes.c_void_p(w.codes.data_ptr()),
-                         ctypes.c_void_p(w.beta.data_ptr()), ctypes.c_void_p(w.scales.data_ptr()),
-                         w.rows, a.cols, ctypes.c_void_p(out.data_ptr()), out.stride(0),
-                         _stream(stream)))
+    need = lib.nq_matmul_workspace_size(a.rows, w.rows, a.cols)
+    if need < 0:
+        raise ValueError("invalid matmul shape")
+    if need > 0 and (workspace is None or workspace.numel() * workspace.element_size() < need):
+        workspace = torch.empty(need, dtype=torch.uint8, device=a.codes.device)
+    ws_ptr = workspace.data_ptr() if need > 0 else 0
+    _check(lib.nq_matmul_ex(ctypes.byref(pa), ctypes.c_void_p(a.codes.data_ptr()),
+                            ctypes.c_void_p(a.beta.data_ptr()),
+                            ctypes.c_void_p(a.scales.data_ptr()), a.rows, ctypes.byref(pw),
+                            ctypes.c_void_p(w.codes.data_ptr()),
+                            ctypes.c_void_p(w.beta.data_ptr()),
+                            ctypes.c_void_p(w.scales.data_ptr()), w.rows, a.cols,
+                            ctypes.c_void_p(out.data_ptr()), out.stride(0),
+                            ctypes.c_void_p(ws_ptr), need, _stream(stream)))
     return out
+
+
+def matmul_workspace_size(M, N, K):
+    return library().nq_matmul_workspace_size(M, N, K)

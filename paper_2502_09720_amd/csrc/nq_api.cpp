@@ -4,6 +4,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 
 #include "nestquant.h"
 #include "nq_kernels.hpp"
@@ -136,24 +137,79 @@ nq_status nq_decode(const nq_params* p, const uint32_t* codes, const uint32_t* b
                     who);
 }
 
-nq_status nq_matmul(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,
-                    const float* a_scales, int64_t M, const nq_params* pw,
-                    const uint32_t* w_codes, const uint32_t* w_beta, const float* w_scales,
-                    int64_t N, int64_t K, float* c, int64_t ldc, void* hip_stream) {
-  const char* who = "nq_matmul";
+static nq_status check_matmul(const nq_params* pa, const uint32_t* a_codes,
+                              const uint32_t* a_beta, const float* a_scales, int64_t M,
+                              const nq_params* pw, const uint32_t* w_codes,
+                              const uint32_t* w_beta, const float* w_scales, int64_t N,
+                              int64_t K, float* c, int64_t ldc, const char* who) {
   if (nq_status s = check_cols(K, who)) return s;
   if (nq_status s = check_params(pa, K, who)) return s;
   if (nq_status s = check_params(pw, K, who)) return s;
   if (M < 0 || M >= kMaxRows || N < 0 || N >= kMaxRows)
     return fail(NQ_ERR_INVALID_ARG, "%s: M, N must be in [0, 2^31)", who);
   if (ldc < N) return fail(NQ_ERR_INVALID_ARG, "%s: ldc < N", who);
-  if (M == 0 || N == 0) return ok();
+  if (M == 0 || N == 0) return NQ_OK;
   if (!a_codes || !a_beta || !a_scales || !w_codes || !w_beta || !w_scales || !c)
     return fail(NQ_ERR_INVALID_ARG, "%s: NULL array pointer", who);
+  return NQ_OK;
+}
+
+int64_t nq_matmul_workspace_size(int64_t M, int64_t N, int64_t K) {
+  if (M < 0 || N < 0 || K < 8 || K % 8 || K > kMaxCols) return -1;
+  if (M <= nq::kFusedMaxM || N == 0) return 0;
+  return (int64_t)nq::decode_once_workspace(M, N, K);
+}
+
+nq_status nq_matmul_ex(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,
+                       const float* a_scales, int64_t M, const nq_params* pw,
+                       const uint32_t* w_codes, const uint32_t* w_beta, const float* w_scales,
+                       int64_t N, int64_t K, float* c, int64_t ldc, void* workspace,
+                       int64_t workspace_bytes, void* hip_stream) {
+  const char* who = "nq_matmul_ex";
+  if (nq_status s = check_matmul(pa, a_codes, a_beta, a_scales, M, pw, w_codes, w_beta,
+                                 w_scales, N, K, c, ldc, who))
+    return s;
+  if (M == 0 || N == 0) return ok();
+  const int64_t need = nq_matmul_workspace_size(M, N, K);
+  if (workspace_bytes < need || (need > 0 && !workspace))
+    return fail(NQ_ERR_INVALID_ARG, "%s: workspace of %lld bytes needed", who, (long long)need);
+  if (need > 0 && !aligned16(workspace))
+    return fail(NQ_ERR_INVALID_ARG, "%s: workspace must be 16-byte aligned", who);
   nq::MatmulOperand A{a_codes, a_beta, a_scales, pa->q, nq::magic_2q(pa->q), M};
   nq::MatmulOperand W{w_codes, w_beta, w_scales, pw->q, nq::magic_2q(pw->q), N};
   const float scale = (float)(pa->base * pw->base * 0.25);
-  return hip_status(nq::launch_matmul(A, W, K, c, ldc, scale, (hipStream_t)hip_stream), who);
+  hipStream_t st = (hipStream_t)hip_stream;
+  if (need == 0) return hip_status(nq::launch_matmul(A, W, K, c, ldc, scale, st), who);
+  static std::once_flag attr_once;
+  static hipError_t attr_err = hipSuccess;
+  std::call_once(attr_once, [] { attr_err = nq::gemm_set_attributes(); });
+  if (attr_err != hipSuccess) return hip_status(attr_err, who);
+  return hip_status(nq::launch_matmul_decode_once(A, W, K, c, ldc, scale, workspace, st), who);
+}
+
+nq_status nq_matmul(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,
+                    const float* a_scales, int64_t M, const nq_params* pw,
+                    const uint32_t* w_codes, const uint32_t* w_beta, const float* w_scales,
+                    int64_t N, int64_t K, float* c, int64_t ldc, void* hip_stream) {
+  const char* who = "nq_matmul";
+  if (nq_status s = check_matmul(pa, a_codes, a_beta, a_scales, M, pw, w_codes, w_beta,
+                                 w_scales, N, K, c, ldc, who))
+    return s;
+  if (M == 0 || N == 0) return ok();
+  const int64_t need = nq_matmul_workspace_size(M, N, K);
+  void* ws = nullptr;
+  hipStream_t st = (hipStream_t)hip_stream;
+  if (need > 0) {
+    const hipError_t e = hipMallocAsync(&ws, (size_t)need, st);
+    if (e != hipSuccess) return hip_status(e, who);
+  }
+  const nq_status s = nq_matmul_ex(pa, a_codes, a_beta, a_scales, M, pw, w_codes, w_beta,
+                                   w_scales, N, K, c, ldc, ws, need, hip_stream);
+  if (ws) {
+    const hipError_t e = hipFreeAsync(ws, st);
+    if (s == NQ_OK && e != hipSuccess) return hip_status(e, who);
+  }
+  return s;
 }
 
 }  // extern "C"

@@ -1,7 +1,8 @@
 // NestQuant row encoder (Sec. 4.2, Alg. 3 with the First-beta strategy of App. F).
 //
 // One lane per 8-entry block.  A row is handled by a group of LANES lanes (a power of two,
-// 8 <= LANES <= 1024); each lane keeps BPT blocks of the row in registers, block
+// 8 <= LANES <= 1024): several rows share a 256-thread workgroup when LANES <= 64, and a
+// workgroup is exactly one row when LANES > 64.  Each lane keeps BPT blocks in registers, block
 // j = lane + i * LANES, so the row is read from HBM exactly once and consecutive lanes read
 // consecutive 8-entry blocks (16 B for bf16/fp16, 32 B for fp32).
 //
@@ -51,8 +52,9 @@ __device__ __forceinline__ void load_block<_Float16>(const _Float16* __restrict_
   }
 }
 
-// Sum over the LANES lanes of a row group.  LANES <= 64: within the wave by xor shuffles.
-// LANES > 64: wave sums, then the waves of the (single) row combine through LDS.
+// Sum over the LANES lanes of a row group.  LANES <= 64: within the wave by xor shuffles
+// (every lane ends with the same, bit-identical sum).  LANES > 64: the workgroup is exactly
+// one row (LANES threads); wave sums are combined through LDS in a fixed order.
 template <int LANES>
 __device__ __forceinline__ double group_sum(double v, double* red) {
 #pragma unroll
@@ -186,10 +188,10 @@ __device__ __forceinline__ void dd_add_square(double& hi, double& lo, float x) {
 // BPT > 0: the row's blocks stay in registers (read once).  BPT == 0: long rows are
 // streamed, reading each block once for the scale and once more for the codes.
 template <typename T, int LANES, int BPT>
-__global__ __launch_bounds__(LANES > 256 ? LANES : 256) void encode_kernel(
+__global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_kernel(
     const T* __restrict__ x, int64_t rows, int cols, int64_t ld_x, EncodeArgs a,
     uint32_t* __restrict__ codes, uint32_t* __restrict__ beta, float* __restrict__ scales) {
-  constexpr int WG = LANES > 256 ? LANES : 256;
+  constexpr int WG = LANES > 64 ? LANES : 256;
   constexpr int ROWS_PER_WG = WG / LANES;
   constexpr int NV = BPT > 0 ? BPT : 1;
   __shared__ double red[2 * (WG / 64)];
@@ -287,7 +289,7 @@ template <typename T, int LANES, int BPT>
 static hipError_t launch_t(const void* x, int64_t rows, int cols, int64_t ld_x,
                            const EncodeArgs& a, uint32_t* codes, uint32_t* beta, float* scales,
                            hipStream_t st) {
-  constexpr int WG = LANES > 256 ? LANES : 256;
+  constexpr int WG = LANES > 64 ? LANES : 256;
   constexpr int RPW = WG / LANES;
   const int64_t grid = (rows + RPW - 1) / RPW;
   hipLaunchKernelGGL((encode_kernel<T, LANES, BPT>), dim3((unsigned)grid), dim3(WG), 0, st,

@@ -105,6 +105,25 @@ def test_matmul_rejects(lib, case):
     assert st == 1
 
 
+def test_workspace_size(lib):
+    assert lib.nq_matmul_workspace_size(64, 4096, 4096) == 0      # fused path
+    ws = lib.nq_matmul_workspace_size(2048, 4096, 4096)
+    assert ws >= (2048 + 4096) * 4096 * 2                          # bf16 tiles of A and W
+    assert lib.nq_matmul_workspace_size(100, 10, 12) == -1
+
+
+def test_matmul_ex_rejects_small_workspace(lib):
+    p = _p()
+    need = lib.nq_matmul_workspace_size(300, 200, 64)
+    assert need > 0
+    st = lib.nq_matmul_ex(ctypes.byref(p), FAKE, FAKE, FAKE, 300, ctypes.byref(p), FAKE, FAKE,
+                          FAKE, 200, 64, FAKE, 200, FAKE, need - 16, S)
+    assert st == 1
+    st = lib.nq_matmul_ex(ctypes.byref(p), FAKE, FAKE, FAKE, 300, ctypes.byref(p), FAKE, FAKE,
+                          FAKE, 200, 64, FAKE, 200, NULL, need, S)
+    assert st == 1
+
+
 def test_matmul_empty_is_noop(lib):
     p = _p()
     assert lib.nq_matmul(ctypes.byref(p), NULL, NULL, NULL, 0, ctypes.byref(p), NULL, NULL,

@@ -230,3 +230,55 @@ def test_end_to_end_small_config(nq):
     C, _, _ = _oracle_product(A32, W32, 14, 14, 4)
     g = got.cpu().numpy().astype(np.float64)
     assert np.linalg.norm(g - C) / np.linalg.norm(C) <= MATMUL_RTOL
+
+
+def _near_midpoint_rows(n, count=12):
+    """Rows (1, b, 0, ..., 0) whose RMS lies within 2^-41 (relative) of an fp32 rounding
+    boundary, so that both sides must settle the rounding of the scale exactly."""
+    j = np.arange(1, 3_000_000)
+    b = (1.0 + j * 2.0 ** -23).astype(np.float32).astype(np.float64)
+    r64 = np.sqrt((1.0 + b * b) / n)
+    r32 = r64.astype(np.float32)
+    up = np.nextafter(r32, np.float32(np.inf)).astype(np.float64)
+    dn = np.nextafter(r32, np.float32(-np.inf)).astype(np.float64)
+    c = r32.astype(np.float64)
+    d = np.minimum(np.abs(r64 - (c + up) / 2), np.abs(r64 - (c + dn) / 2)) / r64
+    picks = b[np.nonzero(d < 2.0 ** -41)[0][:count]]
+    rows = np.zeros((2 * len(picks), n))
+    rng = np.random.default_rng(n)
+    for i, bb in enumerate(picks):
+        rows[2 * i, 0], rows[2 * i, 1] = 1.0, bb
+        rows[2 * i + 1] = rng.standard_normal(n)     # interleave ordinary rows
+    return rows
+
+
+@pytest.mark.parametrize("n", [8, 64, 1024, 4096, 20000])
+def test_encode_scale_near_rounding_boundary(nq, n):
+    x = _near_midpoint_rows(n)
+    store, x32 = workloads.round_to(x, "f32")
+    check_encode(nq, store, x32, "f32", 14, 4)
+
+
+def test_matmul_internal_workspace_matches_ex(nq):
+    """nq_matmul (stream-ordered internal workspace) equals nq_matmul_ex (caller workspace)."""
+    import ctypes
+    torch = __import__("torch")
+    from paper_2502_09720_amd.binding import _params, _stream
+    _, A32 = workloads.random_rows(70, 300, 256, dtype="bf16")
+    _, W32 = workloads.random_rows(71, 200, 256, dtype="bf16", scale=0.02)
+    C, (ac, ab, ar, ba), (wc, wb, wr, bw) = _oracle_product(A32, W32, 14, 14, 4)
+    a = upload_coded(ac, ab, ar, 300, 256, 14, 4, ba)
+    w = upload_coded(wc, wb, wr, 200, 256, 14, 4, bw)
+    ref = nq.matmul(a, w)
+    out = torch.empty(300, 200, device="cuda")
+    pa, pw = _params(14, 4, ba), _params(14, 4, bw)
+    vp = ctypes.c_void_p
+    st = nq.library().nq_matmul(ctypes.byref(pa), vp(a.codes.data_ptr()), vp(a.beta.data_ptr()),
+                                vp(a.scales.data_ptr()), 300, ctypes.byref(pw),
+                                vp(w.codes.data_ptr()), vp(w.beta.data_ptr()),
+                                vp(w.scales.data_ptr()), 200, 256, vp(out.data_ptr()), 200,
+                                _stream(None))
+    assert st == 0
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref)
+    assert np.linalg.norm(out.cpu().numpy() - C) / np.linalg.norm(C) < 1e-6
