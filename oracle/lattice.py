@@ -122,7 +122,9 @@ def nearest_e8(y):
 
     y: float array of shape (..., 8) whose entries are exact binary fractions (fp32 values
     widened to fp64 are); every intermediate below is then exact except the candidate gap,
-    whose sign is settled exactly.  Returns P = 2 Q_E8(y) as int64 of the same shape.
+    whose sign is settled exactly.  (The distance to the nearest integer is taken as
+    |y - rint(y)|, which is exact; y - floor(y) is not, for tiny negative y.)  Returns
+    P = 2 Q_E8(y) as int64 of the same shape.
     """
     y = np.asarray(y, dtype=np.float64)
     shape = y.shape
@@ -131,9 +133,8 @@ def nearest_e8(y):
     rows = np.arange(n)
 
     d = np.floor(y)
-    f = y - d                              # position inside [d, d+1): exact
-    e = np.minimum(f, 1.0 - f)             # distance to the nearest integer: exact
-    g = f > 0.5                            # round up (an exact half rounds down)
+    g = y > d + 0.5                        # round up (an exact half rounds down)
+    e = np.abs(y - np.rint(y))             # distance to the nearest integer: exact
     s = np.where(g, 1, -1).astype(np.int64)
     di = d.astype(np.int64)
 

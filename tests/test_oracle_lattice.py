@@ -99,7 +99,7 @@ def brute_nearest(y):
 def adversarial_inputs(rng, n):
     out = []
     for _ in range(n):
-        kind = rng.integers(0, 6)
+        kind = rng.integers(0, 7)
         if kind == 0:     # exact halves and integers
             y = rng.integers(-6, 6, 8) + rng.choice([0.0, 0.5], 8)
         elif kind == 1:   # repeated distances: values sharing a fractional part
@@ -112,8 +112,12 @@ def adversarial_inputs(rng, n):
         elif kind == 4:   # tiny values near 0 with a few halves
             y = rng.standard_normal(8) * 1e-6
             y[rng.integers(0, 8)] = 0.5
-        else:             # eighth grid
+        elif kind == 5:   # eighth grid
             y = rng.integers(-40, 40, 8) / 8.0
+        else:             # tiny entries of both signs next to exact zeros and halves
+            y = rng.choice([0.0, 0.5, -0.5, 1.0], 8)
+            k = rng.integers(1, 4)
+            y[:k] = rng.choice([-1.0, 1.0], k) * 10.0 ** rng.uniform(-30, -8, k)
         out.append(y.astype(np.float32).astype(np.float64))
     return np.array(out)
 
