@@ -106,6 +106,7 @@ nq_status nq_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t
   a.k = p->k;
   a.rq = (float)(1.0 / p->q);
   a.m2q = nq::magic_2q(p->q);
+  a.mq = nq::magic_q(p->q);
   for (int t = 0; t < 4; ++t) a.beta[t] = (double)(t + 1) * p->base;
   return hip_status(nq::launch_encode(x, (int)x_dtype, rows, (int)cols, ld_x, a, codes, beta_idx,
                                       scales, (hipStream_t)hip_stream),

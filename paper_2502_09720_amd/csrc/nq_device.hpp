@@ -50,30 +50,31 @@ __device__ __forceinline__ int exact_sign_sum(const double (&t)[N]) {
 // ---------------------------------------------------------------------------------------
 // Nearest point of E8 to an fp32 8-vector (App. C, Alg. 5, Conway-Sloane), in 2E8 units.
 //
-// Per coordinate: d = floor(y), f = y - d (exact for |y| < 2^23), e = distance to the
-// nearest integer = min(f, 1 - f) (exact), g = [f > 1/2] (an exact half rounds down).
-// The D8 candidate is d + g with a parity fix at argmax e (lowest index); the D8+1/2
-// candidate is d + 1/2 with a parity fix at argmin e (lowest index) moving towards y.
-// D8 wins iff the gap  sum e - 2 + odd1 (1 - 2 e_p) - odd2 2 e_r  is negative; a zero gap
-// returns D8+1/2.  The gap is evaluated in fp32 (about a dozen roundings, each below
-// 2^-24 * 8, so the error is below 1e-5); when |gap| < 1e-5 its sign is recomputed exactly
-// from the exact fp32 terms with exact_sign_sum.
+// Per coordinate: d = floor(y); g = [y > d + 1/2] (an exact half rounds down); the distance
+// to the nearest integer e = |y - rint(y)| (exact for |y| < 2^23, also for tiny y).  The D8
+// candidate is d + g with a parity fix at argmax e (lowest index) moving to the other
+// neighbouring integer; the D8+1/2 candidate is d + 1/2 with a parity fix at argmin e
+// (lowest index) moving towards y.  D8 wins iff the gap
+//   sum e - 2 + odd1 (1 - 2 e_p) - odd2 2 e_r
+// is negative; a zero gap returns D8+1/2.  The gap is evaluated in fp32 (about a dozen
+// roundings, each below 2^-24 * 8, so the error is below 1e-5); when |gap| < 1e-5 its sign
+// is recomputed exactly from the exact fp32 terms with exact_sign_sum.
+//
+// In 2E8 units every output is P_l = 2 d_l + delta_l with delta_l = 2 g_l (D8), 1 (D8+1/2);
+// at the fixed coordinate delta = 2 - 2 g (D8) or 4 g - 1 (D8+1/2).
 // ---------------------------------------------------------------------------------------
 __device__ __forceinline__ void nearest_e8(const float (&y)[8], int (&P)[8]) {
   float e[8];
-  int d[8];
-  int g[8];
-  int sum_x1 = 0, sum_d = 0;
+  int d[8], g[8];
 #pragma unroll
   for (int l = 0; l < 8; ++l) {
     const float fl = floorf(y[l]);
-    const float f = y[l] - fl;
-    g[l] = f > 0.5f ? 1 : 0;
-    e[l] = g[l] ? (1.0f - f) : f;
     d[l] = (int)fl;
-    sum_d += d[l];
-    sum_x1 += d[l] + g[l];
+    g[l] = (y[l] > fl + 0.5f) ? 1 : 0;
+    e[l] = fabsf(y[l] - rintf(y[l]));
   }
+  const int sum_d = ((d[0] + d[1]) + (d[2] + d[3])) + ((d[4] + d[5]) + (d[6] + d[7]));
+  const int sum_g = ((g[0] + g[1]) + (g[2] + g[3])) + ((g[4] + g[5]) + (g[6] + g[7]));
   int p = 0, r = 0;
   float ep = e[0], er = e[0];
 #pragma unroll
@@ -85,7 +86,7 @@ __device__ __forceinline__ void nearest_e8(const float (&y)[8], int (&P)[8]) {
     r = dn ? l : r;
     er = dn ? e[l] : er;
   }
-  const int odd1 = sum_x1 & 1;
+  const int odd1 = (sum_d + sum_g) & 1;
   const int odd2 = sum_d & 1;
   float se = e[0];
 #pragma unroll
@@ -106,12 +107,14 @@ __device__ __forceinline__ void nearest_e8(const float (&y)[8], int (&P)[8]) {
     t[11] = odd2 ? -2.0 * (double)er : 0.0;
     d8 = exact_sign_sum<12>(t) < 0;
   }
+  // delta for g = 0 / g = 1, off and on the fixed coordinate
+  const int a_g0 = d8 ? 0 : 1, a_g1 = d8 ? 2 : 1;
+  const int b_g0 = d8 ? 2 : -1, b_g1 = d8 ? 0 : 3;
+  const int fix = d8 ? (odd1 ? p : 8) : (odd2 ? r : 8);
 #pragma unroll
   for (int l = 0; l < 8; ++l) {
-    const int s = 2 * g[l] - 1;
-    const int a = 2 * (d[l] + g[l]) - ((odd1 && l == p) ? 2 * s : 0);
-    const int b = 2 * d[l] + 1 + ((odd2 && l == r) ? 2 * s : 0);
-    P[l] = d8 ? a : b;
+    const int delta = (l == fix) ? (g[l] ? b_g1 : b_g0) : (g[l] ? a_g1 : a_g0);
+    P[l] = 2 * d[l] + delta;
   }
 }
 
@@ -120,30 +123,57 @@ __device__ __forceinline__ void nearest_e8(const float (&y)[8], int (&P)[8]) {
 // P lies strictly inside the cell q V of q 2E8 iff the bound is < 2q, strictly outside iff
 // it is > 2q; equality is the cell boundary.
 __device__ __forceinline__ int e8_root_bound(const int (&P)[8]) {
-  int m1 = 0, m2 = 0, sa = 0, mn = 0x7fffffff, neg = 0;
+  int a[8];
 #pragma unroll
-  for (int l = 0; l < 8; ++l) {
-    const int a = abs(P[l]);
-    m2 = max(m2, min(m1, a));
-    m1 = max(m1, a);
-    sa += a;
-    mn = min(mn, a);
-    neg ^= (P[l] < 0) ? 1 : 0;
+  for (int l = 0; l < 8; ++l) a[l] = abs(P[l]);
+  int m1 = max(a[0], a[1]), m2 = min(a[0], a[1]);
+#pragma unroll
+  for (int l = 2; l < 8; ++l) {
+    m2 = max(m2, min(m1, a[l]));  // the median of (m1, m2, a) since m2 <= m1
+    m1 = max(m1, a[l]);
   }
+  const int sa = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
+  const int mn = min(min(min(a[0], a[1]), min(a[2], a[3])), min(min(a[4], a[5]), min(a[6], a[7])));
+  const int neg = (int)(((uint32_t)(P[0] ^ P[1] ^ P[2] ^ P[3] ^ P[4] ^ P[5] ^ P[6] ^ P[7])) >> 31);
   return max(m1 + m2, (sa - 2 * neg * mn) >> 1);
 }
 
-// v mod q in [0, q) for |v| < 2^24 using an fp32 reciprocal estimate and one correction.
-__device__ __forceinline__ int mod_q(int v, int q, float rq) {
+// Root bound of a real 8-vector: max over the 240 roots lambda of <x, lambda>.  For the
+// nearest point p of E8 to x, |max<2p, lambda> - 2 max<x, lambda>| <= 2 |p - x| |lambda|
+// <= 2 sqrt(2), since the covering radius of E8 is 1 and roots have norm sqrt(2).
+__device__ __forceinline__ float root_bound_f(const float (&x)[8]) {
+  float a[8];
+#pragma unroll
+  for (int l = 0; l < 8; ++l) a[l] = fabsf(x[l]);
+  float m1 = fmaxf(a[0], a[1]), m2 = fminf(a[0], a[1]);
+#pragma unroll
+  for (int l = 2; l < 8; ++l) {
+    m2 = fmaxf(m2, fminf(m1, a[l]));
+    m1 = fmaxf(m1, a[l]);
+  }
+  const float sa = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
+  const float mn = fminf(fminf(fminf(a[0], a[1]), fminf(a[2], a[3])),
+                         fminf(fminf(a[4], a[5]), fminf(a[6], a[7])));
+  int neg = 0;
+#pragma unroll
+  for (int l = 0; l < 8; ++l) neg ^= (x[l] < 0.0f) ? 1 : 0;
+  return fmaxf(m1 + m2, 0.5f * (sa - (neg ? 2.0f * mn : 0.0f)));
+}
+
+// v mod q in [0, q): exact for |v| < 2^24 (fp32 reciprocal estimate and one correction).
+__device__ __forceinline__ int mod_q_general(int v, int q, float rq) {
   const int n = (int)floorf((float)v * rq);
-  int r = v - n * q;
+  int r = v - __mul24(n, q);
   r += (r < 0) ? q : 0;
   r -= (r >= q) ? q : 0;
   return r;
 }
 
 // Alg. 1 after the nearest-point step: the codes G^-1 P mod q, packed as nibbles.
-__device__ __forceinline__ uint32_t encode_codes(const int (&P)[8], int q, float rq) {
+// Fast path (|P_i| < 512, always true for points that do not overload, |P_i| <= 2q): add a
+// bias of 1024 q to make v non-negative and divide with a 24-bit multiply,
+// floor(u / q) = (u * mq) >> 20 with mq = ceil(2^20 / q), exact for u < 2^20 / q.
+__device__ __forceinline__ uint32_t encode_codes(const int (&P)[8], int q, float rq, uint32_t mq) {
   int v[8];
   v[0] = P[0];
   v[2] = (P[1] - P[0]) >> 1;
@@ -153,15 +183,32 @@ __device__ __forceinline__ uint32_t encode_codes(const int (&P)[8], int q, float
   v[5] = (P[6] - P[0]) >> 1;
   v[7] = (P[7] - P[0]) >> 1;
   v[1] = (5 * P[0] - P[1] - P[2] - P[3] + P[4] - P[5] - P[6] - P[7]) >> 2;
-  uint32_t w = 0;
+  int big = 0;
 #pragma unroll
-  for (int l = 0; l < 8; ++l) w |= (uint32_t)mod_q(v[l], q, rq) << (4 * l);
+  for (int l = 0; l < 8; ++l) big |= abs(P[l]);
+  uint32_t w = 0;
+  if (big < 512) {
+    // |v| <= 3 * 511 < 1024 q, so u = v + 1024 q lies in [0, 2048 q) and 2048 q < 2^20 / q
+    const int bias = q << 10;
+#pragma unroll
+    for (int l = 0; l < 8; ++l) {
+      const uint32_t u = (uint32_t)(v[l] + bias);
+      const uint32_t n = __umul24(u, mq) >> 20;
+      w |= (u - __umul24(n, (uint32_t)q)) << (4 * l);
+    }
+  } else {
+#pragma unroll
+    for (int l = 0; l < 8; ++l) w |= (uint32_t)mod_q_general(v[l], q, rq) << (4 * l);
+  }
   return w;
 }
 
 // Alg. 2 on one packed code word: X = G c, then X - q * 2 Q_E8(X / 2q) with Alg. 5 in
 // exact integers (all distances multiplied by 2q; same tie rules as nearest_e8).
-// m2q = ceil(2^16 / (2q)) gives floor(X / 2q) = (X * m2q) >> 16 exactly for 0 <= X < 2^11.
+// m2q = ceil(2^16 / (2q)) gives floor(X / 2q) = (X * m2q) >> 16 exactly for 0 <= X < 2^11,
+// and X <= 15 + 60 + 180 = 255 here.  Rounding half down, round(X / 2q) = floor((X + q - 1)
+// / 2q).  Outputs X2_l = X_l - 2q x1_l (D8) or X_l - q (2 d_l + 1) (D8+1/2); with f = X - 2q d
+// these are f - 2q g and f - q.
 __device__ __forceinline__ void decode_word(uint32_t w, int q, uint32_t m2q, int (&X2)[8]) {
   int c[8];
 #pragma unroll
@@ -171,54 +218,56 @@ __device__ __forceinline__ void decode_word(uint32_t w, int q, uint32_t m2q, int
   X[1] = c[0] + 2 * c[2];
   X[2] = c[0] + 2 * c[4];
   X[3] = c[0] + 2 * c[6];
-  X[4] = c[0] + 4 * c[1] + 2 * (c[2] + c[3] + c[4] + c[5] + c[6] + c[7]);
+  X[4] = c[0] + 4 * c[1] + 2 * ((c[2] + c[3]) + (c[4] + c[5]) + (c[6] + c[7]));
   X[5] = c[0] + 2 * c[3];
   X[6] = c[0] + 2 * c[5];
   X[7] = c[0] + 2 * c[7];
   const int den = 2 * q;
-  int d[8], g[8], E[8];
-  int sx1 = 0, sd = 0, sE = 0;
+  const uint32_t half_off = (uint32_t)(q - 1) * m2q;
+  int d[8], g[8], f[8], E[8];
 #pragma unroll
   for (int l = 0; l < 8; ++l) {
-    d[l] = (int)(((uint32_t)X[l] * m2q) >> 16);
-    const int f = X[l] - den * d[l];
-    g[l] = (2 * f > den) ? 1 : 0;
-    E[l] = min(f, den - f);
-    sx1 += d[l] + g[l];
-    sd += d[l];
-    sE += E[l];
+    d[l] = (int)(__umul24((uint32_t)X[l], m2q) >> 16);
+    const int x1 = (int)((__umul24((uint32_t)X[l], m2q) + half_off) >> 16);
+    g[l] = x1 - d[l];
+    f[l] = X[l] - __mul24(den, d[l]);
+    E[l] = min(f[l], den - f[l]);
   }
-  int p = 0, r = 0;
-  int Ep = E[0], Er = E[0];
+  const int sum_d = ((d[0] + d[1]) + (d[2] + d[3])) + ((d[4] + d[5]) + (d[6] + d[7]));
+  const int sum_g = ((g[0] + g[1]) + (g[2] + g[3])) + ((g[4] + g[5]) + (g[6] + g[7]));
+  const int sE = ((E[0] + E[1]) + (E[2] + E[3])) + ((E[4] + E[5]) + (E[6] + E[7]));
+  // argmax E / argmin E with the lowest index on ties, through keys E*8 + index
+  int kmax = (E[0] << 3) | 7, kmin = E[0] << 3;
 #pragma unroll
   for (int l = 1; l < 8; ++l) {
-    const bool up = E[l] > Ep;    // strict: the lowest index wins ties
-    const bool dn = E[l] < Er;
-    p = up ? l : p;
-    Ep = up ? E[l] : Ep;
-    r = dn ? l : r;
-    Er = dn ? E[l] : Er;
+    kmax = max(kmax, (E[l] << 3) | (7 - l));
+    kmin = min(kmin, (E[l] << 3) | l);
   }
-  const int odd1 = sx1 & 1, odd2 = sd & 1;
+  const int p = 7 - (kmax & 7), Ep = kmax >> 3;
+  const int r = kmin & 7, Er = kmin >> 3;
+  const int odd1 = (sum_d + sum_g) & 1, odd2 = sum_d & 1;
   const int gap = sE - 2 * den + (odd1 ? den - 2 * Ep : 0) - (odd2 ? 2 * Er : 0);
   const bool d8 = gap < 0;
+  // X2 = f - 2q g (D8) or f - q (D8+1/2); the fixed coordinate moves by +-2q:
+  // D8: to f - 2q g + 2q (2 g - 1);  D8+1/2: to f - q - 2q (2 g - 1)
+  const int fix = d8 ? (odd1 ? p : 8) : (odd2 ? r : 8);
 #pragma unroll
   for (int l = 0; l < 8; ++l) {
-    const int s = 2 * g[l] - 1;
-    const int a = 2 * (d[l] + g[l]) - ((odd1 && l == p) ? 2 * s : 0);
-    const int b = 2 * d[l] + 1 + ((odd2 && l == r) ? 2 * s : 0);
-    X2[l] = X[l] - q * (d8 ? a : b);
+    const int v = d8 ? (g[l] ? f[l] - den : f[l]) : f[l] - q;
+    const bool up = (g[l] != 0) == d8;     // D8 moves by +2q s, D8+1/2 by -2q s, s = 2g - 1
+    X2[l] = (l == fix) ? (up ? v + den : v - den) : v;
   }
 }
 
 // First-beta overload test of one candidate point (Sec. 4.1): overloaded iff
 // decode(encode(P)) != P.  The root bound settles every point off the cell boundary; on
 // the boundary the literal decode decides (Alg. 5's tie rules make it tie-dependent).
-__device__ __forceinline__ bool overloaded(const int (&P)[8], int q, float rq, uint32_t m2q) {
+__device__ __forceinline__ bool overloaded(const int (&P)[8], int q, float rq, uint32_t mq,
+                                           uint32_t m2q) {
   const int M = e8_root_bound(P);
   if (M != 2 * q) return M > 2 * q;
   int X2[8];
-  decode_word(encode_codes(P, q, rq), q, m2q, X2);
+  decode_word(encode_codes(P, q, rq, mq), q, m2q, X2);
   bool diff = false;
 #pragma unroll
   for (int l = 0; l < 8; ++l) diff |= (X2[l] != P[l]);

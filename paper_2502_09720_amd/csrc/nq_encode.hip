@@ -15,6 +15,13 @@
 
 namespace nq {
 
+constexpr int a_max_k = 4;
+constexpr float kRootMargin = 2.8284272f + 0.02f;  // 2 sqrt(2), rounded up, + slack
+
+__device__ __forceinline__ float pick4(const float (&c)[4], int t) {
+  return t == 0 ? c[0] : (t == 1 ? c[1] : (t == 2 ? c[2] : c[3]));
+}
+
 template <typename T>
 __device__ __forceinline__ void load_block(const T* __restrict__ p, float (&v)[8]);
 
@@ -128,21 +135,44 @@ __device__ __forceinline__ float next_down(float v) { return __uint_as_float(__f
 
 // First-beta search for one block (App. F): the smallest t whose nearest E8 point of
 // y = fl32(x * c_t) survives decode(encode(.)); t = k when every beta overloads.
+//
+// The overload test of a candidate P_t compares its root bound M(P_t) with 2q.  Since
+// |M(P_t) - 2 M(y_t)| <= 2 sqrt(2) and M(y_t) = c_t M(x) up to fp32 rounding, the bound
+// u_t = 2 c_t M(x) settles most betas without computing P_t: u_t - margin > 2q means t
+// surely overloads (it is skipped), u_t + margin < 2q means it surely does not (no test).
+// The margin 2 sqrt(2) + 0.02 + 2^-12 u_t covers the covering-radius term and the fp32
+// rounding of y_t, M and u_t (together below 2^-19 u_t).  Only betas in between are computed and tested.
 __device__ __forceinline__ void encode_block(const float (&v)[8], const float (&c)[4],
                                              const EncodeArgs& a, uint32_t& word, int& tsel) {
-  int P[8];
-  tsel = a.k - 1;
-  for (int t = 0; t < a.k; ++t) {
-    float y[8];
+  const float mx = root_bound_f(v);
+  const float two_q = (float)(2 * a.q);
+  int t = a.k - 1;
+  bool sure = false;
 #pragma unroll
-    for (int l = 0; l < 8; ++l) y[l] = v[l] * c[t];
-    nearest_e8(y, P);
-    if (t == a.k - 1 || !overloaded(P, a.q, a.rq, a.m2q)) {
-      tsel = t;
-      break;
+  for (int s = a_max_k - 1; s >= 0; --s) {
+    if (s < a.k) {
+      const float u = 2.0f * c[s] * mx;
+      const float margin = kRootMargin + u * 0x1p-12f;
+      if (u - margin <= two_q) {   // not surely overloaded: the first such beta is the start
+        t = s;
+        sure = (u + margin < two_q);
+      }
     }
   }
-  word = encode_codes(P, a.q, a.rq);
+  int P[8];
+  for (;;) {
+    float y[8];
+    const float ct = pick4(c, t);
+#pragma unroll
+    for (int l = 0; l < 8; ++l) y[l] = v[l] * ct;
+    nearest_e8(y, P);
+    if (t == a.k - 1 || sure || !overloaded(P, a.q, a.rq, a.mq, a.m2q)) break;
+    ++t;
+    const float u = 2.0f * pick4(c, t) * mx;
+    sure = (u + kRootMargin + u * 0x1p-12f < two_q);
+  }
+  tsel = t;
+  word = encode_codes(P, a.q, a.rq, a.mq);
 }
 
 // Exact RN32(sqrt(S / n)) from a double-double S and a candidate r within a few ulps.

@@ -12,13 +12,15 @@
 //   2. gemm_kernel: bf16 MFMA GEMM (C = T_A T_W^T, fp32 accumulation) with the epilogue
 //      C_ij = acc * r_Ai * r_Wj * base_A * base_W / 4.
 //
-// GEMM tiling (gfx950): a 256-thread workgroup owns a 256 x 128 tile of C; its four waves
-// (2 x 2) own 128 x 64 each, as 4 x 2 v_mfma_f32_32x32x16_bf16 tiles (128 fp32
-// accumulators per lane).  K advances 64 per stage through two LDS buffers (row stride
-// 144 B: 128 B of data + 16 B pad keeps the 16-byte fragment reads conflict-free); the
-// next stage's global loads are issued before the current stage's MFMAs.  Workgroups are
-// mapped so that the tiles resident on one XCD (workgroup id mod 8) form a compact 4 x 8
-// block of the tile grid and share their A and W rows in that XCD's L2.
+// GEMM tiling (gfx950): a workgroup of NW = WM x WN waves owns a BM x BN tile of C; each
+// wave owns (BM/WM) x (BN/WN) as v_mfma_f32_32x32x16_bf16 tiles.  K advances 64 bf16
+// (128 B per row) per stage through NSTAGE LDS buffers filled by global_load_lds_dwordx4:
+// each wave instruction moves 8 rows x 128 B straight into LDS (no register staging).  The
+// 16-byte chunk c of row r is stored at chunk c ^ (r & 7), so that the fragment reads (32
+// rows, one chunk) hit distinct LDS banks.  Stage k+NSTAGE-1 is loaded while stage k is
+// multiplied.  Workgroups are mapped so that the tiles resident on one XCD (workgroup id
+// mod 8) form a compact 4-row band of the tile grid and share their A and W rows in that
+// XCD's L2.
 #include "nq_device.hpp"
 #include "nq_kernels.hpp"
 
@@ -28,11 +30,27 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 namespace gemm {
-constexpr int BM = 256;
-constexpr int BN = 128;
-constexpr int BK = 64;            // bf16 per stage
-constexpr int ROWB = BK * 2 + 16;  // LDS bytes per tile row (padded)
+constexpr int BK = 64;  // bf16 per stage (128 B per row)
 constexpr int GROUP_M = 4;
+
+// A tile configuration: BM x BN tile, WM x WN waves, NSTAGE LDS buffers.
+template <int BM_, int BN_, int WM_, int WN_, int NSTAGE_>
+struct Cfg {
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, NSTAGE = NSTAGE_;
+  static constexpr int NW = WM * WN;
+  static constexpr int TM = BM / WM / 32;  // 32x32 MFMA tiles per wave along M
+  static constexpr int TN = BN / WN / 32;
+  static constexpr int STAGE_BYTES = (BM + BN) * BK * 2;
+  static constexpr int GROUPS = (BM + BN) / 8;  // 8-row groups per stage
+  static constexpr int GROUPS_PER_WAVE = GROUPS / NW;
+  static_assert(GROUPS % NW == 0, "row groups must split evenly over the waves");
+  static_assert(NSTAGE * STAGE_BYTES <= 160 * 1024, "LDS is 160 KB");
+};
+
+// 256 x 128 tiles (one per CU for the 8B prefill shapes) and 256 x 256 tiles (half the
+// global->LDS traffic per flop, for products with at least one tile per CU).
+using CfgMid = Cfg<256, 128, 4, 2, 3>;
+using CfgBig = Cfg<256, 256, 4, 2, 2>;
 }  // namespace gemm
 
 // t * X2 of every block of a coded operand, as bf16, into ws[rows_p][k_p] (zero padding).
@@ -61,104 +79,174 @@ __global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__
 }
 
 __device__ __forceinline__ void tile_coords(int bid, int tm, int tn, int& pm, int& pn) {
+  constexpr int GROUP_M = gemm::GROUP_M;
   // XCD-contiguous numbering: workgroups bid, bid+8, ... run on one XCD
   const int total = tm * tn;
   int t = bid;
   if ((total & 7) == 0) t = (bid & 7) * (total >> 3) + (bid >> 3);
-  const int width = gemm::GROUP_M * tn;
+  const int width = GROUP_M * tn;
   const int g = t / width;
-  const int first = g * gemm::GROUP_M;
-  const int gm = min(tm - first, gemm::GROUP_M);
+  const int first = g * GROUP_M;
+  const int gm = min(tm - first, GROUP_M);
   const int r = t - g * width;
   pm = first + r % gm;
   pn = r / gm;
 }
 
-__global__ __launch_bounds__(256, 1) void gemm_kernel(const u32x4* __restrict__ ta,
-                                                      const u32x4* __restrict__ tw, int kp,
-                                                      int tm, int tn, const float* __restrict__ ra,
-                                                      const float* __restrict__ rw, int64_t M,
-                                                      int64_t N, float* __restrict__ c,
-                                                      int64_t ldc, float scale) {
-  using namespace gemm;
-  extern __shared__ __attribute__((aligned(16))) unsigned char lds[];
-  // buffer b of the A tile at lds + b*BM*ROWB; of the W tile after both A buffers
-  auto As = [&](int b) { return lds + b * (BM * ROWB); };
-  auto Ws = [&](int b) { return lds + 2 * BM * ROWB + b * (BN * ROWB); };
+typedef __attribute__((address_space(3))) void lds_void;
+
+// LDS swizzle: chunk c of row r lives at chunk c ^ swz(r), with
+// swz(r) = (r mod 8) ^ ((r / 8) mod 4), a function of r mod 32 only (every 32-row MFMA tile
+// starts at a multiple of 32).  The 16-byte fragment reads of 32 consecutive rows at one
+// logical chunk then fall in distinct bank groups whether the LDS serves 8, 16 or 32
+// lanes of a 128-bit read per cycle.
+__device__ __forceinline__ int swz(int r) { return (r ^ ((r >> 3) & 3)) & 7; }
+
+template <class C>
+__global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
+    const u32x4* __restrict__ ta, const u32x4* __restrict__ tw, int kp, int tm, int tn,
+    const float* __restrict__ ra, const float* __restrict__ rw, int64_t M, int64_t N,
+    float* __restrict__ c, int64_t ldc, float scale) {
+  constexpr int BM = C::BM, BN = C::BN, WM = C::WM, WN = C::WN, NSTAGE = C::NSTAGE;
+  constexpr int NW = C::NW, TM = C::TM, TN = C::TN, STAGE_BYTES = C::STAGE_BYTES;
+  constexpr int GROUPS_PER_WAVE = C::GROUPS_PER_WAVE;
+  constexpr int BK = gemm::BK;
+  extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
 
   int pm, pn;
   tile_coords(blockIdx.x, tm, tn, pm, pn);
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
   const int kc = kp >> 3;  // 16-byte chunks per row
 
-  // global -> register staging: thread loads chunk (tid & 7) of rows (tid >> 3) + 32 i
-  const u32x4* ga = ta + ((int64_t)pm * BM + (tid >> 3)) * kc + (tid & 7);
-  const u32x4* gw = tw + ((int64_t)pn * BN + (tid >> 3)) * kc + (tid & 7);
-  const int soff = (tid >> 3) * ROWB + (tid & 7) * 16;
-  u32x4 ra_[BM / 32], rw_[BN / 32];
-
-  auto gload = [&](int ks) {
+  // This lane's source for each of the wave's row groups: row (lane >> 3) of the group,
+  // stored at physical chunk lane & 7, i.e. logical chunk (lane & 7) ^ swz(row).
+  const int lrow = lane >> 3;
+  const u32x4* src[GROUPS_PER_WAVE];
+  int dst[GROUPS_PER_WAVE];
 #pragma unroll
-    for (int i = 0; i < BM / 32; ++i) ra_[i] = __builtin_nontemporal_load(ga + (int64_t)i * 32 * kc + ks * (BK / 8));
+  for (int i = 0; i < GROUPS_PER_WAVE; ++i) {
+    const int grp = wave + i * NW;              // 0 .. GROUPS-1; A groups first
+    const int row = grp * 8 + lrow;             // row within the stage (A rows, then W rows)
+    const int lchunk = (lane & 7) ^ swz(row);
+    if (grp < BM / 8) {
+      src[i] = ta + ((int64_t)pm * BM + row) * kc + lchunk;
+    } else {
+      src[i] = tw + ((int64_t)pn * BN + (row - BM)) * kc + lchunk;
+    }
+    dst[i] = grp * 1024;                        // 8 rows x 128 B
+  }
+  auto load_stage = [&](int ks) {
+    unsigned char* base = lds + (ks % NSTAGE) * STAGE_BYTES;
 #pragma unroll
-    for (int i = 0; i < BN / 32; ++i) rw_[i] = __builtin_nontemporal_load(gw + (int64_t)i * 32 * kc + ks * (BK / 8));
+    for (int i = 0; i < GROUPS_PER_WAVE; ++i)
+      __builtin_amdgcn_global_load_lds((const void*)(src[i] + ks * (BK / 8)),
+                                       (lds_void*)(base + dst[i]), 16, 0, 0);
   };
-  auto swrite = [&](int b) {
-#pragma unroll
-    for (int i = 0; i < BM / 32; ++i) *reinterpret_cast<u32x4*>(As(b) + soff + i * 32 * ROWB) = ra_[i];
-#pragma unroll
-    for (int i = 0; i < BN / 32; ++i) *reinterpret_cast<u32x4*>(Ws(b) + soff + i * 32 * ROWB) = rw_[i];
-  };
 
-  f32x16 acc[4][2];
+  f32x16 acc[TM][TN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
 
+  // fragment reads: row (lane & 31) of a 32-row tile, logical chunk 2 kk + (lane >> 5).  The
+  // swizzle depends only on the row modulo 32, and every 32-row tile starts at a multiple
+  // of 32, so one offset per kk serves all of this lane's A and W tiles.
+  const int frow = lane & 31;
+  const int abase = (wm * (BM / WM) + frow) * 128;
+  const int wbase = BM * 128 + (wn * (BN / WN) + frow) * 128;
+  int coff[BK / 16];
+#pragma unroll
+  for (int kk = 0; kk < BK / 16; ++kk) coff[kk] = ((2 * kk + (lane >> 5)) ^ swz(frow)) * 16;
+
   const int nks = kp / BK;
-  gload(0);
-  swrite(0);
-  __syncthreads();
-  // fragment read offsets: row (lane & 31) of the 32-row tile, 16-byte chunk (lane >> 5)
-  const int aoff = (wm * 128 + (lane & 31)) * ROWB + (lane >> 5) * 16;
-  const int woff = (wn * 64 + (lane & 31)) * ROWB + (lane >> 5) * 16;
+#pragma unroll
+  for (int s = 0; s < NSTAGE - 1; ++s)
+    if (s < nks) load_stage(s);
+
   for (int ks = 0; ks < nks; ++ks) {
-    const int b = ks & 1;
-    if (ks + 1 < nks) gload(ks + 1);
-#pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      bf16x8 af[4], bfr[2];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        af[i] = *reinterpret_cast<const bf16x8*>(As(b) + aoff + i * 32 * ROWB + kk * 32);
-#pragma unroll
-      for (int j = 0; j < 2; ++j)
-        bfr[j] = *reinterpret_cast<const bf16x8*>(Ws(b) + woff + j * 32 * ROWB + kk * 32);
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+    // stage ks has landed when at most the later stages' loads are outstanding
+    if (ks + NSTAGE - 2 < nks) {
+      __builtin_amdgcn_s_waitcnt((GROUPS_PER_WAVE * (NSTAGE - 2)) | (0x7 << 4) | (0xF << 8));
+    } else {
+      __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xF << 8));
     }
-    if (ks + 1 < nks) swrite(b ^ 1);
-    __syncthreads();
+    // Barrier without a memory fence: a fence would wait for every outstanding LDS DMA,
+    // including the stages still being prefetched.  Each wave has waited for its own
+    // loads of stage ks above, and its reads of the buffer reloaded below finished before
+    // the MFMAs that consumed them.  The signal fences keep the compiler from moving LDS
+    // accesses across the barrier.
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    const bool prefetch = ks + NSTAGE - 1 < nks;
+    unsigned char* nb = lds + ((ks + NSTAGE - 1) % NSTAGE) * STAGE_BYTES;
+    const unsigned char* sb = lds + (ks % NSTAGE) * STAGE_BYTES;
+    // Fragments are double-buffered in registers.  Within a step the MFMAs are interleaved
+    // one by one with the LDS reads of the next step and with this wave's share of the
+    // next stage's global loads, so that neither the LDS nor the texture path receives
+    // its requests in one burst that would hold up the MFMA issue.
+    bf16x8 af[2][TM], bfr[2][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+      af[0][i] = *reinterpret_cast<const bf16x8*>(sb + abase + i * 32 * 128 + coff[0]);
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+      bfr[0][j] = *reinterpret_cast<const bf16x8*>(sb + wbase + j * 32 * 128 + coff[0]);
+    constexpr int KSTEPS = BK / 16;
+    constexpr int LOADS_PER_STEP = (GROUPS_PER_WAVE + KSTEPS - 1) / KSTEPS;
+#pragma unroll
+    for (int kk = 0; kk < KSTEPS; ++kk) {
+      const int cur = kk & 1;
+#pragma unroll
+      for (int m = 0; m < TM * TN; ++m) {
+        const int i = m / TN, j = m % TN;
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
+        if (kk + 1 < KSTEPS) {
+          if (m < TM) {
+            af[cur ^ 1][m] = *reinterpret_cast<const bf16x8*>(sb + abase + m * 32 * 128 + coff[kk + 1]);
+          } else if (m < TM + TN) {
+            bfr[cur ^ 1][m - TM] = *reinterpret_cast<const bf16x8*>(sb + wbase + (m - TM) * 32 * 128 + coff[kk + 1]);
+          }
+        }
+        const int g = kk * LOADS_PER_STEP + m;
+        if (prefetch && m < LOADS_PER_STEP && g < GROUPS_PER_WAVE)
+          __builtin_amdgcn_global_load_lds((const void*)(src[g] + (ks + NSTAGE - 1) * (BK / 8)),
+                                           (lds_void*)(nb + dst[g]), 16, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // reads and loads left over when a step has fewer MFMAs than them
+#pragma unroll
+      for (int m = TM * TN; m < TM + TN || m < LOADS_PER_STEP; ++m) {
+        if (kk + 1 < KSTEPS) {
+          if (m < TM) {
+            af[cur ^ 1][m] = *reinterpret_cast<const bf16x8*>(sb + abase + m * 32 * 128 + coff[kk + 1]);
+          } else if (m < TM + TN) {
+            bfr[cur ^ 1][m - TM] = *reinterpret_cast<const bf16x8*>(sb + wbase + (m - TM) * 32 * 128 + coff[kk + 1]);
+          }
+        }
+        const int g = kk * LOADS_PER_STEP + m;
+        if (prefetch && m < LOADS_PER_STEP && g < GROUPS_PER_WAVE)
+          __builtin_amdgcn_global_load_lds((const void*)(src[g] + (ks + NSTAGE - 1) * (BK / 8)),
+                                           (lds_void*)(nb + dst[g]), 16, 0, 0);
+      }
+    }
   }
 
   // Epilogue.  32x32 accumulator layout: lane l holds column l%32; register e holds row
   // 8*(e/4) + 4*(l/32) + (e%4).
-  const int64_t m0 = (int64_t)pm * BM + wm * 128;
-  const int64_t n0 = (int64_t)pn * BN + wn * 64;
+  const int64_t m0 = (int64_t)pm * BM + wm * (BM / WM);
+  const int64_t n0 = (int64_t)pn * BN + wn * (BN / WN);
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < TN; ++j) {
     const int64_t col = n0 + j * 32 + (lane & 31);
     const float sw = col < N ? rw[col] * scale : 0.0f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const int64_t row = m0 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
@@ -167,12 +255,23 @@ __global__ __launch_bounds__(256, 1) void gemm_kernel(const u32x4* __restrict__ 
   }
 }
 
+// Both tile configurations pad M to 256; N is padded to 256 (a multiple of both BN).
 size_t decode_once_workspace(int64_t M, int64_t N, int64_t K) {
   using namespace gemm;
-  const int64_t mp = (M + BM - 1) / BM * BM;
-  const int64_t np = (N + BN - 1) / BN * BN;
+  const int64_t mp = (M + 255) / 256 * 256;
+  const int64_t np = (N + 255) / 256 * 256;
   const int64_t kp = (K + BK - 1) / BK * BK;
   return (size_t)((mp + np) * kp * 2);
+}
+
+template <class C>
+static void launch_gemm(const u32x4* wa, const u32x4* ww, int kp, int64_t mp, int64_t np,
+                        const MatmulOperand& A, const MatmulOperand& W, float* c, int64_t ldc,
+                        float scale, hipStream_t st) {
+  const int tm = (int)(mp / C::BM), tn = (int)(np / C::BN);
+  hipLaunchKernelGGL(gemm_kernel<C>, dim3((unsigned)(tm * tn)), dim3(C::NW * 64),
+                     (size_t)C::NSTAGE * C::STAGE_BYTES, st, wa, ww, kp, tm, tn, A.scales,
+                     W.scales, A.rows, W.rows, c, ldc, scale);
 }
 
 hipError_t launch_matmul_decode_once(const MatmulOperand& A, const MatmulOperand& W, int64_t K,
@@ -180,8 +279,8 @@ hipError_t launch_matmul_decode_once(const MatmulOperand& A, const MatmulOperand
                                      hipStream_t st) {
   using namespace gemm;
   const int nb = (int)(K / 8);
-  const int64_t mp = (A.rows + BM - 1) / BM * BM;
-  const int64_t np = (W.rows + BN - 1) / BN * BN;
+  const int64_t mp = (A.rows + 255) / 256 * 256;
+  const int64_t np = (W.rows + 255) / 256 * 256;
   const int kp = (int)((K + BK - 1) / BK * BK);
   const int nbp = kp / 8;
   u32x4* wa = reinterpret_cast<u32x4*>(ws);
@@ -190,18 +289,24 @@ hipError_t launch_matmul_decode_once(const MatmulOperand& A, const MatmulOperand
                      A.codes, A.beta, A.rows, nb, mp, nbp, A.q, A.m2q, wa);
   hipLaunchKernelGGL(tiles_kernel, dim3((unsigned)((np * nbp + 255) / 256)), dim3(256), 0, st,
                      W.codes, W.beta, W.rows, nb, np, nbp, W.q, W.m2q, ww);
-  const int tm = (int)(mp / BM), tn = (int)(np / BN);
-  const size_t lds = (size_t)2 * (BM + BN) * ROWB;
-  hipLaunchKernelGGL(gemm_kernel, dim3((unsigned)(tm * tn)), dim3(256), lds, st, wa, ww, kp, tm,
-                     tn, A.scales, W.scales, A.rows, W.rows, c, ldc, scale);
+  // 256 x 256 tiles once they give every CU a tile, else 256 x 128
+  if ((mp / 256) * (np / 256) >= 256) {
+    launch_gemm<CfgBig>(wa, ww, kp, mp, np, A, W, c, ldc, scale, st);
+  } else {
+    launch_gemm<CfgMid>(wa, ww, kp, mp, np, A, W, c, ldc, scale, st);
+  }
   return hipGetLastError();
 }
 
 hipError_t gemm_set_attributes() {
   using namespace gemm;
-  return hipFuncSetAttribute((const void*)gemm_kernel,
+  hipError_t e = hipFuncSetAttribute((const void*)gemm_kernel<CfgMid>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize,
+                                     CfgMid::NSTAGE * CfgMid::STAGE_BYTES);
+  if (e != hipSuccess) return e;
+  return hipFuncSetAttribute((const void*)gemm_kernel<CfgBig>,
                              hipFuncAttributeMaxDynamicSharedMemorySize,
-                             (int)(2 * (BM + BN) * ROWB));
+                             CfgBig::NSTAGE * CfgBig::STAGE_BYTES);
 }
 
 }  // namespace nq

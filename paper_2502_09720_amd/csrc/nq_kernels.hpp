@@ -11,6 +11,7 @@ struct EncodeArgs {
   int k;           // number of betas
   float rq;        // fl32(1 / q), estimate for the mod-q reduction
   uint32_t m2q;    // ceil(2^16 / (2q)): floor(X / 2q) = (X * m2q) >> 16 for 0 <= X < 2^11
+  uint32_t mq;     // ceil(2^20 / q): floor(u / q) = (u * mq) >> 20 for 0 <= u < 2048 q
   double beta[4];  // fl64(t * base), t = 1..4
 };
 
@@ -51,5 +52,6 @@ hipError_t gemm_set_attributes();
 constexpr int64_t kFusedMaxM = 64;
 
 inline uint32_t magic_2q(int q) { return (uint32_t)((65536 + 2 * q - 1) / (2 * q)); }
+inline uint32_t magic_q(int q) { return (uint32_t)(((1u << 20) + q - 1) / q); }
 
 }  // namespace nq

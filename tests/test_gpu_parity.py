@@ -282,3 +282,17 @@ def test_matmul_internal_workspace_matches_ex(nq):
     torch.cuda.synchronize()
     assert torch.equal(out, ref)
     assert np.linalg.norm(out.cpu().numpy() - C) / np.linalg.norm(C) < 1e-6
+
+
+def test_encode_tiny_entries(nq):
+    """Entries many orders of magnitude below the row scale (the lattice input is then a
+    tiny number of either sign next to exact zeros), in fp32 and bf16."""
+    rng = np.random.default_rng(77)
+    x = rng.standard_normal((64, 256))
+    mask = rng.random((64, 256)) < 0.3
+    x[mask] = rng.choice([-1.0, 1.0], mask.sum()) * 10.0 ** rng.uniform(-30, -6, mask.sum())
+    x[rng.random((64, 256)) < 0.1] = 0.0
+    for dtype in ("f32", "bf16"):
+        store, x32 = workloads.round_to(x, dtype)
+        check_encode(nq, store, x32, dtype, 14, 4)
+        check_encode(nq, store, x32, dtype, 7, 4)
