@@ -30,11 +30,14 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict_
   const uint32_t bw = beta[row * nbw + (j >> 4)];
   const int t = (int)((bw >> (2 * (j & 15))) & 3u);
   const double sc = (double)scales[row] * a.half_beta[t];
-  int X2[8];
-  decode_word(w, a.q, a.m2q, X2);
+  uint32_t X2p[4];
+  decode_word_pk(w, a.q, a.m2q, X2p);
   float v[8];
 #pragma unroll
-  for (int l = 0; l < 8; ++l) v[l] = (float)(sc * (double)X2[l]);
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = (float)(sc * (double)(int)(short)(X2p[i] & 0xFFFFu));
+    v[2 * i + 1] = (float)(sc * (double)((int)X2p[i] >> 16));
+  }
   if constexpr (OUT == 0) {
     f32x4* o = reinterpret_cast<f32x4*>((float*)out + row * ld_out + 8 * j);
     const f32x4 lo = {v[0], v[1], v[2], v[3]};

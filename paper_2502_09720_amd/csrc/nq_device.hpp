@@ -259,19 +259,200 @@ __device__ __forceinline__ void decode_word(uint32_t w, int q, uint32_t m2q, int
   }
 }
 
+// ---------------------------------------------------------------------------------------
+// Alg. 2 on one code word with two coordinates per 32-bit register (packed 16-bit integer
+// instructions).  Same arithmetic and tie rules as decode_word; output X2 as four packed
+// int16 pairs (coordinates 2i, 2i+1 in the low and high halves of word i).
+//
+// Shifting X by 2q * v with v in D8 leaves the decode unchanged (Alg. 5 commutes with D8
+// shifts), so only f = X mod 2q per coordinate and the parity pi of sum floor(X / 2q)
+// matter.  With h = f - q: the D8+1/2 residual is h, the D8 residual is f - 2q [h > 0], the
+// distance to the nearest integer (times 2q) is q - |h|, so argmax / argmin of it are
+// argmin / argmax |h| (lowest index), and the gap of Alg. 5 times 2q is
+//   4q - sum |h| + odd1 * 2 min|h| - pi * (2q - 2 max|h|),   odd1 = (pi + #[h > 0]) mod 2.
+// ---------------------------------------------------------------------------------------
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+typedef short i16x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ u16x2 as_u16x2(uint32_t v) { return __builtin_bit_cast(u16x2, v); }
+__device__ __forceinline__ i16x2 as_i16x2(uint32_t v) { return __builtin_bit_cast(i16x2, v); }
+__device__ __forceinline__ uint32_t bits32(u16x2 v) { return __builtin_bit_cast(uint32_t, v); }
+__device__ __forceinline__ uint32_t bits32(i16x2 v) { return __builtin_bit_cast(uint32_t, v); }
+
+__device__ __forceinline__ void decode_word_pk(uint32_t w, int q, uint32_t m2q,
+                                               uint32_t (&X2)[4]) {
+  const uint32_t E = w & 0x0F0F0F0Fu;         // bytes c0 c2 c4 c6
+  const uint32_t O = (w >> 4) & 0x0F0F0F0Fu;  // bytes c1 c3 c5 c7
+  // v_perm_b32 selectors (byte 0x0c reads as zero): pairs as 16-bit lanes
+  const u16x2 cc = as_u16x2(__builtin_amdgcn_perm(0u, E, 0x0C000C00u));   // (c0, c0)
+  const u16x2 p02 = as_u16x2(__builtin_amdgcn_perm(0u, E, 0x0C010C0Cu));  // (0, c2)
+  const u16x2 p46 = as_u16x2(__builtin_amdgcn_perm(0u, E, 0x0C030C02u));  // (c4, c6)
+  const u16x2 p13 = as_u16x2(__builtin_amdgcn_perm(0u, O, 0x0C010C00u));  // (c1, c3)
+  const u16x2 p57 = as_u16x2(__builtin_amdgcn_perm(0u, O, 0x0C030C02u));  // (c5, c7)
+  const u16x2 two = {2, 2};
+  const uint32_t sum_c = __builtin_amdgcn_sad_u8(E, 0u, __builtin_amdgcn_sad_u8(O, 0u, 0u));
+  const uint32_t c0 = E & 0xFFu;
+  // X = G c: X1 = c0 + 2 c2, X2/X3 = c0 + 2 (c4, c6), X5 = c0 + 2 c3, X6/X7 = c0 + 2 (c5, c7),
+  // X4 = c0 + 4 c1 + 2 (c2 + ... + c7) = (c0 + 2 c1) + 2 (sum c - c0)
+  uint32_t R[4];
+  R[0] = bits32(cc + p02 * two);
+  R[1] = bits32(cc + p46 * two);
+  R[2] = bits32(cc + p13 * two) + 2u * (sum_c - c0);  // low half stays below 2^16
+  R[3] = bits32(cc + p57 * two);
+  const uint32_t den = 2u * (uint32_t)q;
+  const u16x2 den2 = {(unsigned short)den, (unsigned short)den};
+  const u16x2 qq = {(unsigned short)q, (unsigned short)q};
+  // f = X mod 2q: X < 3q for every coordinate but X4, so one conditional subtraction
+  uint32_t m[4], f[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const u16x2 x = as_u16x2(R[i]);
+    const u16x2 xm = x - den2;                  // wraps when X < 2q
+    m[i] = bits32(xm);
+    f[i] = bits32(__builtin_elementwise_min(x, xm));
+  }
+  const uint32_t X4 = R[2] & 0xFFFFu;
+  const uint32_t d4 = __umul24(X4, m2q) >> 16;
+  const uint32_t f4 = X4 - __umul24(d4, den);
+  f[2] = (f[2] & 0xFFFF0000u) | f4;
+  // parity of sum floor(X / 2q): bit 15 of each (X - 2q) lane is set iff X < 2q
+  const uint32_t lt = (m[0] & 0x80008000u) | ((m[1] & 0x80008000u) >> 1) |
+                      ((m[2] & 0x80000000u) >> 2) | ((m[3] & 0x80008000u) >> 3);
+  const uint32_t pi = (1u + __builtin_popcount(lt) + d4) & 1u;   // (7 - #lt + d4) mod 2
+  // h = f - q, |h|, g = [h > 0] (sign bit of -h)
+  uint32_t h[4], neg[4], ah[4];
+  uint32_t sum_ah = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const i16x2 hh = as_i16x2(bits32(as_u16x2(f[i]) - qq));
+    const i16x2 nn = -hh;
+    h[i] = bits32(hh);
+    neg[i] = bits32(nn);
+    ah[i] = bits32(__builtin_elementwise_max(hh, nn));
+    sum_ah = __builtin_amdgcn_sad_u16(f[i], bits32(qq), sum_ah);
+  }
+  const uint32_t gb = (neg[0] & 0x80008000u) | ((neg[1] & 0x80008000u) >> 1) |
+                      ((neg[2] & 0x80008000u) >> 2) | ((neg[3] & 0x80008000u) >> 3);
+  const uint32_t odd1 = (pi + __builtin_popcount(gb)) & 1u;
+  // keys |h| * 8 + index (min: argmin |h|, lowest index) and |h| * 8 + 7 - index (max)
+  const uint32_t kidx_min[4] = {0x00010000u, 0x00030002u, 0x00050004u, 0x00070006u};
+  const uint32_t kidx_max[4] = {0x00060007u, 0x00040005u, 0x00020003u, 0x00000001u};
+  const u16x2 eight = {8, 8};
+  u16x2 kmin2 = as_u16x2(ah[0]) * eight + as_u16x2(kidx_min[0]);
+  u16x2 kmax2 = as_u16x2(ah[0]) * eight + as_u16x2(kidx_max[0]);
+#pragma unroll
+  for (int i = 1; i < 4; ++i) {
+    kmin2 = __builtin_elementwise_min(kmin2, as_u16x2(ah[i]) * eight + as_u16x2(kidx_min[i]));
+    kmax2 = __builtin_elementwise_max(kmax2, as_u16x2(ah[i]) * eight + as_u16x2(kidx_max[i]));
+  }
+  const uint32_t kmin = min((uint32_t)kmin2.x, (uint32_t)kmin2.y);
+  const uint32_t kmax = max((uint32_t)kmax2.x, (uint32_t)kmax2.y);
+  const int p = (int)(kmin & 7u), r = 7 - (int)(kmax & 7u);
+  const int minh = (int)(kmin >> 3), maxh = (int)(kmax >> 3);
+  const int gap = 4 * q - (int)sum_ah + (odd1 ? 2 * minh : 0) - (pi ? 2 * q - 2 * maxh : 0);
+  const bool d8 = gap < 0;
+  // residuals: D8 c = f - 2q g, D8+1/2 h
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const u16x2 g2 = as_u16x2(neg[i]) >> (u16x2){15, 15};
+    const uint32_t c = bits32(as_u16x2(f[i]) - g2 * den2);
+    X2[i] = d8 ? c : h[i];
+  }
+  // the fixed coordinate moves by +-2q: D8 by +2q s, D8+1/2 by -2q s, s = 2 g - 1
+  const int idx = d8 ? p : r;
+  const bool fix = d8 ? (odd1 != 0) : (pi != 0);
+  const int pos = (idx & 1) ? 31 - (idx >> 1) : 15 - (idx >> 1);
+  const bool gi = ((gb >> pos) & 1u) != 0;
+  const int delta = fix ? ((gi == d8) ? (int)den : -(int)den) : 0;
+  const uint32_t dl = ((uint32_t)delta & 0xFFFFu) << (16 * (idx & 1));
+  const int word = idx >> 1;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    X2[i] = bits32(as_u16x2(X2[i]) + as_u16x2(word == i ? dl : 0u));
+}
+
+// t * X2 of one block as eight bf16 (exact: |t X2| <= 4 * 32 = 128 < 2^8): the upper halves
+// of the fp32 values, coordinates 2i and 2i+1 in word i.
+__device__ __forceinline__ u32x4 decode_tile_bf16(uint32_t w, int t, int q, uint32_t m2q) {
+  uint32_t X2p[4];
+  decode_word_pk(w, q, m2q, X2p);
+  uint32_t o[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int lo = (int)(short)(X2p[i] & 0xFFFFu) * t;
+    const int hi = ((int)X2p[i] >> 16) * t;
+    o[i] = __builtin_amdgcn_perm(__float_as_uint((float)hi), __float_as_uint((float)lo),
+                                 0x07060302u);
+  }
+  return u32x4{o[0], o[1], o[2], o[3]};
+}
+
+// The decoder's residual X - q * 2 Q_E8(X / 2q) for integer X >= 0 (< 2^11), scalar form of
+// decode_word without the generator step.
+__device__ __forceinline__ void residual_from_X(const int (&X)[8], int q, uint32_t m2q,
+                                                int (&X2)[8]) {
+  const int den = 2 * q;
+  const uint32_t half_off = (uint32_t)(q - 1) * m2q;
+  int d[8], g[8], f[8], E[8];
+#pragma unroll
+  for (int l = 0; l < 8; ++l) {
+    d[l] = (int)(__umul24((uint32_t)X[l], m2q) >> 16);
+    const int x1 = (int)((__umul24((uint32_t)X[l], m2q) + half_off) >> 16);
+    g[l] = x1 - d[l];
+    f[l] = X[l] - __mul24(den, d[l]);
+    E[l] = min(f[l], den - f[l]);
+  }
+  const int sum_d = ((d[0] + d[1]) + (d[2] + d[3])) + ((d[4] + d[5]) + (d[6] + d[7]));
+  const int sum_g = ((g[0] + g[1]) + (g[2] + g[3])) + ((g[4] + g[5]) + (g[6] + g[7]));
+  const int sE = ((E[0] + E[1]) + (E[2] + E[3])) + ((E[4] + E[5]) + (E[6] + E[7]));
+  int kmax = (E[0] << 3) | 7, kmin = E[0] << 3;
+#pragma unroll
+  for (int l = 1; l < 8; ++l) {
+    kmax = max(kmax, (E[l] << 3) | (7 - l));
+    kmin = min(kmin, (E[l] << 3) | l);
+  }
+  const int p = 7 - (kmax & 7), Ep = kmax >> 3;
+  const int r = kmin & 7, Er = kmin >> 3;
+  const int odd1 = (sum_d + sum_g) & 1, odd2 = sum_d & 1;
+  const int gap = sE - 2 * den + (odd1 ? den - 2 * Ep : 0) - (odd2 ? 2 * Er : 0);
+  const bool d8 = gap < 0;
+  const int fix = d8 ? (odd1 ? p : 8) : (odd2 ? r : 8);
+#pragma unroll
+  for (int l = 0; l < 8; ++l) {
+    const int v = d8 ? (g[l] ? f[l] - den : f[l]) : f[l] - q;
+    const bool up = (g[l] != 0) == d8;
+    X2[l] = (l == fix) ? (up ? v + den : v - den) : v;
+  }
+}
+
 // First-beta overload test of one candidate point (Sec. 4.1): overloaded iff
-// decode(encode(P)) != P.  The root bound settles every point off the cell boundary; on
-// the boundary the literal decode decides (Alg. 5's tie rules make it tie-dependent).
-__device__ __forceinline__ bool overloaded(const int (&P)[8], int q, float rq, uint32_t mq,
-                                           uint32_t m2q) {
-  const int M = e8_root_bound(P);
-  if (M != 2 * q) return M > 2 * q;
-  int X2[8];
-  decode_word(encode_codes(P, q, rq, mq), q, m2q, X2);
+// decode(encode(P)) != P.  The root bound settles every point off the cell boundary.  On the
+// boundary (M(P) = 2q, where Alg. 5's tie rules decide) the literal test is evaluated
+// without building the code word: the decoder sees X = G (G^-1 P mod q) = P + 2q v with v in
+// E8, and the residual of Alg. 2 is unchanged by D8 shifts of X / 2q, so it equals the
+// residual of P (v in D8) or of P + q (1,...,1) (v in D8 + 1/2).  v lies in D8 + 1/2 exactly
+// when floor(P_0 / q) is odd (column 0 of G is the only odd column).  An offset of 4q
+// (= 2q * (2,...,2), in D8) keeps X non-negative.
+__device__ __forceinline__ bool boundary_overloaded(const int (&P)[8], int q, uint32_t mq,
+                                                    uint32_t m2q) {
+  const uint32_t u0 = (uint32_t)(P[0] + 4 * q);               // P_0 >= -2q on the boundary
+  const int odd = (int)((__umul24(u0, mq) >> 20) & 1u);       // parity of floor(P_0 / q)
+  const int off = 4 * q + (odd ? q : 0);
+  int X[8], X2[8];
+#pragma unroll
+  for (int l = 0; l < 8; ++l) X[l] = P[l] + off;
+  residual_from_X(X, q, m2q, X2);
   bool diff = false;
 #pragma unroll
   for (int l = 0; l < 8; ++l) diff |= (X2[l] != P[l]);
   return diff;
+}
+
+__device__ __forceinline__ bool overloaded(const int (&P)[8], int q, float rq, uint32_t mq,
+                                           uint32_t m2q) {
+  const int M = e8_root_bound(P);
+  if (M != 2 * q) return M > 2 * q;
+  return boundary_overloaded(P, q, mq, m2q);
 }
 
 }  // namespace nq

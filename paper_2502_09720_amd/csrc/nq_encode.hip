@@ -313,6 +313,283 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_kernel(
 }
 
 // ---------------------------------------------------------------------------------------
+// Wave-compacted encoder.
+//
+// A wave owns 64 * BPT blocks ("slots"): slot i of lane l is block j of row row_w, with
+//   LANES <  64: row_w = i * (64 / LANES) + l / LANES, j = l % LANES  (a row per lane group
+//                and pass; 64 / LANES * BPT rows per wave)
+//   LANES == 64: row_w = 0, j = l + 64 i                              (one row per wave)
+//   LANES == 256: row_w = 0, j = 64 * wave + l + 256 i                (one row per workgroup)
+// Phase 1 evaluates every slot at the predicted beta (see encode_block) and finishes it
+// unless the point's root bound says it overloads or lies on the cell boundary.  Those slots
+// (about 18% on Gaussian-like rows) go to a per-wave queue in LDS, and phase 2 finishes them
+// with every lane busy, instead of the whole wave paying for the work a few lanes need.  Two-bit beta
+// indices are staged in LDS and packed into words at the end.
+// ---------------------------------------------------------------------------------------
+template <int LANES, int BPT>
+struct SlotMap {
+  static constexpr bool WGROW = LANES > 64;
+  static constexpr int RPP = LANES < 64 ? 64 / LANES : 1;           // rows per pass
+  static constexpr int ROWS_PER_WAVE = LANES < 64 ? RPP * BPT : 1;
+  static constexpr int SLOTS = 64 * BPT;
+  __device__ static int row_w(int i, int l) { return LANES < 64 ? i * RPP + l / LANES : 0; }
+  __device__ static int j(int i, int l, int wave) {
+    return LANES < 64 ? l % LANES : (LANES == 64 ? l + 64 * i : 64 * wave + l + LANES * i);
+  }
+};
+
+// Finish a block from a given first beta: loop until a point survives (or t = k).
+__device__ __forceinline__ void finish_block(const float (&v)[8], const float (&c)[4], int t,
+                                             const EncodeArgs& a, uint32_t& word, int& tsel) {
+  const float mx = root_bound_f(v);
+  const float two_q = (float)(2 * a.q);
+  int P[8];
+  for (;;) {
+    const float ct = pick4(c, t);
+    float y[8];
+#pragma unroll
+    for (int l = 0; l < 8; ++l) y[l] = v[l] * ct;
+    nearest_e8(y, P);
+    const float u = 2.0f * ct * mx;
+    const bool sure = u + kRootMargin + u * 0x1p-12f < two_q;
+    if (t == a.k - 1 || sure || !overloaded(P, a.q, a.rq, a.mq, a.m2q)) break;
+    ++t;
+  }
+  tsel = t;
+  word = encode_codes(P, a.q, a.rq, a.mq);
+}
+
+// Raw input of one block kept in registers: 16 B for 16-bit types, 32 B for fp32.
+template <typename T> struct RawBlock { u32x4 w; };
+template <> struct RawBlock<float> { f32x4 a, b; };
+
+template <typename T>
+__device__ __forceinline__ void load_raw(const T* __restrict__ p, RawBlock<T>& r) {
+  r.w = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+template <>
+__device__ __forceinline__ void load_raw<float>(const float* __restrict__ p, RawBlock<float>& r) {
+  r.a = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p));
+  r.b = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p) + 1);
+}
+template <typename T>
+__device__ __forceinline__ void zero_raw(RawBlock<T>& r) { r.w = u32x4{0u, 0u, 0u, 0u}; }
+template <>
+__device__ __forceinline__ void zero_raw<float>(RawBlock<float>& r) {
+  r.a = f32x4{0.f, 0.f, 0.f, 0.f};
+  r.b = r.a;
+}
+template <typename T>
+__device__ __forceinline__ void unpack_raw(const RawBlock<T>& r, float (&v)[8]);
+template <>
+__device__ __forceinline__ void unpack_raw<float>(const RawBlock<float>& r, float (&v)[8]) {
+  v[0] = r.a.x; v[1] = r.a.y; v[2] = r.a.z; v[3] = r.a.w;
+  v[4] = r.b.x; v[5] = r.b.y; v[6] = r.b.z; v[7] = r.b.w;
+}
+template <>
+__device__ __forceinline__ void unpack_raw<uint16_t>(const RawBlock<uint16_t>& r, float (&v)[8]) {
+  const uint32_t w[4] = {r.w.x, r.w.y, r.w.z, r.w.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = __uint_as_float(w[i] << 16);
+    v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+template <>
+__device__ __forceinline__ void unpack_raw<_Float16>(const RawBlock<_Float16>& r, float (&v)[8]) {
+  const uint32_t w[4] = {r.w.x, r.w.y, r.w.z, r.w.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = (float)__builtin_bit_cast(_Float16, (uint16_t)(w[i] & 0xffffu));
+    v[2 * i + 1] = (float)__builtin_bit_cast(_Float16, (uint16_t)(w[i] >> 16));
+  }
+}
+
+// First beta that the root bound does not rule out, and whether it surely does not overload.
+__device__ __forceinline__ int predict_beta(float mx, const float (&c)[4], const EncodeArgs& a,
+                                            bool& sure) {
+  const float two_q = (float)(2 * a.q);
+  int t0 = a.k - 1;
+  sure = false;
+#pragma unroll
+  for (int s = a_max_k - 1; s >= 0; --s) {
+    if (s < a.k) {
+      const float u = 2.0f * c[s] * mx;
+      const float margin = kRootMargin + u * 0x1p-12f;
+      if (u - margin <= two_q) {
+        t0 = s;
+        sure = (u + margin < two_q);
+      }
+    }
+  }
+  return t0;
+}
+
+template <typename T, int LANES, int BPT>
+__global__ __launch_bounds__(256) void encode_wave_kernel(
+    const T* __restrict__ x, int64_t rows, int cols, int64_t ld_x, EncodeArgs a,
+    uint32_t* __restrict__ codes, uint32_t* __restrict__ beta, float* __restrict__ scales) {
+  using SM = SlotMap<LANES, BPT>;
+  constexpr int SLOTS = SM::SLOTS;
+  constexpr int RW = SM::ROWS_PER_WAVE;
+  __shared__ double red[8];
+  __shared__ uint32_t queue[4][SLOTS];
+  __shared__ uint8_t tsl[4][SLOTS];
+  __shared__ float crow[4][RW][4];
+  __shared__ float rrow[4][RW];
+
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int nb = cols >> 3;
+  const int nbw = (nb + 15) >> 4;
+  const int64_t row0 = SM::WGROW ? (int64_t)blockIdx.x : ((int64_t)blockIdx.x * 4 + wave) * RW;
+  const double n = (double)cols;
+
+  // ---- load the slots (raw) and compute the row scales ----
+  RawBlock<T> raw[BPT];
+#pragma unroll
+  for (int i = 0; i < BPT; ++i) {
+    const int rw = SM::row_w(i, lane), j = SM::j(i, lane, wave);
+    const int64_t row = row0 + rw;
+    if (row < rows && j < nb) {
+      load_raw<T>(x + row * ld_x + 8 * j, raw[i]);
+    } else {
+      zero_raw<T>(raw[i]);
+    }
+  }
+  auto sumsq = [&](int i) {
+    float v[8];
+    unpack_raw<T>(raw[i], v);
+    double s = 0.0;
+#pragma unroll
+    for (int l = 0; l < 8; ++l) s = __builtin_fma((double)v[l], (double)v[l], s);
+    return s;
+  };
+  auto sumsq_dd = [&](int i, double& hi, double& lo) {
+    float v[8];
+    unpack_raw<T>(raw[i], v);
+#pragma unroll
+    for (int l = 0; l < 8; ++l) dd_add_square(hi, lo, v[l]);
+  };
+  auto set_row = [&](int rw, float r) {
+    const bool coded = (r > 0.0f) && isfinite(r);
+    rrow[wave][rw] = coded ? r : 0.0f;
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      crow[wave][rw][t] = coded ? (float)(1.0 / ((double)r * a.beta[t])) : 0.0f;
+  };
+  if constexpr (LANES < 64) {
+    // one row per lane group and pass: group reductions by shuffles only
+#pragma unroll
+    for (int i = 0; i < BPT; ++i) {
+      const double s = group_sum<LANES>(sumsq(i), red);
+      bool sure;
+      float r = rms_candidate(s, n, sure);
+      if (!sure) {
+        double hi = 0.0, lo = 0.0;
+        sumsq_dd(i, hi, lo);
+        group_sum_dd<LANES>(hi, lo, red);
+        r = exact_rms(hi, lo, n, r);
+      }
+      const int rw = SM::row_w(i, lane);
+      if (lane % LANES == 0) {
+        set_row(rw, r);
+        if (row0 + rw < rows) scales[row0 + rw] = r;
+      }
+    }
+  } else {
+    double s = 0.0;
+#pragma unroll
+    for (int i = 0; i < BPT; ++i) s += sumsq(i);
+    s = group_sum<LANES>(s, red);       // LANES == 256: every thread gets the same sum
+    bool sure;
+    float r = rms_candidate(s, n, sure);
+    if (!sure) {                        // uniform over the wave (LANES 64) or workgroup (256)
+      double hi = 0.0, lo = 0.0;
+#pragma unroll
+      for (int i = 0; i < BPT; ++i) sumsq_dd(i, hi, lo);
+      group_sum_dd<LANES>(hi, lo, red);
+      r = exact_rms(hi, lo, n, r);
+    }
+    if (lane == 0) {
+      set_row(0, r);
+      if (row0 < rows && (!SM::WGROW || wave == 0)) scales[row0] = r;
+    }
+  }
+
+  // ---- phase 1: slots whose predicted beta surely does not overload ----
+  int qn = 0;   // queue length, uniform over the wave
+#pragma unroll
+  for (int i = 0; i < BPT; ++i) {
+    const int rw = SM::row_w(i, lane), j = SM::j(i, lane, wave);
+    const int64_t row = row0 + rw;
+    const bool valid = row < rows && j < nb;
+    const bool coded = valid && rrow[wave][rw] != 0.0f;
+    float v[8], c[4];
+    unpack_raw<T>(raw[i], v);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) c[t] = crow[wave][rw][t];
+    bool sure = false;
+    int t0 = 0;
+    if (coded) t0 = predict_beta(root_bound_f(v), c, a, sure);
+    // the last beta needs no test either
+    const bool direct = coded && (sure || t0 == a.k - 1);
+    const bool need = coded && !direct;
+    uint32_t word = 0;
+    if (direct) {
+      float y[8];
+      const float ct = pick4(c, t0);
+#pragma unroll
+      for (int l = 0; l < 8; ++l) y[l] = v[l] * ct;
+      int P[8];
+      nearest_e8(y, P);
+      word = encode_codes(P, a.q, a.rq, a.mq);
+    }
+    const uint64_t mask = __ballot(need);
+    if (need) {
+      const int pos = qn + __popcll(mask & ((1ull << lane) - 1ull));
+      queue[wave][pos] = ((uint32_t)(i * 64 + lane) << 2) | (uint32_t)t0;
+    } else if (valid) {
+      codes[row * nb + j] = word;
+      tsl[wave][i * 64 + lane] = (uint8_t)(direct ? t0 : 0);
+    }
+    qn += __popcll(mask);
+  }
+
+  // ---- phase 2: the queued slots, compacted over the wave ----
+  for (int base = 0; base < qn; base += 64) {
+    if (base + lane < qn) {
+      const uint32_t e = queue[wave][base + lane];
+      const int sl = (int)(e >> 2), t = (int)(e & 3u);
+      const int i = sl >> 6, l = sl & 63;
+      const int rw = SM::row_w(i, l), j = SM::j(i, l, wave);
+      const int64_t row = row0 + rw;
+      float xv[8], c[4];
+      load_block<T>(x + row * ld_x + 8 * j, xv);
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt) c[tt] = crow[wave][rw][tt];
+      uint32_t word;
+      int tsel;
+      finish_block(xv, c, t, a, word, tsel);
+      codes[row * nb + j] = word;
+      tsl[wave][sl] = (uint8_t)tsel;
+    }
+  }
+
+  // ---- beta words: 16 two-bit indices of consecutive blocks (consecutive lanes) ----
+#pragma unroll
+  for (int i = 0; i < BPT; ++i) {
+    const int rw = SM::row_w(i, lane), j = SM::j(i, lane, wave);
+    const int64_t row = row0 + rw;
+    if (row < rows && j < nb && (j & 15) == 0) {
+      uint32_t bits = 0;
+      const int cnt = min(min(16, nb - j), LANES < 16 ? LANES : 16);
+      for (int m = 0; m < cnt; ++m) bits |= (uint32_t)tsl[wave][i * 64 + lane + m] << (2 * m);
+      beta[row * nbw + (j >> 4)] = bits;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------
 // launch
 // ---------------------------------------------------------------------------------------
 template <typename T, int LANES, int BPT>
@@ -327,23 +604,38 @@ static hipError_t launch_t(const void* x, int64_t rows, int cols, int64_t ld_x,
   return hipGetLastError();
 }
 
+template <typename T, int LANES, int BPT>
+static hipError_t launch_w(const void* x, int64_t rows, int cols, int64_t ld_x,
+                           const EncodeArgs& a, uint32_t* codes, uint32_t* beta, float* scales,
+                           hipStream_t st) {
+  using SM = SlotMap<LANES, BPT>;
+  const int64_t rows_per_wg = SM::WGROW ? 1 : 4 * SM::ROWS_PER_WAVE;
+  const int64_t grid = (rows + rows_per_wg - 1) / rows_per_wg;
+  hipLaunchKernelGGL((encode_wave_kernel<T, LANES, BPT>), dim3((unsigned)grid), dim3(256), 0, st,
+                     (const T*)x, rows, cols, ld_x, a, codes, beta, scales);
+  return hipGetLastError();
+}
+
 template <typename T>
 static hipError_t launch_dtype(const void* x, int64_t rows, int cols, int64_t ld_x,
                                const EncodeArgs& a, uint32_t* codes, uint32_t* beta,
                                float* scales, hipStream_t st) {
   const int nb = cols / 8;
+#define NQ_W(L, B) return launch_w<T, L, B>(x, rows, cols, ld_x, a, codes, beta, scales, st)
 #define NQ_L(L, B) return launch_t<T, L, B>(x, rows, cols, ld_x, a, codes, beta, scales, st)
-  if (nb <= 8) NQ_L(8, 1);
-  if (nb <= 16) NQ_L(16, 1);
-  if (nb <= 32) NQ_L(32, 1);
-  if (nb <= 64) NQ_L(64, 1);
-  if (nb <= 128) NQ_L(128, 1);
-  if (nb <= 256) NQ_L(256, 1);
-  if (nb <= 512) NQ_L(256, 2);
-  if (nb <= 1024) NQ_L(256, 4);
-  if (nb <= 2048) NQ_L(256, 8);
+  // short rows: several rows per lane group, 512 blocks per wave when there are enough rows
+  if (nb <= 8) { if (rows >= 4096) NQ_W(8, 8); NQ_W(8, 1); }
+  if (nb <= 16) { if (rows >= 2048) NQ_W(16, 8); NQ_W(16, 1); }
+  if (nb <= 32) { if (rows >= 1024) NQ_W(32, 8); NQ_W(32, 1); }
+  if (nb <= 64) { if (rows >= 512) NQ_W(64, 8); NQ_W(64, 1); }
+  if (nb <= 128) NQ_W(64, 2);
+  if (nb <= 256) NQ_W(64, 4);
+  if (nb <= 512) NQ_W(256, 2);
+  if (nb <= 1024) NQ_W(256, 4);
+  if (nb <= 2048) NQ_W(256, 8);
   if (nb <= 4096) NQ_L(512, 8);
   NQ_L(1024, 0);
+#undef NQ_W
 #undef NQ_L
 }
 

@@ -68,12 +68,7 @@ __global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__
     const uint32_t w = __builtin_nontemporal_load(codes + row * nb + j);
     const uint32_t bw = beta[row * ((nb + 15) >> 4) + (j >> 4)];
     const int t = (int)((bw >> (2 * (j & 15))) & 3u) + 1;
-    int X2[8];
-    decode_word(w, q, m2q, X2);
-    uint32_t h[8];
-#pragma unroll
-    for (int l = 0; l < 8; ++l) h[l] = __float_as_uint((float)(t * X2[l])) >> 16;
-    out = u32x4{h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16)};
+    out = decode_tile_bf16(w, t, q, m2q);
   }
   ws[gid] = out;
 }

@@ -22,21 +22,6 @@ constexpr int BN = 128;
 constexpr int KBLK = 8;         // blocks per K step
 constexpr int LDS_STRIDE = 9;   // uint4 per tile row (8 blocks + 1 pad against bank conflicts)
 
-// t * X2 of one block as eight bf16 (exact: |t X2| <= 4 * 32).
-__device__ __forceinline__ uint4 decode_tile_block(uint32_t w, int t, int q, uint32_t m2q) {
-  int X2[8];
-  decode_word(w, q, m2q, X2);
-  uint32_t h[8];
-#pragma unroll
-  for (int l = 0; l < 8; ++l) h[l] = __float_as_uint((float)(t * X2[l])) >> 16;
-  uint4 r;
-  r.x = h[0] | (h[1] << 16);
-  r.y = h[2] | (h[3] << 16);
-  r.z = h[4] | (h[5] << 16);
-  r.w = h[6] | (h[7] << 16);
-  return r;
-}
-
 __device__ __forceinline__ void decode_tile(const MatmulOperand& op, int64_t row0, int nb, int kb0,
                                             uint4 (*lds)[LDS_STRIDE]) {
   const int nbw = (nb + 15) >> 4;
@@ -52,7 +37,8 @@ __device__ __forceinline__ void decode_tile(const MatmulOperand& op, int64_t row
       const uint32_t w = op.codes[gr * nb + gb];
       const uint32_t bw = op.beta[gr * nbw + (gb >> 4)];
       const int t = (int)((bw >> (2 * (gb & 15))) & 3u) + 1;
-      val = decode_tile_block(w, t, op.q, op.m2q);
+      const u32x4 v = decode_tile_bf16(w, t, op.q, op.m2q);
+      val = make_uint4(v.x, v.y, v.z, v.w);
     }
     lds[r][b] = val;
   }
