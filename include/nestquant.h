@@ -94,25 +94,26 @@ nq_status nq_decode(const nq_params* p, const uint32_t* codes, const uint32_t* b
  *   c: device, M x N floats, row i at c + i*ldc, ldc >= N.
  * C_ij = r_Ai r_Wj base_A base_W / 4 * sum_blocks <t_A X2_A, t_W X2_W>; the integer tiles
  * t*X2 are exact in bf16 and contracted with fp32 accumulation.
- * For M > 64 the product decodes every block once into a workspace of
- * nq_matmul_workspace_size(M, N, K) bytes, which nq_matmul takes from the stream-ordered
- * allocator of the current device (hipMallocAsync / hipFreeAsync on hip_stream); use
- * nq_matmul_ex to pass a workspace instead. */
+ * Every block of both operands is decoded exactly once; the decoded activation (and, for
+ * M > 64, the decoded weight) lives in a workspace of nq_matmul_workspace_size(M, N, K)
+ * bytes, which nq_matmul takes from the stream-ordered allocator of the current device
+ * (hipMallocAsync / hipFreeAsync on hip_stream); use nq_matmul_ex to pass a workspace. */
 nq_status nq_matmul(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,
                     const float* a_scales, int64_t M, const nq_params* pw,
                     const uint32_t* w_codes, const uint32_t* w_beta, const float* w_scales,
                     int64_t N, int64_t K, float* c, int64_t ldc, void* hip_stream);
 
 /* nq_matmul with a caller-owned device workspace (16-byte aligned, at least
- * nq_matmul_workspace_size(M, N, K) bytes; may be NULL when that size is 0).  The workspace
- * is used as scratch until the call's kernels finish on hip_stream. */
+ * nq_matmul_workspace_size(M, N, K) bytes).  The workspace is used as scratch until the
+ * call's kernels finish on hip_stream. */
 nq_status nq_matmul_ex(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,
                        const float* a_scales, int64_t M, const nq_params* pw,
                        const uint32_t* w_codes, const uint32_t* w_beta, const float* w_scales,
                        int64_t N, int64_t K, float* c, int64_t ldc, void* workspace,
                        int64_t workspace_bytes, void* hip_stream);
 
-/* Workspace bytes nq_matmul_ex needs for an M x N x K product (0: none; -1: invalid). */
+/* Workspace bytes nq_matmul_ex needs for an M x N x K product (0 when M or N is 0; -1 for
+ * an invalid K). */
 int64_t nq_matmul_workspace_size(int64_t M, int64_t N, int64_t K);
 
 /* Sizes of the code and beta-index arrays for a rows x cols matrix (-1 if invalid). */

@@ -157,7 +157,8 @@ static nq_status check_matmul(const nq_params* pa, const uint32_t* a_codes,
 
 int64_t nq_matmul_workspace_size(int64_t M, int64_t N, int64_t K) {
   if (M < 0 || N < 0 || K < 8 || K % 8 || K > kMaxCols) return -1;
-  if (M <= nq::kFusedMaxM || N == 0) return 0;
+  if (M == 0 || N == 0) return 0;
+  if (M <= nq::kFusedMaxM) return (int64_t)nq::skinny_workspace(M, K);
   return (int64_t)nq::decode_once_workspace(M, N, K);
 }
 
@@ -180,7 +181,8 @@ nq_status nq_matmul_ex(const nq_params* pa, const uint32_t* a_codes, const uint3
   nq::MatmulOperand W{w_codes, w_beta, w_scales, pw->q, nq::magic_2q(pw->q), N};
   const float scale = (float)(pa->base * pw->base * 0.25);
   hipStream_t st = (hipStream_t)hip_stream;
-  if (need == 0) return hip_status(nq::launch_matmul(A, W, K, c, ldc, scale, st), who);
+  if (M <= nq::kFusedMaxM)
+    return hip_status(nq::launch_matmul_skinny(A, W, K, c, ldc, scale, workspace, st), who);
   static std::once_flag attr_once;
   static hipError_t attr_err = hipSuccess;
   std::call_once(attr_once, [] { attr_err = nq::gemm_set_attributes(); });

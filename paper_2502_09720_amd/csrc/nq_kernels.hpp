@@ -38,8 +38,10 @@ hipError_t launch_decode(const uint32_t* codes, const uint32_t* beta, const floa
                          int64_t rows, int cols, void* out, int out_dtype, int64_t ld_out,
                          const DecodeArgs& a, hipStream_t st);
 
-hipError_t launch_matmul(const MatmulOperand& A, const MatmulOperand& W, int64_t K, float* c,
-                         int64_t ldc, float scale, hipStream_t st);
+// Small M (skinny): decode A once into a bf16 tile, then decode W straight into MFMA operands.
+size_t skinny_workspace(int64_t M, int64_t K);
+hipError_t launch_matmul_skinny(const MatmulOperand& A, const MatmulOperand& W, int64_t K,
+                                float* c, int64_t ldc, float scale, void* ws, hipStream_t st);
 
 // Decode-once path (large M): workspace bytes, launch (tiles + GEMM), one-time attributes.
 size_t decode_once_workspace(int64_t M, int64_t N, int64_t K);
@@ -48,7 +50,7 @@ hipError_t launch_matmul_decode_once(const MatmulOperand& A, const MatmulOperand
                                      hipStream_t st);
 hipError_t gemm_set_attributes();
 
-// M at or below this uses the fused kernel (no workspace); above it, decode-once.
+// M at or below this uses the skinny kernel; above it, decode-once.
 constexpr int64_t kFusedMaxM = 64;
 
 inline uint32_t magic_2q(int q) { return (uint32_t)((65536 + 2 * q - 1) / (2 * q)); }

@@ -1,120 +1,115 @@
-// Coded matrix product C = A_hat * W_hat^T (Alg. 4 of the NestQuant paper for every pair of
-// rows), fused: code words are decoded (Alg. 2) into LDS as exact bf16 integer tiles t*X2
-// and contracted on the bf16 matrix cores with fp32 accumulation; the per-row scales and
-// base_A * base_W / 4 are applied in the epilogue.
+// Coded matrix product for small M (decode-shaped layers: a few activation rows against a
+// large coded weight), C = A_hat * W_hat^T, Alg. 4 of the NestQuant paper for every pair of
+// rows.
 //
-// Tiling: a 256-thread workgroup (4 waves) owns a 128 x 128 tile of C; each wave owns a
-// 64 x 64 quadrant as 2 x 2 v_mfma_f32_32x32x16_bf16 tiles.  The K loop steps over 8 blocks
-// (64 entries): the 128 rows of A and of W times 8 blocks are decoded (4 + 4 per thread)
-// into LDS, one 16-byte bf16x8 per block.  The MFMA A operand of lane l is the 8 K-values
-// of row l%32 at K offset 8*(l/32), i.e. exactly one decoded block, so each fragment load is
-// one 16-byte LDS read.
+// Here the weight decode dominates (the product is a few flops per decoded weight entry),
+// so every block of W is decoded exactly once, straight into a matrix-core operand: for
+// v_mfma_f32_16x16x32_bf16 the B operand of lane l is the 8 K-values of column l % 16 at
+// K offset 8 (l / 16), i.e. exactly one decoded block (t * X2, exact in bf16), so each lane
+// decodes its own block and no LDS staging is needed.  The activation (at most 64 rows) is
+// decoded once beforehand into a bf16 tile (tiles_kernel) that stays in cache; its
+// fragments are loaded per step for up to four 16-row M tiles.  A workgroup owns 16
+// columns of C; its four waves split K and combine their partial sums through LDS before
+// the epilogue C_ij = acc * r_Ai * r_Wj * base_A * base_W / 4.
 #include "nq_device.hpp"
 #include "nq_kernels.hpp"
 
 namespace nq {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int BM = 128;
-constexpr int BN = 128;
-constexpr int KBLK = 8;         // blocks per K step
-constexpr int LDS_STRIDE = 9;   // uint4 per tile row (8 blocks + 1 pad against bank conflicts)
+__global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__ codes,
+                                                    const uint32_t* __restrict__ beta,
+                                                    int64_t rows, int nb, int64_t rows_p,
+                                                    int nb_p, int q, uint32_t m2q,
+                                                    u32x4* __restrict__ ws);
 
-__device__ __forceinline__ void decode_tile(const MatmulOperand& op, int64_t row0, int nb, int kb0,
-                                            uint4 (*lds)[LDS_STRIDE]) {
+template <int MT>
+__global__ __launch_bounds__(256) void skinny_kernel(const u32x4* __restrict__ ta, int nbp,
+                                                     MatmulOperand A, MatmulOperand W, int nb,
+                                                     float* __restrict__ c, int64_t ldc,
+                                                     float scale) {
+  __shared__ f32x4 part[3][MT][64];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int col = lane & 15, kg = lane >> 4;
+  const int64_t n = (int64_t)blockIdx.x * 16 + col;
+  const bool nok = n < W.rows;
   const int nbw = (nb + 15) >> 4;
+  const uint32_t* wc = W.codes + (nok ? n : 0) * nb;
+  const uint32_t* wb = W.beta + (nok ? n : 0) * nbw;
+
+  // K in steps of 32 (4 blocks); wave w takes a contiguous quarter of the steps
+  const int nsteps = nbp / 4;
+  const int s0 = (int)((int64_t)nsteps * wave / 4), s1 = (int)((int64_t)nsteps * (wave + 1) / 4);
+
+  f32x4 acc[MT];
 #pragma unroll
-  for (int it = 0; it < (BM * KBLK) / 256; ++it) {
-    const int idx = threadIdx.x + it * 256;
-    const int r = idx / KBLK;
-    const int b = idx % KBLK;
-    const int64_t gr = row0 + r;
-    const int gb = kb0 + b;
-    uint4 val = make_uint4(0, 0, 0, 0);
-    if (gr < op.rows && gb < nb) {
-      const uint32_t w = op.codes[gr * nb + gb];
-      const uint32_t bw = op.beta[gr * nbw + (gb >> 4)];
-      const int t = (int)((bw >> (2 * (gb & 15))) & 3u) + 1;
-      const u32x4 v = decode_tile_bf16(w, t, op.q, op.m2q);
-      val = make_uint4(v.x, v.y, v.z, v.w);
+  for (int m = 0; m < MT; ++m) acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int s = s0; s < s1; ++s) {
+    const int blk = 4 * s + kg;
+    u32x4 b = {0u, 0u, 0u, 0u};
+    if (nok && blk < nb) {
+      const uint32_t w = wc[blk];
+      const int t = (int)((wb[blk >> 4] >> (2 * (blk & 15))) & 3u) + 1;
+      b = decode_tile_bf16(w, t, W.q, W.m2q);
     }
-    lds[r][b] = val;
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      const u32x4 a = ta[(int64_t)(16 * m + col) * nbp + blk];
+      acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                       __builtin_bit_cast(bf16x8, b), acc[m],
+                                                       0, 0, 0);
+    }
+  }
+
+  if (wave > 0) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m) part[wave - 1][m][lane] = acc[m];
+  }
+  __syncthreads();
+  if (wave == 0) {
+    // 16x16 accumulator layout: lane l holds column l % 16, register e holds row 4 (l/16) + e
+    const float sw = nok ? W.scales[n] * scale : 0.0f;
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      f32x4 v = acc[m];
+#pragma unroll
+      for (int w = 0; w < 3; ++w) {
+        const f32x4 o = part[w][m][lane];
+        v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
+      }
+      const float vv[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int64_t row = 16 * m + 4 * kg + e;
+        if (nok && row < A.rows) c[row * ldc + n] = vv[e] * (A.scales[row] * sw);
+      }
+    }
   }
 }
 
-__global__ __launch_bounds__(256) void matmul_kernel(MatmulOperand A, MatmulOperand W, int nb,
-                                                     int tiles_n, float* __restrict__ c,
-                                                     int64_t ldc, float scale) {
-  __shared__ uint4 As[BM][LDS_STRIDE];
-  __shared__ uint4 Ws[BN][LDS_STRIDE];
-
-  const int tile = blockIdx.x;
-  const int64_t m0 = (int64_t)(tile / tiles_n) * BM;
-  const int64_t n0 = (int64_t)(tile % tiles_n) * BN;
-  const int wave = threadIdx.x >> 6;
-  const int lane = threadIdx.x & 63;
-  const int wm = wave >> 1, wn = wave & 1;
-
-  f32x16 acc[2][2];
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
-
-  for (int kb0 = 0; kb0 < nb; kb0 += KBLK) {
-    decode_tile(A, m0, nb, kb0, As);
-    decode_tile(W, n0, nb, kb0, Ws);
-    __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < KBLK / 2; ++kk) {
-      bf16x8 af[2], bfr[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const uint4 u = As[wm * 64 + i * 32 + (lane & 31)][2 * kk + (lane >> 5)];
-        af[i] = __builtin_bit_cast(bf16x8, u);
-      }
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const uint4 u = Ws[wn * 64 + j * 32 + (lane & 31)][2 * kk + (lane >> 5)];
-        bfr[j] = __builtin_bit_cast(bf16x8, u);
-      }
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
-    }
-    __syncthreads();
-  }
-
-  // Epilogue.  32x32 accumulator layout: lane l holds column l%32; register e holds row
-  // 8*(e/4) + 4*(l/32) + (e%4).
-#pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int64_t col = n0 + wn * 64 + j * 32 + (lane & 31);
-      if (col >= W.rows) continue;
-      const float sw = W.scales[col] * scale;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int64_t row = m0 + wm * 64 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        if (row < A.rows) c[row * ldc + col] = acc[i][j][e] * (A.scales[row] * sw);
-      }
-    }
+size_t skinny_workspace(int64_t M, int64_t K) {
+  const int64_t mp = (M + 15) / 16 * 16;
+  const int64_t kp = (K + 31) / 32 * 32;
+  return (size_t)(mp * kp * 2);
 }
 
-hipError_t launch_matmul(const MatmulOperand& A, const MatmulOperand& W, int64_t K, float* c,
-                         int64_t ldc, float scale, hipStream_t st) {
+hipError_t launch_matmul_skinny(const MatmulOperand& A, const MatmulOperand& W, int64_t K,
+                                float* c, int64_t ldc, float scale, void* ws, hipStream_t st) {
   const int nb = (int)(K / 8);
-  const int64_t tiles_m = (A.rows + BM - 1) / BM;
-  const int64_t tiles_n = (W.rows + BN - 1) / BN;
-  hipLaunchKernelGGL(matmul_kernel, dim3((unsigned)(tiles_m * tiles_n)), dim3(256), 0, st, A, W,
-                     nb, (int)tiles_n, c, ldc, scale);
+  const int64_t mp = (A.rows + 15) / 16 * 16;
+  const int nbp = (int)((K + 31) / 32 * 32 / 8);
+  u32x4* ta = reinterpret_cast<u32x4*>(ws);
+  hipLaunchKernelGGL(tiles_kernel, dim3((unsigned)((mp * nbp + 255) / 256)), dim3(256), 0, st,
+                     A.codes, A.beta, A.rows, nb, mp, nbp, A.q, A.m2q, ta);
+  const unsigned grid = (unsigned)((W.rows + 15) / 16);
+  switch (mp / 16) {
+    case 1: hipLaunchKernelGGL(skinny_kernel<1>, dim3(grid), dim3(256), 0, st, ta, nbp, A, W, nb, c, ldc, scale); break;
+    case 2: hipLaunchKernelGGL(skinny_kernel<2>, dim3(grid), dim3(256), 0, st, ta, nbp, A, W, nb, c, ldc, scale); break;
+    case 3: hipLaunchKernelGGL(skinny_kernel<3>, dim3(grid), dim3(256), 0, st, ta, nbp, A, W, nb, c, ldc, scale); break;
+    default: hipLaunchKernelGGL(skinny_kernel<4>, dim3(grid), dim3(256), 0, st, ta, nbp, A, W, nb, c, ldc, scale); break;
+  }
   return hipGetLastError();
 }
 

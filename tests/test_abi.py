@@ -106,7 +106,8 @@ def test_matmul_rejects(lib, case):
 
 
 def test_workspace_size(lib):
-    assert lib.nq_matmul_workspace_size(64, 4096, 4096) == 0      # fused path
+    assert lib.nq_matmul_workspace_size(16, 4096, 4096) == 16 * 4096 * 2   # skinny: A tile
+    assert lib.nq_matmul_workspace_size(0, 4096, 4096) == 0
     ws = lib.nq_matmul_workspace_size(2048, 4096, 4096)
     assert ws >= (2048 + 4096) * 4096 * 2                          # bf16 tiles of A and W
     assert lib.nq_matmul_workspace_size(100, 10, 12) == -1

@@ -182,6 +182,8 @@ MATMUL_CASES = [
     (5, 16, 300, 2048, 7, 7, 4),
     (6, 200, 40, 136, 5, 3, 2),
     (7, 33, 65, 64, 14, 14, 1),
+    (8, 20, 50, 264, 14, 16, 3),
+    (9, 48, 1000, 4096, 14, 14, 4),
 ]
 
 
