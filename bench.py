@@ -36,7 +36,55 @@ def parse():
     ap.add_argument("--q", type=int, default=None, help="override q (workload 4 has q=7 too)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-rows", type=int, default=512)
+    ap.add_argument("--kv", action="store_true",
+                    help="standalone nq_encode / nq_decode of the 2^28-entry fp16 KV-like "
+                         "matrix (2^21 rows of 128) against the HBM roofline")
     return ap.parse_args()
+
+
+def kv_roofline(args):
+    """nq_encode and nq_decode of X (2^21 x 128 fp16 N(0,1)) against 8 TB/s."""
+    import numpy as np
+    import torch
+    import workloads
+    import paper_2502_09720_amd as nq
+
+    c = workloads.CONFIGS[5]
+    rows, cols = c["X_rows"], c["X_cols"]
+    dev = torch.device("cuda:0")
+    X = torch.empty(rows, cols, dtype=torch.float16, device=dev)
+    step = 1 << 17
+    for r0 in range(0, rows, step):
+        st, _, _ = workloads.operand(5, "X", row_range=(r0, min(rows, r0 + step)))
+        X[r0:r0 + len(st)] = torch.from_numpy(st).to(dev)
+    q, k = 14, 4
+    coded = nq.encode(X, q=q, k=k)
+    out = torch.empty_like(X)
+    nb = cols // 8
+    io = rows * cols * 2
+    coded_bytes = rows * nb * 4 + rows * ((nb + 15) // 16) * 4 + rows * 4
+    res = {}
+    for name, fn in (("nq_encode", lambda: nq.encode(X, q=q, k=k, out=(coded.codes, coded.beta,
+                                                                        coded.scales))),
+                     ("nq_decode", lambda: nq.decode(coded, torch.float16, out=out))):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        gbps = (io + coded_bytes) / (ms * 1e-3) / 1e9
+        res[name] = {"ms": ms, "GBps": gbps, "hbm_frac": gbps / HBM_PEAK_GBPS,
+                     "bytes": io + coded_bytes}
+    print(json.dumps({"metric": "nq_encode / nq_decode GB/s, 2^28 fp16 entries in rows of 128",
+                      "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+                      "dtype": "f16", "data": "synthetic",
+                      "config": {"workload": "KV-like 2^21 x 128 fp16 N(0,1), q=14, k=4"},
+                      "results": res}))
 
 
 def algorithmic(M, N, K, in_bytes):
@@ -100,6 +148,10 @@ def main():
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1"}))
         sys.exit(2)
+
+    if args.kv:
+        kv_roofline(args)
+        return
 
     import numpy as np
     import torch

@@ -19,14 +19,15 @@ template <int OUT>  // 0 = fp32, 1 = fp16, 2 = bf16
 __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict__ codes,
                                                      const uint32_t* __restrict__ beta,
                                                      const float* __restrict__ scales,
-                                                     int64_t rows, int nb, void* __restrict__ out,
-                                                     int64_t ld_out, DecodeArgs a) {
-  const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t row = gid / nb;
-  if (row >= rows) return;
-  const int j = (int)(gid - row * nb);
+                                                     int64_t rows, int nb, int lg,
+                                                     void* __restrict__ out, int64_t ld_out,
+                                                     DecodeArgs a) {
+  int64_t row;
+  int j;
+  grid_block(nb, lg, row, j);
+  if (row >= rows || j >= nb) return;
   const int nbw = (nb + 15) >> 4;
-  const uint32_t w = __builtin_nontemporal_load(codes + gid);
+  const uint32_t w = __builtin_nontemporal_load(codes + row * nb + j);
   const uint32_t bw = beta[row * nbw + (j >> 4)];
   const int t = (int)((bw >> (2 * (j & 15))) & 3u);
   const double sc = (double)scales[row] * a.half_beta[t];
@@ -64,20 +65,22 @@ hipError_t launch_decode(const uint32_t* codes, const uint32_t* beta, const floa
                          int64_t rows, int cols, void* out, int out_dtype, int64_t ld_out,
                          const DecodeArgs& a, hipStream_t st) {
   const int nb = cols / 8;
-  const int64_t total = rows * nb;
-  const unsigned grid = (unsigned)((total + 255) / 256);
+  int lg;
+  int64_t wgs;
+  grid_shape(rows, nb, lg, wgs);
+  const unsigned grid = (unsigned)wgs;
   switch (out_dtype) {
     case 0:
       hipLaunchKernelGGL(decode_kernel<0>, dim3(grid), dim3(256), 0, st, codes, beta, scales, rows,
-                         nb, out, ld_out, a);
+                         nb, lg, out, ld_out, a);
       break;
     case 1:
       hipLaunchKernelGGL(decode_kernel<1>, dim3(grid), dim3(256), 0, st, codes, beta, scales, rows,
-                         nb, out, ld_out, a);
+                         nb, lg, out, ld_out, a);
       break;
     default:
       hipLaunchKernelGGL(decode_kernel<2>, dim3(grid), dim3(256), 0, st, codes, beta, scales, rows,
-                         nb, out, ld_out, a);
+                         nb, lg, out, ld_out, a);
       break;
   }
   return hipGetLastError();

@@ -371,6 +371,20 @@ __device__ __forceinline__ void decode_word_pk(uint32_t w, int q, uint32_t m2q,
     X2[i] = bits32(as_u16x2(X2[i]) + as_u16x2(word == i ? dl : 0u));
 }
 
+// One thread per block of a rows x nb grid of blocks, 256 threads per workgroup: rows
+// shorter than 256 blocks are packed (a power-of-two group of lanes per row), longer rows
+// are cut into 256-block segments.  lg = log2 of the group size (for nb <= 256) or -1.
+__device__ __forceinline__ void grid_block(int nb, int lg, int64_t& row, int& j) {
+  if (lg >= 0) {
+    row = (int64_t)blockIdx.x * (256 >> lg) + (threadIdx.x >> lg);
+    j = threadIdx.x & ((1 << lg) - 1);
+  } else {
+    const uint32_t segs = ((uint32_t)nb + 255u) / 256u;
+    row = blockIdx.x / segs;
+    j = (int)(blockIdx.x - (uint32_t)row * segs) * 256 + threadIdx.x;
+  }
+}
+
 // t * X2 of one block as eight bf16 (exact: |t X2| <= 4 * 32 = 128 < 2^8): the upper halves
 // of the fp32 values, coordinates 2i and 2i+1 in word i.
 __device__ __forceinline__ u32x4 decode_tile_bf16(uint32_t w, int t, int q, uint32_t m2q) {

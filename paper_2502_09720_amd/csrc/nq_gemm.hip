@@ -53,16 +53,17 @@ using CfgMid = Cfg<256, 128, 4, 2, 3>;
 using CfgBig = Cfg<256, 256, 4, 2, 2>;
 }  // namespace gemm
 
-// t * X2 of every block of a coded operand, as bf16, into ws[rows_p][k_p] (zero padding).
+// t * X2 of every block of a coded operand, as bf16, into ws[rows_p][nb_p blocks] (zero
+// padding), one thread per block (grid_block).
 __global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__ codes,
                                                     const uint32_t* __restrict__ beta,
                                                     int64_t rows, int nb, int64_t rows_p,
-                                                    int nb_p, int q, uint32_t m2q,
+                                                    int nb_p, int q, uint32_t m2q, int lg,
                                                     u32x4* __restrict__ ws) {
-  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t row = gid / nb_p;
-  if (row >= rows_p) return;
-  const int j = (int)(gid - row * nb_p);
+  int64_t row;
+  int j;
+  grid_block(nb_p, lg, row, j);
+  if (row >= rows_p || j >= nb_p) return;
   u32x4 out = {0u, 0u, 0u, 0u};
   if (row < rows && j < nb) {
     const uint32_t w = __builtin_nontemporal_load(codes + row * nb + j);
@@ -70,7 +71,7 @@ __global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__
     const int t = (int)((bw >> (2 * (j & 15))) & 3u) + 1;
     out = decode_tile_bf16(w, t, q, m2q);
   }
-  ws[gid] = out;
+  ws[row * nb_p + j] = out;
 }
 
 __device__ __forceinline__ void tile_coords(int bid, int tm, int tn, int& pm, int& pn) {
@@ -280,10 +281,14 @@ hipError_t launch_matmul_decode_once(const MatmulOperand& A, const MatmulOperand
   const int nbp = kp / 8;
   u32x4* wa = reinterpret_cast<u32x4*>(ws);
   u32x4* ww = wa + mp * nbp;
-  hipLaunchKernelGGL(tiles_kernel, dim3((unsigned)((mp * nbp + 255) / 256)), dim3(256), 0, st,
-                     A.codes, A.beta, A.rows, nb, mp, nbp, A.q, A.m2q, wa);
-  hipLaunchKernelGGL(tiles_kernel, dim3((unsigned)((np * nbp + 255) / 256)), dim3(256), 0, st,
-                     W.codes, W.beta, W.rows, nb, np, nbp, W.q, W.m2q, ww);
+  int lg;
+  int64_t wgs;
+  grid_shape(mp, nbp, lg, wgs);
+  hipLaunchKernelGGL(tiles_kernel, dim3((unsigned)wgs), dim3(256), 0, st, A.codes, A.beta,
+                     A.rows, nb, mp, nbp, A.q, A.m2q, lg, wa);
+  grid_shape(np, nbp, lg, wgs);
+  hipLaunchKernelGGL(tiles_kernel, dim3((unsigned)wgs), dim3(256), 0, st, W.codes, W.beta,
+                     W.rows, nb, np, nbp, W.q, W.m2q, lg, ww);
   // 256 x 256 tiles once they give every CU a tile, else 256 x 128
   if ((mp / 256) * (np / 256) >= 256) {
     launch_gemm<CfgBig>(wa, ww, kp, mp, np, A, W, c, ldc, scale, st);

@@ -53,6 +53,20 @@ hipError_t gemm_set_attributes();
 // M at or below this uses the skinny kernel; above it, decode-once.
 constexpr int64_t kFusedMaxM = 64;
 
+// Launch shape for grid_block: log2 of the lanes per row (-1: 256-block segments) and the
+// number of workgroups.
+inline void grid_shape(int64_t rows, int nb, int& lg, int64_t& wgs) {
+  if (nb <= 256) {
+    lg = 0;
+    while ((1 << lg) < nb) ++lg;
+    const int64_t per = 256 >> lg;
+    wgs = (rows + per - 1) / per;
+  } else {
+    lg = -1;
+    wgs = rows * ((nb + 255) / 256);
+  }
+}
+
 inline uint32_t magic_2q(int q) { return (uint32_t)((65536 + 2 * q - 1) / (2 * q)); }
 inline uint32_t magic_q(int q) { return (uint32_t)(((1u << 20) + q - 1) / q); }
 

@@ -21,7 +21,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 __global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__ codes,
                                                     const uint32_t* __restrict__ beta,
                                                     int64_t rows, int nb, int64_t rows_p,
-                                                    int nb_p, int q, uint32_t m2q,
+                                                    int nb_p, int q, uint32_t m2q, int lg,
                                                     u32x4* __restrict__ ws);
 
 template <int MT>
@@ -101,8 +101,11 @@ hipError_t launch_matmul_skinny(const MatmulOperand& A, const MatmulOperand& W, 
   const int64_t mp = (A.rows + 15) / 16 * 16;
   const int nbp = (int)((K + 31) / 32 * 32 / 8);
   u32x4* ta = reinterpret_cast<u32x4*>(ws);
-  hipLaunchKernelGGL(tiles_kernel, dim3((unsigned)((mp * nbp + 255) / 256)), dim3(256), 0, st,
-                     A.codes, A.beta, A.rows, nb, mp, nbp, A.q, A.m2q, ta);
+  int lg;
+  int64_t wgs;
+  grid_shape(mp, nbp, lg, wgs);
+  hipLaunchKernelGGL(tiles_kernel, dim3((unsigned)wgs), dim3(256), 0, st, A.codes, A.beta, A.rows,
+                     nb, mp, nbp, A.q, A.m2q, lg, ta);
   const unsigned grid = (unsigned)((W.rows + 15) / 16);
   switch (mp / 16) {
     case 1: hipLaunchKernelGGL(skinny_kernel<1>, dim3(grid), dim3(256), 0, st, ta, nbp, A, W, nb, c, ldc, scale); break;
