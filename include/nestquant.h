@@ -112,6 +112,21 @@ nq_status nq_matmul_ex(const nq_params* pa, const uint32_t* a_codes, const uint3
                        int64_t N, int64_t K, float* c, int64_t ldc, void* workspace,
                        int64_t workspace_bytes, void* hip_stream);
 
+/* The two stages of nq_matmul_ex, for callers that time or schedule them separately.
+ * stages is a bit mask: NQ_STAGE_DECODE decodes the operands into the workspace (every
+ * block of A and, for M > 64, of W, as bf16 t*X2), NQ_STAGE_CONTRACT computes C from the
+ * workspace (for M <= 64 it also decodes W, straight into matrix-core operands).  A DECODE
+ * call followed by a CONTRACT call with the same arguments on the same stream is exactly
+ * nq_matmul_ex (stages = NQ_STAGE_DECODE | NQ_STAGE_CONTRACT); the workspace must not be
+ * changed in between.  Arguments are validated as in nq_matmul_ex; any other bit, or an
+ * empty mask, is NQ_ERR_INVALID_ARG. */
+enum { NQ_STAGE_DECODE = 1, NQ_STAGE_CONTRACT = 2 };
+nq_status nq_matmul_stages(int32_t stages, const nq_params* pa, const uint32_t* a_codes,
+                           const uint32_t* a_beta, const float* a_scales, int64_t M,
+                           const nq_params* pw, const uint32_t* w_codes, const uint32_t* w_beta,
+                           const float* w_scales, int64_t N, int64_t K, float* c, int64_t ldc,
+                           void* workspace, int64_t workspace_bytes, void* hip_stream);
+
 /* Workspace bytes nq_matmul_ex needs for an M x N x K product (0 when M or N is 0; -1 for
  * an invalid K). */
 int64_t nq_matmul_workspace_size(int64_t M, int64_t N, int64_t K);

@@ -7,6 +7,8 @@ library has not been built.
 """
 
 from .binding import (  # noqa: F401
+    STAGE_CONTRACT,
+    STAGE_DECODE,
     Coded,
     NQError,
     decode,

@@ -46,9 +46,11 @@ def library():
                                   f32p, i64, vp]
         lib.nq_matmul_ex.argtypes = [pp, u32p, u32p, f32p, i64, pp, u32p, u32p, f32p, i64, i64,
                                      f32p, i64, vp, i64, vp]
+        lib.nq_matmul_stages.argtypes = [ctypes.c_int32, pp, u32p, u32p, f32p, i64, pp, u32p,
+                                         u32p, f32p, i64, i64, f32p, i64, vp, i64, vp]
         lib.nq_matmul_workspace_size.argtypes = [i64, i64, i64]
         lib.nq_matmul_workspace_size.restype = i64
-        for f in ("nq_encode", "nq_decode", "nq_matmul", "nq_matmul_ex"):
+        for f in ("nq_encode", "nq_decode", "nq_matmul", "nq_matmul_ex", "nq_matmul_stages"):
             getattr(lib, f).restype = ctypes.c_int
         lib.nq_codes_words.argtypes = [i64, i64]
         lib.nq_codes_words.restype = i64
@@ -151,10 +153,16 @@ def decode(coded, out_dtype=None, stream=None, out=None):
     return out
 
 
-def matmul(a, w, stream=None, out=None, workspace=None):
+STAGE_DECODE = 1
+STAGE_CONTRACT = 2
+
+
+def matmul(a, w, stream=None, out=None, workspace=None, stages=STAGE_DECODE | STAGE_CONTRACT):
     """nq_matmul: C = A_hat W_hat^T (fp32, M x N) from two coded operands.
 
-    The decode-once workspace (large M) is taken from torch's allocator unless given."""
+    The decode-once workspace is taken from torch's allocator unless given.  ``stages``
+    selects part of the call (nq_matmul_stages): STAGE_DECODE fills the workspace,
+    STAGE_CONTRACT computes C from it; both (the default) is nq_matmul_ex."""
     import torch
     if a.cols != w.cols:
         raise ValueError("K mismatch")
@@ -166,16 +174,20 @@ def matmul(a, w, stream=None, out=None, workspace=None):
     if need < 0:
         raise ValueError("invalid matmul shape")
     if need > 0 and (workspace is None or workspace.numel() * workspace.element_size() < need):
+        if stages != STAGE_DECODE | STAGE_CONTRACT:
+            raise ValueError("a staged matmul needs a workspace of matmul_workspace_size bytes")
         workspace = torch.empty(need, dtype=torch.uint8, device=a.codes.device)
     ws_ptr = workspace.data_ptr() if need > 0 else 0
-    _check(lib.nq_matmul_ex(ctypes.byref(pa), ctypes.c_void_p(a.codes.data_ptr()),
-                            ctypes.c_void_p(a.beta.data_ptr()),
-                            ctypes.c_void_p(a.scales.data_ptr()), a.rows, ctypes.byref(pw),
-                            ctypes.c_void_p(w.codes.data_ptr()),
-                            ctypes.c_void_p(w.beta.data_ptr()),
-                            ctypes.c_void_p(w.scales.data_ptr()), w.rows, a.cols,
-                            ctypes.c_void_p(out.data_ptr()), out.stride(0),
-                            ctypes.c_void_p(ws_ptr), need, _stream(stream)))
+    args = (ctypes.byref(pa), ctypes.c_void_p(a.codes.data_ptr()),
+            ctypes.c_void_p(a.beta.data_ptr()), ctypes.c_void_p(a.scales.data_ptr()), a.rows,
+            ctypes.byref(pw), ctypes.c_void_p(w.codes.data_ptr()),
+            ctypes.c_void_p(w.beta.data_ptr()), ctypes.c_void_p(w.scales.data_ptr()), w.rows,
+            a.cols, ctypes.c_void_p(out.data_ptr()), out.stride(0), ctypes.c_void_p(ws_ptr),
+            need, _stream(stream))
+    if stages == STAGE_DECODE | STAGE_CONTRACT:
+        _check(lib.nq_matmul_ex(*args))
+    else:
+        _check(lib.nq_matmul_stages(stages, *args))
     return out
 
 

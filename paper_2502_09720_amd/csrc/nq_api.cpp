@@ -162,12 +162,14 @@ int64_t nq_matmul_workspace_size(int64_t M, int64_t N, int64_t K) {
   return (int64_t)nq::decode_once_workspace(M, N, K);
 }
 
-nq_status nq_matmul_ex(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,
-                       const float* a_scales, int64_t M, const nq_params* pw,
-                       const uint32_t* w_codes, const uint32_t* w_beta, const float* w_scales,
-                       int64_t N, int64_t K, float* c, int64_t ldc, void* workspace,
-                       int64_t workspace_bytes, void* hip_stream) {
-  const char* who = "nq_matmul_ex";
+static nq_status matmul_stages(int32_t stages, const nq_params* pa, const uint32_t* a_codes,
+                               const uint32_t* a_beta, const float* a_scales, int64_t M,
+                               const nq_params* pw, const uint32_t* w_codes,
+                               const uint32_t* w_beta, const float* w_scales, int64_t N,
+                               int64_t K, float* c, int64_t ldc, void* workspace,
+                               int64_t workspace_bytes, void* hip_stream, const char* who) {
+  if (stages < 1 || stages > 3)
+    return fail(NQ_ERR_INVALID_ARG, "%s: stages must be a non-empty mask of NQ_STAGE_*", who);
   if (nq_status s = check_matmul(pa, a_codes, a_beta, a_scales, M, pw, w_codes, w_beta,
                                  w_scales, N, K, c, ldc, who))
     return s;
@@ -182,12 +184,33 @@ nq_status nq_matmul_ex(const nq_params* pa, const uint32_t* a_codes, const uint3
   const float scale = (float)(pa->base * pw->base * 0.25);
   hipStream_t st = (hipStream_t)hip_stream;
   if (M <= nq::kFusedMaxM)
-    return hip_status(nq::launch_matmul_skinny(A, W, K, c, ldc, scale, workspace, st), who);
+    return hip_status(nq::launch_matmul_skinny(stages, A, W, K, c, ldc, scale, workspace, st),
+                      who);
   static std::once_flag attr_once;
   static hipError_t attr_err = hipSuccess;
   std::call_once(attr_once, [] { attr_err = nq::gemm_set_attributes(); });
   if (attr_err != hipSuccess) return hip_status(attr_err, who);
-  return hip_status(nq::launch_matmul_decode_once(A, W, K, c, ldc, scale, workspace, st), who);
+  return hip_status(
+      nq::launch_matmul_decode_once(stages, A, W, K, c, ldc, scale, workspace, st), who);
+}
+
+nq_status nq_matmul_ex(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,
+                       const float* a_scales, int64_t M, const nq_params* pw,
+                       const uint32_t* w_codes, const uint32_t* w_beta, const float* w_scales,
+                       int64_t N, int64_t K, float* c, int64_t ldc, void* workspace,
+                       int64_t workspace_bytes, void* hip_stream) {
+  return matmul_stages(NQ_STAGE_DECODE | NQ_STAGE_CONTRACT, pa, a_codes, a_beta, a_scales, M,
+                       pw, w_codes, w_beta, w_scales, N, K, c, ldc, workspace, workspace_bytes,
+                       hip_stream, "nq_matmul_ex");
+}
+
+nq_status nq_matmul_stages(int32_t stages, const nq_params* pa, const uint32_t* a_codes,
+                           const uint32_t* a_beta, const float* a_scales, int64_t M,
+                           const nq_params* pw, const uint32_t* w_codes, const uint32_t* w_beta,
+                           const float* w_scales, int64_t N, int64_t K, float* c, int64_t ldc,
+                           void* workspace, int64_t workspace_bytes, void* hip_stream) {
+  return matmul_stages(stages, pa, a_codes, a_beta, a_scales, M, pw, w_codes, w_beta, w_scales,
+                       N, K, c, ldc, workspace, workspace_bytes, hip_stream, "nq_matmul_stages");
 }
 
 nq_status nq_matmul(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,

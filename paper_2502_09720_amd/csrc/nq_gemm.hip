@@ -164,6 +164,25 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
   for (int s = 0; s < NSTAGE - 1; ++s)
     if (s < nks) load_stage(s);
 
+  // Row and column scales of this lane's outputs, fetched now so that the epilogue issues
+  // only stores.  32x32 accumulator layout: lane l holds column l % 32; register e holds
+  // row 8 (e / 4) + 4 (l / 32) + (e % 4).  Indices are clamped into range (M, N >= 1).
+  const int64_t m0 = (int64_t)pm * BM + wm * (BM / WM) + 4 * (lane >> 5);
+  const int64_t n0 = (int64_t)pn * BN + wn * (BN / WN) + (lane & 31);
+  float rs[TM][16], cs[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int64_t row = m0 + i * 32 + 8 * (e >> 2) + (e & 3);
+      rs[i][e] = ra[row < M ? row : M - 1];
+    }
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int64_t col = n0 + j * 32;
+    cs[j] = rw[col < N ? col : N - 1] * scale;
+  }
+
   for (int ks = 0; ks < nks; ++ks) {
     // stage ks has landed when at most the later stages' loads are outstanding
     if (ks + NSTAGE - 2 < nks) {
@@ -233,22 +252,19 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
     }
   }
 
-  // Epilogue.  32x32 accumulator layout: lane l holds column l%32; register e holds row
-  // 8*(e/4) + 4*(l/32) + (e%4).
-  const int64_t m0 = (int64_t)pm * BM + wm * (BM / WM);
-  const int64_t n0 = (int64_t)pn * BN + wn * (BN / WN);
+  // Epilogue: C = acc * r_A * (r_W * scale); whole tiles skip the bounds tests.
+  float* cp = c + m0 * ldc + n0;
+  const bool whole = m0 - 4 * (lane >> 5) + BM / WM <= M && n0 - (lane & 31) + BN / WN <= N;
 #pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    const int64_t col = n0 + j * 32 + (lane & 31);
-    const float sw = col < N ? rw[col] * scale : 0.0f;
+  for (int j = 0; j < TN; ++j)
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int64_t row = m0 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        if (row < M && col < N) c[row * ldc + col] = acc[i][j][e] * (ra[row] * sw);
+        const int r = i * 32 + 8 * (e >> 2) + (e & 3);
+        if (whole || (m0 + r < M && n0 + j * 32 < N))
+          cp[r * ldc + j * 32] = acc[i][j][e] * (rs[i][e] * cs[j]);
       }
-  }
 }
 
 // Both tile configurations pad M to 256; N is padded to 256 (a multiple of both BN).
@@ -270,8 +286,8 @@ static void launch_gemm(const u32x4* wa, const u32x4* ww, int kp, int64_t mp, in
                      W.scales, A.rows, W.rows, c, ldc, scale);
 }
 
-hipError_t launch_matmul_decode_once(const MatmulOperand& A, const MatmulOperand& W, int64_t K,
-                                     float* c, int64_t ldc, float scale, void* ws,
+hipError_t launch_matmul_decode_once(int stages, const MatmulOperand& A, const MatmulOperand& W,
+                                     int64_t K, float* c, int64_t ldc, float scale, void* ws,
                                      hipStream_t st) {
   using namespace gemm;
   const int nb = (int)(K / 8);
@@ -281,14 +297,17 @@ hipError_t launch_matmul_decode_once(const MatmulOperand& A, const MatmulOperand
   const int nbp = kp / 8;
   u32x4* wa = reinterpret_cast<u32x4*>(ws);
   u32x4* ww = wa + mp * nbp;
-  int lg;
-  int64_t wgs;
-  grid_shape(mp, nbp, lg, wgs);
-  hipLaunchKernelGGL(tiles_kernel, dim3((unsigned)wgs), dim3(256), 0, st, A.codes, A.beta,
-                     A.rows, nb, mp, nbp, A.q, A.m2q, lg, wa);
-  grid_shape(np, nbp, lg, wgs);
-  hipLaunchKernelGGL(tiles_kernel, dim3((unsigned)wgs), dim3(256), 0, st, W.codes, W.beta,
-                     W.rows, nb, np, nbp, W.q, W.m2q, lg, ww);
+  if (stages & 1) {
+    int lg;
+    int64_t wgs;
+    grid_shape(mp, nbp, lg, wgs);
+    hipLaunchKernelGGL(tiles_kernel, dim3((unsigned)wgs), dim3(256), 0, st, A.codes, A.beta,
+                       A.rows, nb, mp, nbp, A.q, A.m2q, lg, wa);
+    grid_shape(np, nbp, lg, wgs);
+    hipLaunchKernelGGL(tiles_kernel, dim3((unsigned)wgs), dim3(256), 0, st, W.codes, W.beta,
+                       W.rows, nb, np, nbp, W.q, W.m2q, lg, ww);
+  }
+  if (!(stages & 2)) return hipGetLastError();
   // 256 x 256 tiles once they give every CU a tile, else 256 x 128
   if ((mp / 256) * (np / 256) >= 256) {
     launch_gemm<CfgBig>(wa, ww, kp, mp, np, A, W, c, ldc, scale, st);

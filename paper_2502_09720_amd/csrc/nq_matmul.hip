@@ -95,17 +95,21 @@ size_t skinny_workspace(int64_t M, int64_t K) {
   return (size_t)(mp * kp * 2);
 }
 
-hipError_t launch_matmul_skinny(const MatmulOperand& A, const MatmulOperand& W, int64_t K,
-                                float* c, int64_t ldc, float scale, void* ws, hipStream_t st) {
+hipError_t launch_matmul_skinny(int stages, const MatmulOperand& A, const MatmulOperand& W,
+                                int64_t K, float* c, int64_t ldc, float scale, void* ws,
+                                hipStream_t st) {
   const int nb = (int)(K / 8);
   const int64_t mp = (A.rows + 15) / 16 * 16;
   const int nbp = (int)((K + 31) / 32 * 32 / 8);
   u32x4* ta = reinterpret_cast<u32x4*>(ws);
-  int lg;
-  int64_t wgs;
-  grid_shape(mp, nbp, lg, wgs);
-  hipLaunchKernelGGL(tiles_kernel, dim3((unsigned)wgs), dim3(256), 0, st, A.codes, A.beta, A.rows,
-                     nb, mp, nbp, A.q, A.m2q, lg, ta);
+  if (stages & 1) {
+    int lg;
+    int64_t wgs;
+    grid_shape(mp, nbp, lg, wgs);
+    hipLaunchKernelGGL(tiles_kernel, dim3((unsigned)wgs), dim3(256), 0, st, A.codes, A.beta,
+                       A.rows, nb, mp, nbp, A.q, A.m2q, lg, ta);
+  }
+  if (!(stages & 2)) return hipGetLastError();
   const unsigned grid = (unsigned)((W.rows + 15) / 16);
   switch (mp / 16) {
     case 1: hipLaunchKernelGGL(skinny_kernel<1>, dim3(grid), dim3(256), 0, st, ta, nbp, A, W, nb, c, ldc, scale); break;

@@ -125,6 +125,30 @@ def test_matmul_ex_rejects_small_workspace(lib):
     assert st == 1
 
 
+@pytest.mark.parametrize("stages", [0, 4, 7, -1])
+def test_matmul_stages_rejects_bad_mask(lib, stages):
+    p = _p()
+    need = lib.nq_matmul_workspace_size(300, 200, 64)
+    st = lib.nq_matmul_stages(stages, ctypes.byref(p), FAKE, FAKE, FAKE, 300, ctypes.byref(p),
+                              FAKE, FAKE, FAKE, 200, 64, FAKE, 200, FAKE, need, S)
+    assert st == 1
+    assert b"stages" in lib.nq_last_error()
+
+
+def test_matmul_stages_validates_like_ex(lib):
+    p = _p()
+    need = lib.nq_matmul_workspace_size(300, 200, 64)
+    for stages in (1, 2, 3):
+        st = lib.nq_matmul_stages(stages, ctypes.byref(p), FAKE, FAKE, FAKE, 300,
+                                  ctypes.byref(p), FAKE, FAKE, FAKE, 200, 64, FAKE, 200, FAKE,
+                                  need - 16, S)
+        assert st == 1
+        st = lib.nq_matmul_stages(stages, ctypes.byref(p), FAKE, FAKE, FAKE, 300,
+                                  ctypes.byref(p), FAKE, FAKE, FAKE, 200, 64, FAKE, 100, FAKE,
+                                  need, S)
+        assert st == 1
+
+
 def test_matmul_empty_is_noop(lib):
     p = _p()
     assert lib.nq_matmul(ctypes.byref(p), NULL, NULL, NULL, 0, ctypes.byref(p), NULL, NULL,

@@ -286,6 +286,27 @@ def test_matmul_internal_workspace_matches_ex(nq):
     assert np.linalg.norm(out.cpu().numpy() - C) / np.linalg.norm(C) < 1e-6
 
 
+@pytest.mark.parametrize("M,N,K", [(40, 300, 512), (300, 200, 256)])
+def test_matmul_stages_compose_to_ex(nq, M, N, K):
+    """nq_matmul_stages(DECODE) then (CONTRACT) is nq_matmul_ex, bit for bit, on both the
+    skinny (M <= 64) and the decode-once path."""
+    torch = __import__("torch")
+    _, A32 = workloads.random_rows(72, M, K, dtype="bf16")
+    _, W32 = workloads.random_rows(73, N, K, dtype="bf16", scale=0.02)
+    C, (ac, ab, ar, ba), (wc, wb, wr, bw) = _oracle_product(A32, W32, 14, 14, 4)
+    a = upload_coded(ac, ab, ar, M, K, 14, 4, ba)
+    w = upload_coded(wc, wb, wr, N, K, 14, 4, bw)
+    ref = nq.matmul(a, w)
+    ws = torch.empty(nq.matmul_workspace_size(M, N, K), dtype=torch.uint8, device="cuda")
+    out = torch.full((M, N), float("nan"), device="cuda")
+    nq.matmul(a, w, out=out, workspace=ws, stages=nq.STAGE_DECODE)
+    assert torch.isnan(out).all()                      # the decode stage writes no output
+    nq.matmul(a, w, out=out, workspace=ws, stages=nq.STAGE_CONTRACT)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref)
+    assert np.linalg.norm(out.cpu().numpy() - C) / np.linalg.norm(C) < 1e-6
+
+
 def test_encode_tiny_entries(nq):
     """Entries many orders of magnitude below the row scale (the lattice input is then a
     tiny number of either sign next to exact zeros), in fp32 and bf16."""
