@@ -63,59 +63,87 @@ __device__ __forceinline__ int exact_sign_sum(const double (&t)[N]) {
 // In 2E8 units every output is P_l = 2 d_l + delta_l with delta_l = 2 g_l (D8), 1 (D8+1/2);
 // at the fixed coordinate delta = 2 - 2 g (D8) or 4 g - 1 (D8+1/2).
 // ---------------------------------------------------------------------------------------
-__device__ __forceinline__ void nearest_e8(const float (&y)[8], int (&P)[8]) {
-  float e[8];
+struct E8Cand {
   int d[8], g[8];
+  float e[8];
+  int p, r, odd1, odd2;
+  float ep, er, gap;
+};
+
+__device__ __forceinline__ void e8_candidates(const float (&y)[8], E8Cand& k) {
 #pragma unroll
   for (int l = 0; l < 8; ++l) {
     const float fl = floorf(y[l]);
-    d[l] = (int)fl;
-    g[l] = (y[l] > fl + 0.5f) ? 1 : 0;
-    e[l] = fabsf(y[l] - rintf(y[l]));
+    k.d[l] = (int)fl;
+    k.g[l] = (y[l] > fl + 0.5f) ? 1 : 0;
+    k.e[l] = fabsf(y[l] - rintf(y[l]));
   }
-  const int sum_d = ((d[0] + d[1]) + (d[2] + d[3])) + ((d[4] + d[5]) + (d[6] + d[7]));
-  const int sum_g = ((g[0] + g[1]) + (g[2] + g[3])) + ((g[4] + g[5]) + (g[6] + g[7]));
+  const int sum_d = ((k.d[0] + k.d[1]) + (k.d[2] + k.d[3])) + ((k.d[4] + k.d[5]) + (k.d[6] + k.d[7]));
+  const int sum_g = ((k.g[0] + k.g[1]) + (k.g[2] + k.g[3])) + ((k.g[4] + k.g[5]) + (k.g[6] + k.g[7]));
   int p = 0, r = 0;
-  float ep = e[0], er = e[0];
+  float ep = k.e[0], er = k.e[0];
 #pragma unroll
   for (int l = 1; l < 8; ++l) {
-    const bool up = e[l] > ep;    // strict: the lowest index wins ties
-    const bool dn = e[l] < er;
+    const bool up = k.e[l] > ep;    // strict: the lowest index wins ties
+    const bool dn = k.e[l] < er;
     p = up ? l : p;
-    ep = up ? e[l] : ep;
+    ep = up ? k.e[l] : ep;
     r = dn ? l : r;
-    er = dn ? e[l] : er;
+    er = dn ? k.e[l] : er;
   }
-  const int odd1 = (sum_d + sum_g) & 1;
-  const int odd2 = sum_d & 1;
-  float se = e[0];
+  k.p = p;
+  k.r = r;
+  k.ep = ep;
+  k.er = er;
+  k.odd1 = (sum_d + sum_g) & 1;
+  k.odd2 = sum_d & 1;
+  float se = k.e[0];
 #pragma unroll
-  for (int l = 1; l < 8; ++l) se = se + e[l];
+  for (int l = 1; l < 8; ++l) se = se + k.e[l];
   float gap = se - 2.0f;
-  if (odd1) gap = gap + (1.0f - 2.0f * ep);
-  if (odd2) gap = gap - 2.0f * er;
-  bool d8;
-  if (fabsf(gap) >= 1.0e-5f) {
-    d8 = gap < 0.0f;
-  } else {
-    double t[12];
+  if (k.odd1) gap = gap + (1.0f - 2.0f * ep);
+  if (k.odd2) gap = gap - 2.0f * er;
+  k.gap = gap;
+}
+
+// The exact sign of the gap from its exact fp32 terms (rare: |fp32 gap| < 1e-5).
+__device__ __forceinline__ bool e8_gap_negative_exact(const E8Cand& k) {
+  double t[12];
 #pragma unroll
-    for (int l = 0; l < 8; ++l) t[l] = (double)e[l];
-    t[8] = -2.0;
-    t[9] = odd1 ? 1.0 : 0.0;
-    t[10] = odd1 ? -2.0 * (double)ep : 0.0;
-    t[11] = odd2 ? -2.0 * (double)er : 0.0;
-    d8 = exact_sign_sum<12>(t) < 0;
-  }
+  for (int l = 0; l < 8; ++l) t[l] = (double)k.e[l];
+  t[8] = -2.0;
+  t[9] = k.odd1 ? 1.0 : 0.0;
+  t[10] = k.odd1 ? -2.0 * (double)k.ep : 0.0;
+  t[11] = k.odd2 ? -2.0 * (double)k.er : 0.0;
+  return exact_sign_sum<12>(t) < 0;
+}
+
+__device__ __forceinline__ void e8_point(const E8Cand& k, bool d8, int (&P)[8]) {
   // delta for g = 0 / g = 1, off and on the fixed coordinate
   const int a_g0 = d8 ? 0 : 1, a_g1 = d8 ? 2 : 1;
   const int b_g0 = d8 ? 2 : -1, b_g1 = d8 ? 0 : 3;
-  const int fix = d8 ? (odd1 ? p : 8) : (odd2 ? r : 8);
+  const int fix = d8 ? (k.odd1 ? k.p : 8) : (k.odd2 ? k.r : 8);
 #pragma unroll
   for (int l = 0; l < 8; ++l) {
-    const int delta = (l == fix) ? (g[l] ? b_g1 : b_g0) : (g[l] ? a_g1 : a_g0);
-    P[l] = 2 * d[l] + delta;
+    const int delta = (l == fix) ? (k.g[l] ? b_g1 : b_g0) : (k.g[l] ? a_g1 : a_g0);
+    P[l] = 2 * k.d[l] + delta;
   }
+}
+
+__device__ __forceinline__ void nearest_e8(const float (&y)[8], int (&P)[8]) {
+  E8Cand k;
+  e8_candidates(y, k);
+  const bool d8 = fabsf(k.gap) >= 1.0e-5f ? k.gap < 0.0f : e8_gap_negative_exact(k);
+  e8_point(k, d8, P);
+}
+
+// nearest_e8 without the exact fallback: false (P unset) when the fp32 gap cannot decide.
+__device__ __forceinline__ bool nearest_e8_fast(const float (&y)[8], int (&P)[8]) {
+  E8Cand k;
+  e8_candidates(y, k);
+  if (fabsf(k.gap) < 1.0e-5f) return false;
+  e8_point(k, k.gap < 0.0f, P);
+  return true;
 }
 
 // max over the 240 roots lambda of E8 of <P, lambda> for P in 2E8 units:

@@ -313,18 +313,23 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_kernel(
 }
 
 // ---------------------------------------------------------------------------------------
-// Wave-compacted encoder.
+// Slot-compacted encoder (rows of up to 2048 blocks).
 //
-// A wave owns 64 * BPT blocks ("slots"): slot i of lane l is block j of row row_w, with
+// A workgroup of four waves owns 256 * BPT blocks ("slots"): slot s = 64 i + l of wave w is
+// block j of row row_w, with
 //   LANES <  64: row_w = i * (64 / LANES) + l / LANES, j = l % LANES  (a row per lane group
 //                and pass; 64 / LANES * BPT rows per wave)
 //   LANES == 64: row_w = 0, j = l + 64 i                              (one row per wave)
-//   LANES == 256: row_w = 0, j = 64 * wave + l + 256 i                (one row per workgroup)
-// Phase 1 evaluates every slot at the predicted beta (see encode_block) and finishes it
-// unless the point's root bound says it overloads or lies on the cell boundary.  Those slots
-// (about 18% on Gaussian-like rows) go to a per-wave queue in LDS, and phase 2 finishes them
-// with every lane busy, instead of the whole wave paying for the work a few lanes need.  Two-bit beta
-// indices are staged in LDS and packed into words at the end.
+//   LANES == 256: row_w = 0, j = 64 w + l + 256 i                     (one row per workgroup)
+// Phase 0 reads every slot from HBM once (all of a lane's loads in flight together), stages
+// it in LDS and forms the row sums of squares; then one lane per row turns its sum into the
+// scale r and the four multipliers c_t.  Phase 1 evaluates every slot at the first beta the
+// root bound of x does not rule out (predict_beta) with the fp32 nearest-point decision,
+// and finishes it unless that decision was too close to call, or the point's exact root
+// bound says it overloads (start again at the next beta) or lies on the cell boundary (the
+// literal test decides).  Those slots (about 12-15% on Gaussian-like and heavy-tailed
+// rows) are queued, and phase 2 finishes them with every lane of the workgroup busy.
+// Two-bit beta indices are staged in LDS and packed into words at the end.
 // ---------------------------------------------------------------------------------------
 template <int LANES, int BPT>
 struct SlotMap {
@@ -335,6 +340,20 @@ struct SlotMap {
   __device__ static int row_w(int i, int l) { return LANES < 64 ? i * RPP + l / LANES : 0; }
   __device__ static int j(int i, int l, int wave) {
     return LANES < 64 ? l % LANES : (LANES == 64 ? l + 64 * i : 64 * wave + l + LANES * i);
+  }
+  // inverse map for block j of row row_w: wave and slot
+  __device__ static void slot_of(int row_w, int j, int wave_hint, int& w, int& s) {
+    if constexpr (LANES < 64) {
+      w = wave_hint;
+      s = (row_w / RPP) * 64 + (row_w % RPP) * LANES + j;
+    } else if constexpr (LANES == 64) {
+      w = wave_hint;
+      s = j;
+    } else {
+      const int rem = j % LANES;
+      w = rem >> 6;
+      s = (j / LANES) * 64 + (rem & 63);
+    }
   }
 };
 
@@ -359,7 +378,7 @@ __device__ __forceinline__ void finish_block(const float (&v)[8], const float (&
   word = encode_codes(P, a.q, a.rq, a.mq);
 }
 
-// Raw input of one block kept in registers: 16 B for 16-bit types, 32 B for fp32.
+// Raw input of one block: 16 B for 16-bit types, 32 B for fp32.
 template <typename T> struct RawBlock { u32x4 w; };
 template <> struct RawBlock<float> { f32x4 a, b; };
 
@@ -432,148 +451,169 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
   using SM = SlotMap<LANES, BPT>;
   constexpr int SLOTS = SM::SLOTS;
   constexpr int RW = SM::ROWS_PER_WAVE;
-  __shared__ double red[8];
+  constexpr int CW = SM::WGROW ? 1 : 4;          // row tables: per wave, or one per workgroup
+  __shared__ RawBlock<T> rawl[4][SLOTS];
   __shared__ uint32_t queue[4][SLOTS];
   __shared__ uint8_t tsl[4][SLOTS];
-  __shared__ float crow[4][RW][4];
-  __shared__ float rrow[4][RW];
+  __shared__ float crow[CW][RW][4];
+  __shared__ float rrow[CW][RW];
+  __shared__ double rsum[4][RW];
+  __shared__ int qlen[4];
 
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int cw = SM::WGROW ? 0 : wave;
   const int nb = cols >> 3;
   const int nbw = (nb + 15) >> 4;
-  const int64_t row0 = SM::WGROW ? (int64_t)blockIdx.x : ((int64_t)blockIdx.x * 4 + wave) * RW;
+  auto row_base = [&](int w) -> int64_t {
+    return SM::WGROW ? (int64_t)blockIdx.x : ((int64_t)blockIdx.x * 4 + w) * RW;
+  };
+  const int64_t row0 = row_base(wave);
   const double n = (double)cols;
 
-  // ---- load the slots (raw) and compute the row scales ----
-  RawBlock<T> raw[BPT];
-#pragma unroll
-  for (int i = 0; i < BPT; ++i) {
-    const int rw = SM::row_w(i, lane), j = SM::j(i, lane, wave);
-    const int64_t row = row0 + rw;
-    if (row < rows && j < nb) {
-      load_raw<T>(x + row * ld_x + 8 * j, raw[i]);
-    } else {
-      zero_raw<T>(raw[i]);
-    }
-  }
-  auto sumsq = [&](int i) {
-    float v[8];
-    unpack_raw<T>(raw[i], v);
-    double s = 0.0;
-#pragma unroll
-    for (int l = 0; l < 8; ++l) s = __builtin_fma((double)v[l], (double)v[l], s);
-    return s;
-  };
-  auto sumsq_dd = [&](int i, double& hi, double& lo) {
-    float v[8];
-    unpack_raw<T>(raw[i], v);
-#pragma unroll
-    for (int l = 0; l < 8; ++l) dd_add_square(hi, lo, v[l]);
-  };
-  auto set_row = [&](int rw, float r) {
-    const bool coded = (r > 0.0f) && isfinite(r);
-    rrow[wave][rw] = coded ? r : 0.0f;
-#pragma unroll
-    for (int t = 0; t < 4; ++t)
-      crow[wave][rw][t] = coded ? (float)(1.0 / ((double)r * a.beta[t])) : 0.0f;
-  };
-  if constexpr (LANES < 64) {
-    // one row per lane group and pass: group reductions by shuffles only
+  // ---- phase 0: stage the slots in LDS, row sums of squares ----
+  {
+    RawBlock<T> raw[BPT];
 #pragma unroll
     for (int i = 0; i < BPT; ++i) {
-      const double s = group_sum<LANES>(sumsq(i), red);
+      const int rw = SM::row_w(i, lane), j = SM::j(i, lane, wave);
+      const int64_t row = row0 + rw;
+      if (row < rows && j < nb) {
+        load_raw<T>(x + row * ld_x + 8 * j, raw[i]);
+      } else {
+        zero_raw<T>(raw[i]);
+      }
+    }
+    double part = 0.0;
+#pragma unroll
+    for (int i = 0; i < BPT; ++i) {
+      rawl[wave][i * 64 + lane] = raw[i];
+      float v[8];
+      unpack_raw<T>(raw[i], v);
+      double s = 0.0;
+#pragma unroll
+      for (int l = 0; l < 8; ++l) s = __builtin_fma((double)v[l], (double)v[l], s);
+      if constexpr (LANES < 64) {
+#pragma unroll
+        for (int m = 1; m < LANES; m <<= 1) s += __shfl_xor(s, m, 64);
+        if (lane % LANES == 0) rsum[wave][SM::row_w(i, lane)] = s;
+      } else {
+        part += s;
+      }
+    }
+    if constexpr (LANES >= 64) {
+#pragma unroll
+      for (int m = 1; m < 64; m <<= 1) part += __shfl_xor(part, m, 64);
+      if (lane == 0) rsum[wave][0] = part;
+    }
+  }
+  __syncthreads();
+
+  // ---- row scales and multipliers: one lane per row ----
+  {
+    const bool mine = SM::WGROW ? threadIdx.x == 0 : lane < RW;
+    const int rw = SM::WGROW ? 0 : lane;
+    const int64_t row = row0 + rw;
+    if (mine && row < rows) {
+      double s = rsum[wave][rw];
+      if constexpr (SM::WGROW) s = ((rsum[0][0] + rsum[1][0]) + rsum[2][0]) + rsum[3][0];
       bool sure;
       float r = rms_candidate(s, n, sure);
       if (!sure) {
+        // rare: the double-double sum of the row, block by block from LDS
         double hi = 0.0, lo = 0.0;
-        sumsq_dd(i, hi, lo);
-        group_sum_dd<LANES>(hi, lo, red);
-        r = exact_rms(hi, lo, n, r);
-      }
-      const int rw = SM::row_w(i, lane);
-      if (lane % LANES == 0) {
-        set_row(rw, r);
-        if (row0 + rw < rows) scales[row0 + rw] = r;
-      }
-    }
-  } else {
-    double s = 0.0;
+        for (int j = 0; j < nb; ++j) {
+          int w, sl;
+          SM::slot_of(rw, j, wave, w, sl);
+          float v[8];
+          unpack_raw<T>(rawl[w][sl], v);
 #pragma unroll
-    for (int i = 0; i < BPT; ++i) s += sumsq(i);
-    s = group_sum<LANES>(s, red);       // LANES == 256: every thread gets the same sum
-    bool sure;
-    float r = rms_candidate(s, n, sure);
-    if (!sure) {                        // uniform over the wave (LANES 64) or workgroup (256)
-      double hi = 0.0, lo = 0.0;
+          for (int l = 0; l < 8; ++l) dd_add_square(hi, lo, v[l]);
+        }
+        double t, e;
+        two_sum(hi, lo, t, e);
+        r = exact_rms(t, e, n, r);
+      }
+      const bool coded = (r > 0.0f) && isfinite(r);
+      rrow[cw][rw] = coded ? r : 0.0f;
 #pragma unroll
-      for (int i = 0; i < BPT; ++i) sumsq_dd(i, hi, lo);
-      group_sum_dd<LANES>(hi, lo, red);
-      r = exact_rms(hi, lo, n, r);
-    }
-    if (lane == 0) {
-      set_row(0, r);
-      if (row0 < rows && (!SM::WGROW || wave == 0)) scales[row0] = r;
+      for (int t = 0; t < 4; ++t)
+        crow[cw][rw][t] = coded ? (float)(1.0 / ((double)r * a.beta[t])) : 0.0f;
+      scales[row] = r;
     }
   }
+  __syncthreads();
 
-  // ---- phase 1: slots whose predicted beta surely does not overload ----
+  // ---- phase 1: every slot at its predicted beta ----
   int qn = 0;   // queue length, uniform over the wave
-#pragma unroll
+#pragma unroll 1
   for (int i = 0; i < BPT; ++i) {
+    const int sl = i * 64 + lane;
     const int rw = SM::row_w(i, lane), j = SM::j(i, lane, wave);
     const int64_t row = row0 + rw;
     const bool valid = row < rows && j < nb;
-    const bool coded = valid && rrow[wave][rw] != 0.0f;
-    float v[8], c[4];
-    unpack_raw<T>(raw[i], v);
+    const bool coded = valid && rrow[cw][rw] != 0.0f;
+    bool queued = false;
+    int start = 0, t0 = 0;
+    int P[8];
+    if (coded) {
+      float v[8], c[4];
+      unpack_raw<T>(rawl[wave][sl], v);
 #pragma unroll
-    for (int t = 0; t < 4; ++t) c[t] = crow[wave][rw][t];
-    bool sure = false;
-    int t0 = 0;
-    if (coded) t0 = predict_beta(root_bound_f(v), c, a, sure);
-    // the last beta needs no test either
-    const bool direct = coded && (sure || t0 == a.k - 1);
-    const bool need = coded && !direct;
-    uint32_t word = 0;
-    if (direct) {
-      float y[8];
+      for (int t = 0; t < 4; ++t) c[t] = crow[cw][rw][t];
+      bool sure;
+      t0 = predict_beta(root_bound_f(v), c, a, sure);
       const float ct = pick4(c, t0);
+      float y[8];
 #pragma unroll
       for (int l = 0; l < 8; ++l) y[l] = v[l] * ct;
-      int P[8];
-      nearest_e8(y, P);
-      word = encode_codes(P, a.q, a.rq, a.mq);
+      if (!nearest_e8_fast(y, P)) {
+        queued = true;                 // decision too close for fp32: redo exactly
+        start = t0;
+      } else if (!sure && t0 < a.k - 1) {
+        const int M = e8_root_bound(P);
+        if (M >= 2 * a.q) {            // overloads (>), or on the boundary (=): decide later
+          queued = true;
+          start = M > 2 * a.q ? t0 + 1 : t0;
+        }
+      }
     }
-    const uint64_t mask = __ballot(need);
-    if (need) {
+    const uint64_t mask = __ballot(queued);
+    if (queued) {
       const int pos = qn + __popcll(mask & ((1ull << lane) - 1ull));
-      queue[wave][pos] = ((uint32_t)(i * 64 + lane) << 2) | (uint32_t)t0;
+      queue[wave][pos] = ((uint32_t)sl << 2) | (uint32_t)start;
     } else if (valid) {
-      codes[row * nb + j] = word;
-      tsl[wave][i * 64 + lane] = (uint8_t)(direct ? t0 : 0);
+      codes[row * nb + j] = coded ? encode_codes(P, a.q, a.rq, a.mq) : 0u;
+      tsl[wave][sl] = (uint8_t)t0;
     }
     qn += __popcll(mask);
   }
+  if (lane == 0) qlen[wave] = qn;
+  __syncthreads();
 
-  // ---- phase 2: the queued slots, compacted over the wave ----
-  for (int base = 0; base < qn; base += 64) {
-    if (base + lane < qn) {
-      const uint32_t e = queue[wave][base + lane];
+  // ---- phase 2: the queued slots of the whole workgroup, every lane busy ----
+  {
+    const int q0 = qlen[0], q1 = q0 + qlen[1], q2 = q1 + qlen[2], total = q2 + qlen[3];
+    for (int idx = threadIdx.x; idx < total; idx += 256) {
+      const int w = (idx >= q0) + (idx >= q1) + (idx >= q2);
+      const int off = w == 0 ? 0 : (w == 1 ? q0 : (w == 2 ? q1 : q2));
+      const uint32_t e = queue[w][idx - off];
       const int sl = (int)(e >> 2), t = (int)(e & 3u);
       const int i = sl >> 6, l = sl & 63;
-      const int rw = SM::row_w(i, l), j = SM::j(i, l, wave);
-      const int64_t row = row0 + rw;
-      float xv[8], c[4];
-      load_block<T>(x + row * ld_x + 8 * j, xv);
+      const int rw = SM::row_w(i, l), j = SM::j(i, l, w);
+      const int64_t row = row_base(w) + rw;
+      const int c2 = SM::WGROW ? 0 : w;
+      float v[8], c[4];
+      unpack_raw<T>(rawl[w][sl], v);
 #pragma unroll
-      for (int tt = 0; tt < 4; ++tt) c[tt] = crow[wave][rw][tt];
+      for (int tt = 0; tt < 4; ++tt) c[tt] = crow[c2][rw][tt];
       uint32_t word;
       int tsel;
-      finish_block(xv, c, t, a, word, tsel);
+      finish_block(v, c, t, a, word, tsel);
       codes[row * nb + j] = word;
-      tsl[wave][sl] = (uint8_t)tsel;
+      tsl[w][sl] = (uint8_t)tsel;
     }
   }
+  __syncthreads();
 
   // ---- beta words: 16 two-bit indices of consecutive blocks (consecutive lanes) ----
 #pragma unroll
