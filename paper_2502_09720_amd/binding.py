@@ -26,7 +26,7 @@ class _Params(ctypes.Structure):
 
 
 def library_path():
-    return os.environ.get("NESTQUANT_LIB", os.path.join(PKG, "libnestquant.so"))
+    return os.environ.get("NESTQUANT_LIB") or os.path.join(PKG, "libnestquant.so")
 
 
 def library():

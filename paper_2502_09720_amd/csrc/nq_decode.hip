@@ -9,12 +9,6 @@
 
 namespace nq {
 
-__device__ __forceinline__ uint32_t f32_to_bf16_bits(float f) {
-  // round to nearest even (the inputs are finite)
-  const uint32_t u = __float_as_uint(f);
-  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-}
-
 template <int OUT>  // 0 = fp32, 1 = fp16, 2 = bf16
 __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict__ codes,
                                                      const uint32_t* __restrict__ beta,
@@ -22,42 +16,50 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict_
                                                      int64_t rows, int nb, int lg,
                                                      void* __restrict__ out, int64_t ld_out,
                                                      DecodeArgs a) {
-  int64_t row;
-  int j;
-  grid_block(nb, lg, row, j);
-  if (row >= rows || j >= nb) return;
+  const GridPos g = grid_block(nb, lg);
+  if (g.rb + g.lr >= rows || g.j >= nb) return;
+  const int j = g.j;
   const int nbw = (nb + 15) >> 4;
-  const uint32_t w = __builtin_nontemporal_load(codes + row * nb + j);
-  const uint32_t bw = beta[row * nbw + (j >> 4)];
+  const uint32_t w = __builtin_nontemporal_load(codes + g.rb * nb + (uint32_t)(g.lr * nb + j));
+  const uint32_t bw = beta[g.rb * nbw + (uint32_t)(g.lr * nbw + (j >> 4))];
   const int t = (int)((bw >> (2 * (j & 15))) & 3u);
-  const double sc = (double)scales[row] * a.half_beta[t];
+  const double sc = (double)scales[g.rb + g.lr] * a.half_beta[t];
   uint32_t X2p[4];
   decode_word_pk(w, a.q, a.m2q, X2p);
-  float v[8];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    v[2 * i] = (float)(sc * (double)(int)(short)(X2p[i] & 0xFFFFu));
-    v[2 * i + 1] = (float)(sc * (double)((int)X2p[i] >> 16));
-  }
   if constexpr (OUT == 0) {
-    f32x4* o = reinterpret_cast<f32x4*>((float*)out + row * ld_out + 8 * j);
+    // fp32: each value rounded once from its fp64 product
+    float v[8];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = (float)(sc * (double)(int)(short)(X2p[i] & 0xFFFFu));
+      v[2 * i + 1] = (float)(sc * (double)((int)X2p[i] >> 16));
+    }
+    f32x4* o = reinterpret_cast<f32x4*>((float*)out + (g.rb + g.lr) * ld_out + 8 * j);
     const f32x4 lo = {v[0], v[1], v[2], v[3]};
     const f32x4 hi = {v[4], v[5], v[6], v[7]};
     __builtin_nontemporal_store(lo, o);
     __builtin_nontemporal_store(hi, o + 1);
   } else {
-    uint32_t h[8];
+    // 16-bit outputs: X2 (|X2| <= 32) times the fp32-rounded scale is within two fp32
+    // roundings (relative 2^-23) of the exact value, far below half an fp16 / bf16 ulp,
+    // so the final rounding lands on the nearest or the adjacent 16-bit value
+    const float s32 = (float)sc;
+    uint32_t pk[4];
 #pragma unroll
-    for (int l = 0; l < 8; ++l) {
+    for (int i = 0; i < 4; ++i) {
+      const float lo = (float)(int)(short)(X2p[i] & 0xFFFFu) * s32;
+      const float hi = (float)((int)X2p[i] >> 16) * s32;
       if constexpr (OUT == 1) {
-        h[l] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)v[l]);
+        pk[i] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)lo) |
+                ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)hi) << 16);
       } else {
-        h[l] = f32_to_bf16_bits(v[l]);
+        pk[i] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)lo) |
+                ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)hi) << 16);
       }
     }
-    const u32x4 pk = {h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
-                      h[6] | (h[7] << 16)};
-    __builtin_nontemporal_store(pk, reinterpret_cast<u32x4*>((uint16_t*)out + row * ld_out + 8 * j));
+    const u32x4 v = {pk[0], pk[1], pk[2], pk[3]};
+    __builtin_nontemporal_store(
+        v, reinterpret_cast<u32x4*>((uint16_t*)out + (g.rb + g.lr) * ld_out + 8 * j));
   }
 }
 

@@ -402,15 +402,26 @@ __device__ __forceinline__ void decode_word_pk(uint32_t w, int q, uint32_t m2q,
 // One thread per block of a rows x nb grid of blocks, 256 threads per workgroup: rows
 // shorter than 256 blocks are packed (a power-of-two group of lanes per row), longer rows
 // are cut into 256-block segments.  lg = log2 of the group size (for nb <= 256) or -1.
-__device__ __forceinline__ void grid_block(int nb, int lg, int64_t& row, int& j) {
+// The workgroup's first row rb is uniform; the thread's row is rb + lr and its block j, so
+// per-thread offsets inside the workgroup's rows fit 32 bits.
+struct GridPos {
+  int64_t rb;
+  int lr, j;
+};
+__device__ __forceinline__ GridPos grid_block(int nb, int lg) {
+  GridPos g;
   if (lg >= 0) {
-    row = (int64_t)blockIdx.x * (256 >> lg) + (threadIdx.x >> lg);
-    j = threadIdx.x & ((1 << lg) - 1);
+    g.rb = (int64_t)blockIdx.x * (256 >> lg);
+    g.lr = (int)(threadIdx.x >> lg);
+    g.j = (int)(threadIdx.x & ((1u << lg) - 1u));
   } else {
     const uint32_t segs = ((uint32_t)nb + 255u) / 256u;
-    row = blockIdx.x / segs;
-    j = (int)(blockIdx.x - (uint32_t)row * segs) * 256 + threadIdx.x;
+    const uint32_t row = blockIdx.x / segs;
+    g.rb = row;
+    g.lr = 0;
+    g.j = (int)(blockIdx.x - row * segs) * 256 + (int)threadIdx.x;
   }
+  return g;
 }
 
 // t * X2 of one block as eight bf16 (exact: |t X2| <= 4 * 32 = 128 < 2^8): the upper halves

@@ -323,11 +323,11 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_kernel(
 //   LANES == 256: row_w = 0, j = 64 w + l + 256 i                     (one row per workgroup)
 // Phase 0 reads every slot from HBM once (all of a lane's loads in flight together), stages
 // it in LDS and forms the row sums of squares; then one lane per row turns its sum into the
-// scale r and the four multipliers c_t.  Phase 1 evaluates every slot at the first beta the
-// root bound of x does not rule out (predict_beta) with the fp32 nearest-point decision,
-// and finishes it unless that decision was too close to call, or the point's exact root
-// bound says it overloads (start again at the next beta) or lies on the cell boundary (the
-// literal test decides).  Those slots (about 12-15% on Gaussian-like and heavy-tailed
+// scale r, the four multipliers c_t and the thresholds of skip_threshold.  Phase 1 evaluates
+// every slot at the first beta the root bound of x does not rule out, with the fp32
+// nearest-point decision, and finishes it unless that decision was too close to call, or
+// the point's exact root bound says it overloads (start again at the next beta) or lies on
+// the cell boundary (the literal test decides).  Those slots (about 12-15% on Gaussian-like and heavy-tailed
 // rows) are queued, and phase 2 finishes them with every lane of the workgroup busy.
 // Two-bit beta indices are staged in LDS and packed into words at the end.
 // ---------------------------------------------------------------------------------------
@@ -424,24 +424,16 @@ __device__ __forceinline__ void unpack_raw<_Float16>(const RawBlock<_Float16>& r
   }
 }
 
-// First beta that the root bound does not rule out, and whether it surely does not overload.
-__device__ __forceinline__ int predict_beta(float mx, const float (&c)[4], const EncodeArgs& a,
-                                            bool& sure) {
-  const float two_q = (float)(2 * a.q);
-  int t0 = a.k - 1;
-  sure = false;
-#pragma unroll
-  for (int s = a_max_k - 1; s >= 0; --s) {
-    if (s < a.k) {
-      const float u = 2.0f * c[s] * mx;
-      const float margin = kRootMargin + u * 0x1p-12f;
-      if (u - margin <= two_q) {
-        t0 = s;
-        sure = (u + margin < two_q);
-      }
-    }
-  }
-  return t0;
+// Threshold on the root bound M(x) of a block above which beta t surely overloads: for the
+// nearest point P of y = fl32(c x), M(P) >= 2 M(y) - 2 sqrt(2) (covering radius 1, roots of
+// norm sqrt(2)) and M(y) = c M(x) up to relative rounding errors below 2^-19 (y, and the
+// fp32 evaluation of M), so M(x) > (2q + 2 sqrt(2) + 0.02) / (2 c (1 - 2^-12)) implies
+// M(P) > 2q.  Rounded up.
+__device__ __forceinline__ float skip_threshold(float c, int q) {
+  const double v = (2.0 * q + (double)kRootMargin) / (2.0 * (double)c * (1.0 - 0x1p-12));
+  float f = (float)v;
+  if ((double)f < v) f = next_up(f);
+  return f;
 }
 
 template <typename T, int LANES, int BPT>
@@ -456,6 +448,7 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
   __shared__ uint32_t queue[4][SLOTS];
   __shared__ uint8_t tsl[4][SLOTS];
   __shared__ float crow[CW][RW][4];
+  __shared__ __attribute__((aligned(16))) float chi[CW][RW][4];
   __shared__ float rrow[CW][RW];
   __shared__ double rsum[4][RW];
   __shared__ int qlen[4];
@@ -536,14 +529,18 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
       const bool coded = (r > 0.0f) && isfinite(r);
       rrow[cw][rw] = coded ? r : 0.0f;
 #pragma unroll
-      for (int t = 0; t < 4; ++t)
-        crow[cw][rw][t] = coded ? (float)(1.0 / ((double)r * a.beta[t])) : 0.0f;
+      for (int t = 0; t < 4; ++t) {
+        const float c = coded ? (float)(1.0 / ((double)r * a.beta[t])) : 0.0f;
+        crow[cw][rw][t] = c;
+        chi[cw][rw][t] = (coded && t < a.k - 1) ? skip_threshold(c, a.q) : INFINITY;
+      }
       scales[row] = r;
     }
   }
   __syncthreads();
 
   // ---- phase 1: every slot at its predicted beta ----
+  uint32_t* __restrict__ codes_w = codes + row0 * nb;   // this wave's rows
   int qn = 0;   // queue length, uniform over the wave
 #pragma unroll 1
   for (int i = 0; i < BPT; ++i) {
@@ -556,20 +553,20 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
     int start = 0, t0 = 0;
     int P[8];
     if (coded) {
-      float v[8], c[4];
+      float v[8];
       unpack_raw<T>(rawl[wave][sl], v);
-#pragma unroll
-      for (int t = 0; t < 4; ++t) c[t] = crow[cw][rw][t];
-      bool sure;
-      t0 = predict_beta(root_bound_f(v), c, a, sure);
-      const float ct = pick4(c, t0);
+      // first beta whose point is not surely overloaded: one threshold test per beta
+      const float mx = root_bound_f(v);
+      const f32x4 hi = *reinterpret_cast<const f32x4*>(chi[cw][rw]);
+      t0 = mx > hi.x ? (mx > hi.y ? (mx > hi.z ? 3 : 2) : 1) : 0;
+      const float ct = crow[cw][rw][t0];
       float y[8];
 #pragma unroll
       for (int l = 0; l < 8; ++l) y[l] = v[l] * ct;
       if (!nearest_e8_fast(y, P)) {
         queued = true;                 // decision too close for fp32: redo exactly
         start = t0;
-      } else if (!sure && t0 < a.k - 1) {
+      } else if (t0 < a.k - 1) {
         const int M = e8_root_bound(P);
         if (M >= 2 * a.q) {            // overloads (>), or on the boundary (=): decide later
           queued = true;
@@ -582,7 +579,7 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
       const int pos = qn + __popcll(mask & ((1ull << lane) - 1ull));
       queue[wave][pos] = ((uint32_t)sl << 2) | (uint32_t)start;
     } else if (valid) {
-      codes[row * nb + j] = coded ? encode_codes(P, a.q, a.rq, a.mq) : 0u;
+      codes_w[rw * nb + j] = coded ? encode_codes(P, a.q, a.rq, a.mq) : 0u;
       tsl[wave][sl] = (uint8_t)t0;
     }
     qn += __popcll(mask);

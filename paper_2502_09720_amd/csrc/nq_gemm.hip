@@ -16,8 +16,8 @@
 // wave owns (BM/WM) x (BN/WN) as v_mfma_f32_32x32x16_bf16 tiles.  K advances 64 bf16
 // (128 B per row) per stage through NSTAGE LDS buffers filled by global_load_lds_dwordx4:
 // each wave instruction moves 8 rows x 128 B straight into LDS (no register staging).  The
-// 16-byte chunk c of row r is stored at chunk c ^ (r & 7), so that the fragment reads (32
-// rows, one chunk) hit distinct LDS banks.  Stage k+NSTAGE-1 is loaded while stage k is
+// 16-byte chunk c of row r is stored at chunk c ^ swz(r) (see swz), so that the fragment
+// reads (32 rows, one chunk) hit distinct LDS banks.  Stage k+NSTAGE-1 is loaded while stage k is
 // multiplied.  Workgroups are mapped so that the tiles resident on one XCD (workgroup id
 // mod 8) form a compact 4-row band of the tile grid and share their A and W rows in that
 // XCD's L2.
@@ -60,18 +60,19 @@ __global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__
                                                     int64_t rows, int nb, int64_t rows_p,
                                                     int nb_p, int q, uint32_t m2q, int lg,
                                                     u32x4* __restrict__ ws) {
-  int64_t row;
-  int j;
-  grid_block(nb_p, lg, row, j);
+  const GridPos g = grid_block(nb_p, lg);
+  const int64_t row = g.rb + g.lr;
+  const int j = g.j;
   if (row >= rows_p || j >= nb_p) return;
   u32x4 out = {0u, 0u, 0u, 0u};
   if (row < rows && j < nb) {
-    const uint32_t w = __builtin_nontemporal_load(codes + row * nb + j);
-    const uint32_t bw = beta[row * ((nb + 15) >> 4) + (j >> 4)];
+    const int nbw = (nb + 15) >> 4;
+    const uint32_t w = __builtin_nontemporal_load(codes + g.rb * nb + (uint32_t)(g.lr * nb + j));
+    const uint32_t bw = beta[g.rb * nbw + (uint32_t)(g.lr * nbw + (j >> 4))];
     const int t = (int)((bw >> (2 * (j & 15))) & 3u) + 1;
     out = decode_tile_bf16(w, t, q, m2q);
   }
-  ws[row * nb_p + j] = out;
+  ws[g.rb * nb_p + (uint32_t)(g.lr * nb_p + j)] = out;
 }
 
 __device__ __forceinline__ void tile_coords(int bid, int tm, int tn, int& pm, int& pn) {
