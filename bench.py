@@ -35,7 +35,6 @@ def parse():
     ap.add_argument("--workload", type=int, default=3, help="workload id (see workloads.py)")
     ap.add_argument("--q", type=int, default=None, help="override q (workload 4 has q=7 too)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-rows", type=int, default=512)
     ap.add_argument("--kv", action="store_true",
                     help="standalone nq_encode / nq_decode of the 2^28-entry fp16 KV-like "
                          "matrix (2^21 rows of 128) against the HBM roofline")
@@ -143,8 +142,11 @@ def algorithmic(M, N, K, in_bytes):
     return enc_bytes, mm_bytes, flops
 
 
-def cpu_baseline(cfg, q, k, sample_rows, flops_full):
-    """The oracle, as it stands, on a bounded sample of the same workload, extrapolated."""
+def cpu_baseline(cfg, q, k, flops_full, min_seconds=10.0, max_reps=5):
+    """The oracle, as it stands, on the whole step of the workload, repeated until about
+    min_seconds of CPU time have been measured: encode of A, decode of A and W into integer
+    tiles, and the exact fp64 product with the scale epilogue.  W's coding is excluded, as
+    on the GPU (W is a weight, coded once)."""
     import numpy as np
     import workloads
     from oracle import nestquant
@@ -155,37 +157,31 @@ def cpu_baseline(cfg, q, k, sample_rows, flops_full):
         blas_threads = 1
     c = workloads.CONFIGS[cfg]
     M, N, K = c["M"], c["N"], c["K"]
-    ma = min(M, sample_rows)
-    nw = min(N, 2 * sample_rows)
-    _, A32, _ = workloads.operand(cfg, "A", row_range=(0, ma))
-    _, W32, _ = workloads.operand(cfg, "W", row_range=(0, nw))
+    _, A32, _ = workloads.operand(cfg, "A")
+    _, W32, _ = workloads.operand(cfg, "W")
     base = nestquant.default_base(q, k)
-    t0 = time.perf_counter()
-    ca, ta, ra = nestquant.quantize_rows(A32, q, k)
-    t1 = time.perf_counter()
-    cw, tw, rw = nestquant.quantize_rows(W32, q, k)   # W is coded offline: not counted
-    t2 = time.perf_counter()
-    TA = nestquant.integer_tiles(ca, ta, q).astype(np.float64)
-    t3 = time.perf_counter()
-    TW = nestquant.integer_tiles(cw, tw, q).astype(np.float64)
-    t4 = time.perf_counter()
-    S = TA @ TW.T
-    _ = S * (ra.astype(np.float64)[:, None] * rw.astype(np.float64)[None, :]) * (base * base / 4)
-    t5 = time.perf_counter()
-    # extrapolate each stage linearly to the full workload
-    t_full = ((t1 - t0) * M / ma + (t3 - t2) * M / ma + (t4 - t3) * N / nw
-              + (t5 - t4) * (M / ma) * (N / nw))
+    cw, tw, rw = nestquant.quantize_rows(W32, q, k)
+    times = []
+    while len(times) < max_reps and (len(times) < 2 or sum(times) < min_seconds):
+        t0 = time.perf_counter()
+        ca, ta, ra = nestquant.quantize_rows(A32, q, k)
+        TA = nestquant.integer_tiles(ca, ta, q).astype(np.float64)
+        TW = nestquant.integer_tiles(cw, tw, q).astype(np.float64)
+        S = TA @ TW.T
+        _ = S * (ra.astype(np.float64)[:, None] * rw.astype(np.float64)[None, :]) * (base * base / 4)
+        times.append(time.perf_counter() - t0)
+        del TA, TW, S
+    step = float(np.mean(times))
     return {
-        "value": flops_full / t_full / 1e12,
+        "value": flops_full / step / 1e12,
         "unit": "TFLOP/s",
         "cores": int(blas_threads),
         "kind": "oracle",
-        "sample": (f"oracle encode of {ma} of {M} A rows, decode of those and of {nw} of {N} "
-                   f"W rows, exact fp64 product {ma}x{nw}x{K}; each stage timed and scaled "
-                   f"linearly to {M}x{N}x{K} (W coding excluded, as on the GPU); numpy "
-                   f"elementwise on 1 thread, BLAS on {blas_threads}; measured "
-                   f"{t5 - t0 - (t2 - t1):.1f} s"),
-        "seconds_full_step_extrapolated": t_full,
+        "sample": (f"the whole step of {M}x{N}x{K} (oracle encode of all {M} A rows, decode of "
+                   f"A and of the {N} coded W rows, exact fp64 product), W coding excluded as "
+                   f"on the GPU; {len(times)} repetitions, {sum(times):.1f} s measured; numpy "
+                   f"elementwise on 1 thread, BLAS on {blas_threads}"),
+        "seconds_per_step": step,
     }
 
 
@@ -328,7 +324,7 @@ def main():
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(cfg, q, k, args.cpu_sample_rows, flops)
+        out["cpu_baseline"] = cpu_baseline(cfg, q, k, flops)
     print(json.dumps(out))
 
 
