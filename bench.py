@@ -23,6 +23,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0     # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+INT8_PEAK_TOPS = 5000.0    # MI355X dense int8 MFMA
 
 METRIC = "nq_matmul TFLOP/s + nq_encode GB/s (q=14,k=4) at Llama-3-8B prefill shapes"
 
@@ -262,6 +263,27 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
+    # the exact int8 contraction (a variant of the product, not part of the step)
+    i8 = None
+    if k * q <= 63:
+        ev8 = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+        ac = nq.encode(As[0], q=q, k=k, out=(codes, beta, scales))
+        for i in range(args.warmup):
+            nq.matmul(ac, wc, out=C, workspace=ws, int8=True)
+        for i in range(args.steps):
+            ev8[i][0].record()
+            nq.matmul(ac, wc, out=C, workspace=ws, stages=nq.STAGE_DECODE, int8=True)
+            ev8[i][1].record()
+            nq.matmul(ac, wc, out=C, workspace=ws, stages=nq.STAGE_CONTRACT, int8=True)
+            ev8[i][2].record()
+        torch.cuda.synchronize()
+        d8 = float(np.mean([e[0].elapsed_time(e[1]) for e in ev8]))
+        c8 = float(np.mean([e[1].elapsed_time(e[2]) for e in ev8]))
+        i8 = {"decode_stage_ms": d8, "contract_stage_ms": c8,
+              "contract_TOPs": flops / (c8 * 1e-3) / 1e12,
+              "contract_int8_frac": flops / (c8 * 1e-3) / 1e12 / INT8_PEAK_TOPS,
+              "matmul_TOPs": flops / ((d8 + c8) * 1e-3) / 1e12}
+
     enc_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
     dec_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
     con_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
@@ -319,6 +341,7 @@ def main():
             "nq_matmul_bytes": mm_bytes,
             "a_rotation_buffers": nbuf,
             "rate_bits_per_entry": float(np.log2(q) + np.log2(k) / 8),
+            "nq_matmul_int8_variant": i8,
         },
         "roofline": roofline,
         "cpu_baseline": None,

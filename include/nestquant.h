@@ -112,15 +112,24 @@ nq_status nq_matmul_ex(const nq_params* pa, const uint32_t* a_codes, const uint3
                        int64_t N, int64_t K, float* c, int64_t ldc, void* workspace,
                        int64_t workspace_bytes, void* hip_stream);
 
-/* The two stages of nq_matmul_ex, for callers that time or schedule them separately.
- * stages is a bit mask: NQ_STAGE_DECODE decodes the operands into the workspace (every
- * block of A and, for M > 64, of W, as bf16 t*X2), NQ_STAGE_CONTRACT computes C from the
- * workspace (for M <= 64 it also decodes W, straight into matrix-core operands).  A DECODE
- * call followed by a CONTRACT call with the same arguments on the same stream is exactly
- * nq_matmul_ex (stages = NQ_STAGE_DECODE | NQ_STAGE_CONTRACT); the workspace must not be
- * changed in between.  Arguments are validated as in nq_matmul_ex; any other bit, or an
- * empty mask, is NQ_ERR_INVALID_ARG. */
-enum { NQ_STAGE_DECODE = 1, NQ_STAGE_CONTRACT = 2 };
+/* The two stages of nq_matmul_ex, for callers that time or schedule them separately, and
+ * the exact int8 contraction.  stages is a bit mask:
+ *   NQ_STAGE_DECODE    decodes the operands into the workspace (every block of A and, for
+ *                      M > 64, of W, as t*X2);
+ *   NQ_STAGE_CONTRACT  computes C from the workspace (for M <= 64 it also decodes W, straight
+ *                      into matrix-core operands);
+ *   NQ_CONTRACT_INT8   stores t*X2 as int8 and contracts on int8 matrix cores with int32
+ *                      accumulation instead of bf16 / fp32.  Every inner product
+ *                      sum <t_A X2_A, t_W X2_W> (Alg. 4 without its scale) is then exact, and
+ *                      C = fp32(sum) * r_A * r_W * base_A * base_W / 4.  It requires
+ *                      k * q <= 63 for both operands (|t X2| <= 2 k q must fit int8), else
+ *                      NQ_ERR_UNSUPPORTED.  Both stages of one product must agree on it.
+ * A DECODE call followed by a CONTRACT call with the same arguments on the same stream is
+ * exactly the call with both bits; DECODE | CONTRACT is nq_matmul_ex.  The workspace must
+ * not change in between.  Arguments are validated as in nq_matmul_ex; any other bit, or no
+ * stage bit, is NQ_ERR_INVALID_ARG.  The workspace size is nq_matmul_workspace_size either
+ * way. */
+enum { NQ_STAGE_DECODE = 1, NQ_STAGE_CONTRACT = 2, NQ_CONTRACT_INT8 = 4 };
 nq_status nq_matmul_stages(int32_t stages, const nq_params* pa, const uint32_t* a_codes,
                            const uint32_t* a_beta, const float* a_scales, int64_t M,
                            const nq_params* pw, const uint32_t* w_codes, const uint32_t* w_beta,

@@ -7,6 +7,7 @@ library has not been built.
 """
 
 from .binding import (  # noqa: F401
+    CONTRACT_INT8,
     STAGE_CONTRACT,
     STAGE_DECODE,
     Coded,

@@ -155,14 +155,17 @@ def decode(coded, out_dtype=None, stream=None, out=None):
 
 STAGE_DECODE = 1
 STAGE_CONTRACT = 2
+CONTRACT_INT8 = 4
 
 
-def matmul(a, w, stream=None, out=None, workspace=None, stages=STAGE_DECODE | STAGE_CONTRACT):
+def matmul(a, w, stream=None, out=None, workspace=None, stages=STAGE_DECODE | STAGE_CONTRACT,
+           int8=False):
     """nq_matmul: C = A_hat W_hat^T (fp32, M x N) from two coded operands.
 
     The decode-once workspace is taken from torch's allocator unless given.  ``stages``
     selects part of the call (nq_matmul_stages): STAGE_DECODE fills the workspace,
-    STAGE_CONTRACT computes C from it; both (the default) is nq_matmul_ex."""
+    STAGE_CONTRACT computes C from it; both (the default) is the whole product.  ``int8``
+    contracts exact int8 tiles on int8 matrix cores (needs k * q <= 63)."""
     import torch
     if a.cols != w.cols:
         raise ValueError("K mismatch")
@@ -173,8 +176,9 @@ def matmul(a, w, stream=None, out=None, workspace=None, stages=STAGE_DECODE | ST
     need = lib.nq_matmul_workspace_size(a.rows, w.rows, a.cols)
     if need < 0:
         raise ValueError("invalid matmul shape")
+    whole = stages == STAGE_DECODE | STAGE_CONTRACT
     if need > 0 and (workspace is None or workspace.numel() * workspace.element_size() < need):
-        if stages != STAGE_DECODE | STAGE_CONTRACT:
+        if not whole:
             raise ValueError("a staged matmul needs a workspace of matmul_workspace_size bytes")
         workspace = torch.empty(need, dtype=torch.uint8, device=a.codes.device)
     ws_ptr = workspace.data_ptr() if need > 0 else 0
@@ -184,10 +188,10 @@ def matmul(a, w, stream=None, out=None, workspace=None, stages=STAGE_DECODE | ST
             ctypes.c_void_p(w.beta.data_ptr()), ctypes.c_void_p(w.scales.data_ptr()), w.rows,
             a.cols, ctypes.c_void_p(out.data_ptr()), out.stride(0), ctypes.c_void_p(ws_ptr),
             need, _stream(stream))
-    if stages == STAGE_DECODE | STAGE_CONTRACT:
+    if whole and not int8:
         _check(lib.nq_matmul_ex(*args))
     else:
-        _check(lib.nq_matmul_stages(stages, *args))
+        _check(lib.nq_matmul_stages(stages | (CONTRACT_INT8 if int8 else 0), *args))
     return out
 
 

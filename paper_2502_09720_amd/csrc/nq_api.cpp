@@ -168,11 +168,19 @@ static nq_status matmul_stages(int32_t stages, const nq_params* pa, const uint32
                                const uint32_t* w_beta, const float* w_scales, int64_t N,
                                int64_t K, float* c, int64_t ldc, void* workspace,
                                int64_t workspace_bytes, void* hip_stream, const char* who) {
-  if (stages < 1 || stages > 3)
-    return fail(NQ_ERR_INVALID_ARG, "%s: stages must be a non-empty mask of NQ_STAGE_*", who);
+  if ((stages & ~(NQ_STAGE_DECODE | NQ_STAGE_CONTRACT | NQ_CONTRACT_INT8)) != 0 ||
+      (stages & (NQ_STAGE_DECODE | NQ_STAGE_CONTRACT)) == 0)
+    return fail(NQ_ERR_INVALID_ARG,
+                "%s: stages must hold NQ_STAGE_DECODE and/or NQ_STAGE_CONTRACT, plus optionally "
+                "NQ_CONTRACT_INT8", who);
   if (nq_status s = check_matmul(pa, a_codes, a_beta, a_scales, M, pw, w_codes, w_beta,
                                  w_scales, N, K, c, ldc, who))
     return s;
+  const bool i8 = (stages & NQ_CONTRACT_INT8) != 0;
+  if (i8 && (pa->k * pa->q > 63 || pw->k * pw->q > 63))
+    return fail(NQ_ERR_UNSUPPORTED,
+                "%s: the int8 contraction needs k * q <= 63 for both operands (|t X2| <= 2 k q "
+                "must fit int8)", who);
   if (M == 0 || N == 0) return ok();
   const int64_t need = nq_matmul_workspace_size(M, N, K);
   if (workspace_bytes < need || (need > 0 && !workspace))
@@ -184,14 +192,14 @@ static nq_status matmul_stages(int32_t stages, const nq_params* pa, const uint32
   const float scale = (float)(pa->base * pw->base * 0.25);
   hipStream_t st = (hipStream_t)hip_stream;
   if (M <= nq::kFusedMaxM)
-    return hip_status(nq::launch_matmul_skinny(stages, A, W, K, c, ldc, scale, workspace, st),
-                      who);
+    return hip_status(
+        nq::launch_matmul_skinny(stages, i8, A, W, K, c, ldc, scale, workspace, st), who);
   static std::once_flag attr_once;
   static hipError_t attr_err = hipSuccess;
   std::call_once(attr_once, [] { attr_err = nq::gemm_set_attributes(); });
   if (attr_err != hipSuccess) return hip_status(attr_err, who);
   return hip_status(
-      nq::launch_matmul_decode_once(stages, A, W, K, c, ldc, scale, workspace, st), who);
+      nq::launch_matmul_decode_once(stages, i8, A, W, K, c, ldc, scale, workspace, st), who);
 }
 
 nq_status nq_matmul_ex(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,

@@ -440,6 +440,22 @@ __device__ __forceinline__ u32x4 decode_tile_bf16(uint32_t w, int t, int q, uint
   return u32x4{o[0], o[1], o[2], o[3]};
 }
 
+// t * X2 of one block as eight int8 (exact when 2 k q <= 127: |X2| <= 2q, t <= k), the
+// coordinates in byte order.  The 16-bit products keep their low byte, which is the
+// two's-complement int8 of a value in [-127, 127].
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ u32x2 decode_tile_i8(uint32_t w, int t, int q, uint32_t m2q) {
+  uint32_t X2p[4];
+  decode_word_pk(w, q, m2q, X2p);
+  const u16x2 tt = {(unsigned short)t, (unsigned short)t};
+  uint32_t p[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) p[i] = bits32(as_u16x2(X2p[i]) * tt);
+  // bytes 0 and 2 of two words: coordinates 4 i .. 4 i + 3
+  return u32x2{__builtin_amdgcn_perm(p[1], p[0], 0x06040200u),
+               __builtin_amdgcn_perm(p[3], p[2], 0x06040200u)};
+}
+
 // The decoder's residual X - q * 2 Q_E8(X / 2q) for integer X >= 0 (< 2^11), scalar form of
 // decode_word without the generator step.
 __device__ __forceinline__ void residual_from_X(const int (&X)[8], int q, uint32_t m2q,

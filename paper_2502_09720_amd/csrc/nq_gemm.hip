@@ -21,6 +21,8 @@
 // multiplied.  Workgroups are mapped so that the tiles resident on one XCD (workgroup id
 // mod 8) form a compact 4-row band of the tile grid and share their A and W rows in that
 // XCD's L2.
+#include <type_traits>
+
 #include "nq_device.hpp"
 #include "nq_kernels.hpp"
 
@@ -28,9 +30,12 @@ namespace nq {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x16 __attribute__((ext_vector_type(16)));
 
 namespace gemm {
-constexpr int BK = 64;  // bf16 per stage (128 B per row)
+constexpr int BK = 64;     // bf16 per stage: 128 B per row (128 int8 for the int8 variant)
+constexpr int BKB = 128;   // bytes per row per stage
 constexpr int GROUP_M = 4;
 
 // A tile configuration: BM x BN tile, WM x WN waves, NSTAGE LDS buffers.
@@ -40,7 +45,7 @@ struct Cfg {
   static constexpr int NW = WM * WN;
   static constexpr int TM = BM / WM / 32;  // 32x32 MFMA tiles per wave along M
   static constexpr int TN = BN / WN / 32;
-  static constexpr int STAGE_BYTES = (BM + BN) * BK * 2;
+  static constexpr int STAGE_BYTES = (BM + BN) * BKB;
   static constexpr int GROUPS = (BM + BN) / 8;  // 8-row groups per stage
   static constexpr int GROUPS_PER_WAVE = GROUPS / NW;
   static_assert(GROUPS % NW == 0, "row groups must split evenly over the waves");
@@ -53,27 +58,39 @@ using CfgMid = Cfg<256, 128, 4, 2, 3>;
 using CfgBig = Cfg<256, 256, 4, 2, 2>;
 }  // namespace gemm
 
-// t * X2 of every block of a coded operand, as bf16, into ws[rows_p][nb_p blocks] (zero
-// padding), one thread per block (grid_block).
+// t * X2 of every block of a coded operand into ws[rows_p][nb_p blocks] (zero padding), one
+// thread per block (grid_block): 8 bf16 (16 B) per block, or 8 int8 (8 B) for the int8
+// contraction.
+template <bool I8>
 __global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__ codes,
                                                     const uint32_t* __restrict__ beta,
                                                     int64_t rows, int nb, int64_t rows_p,
                                                     int nb_p, int q, uint32_t m2q, int lg,
-                                                    u32x4* __restrict__ ws) {
+                                                    void* __restrict__ ws) {
   const GridPos g = grid_block(nb_p, lg);
   const int64_t row = g.rb + g.lr;
   const int j = g.j;
   if (row >= rows_p || j >= nb_p) return;
-  u32x4 out = {0u, 0u, 0u, 0u};
+  using V = typename std::conditional<I8, u32x2, u32x4>::type;
+  V out = {};
   if (row < rows && j < nb) {
     const int nbw = (nb + 15) >> 4;
     const uint32_t w = __builtin_nontemporal_load(codes + g.rb * nb + (uint32_t)(g.lr * nb + j));
     const uint32_t bw = beta[g.rb * nbw + (uint32_t)(g.lr * nbw + (j >> 4))];
     const int t = (int)((bw >> (2 * (j & 15))) & 3u) + 1;
-    out = decode_tile_bf16(w, t, q, m2q);
+    if constexpr (I8) {
+      out = decode_tile_i8(w, t, q, m2q);
+    } else {
+      out = decode_tile_bf16(w, t, q, m2q);
+    }
   }
-  ws[g.rb * nb_p + (uint32_t)(g.lr * nb_p + j)] = out;
+  reinterpret_cast<V*>(ws)[g.rb * nb_p + (uint32_t)(g.lr * nb_p + j)] = out;
 }
+
+template __global__ void tiles_kernel<false>(const uint32_t*, const uint32_t*, int64_t, int,
+                                             int64_t, int, int, uint32_t, int, void*);
+template __global__ void tiles_kernel<true>(const uint32_t*, const uint32_t*, int64_t, int,
+                                            int64_t, int, int, uint32_t, int, void*);
 
 __device__ __forceinline__ void tile_coords(int bid, int tm, int tn, int& pm, int& pn) {
   constexpr int GROUP_M = gemm::GROUP_M;
@@ -99,15 +116,18 @@ typedef __attribute__((address_space(3))) void lds_void;
 // lanes of a 128-bit read per cycle.
 __device__ __forceinline__ int swz(int r) { return (r ^ ((r >> 3) & 3)) & 7; }
 
-template <class C>
+// kc: row length of both tiles in 16-byte chunks (a multiple of 8).  I8: int8 tiles and
+// v_mfma_i32_32x32x32_i8 (exact int32 sums); else bf16 tiles and v_mfma_f32_32x32x16_bf16.
+// Both consume 16 B per lane per MFMA, so staging, swizzle and fragment reads are the same.
+template <class C, bool I8>
 __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
-    const u32x4* __restrict__ ta, const u32x4* __restrict__ tw, int kp, int tm, int tn,
+    const u32x4* __restrict__ ta, const u32x4* __restrict__ tw, int kc, int tm, int tn,
     const float* __restrict__ ra, const float* __restrict__ rw, int64_t M, int64_t N,
     float* __restrict__ c, int64_t ldc, float scale) {
   constexpr int BM = C::BM, BN = C::BN, WM = C::WM, WN = C::WN, NSTAGE = C::NSTAGE;
   constexpr int NW = C::NW, TM = C::TM, TN = C::TN, STAGE_BYTES = C::STAGE_BYTES;
   constexpr int GROUPS_PER_WAVE = C::GROUPS_PER_WAVE;
-  constexpr int BK = gemm::BK;
+  constexpr int CH = gemm::BKB / 16;  // 16-byte chunks per row per stage
   extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
 
   int pm, pn;
@@ -115,7 +135,6 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
   const int tid = threadIdx.x;
   const int wave = tid >> 6, lane = tid & 63;
   const int wm = wave / WN, wn = wave % WN;
-  const int kc = kp >> 3;  // 16-byte chunks per row
 
   // This lane's source for each of the wave's row groups: row (lane >> 3) of the group,
   // stored at physical chunk lane & 7, i.e. logical chunk (lane & 7) ^ swz(row).
@@ -138,17 +157,16 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
     unsigned char* base = lds + (ks % NSTAGE) * STAGE_BYTES;
 #pragma unroll
     for (int i = 0; i < GROUPS_PER_WAVE; ++i)
-      __builtin_amdgcn_global_load_lds((const void*)(src[i] + ks * (BK / 8)),
+      __builtin_amdgcn_global_load_lds((const void*)(src[i] + ks * CH),
                                        (lds_void*)(base + dst[i]), 16, 0, 0);
   };
 
-  f32x16 acc[TM][TN];
+  using Acc = typename std::conditional<I8, i32x16, f32x16>::type;
+  Acc acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+    for (int j = 0; j < TN; ++j) acc[i][j] = Acc{};
 
   // fragment reads: row (lane & 31) of a 32-row tile, logical chunk 2 kk + (lane >> 5).  The
   // swizzle depends only on the row modulo 32, and every 32-row tile starts at a multiple
@@ -156,11 +174,11 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
   const int frow = lane & 31;
   const int abase = (wm * (BM / WM) + frow) * 128;
   const int wbase = BM * 128 + (wn * (BN / WN) + frow) * 128;
-  int coff[BK / 16];
+  int coff[CH / 2];
 #pragma unroll
-  for (int kk = 0; kk < BK / 16; ++kk) coff[kk] = ((2 * kk + (lane >> 5)) ^ swz(frow)) * 16;
+  for (int kk = 0; kk < CH / 2; ++kk) coff[kk] = ((2 * kk + (lane >> 5)) ^ swz(frow)) * 16;
 
-  const int nks = kp / BK;
+  const int nks = kc / CH;
 #pragma unroll
   for (int s = 0; s < NSTAGE - 1; ++s)
     if (s < nks) load_stage(s);
@@ -206,14 +224,14 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
     // one by one with the LDS reads of the next step and with this wave's share of the
     // next stage's global loads, so that neither the LDS nor the texture path receives
     // its requests in one burst that would hold up the MFMA issue.
-    bf16x8 af[2][TM], bfr[2][TN];
+    u32x4 af[2][TM], bfr[2][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
-      af[0][i] = *reinterpret_cast<const bf16x8*>(sb + abase + i * 32 * 128 + coff[0]);
+      af[0][i] = *reinterpret_cast<const u32x4*>(sb + abase + i * 32 * 128 + coff[0]);
 #pragma unroll
     for (int j = 0; j < TN; ++j)
-      bfr[0][j] = *reinterpret_cast<const bf16x8*>(sb + wbase + j * 32 * 128 + coff[0]);
-    constexpr int KSTEPS = BK / 16;
+      bfr[0][j] = *reinterpret_cast<const u32x4*>(sb + wbase + j * 32 * 128 + coff[0]);
+    constexpr int KSTEPS = CH / 2;  // MFMAs per (i, j) per stage: 32 B of K each
     constexpr int LOADS_PER_STEP = (GROUPS_PER_WAVE + KSTEPS - 1) / KSTEPS;
 #pragma unroll
     for (int kk = 0; kk < KSTEPS; ++kk) {
@@ -221,17 +239,25 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
 #pragma unroll
       for (int m = 0; m < TM * TN; ++m) {
         const int i = m / TN, j = m % TN;
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[cur][i], bfr[cur][j], acc[i][j], 0, 0, 0);
+        if constexpr (I8) {
+          acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(
+              __builtin_bit_cast(i32x4, af[cur][i]), __builtin_bit_cast(i32x4, bfr[cur][j]),
+              acc[i][j], 0, 0, 0);
+        } else {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8, af[cur][i]), __builtin_bit_cast(bf16x8, bfr[cur][j]),
+              acc[i][j], 0, 0, 0);
+        }
         if (kk + 1 < KSTEPS) {
           if (m < TM) {
-            af[cur ^ 1][m] = *reinterpret_cast<const bf16x8*>(sb + abase + m * 32 * 128 + coff[kk + 1]);
+            af[cur ^ 1][m] = *reinterpret_cast<const u32x4*>(sb + abase + m * 32 * 128 + coff[kk + 1]);
           } else if (m < TM + TN) {
-            bfr[cur ^ 1][m - TM] = *reinterpret_cast<const bf16x8*>(sb + wbase + (m - TM) * 32 * 128 + coff[kk + 1]);
+            bfr[cur ^ 1][m - TM] = *reinterpret_cast<const u32x4*>(sb + wbase + (m - TM) * 32 * 128 + coff[kk + 1]);
           }
         }
         const int g = kk * LOADS_PER_STEP + m;
         if (prefetch && m < LOADS_PER_STEP && g < GROUPS_PER_WAVE)
-          __builtin_amdgcn_global_load_lds((const void*)(src[g] + (ks + NSTAGE - 1) * (BK / 8)),
+          __builtin_amdgcn_global_load_lds((const void*)(src[g] + (ks + NSTAGE - 1) * CH),
                                            (lds_void*)(nb + dst[g]), 16, 0, 0);
         __builtin_amdgcn_sched_barrier(0);
       }
@@ -240,14 +266,14 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
       for (int m = TM * TN; m < TM + TN || m < LOADS_PER_STEP; ++m) {
         if (kk + 1 < KSTEPS) {
           if (m < TM) {
-            af[cur ^ 1][m] = *reinterpret_cast<const bf16x8*>(sb + abase + m * 32 * 128 + coff[kk + 1]);
+            af[cur ^ 1][m] = *reinterpret_cast<const u32x4*>(sb + abase + m * 32 * 128 + coff[kk + 1]);
           } else if (m < TM + TN) {
-            bfr[cur ^ 1][m - TM] = *reinterpret_cast<const bf16x8*>(sb + wbase + (m - TM) * 32 * 128 + coff[kk + 1]);
+            bfr[cur ^ 1][m - TM] = *reinterpret_cast<const u32x4*>(sb + wbase + (m - TM) * 32 * 128 + coff[kk + 1]);
           }
         }
         const int g = kk * LOADS_PER_STEP + m;
         if (prefetch && m < LOADS_PER_STEP && g < GROUPS_PER_WAVE)
-          __builtin_amdgcn_global_load_lds((const void*)(src[g] + (ks + NSTAGE - 1) * (BK / 8)),
+          __builtin_amdgcn_global_load_lds((const void*)(src[g] + (ks + NSTAGE - 1) * CH),
                                            (lds_void*)(nb + dst[g]), 16, 0, 0);
       }
     }
@@ -264,11 +290,12 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
       for (int e = 0; e < 16; ++e) {
         const int r = i * 32 + 8 * (e >> 2) + (e & 3);
         if (whole || (m0 + r < M && n0 + j * 32 < N))
-          cp[r * ldc + j * 32] = acc[i][j][e] * (rs[i][e] * cs[j]);
+          cp[r * ldc + j * 32] = (float)acc[i][j][e] * (rs[i][e] * cs[j]);
       }
 }
 
-// Both tile configurations pad M to 256; N is padded to 256 (a multiple of both BN).
+// Both tile configurations pad M to 256; N is padded to 256 (a multiple of both BN).  Rows
+// are padded to 128 B: 64 bf16, or 128 int8 (never more bytes than the bf16 tiles).
 size_t decode_once_workspace(int64_t M, int64_t N, int64_t K) {
   using namespace gemm;
   const int64_t mp = (M + 255) / 256 * 256;
@@ -277,56 +304,68 @@ size_t decode_once_workspace(int64_t M, int64_t N, int64_t K) {
   return (size_t)((mp + np) * kp * 2);
 }
 
-template <class C>
-static void launch_gemm(const u32x4* wa, const u32x4* ww, int kp, int64_t mp, int64_t np,
+template <class C, bool I8>
+static void launch_gemm(const u32x4* wa, const u32x4* ww, int kc, int64_t mp, int64_t np,
                         const MatmulOperand& A, const MatmulOperand& W, float* c, int64_t ldc,
                         float scale, hipStream_t st) {
   const int tm = (int)(mp / C::BM), tn = (int)(np / C::BN);
-  hipLaunchKernelGGL(gemm_kernel<C>, dim3((unsigned)(tm * tn)), dim3(C::NW * 64),
-                     (size_t)C::NSTAGE * C::STAGE_BYTES, st, wa, ww, kp, tm, tn, A.scales,
+  hipLaunchKernelGGL((gemm_kernel<C, I8>), dim3((unsigned)(tm * tn)), dim3(C::NW * 64),
+                     (size_t)C::NSTAGE * C::STAGE_BYTES, st, wa, ww, kc, tm, tn, A.scales,
                      W.scales, A.rows, W.rows, c, ldc, scale);
 }
 
-hipError_t launch_matmul_decode_once(int stages, const MatmulOperand& A, const MatmulOperand& W,
-                                     int64_t K, float* c, int64_t ldc, float scale, void* ws,
-                                     hipStream_t st) {
+template <bool I8>
+static hipError_t decode_once(int stages, const MatmulOperand& A, const MatmulOperand& W,
+                              int64_t K, float* c, int64_t ldc, float scale, void* ws,
+                              hipStream_t st) {
   using namespace gemm;
   const int nb = (int)(K / 8);
   const int64_t mp = (A.rows + 255) / 256 * 256;
   const int64_t np = (W.rows + 255) / 256 * 256;
-  const int kp = (int)((K + BK - 1) / BK * BK);
-  const int nbp = kp / 8;
+  constexpr int EB = I8 ? 1 : 2;                       // bytes per element
+  const int64_t kp = (K * EB + BKB - 1) / BKB * BKB / EB;
+  const int nbp = (int)(kp / 8);
+  const int kc = (int)(kp * EB / 16);
   u32x4* wa = reinterpret_cast<u32x4*>(ws);
-  u32x4* ww = wa + mp * nbp;
+  u32x4* ww = wa + mp * kc;
   if (stages & 1) {
     int lg;
     int64_t wgs;
     grid_shape(mp, nbp, lg, wgs);
-    hipLaunchKernelGGL(tiles_kernel, dim3((unsigned)wgs), dim3(256), 0, st, A.codes, A.beta,
-                       A.rows, nb, mp, nbp, A.q, A.m2q, lg, wa);
+    hipLaunchKernelGGL(tiles_kernel<I8>, dim3((unsigned)wgs), dim3(256), 0, st, A.codes,
+                       A.beta, A.rows, nb, mp, nbp, A.q, A.m2q, lg, (void*)wa);
     grid_shape(np, nbp, lg, wgs);
-    hipLaunchKernelGGL(tiles_kernel, dim3((unsigned)wgs), dim3(256), 0, st, W.codes, W.beta,
-                       W.rows, nb, np, nbp, W.q, W.m2q, lg, ww);
+    hipLaunchKernelGGL(tiles_kernel<I8>, dim3((unsigned)wgs), dim3(256), 0, st, W.codes,
+                       W.beta, W.rows, nb, np, nbp, W.q, W.m2q, lg, (void*)ww);
   }
   if (!(stages & 2)) return hipGetLastError();
   // 256 x 256 tiles once they give every CU a tile, else 256 x 128
   if ((mp / 256) * (np / 256) >= 256) {
-    launch_gemm<CfgBig>(wa, ww, kp, mp, np, A, W, c, ldc, scale, st);
+    launch_gemm<CfgBig, I8>(wa, ww, kc, mp, np, A, W, c, ldc, scale, st);
   } else {
-    launch_gemm<CfgMid>(wa, ww, kp, mp, np, A, W, c, ldc, scale, st);
+    launch_gemm<CfgMid, I8>(wa, ww, kc, mp, np, A, W, c, ldc, scale, st);
   }
   return hipGetLastError();
 }
 
+hipError_t launch_matmul_decode_once(int stages, bool i8, const MatmulOperand& A,
+                                     const MatmulOperand& W, int64_t K, float* c, int64_t ldc,
+                                     float scale, void* ws, hipStream_t st) {
+  return i8 ? decode_once<true>(stages, A, W, K, c, ldc, scale, ws, st)
+            : decode_once<false>(stages, A, W, K, c, ldc, scale, ws, st);
+}
+
 hipError_t gemm_set_attributes() {
   using namespace gemm;
-  hipError_t e = hipFuncSetAttribute((const void*)gemm_kernel<CfgMid>,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize,
-                                     CfgMid::NSTAGE * CfgMid::STAGE_BYTES);
-  if (e != hipSuccess) return e;
-  return hipFuncSetAttribute((const void*)gemm_kernel<CfgBig>,
-                             hipFuncAttributeMaxDynamicSharedMemorySize,
-                             CfgBig::NSTAGE * CfgBig::STAGE_BYTES);
+  const void* k[4] = {(const void*)gemm_kernel<CfgMid, false>, (const void*)gemm_kernel<CfgMid, true>,
+                      (const void*)gemm_kernel<CfgBig, false>, (const void*)gemm_kernel<CfgBig, true>};
+  const int bytes[4] = {CfgMid::NSTAGE * CfgMid::STAGE_BYTES, CfgMid::NSTAGE * CfgMid::STAGE_BYTES,
+                        CfgBig::NSTAGE * CfgBig::STAGE_BYTES, CfgBig::NSTAGE * CfgBig::STAGE_BYTES};
+  for (int i = 0; i < 4; ++i) {
+    const hipError_t e = hipFuncSetAttribute(k[i], hipFuncAttributeMaxDynamicSharedMemorySize, bytes[i]);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace nq

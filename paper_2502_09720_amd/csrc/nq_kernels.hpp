@@ -38,17 +38,19 @@ hipError_t launch_decode(const uint32_t* codes, const uint32_t* beta, const floa
                          int64_t rows, int cols, void* out, int out_dtype, int64_t ld_out,
                          const DecodeArgs& a, hipStream_t st);
 
-// Small M (skinny): decode A once into a bf16 tile, then decode W straight into MFMA operands.
+// Small M (skinny): decode A once into a tile, then decode W straight into MFMA operands.
+// stages: bit 0 decodes into the workspace, bit 1 contracts (see nq_matmul_stages); i8:
+// int8 tiles and int8 matrix cores (exact int32 sums) instead of bf16.
 size_t skinny_workspace(int64_t M, int64_t K);
-// stages: bit 0 decodes into the workspace, bit 1 contracts (see nq_matmul_stages)
-hipError_t launch_matmul_skinny(int stages, const MatmulOperand& A, const MatmulOperand& W, int64_t K,
-                                float* c, int64_t ldc, float scale, void* ws, hipStream_t st);
+hipError_t launch_matmul_skinny(int stages, bool i8, const MatmulOperand& A,
+                                const MatmulOperand& W, int64_t K, float* c, int64_t ldc,
+                                float scale, void* ws, hipStream_t st);
 
 // Decode-once path (large M): workspace bytes, launch (tiles + GEMM), one-time attributes.
 size_t decode_once_workspace(int64_t M, int64_t N, int64_t K);
-hipError_t launch_matmul_decode_once(int stages, const MatmulOperand& A, const MatmulOperand& W, int64_t K,
-                                     float* c, int64_t ldc, float scale, void* ws,
-                                     hipStream_t st);
+hipError_t launch_matmul_decode_once(int stages, bool i8, const MatmulOperand& A,
+                                     const MatmulOperand& W, int64_t K, float* c, int64_t ldc,
+                                     float scale, void* ws, hipStream_t st);
 hipError_t gemm_set_attributes();
 
 // M at or below this uses the skinny kernel; above it, decode-once.

@@ -125,7 +125,7 @@ def test_matmul_ex_rejects_small_workspace(lib):
     assert st == 1
 
 
-@pytest.mark.parametrize("stages", [0, 4, 7, -1])
+@pytest.mark.parametrize("stages", [0, 4, 8, 11, -1])
 def test_matmul_stages_rejects_bad_mask(lib, stages):
     p = _p()
     need = lib.nq_matmul_workspace_size(300, 200, 64)
@@ -147,6 +147,20 @@ def test_matmul_stages_validates_like_ex(lib):
                                   ctypes.byref(p), FAKE, FAKE, FAKE, 200, 64, FAKE, 100, FAKE,
                                   need, S)
         assert st == 1
+
+
+@pytest.mark.parametrize("q,k,ok", [(14, 4, True), (15, 4, True), (16, 4, False),
+                                    (16, 3, True), (8, 4, True), (12, 4, True)])
+def test_matmul_int8_needs_small_kq(lib, q, k, ok):
+    """k * q <= 63 keeps |t X2| <= 2 k q within int8; larger products are refused.  M = 0, so
+    an accepted call returns before any launch."""
+    good, test = _p(), _p(q=q, k=k)
+    for pa, pw in ((good, test), (test, good)):
+        st = lib.nq_matmul_stages(7, ctypes.byref(pa), FAKE, FAKE, FAKE, 0, ctypes.byref(pw),
+                                  FAKE, FAKE, FAKE, 200, 64, FAKE, 200, FAKE, 0, S)
+        assert st == (0 if ok else 2)
+        if not ok:
+            assert b"int8" in lib.nq_last_error()
 
 
 def test_matmul_empty_is_noop(lib):

@@ -307,6 +307,69 @@ def test_matmul_stages_compose_to_ex(nq, M, N, K):
     assert np.linalg.norm(out.cpu().numpy() - C) / np.linalg.norm(C) < 1e-6
 
 
+INT8_CASES = [c for c in MATMUL_CASES if c[6] * max(c[4], c[5]) <= 63] + [
+    (10, 300, 520, 1160, 14, 14, 4),
+    (11, 513, 260, 4096, 15, 15, 4),
+    (12, 64, 700, 1032, 15, 14, 4),
+]
+
+
+@pytest.mark.parametrize("case", INT8_CASES, ids=lambda c: f"{c[1]}x{c[2]}x{c[3]}-q{c[4]}/{c[5]}k{c[6]}")
+def test_matmul_int8_parity(nq, case):
+    """Exact int8 contraction: every inner sum is an exact integer, so each output is within
+    a few fp32 roundings of the oracle's value relative to that value itself, even where the
+    sum cancels."""
+    torch = __import__("torch")
+    seed, M, N, K, qa, qw, k = case
+    _, A32 = workloads.random_rows(seed, M, K, dtype="bf16", dist="t4")
+    _, W32 = workloads.random_rows(seed + 1000, N, K, dtype="bf16", scale=0.02)
+    C, (ac, ab, ar, ba), (wc, wb, wr, bw) = _oracle_product(A32, W32, qa, qw, k)
+    a = upload_coded(ac, ab, ar, M, K, qa, k, ba)
+    w = upload_coded(wc, wb, wr, N, K, qw, k, bw)
+    got = nq.matmul(a, w, int8=True)
+    torch.cuda.synchronize()
+    g = got.cpu().numpy().astype(np.float64)
+    rel = np.linalg.norm(g - C) / max(np.linalg.norm(C), 1e-300)
+    assert rel <= 1e-6, f"relative Frobenius error {rel}"
+    bad = np.abs(g - C) > 4e-7 * np.abs(C)
+    if bad.any():
+        i = tuple(np.argwhere(bad)[0])
+        pytest.fail(f"{bad.sum()} outputs off by more than 4e-7 relative; first {i}: "
+                    f"got {g[i]!r} want {C[i]!r}")
+
+
+@pytest.mark.parametrize("M,N,K", [(40, 300, 1032), (300, 200, 264)])
+def test_matmul_int8_tiles_exact(nq, M, N, K):
+    """The int8 decode stage writes t * X2 of every block bit-exactly (the oracle's integer
+    tiles), zero-padded to the tile grid."""
+    torch = __import__("torch")
+    _, A32 = workloads.random_rows(74, M, K, dtype="bf16", dist="t4")
+    _, W32 = workloads.random_rows(75, N, K, dtype="bf16", scale=0.02)
+    _, (ac, ab, ar, ba), (wc, wb, wr, bw) = _oracle_product(A32, W32, 14, 14, 4)
+    a = upload_coded(ac, ab, ar, M, K, 14, 4, ba)
+    w = upload_coded(wc, wb, wr, N, K, 14, 4, bw)
+    ws = torch.zeros(nq.matmul_workspace_size(M, N, K), dtype=torch.uint8, device="cuda")
+    out = torch.empty(M, N, device="cuda")
+    nq.matmul(a, w, out=out, workspace=ws, stages=nq.STAGE_DECODE, int8=True)
+    torch.cuda.synchronize()
+    buf = ws.cpu().numpy().view(np.int8)
+    kp = -(-K // 128) * 128
+    ca, ta, _ = nestquant.quantize_rows(A32, 14, 4)
+    TA = nestquant.integer_tiles(ca, ta, 14)
+    if M <= 64:
+        tiles = [(0, -(-M // 16) * 16, TA)]
+    else:
+        cw, tw, _ = nestquant.quantize_rows(W32, 14, 4)
+        TW = nestquant.integer_tiles(cw, tw, 14)
+        mp, np_ = -(-M // 256) * 256, -(-N // 256) * 256
+        tiles = [(0, mp, TA), (mp * kp, np_, TW)]
+    for off, rows_p, T in tiles:
+        got = buf[off:off + rows_p * kp].reshape(rows_p, kp)
+        want = np.zeros((rows_p, kp), np.int64)
+        want[:T.shape[0], :T.shape[1]] = T
+        assert np.array_equal(got.astype(np.int64), want), first_mismatch(got.astype(np.int64), want)
+
+
 def test_encode_tiny_entries(nq):
     """Entries many orders of magnitude below the row scale (the lattice input is then a
     tiny number of either sign next to exact zeros), in fp32 and bf16."""
