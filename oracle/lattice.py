@@ -13,6 +13,8 @@ Paper passages followed:
   whether to round up (g), fix the parity of each candidate by moving the single coordinate
   whose move costs least, and keep the candidate with the smaller squared distance.
 * App. E: the generator G of 2E8 (not E8), so that lattice points are integer vectors.
+* App. D (NestQuantM): a decoder-side variant f of the oracle that fixes the parity of both
+  candidates at the first coordinate instead of at argmax / argmin (``nearest_e8_m_rational``).
 
 Points are carried in "2E8 units": a point p of E8 is stored as the integer vector P = 2p.
 
@@ -190,6 +192,42 @@ def nearest_e8_rational(num, den):
     h2[rows[odd2], r[odd2]] += 2 * s[rows[odd2], r[odd2]]
 
     gap = e.sum(axis=1) - 2 * den + odd1 * (den - 2 * e[rows, p]) - odd2 * (2 * e[rows, r])
+    d8 = gap < 0
+    P = np.where(d8[:, None], 2 * x1, h2)
+    return P.reshape(shape)
+
+
+def nearest_e8_m_rational(num, den):
+    """The NestQuantM oracle f (App. D) at num / den, in exact integer arithmetic.
+
+    Alg. 5 with the parity of each candidate fixed at the first coordinate: the D8 candidate
+    (nearest integer vector, halves down) moves its first coordinate to the other
+    neighbouring integer when its sum is odd; the D8+1/2 candidate (d + 1/2) moves its first
+    coordinate to the other neighbouring half-integer, towards the input, when sum d is odd.
+    The closer candidate wins, a tie going to D8+1/2 as in ``nearest_e8``.  Distances are
+    kept multiplied by den.  Returns 2 f(num / den) as int64.
+    """
+    num = np.asarray(num, dtype=np.int64)
+    shape = num.shape
+    num = num.reshape(-1, 8)
+    den = int(den)
+
+    d = num // den
+    f = num - den * d
+    e = np.minimum(f, den - f)             # den * distance to the nearest integer
+    g = 2 * f > den
+    s = np.where(g, 1, -1).astype(np.int64)
+
+    x1 = d + g
+    odd1 = (x1.sum(axis=1) & 1).astype(bool)
+    x1[odd1, 0] -= s[odd1, 0]
+
+    h2 = 2 * d + 1
+    odd2 = (d.sum(axis=1) & 1).astype(bool)
+    h2[odd2, 0] += 2 * s[odd2, 0]
+
+    e0 = e[:, 0]
+    gap = e.sum(axis=1) - 2 * den + odd1 * (den - 2 * e0) - odd2 * (2 * e0)
     d8 = gap < 0
     P = np.where(d8[:, None], 2 * x1, h2)
     return P.reshape(shape)

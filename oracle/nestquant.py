@@ -13,6 +13,8 @@ Paper passages followed:
 * Sec. 3 "Overload avoidance via union of Voronoi codes": the codebook is the union of
   the k scaled Voronoi codes; the rate is log2(q) + log2(k)/8 bits per entry.
 * Sec. 4.2, Alg. 4 (Dot product): sum over blocks of <p1, p2> beta_{B1} beta_{B2}.
+* App. D (NestQuantM): the same encoder with overload judged by, and reconstruction made
+  with, the NestQuantM decoder (``decoder="m"`` throughout).
 
 Readings where the paper is silent:
 
@@ -118,7 +120,7 @@ def multipliers(r32, k, base):
 # Block quantizer: one 8-vector at k scales (Alg. 3 inner loop, App. F strategies)
 # ----------------------------------------------------------------------------------------
 
-def quantize_blocks(xb32, mult32, q, strategy="first", v64=None, betas=None):
+def quantize_blocks(xb32, mult32, q, strategy="first", v64=None, betas=None, decoder="full"):
     """Quantize 8-blocks with the union of k scaled Voronoi codes.
 
     xb32:   (nb, 8) fp32 blocks.
@@ -138,7 +140,7 @@ def quantize_blocks(xb32, mult32, q, strategy="first", v64=None, betas=None):
         y = (xb32 * mult32[:, t:t + 1]).astype(np.float32)   # one fp32 multiply per entry
         P[:, t] = nearest_e8(y.astype(np.float64))
         codes[:, t] = encode_point(P[:, t], q)
-        X2[:, t] = decode(codes[:, t], q)
+        X2[:, t] = decode(codes[:, t], q, decoder)
     over = np.any(X2 != P, axis=2)
 
     if strategy == "first":
@@ -154,7 +156,7 @@ def quantize_blocks(xb32, mult32, q, strategy="first", v64=None, betas=None):
     return codes[rows, t_sel], t_sel + 1, over, P
 
 
-def quantize_rows(x, q, k, base=None, strategy="first"):
+def quantize_rows(x, q, k, base=None, strategy="first", decoder="full"):
     """Alg. 3 on every row of x (rows, n), n a multiple of 8; x must be fp32-representable.
 
     Returns (codes (rows, n/8, 8) int64, t (rows, n/8) int64 in [1, k], r (rows,) fp32).
@@ -180,7 +182,7 @@ def quantize_rows(x, q, k, base=None, strategy="first"):
         if strategy == "opt":
             v64 = (x32[nz].astype(np.float64) / r[nz].astype(np.float64)[:, None]).reshape(-1, 8)
             betas = np.arange(1, k + 1) * np.float64(base)
-        cb, tb, _, _ = quantize_blocks(xb, mb, q, strategy, v64, betas)
+        cb, tb, _, _ = quantize_blocks(xb, mb, q, strategy, v64, betas, decoder)
         codes[nz] = cb.reshape(-1, nb, 8)
         t[nz] = tb.reshape(-1, nb)
     return codes, t, r
@@ -190,14 +192,14 @@ def quantize_rows(x, q, k, base=None, strategy="first"):
 # Decoding, dot product (Alg. 4) and the coded matrix product
 # ----------------------------------------------------------------------------------------
 
-def decoded_points(codes, q):
+def decoded_points(codes, q, decoder="full"):
     """Decoded lattice points in 2E8 units, X2 = 2 p (Alg. 2), same shape as codes."""
-    return decode(codes, q)
+    return decode(codes, q, decoder)
 
 
-def decode_rows(codes, t, r, q, base):
+def decode_rows(codes, t, r, q, base, decoder="full"):
     """Reconstruction x_hat = r * beta_t * p = r * base * t * X2 / 2 in fp64; (rows, n)."""
-    X2 = decode(codes, q).astype(np.float64)                 # (rows, nb, 8)
+    X2 = decode(codes, q, decoder).astype(np.float64)       # (rows, nb, 8)
     scale = (np.asarray(r, np.float32).astype(np.float64)[:, None] * float(base)
              * np.asarray(t, np.float64) / 2.0)
     return (X2 * scale[:, :, None]).reshape(codes.shape[0], -1)
@@ -215,21 +217,22 @@ def dot_coded(c1, t1, r1, q1, base1, c2, t2, r2, q2, base2):
     return float(ans * Fraction(float(r1)) * Fraction(float(r2)))
 
 
-def integer_tiles(codes, t, q):
+def integer_tiles(codes, t, q, decoder="full"):
     """T = t * X2 per entry (integers, |T| <= 2q k), shape (rows, n)."""
-    X2 = decode(codes, q)
+    X2 = decode(codes, q, decoder)
     return (X2 * np.asarray(t)[:, :, None]).reshape(codes.shape[0], -1)
 
 
-def coded_matmul(a_codes, a_t, a_r, qa, base_a, w_codes, w_t, w_r, qw, base_w):
+def coded_matmul(a_codes, a_t, a_r, qa, base_a, w_codes, w_t, w_r, qw, base_w,
+                 decoder_a="full", decoder_w="full"):
     """C = A_hat W_hat^T from the two coded operands (Alg. 4 for every row pair).
 
     C_ij = r_Ai r_Wj base_A base_W / 4 * sum_blocks <t_A X2_A, t_W X2_W>.  The integer
     sums are formed with an fp64 matrix product, which is exact because every partial sum
     is an integer below 2^53.  Returns fp64 (M, N).
     """
-    TA = integer_tiles(a_codes, a_t, qa).astype(np.float64)
-    TW = integer_tiles(w_codes, w_t, qw).astype(np.float64)
+    TA = integer_tiles(a_codes, a_t, qa, decoder_a).astype(np.float64)
+    TW = integer_tiles(w_codes, w_t, qw, decoder_w).astype(np.float64)
     bound = float(np.abs(TA).max(initial=0)) * float(np.abs(TW).max(initial=0)) * TA.shape[1]
     assert bound < 2.0 ** 53, "integer sums would not be exact in fp64"
     S = TA @ TW.T
