@@ -52,16 +52,28 @@ typedef enum {
 
 typedef enum { NQ_F32 = 0, NQ_F16 = 1, NQ_BF16 = 2 } nq_dtype;
 
+/* Decoder of the code (part of its definition: the encoder's overload test uses it).
+ *   NQ_DECODER_FULL  Alg. 2 with the Gosset oracle of Alg. 5 (App. C);
+ *   NQ_DECODER_M     NestQuantM (App. D): the oracle's parity fixes at the first coordinate
+ *                    (no argmin / argmax); the encoder is unchanged except that a point
+ *                    counts as overloaded when this decoder does not reproduce it. */
+typedef enum { NQ_DECODER_FULL = 0, NQ_DECODER_M = 1 } nq_decoder;
+
 /* Quantizer parameters (Sec. 4.2, App. F):
- *   q    nesting ratio, 2 <= q <= 16 (codes are nibbles);
- *   k    number of betas, 1 <= k <= 4 (2-bit beta indices);
- *   base beta_t = t * base for t = 1..k; finite, > 0, and large enough that
- *        sqrt(cols) / base < 2^21 (bounds the lattice input |y| <= sqrt(cols) / base).
- *        The paper's grid "k betas uniform on [0, 10] / q" is base = 10 / (k q). */
+ *   q        nesting ratio, 2 <= q <= 16 (codes are nibbles);
+ *   k        number of betas, 1 <= k <= 4 (2-bit beta indices);
+ *   base     beta_t = t * base for t = 1..k; finite, > 0, and large enough that
+ *            sqrt(cols) / base < 2^21 (bounds the lattice input |y| <= sqrt(cols) / base).
+ *            The paper's grid "k betas uniform on [0, 10] / q" is base = 10 / (k q);
+ *   decoder  an nq_decoder value (0 = Alg. 2 / Alg. 5);
+ *   reserved must be 0.
+ * Codes made with one decoder must be decoded and multiplied with the same one. */
 typedef struct {
   int32_t q;
   int32_t k;
   double base;
+  int32_t decoder;
+  int32_t reserved;
 } nq_params;
 
 /* Alg. 3 + First-beta (App. F) on each row of x.

@@ -8,6 +8,8 @@ library has not been built.
 
 from .binding import (  # noqa: F401
     CONTRACT_INT8,
+    DECODER_FULL,
+    DECODER_M,
     STAGE_CONTRACT,
     STAGE_DECODE,
     Coded,

@@ -22,7 +22,12 @@ class NQError(RuntimeError):
 
 
 class _Params(ctypes.Structure):
-    _fields_ = [("q", ctypes.c_int32), ("k", ctypes.c_int32), ("base", ctypes.c_double)]
+    _fields_ = [("q", ctypes.c_int32), ("k", ctypes.c_int32), ("base", ctypes.c_double),
+                ("decoder", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+DECODER_FULL = 0   # Alg. 2 with the Gosset oracle of Alg. 5
+DECODER_M = 1      # NestQuantM (App. D): parity fixes at the first coordinate
 
 
 def library_path():
@@ -77,8 +82,9 @@ def default_base(q, k):
     return 10.0 / (k * q)
 
 
-def _params(q, k, base):
-    return _Params(int(q), int(k), float(default_base(q, k) if base is None else base))
+def _params(q, k, base, decoder=DECODER_FULL):
+    return _Params(int(q), int(k), float(default_base(q, k) if base is None else base),
+                   int(decoder), 0)
 
 
 def _stream(stream):
@@ -111,10 +117,12 @@ class Coded(NamedTuple):
     q: int
     k: int
     base: float
+    decoder: int = DECODER_FULL
 
 
-def encode(x, q=14, k=4, base=None, stream=None, out=None):
-    """nq_encode on a 2-D cuda tensor (fp32 / fp16 / bf16, unit stride along rows)."""
+def encode(x, q=14, k=4, base=None, stream=None, out=None, decoder=DECODER_FULL):
+    """nq_encode on a 2-D cuda tensor (fp32 / fp16 / bf16, unit stride along rows).
+    ``decoder`` is the decoder the code is defined with (DECODER_FULL or DECODER_M)."""
     import torch
     if x.dim() != 2 or x.stride(1) != 1 or not x.is_cuda:
         raise ValueError("x must be a 2-D cuda tensor with unit column stride")
@@ -129,12 +137,12 @@ def encode(x, q=14, k=4, base=None, stream=None, out=None):
         scales = torch.empty(rows, dtype=torch.float32, device=x.device)
     else:
         codes, beta, scales = out
-    p = _params(q, k, base)
+    p = _params(q, k, base, decoder)
     _check(lib.nq_encode(ctypes.byref(p), ctypes.c_void_p(x.data_ptr()), _dtype_code(x.dtype),
                          rows, cols, x.stride(0), ctypes.c_void_p(codes.data_ptr()),
                          ctypes.c_void_p(beta.data_ptr()), ctypes.c_void_p(scales.data_ptr()),
                          _stream(stream)))
-    return Coded(codes, beta, scales, rows, cols, int(q), int(k), p.base)
+    return Coded(codes, beta, scales, rows, cols, int(q), int(k), p.base, int(decoder))
 
 
 def decode(coded, out_dtype=None, stream=None, out=None):
@@ -143,7 +151,7 @@ def decode(coded, out_dtype=None, stream=None, out=None):
     dt = torch.float32 if out_dtype is None else out_dtype
     if out is None:
         out = torch.empty(coded.rows, coded.cols, dtype=dt, device=coded.codes.device)
-    p = _params(coded.q, coded.k, coded.base)
+    p = _params(coded.q, coded.k, coded.base, coded.decoder)
     lib = library()
     _check(lib.nq_decode(ctypes.byref(p), ctypes.c_void_p(coded.codes.data_ptr()),
                          ctypes.c_void_p(coded.beta.data_ptr()),
@@ -171,7 +179,7 @@ def matmul(a, w, stream=None, out=None, workspace=None, stages=STAGE_DECODE | ST
         raise ValueError("K mismatch")
     if out is None:
         out = torch.empty(a.rows, w.rows, dtype=torch.float32, device=a.codes.device)
-    pa, pw = _params(a.q, a.k, a.base), _params(w.q, w.k, w.base)
+    pa, pw = _params(a.q, a.k, a.base, a.decoder), _params(w.q, w.k, w.base, w.decoder)
     lib = library()
     need = lib.nq_matmul_workspace_size(a.rows, w.rows, a.cols)
     if need < 0:

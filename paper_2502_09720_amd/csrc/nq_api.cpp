@@ -35,6 +35,9 @@ nq_status check_params(const nq_params* p, int64_t cols, const char* who) {
   if (p->k < 1 || p->k > 4) return fail(NQ_ERR_INVALID_ARG, "%s: k=%d outside [1,4]", who, p->k);
   if (!std::isfinite(p->base) || !(p->base > 0.0))
     return fail(NQ_ERR_INVALID_ARG, "%s: base must be finite and > 0", who);
+  if (p->decoder != NQ_DECODER_FULL && p->decoder != NQ_DECODER_M)
+    return fail(NQ_ERR_INVALID_ARG, "%s: decoder=%d is not an nq_decoder", who, p->decoder);
+  if (p->reserved != 0) return fail(NQ_ERR_INVALID_ARG, "%s: reserved must be 0", who);
   if (std::sqrt((double)cols) / p->base >= 2097152.0)
     return fail(NQ_ERR_INVALID_ARG, "%s: base too small for cols=%lld (sqrt(cols)/base >= 2^21)",
                 who, (long long)cols);
@@ -83,7 +86,7 @@ const char* nq_status_string(nq_status s) {
 
 const char* nq_last_error(void) { return g_last_error; }
 
-int32_t nq_version(void) { return 100; }
+int32_t nq_version(void) { return 200; }
 
 nq_status nq_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t rows,
                     int64_t cols, int64_t ld_x, uint32_t* codes, uint32_t* beta_idx,
@@ -107,6 +110,7 @@ nq_status nq_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t
   a.rq = (float)(1.0 / p->q);
   a.m2q = nq::magic_2q(p->q);
   a.mq = nq::magic_q(p->q);
+  a.decoder = p->decoder;
   for (int t = 0; t < 4; ++t) a.beta[t] = (double)(t + 1) * p->base;
   return hip_status(nq::launch_encode(x, (int)x_dtype, rows, (int)cols, ld_x, a, codes, beta_idx,
                                       scales, (hipStream_t)hip_stream),
@@ -132,6 +136,7 @@ nq_status nq_decode(const nq_params* p, const uint32_t* codes, const uint32_t* b
   nq::DecodeArgs a;
   a.q = p->q;
   a.m2q = nq::magic_2q(p->q);
+  a.decoder = p->decoder;
   for (int t = 0; t < 4; ++t) a.half_beta[t] = ((double)(t + 1) * p->base) * 0.5;
   return hip_status(nq::launch_decode(codes, beta_idx, scales, rows, (int)cols, out,
                                       (int)out_dtype, ld_out, a, (hipStream_t)hip_stream),
@@ -187,8 +192,8 @@ static nq_status matmul_stages(int32_t stages, const nq_params* pa, const uint32
     return fail(NQ_ERR_INVALID_ARG, "%s: workspace of %lld bytes needed", who, (long long)need);
   if (need > 0 && !aligned16(workspace))
     return fail(NQ_ERR_INVALID_ARG, "%s: workspace must be 16-byte aligned", who);
-  nq::MatmulOperand A{a_codes, a_beta, a_scales, pa->q, nq::magic_2q(pa->q), M};
-  nq::MatmulOperand W{w_codes, w_beta, w_scales, pw->q, nq::magic_2q(pw->q), N};
+  nq::MatmulOperand A{a_codes, a_beta, a_scales, pa->q, nq::magic_2q(pa->q), M, pa->decoder};
+  nq::MatmulOperand W{w_codes, w_beta, w_scales, pw->q, nq::magic_2q(pw->q), N, pw->decoder};
   const float scale = (float)(pa->base * pw->base * 0.25);
   hipStream_t st = (hipStream_t)hip_stream;
   if (M <= nq::kFusedMaxM)

@@ -1,5 +1,6 @@
-// NestQuant decoder: Alg. 2 (Voronoi decode over 2E8) followed by the inverse scaling
-// x_hat = r * beta_t * p (Alg. 3's normalization undone).
+// NestQuant decoder: Alg. 2 (Voronoi decode over 2E8, with the Gosset oracle of Alg. 5 or
+// NestQuantM's of App. D) followed by the inverse scaling x_hat = r * beta_t * p (Alg. 3's
+// normalization undone).
 //
 // One lane per 8-entry block: read one code word, the row's beta word and scale, decode in
 // exact integer arithmetic, and write the 8 values (32 B fp32 or 16 B fp16/bf16) with one
@@ -9,7 +10,7 @@
 
 namespace nq {
 
-template <int OUT>  // 0 = fp32, 1 = fp16, 2 = bf16
+template <int OUT, bool M>  // OUT: 0 = fp32, 1 = fp16, 2 = bf16; M: NestQuantM decoder
 __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict__ codes,
                                                      const uint32_t* __restrict__ beta,
                                                      const float* __restrict__ scales,
@@ -25,7 +26,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict_
   const int t = (int)((bw >> (2 * (j & 15))) & 3u);
   const double sc = (double)scales[g.rb + g.lr] * a.half_beta[t];
   uint32_t X2p[4];
-  decode_word_pk(w, a.q, a.m2q, X2p);
+  decode_word_pk<M>(w, a.q, a.m2q, X2p);
   if constexpr (OUT == 0) {
     // fp32: each value rounded once from its fp64 product
     float v[8];
@@ -71,20 +72,16 @@ hipError_t launch_decode(const uint32_t* codes, const uint32_t* beta, const floa
   int64_t wgs;
   grid_shape(rows, nb, lg, wgs);
   const unsigned grid = (unsigned)wgs;
+#define NQ_DEC(O, MM)                                                                       \
+  hipLaunchKernelGGL((decode_kernel<O, MM>), dim3(grid), dim3(256), 0, st, codes, beta,     \
+                     scales, rows, nb, lg, out, ld_out, a)
+  const bool m = a.decoder != 0;
   switch (out_dtype) {
-    case 0:
-      hipLaunchKernelGGL(decode_kernel<0>, dim3(grid), dim3(256), 0, st, codes, beta, scales, rows,
-                         nb, lg, out, ld_out, a);
-      break;
-    case 1:
-      hipLaunchKernelGGL(decode_kernel<1>, dim3(grid), dim3(256), 0, st, codes, beta, scales, rows,
-                         nb, lg, out, ld_out, a);
-      break;
-    default:
-      hipLaunchKernelGGL(decode_kernel<2>, dim3(grid), dim3(256), 0, st, codes, beta, scales, rows,
-                         nb, lg, out, ld_out, a);
-      break;
+    case 0: if (m) NQ_DEC(0, true); else NQ_DEC(0, false); break;
+    case 1: if (m) NQ_DEC(1, true); else NQ_DEC(1, false); break;
+    default: if (m) NQ_DEC(2, true); else NQ_DEC(2, false); break;
   }
+#undef NQ_DEC
   return hipGetLastError();
 }
 

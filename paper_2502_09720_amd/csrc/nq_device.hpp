@@ -231,66 +231,13 @@ __device__ __forceinline__ uint32_t encode_codes(const int (&P)[8], int q, float
   return w;
 }
 
-// Alg. 2 on one packed code word: X = G c, then X - q * 2 Q_E8(X / 2q) with Alg. 5 in
-// exact integers (all distances multiplied by 2q; same tie rules as nearest_e8).
-// m2q = ceil(2^16 / (2q)) gives floor(X / 2q) = (X * m2q) >> 16 exactly for 0 <= X < 2^11,
-// and X <= 15 + 60 + 180 = 255 here.  Rounding half down, round(X / 2q) = floor((X + q - 1)
-// / 2q).  Outputs X2_l = X_l - 2q x1_l (D8) or X_l - q (2 d_l + 1) (D8+1/2); with f = X - 2q d
-// these are f - 2q g and f - q.
-__device__ __forceinline__ void decode_word(uint32_t w, int q, uint32_t m2q, int (&X2)[8]) {
-  int c[8];
-#pragma unroll
-  for (int l = 0; l < 8; ++l) c[l] = (int)((w >> (4 * l)) & 15u);
-  int X[8];
-  X[0] = c[0];
-  X[1] = c[0] + 2 * c[2];
-  X[2] = c[0] + 2 * c[4];
-  X[3] = c[0] + 2 * c[6];
-  X[4] = c[0] + 4 * c[1] + 2 * ((c[2] + c[3]) + (c[4] + c[5]) + (c[6] + c[7]));
-  X[5] = c[0] + 2 * c[3];
-  X[6] = c[0] + 2 * c[5];
-  X[7] = c[0] + 2 * c[7];
-  const int den = 2 * q;
-  const uint32_t half_off = (uint32_t)(q - 1) * m2q;
-  int d[8], g[8], f[8], E[8];
-#pragma unroll
-  for (int l = 0; l < 8; ++l) {
-    d[l] = (int)(__umul24((uint32_t)X[l], m2q) >> 16);
-    const int x1 = (int)((__umul24((uint32_t)X[l], m2q) + half_off) >> 16);
-    g[l] = x1 - d[l];
-    f[l] = X[l] - __mul24(den, d[l]);
-    E[l] = min(f[l], den - f[l]);
-  }
-  const int sum_d = ((d[0] + d[1]) + (d[2] + d[3])) + ((d[4] + d[5]) + (d[6] + d[7]));
-  const int sum_g = ((g[0] + g[1]) + (g[2] + g[3])) + ((g[4] + g[5]) + (g[6] + g[7]));
-  const int sE = ((E[0] + E[1]) + (E[2] + E[3])) + ((E[4] + E[5]) + (E[6] + E[7]));
-  // argmax E / argmin E with the lowest index on ties, through keys E*8 + index
-  int kmax = (E[0] << 3) | 7, kmin = E[0] << 3;
-#pragma unroll
-  for (int l = 1; l < 8; ++l) {
-    kmax = max(kmax, (E[l] << 3) | (7 - l));
-    kmin = min(kmin, (E[l] << 3) | l);
-  }
-  const int p = 7 - (kmax & 7), Ep = kmax >> 3;
-  const int r = kmin & 7, Er = kmin >> 3;
-  const int odd1 = (sum_d + sum_g) & 1, odd2 = sum_d & 1;
-  const int gap = sE - 2 * den + (odd1 ? den - 2 * Ep : 0) - (odd2 ? 2 * Er : 0);
-  const bool d8 = gap < 0;
-  // X2 = f - 2q g (D8) or f - q (D8+1/2); the fixed coordinate moves by +-2q:
-  // D8: to f - 2q g + 2q (2 g - 1);  D8+1/2: to f - q - 2q (2 g - 1)
-  const int fix = d8 ? (odd1 ? p : 8) : (odd2 ? r : 8);
-#pragma unroll
-  for (int l = 0; l < 8; ++l) {
-    const int v = d8 ? (g[l] ? f[l] - den : f[l]) : f[l] - q;
-    const bool up = (g[l] != 0) == d8;     // D8 moves by +2q s, D8+1/2 by -2q s, s = 2g - 1
-    X2[l] = (l == fix) ? (up ? v + den : v - den) : v;
-  }
-}
-
 // ---------------------------------------------------------------------------------------
 // Alg. 2 on one code word with two coordinates per 32-bit register (packed 16-bit integer
-// instructions).  Same arithmetic and tie rules as decode_word; output X2 as four packed
-// int16 pairs (coordinates 2i, 2i+1 in the low and high halves of word i).
+// instructions): X = G c, then X - q * 2 Q(X / 2q) in exact integers (all distances times
+// 2q), Q = Alg. 5 with the tie rules of nearest_e8, or (M) the NestQuantM oracle of App. D,
+// whose parity fixes are at the first coordinate (no argmin / argmax).  Output X2 as four
+// packed int16 pairs (coordinates 2i, 2i+1 in the low and high halves of word i).
+// m2q = ceil(2^16 / (2q)) gives floor(X / 2q) = (X * m2q) >> 16 exactly for 0 <= X < 2^11.
 //
 // Shifting X by 2q * v with v in D8 leaves the decode unchanged (Alg. 5 commutes with D8
 // shifts), so only f = X mod 2q per coordinate and the parity pi of sum floor(X / 2q)
@@ -307,6 +254,7 @@ __device__ __forceinline__ i16x2 as_i16x2(uint32_t v) { return __builtin_bit_cas
 __device__ __forceinline__ uint32_t bits32(u16x2 v) { return __builtin_bit_cast(uint32_t, v); }
 __device__ __forceinline__ uint32_t bits32(i16x2 v) { return __builtin_bit_cast(uint32_t, v); }
 
+template <bool M = false>
 __device__ __forceinline__ void decode_word_pk(uint32_t w, int q, uint32_t m2q,
                                                uint32_t (&X2)[4]) {
   const uint32_t E = w & 0x0F0F0F0Fu;         // bytes c0 c2 c4 c6
@@ -362,21 +310,28 @@ __device__ __forceinline__ void decode_word_pk(uint32_t w, int q, uint32_t m2q,
   const uint32_t gb = (neg[0] & 0x80008000u) | ((neg[1] & 0x80008000u) >> 1) |
                       ((neg[2] & 0x80008000u) >> 2) | ((neg[3] & 0x80008000u) >> 3);
   const uint32_t odd1 = (pi + __builtin_popcount(gb)) & 1u;
-  // keys |h| * 8 + index (min: argmin |h|, lowest index) and |h| * 8 + 7 - index (max)
-  const uint32_t kidx_min[4] = {0x00010000u, 0x00030002u, 0x00050004u, 0x00070006u};
-  const uint32_t kidx_max[4] = {0x00060007u, 0x00040005u, 0x00020003u, 0x00000001u};
-  const u16x2 eight = {8, 8};
-  u16x2 kmin2 = as_u16x2(ah[0]) * eight + as_u16x2(kidx_min[0]);
-  u16x2 kmax2 = as_u16x2(ah[0]) * eight + as_u16x2(kidx_max[0]);
+  int p = 0, r = 0, minh, maxh;
+  if constexpr (M) {
+    minh = maxh = (int)(short)(ah[0] & 0xFFFFu);       // both fixes at coordinate 0
+  } else {
+    // keys |h| * 8 + index (min: argmin |h|, lowest index) and |h| * 8 + 7 - index (max)
+    const uint32_t kidx_min[4] = {0x00010000u, 0x00030002u, 0x00050004u, 0x00070006u};
+    const uint32_t kidx_max[4] = {0x00060007u, 0x00040005u, 0x00020003u, 0x00000001u};
+    const u16x2 eight = {8, 8};
+    u16x2 kmin2 = as_u16x2(ah[0]) * eight + as_u16x2(kidx_min[0]);
+    u16x2 kmax2 = as_u16x2(ah[0]) * eight + as_u16x2(kidx_max[0]);
 #pragma unroll
-  for (int i = 1; i < 4; ++i) {
-    kmin2 = __builtin_elementwise_min(kmin2, as_u16x2(ah[i]) * eight + as_u16x2(kidx_min[i]));
-    kmax2 = __builtin_elementwise_max(kmax2, as_u16x2(ah[i]) * eight + as_u16x2(kidx_max[i]));
+    for (int i = 1; i < 4; ++i) {
+      kmin2 = __builtin_elementwise_min(kmin2, as_u16x2(ah[i]) * eight + as_u16x2(kidx_min[i]));
+      kmax2 = __builtin_elementwise_max(kmax2, as_u16x2(ah[i]) * eight + as_u16x2(kidx_max[i]));
+    }
+    const uint32_t kmin = min((uint32_t)kmin2.x, (uint32_t)kmin2.y);
+    const uint32_t kmax = max((uint32_t)kmax2.x, (uint32_t)kmax2.y);
+    p = (int)(kmin & 7u);
+    r = 7 - (int)(kmax & 7u);
+    minh = (int)(kmin >> 3);
+    maxh = (int)(kmax >> 3);
   }
-  const uint32_t kmin = min((uint32_t)kmin2.x, (uint32_t)kmin2.y);
-  const uint32_t kmax = max((uint32_t)kmax2.x, (uint32_t)kmax2.y);
-  const int p = (int)(kmin & 7u), r = 7 - (int)(kmax & 7u);
-  const int minh = (int)(kmin >> 3), maxh = (int)(kmax >> 3);
   const int gap = 4 * q - (int)sum_ah + (odd1 ? 2 * minh : 0) - (pi ? 2 * q - 2 * maxh : 0);
   const bool d8 = gap < 0;
   // residuals: D8 c = f - 2q g, D8+1/2 h
@@ -426,9 +381,10 @@ __device__ __forceinline__ GridPos grid_block(int nb, int lg) {
 
 // t * X2 of one block as eight bf16 (exact: |t X2| <= 4 * 32 = 128 < 2^8): the upper halves
 // of the fp32 values, coordinates 2i and 2i+1 in word i.
+template <bool M = false>
 __device__ __forceinline__ u32x4 decode_tile_bf16(uint32_t w, int t, int q, uint32_t m2q) {
   uint32_t X2p[4];
-  decode_word_pk(w, q, m2q, X2p);
+  decode_word_pk<M>(w, q, m2q, X2p);
   uint32_t o[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -444,9 +400,10 @@ __device__ __forceinline__ u32x4 decode_tile_bf16(uint32_t w, int t, int q, uint
 // coordinates in byte order.  The 16-bit products keep their low byte, which is the
 // two's-complement int8 of a value in [-127, 127].
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+template <bool M = false>
 __device__ __forceinline__ u32x2 decode_tile_i8(uint32_t w, int t, int q, uint32_t m2q) {
   uint32_t X2p[4];
-  decode_word_pk(w, q, m2q, X2p);
+  decode_word_pk<M>(w, q, m2q, X2p);
   const u16x2 tt = {(unsigned short)t, (unsigned short)t};
   uint32_t p[4];
 #pragma unroll
@@ -456,8 +413,10 @@ __device__ __forceinline__ u32x2 decode_tile_i8(uint32_t w, int t, int q, uint32
                __builtin_amdgcn_perm(p[3], p[2], 0x06040200u)};
 }
 
-// The decoder's residual X - q * 2 Q_E8(X / 2q) for integer X >= 0 (< 2^11), scalar form of
-// decode_word without the generator step.
+// The decoder's residual X - q * 2 Q(X / 2q) for integer X >= 0 (< 2^11), Q = Alg. 5 or
+// (M) the NestQuantM oracle: the scalar form of decode_word_pk without the generator step.
+// Rounding half down, round(X / 2q) = floor((X + q - 1) / 2q).
+template <bool M = false>
 __device__ __forceinline__ void residual_from_X(const int (&X)[8], int q, uint32_t m2q,
                                                 int (&X2)[8]) {
   const int den = 2 * q;
@@ -474,14 +433,19 @@ __device__ __forceinline__ void residual_from_X(const int (&X)[8], int q, uint32
   const int sum_d = ((d[0] + d[1]) + (d[2] + d[3])) + ((d[4] + d[5]) + (d[6] + d[7]));
   const int sum_g = ((g[0] + g[1]) + (g[2] + g[3])) + ((g[4] + g[5]) + (g[6] + g[7]));
   const int sE = ((E[0] + E[1]) + (E[2] + E[3])) + ((E[4] + E[5]) + (E[6] + E[7]));
-  int kmax = (E[0] << 3) | 7, kmin = E[0] << 3;
+  int p = 0, r = 0, Ep = E[0], Er = E[0];
+  if constexpr (!M) {
+    int kmax = (E[0] << 3) | 7, kmin = E[0] << 3;
 #pragma unroll
-  for (int l = 1; l < 8; ++l) {
-    kmax = max(kmax, (E[l] << 3) | (7 - l));
-    kmin = min(kmin, (E[l] << 3) | l);
+    for (int l = 1; l < 8; ++l) {
+      kmax = max(kmax, (E[l] << 3) | (7 - l));
+      kmin = min(kmin, (E[l] << 3) | l);
+    }
+    p = 7 - (kmax & 7);
+    Ep = kmax >> 3;
+    r = kmin & 7;
+    Er = kmin >> 3;
   }
-  const int p = 7 - (kmax & 7), Ep = kmax >> 3;
-  const int r = kmin & 7, Er = kmin >> 3;
   const int odd1 = (sum_d + sum_g) & 1, odd2 = sum_d & 1;
   const int gap = sE - 2 * den + (odd1 ? den - 2 * Ep : 0) - (odd2 ? 2 * Er : 0);
   const bool d8 = gap < 0;
@@ -497,11 +461,13 @@ __device__ __forceinline__ void residual_from_X(const int (&X)[8], int q, uint32
 // First-beta overload test of one candidate point (Sec. 4.1): overloaded iff
 // decode(encode(P)) != P.  The root bound settles every point off the cell boundary.  On the
 // boundary (M(P) = 2q, where Alg. 5's tie rules decide) the literal test is evaluated
-// without building the code word: the decoder sees X = G (G^-1 P mod q) = P + 2q v with v in
-// E8, and the residual of Alg. 2 is unchanged by D8 shifts of X / 2q, so it equals the
-// residual of P (v in D8) or of P + q (1,...,1) (v in D8 + 1/2).  v lies in D8 + 1/2 exactly
-// when floor(P_0 / q) is odd (column 0 of G is the only odd column).  An offset of 4q
-// (= 2q * (2,...,2), in D8) keeps X non-negative.
+// without building the code word (boundary_overloaded; also the NestQuantM test): the
+// decoder sees X = G (G^-1 P mod q) = P + 2q v with v in E8, and the residual of Alg. 2 is
+// unchanged by D8 shifts of X / 2q (for both oracles), so it equals the residual of P
+// (v in D8) or of P + q (1,...,1) (v in D8 + 1/2).  v lies in D8 + 1/2 exactly when
+// floor(P_0 / q) is odd (column 0 of G is the only odd column).  An offset of 4q
+// (= 2q * (2,...,2), in D8) keeps X non-negative for P_0 >= -2q.
+template <bool M = false>
 __device__ __forceinline__ bool boundary_overloaded(const int (&P)[8], int q, uint32_t mq,
                                                     uint32_t m2q) {
   const uint32_t u0 = (uint32_t)(P[0] + 4 * q);               // P_0 >= -2q on the boundary
@@ -510,7 +476,7 @@ __device__ __forceinline__ bool boundary_overloaded(const int (&P)[8], int q, ui
   int X[8], X2[8];
 #pragma unroll
   for (int l = 0; l < 8; ++l) X[l] = P[l] + off;
-  residual_from_X(X, q, m2q, X2);
+  residual_from_X<M>(X, q, m2q, X2);
   bool diff = false;
 #pragma unroll
   for (int l = 0; l < 8; ++l) diff |= (X2[l] != P[l]);
@@ -522,6 +488,22 @@ __device__ __forceinline__ bool overloaded(const int (&P)[8], int q, float rq, u
   const int M = e8_root_bound(P);
   if (M != 2 * q) return M > 2 * q;
   return boundary_overloaded(P, q, mq, m2q);
+}
+
+// The same test for the NestQuantM decoder (App. D).  Every point that decoder returns lies
+// in the box |P_0| <= 2q, |P_i| <= q (i > 0); outside it P surely overloads, and inside it
+// (where P_0 >= -2q, as boundary_overloaded needs) the literal test decides.
+__device__ __forceinline__ bool in_m_box(const int (&P)[8], int q) {
+  int m = 0;
+#pragma unroll
+  for (int l = 1; l < 8; ++l) m = max(m, abs(P[l]));
+  return m <= q && abs(P[0]) <= 2 * q;
+}
+
+__device__ __forceinline__ bool overloaded_m(const int (&P)[8], int q, uint32_t mq,
+                                             uint32_t m2q) {
+  if (!in_m_box(P, q)) return true;
+  return boundary_overloaded<true>(P, q, mq, m2q);
 }
 
 }  // namespace nq

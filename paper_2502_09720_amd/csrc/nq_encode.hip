@@ -133,6 +133,20 @@ __device__ __forceinline__ int cmp_sum_square(double hi, double lo, double n, do
 __device__ __forceinline__ float next_up(float v) { return __uint_as_float(__float_as_uint(v) + 1u); }
 __device__ __forceinline__ float next_down(float v) { return __uint_as_float(__float_as_uint(v) - 1u); }
 
+// NestQuantM (App. D): every point its decoder reproduces lies in |P_0| <= 2q, |P_i| <= q.
+// The nearest point P of y has |P_i - 2 y_i| <= 2 (covering radius 1), so a block whose
+// statistic s = max(2 max_{i>0} |x_i|, |x_0|) has s c > (q + 2)(1 + 2^-12) surely overloads
+// at the multiplier c (the slack covers the rounding of y = fl32(x c)).
+__device__ __forceinline__ float m_stat(const float (&x)[8]) {
+  float m = fabsf(x[1]);
+#pragma unroll
+  for (int l = 2; l < 8; ++l) m = fmaxf(m, fabsf(x[l]));
+  return fmaxf(2.0f * m, fabsf(x[0]));
+}
+__device__ __forceinline__ bool m_skip(float s, float c, int q) {
+  return s * c > (float)(q + 2) * (1.0f + 0x1p-12f);
+}
+
 // First-beta search for one block (App. F): the smallest t whose nearest E8 point of
 // y = fl32(x * c_t) survives decode(encode(.)); t = k when every beta overloads.
 //
@@ -144,6 +158,25 @@ __device__ __forceinline__ float next_down(float v) { return __uint_as_float(__f
 // rounding of y_t, M and u_t (together below 2^-19 u_t).  Only betas in between are computed and tested.
 __device__ __forceinline__ void encode_block(const float (&v)[8], const float (&c)[4],
                                              const EncodeArgs& a, uint32_t& word, int& tsel) {
+  if (a.decoder) {
+    // NestQuantM: skip the betas its box rules out, then test each with its decoder
+    const float st = m_stat(v);
+    int t = 0;
+    while (t < a.k - 1 && m_skip(st, pick4(c, t), a.q)) ++t;
+    int P[8];
+    for (;;) {
+      float y[8];
+      const float ct = pick4(c, t);
+#pragma unroll
+      for (int l = 0; l < 8; ++l) y[l] = v[l] * ct;
+      nearest_e8(y, P);
+      if (t == a.k - 1 || !overloaded_m(P, a.q, a.mq, a.m2q)) break;
+      ++t;
+    }
+    tsel = t;
+    word = encode_codes(P, a.q, a.rq, a.mq);
+    return;
+  }
   const float mx = root_bound_f(v);
   const float two_q = (float)(2 * a.q);
   int t = a.k - 1;
@@ -360,7 +393,8 @@ struct SlotMap {
 // Finish a block from a given first beta: loop until a point survives (or t = k).
 __device__ __forceinline__ void finish_block(const float (&v)[8], const float (&c)[4], int t,
                                              const EncodeArgs& a, uint32_t& word, int& tsel) {
-  const float mx = root_bound_f(v);
+  const bool m = a.decoder != 0;
+  const float mx = m ? 0.0f : root_bound_f(v);
   const float two_q = (float)(2 * a.q);
   int P[8];
   for (;;) {
@@ -369,9 +403,14 @@ __device__ __forceinline__ void finish_block(const float (&v)[8], const float (&
 #pragma unroll
     for (int l = 0; l < 8; ++l) y[l] = v[l] * ct;
     nearest_e8(y, P);
-    const float u = 2.0f * ct * mx;
-    const bool sure = u + kRootMargin + u * 0x1p-12f < two_q;
-    if (t == a.k - 1 || sure || !overloaded(P, a.q, a.rq, a.mq, a.m2q)) break;
+    if (t == a.k - 1) break;
+    if (m) {
+      if (!overloaded_m(P, a.q, a.mq, a.m2q)) break;
+    } else {
+      const float u = 2.0f * ct * mx;
+      const bool sure = u + kRootMargin + u * 0x1p-12f < two_q;
+      if (sure || !overloaded(P, a.q, a.rq, a.mq, a.m2q)) break;
+    }
     ++t;
   }
   tsel = t;
@@ -429,6 +468,14 @@ __device__ __forceinline__ void unpack_raw<_Float16>(const RawBlock<_Float16>& r
 // norm sqrt(2)) and M(y) = c M(x) up to relative rounding errors below 2^-19 (y, and the
 // fp32 evaluation of M), so M(x) > (2q + 2 sqrt(2) + 0.02) / (2 c (1 - 2^-12)) implies
 // M(P) > 2q.  Rounded up.
+// The NestQuantM counterpart for the statistic m_stat: (q + 2)(1 + 2^-12) / c, rounded up.
+__device__ __forceinline__ float skip_threshold_m(float c, int q) {
+  const double v = (double)(q + 2) * (1.0 + 0x1p-12) / (double)c;
+  float f = (float)v;
+  if ((double)f < v) f = next_up(f);
+  return f;
+}
+
 __device__ __forceinline__ float skip_threshold(float c, int q) {
   const double v = (2.0 * q + (double)kRootMargin) / (2.0 * (double)c * (1.0 - 0x1p-12));
   float f = (float)v;
@@ -532,7 +579,9 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
       for (int t = 0; t < 4; ++t) {
         const float c = coded ? (float)(1.0 / ((double)r * a.beta[t])) : 0.0f;
         crow[cw][rw][t] = c;
-        chi[cw][rw][t] = (coded && t < a.k - 1) ? skip_threshold(c, a.q) : INFINITY;
+        chi[cw][rw][t] = (coded && t < a.k - 1)
+                             ? (a.decoder ? skip_threshold_m(c, a.q) : skip_threshold(c, a.q))
+                             : INFINITY;
       }
       scales[row] = r;
     }
@@ -556,7 +605,7 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
       float v[8];
       unpack_raw<T>(rawl[wave][sl], v);
       // first beta whose point is not surely overloaded: one threshold test per beta
-      const float mx = root_bound_f(v);
+      const float mx = a.decoder ? m_stat(v) : root_bound_f(v);
       const f32x4 hi = *reinterpret_cast<const f32x4*>(chi[cw][rw]);
       t0 = mx > hi.x ? (mx > hi.y ? (mx > hi.z ? 3 : 2) : 1) : 0;
       const float ct = crow[cw][rw][t0];
@@ -567,10 +616,17 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
         queued = true;                 // decision too close for fp32: redo exactly
         start = t0;
       } else if (t0 < a.k - 1) {
-        const int M = e8_root_bound(P);
-        if (M >= 2 * a.q) {            // overloads (>), or on the boundary (=): decide later
-          queued = true;
-          start = M > 2 * a.q ? t0 + 1 : t0;
+        if (a.decoder) {
+          if (overloaded_m(P, a.q, a.mq, a.m2q)) {   // NestQuantM: its decoder decides
+            queued = true;
+            start = t0 + 1;
+          }
+        } else {
+          const int M = e8_root_bound(P);
+          if (M >= 2 * a.q) {          // overloads (>), or on the boundary (=): decide later
+            queued = true;
+            start = M > 2 * a.q ? t0 + 1 : t0;
+          }
         }
       }
     }

@@ -61,7 +61,7 @@ using CfgBig = Cfg<256, 256, 4, 2, 2>;
 // t * X2 of every block of a coded operand into ws[rows_p][nb_p blocks] (zero padding), one
 // thread per block (grid_block): 8 bf16 (16 B) per block, or 8 int8 (8 B) for the int8
 // contraction.
-template <bool I8>
+template <bool I8, bool M>
 __global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__ codes,
                                                     const uint32_t* __restrict__ beta,
                                                     int64_t rows, int nb, int64_t rows_p,
@@ -79,18 +79,31 @@ __global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__
     const uint32_t bw = beta[g.rb * nbw + (uint32_t)(g.lr * nbw + (j >> 4))];
     const int t = (int)((bw >> (2 * (j & 15))) & 3u) + 1;
     if constexpr (I8) {
-      out = decode_tile_i8(w, t, q, m2q);
+      out = decode_tile_i8<M>(w, t, q, m2q);
     } else {
-      out = decode_tile_bf16(w, t, q, m2q);
+      out = decode_tile_bf16<M>(w, t, q, m2q);
     }
   }
   reinterpret_cast<V*>(ws)[g.rb * nb_p + (uint32_t)(g.lr * nb_p + j)] = out;
 }
 
-template __global__ void tiles_kernel<false>(const uint32_t*, const uint32_t*, int64_t, int,
-                                             int64_t, int, int, uint32_t, int, void*);
-template __global__ void tiles_kernel<true>(const uint32_t*, const uint32_t*, int64_t, int,
-                                            int64_t, int, int, uint32_t, int, void*);
+// Launch tiles_kernel for one operand with its decoder.
+template <bool I8>
+void launch_tiles(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void* ws,
+                  hipStream_t st) {
+  int lg;
+  int64_t wgs;
+  grid_shape(rows_p, nb_p, lg, wgs);
+  if (X.decoder) {
+    hipLaunchKernelGGL((tiles_kernel<I8, true>), dim3((unsigned)wgs), dim3(256), 0, st, X.codes,
+                       X.beta, X.rows, nb, rows_p, nb_p, X.q, X.m2q, lg, ws);
+  } else {
+    hipLaunchKernelGGL((tiles_kernel<I8, false>), dim3((unsigned)wgs), dim3(256), 0, st, X.codes,
+                       X.beta, X.rows, nb, rows_p, nb_p, X.q, X.m2q, lg, ws);
+  }
+}
+template void launch_tiles<false>(const MatmulOperand&, int, int64_t, int, void*, hipStream_t);
+template void launch_tiles<true>(const MatmulOperand&, int, int64_t, int, void*, hipStream_t);
 
 __device__ __forceinline__ void tile_coords(int bid, int tm, int tn, int& pm, int& pn) {
   constexpr int GROUP_M = gemm::GROUP_M;
@@ -329,14 +342,8 @@ static hipError_t decode_once(int stages, const MatmulOperand& A, const MatmulOp
   u32x4* wa = reinterpret_cast<u32x4*>(ws);
   u32x4* ww = wa + mp * kc;
   if (stages & 1) {
-    int lg;
-    int64_t wgs;
-    grid_shape(mp, nbp, lg, wgs);
-    hipLaunchKernelGGL(tiles_kernel<I8>, dim3((unsigned)wgs), dim3(256), 0, st, A.codes,
-                       A.beta, A.rows, nb, mp, nbp, A.q, A.m2q, lg, (void*)wa);
-    grid_shape(np, nbp, lg, wgs);
-    hipLaunchKernelGGL(tiles_kernel<I8>, dim3((unsigned)wgs), dim3(256), 0, st, W.codes,
-                       W.beta, W.rows, nb, np, nbp, W.q, W.m2q, lg, (void*)ww);
+    launch_tiles<I8>(A, nb, mp, nbp, (void*)wa, st);
+    launch_tiles<I8>(W, nb, np, nbp, (void*)ww, st);
   }
   if (!(stages & 2)) return hipGetLastError();
   // 256 x 256 tiles once they give every CU a tile, else 256 x 128

@@ -12,12 +12,14 @@ struct EncodeArgs {
   float rq;        // fl32(1 / q), estimate for the mod-q reduction
   uint32_t m2q;    // ceil(2^16 / (2q)): floor(X / 2q) = (X * m2q) >> 16 for 0 <= X < 2^11
   uint32_t mq;     // ceil(2^20 / q): floor(u / q) = (u * mq) >> 20 for 0 <= u < 2048 q
+  int decoder;     // 0: Alg. 2 / Alg. 5, 1: NestQuantM (App. D)
   double beta[4];  // fl64(t * base), t = 1..4
 };
 
 struct DecodeArgs {
   int q;
   uint32_t m2q;
+  int decoder;
   double half_beta[4];  // fl64(t * base) / 2 (exact halving), t = 1..4
 };
 
@@ -28,6 +30,7 @@ struct MatmulOperand {
   int q;
   uint32_t m2q;
   int64_t rows;
+  int decoder;
 };
 
 hipError_t launch_encode(const void* x, int dtype, int64_t rows, int cols, int64_t ld_x,

@@ -22,32 +22,29 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
 template <bool I8>
-__global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__ codes,
-                                                    const uint32_t* __restrict__ beta,
-                                                    int64_t rows, int nb, int64_t rows_p,
-                                                    int nb_p, int q, uint32_t m2q, int lg,
-                                                    void* __restrict__ ws);
+void launch_tiles(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void* ws,
+                  hipStream_t st);
 
 // W block j of this lane's column as a matrix-core operand.  bf16: one block (8 values,
 // 16 B); int8: two consecutive blocks (16 values, 16 B).
-template <bool I8>
+template <bool I8, bool M>
 __device__ __forceinline__ u32x4 w_operand(const uint32_t* wc, const uint32_t* wb, int blk,
                                            int nb, const MatmulOperand& W) {
   if constexpr (I8) {
     u32x2 lo = {0u, 0u}, hi = {0u, 0u};
     if (blk < nb) {
-      lo = decode_tile_i8(wc[blk], (int)((wb[blk >> 4] >> (2 * (blk & 15))) & 3u) + 1, W.q,
+      lo = decode_tile_i8<M>(wc[blk], (int)((wb[blk >> 4] >> (2 * (blk & 15))) & 3u) + 1, W.q,
                           W.m2q);
     }
     if (blk + 1 < nb) {
       const int b1 = blk + 1;
-      hi = decode_tile_i8(wc[b1], (int)((wb[b1 >> 4] >> (2 * (b1 & 15))) & 3u) + 1, W.q,
+      hi = decode_tile_i8<M>(wc[b1], (int)((wb[b1 >> 4] >> (2 * (b1 & 15))) & 3u) + 1, W.q,
                           W.m2q);
     }
     return u32x4{lo.x, lo.y, hi.x, hi.y};
   } else {
     if (blk >= nb) return u32x4{0u, 0u, 0u, 0u};
-    return decode_tile_bf16(wc[blk], (int)((wb[blk >> 4] >> (2 * (blk & 15))) & 3u) + 1, W.q,
+    return decode_tile_bf16<M>(wc[blk], (int)((wb[blk >> 4] >> (2 * (blk & 15))) & 3u) + 1, W.q,
                             W.m2q);
   }
 }
@@ -56,7 +53,7 @@ __device__ __forceinline__ u32x4 w_operand(const uint32_t* wc, const uint32_t* w
 // v_mfma_f32_16x16x32_bf16) or 64 (int8, v_mfma_i32_16x16x64_i8) values of K: lane l holds
 // column l % 16 at K offset (step size / 4) * (l / 16), 16 B of it.  ta is the decoded A
 // tile, [16 * MT][kcb] 16-byte chunks.
-template <int MT, bool I8>
+template <int MT, bool I8, bool MW>
 __global__ __launch_bounds__(256) void skinny_kernel(const u32x4* __restrict__ ta, int kcb,
                                                      MatmulOperand A, MatmulOperand W, int nb,
                                                      float* __restrict__ c, int64_t ldc,
@@ -82,7 +79,7 @@ __global__ __launch_bounds__(256) void skinny_kernel(const u32x4* __restrict__ t
 
   for (int s = s0; s < s1; ++s) {
     const int blk = (4 * s + kg) * BPL;
-    const u32x4 b = nok ? w_operand<I8>(wc, wb, blk, nb, W) : u32x4{0u, 0u, 0u, 0u};
+    const u32x4 b = nok ? w_operand<I8, MW>(wc, wb, blk, nb, W) : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
       const u32x4 a = ta[(int64_t)(16 * m + col) * kcb + 4 * s + kg];
@@ -141,21 +138,22 @@ static hipError_t skinny(int stages, const MatmulOperand& A, const MatmulOperand
   const int nbp = (int)(kp / 8);
   const int kcb = (int)(kp * EB / 16);
   u32x4* ta = reinterpret_cast<u32x4*>(ws);
-  if (stages & 1) {
-    int lg;
-    int64_t wgs;
-    grid_shape(mp, nbp, lg, wgs);
-    hipLaunchKernelGGL(tiles_kernel<I8>, dim3((unsigned)wgs), dim3(256), 0, st, A.codes,
-                       A.beta, A.rows, nb, mp, nbp, A.q, A.m2q, lg, (void*)ta);
-  }
+  if (stages & 1) launch_tiles<I8>(A, nb, mp, nbp, (void*)ta, st);
   if (!(stages & 2)) return hipGetLastError();
   const unsigned grid = (unsigned)((W.rows + 15) / 16);
+#define NQ_SK(MT, MW)                                                                     \
+  hipLaunchKernelGGL((skinny_kernel<MT, I8, MW>), dim3(grid), dim3(256), 0, st, ta, kcb, A, W, \
+                     nb, c, ldc, scale)
+#define NQ_SK2(MT) \
+  if (W.decoder) NQ_SK(MT, true); else NQ_SK(MT, false)
   switch (mp / 16) {
-    case 1: hipLaunchKernelGGL((skinny_kernel<1, I8>), dim3(grid), dim3(256), 0, st, ta, kcb, A, W, nb, c, ldc, scale); break;
-    case 2: hipLaunchKernelGGL((skinny_kernel<2, I8>), dim3(grid), dim3(256), 0, st, ta, kcb, A, W, nb, c, ldc, scale); break;
-    case 3: hipLaunchKernelGGL((skinny_kernel<3, I8>), dim3(grid), dim3(256), 0, st, ta, kcb, A, W, nb, c, ldc, scale); break;
-    default: hipLaunchKernelGGL((skinny_kernel<4, I8>), dim3(grid), dim3(256), 0, st, ta, kcb, A, W, nb, c, ldc, scale); break;
+    case 1: NQ_SK2(1); break;
+    case 2: NQ_SK2(2); break;
+    case 3: NQ_SK2(3); break;
+    default: NQ_SK2(4); break;
   }
+#undef NQ_SK2
+#undef NQ_SK
   return hipGetLastError();
 }
 

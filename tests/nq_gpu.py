@@ -28,20 +28,20 @@ def u32(t, shape=None):
     return a if shape is None else a.reshape(shape)
 
 
-def oracle_encode(x32, q, k, base=None):
+def oracle_encode(x32, q, k, base=None, decoder="full"):
     """Packed oracle codes (rows, nb), beta words (rows, nbw) and scales (rows,)."""
-    codes, t, r = nestquant.quantize_rows(x32, q, k, base)
+    codes, t, r = nestquant.quantize_rows(x32, q, k, base, decoder=decoder)
     return layout.pack_codes(codes), layout.pack_beta(t), r
 
 
-def upload_coded(codes_w, beta_w, scales, rows, cols, q, k, base):
-    """Oracle-packed arrays -> a device Coded operand."""
+def upload_coded(codes_w, beta_w, scales, rows, cols, q, k, base, decoder=0):
+    """Oracle-packed arrays -> a device Coded operand (decoder: 0 full, 1 NestQuantM)."""
     torch = torch_mod()
     from paper_2502_09720_amd import Coded
     c = torch.from_numpy(np.ascontiguousarray(codes_w).reshape(-1).view(np.int32)).cuda()
     b = torch.from_numpy(np.ascontiguousarray(beta_w).reshape(-1).view(np.int32)).cuda()
     s = torch.from_numpy(np.ascontiguousarray(scales, dtype=np.float32)).cuda()
-    return Coded(c, b, s, rows, cols, q, k, base)
+    return Coded(c, b, s, rows, cols, q, k, base, decoder)
 
 
 def first_mismatch(a, b):

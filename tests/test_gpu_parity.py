@@ -31,7 +31,7 @@ def nq():
     return nq
 
 
-def check_encode(nq, store, x32, dtype, q, k, base=None, ld_pad=0):
+def check_encode(nq, store, x32, dtype, q, k, base=None, ld_pad=0, decoder="full"):
     torch = __import__("torch")
     rows, cols = x32.shape
     if ld_pad:
@@ -40,13 +40,13 @@ def check_encode(nq, store, x32, dtype, q, k, base=None, ld_pad=0):
         xd = to_device(big, dtype)[:, :cols]
     else:
         xd = to_device(store, dtype)
-    got = nq.encode(xd, q=q, k=k, base=base)
+    got = nq.encode(xd, q=q, k=k, base=base, decoder=0 if decoder == "full" else 1)
     torch.cuda.synchronize()
     nb = cols // 8
     gc = u32(got.codes, (rows, nb))
     gb = u32(got.beta, (rows, (nb + 15) // 16))
     gs = got.scales.cpu().numpy()
-    oc, ob, os_ = oracle_encode(x32, q, k, base)
+    oc, ob, os_ = oracle_encode(x32, q, k, base, decoder)
     assert first_mismatch(gs.view(np.uint32), os_.view(np.uint32)) is None, \
         "scales: " + first_mismatch(gs.view(np.uint32), os_.view(np.uint32))
     m = first_mismatch(gc, oc)
@@ -382,3 +382,80 @@ def test_encode_tiny_entries(nq):
         store, x32 = workloads.round_to(x, dtype)
         check_encode(nq, store, x32, dtype, 14, 4)
         check_encode(nq, store, x32, dtype, 7, 4)
+
+
+# ------------------------------------------------------------------------------------------
+# NestQuantM (App. D): the same encoder, overload judged by the NestQuantM decoder
+# ------------------------------------------------------------------------------------------
+
+M_ENCODE_CASES = [
+    # (seed, rows, cols, dtype, dist, scale, q, k)
+    (40, 64, 512, "f32", "normal", 1.0, 16, 4),
+    (41, 200, 128, "f16", "normal", 1.0, 16, 4),
+    (42, 37, 8, "bf16", "t4", 1.0, 14, 4),
+    (43, 9, 4096, "bf16", "t4", 1.0, 14, 4),
+    (44, 3, 20000, "bf16", "normal", 1.0, 16, 4),
+    (45, 50, 96, "bf16", "uniform", 1.0, 3, 2),
+    (46, 40, 256, "f32", "normal", 1.0, 7, 3),
+]
+
+
+@pytest.mark.parametrize("case", M_ENCODE_CASES, ids=lambda c: f"s{c[0]}-{c[1]}x{c[2]}-{c[3]}-q{c[6]}k{c[7]}")
+def test_encode_parity_nestquantm(nq, case):
+    seed, rows, cols, dtype, dist, scale, q, k = case
+    store, x32 = workloads.random_rows(seed, rows, cols, dtype=dtype, scale=scale, dist=dist)
+    check_encode(nq, store, x32, dtype, q, k, decoder="m")
+
+
+def test_encode_ties_nestquantm(nq):
+    x = _tie_rows(47)
+    for q, k in [(16, 4), (14, 4), (4, 2)]:
+        store, x32 = workloads.round_to(x, "f32")
+        check_encode(nq, store, x32, "f32", q, k, decoder="m")
+
+
+@pytest.mark.parametrize("out", ["f32", "f16", "bf16"])
+def test_decode_parity_nestquantm(nq, out):
+    torch = __import__("torch")
+    _, x32 = workloads.random_rows(48, 100, 264, dtype="bf16")
+    codes, t, r = nestquant.quantize_rows(x32, 16, 4, decoder="m")
+    from oracle import layout
+    coded = upload_coded(layout.pack_codes(codes), layout.pack_beta(t), r, 100, 264, 16, 4,
+                         nestquant.default_base(16, 4), 1)
+    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[out]
+    got = decoded_to_f64(nq.decode(coded, tdt), out)
+    want = nestquant.decode_rows(codes, t, r, 16, nestquant.default_base(16, 4), decoder="m")
+    assert np.all(np.abs(got - want) <= ulp_in(out, want))
+    # the NestQuantM decoder really differs from Alg. 5 on these codes
+    full = nestquant.decode_rows(codes, t, r, 16, nestquant.default_base(16, 4))
+    assert np.any(full != want)
+
+
+M_MATMUL_CASES = [
+    # (seed, M, N, K, q, k, int8)
+    (50, 1, 1000, 1024, 16, 4, False),
+    (51, 16, 300, 2048, 16, 4, False),
+    (52, 200, 130, 520, 16, 4, False),
+    (53, 130, 70, 264, 14, 4, True),
+    (54, 40, 500, 1032, 15, 4, True),
+]
+
+
+@pytest.mark.parametrize("case", M_MATMUL_CASES, ids=lambda c: f"{c[1]}x{c[2]}x{c[3]}-q{c[4]}k{c[5]}-{'i8' if c[6] else 'bf16'}")
+def test_matmul_parity_nestquantm(nq, case):
+    torch = __import__("torch")
+    seed, M, N, K, q, k, i8 = case
+    _, A32 = workloads.random_rows(seed, M, K, dtype="bf16", dist="t4")
+    _, W32 = workloads.random_rows(seed + 1000, N, K, dtype="bf16", scale=0.02)
+    b = nestquant.default_base(q, k)
+    ca, ta, ra = nestquant.quantize_rows(A32, q, k, decoder="m")
+    cw, tw, rw = nestquant.quantize_rows(W32, q, k, decoder="m")
+    C = nestquant.coded_matmul(ca, ta, ra, q, b, cw, tw, rw, q, b, "m", "m")
+    from oracle import layout
+    a = upload_coded(layout.pack_codes(ca), layout.pack_beta(ta), ra, M, K, q, k, b, 1)
+    w = upload_coded(layout.pack_codes(cw), layout.pack_beta(tw), rw, N, K, q, k, b, 1)
+    got = nq.matmul(a, w, int8=i8)
+    torch.cuda.synchronize()
+    g = got.cpu().numpy().astype(np.float64)
+    rel = np.linalg.norm(g - C) / max(np.linalg.norm(C), 1e-300)
+    assert rel <= (1e-6 if i8 else MATMUL_RTOL), f"relative Frobenius error {rel}"
