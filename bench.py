@@ -39,10 +39,67 @@ def parse():
     ap.add_argument("--kv", action="store_true",
                     help="standalone nq_encode / nq_decode of the 2^28-entry fp16 KV-like "
                          "matrix (2^21 rows of 128) against the HBM roofline")
+    ap.add_argument("--gemv", action="store_true",
+                    help="the paper's GEMV: one coded 8192-vector times a coded 8192 x 8192 "
+                         "matrix, q=16, k=4, NestQuantM and full decoders, against HBM")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="calibration only: time a plain device-to-device copy of this many "
                          "bytes (the reference for the HBM byte counters)")
     return ap.parse_args()
+
+
+def gemv_roofline(args):
+    """The paper's GEMV (App. E runtime table): C = a W^T with a 1 x 8192 and W 8192 x 8192,
+    both NestQuant-coded at q=16, k=4 (4.25 bits per entry), with the NestQuantM decoder (the
+    paper's kernel) and with the full decoder.  W ~ N(0, 0.02^2) bf16 and a ~ N(0, 1) bf16,
+    drawn from seeded streams; W is rotated over enough copies (> 256 MB) that the Infinity
+    Cache cannot hold it.  Bytes = coded W + coded a + fp32 output."""
+    import numpy as np
+    import torch
+    import workloads
+    import paper_2502_09720_amd as nq
+    dev = torch.device("cuda:0")
+    n = 8192
+    q, k = 16, 4
+    sa, _ = workloads.random_rows(8192, 1, n, dtype="bf16")
+    sw, _ = workloads.random_rows(8193, n, n, dtype="bf16", scale=0.02)
+    A = torch.from_numpy(sa.view(np.int16)).to(dev).view(torch.bfloat16)
+    W = torch.from_numpy(sw.view(np.int16)).to(dev).view(torch.bfloat16)
+    nb = n // 8
+    coded_w = n * nb * 4 + n * ((nb + 15) // 16) * 4 + n * 4
+    nbuf = -(-256 * 2**20 // coded_w) + 1
+    res = {}
+    for name, dec in (("nestquantm", nq.DECODER_M), ("full", nq.DECODER_FULL)):
+        ac = nq.encode(A, q=q, k=k, decoder=dec)
+        wcs = [nq.encode(W, q=q, k=k, decoder=dec) for _ in range(nbuf)]
+        C = torch.empty(1, n, dtype=torch.float32, device=dev)
+        ws = torch.empty(nq.matmul_workspace_size(1, n, n), dtype=torch.uint8, device=dev)
+        for i in range(args.warmup):
+            nq.matmul(ac, wcs[i % nbuf], out=C, workspace=ws)
+        torch.cuda.synchronize()
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+        for i in range(args.steps):
+            ev[i][0].record()
+            nq.matmul(ac, wcs[i % nbuf], out=C, workspace=ws, stages=nq.STAGE_DECODE)
+            ev[i][1].record()
+            nq.matmul(ac, wcs[i % nbuf], out=C, workspace=ws, stages=nq.STAGE_CONTRACT)
+            ev[i][2].record()
+        torch.cuda.synchronize()
+        dec_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+        con_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+        byts = coded_w + nb * 4 + 4 + 4 + n * 4
+        res[name] = {"us": (dec_ms + con_ms) * 1e3, "decode_stage_us": dec_ms * 1e3,
+                     "contract_us": con_ms * 1e3,
+                     "contract_GBps": byts / (con_ms * 1e-3) / 1e9,
+                     "contract_hbm_frac": byts / (con_ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+                     "bytes": byts, "w_copies": nbuf}
+        del wcs
+    print(json.dumps({"metric": "coded GEMV time, 8192 x 8192, q=16, k=4 (4.25 bits/entry)",
+                      "unit": "us", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+                      "dtype": "bf16", "data": "synthetic",
+                      "config": {"workload": "GEMV a (1x8192) W^T (8192x8192), W N(0,0.02^2)"},
+                      "results": res,
+                      "paper_context": "NestQuantM 60 us on an NVIDIA A100 (App. E table)"}))
 
 
 def copy_calibration(args):
@@ -197,6 +254,9 @@ def main():
         return
     if args.copy_bytes:
         copy_calibration(args)
+        return
+    if args.gemv:
+        gemv_roofline(args)
         return
 
     import numpy as np

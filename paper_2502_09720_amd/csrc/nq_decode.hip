@@ -10,7 +10,7 @@
 
 namespace nq {
 
-template <int OUT, bool M>  // OUT: 0 = fp32, 1 = fp16, 2 = bf16; M: NestQuantM decoder
+template <int OUT, int DV>  // OUT: 0 = fp32, 1 = fp16, 2 = bf16; DV: decoder_variant
 __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict__ codes,
                                                      const uint32_t* __restrict__ beta,
                                                      const float* __restrict__ scales,
@@ -26,7 +26,21 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict_
   const int t = (int)((bw >> (2 * (j & 15))) & 3u);
   const double sc = (double)scales[g.rb + g.lr] * a.half_beta[t];
   uint32_t X2p[4];
-  decode_word_pk<M>(w, a.q, a.m2q, X2p);
+  if constexpr (DV == 2) {
+    // byte-SIMD NestQuantM at q = 16: repack the signed bytes as int16 pairs
+    uint32_t xa, xb;
+    int x0;
+    decode_word_m16(w, xa, xb, x0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t x = i < 2 ? xa : xb;
+      const int lo = i == 0 ? x0 : ((int)(int8_t)(uint8_t)(x >> (16 * (i & 1))) >> 2);
+      const int hi = (int)(int8_t)(uint8_t)(x >> (16 * (i & 1) + 8)) >> 2;
+      X2p[i] = ((uint32_t)lo & 0xFFFFu) | ((uint32_t)hi << 16);
+    }
+  } else {
+    decode_word_pk<DV == 1>(w, a.q, a.m2q, X2p);
+  }
   if constexpr (OUT == 0) {
     // fp32: each value rounded once from its fp64 product
     float v[8];
@@ -72,15 +86,18 @@ hipError_t launch_decode(const uint32_t* codes, const uint32_t* beta, const floa
   int64_t wgs;
   grid_shape(rows, nb, lg, wgs);
   const unsigned grid = (unsigned)wgs;
-#define NQ_DEC(O, MM)                                                                       \
-  hipLaunchKernelGGL((decode_kernel<O, MM>), dim3(grid), dim3(256), 0, st, codes, beta,     \
+#define NQ_DEC(O, DV)                                                                       \
+  hipLaunchKernelGGL((decode_kernel<O, DV>), dim3(grid), dim3(256), 0, st, codes, beta,     \
                      scales, rows, nb, lg, out, ld_out, a)
-  const bool m = a.decoder != 0;
+#define NQ_DEC3(O) \
+  if (dv == 0) NQ_DEC(O, 0); else if (dv == 1) NQ_DEC(O, 1); else NQ_DEC(O, 2)
+  const int dv = decoder_variant(a.decoder, a.q);
   switch (out_dtype) {
-    case 0: if (m) NQ_DEC(0, true); else NQ_DEC(0, false); break;
-    case 1: if (m) NQ_DEC(1, true); else NQ_DEC(1, false); break;
-    default: if (m) NQ_DEC(2, true); else NQ_DEC(2, false); break;
+    case 0: NQ_DEC3(0); break;
+    case 1: NQ_DEC3(1); break;
+    default: NQ_DEC3(2); break;
   }
+#undef NQ_DEC3
 #undef NQ_DEC
   return hipGetLastError();
 }

@@ -354,6 +354,59 @@ __device__ __forceinline__ void decode_word_pk(uint32_t w, int q, uint32_t m2q,
     X2[i] = bits32(as_u16x2(X2[i]) + as_u16x2(word == i ? dl : 0u));
 }
 
+// ---------------------------------------------------------------------------------------
+// NestQuantM decode at q = 16 with four coordinates per register (byte SIMD).  With 2q = 32
+// every X = G c fits a byte (X4 <= 15 + 2 * 120 = 255, the others <= 45), floor(X / 32) and
+// X mod 32 are a shift and a mask per byte, sum |X mod 32 - 16| is one v_sad_u8 per four
+// coordinates, and without argmin / argmax only coordinate 0 is ever flipped.  Same
+// arithmetic and tie rules as decode_word_pk<true> at q = 16.
+//
+// Outputs: x0 = X2_0 (the flipped coordinate, |x0| <= 32) and, in xa (coordinates 0-3) and
+// xb (4-7), every coordinate before the flip as a 6-bit two's-complement field shifted to
+// the top of its byte, so that the signed byte is 4 X2_l (|X2_l| <= 16 there): the D8
+// residual f - 32 g is f | (g << 5) in 6 bits, the D8+1/2 residual f - 16 is
+// f ^ 0x30 ^ ((f & 0x10) << 1).  Only OR / XOR / shifts, no carries between bytes.
+// ---------------------------------------------------------------------------------------
+__device__ __forceinline__ void decode_word_m16(uint32_t w, uint32_t& xa, uint32_t& xb, int& x0) {
+  const uint32_t E = w & 0x0F0F0F0Fu;           // bytes c0 c2 c4 c6
+  const uint32_t O = (w >> 4) & 0x0F0F0F0Fu;    // bytes c1 c3 c5 c7
+  const uint32_t c0 = E & 0xFFu;
+  const uint32_t sum_c = __builtin_amdgcn_sad_u8(E, 0u, __builtin_amdgcn_sad_u8(O, 0u, 0u));
+  // (X0..X3) = c0 + 2 (0, c2, c4, c6); (X4..X7) = c0 + 2 (c1 + sum c - c0, c3, c5, c7)
+  const uint32_t c0x4 = __builtin_amdgcn_perm(0u, c0, 0x00000000u);   // c0 in every byte
+  const uint32_t Xa = c0x4 + ((E & 0xFFFFFF00u) << 1);
+  const uint32_t Xb = c0x4 + (((O & 0xFFFFFF00u) | ((O & 0xFFu) + sum_c - c0)) << 1);
+  const uint32_t Fa = Xa & 0x1F1F1F1Fu, Fb = Xb & 0x1F1F1F1Fu;              // X mod 32
+  const uint32_t Da = (Xa >> 5) & 0x07070707u, Db = (Xb >> 5) & 0x07070707u;  // floor(X / 32)
+  // g = [f > 16] (an exact half rounds down): bit 5 of f + 15
+  const uint32_t Ga = ((Fa + 0x0F0F0F0Fu) >> 5) & 0x01010101u;
+  const uint32_t Gb = ((Fb + 0x0F0F0F0Fu) >> 5) & 0x01010101u;
+  const uint32_t sum_h = __builtin_amdgcn_sad_u8(Fa, 0x10101010u,
+                                                 __builtin_amdgcn_sad_u8(Fb, 0x10101010u, 0u));
+  const uint32_t pi = __builtin_amdgcn_sad_u8(Da, 0u, __builtin_amdgcn_sad_u8(Db, 0u, 0u)) & 1u;
+  const uint32_t odd1 = (pi + __builtin_popcount(Ga | (Gb << 1))) & 1u;
+  const int f0 = (int)(Fa & 0xFFu);
+  const int h0 = abs(f0 - 16);
+  // Alg. 5's gap times 2q with both fixes at coordinate 0: 4q - sum|h| + odd1 2|h0| - pi (2q - 2|h0|)
+  const int gap = 64 - (int)sum_h + (odd1 ? 2 * h0 : 0) - (pi ? 32 - 2 * h0 : 0);
+  const bool d8 = gap < 0;
+  const uint32_t m = 0u - (uint32_t)d8;                       // all ones for D8
+  const uint32_t ra = Fa ^ 0x30303030u ^ ((Fa & 0x10101010u) << 1);
+  const uint32_t rb = Fb ^ 0x30303030u ^ ((Fb & 0x10101010u) << 1);
+  xa = (ra ^ (((Fa | (Ga << 5)) ^ ra) & m)) << 2;
+  xb = (rb ^ (((Fb | (Gb << 5)) ^ rb) & m)) << 2;
+  // coordinate 0 moves by +32 s (D8) or -32 s (D8+1/2), s = 2 g0 - 1
+  const bool g0 = (Ga & 1u) != 0;
+  const int r0 = d8 ? (g0 ? f0 - 32 : f0) : f0 - 16;
+  const bool fix = d8 ? (odd1 != 0) : (pi != 0);
+  x0 = r0 + (fix ? ((g0 == d8) ? 32 : -32) : 0);
+}
+
+// Signed byte b of x as a float.
+__device__ __forceinline__ float sbyte_f32(uint32_t x, int b) {
+  return (float)(int)(int8_t)(uint8_t)(x >> (8 * b));
+}
+
 // One thread per block of a rows x nb grid of blocks, 256 threads per workgroup: rows
 // shorter than 256 blocks are packed (a power-of-two group of lanes per row), longer rows
 // are cut into 256-block segments.  lg = log2 of the group size (for nb <= 256) or -1.
@@ -381,10 +434,25 @@ __device__ __forceinline__ GridPos grid_block(int nb, int lg) {
 
 // t * X2 of one block as eight bf16 (exact: |t X2| <= 4 * 32 = 128 < 2^8): the upper halves
 // of the fp32 values, coordinates 2i and 2i+1 in word i.
-template <bool M = false>
+template <int DV = 0>
 __device__ __forceinline__ u32x4 decode_tile_bf16(uint32_t w, int t, int q, uint32_t m2q) {
+  if constexpr (DV == 2) {
+    uint32_t xa, xb;
+    int x0;
+    decode_word_m16(w, xa, xb, x0);
+    const float tq = 0.25f * (float)t;    // bytes hold 4 X2 (exact)
+    uint32_t o[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t x = i < 2 ? xa : xb;
+      const float lo = i == 0 ? (float)(x0 * t) : sbyte_f32(x, 2 * (i & 1)) * tq;
+      const float hi = sbyte_f32(x, 2 * (i & 1) + 1) * tq;
+      o[i] = __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
+    }
+    return u32x4{o[0], o[1], o[2], o[3]};
+  }
   uint32_t X2p[4];
-  decode_word_pk<M>(w, q, m2q, X2p);
+  decode_word_pk<DV == 1>(w, q, m2q, X2p);
   uint32_t o[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -400,10 +468,10 @@ __device__ __forceinline__ u32x4 decode_tile_bf16(uint32_t w, int t, int q, uint
 // coordinates in byte order.  The 16-bit products keep their low byte, which is the
 // two's-complement int8 of a value in [-127, 127].
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-template <bool M = false>
+template <int DV = 0>
 __device__ __forceinline__ u32x2 decode_tile_i8(uint32_t w, int t, int q, uint32_t m2q) {
   uint32_t X2p[4];
-  decode_word_pk<M>(w, q, m2q, X2p);
+  decode_word_pk<DV != 0>(w, q, m2q, X2p);
   const u16x2 tt = {(unsigned short)t, (unsigned short)t};
   uint32_t p[4];
 #pragma unroll

@@ -61,7 +61,7 @@ using CfgBig = Cfg<256, 256, 4, 2, 2>;
 // t * X2 of every block of a coded operand into ws[rows_p][nb_p blocks] (zero padding), one
 // thread per block (grid_block): 8 bf16 (16 B) per block, or 8 int8 (8 B) for the int8
 // contraction.
-template <bool I8, bool M>
+template <bool I8, int DV>
 __global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__ codes,
                                                     const uint32_t* __restrict__ beta,
                                                     int64_t rows, int nb, int64_t rows_p,
@@ -79,9 +79,9 @@ __global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__
     const uint32_t bw = beta[g.rb * nbw + (uint32_t)(g.lr * nbw + (j >> 4))];
     const int t = (int)((bw >> (2 * (j & 15))) & 3u) + 1;
     if constexpr (I8) {
-      out = decode_tile_i8<M>(w, t, q, m2q);
+      out = decode_tile_i8<DV>(w, t, q, m2q);
     } else {
-      out = decode_tile_bf16<M>(w, t, q, m2q);
+      out = decode_tile_bf16<DV>(w, t, q, m2q);
     }
   }
   reinterpret_cast<V*>(ws)[g.rb * nb_p + (uint32_t)(g.lr * nb_p + j)] = out;
@@ -94,13 +94,15 @@ void launch_tiles(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void
   int lg;
   int64_t wgs;
   grid_shape(rows_p, nb_p, lg, wgs);
-  if (X.decoder) {
-    hipLaunchKernelGGL((tiles_kernel<I8, true>), dim3((unsigned)wgs), dim3(256), 0, st, X.codes,
-                       X.beta, X.rows, nb, rows_p, nb_p, X.q, X.m2q, lg, ws);
-  } else {
-    hipLaunchKernelGGL((tiles_kernel<I8, false>), dim3((unsigned)wgs), dim3(256), 0, st, X.codes,
-                       X.beta, X.rows, nb, rows_p, nb_p, X.q, X.m2q, lg, ws);
+#define NQ_TL(DV)                                                                            \
+  hipLaunchKernelGGL((tiles_kernel<I8, DV>), dim3((unsigned)wgs), dim3(256), 0, st, X.codes,    \
+                     X.beta, X.rows, nb, rows_p, nb_p, X.q, X.m2q, lg, ws)
+  switch (decoder_variant(X.decoder, X.q)) {
+    case 0: NQ_TL(0); break;
+    case 1: NQ_TL(1); break;
+    default: NQ_TL(2); break;
   }
+#undef NQ_TL
 }
 template void launch_tiles<false>(const MatmulOperand&, int, int64_t, int, void*, hipStream_t);
 template void launch_tiles<true>(const MatmulOperand&, int, int64_t, int, void*, hipStream_t);

@@ -11,6 +11,7 @@
 // fragments are loaded per step for up to four 16-row M tiles.  A workgroup owns 16
 // columns of C; its four waves split K and combine their partial sums through LDS before
 // the epilogue C_ij = acc * r_Ai * r_Wj * base_A * base_W / 4.
+#include <algorithm>
 #include <type_traits>
 
 #include "nq_device.hpp"
@@ -25,74 +26,137 @@ template <bool I8>
 void launch_tiles(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void* ws,
                   hipStream_t st);
 
-// W block j of this lane's column as a matrix-core operand.  bf16: one block (8 values,
-// 16 B); int8: two consecutive blocks (16 values, 16 B).
-template <bool I8, bool M>
-__device__ __forceinline__ u32x4 w_operand(const uint32_t* wc, const uint32_t* wb, int blk,
-                                           int nb, const MatmulOperand& W) {
-  if constexpr (I8) {
-    u32x2 lo = {0u, 0u}, hi = {0u, 0u};
-    if (blk < nb) {
-      lo = decode_tile_i8<M>(wc[blk], (int)((wb[blk >> 4] >> (2 * (blk & 15))) & 3u) + 1, W.q,
-                          W.m2q);
-    }
-    if (blk + 1 < nb) {
-      const int b1 = blk + 1;
-      hi = decode_tile_i8<M>(wc[b1], (int)((wb[b1 >> 4] >> (2 * (b1 & 15))) & 3u) + 1, W.q,
-                          W.m2q);
-    }
-    return u32x4{lo.x, lo.y, hi.x, hi.y};
-  } else {
-    if (blk >= nb) return u32x4{0u, 0u, 0u, 0u};
-    return decode_tile_bf16<M>(wc[blk], (int)((wb[blk >> 4] >> (2 * (blk & 15))) & 3u) + 1, W.q,
-                            W.m2q);
-  }
-}
-
-// One workgroup per 16 columns of C; four waves split K.  Per step a wave covers 32 (bf16,
-// v_mfma_f32_16x16x32_bf16) or 64 (int8, v_mfma_i32_16x16x64_i8) values of K: lane l holds
-// column l % 16 at K offset (step size / 4) * (l / 16), 16 B of it.  ta is the decoded A
-// tile, [16 * MT][kcb] 16-byte chunks.
-template <int MT, bool I8, bool MW>
-__global__ __launch_bounds__(256) void skinny_kernel(const u32x4* __restrict__ ta, int kcb,
-                                                     MatmulOperand A, MatmulOperand W, int nb,
-                                                     float* __restrict__ c, int64_t ldc,
-                                                     float scale) {
+// One workgroup per 16 columns of C; its NWV waves split K.  An MFMA sums over its K values
+// in any order as long as both operands follow it, so K is dealt in chunks of 4 PD steps'
+// worth of blocks (32 blocks for bf16, PD = 8) and lane (column l % 16, group g = l / 16)
+// takes the g-th quarter of each chunk, one block (bf16, v_mfma_f32_16x16x32_bf16) or two
+// (int8, v_mfma_i32_16x16x64_i8) per step.  A lane's code words of a chunk are then
+// contiguous (two or four 16-byte loads) and share one beta word, and its A fragments are
+// the matching 16-byte chunks of the decoded A tile ta ([16 * MT][kcb] chunks; rows at or
+// past M are not read).  Buffer loads with 32-bit offsets and the hardware range check:
+// words out of range read as 0 (a zero code word decodes to zero); a chunk that runs past
+// the end of a row is read word by word, the words past the row made out of range.  The
+// next chunk's words are loaded while the current one is decoded (two register sets in
+// turn).  The host keeps W's code array below
+// 2^31 bytes per launch.
+template <int MT, bool I8, int DVW, int NWV>
+__global__ __launch_bounds__(NWV * 64) void skinny_kernel(const u32x4* __restrict__ ta, int kcb,
+                                                          MatmulOperand A, MatmulOperand W,
+                                                          int nb, float* __restrict__ c,
+                                                          int64_t ldc, float scale) {
   using Acc = typename std::conditional<I8, i32x4, f32x4>::type;
-  __shared__ Acc part[3][MT][64];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  constexpr int BPL = I8 ? 2 : 1;        // blocks per lane per step
+  constexpr int PD = MT <= 2 ? 8 : 4;    // steps per chunk
+  constexpr int WPL = PD * BPL;          // code words per lane per chunk (8 or 16, or 4 / 8)
+  constexpr int CB = 4 * WPL;            // blocks per chunk
+  constexpr uint32_t OOB = 0x80000000u;  // beyond every range below
+  __shared__ Acc part[NWV - 1][MT][64];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // uniform: scalar
+  const int lane = threadIdx.x & 63;
   const int col = lane & 15, kg = lane >> 4;
   const int64_t n = (int64_t)blockIdx.x * 16 + col;
   const bool nok = n < W.rows;
   const int nbw = (nb + 15) >> 4;
-  const uint32_t* wc = W.codes + (nok ? n : 0) * nb;
-  const uint32_t* wb = W.beta + (nok ? n : 0) * nbw;
-  constexpr int BPL = I8 ? 2 : 1;   // blocks per lane per step
+  const __amdgpu_buffer_rsrc_t rc =
+      __builtin_amdgcn_make_buffer_rsrc((void*)W.codes, (short)0, (int)(W.rows * nb * 4), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rb =
+      __builtin_amdgcn_make_buffer_rsrc((void*)W.beta, (short)0, (int)(W.rows * nbw * 4), 0x00020000);
+  const __amdgpu_buffer_rsrc_t ra =
+      __builtin_amdgcn_make_buffer_rsrc((void*)ta, (short)0, 16 * MT * kcb * 16, 0x00020000);
+  const uint32_t cbase = nok ? (uint32_t)(n * nb) * 4u : OOB;
+  const uint32_t bbase = nok ? (uint32_t)(n * nbw) * 4u : OOB;
 
-  // K in steps of 4 * BPL blocks; wave w takes a contiguous quarter of the steps
-  const int nsteps = kcb / 4;
-  const int s0 = (int)((int64_t)nsteps * wave / 4), s1 = (int)((int64_t)nsteps * (wave + 1) / 4);
+  // chunks of CB blocks; wave w takes a contiguous share of them
+  const int nbp = kcb * 16 / (I8 ? 8 : 16);            // padded blocks per row of the A tile
+  const int nch = (nbp + CB - 1) / CB;
+  const int c0 = (int)((int64_t)nch * wave / NWV), c1 = (int)((int64_t)nch * (wave + 1) / NWV);
+
+  struct Words {
+    uint32_t w[WPL];
+    uint32_t b;
+  };
+  // 16-byte loads when every row starts 16-byte aligned and the chunk lies inside the row;
+  // otherwise one word at a time, blocks past the row read as out of range
+  const bool rows16 = (nb & 3) == 0;
+  auto load_w = [&](int ch, Words& x) {
+    const int blk0 = ch * CB + kg * WPL;                 // first block of this lane's quarter
+    const uint32_t past = ch < c1 ? 0u : OOB;           // beyond the wave's chunks: nothing
+    if (rows16 && ch * CB + CB <= nb) {
+#pragma unroll
+      for (int v = 0; v < WPL / 4; ++v) {
+        const u32x4 q = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                       rc, (cbase + 4u * (uint32_t)(blk0 + 4 * v)) | past, 0, 0));
+        x.w[4 * v] = q.x; x.w[4 * v + 1] = q.y; x.w[4 * v + 2] = q.z; x.w[4 * v + 3] = q.w;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < WPL; ++j)
+        x.w[j] = __builtin_amdgcn_raw_buffer_load_b32(
+            rc, (blk0 + j < nb ? cbase + 4u * (uint32_t)(blk0 + j) : OOB) | past, 0, 0);
+    }
+    x.b = __builtin_amdgcn_raw_buffer_load_b32(rb, (bbase + 4u * (uint32_t)(blk0 >> 4)) | past, 0, 0);
+  };
 
   Acc acc[MT];
 #pragma unroll
   for (int m = 0; m < MT; ++m) acc[m] = Acc{};
 
-  for (int s = s0; s < s1; ++s) {
-    const int blk = (4 * s + kg) * BPL;
-    const u32x4 b = nok ? w_operand<I8, MW>(wc, wb, blk, nb, W) : u32x4{0u, 0u, 0u, 0u};
+  // A fragments of chunk ch: row 16 m + col, the 16-byte chunk holding the step's blocks
+  u32x4 af[PD][MT];
+  auto load_a = [&](int ch) {
+    const int blk0 = ch * CB + kg * WPL;
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
-      const u32x4 a = ta[(int64_t)(16 * m + col) * kcb + 4 * s + kg];
-      if constexpr (I8) {
-        acc[m] = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, a),
-                                                       __builtin_bit_cast(i32x4, b), acc[m],
-                                                       0, 0, 0);
-      } else {
-        acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                         __builtin_bit_cast(bf16x8, b), acc[m],
-                                                         0, 0, 0);
+      const bool row_ok = 16 * m + col < A.rows;
+#pragma unroll
+      for (int i = 0; i < PD; ++i) {
+        const int blk = blk0 + i * BPL;
+        const uint32_t off = (uint32_t)((16 * m + col) * kcb + blk / BPL) * 16u;
+        af[i][m] = row_ok && blk < nbp
+                       ? __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, off, 0, 0))
+                       : u32x4{0u, 0u, 0u, 0u};
       }
     }
+  };
+  auto compute = [&](int ch, Words& x) {
+    const int blk0 = ch * CB + kg * WPL;
+#pragma unroll
+    for (int i = 0; i < PD; ++i) {
+      const int blk = blk0 + i * BPL;
+      u32x4 b;
+      if constexpr (I8) {
+        const u32x2 lo = decode_tile_i8<DVW>(x.w[2 * i], (int)((x.b >> (2 * (blk & 15))) & 3u) + 1, W.q, W.m2q);
+        const u32x2 hi = decode_tile_i8<DVW>(x.w[2 * i + 1], (int)((x.b >> (2 * ((blk + 1) & 15))) & 3u) + 1, W.q, W.m2q);
+        b = u32x4{lo.x, lo.y, hi.x, hi.y};
+      } else {
+        b = decode_tile_bf16<DVW>(x.w[i], (int)((x.b >> (2 * (blk & 15))) & 3u) + 1, W.q, W.m2q);
+      }
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        if constexpr (I8) {
+          acc[m] = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, af[i][m]),
+                                                         __builtin_bit_cast(i32x4, b), acc[m], 0,
+                                                         0, 0);
+        } else {
+          acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, af[i][m]),
+                                                           __builtin_bit_cast(bf16x8, b), acc[m],
+                                                           0, 0, 0);
+        }
+      }
+    }
+  };
+
+  Words x0, x1;
+  load_w(c0, x0);
+  for (int ch = c0; ch < c1; ch += 2) {
+    load_a(ch);                  // before the next W words: loads complete in order
+    load_w(ch + 1, x1);
+    compute(ch, x0);
+    if (ch + 1 >= c1) break;
+    load_a(ch + 1);
+    load_w(ch + 2, x0);
+    compute(ch + 1, x1);
   }
 
   if (wave > 0) {
@@ -107,7 +171,7 @@ __global__ __launch_bounds__(256) void skinny_kernel(const u32x4* __restrict__ t
     for (int m = 0; m < MT; ++m) {
       Acc v = acc[m];
 #pragma unroll
-      for (int w = 0; w < 3; ++w) {
+      for (int w = 0; w < NWV - 1; ++w) {
         const Acc o = part[w][m][lane];
         v.x += o.x; v.y += o.y; v.z += o.z; v.w += o.w;
       }
@@ -129,6 +193,29 @@ size_t skinny_workspace(int64_t M, int64_t K) {
 }
 
 template <bool I8>
+static hipError_t skinny_launch(const MatmulOperand& A, const MatmulOperand& W, const u32x4* ta,
+                                int kcb, int nb, float* c, int64_t ldc, float scale,
+                                hipStream_t st) {
+  const int64_t mp = (A.rows + 15) / 16 * 16;
+  const unsigned grid = (unsigned)((W.rows + 15) / 16);
+#define NQ_SK(MT, DV)                                                                     \
+  hipLaunchKernelGGL((skinny_kernel<MT, I8, DV, 8>), dim3(grid), dim3(512), 0, st, ta, kcb, A, \
+                     W, nb, c, ldc, scale)
+  const int dvw = decoder_variant(W.decoder, W.q);
+#define NQ_SK2(MT) \
+  if (dvw == 0) NQ_SK(MT, 0); else if (dvw == 1) NQ_SK(MT, 1); else NQ_SK(MT, 2)
+  switch (mp / 16) {
+    case 1: NQ_SK2(1); break;
+    case 2: NQ_SK2(2); break;
+    case 3: NQ_SK2(3); break;
+    default: NQ_SK2(4); break;
+  }
+#undef NQ_SK2
+#undef NQ_SK
+  return hipGetLastError();
+}
+
+template <bool I8>
 static hipError_t skinny(int stages, const MatmulOperand& A, const MatmulOperand& W, int64_t K,
                          float* c, int64_t ldc, float scale, void* ws, hipStream_t st) {
   const int nb = (int)(K / 8);
@@ -140,20 +227,18 @@ static hipError_t skinny(int stages, const MatmulOperand& A, const MatmulOperand
   u32x4* ta = reinterpret_cast<u32x4*>(ws);
   if (stages & 1) launch_tiles<I8>(A, nb, mp, nbp, (void*)ta, st);
   if (!(stages & 2)) return hipGetLastError();
-  const unsigned grid = (unsigned)((W.rows + 15) / 16);
-#define NQ_SK(MT, MW)                                                                     \
-  hipLaunchKernelGGL((skinny_kernel<MT, I8, MW>), dim3(grid), dim3(256), 0, st, ta, kcb, A, W, \
-                     nb, c, ldc, scale)
-#define NQ_SK2(MT) \
-  if (W.decoder) NQ_SK(MT, true); else NQ_SK(MT, false)
-  switch (mp / 16) {
-    case 1: NQ_SK2(1); break;
-    case 2: NQ_SK2(2); break;
-    case 3: NQ_SK2(3); break;
-    default: NQ_SK2(4); break;
+  // W in column ranges whose code words stay below 2^31 bytes (buffer-load offsets)
+  const int64_t max_rows = (((int64_t)1 << 31) - 1) / ((int64_t)nb * 4) / 16 * 16;
+  for (int64_t r0 = 0; r0 < W.rows; r0 += max_rows) {
+    MatmulOperand Wc = W;
+    const int64_t rows = std::min(max_rows, W.rows - r0);
+    Wc.codes = W.codes + r0 * nb;
+    Wc.beta = W.beta + r0 * ((nb + 15) / 16);
+    Wc.scales = W.scales + r0;
+    Wc.rows = rows;
+    const hipError_t e = skinny_launch<I8>(A, Wc, ta, kcb, nb, c + r0, ldc, scale, st);
+    if (e != hipSuccess) return e;
   }
-#undef NQ_SK2
-#undef NQ_SK
   return hipGetLastError();
 }
 
