@@ -323,6 +323,27 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
+    # the Hadamard rotation in front of the encoder (Sec. 5; not part of the step)
+    rot = None
+    try:
+        Y = torch.empty(M, K, dtype=torch.float32, device=dev)
+        for i in range(args.warmup):
+            nq.rotate(As[i % nbuf], out=Y)
+        torch.cuda.synchronize()
+        er = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+        for i in range(args.steps):
+            er[i][0].record()
+            nq.rotate(As[i % nbuf], out=Y)
+            er[i][1].record()
+        torch.cuda.synchronize()
+        rms = float(np.mean([e[0].elapsed_time(e[1]) for e in er]))
+        rbytes = M * K * (in_bytes + 4)
+        rot = {"ms": rms, "GBps": rbytes / (rms * 1e-3) / 1e9,
+               "hbm_frac": rbytes / (rms * 1e-3) / 1e9 / HBM_PEAK_GBPS, "bytes": rbytes}
+        del Y
+    except nq.NQError:
+        pass                                  # K not 2^k or 28 * 2^k
+
     # the exact int8 contraction (a variant of the product, not part of the step)
     i8 = None
     if k * q <= 63:
@@ -402,6 +423,7 @@ def main():
             "a_rotation_buffers": nbuf,
             "rate_bits_per_entry": float(np.log2(q) + np.log2(k) / 8),
             "nq_matmul_int8_variant": i8,
+            "nq_rotate_A": rot,
         },
         "roofline": roofline,
         "cpu_baseline": None,

@@ -148,6 +148,21 @@ nq_status nq_matmul_stages(int32_t stages, const nq_params* pa, const uint32_t* 
                            const float* w_scales, int64_t N, int64_t K, float* c, int64_t ldc,
                            void* workspace, int64_t workspace_bytes, void* hip_stream);
 
+/* Online rotation of rows before quantization (Sec. 5, "LLM quantization"): y = x U for
+ * every row, with U = H_n / sqrt(n) (Sylvester's Hadamard matrix) when cols = n = 2^k, and
+ * U = (H_28 kron H_{2^k}) / sqrt(n) when n = 28 * 2^k (Llama-3's 14336 and 28672), H_28 from
+ * Paley's second construction at q = 13.  Since U is orthogonal, A W^T = (A U)(W U)^T: the
+ * rotation spreads outlier channels before nq_encode.
+ *   x    device, rows x cols of x_dtype, row i at x + i * ld_x (16-byte aligned rows);
+ *   y    device fp32 rows x cols, row i at y + i * ld_y (16-byte aligned rows); may not
+ *        overlap x.
+ * Supported: cols = 2^k or 28 * 2^k with 2^k >= 8 and cols <= 32768, else
+ * NQ_ERR_UNSUPPORTED.  Arithmetic: fp32 fast Walsh-Hadamard transform (stages h = 1, 2, 4, ...
+ * along each length-2^k segment), then for 28 * 2^k the H_28 sums in index order, then one
+ * multiplication by fl32(1 / sqrt(n)).  rows == 0 is a no-op. */
+nq_status nq_rotate(const void* x, nq_dtype x_dtype, int64_t rows, int64_t cols, int64_t ld_x,
+                    float* y, int64_t ld_y, void* hip_stream);
+
 /* Workspace bytes nq_matmul_ex needs for an M x N x K product (0 when M or N is 0; -1 for
  * an invalid K). */
 int64_t nq_matmul_workspace_size(int64_t M, int64_t N, int64_t K);

@@ -23,4 +23,5 @@ from .binding import (  # noqa: F401
     matmul_workspace_size,
     nq_beta_words,
     nq_codes_words,
+    rotate,
 )

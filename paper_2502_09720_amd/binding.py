@@ -53,6 +53,8 @@ def library():
                                      f32p, i64, vp, i64, vp]
         lib.nq_matmul_stages.argtypes = [ctypes.c_int32, pp, u32p, u32p, f32p, i64, pp, u32p,
                                          u32p, f32p, i64, i64, f32p, i64, vp, i64, vp]
+        lib.nq_rotate.argtypes = [vp, ctypes.c_int, i64, i64, i64, f32p, i64, vp]
+        lib.nq_rotate.restype = ctypes.c_int
         lib.nq_matmul_workspace_size.argtypes = [i64, i64, i64]
         lib.nq_matmul_workspace_size.restype = i64
         for f in ("nq_encode", "nq_decode", "nq_matmul", "nq_matmul_ex", "nq_matmul_stages"):
@@ -200,6 +202,21 @@ def matmul(a, w, stream=None, out=None, workspace=None, stages=STAGE_DECODE | ST
         _check(lib.nq_matmul_ex(*args))
     else:
         _check(lib.nq_matmul_stages(stages | (CONTRACT_INT8 if int8 else 0), *args))
+    return out
+
+
+def rotate(x, out=None, stream=None):
+    """nq_rotate: y = x U in fp32 for every row of a 2-D cuda tensor (Sec. 5 Hadamard
+    rotation; cols = 2^k or 28 * 2^k, at most 32768)."""
+    import torch
+    if x.dim() != 2 or x.stride(1) != 1 or not x.is_cuda:
+        raise ValueError("x must be a 2-D cuda tensor with unit column stride")
+    rows, cols = x.shape
+    if out is None:
+        out = torch.empty(rows, cols, dtype=torch.float32, device=x.device)
+    _check(library().nq_rotate(ctypes.c_void_p(x.data_ptr()), _dtype_code(x.dtype), rows, cols,
+                               x.stride(0), ctypes.c_void_p(out.data_ptr()), out.stride(0),
+                               _stream(stream)))
     return out
 
 

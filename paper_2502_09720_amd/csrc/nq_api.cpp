@@ -160,6 +160,38 @@ static nq_status check_matmul(const nq_params* pa, const uint32_t* a_codes,
   return NQ_OK;
 }
 
+nq_status nq_rotate(const void* x, nq_dtype x_dtype, int64_t rows, int64_t cols, int64_t ld_x,
+                    float* y, int64_t ld_y, void* hip_stream) {
+  const char* who = "nq_rotate";
+  if (x_dtype != NQ_F32 && x_dtype != NQ_F16 && x_dtype != NQ_BF16)
+    return fail(NQ_ERR_UNSUPPORTED, "%s: unsupported input dtype %d", who, (int)x_dtype);
+  int p = 0;
+  if (cols < 8 || nq::rotation_split(cols, p) == 0)
+    return fail(NQ_ERR_UNSUPPORTED, "%s: cols=%lld is not 2^k or 28 * 2^k (2^k >= 8, <= %d)",
+                who, (long long)cols, nq::kRotateMaxCols);
+  if (rows < 0 || rows >= kMaxRows)
+    return fail(NQ_ERR_INVALID_ARG, "%s: rows=%lld outside [0, 2^31)", who, (long long)rows);
+  if (ld_x < cols || ld_y < cols) return fail(NQ_ERR_INVALID_ARG, "%s: ld < cols", who);
+  if (rows == 0) return ok();
+  if (!x || !y) return fail(NQ_ERR_INVALID_ARG, "%s: NULL array pointer", who);
+  if (!aligned16(x) || (ld_x * (int64_t)dtype_size(x_dtype)) % 16 != 0 || !aligned16(y) ||
+      (ld_y * 4) % 16 != 0)
+    return fail(NQ_ERR_INVALID_ARG, "%s: rows must be 16-byte aligned", who);
+  const char* xb = (const char*)x;
+  const char* yb = (const char*)y;
+  const int64_t xbytes = ((rows - 1) * ld_x + cols) * (int64_t)dtype_size(x_dtype);
+  const int64_t ybytes = ((rows - 1) * ld_y + cols) * 4;
+  if (xb < yb + ybytes && yb < xb + xbytes)
+    return fail(NQ_ERR_INVALID_ARG, "%s: x and y overlap", who);
+  static std::once_flag attr_once;
+  static hipError_t attr_err = hipSuccess;
+  std::call_once(attr_once, [] { attr_err = nq::rotate_set_attributes(); });
+  if (attr_err != hipSuccess) return hip_status(attr_err, who);
+  return hip_status(nq::launch_rotate(x, (int)x_dtype, rows, (int)cols, ld_x, y, ld_y,
+                                      (hipStream_t)hip_stream),
+                    who);
+}
+
 int64_t nq_matmul_workspace_size(int64_t M, int64_t N, int64_t K) {
   if (M < 0 || N < 0 || K < 8 || K % 8 || K > kMaxCols) return -1;
   if (M == 0 || N == 0) return 0;

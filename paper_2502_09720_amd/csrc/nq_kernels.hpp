@@ -56,6 +56,14 @@ hipError_t launch_matmul_decode_once(int stages, bool i8, const MatmulOperand& A
                                      float scale, void* ws, hipStream_t st);
 hipError_t gemm_set_attributes();
 
+// Hadamard rotation of rows (nq_rotate): columns 2^k or 28 * 2^k (2^k >= 8), at most this.
+constexpr int kRotateMaxCols = 32768;
+// m (1 or 28, 0 if unsupported) and p = n / m
+int rotation_split(int64_t n, int& p);
+hipError_t rotate_set_attributes();
+hipError_t launch_rotate(const void* x, int dtype, int64_t rows, int n, int64_t ld_x, float* y,
+                         int64_t ld_y, hipStream_t st);
+
 // M at or below this uses the skinny kernel; above it, decode-once.
 constexpr int64_t kFusedMaxM = 64;
 

@@ -190,3 +190,22 @@ def test_params_layout():
     from paper_2502_09720_amd.binding import _Params
     assert ctypes.sizeof(_Params) == 24
     assert _Params.base.offset == 8 and _Params.decoder.offset == 16
+
+
+@pytest.mark.parametrize("case", [
+    dict(cols=24), dict(cols=11008), dict(cols=65536), dict(cols=4), dict(dtype=5),
+    dict(rows=-1), dict(ld=8), dict(y=NULL), dict(x=ctypes.c_void_p(0x1004)),
+    dict(y=ctypes.c_void_p(0x1000)),                 # y overlaps x
+])
+def test_rotate_rejects(lib, case):
+    args = dict(rows=4, cols=64, ld=64, x=FAKE, y=ctypes.c_void_p(0x100000), dtype=0)
+    args.update(case)
+    st = lib.nq_rotate(args["x"], args["dtype"], args["rows"], args["cols"], args["ld"],
+                       args["y"], args["ld"] if args["ld"] >= 64 else 64, S)
+    assert st in (1, 2)
+    assert lib.nq_last_error()
+
+
+def test_rotate_zero_rows_is_noop(lib):
+    assert lib.nq_rotate(NULL, 0, 0, 4096, 4096, NULL, 4096, S) == 0
+    assert lib.nq_rotate(NULL, 0, 0, 14336, 14336, NULL, 14336, S) == 0

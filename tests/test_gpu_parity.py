@@ -459,3 +459,62 @@ def test_matmul_parity_nestquantm(nq, case):
     g = got.cpu().numpy().astype(np.float64)
     rel = np.linalg.norm(g - C) / max(np.linalg.norm(C), 1e-300)
     assert rel <= (1e-6 if i8 else MATMUL_RTOL), f"relative Frobenius error {rel}"
+
+
+# ------------------------------------------------------------------------------------------
+# Hadamard rotation (Sec. 5) and rotate-then-encode
+# ------------------------------------------------------------------------------------------
+
+ROTATE_CASES = [
+    # (seed, rows, cols, dtype, dist)
+    (60, 37, 8, "f32", "normal"),
+    (61, 300, 128, "f16", "normal"),
+    (62, 17, 1024, "bf16", "t4"),
+    (63, 9, 4096, "bf16", "t4"),
+    (64, 5, 32768, "f32", "normal"),
+    (65, 11, 224, "f32", "normal"),
+    (66, 7, 1792, "bf16", "normal"),
+    (67, 4, 14336, "bf16", "normal"),
+    (68, 3, 28672, "f16", "normal"),
+]
+
+
+@pytest.mark.parametrize("case", ROTATE_CASES, ids=lambda c: f"{c[1]}x{c[2]}-{c[3]}")
+def test_rotate_parity(nq, case):
+    """nq_rotate equals the oracle's fp32 transform bit for bit (same operation order)."""
+    torch = __import__("torch")
+    from oracle import rotation
+    seed, rows, cols, dtype, dist = case
+    store, x32 = workloads.random_rows(seed, rows, cols, dtype=dtype, dist=dist)
+    x32[0, :] = 0.0
+    if dtype == "f32":
+        store[0, :] = 0.0
+    else:
+        store[0, :] = 0
+    got = nq.rotate(to_device(store, dtype))
+    torch.cuda.synchronize()
+    want = rotation.rotate_rows(x32)
+    m = first_mismatch(got.cpu().numpy().view(np.uint32), want.view(np.uint32))
+    assert m is None, m
+
+
+def test_rotate_then_encode_parity(nq):
+    """Outlier columns, rotated, then coded: codes bit-exact against the oracle's rotation
+    followed by its encoder, and the rotation cuts the all-overload blocks."""
+    torch = __import__("torch")
+    from oracle import rotation
+    rng = np.random.default_rng(69)
+    x = rng.standard_normal((64, 14336))
+    x[:, rng.choice(14336, 143, replace=False)] *= 20.0
+    store, x32 = workloads.round_to(x, "bf16")
+    y = nq.rotate(to_device(store, "bf16"))
+    got = nq.encode(y, q=14, k=4)
+    torch.cuda.synchronize()
+    yr = rotation.rotate_rows(x32)
+    oc, ob, os_ = oracle_encode(yr, 14, 4)
+    assert first_mismatch(u32(got.codes, oc.shape), oc) is None
+    assert first_mismatch(u32(got.beta, ob.shape), ob) is None
+    assert np.array_equal(got.scales.cpu().numpy().view(np.uint32), os_.view(np.uint32))
+    _, t_plain, _ = nestquant.quantize_rows(x32[:8], 14, 4)
+    _, t_rot, _ = nestquant.quantize_rows(yr[:8], 14, 4)
+    assert (t_rot == 4).mean() < (t_plain == 4).mean()
