@@ -15,9 +15,12 @@ It shares no code with the GPU path.  It is written from the paper
                    strategies (App. F), decoding, the dot product of two coded vectors
                    (Alg. 4) and the coded matrix product built from it;
 * ``layout``    -- the packed storage of codes, beta indices and scales;
-* ``theory``    -- closed forms the paper states (rate, Gamma(R) bound, NSM of E8).
+* ``theory``    -- closed forms the paper states (rate, Gamma(R) bound, NSM of E8);
+* ``rotation``  -- the Hadamard rotation of rows (Sec. 5);
+* ``beta_dp``   -- the choice of the beta set (App. F, Alg. 6) and the synthetic
+                   rate-distortion frontier (Sec. 6.1).
 
 Every function that the paper does not fix completely states the reading it takes.
 """
 
-from . import lattice, voronoi, nestquant, layout, theory  # noqa: F401
+from . import lattice, voronoi, nestquant, layout, theory, rotation, beta_dp  # noqa: F401

@@ -9,7 +9,8 @@ Paper passages followed:
   coefficients beta_1 < ... < beta_k and keep the index of the one used.
 * App. F, "First-beta": use the smallest beta that does not overload.  "Opt-beta" (the
   literal loop of Alg. 3): try every beta and keep the one with the smallest squared error
-  (the first one on an exact tie, since Alg. 3 replaces only on a strict improvement).
+  (the first one on an exact tie, since Alg. 3 replaces only on a strict improvement); the
+  error is ||beta_t X2_t / 2 - x / r||^2 in fp64, squares added in coordinate order.
 * Sec. 3 "Overload avoidance via union of Voronoi codes": the codebook is the union of
   the k scaled Voronoi codes; the rate is log2(q) + log2(k)/8 bits per entry.
 * Sec. 4.2, Alg. 4 (Dot product): sum over blocks of <p1, p2> beta_{B1} beta_{B2}.
@@ -120,6 +121,18 @@ def multipliers(r32, k, base):
 # Block quantizer: one 8-vector at k scales (Alg. 3 inner loop, App. F strategies)
 # ----------------------------------------------------------------------------------------
 
+def opt_errors(X2, v64, betas):
+    """Opt-beta's reconstruction errors ||beta_t X2_t / 2 - v||^2 for every block and beta,
+    (nb, k), in fp64 with the eight squares added left to right (a fixed order, so that the
+    comparison between betas is reproducible)."""
+    b = np.asarray(betas, dtype=np.float64)
+    err = np.zeros(X2.shape[:2], dtype=np.float64)
+    for l in range(8):
+        d = b[None, :] * X2[:, :, l] / 2.0 - v64[:, None, l]
+        err = err + d * d
+    return err
+
+
 def quantize_blocks(xb32, mult32, q, strategy="first", v64=None, betas=None, decoder="full"):
     """Quantize 8-blocks with the union of k scaled Voronoi codes.
 
@@ -147,8 +160,7 @@ def quantize_blocks(xb32, mult32, q, strategy="first", v64=None, betas=None, dec
         ok = ~over
         t_sel = np.where(ok.any(axis=1), np.argmax(ok, axis=1), k - 1)
     elif strategy == "opt":
-        b = np.asarray(betas, dtype=np.float64)
-        err = ((b[None, :, None] * X2 / 2.0 - v64[:, None, :]) ** 2).sum(axis=2)
+        err = opt_errors(X2, v64, betas)
         t_sel = np.argmin(err, axis=1)                        # first minimum
     else:
         raise ValueError(strategy)
