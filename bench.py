@@ -344,6 +344,19 @@ def main():
     except nq.NQError:
         pass                                  # K not 2^k or 28 * 2^k
 
+    # Opt-beta encoding of A (App. F; every beta tried, a strategy of the encoder that the
+    # step does not use)
+    eo = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    for i in range(args.warmup):
+        nq.encode(As[i % nbuf], q=q, k=k, out=(codes, beta, scales), strategy=nq.OPT_BETA)
+    for i in range(args.steps):
+        eo[i][0].record()
+        nq.encode(As[i % nbuf], q=q, k=k, out=(codes, beta, scales), strategy=nq.OPT_BETA)
+        eo[i][1].record()
+    torch.cuda.synchronize()
+    oms = float(np.mean([e[0].elapsed_time(e[1]) for e in eo]))
+    opt = {"ms": oms, "GBps": enc_bytes / (oms * 1e-3) / 1e9}
+
     # the exact int8 contraction (a variant of the product, not part of the step)
     i8 = None
     if k * q <= 63:
@@ -424,6 +437,7 @@ def main():
             "rate_bits_per_entry": float(np.log2(q) + np.log2(k) / 8),
             "nq_matmul_int8_variant": i8,
             "nq_rotate_A": rot,
+            "nq_encode_A_opt_beta": opt,
         },
         "roofline": roofline,
         "cpu_baseline": None,

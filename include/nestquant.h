@@ -59,6 +59,16 @@ typedef enum { NQ_F32 = 0, NQ_F16 = 1, NQ_BF16 = 2 } nq_dtype;
  *                    counts as overloaded when this decoder does not reproduce it. */
 typedef enum { NQ_DECODER_FULL = 0, NQ_DECODER_M = 1 } nq_decoder;
 
+/* How the encoder picks one of the k betas for a block (App. F).  Both give the same code
+ * format; decoding and the matrix product do not look at it.
+ *   NQ_FIRST_BETA  the smallest beta that does not overload (t = k if all do);
+ *   NQ_OPT_BETA    every beta is tried and the one whose reconstruction
+ *                  beta_t * X2_t / 2 is nearest to the normalized block x / r is kept: the
+ *                  error is sum over l = 0..7, in that order, of d_l^2 with
+ *                  d_l = fl64(fl64(beta_t * X2_t,l) / 2 - fl64(x_l / r)), every step
+ *                  rounded in fp64, and the first t with the least error wins. */
+typedef enum { NQ_FIRST_BETA = 0, NQ_OPT_BETA = 1 } nq_strategy;
+
 /* Quantizer parameters (Sec. 4.2, App. F):
  *   q        nesting ratio, 2 <= q <= 16 (codes are nibbles);
  *   k        number of betas, 1 <= k <= 4 (2-bit beta indices);
@@ -66,17 +76,17 @@ typedef enum { NQ_DECODER_FULL = 0, NQ_DECODER_M = 1 } nq_decoder;
  *            sqrt(cols) / base < 2^21 (bounds the lattice input |y| <= sqrt(cols) / base).
  *            The paper's grid "k betas uniform on [0, 10] / q" is base = 10 / (k q);
  *   decoder  an nq_decoder value (0 = Alg. 2 / Alg. 5);
- *   reserved must be 0.
+ *   strategy an nq_strategy value (0 = First-beta); used by nq_encode only.
  * Codes made with one decoder must be decoded and multiplied with the same one. */
 typedef struct {
   int32_t q;
   int32_t k;
   double base;
   int32_t decoder;
-  int32_t reserved;
+  int32_t strategy;
 } nq_params;
 
-/* Alg. 3 + First-beta (App. F) on each row of x.
+/* Alg. 3 with the beta strategy p->strategy (App. F) on each row of x.
  *   x        device, rows x cols of dtype x_dtype (NQ_F32, NQ_F16 or NQ_BF16), row i at
  *            x + i*ld_x elements; ld_x >= cols; cols % 8 == 0, 8 <= cols <= 65536.
  *   codes    device, nq_codes_words(rows, cols) uint32 (output);
@@ -85,8 +95,9 @@ typedef struct {
  * Per row: r = RMS; for every 8-block, for t = 1..k the block y = fl32(x * c_t) with
  * c_t = fl32(1 / fl64(r * fl64(t * base))) is rounded to the nearest E8 point (Alg. 5;
  * ties: exact halves round down, lowest index on argmin/argmax ties, equal D8 / D8+1/2
- * distances pick D8+1/2); the first t whose point survives decode(encode(.)) (no
- * overload, Sec. 4.1) is kept, else t = k.  A zero row gives r = 0, codes 0, index 0.
+ * distances pick D8+1/2).  First-beta keeps the first t whose point survives
+ * decode(encode(.)) (no overload, Sec. 4.1), else t = k; Opt-beta keeps the t of least
+ * reconstruction error (nq_strategy).  A zero row gives r = 0, codes 0, index 0.
  * Non-finite inputs give unspecified (but in-range) codes. */
 nq_status nq_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t rows,
                     int64_t cols, int64_t ld_x, uint32_t* codes, uint32_t* beta_idx,

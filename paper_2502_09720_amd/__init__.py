@@ -10,6 +10,8 @@ from .binding import (  # noqa: F401
     CONTRACT_INT8,
     DECODER_FULL,
     DECODER_M,
+    FIRST_BETA,
+    OPT_BETA,
     STAGE_CONTRACT,
     STAGE_DECODE,
     Coded,

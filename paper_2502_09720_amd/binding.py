@@ -23,11 +23,13 @@ class NQError(RuntimeError):
 
 class _Params(ctypes.Structure):
     _fields_ = [("q", ctypes.c_int32), ("k", ctypes.c_int32), ("base", ctypes.c_double),
-                ("decoder", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("decoder", ctypes.c_int32), ("strategy", ctypes.c_int32)]
 
 
 DECODER_FULL = 0   # Alg. 2 with the Gosset oracle of Alg. 5
 DECODER_M = 1      # NestQuantM (App. D): parity fixes at the first coordinate
+FIRST_BETA = 0     # App. F: the smallest beta that does not overload
+OPT_BETA = 1       # App. F: the beta of least reconstruction error
 
 
 def library_path():
@@ -84,9 +86,9 @@ def default_base(q, k):
     return 10.0 / (k * q)
 
 
-def _params(q, k, base, decoder=DECODER_FULL):
+def _params(q, k, base, decoder=DECODER_FULL, strategy=FIRST_BETA):
     return _Params(int(q), int(k), float(default_base(q, k) if base is None else base),
-                   int(decoder), 0)
+                   int(decoder), int(strategy))
 
 
 def _stream(stream):
@@ -122,9 +124,11 @@ class Coded(NamedTuple):
     decoder: int = DECODER_FULL
 
 
-def encode(x, q=14, k=4, base=None, stream=None, out=None, decoder=DECODER_FULL):
+def encode(x, q=14, k=4, base=None, stream=None, out=None, decoder=DECODER_FULL,
+           strategy=FIRST_BETA):
     """nq_encode on a 2-D cuda tensor (fp32 / fp16 / bf16, unit stride along rows).
-    ``decoder`` is the decoder the code is defined with (DECODER_FULL or DECODER_M)."""
+    ``decoder`` is the decoder the code is defined with (DECODER_FULL or DECODER_M);
+    ``strategy`` picks the beta of each block (FIRST_BETA or OPT_BETA)."""
     import torch
     if x.dim() != 2 or x.stride(1) != 1 or not x.is_cuda:
         raise ValueError("x must be a 2-D cuda tensor with unit column stride")
@@ -139,7 +143,7 @@ def encode(x, q=14, k=4, base=None, stream=None, out=None, decoder=DECODER_FULL)
         scales = torch.empty(rows, dtype=torch.float32, device=x.device)
     else:
         codes, beta, scales = out
-    p = _params(q, k, base, decoder)
+    p = _params(q, k, base, decoder, strategy)
     _check(lib.nq_encode(ctypes.byref(p), ctypes.c_void_p(x.data_ptr()), _dtype_code(x.dtype),
                          rows, cols, x.stride(0), ctypes.c_void_p(codes.data_ptr()),
                          ctypes.c_void_p(beta.data_ptr()), ctypes.c_void_p(scales.data_ptr()),

@@ -37,7 +37,8 @@ nq_status check_params(const nq_params* p, int64_t cols, const char* who) {
     return fail(NQ_ERR_INVALID_ARG, "%s: base must be finite and > 0", who);
   if (p->decoder != NQ_DECODER_FULL && p->decoder != NQ_DECODER_M)
     return fail(NQ_ERR_INVALID_ARG, "%s: decoder=%d is not an nq_decoder", who, p->decoder);
-  if (p->reserved != 0) return fail(NQ_ERR_INVALID_ARG, "%s: reserved must be 0", who);
+  if (p->strategy != NQ_FIRST_BETA && p->strategy != NQ_OPT_BETA)
+    return fail(NQ_ERR_INVALID_ARG, "%s: strategy=%d is not an nq_strategy", who, p->strategy);
   if (std::sqrt((double)cols) / p->base >= 2097152.0)
     return fail(NQ_ERR_INVALID_ARG, "%s: base too small for cols=%lld (sqrt(cols)/base >= 2^21)",
                 who, (long long)cols);
@@ -86,7 +87,7 @@ const char* nq_status_string(nq_status s) {
 
 const char* nq_last_error(void) { return g_last_error; }
 
-int32_t nq_version(void) { return 200; }
+int32_t nq_version(void) { return 300; }
 
 nq_status nq_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t rows,
                     int64_t cols, int64_t ld_x, uint32_t* codes, uint32_t* beta_idx,
@@ -111,6 +112,7 @@ nq_status nq_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t
   a.m2q = nq::magic_2q(p->q);
   a.mq = nq::magic_q(p->q);
   a.decoder = p->decoder;
+  a.strategy = p->strategy;
   for (int t = 0; t < 4; ++t) a.beta[t] = (double)(t + 1) * p->base;
   return hip_status(nq::launch_encode(x, (int)x_dtype, rows, (int)cols, ld_x, a, codes, beta_idx,
                                       scales, (hipStream_t)hip_stream),

@@ -1,4 +1,5 @@
-// NestQuant row encoder (Sec. 4.2, Alg. 3 with the First-beta strategy of App. F).
+// NestQuant row encoder (Sec. 4.2, Alg. 3 with the First-beta or Opt-beta strategy of
+// App. F).
 //
 // One lane per 8-entry block.  A row is handled by a group of LANES lanes (a power of two,
 // 8 <= LANES <= 1024): several rows share a 256-thread workgroup when LANES <= 64, and a
@@ -208,6 +209,50 @@ __device__ __forceinline__ void encode_block(const float (&v)[8], const float (&
   word = encode_codes(P, a.q, a.rq, a.mq);
 }
 
+// Opt-beta for one block (App. F): every beta is tried; the code of the nearest point of
+// y_t = fl32(x c_t) is decoded (Alg. 2 with the code's decoder) to X2_t and compared with
+// the normalized block x / r: err_t = sum over l = 0..7, in that order, of d_l^2 with
+// d_l = fl64(beta_t X2_t,l) / 2 - fl64(x_l / r), each step rounded in fp64 (the library is
+// built without contraction).  The first t of least error is kept.
+__device__ __forceinline__ void opt_block(const float (&v)[8], const float (&c)[4], float r,
+                                          const EncodeArgs& a, uint32_t& word, int& tsel) {
+  double xn[8];
+#pragma unroll
+  for (int l = 0; l < 8; ++l) xn[l] = (double)v[l] / (double)r;
+  double best = INFINITY;
+  word = 0u;
+  tsel = 0;
+#pragma unroll 1
+  for (int t = 0; t < a.k; ++t) {
+    const float ct = pick4(c, t);
+    float y[8];
+#pragma unroll
+    for (int l = 0; l < 8; ++l) y[l] = v[l] * ct;
+    int P[8];
+    nearest_e8(y, P);
+    const uint32_t w = encode_codes(P, a.q, a.rq, a.mq);
+    uint32_t X2[4];
+    if (a.decoder) {
+      decode_word_pk<true>(w, a.q, a.m2q, X2);
+    } else {
+      decode_word_pk<false>(w, a.q, a.m2q, X2);
+    }
+    const double bt = a.beta[t];
+    double err = 0.0;
+#pragma unroll
+    for (int l = 0; l < 8; ++l) {
+      const int x2 = (int)(short)((X2[l >> 1] >> (16 * (l & 1))) & 0xFFFFu);
+      const double d = bt * (double)x2 / 2.0 - xn[l];
+      err = err + d * d;
+    }
+    if (err < best) {
+      best = err;
+      word = w;
+      tsel = t;
+    }
+  }
+}
+
 // Exact RN32(sqrt(S / n)) from a double-double S and a candidate r within a few ulps.
 __device__ __forceinline__ float exact_rms(double hi, double lo, double n, float r) {
   for (int it = 0; it < 4; ++it) {
@@ -333,7 +378,13 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_kernel(
     }
     uint32_t word = 0;
     int tsel = 0;
-    if (mine && coded) encode_block(*reinterpret_cast<float(*)[8]>(vb), c, a, word, tsel);
+    if (mine && coded) {
+      if (a.strategy) {
+        opt_block(*reinterpret_cast<float(*)[8]>(vb), c, r, a, word, tsel);
+      } else {
+        encode_block(*reinterpret_cast<float(*)[8]>(vb), c, a, word, tsel);
+      }
+    }
     if (mine) crow[j] = word;
     // two-bit beta indices: OR over the 16 consecutive blocks of one word
     uint32_t bits = mine ? ((uint32_t)tsel << (2 * (j & 15))) : 0u;
@@ -362,6 +413,7 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_kernel(
 // the point's exact root bound says it overloads (start again at the next beta) or lies on
 // the cell boundary (the literal test decides).  Those slots (about 12-15% on Gaussian-like and heavy-tailed
 // rows) are queued, and phase 2 finishes them with every lane of the workgroup busy.
+// With Opt-beta, phase 1 evaluates every beta of every slot (opt_block) and queues nothing.
 // Two-bit beta indices are staged in LDS and packed into words at the end.
 // ---------------------------------------------------------------------------------------
 template <int LANES, int BPT>
@@ -598,6 +650,23 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
     const int64_t row = row0 + rw;
     const bool valid = row < rows && j < nb;
     const bool coded = valid && rrow[cw][rw] != 0.0f;
+    if (a.strategy) {
+      // Opt-beta: every beta of every block is evaluated here (nothing is queued)
+      if (valid) {
+        uint32_t word = 0u;
+        int tsel = 0;
+        if (coded) {
+          float v[8], c[4];
+          unpack_raw<T>(rawl[wave][sl], v);
+#pragma unroll
+          for (int t = 0; t < 4; ++t) c[t] = crow[cw][rw][t];
+          opt_block(v, c, rrow[cw][rw], a, word, tsel);
+        }
+        codes_w[rw * nb + j] = word;
+        tsl[wave][sl] = (uint8_t)tsel;
+      }
+      continue;
+    }
     bool queued = false;
     int start = 0, t0 = 0;
     int P[8];

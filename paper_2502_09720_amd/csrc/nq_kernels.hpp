@@ -13,6 +13,7 @@ struct EncodeArgs {
   uint32_t m2q;    // ceil(2^16 / (2q)): floor(X / 2q) = (X * m2q) >> 16 for 0 <= X < 2^11
   uint32_t mq;     // ceil(2^20 / q): floor(u / q) = (u * mq) >> 20 for 0 <= u < 2048 q
   int decoder;     // 0: Alg. 2 / Alg. 5, 1: NestQuantM (App. D)
+  int strategy;    // 0: First-beta, 1: Opt-beta (App. F)
   double beta[4];  // fl64(t * base), t = 1..4
 };
 

@@ -28,9 +28,9 @@ def u32(t, shape=None):
     return a if shape is None else a.reshape(shape)
 
 
-def oracle_encode(x32, q, k, base=None, decoder="full"):
+def oracle_encode(x32, q, k, base=None, decoder="full", strategy="first"):
     """Packed oracle codes (rows, nb), beta words (rows, nbw) and scales (rows,)."""
-    codes, t, r = nestquant.quantize_rows(x32, q, k, base, decoder=decoder)
+    codes, t, r = nestquant.quantize_rows(x32, q, k, base, strategy=strategy, decoder=decoder)
     return layout.pack_codes(codes), layout.pack_beta(t), r
 
 

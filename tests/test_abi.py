@@ -57,14 +57,14 @@ NULL = ctypes.c_void_p(0)
 S = ctypes.c_void_p(0)
 
 
-def _pd(decoder, reserved=0):
+def _pd(decoder, strategy=0):
     p = _p()
-    p.decoder, p.reserved = decoder, reserved
+    p.decoder, p.strategy = decoder, strategy
     return p
 
 
 @pytest.mark.parametrize("case", [
-    dict(p=_pd(2)), dict(p=_pd(-1)), dict(p=_pd(0, 1)),
+    dict(p=_pd(2)), dict(p=_pd(-1)), dict(p=_pd(0, 2)), dict(p=_pd(0, -1)),
     dict(p=None), dict(p=_p(q=1)), dict(p=_p(q=17)), dict(p=_p(k=0)), dict(p=_p(k=5)),
     dict(p=_p(base=0.0)), dict(p=_p(base=-1.0)), dict(p=_p(base=float("nan"))),
     dict(p=_p(base=1e-9)), dict(cols=12), dict(cols=0), dict(cols=65544), dict(rows=-1),
@@ -185,11 +185,12 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
 
 
 def test_params_layout():
-    """nq_params is {int32 q, int32 k, double base, int32 decoder, int32 reserved}: 24 bytes,
-    base at offset 8, decoder at 16."""
+    """nq_params is {int32 q, int32 k, double base, int32 decoder, int32 strategy}: 24 bytes,
+    base at offset 8, decoder at 16, strategy at 20."""
     from paper_2502_09720_amd.binding import _Params
     assert ctypes.sizeof(_Params) == 24
     assert _Params.base.offset == 8 and _Params.decoder.offset == 16
+    assert _Params.strategy.offset == 20
 
 
 @pytest.mark.parametrize("case", [

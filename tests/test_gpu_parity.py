@@ -31,7 +31,8 @@ def nq():
     return nq
 
 
-def check_encode(nq, store, x32, dtype, q, k, base=None, ld_pad=0, decoder="full"):
+def check_encode(nq, store, x32, dtype, q, k, base=None, ld_pad=0, decoder="full",
+                 strategy="first"):
     torch = __import__("torch")
     rows, cols = x32.shape
     if ld_pad:
@@ -40,13 +41,14 @@ def check_encode(nq, store, x32, dtype, q, k, base=None, ld_pad=0, decoder="full
         xd = to_device(big, dtype)[:, :cols]
     else:
         xd = to_device(store, dtype)
-    got = nq.encode(xd, q=q, k=k, base=base, decoder=0 if decoder == "full" else 1)
+    got = nq.encode(xd, q=q, k=k, base=base, decoder=0 if decoder == "full" else 1,
+                    strategy=nq.FIRST_BETA if strategy == "first" else nq.OPT_BETA)
     torch.cuda.synchronize()
     nb = cols // 8
     gc = u32(got.codes, (rows, nb))
     gb = u32(got.beta, (rows, (nb + 15) // 16))
     gs = got.scales.cpu().numpy()
-    oc, ob, os_ = oracle_encode(x32, q, k, base, decoder)
+    oc, ob, os_ = oracle_encode(x32, q, k, base, decoder, strategy)
     assert first_mismatch(gs.view(np.uint32), os_.view(np.uint32)) is None, \
         "scales: " + first_mismatch(gs.view(np.uint32), os_.view(np.uint32))
     m = first_mismatch(gc, oc)
@@ -129,6 +131,53 @@ def test_encode_outlier_columns(nq):
     store, x32 = workloads.round_to(x, "bf16")
     check_encode(nq, store, x32, "bf16", 14, 4)
     check_encode(nq, store, x32, "bf16", 7, 4)
+
+
+# Opt-beta (App. F): the least-error beta, bit-exact against the oracle's fp64 errors.
+# Cases cover every encoder shape (lane groups of 8 .. 256, the streaming kernel beyond
+# 2048 blocks), heavy tails (overloaded betas decode far away), ties and both decoders.
+OPT_CASES = [c for c in ENCODE_CASES if c[0] in (1, 2, 4, 6, 7, 8, 9, 11, 13, 14, 16)]
+
+
+@pytest.mark.parametrize("case", OPT_CASES, ids=lambda c: f"s{c[0]}-{c[1]}x{c[2]}-{c[3]}-q{c[6]}k{c[7]}")
+def test_encode_opt_beta_parity(nq, case):
+    seed, rows, cols, dtype, dist, scale, q, k = case
+    store, x32 = workloads.random_rows(seed, rows, cols, dtype=dtype, scale=scale, dist=dist)
+    check_encode(nq, store, x32, dtype, q, k, strategy="opt")
+
+
+@pytest.mark.parametrize("decoder", ["full", "m"])
+def test_encode_opt_beta_ties_and_outliers(nq, decoder):
+    x = _tie_rows(77)
+    store, x32 = workloads.round_to(x, "bf16")
+    check_encode(nq, store, x32, "bf16", 16 if decoder == "m" else 14, 4, decoder=decoder,
+                 strategy="opt")
+    store, x32 = workloads.random_rows(41, 24, 1024, dtype="bf16")
+    x = x32.astype(np.float64)
+    x[:, ::97] *= 20.0
+    store, x32 = workloads.round_to(x, "bf16")
+    check_encode(nq, store, x32, "bf16", 16 if decoder == "m" else 14, 4, decoder=decoder,
+                 strategy="opt")
+    check_encode(nq, store, x32, "bf16", 10, 2, base=0.11, decoder=decoder, strategy="opt")
+
+
+def test_encode_opt_beta_differs_from_first_beta(nq):
+    """The two strategies are different functions: on Gaussian rows some blocks take a
+    larger beta under Opt-beta than the first non-overloading one, and the decoded error
+    of Opt-beta is never larger per block."""
+    torch = __import__("torch")
+    store, x32 = workloads.random_rows(42, 64, 1024, dtype="f32")
+    xd = to_device(store, "f32")
+    a = nq.encode(xd, 14, 4, strategy=nq.FIRST_BETA)
+    b = nq.encode(xd, 14, 4, strategy=nq.OPT_BETA)
+    da, db = nq.decode(a), nq.decode(b)
+    torch.cuda.synchronize()
+    assert not np.array_equal(u32(a.beta), u32(b.beta))
+    x = x32.astype(np.float64)
+    ea = ((da.cpu().numpy().astype(np.float64) - x) ** 2).reshape(64, -1, 8).sum(-1)
+    eb = ((db.cpu().numpy().astype(np.float64) - x) ** 2).reshape(64, -1, 8).sum(-1)
+    assert (eb <= ea * (1 + 1e-6) + 1e-12).all()
+    assert eb.sum() < ea.sum()
 
 
 def test_encode_non_finite_rows_are_zero(nq):
