@@ -17,7 +17,8 @@ TEST INFRASTRUCTURE ONLY (see the package docstring).
 * ``first_beta_loss``: the total First-beta error of a given beta subset (what Alg. 6
   minimizes), for checking the DP against brute force.
 * ``synthetic_frontier``: Sec. 6.1's experiment at a small size: for each (q, k) the DP picks
-  k betas from the grid {1/2, 1, ..., 25} / q on sample vectors; the rate is
+  k betas from the grid {1/2, 1, ..., 25} / q on sample vectors, both matrices are coded with
+  them (Alg. 3, First-beta) and multiplied from the codes (Alg. 4); the rate is
   log2 q + H(p) / 8, H the entropy of the betas' usage (the printed formula has the sign of
   the entropy term flipped; read as the entropy), and the error is the root mean squared
   error per entry of A_hat B_hat^T against A B^T for A, B with iid N(0,1) entries, divided by
@@ -36,7 +37,8 @@ from .voronoi import decode, encode_point
 
 
 def block_stats(v64, betas, q, decoder="full"):
-    """(mse (n, m), overload (n, m)) of sample 8-vectors v64 (n, 8) at each beta."""
+    """(mse (n, m), overload (n, m)) of sample 8-vectors v64 (n, 8) at each beta; the eight
+    squares of mse are added in coordinate order."""
     v64 = np.asarray(v64, dtype=np.float64)
     n, m = v64.shape[0], len(betas)
     mse = np.empty((n, m))
@@ -47,7 +49,11 @@ def block_stats(v64, betas, q, decoder="full"):
         P = nearest_e8(y)
         X2 = decode(encode_point(P, q), q, decoder)
         over[:, i] = np.any(X2 != P, axis=1)
-        mse[:, i] = ((b * X2 / 2.0 - v64) ** 2).sum(axis=1)
+        acc = np.zeros(n)
+        for l in range(8):
+            d = b * X2[:, l] / 2.0 - v64[:, l]
+            acc = acc + d * d
+        mse[:, i] = acc
     return mse, over
 
 
@@ -121,36 +127,32 @@ def usage_entropy_bits(t, k):
 
 
 def synthetic_frontier(qs, ks, n=512, dim=1024, calib=10000, seed=0, decoder="full"):
-    """Points (q, k, betas, rate bits per entry, normalized RMSE of A_hat B_hat^T) of Sec. 6.1
-    at a small size: A, B of shape (n, dim) with iid N(0, 1) entries."""
-    from .nestquant import quantize_blocks, row_scale
+    """Points (q, k, mult, rate bits per entry, normalized RMSE of A_hat B_hat^T) of Sec. 6.1
+    at a small size: A, B of shape (n, dim) with iid N(0, 1) entries.  The candidate betas
+    are the grid (1/2) {1, ..., 50} / q, i.e. mult_j = j times base = 1 / (2q); the chosen
+    set is returned as its multiples."""
+    from .nestquant import betas, coded_matmul, quantize_rows
     rng = np.random.default_rng(seed)
     A = rng.standard_normal((n, dim)).astype(np.float32)
     B = rng.standard_normal((n, dim)).astype(np.float32)
     exact = A.astype(np.float64) @ B.astype(np.float64).T
-    grid = np.arange(1, 51) / 2.0
     cal = rng.standard_normal((calib, 8))
+    grid = np.arange(1, 51)
     out = []
     for q in qs:
-        betas_all = grid / q
-        mse, over = block_stats(cal, betas_all, q, decoder)
+        base = 1.0 / (2 * q)
+        mse, over = block_stats(cal, betas(len(grid), base, grid), q, decoder)
         for k in ks:
             idx, _ = dp_betas(mse, over, k)
             if idx is None:
                 continue
-            betas = betas_all[idx]
-            recs, ts = [], []
-            for M in (A, B):
-                r = row_scale(M).astype(np.float64)
-                v = M.astype(np.float64) / r[:, None]
-                mult = np.tile((1.0 / betas).astype(np.float32), (M.size // 8, 1))
-                xb = v.reshape(-1, 8).astype(np.float32)
-                codes, t, _, _ = quantize_blocks(xb, mult, q, "first", decoder=decoder)
-                X2 = decode(codes, q, decoder)
-                rec = (betas[t - 1][:, None] * X2 / 2.0).reshape(M.shape) * r[:, None]
-                recs.append(rec)
-                ts.append(t)
-            rate = math.log2(q) + usage_entropy_bits(np.concatenate(ts), k) / 8.0
-            err = recs[0] @ recs[1].T - exact
-            out.append((q, k, betas, rate, float(np.sqrt((err ** 2).mean() / dim))))
+            mult = grid[idx]
+            ca, ta, ra = quantize_rows(A, q, k, base, decoder=decoder, mult=mult)
+            cb, tb, rb = quantize_rows(B, q, k, base, decoder=decoder, mult=mult)
+            C = coded_matmul(ca, ta, ra, q, base, cb, tb, rb, q, base, decoder, decoder,
+                             mult, mult)
+            rate = math.log2(q) + usage_entropy_bits(np.concatenate([ta.ravel(), tb.ravel()]),
+                                                     k) / 8.0
+            err = C - exact
+            out.append((q, k, mult, rate, float(np.sqrt((err ** 2).mean() / dim))))
     return out

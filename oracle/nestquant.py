@@ -23,7 +23,9 @@ Readings where the paper is silent:
   nearest to the exact value (ties to even); a zero row has r = 0 and is coded as all-zero
   codes with beta index 1.
 * Beta grid.  beta_t = t * base, t = 1..k, with base = 10 / (k q): App. F's table takes the
-  k betas uniform on [0, 10], in the paper's "/q" units (App. G).
+  k betas uniform on [0, 10], in the paper's "/q" units (App. G).  A set chosen by the
+  dynamic program of App. F (from the grid (1/2) {1, ..., 50} / q) is given as integer
+  multiples: beta_t = mult_t * base with mult_1 < ... < mult_k (``mult``; None = 1..k).
 * Lattice input.  The multiplier for beta_t is c_t = fl32(1 / fl64(r * fl64(t * base)))
   (fp64 product, fp64 division, one rounding to fp32) and the block sent to the E8
   quantizer is y = fl32(x * c_t), computed with one fp32 multiply per entry.
@@ -105,15 +107,30 @@ def row_scale(x32):
     return r32
 
 
-def multipliers(r32, k, base):
-    """c_t = fl32(1 / fl64(r * fl64(t * base))) for t = 1..k; shape (rows, k).  Rows with
+def beta_mults(k, mult=None):
+    """The integer multiples m_t of base, t = 1..k (beta_t = m_t * base): 1..k by default."""
+    if mult is None:
+        return np.arange(1, k + 1, dtype=np.int64)
+    m = np.asarray(mult, dtype=np.int64)[:k]
+    if m.shape[0] != k or m[0] < 1 or (np.diff(m) <= 0).any():
+        raise ValueError("mult must hold k strictly increasing positive integers")
+    return m
+
+
+def betas(k, base, mult=None):
+    """beta_t = fl64(m_t * base), t = 1..k."""
+    return beta_mults(k, mult).astype(np.float64) * np.float64(base)
+
+
+def multipliers(r32, k, base, mult=None):
+    """c_t = fl32(1 / fl64(r * fl64(m_t * base))) for t = 1..k; shape (rows, k).  Rows with
     r = 0 get 0 (they are coded as zeros and never multiplied)."""
     r64 = np.asarray(r32, dtype=np.float32).astype(np.float64)
     out = np.zeros((r64.shape[0], k), dtype=np.float32)
     nz = r64 != 0
+    b = betas(k, base, mult)
     for t in range(1, k + 1):
-        beta_t = np.float64(t) * np.float64(base)
-        out[nz, t - 1] = (1.0 / (r64[nz] * beta_t)).astype(np.float32)
+        out[nz, t - 1] = (1.0 / (r64[nz] * b[t - 1])).astype(np.float32)
     return out
 
 
@@ -168,8 +185,9 @@ def quantize_blocks(xb32, mult32, q, strategy="first", v64=None, betas=None, dec
     return codes[rows, t_sel], t_sel + 1, over, P
 
 
-def quantize_rows(x, q, k, base=None, strategy="first", decoder="full"):
+def quantize_rows(x, q, k, base=None, strategy="first", decoder="full", mult=None):
     """Alg. 3 on every row of x (rows, n), n a multiple of 8; x must be fp32-representable.
+    beta_t = mult_t * base (mult None: t * base).
 
     Returns (codes (rows, n/8, 8) int64, t (rows, n/8) int64 in [1, k], r (rows,) fp32).
     """
@@ -183,18 +201,18 @@ def quantize_rows(x, q, k, base=None, strategy="first", decoder="full"):
         raise ValueError("row length must be a multiple of 8")
     nb = n // 8
     r = row_scale(x32)
-    c = multipliers(r, k, base)
+    c = multipliers(r, k, base, mult)
     codes = np.zeros((rows, nb, 8), dtype=np.int64)
     t = np.ones((rows, nb), dtype=np.int64)
     nz = r != 0
     if nz.any():
         xb = x32[nz].reshape(-1, 8)
         mb = np.repeat(c[nz], nb, axis=0)
-        v64 = betas = None
+        v64 = bts = None
         if strategy == "opt":
             v64 = (x32[nz].astype(np.float64) / r[nz].astype(np.float64)[:, None]).reshape(-1, 8)
-            betas = np.arange(1, k + 1) * np.float64(base)
-        cb, tb, _, _ = quantize_blocks(xb, mb, q, strategy, v64, betas, decoder)
+            bts = betas(k, base, mult)
+        cb, tb, _, _ = quantize_blocks(xb, mb, q, strategy, v64, bts, decoder)
         codes[nz] = cb.reshape(-1, nb, 8)
         t[nz] = tb.reshape(-1, nb)
     return codes, t, r
@@ -209,42 +227,53 @@ def decoded_points(codes, q, decoder="full"):
     return decode(codes, q, decoder)
 
 
-def decode_rows(codes, t, r, q, base, decoder="full"):
-    """Reconstruction x_hat = r * beta_t * p = r * base * t * X2 / 2 in fp64; (rows, n)."""
+def _mult_of(t, mult):
+    """m_t for an array of beta indices t (1-based): t itself, or the table mult."""
+    t = np.asarray(t, dtype=np.int64)
+    if mult is None:
+        return t
+    return beta_mults(len(mult), mult)[t - 1]
+
+
+def decode_rows(codes, t, r, q, base, decoder="full", mult=None):
+    """Reconstruction x_hat = r * beta_t * p = r * base * m_t * X2 / 2 in fp64; (rows, n)."""
     X2 = decode(codes, q, decoder).astype(np.float64)       # (rows, nb, 8)
     scale = (np.asarray(r, np.float32).astype(np.float64)[:, None] * float(base)
-             * np.asarray(t, np.float64) / 2.0)
+             * _mult_of(t, mult).astype(np.float64) / 2.0)
     return (X2 * scale[:, :, None]).reshape(codes.shape[0], -1)
 
 
-def dot_coded(c1, t1, r1, q1, base1, c2, t2, r2, q2, base2):
+def dot_coded(c1, t1, r1, q1, base1, c2, t2, r2, q2, base2, mult1=None, mult2=None):
     """Alg. 4 for two coded vectors (blocks (nb, 8)): sum_j <p1_j, p2_j> beta1_j beta2_j,
-    times the row scales r1 * r2 that Alg. 4 leaves out.  Plain loop, exact rationals."""
+    times the row scales r1 * r2 that Alg. 4 leaves out.  Plain loop, exact rationals
+    (beta = base * m_t taken as exact rationals, not as the rounded fp64 betas)."""
     p1 = decode(np.asarray(c1), q1)
     p2 = decode(np.asarray(c2), q2)
+    m1 = _mult_of(t1, mult1)
+    m2 = _mult_of(t2, mult2)
     ans = Fraction(0)
     for j in range(p1.shape[0]):
         ip = Fraction(int(np.dot(p1[j], p2[j])), 4)           # <X2_1, X2_2> / 4 = <p1, p2>
-        ans += ip * Fraction(base1) * int(t1[j]) * Fraction(base2) * int(t2[j])
+        ans += ip * Fraction(base1) * int(m1[j]) * Fraction(base2) * int(m2[j])
     return float(ans * Fraction(float(r1)) * Fraction(float(r2)))
 
 
-def integer_tiles(codes, t, q, decoder="full"):
-    """T = t * X2 per entry (integers, |T| <= 2q k), shape (rows, n)."""
+def integer_tiles(codes, t, q, decoder="full", mult=None):
+    """T = m_t * X2 per entry (integers, |T| <= 2q m_k), shape (rows, n)."""
     X2 = decode(codes, q, decoder)
-    return (X2 * np.asarray(t)[:, :, None]).reshape(codes.shape[0], -1)
+    return (X2 * _mult_of(t, mult)[:, :, None]).reshape(codes.shape[0], -1)
 
 
 def coded_matmul(a_codes, a_t, a_r, qa, base_a, w_codes, w_t, w_r, qw, base_w,
-                 decoder_a="full", decoder_w="full"):
+                 decoder_a="full", decoder_w="full", mult_a=None, mult_w=None):
     """C = A_hat W_hat^T from the two coded operands (Alg. 4 for every row pair).
 
-    C_ij = r_Ai r_Wj base_A base_W / 4 * sum_blocks <t_A X2_A, t_W X2_W>.  The integer
+    C_ij = r_Ai r_Wj base_A base_W / 4 * sum_blocks <m_A X2_A, m_W X2_W>.  The integer
     sums are formed with an fp64 matrix product, which is exact because every partial sum
     is an integer below 2^53.  Returns fp64 (M, N).
     """
-    TA = integer_tiles(a_codes, a_t, qa, decoder_a).astype(np.float64)
-    TW = integer_tiles(w_codes, w_t, qw, decoder_w).astype(np.float64)
+    TA = integer_tiles(a_codes, a_t, qa, decoder_a, mult_a).astype(np.float64)
+    TW = integer_tiles(w_codes, w_t, qw, decoder_w, mult_w).astype(np.float64)
     bound = float(np.abs(TA).max(initial=0)) * float(np.abs(TW).max(initial=0)) * TA.shape[1]
     assert bound < 2.0 ** 53, "integer sums would not be exact in fp64"
     S = TA @ TW.T

@@ -138,6 +138,60 @@ def test_first_beta_rule(rng):
     assert np.all((codes >= 0) & (codes < q))
 
 
+def test_beta_multiples_scaled_grid_is_the_same_code():
+    """beta_t = m_t * base with m_t = 4 t and base / 4 is the uniform grid t * base exactly
+    (a power-of-two rescaling), so the codes, indices and scales are identical."""
+    from workloads import random_rows
+    _, x = random_rows(14, 24, 256, dtype="bf16", dist="t4")
+    base = nestquant.default_base(14, 4)
+    c0, t0, r0 = nestquant.quantize_rows(x, 14, 4)
+    c1, t1, r1 = nestquant.quantize_rows(x, 14, 4, base / 4, mult=(4, 8, 12, 16))
+    assert np.array_equal(c0, c1) and np.array_equal(t0, t1) and np.array_equal(r0, r1)
+    d0 = nestquant.decode_rows(c0, t0, r0, 14, base)
+    d1 = nestquant.decode_rows(c1, t1, r1, 14, base / 4, mult=(4, 8, 12, 16))
+    assert np.array_equal(d0, d1)
+
+
+@pytest.mark.parametrize("mult,q", [((6, 8, 10, 15), 16), ((3, 5, 9), 14), ((7,), 7)])
+def test_first_beta_rule_with_beta_multiples(mult, q):
+    """With an arbitrary increasing beta set, First-beta keeps the first beta whose point
+    survives decode(encode(.)), re-derived here block by block from the definition."""
+    from workloads import random_rows
+    _, x = random_rows(15 + q, 16, 256, dtype="f32", dist="t4")
+    k, base = len(mult), 1.0 / (2 * q)
+    codes, t, r = nestquant.quantize_rows(x, q, k, base, mult=mult)
+    xb, cb, tb = x.reshape(-1, 8), codes.reshape(-1, 8), t.reshape(-1)
+    rb = np.repeat(r, 32)
+    for i in range(0, xb.shape[0], 5):
+        pts = []
+        for m in mult:
+            c = np.float32(1.0 / (np.float64(rb[i]) * (np.float64(m) * base)))
+            pts.append(lattice.nearest_e8((xb[i] * c).astype(np.float32).astype(np.float64)))
+        ok = [not voronoi.overloaded(P, q) for P in pts]
+        want = ok.index(True) + 1 if any(ok) else k
+        assert tb[i] == want
+        assert np.array_equal(voronoi.encode_point(pts[want - 1], q), cb[i])
+
+
+def test_coded_product_with_beta_multiples():
+    from workloads import random_rows
+    _, A = random_rows(23, 5, 64, dtype="f32")
+    _, W = random_rows(24, 4, 64, dtype="bf16", scale=0.02)
+    ma, mw, q = (6, 8, 10, 15), (2, 3, 5, 11), 14
+    base = 1.0 / (2 * q)
+    ca, ta, ra = nestquant.quantize_rows(A, q, 4, base, mult=ma)
+    cw, tw, rw = nestquant.quantize_rows(W, q, 4, base, mult=mw)
+    C = nestquant.coded_matmul(ca, ta, ra, q, base, cw, tw, rw, q, base, mult_a=ma, mult_w=mw)
+    for i in range(5):
+        for j in range(4):
+            ref = nestquant.dot_coded(ca[i], ta[i], ra[i], q, base, cw[j], tw[j], rw[j], q,
+                                      base, ma, mw)
+            assert C[i, j] == pytest.approx(ref, rel=1e-13, abs=1e-300)
+    Ahat = nestquant.decode_rows(ca, ta, ra, q, base, mult=ma)
+    What = nestquant.decode_rows(cw, tw, rw, q, base, mult=mw)
+    assert np.allclose(C, Ahat @ What.T, rtol=1e-12, atol=0)
+
+
 def test_lattice_points_reproduced(rng):
     q = 14
     # E8 points well inside q V: decode(encode) reproduces them exactly
