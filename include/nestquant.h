@@ -72,18 +72,25 @@ typedef enum { NQ_FIRST_BETA = 0, NQ_OPT_BETA = 1 } nq_strategy;
 /* Quantizer parameters (Sec. 4.2, App. F):
  *   q        nesting ratio, 2 <= q <= 16 (codes are nibbles);
  *   k        number of betas, 1 <= k <= 4 (2-bit beta indices);
- *   base     beta_t = t * base for t = 1..k; finite, > 0, and large enough that
+ *   base     beta_t = mult_t * base for t = 1..k; finite, > 0, and large enough that
  *            sqrt(cols) / base < 2^21 (bounds the lattice input |y| <= sqrt(cols) / base).
- *            The paper's grid "k betas uniform on [0, 10] / q" is base = 10 / (k q);
+ *            The paper's grid "k betas uniform on [0, 10] / q" is base = 10 / (k q) with
+ *            mult_t = t;
  *   decoder  an nq_decoder value (0 = Alg. 2 / Alg. 5);
- *   strategy an nq_strategy value (0 = First-beta); used by nq_encode only.
- * Codes made with one decoder must be decoded and multiplied with the same one. */
+ *   strategy an nq_strategy value (0 = First-beta); used by nq_encode only;
+ *   mult     the integer multiples of base: all zero for (1, 2, 3, 4) (the uniform grid), or
+ *            1 <= mult[0] < ... < mult[k-1] <= 64 with mult[k..3] = 0, e.g. a set chosen by
+ *            the dynamic program of App. F from the grid (1/2) {1, ..., 50} / q, which is
+ *            base = 1 / (2q) with multiples 1..50.  Each beta is fl64(mult_t * base).
+ * Codes made with one decoder must be decoded and multiplied with the same one, and with
+ * the same base and mult. */
 typedef struct {
   int32_t q;
   int32_t k;
   double base;
   int32_t decoder;
   int32_t strategy;
+  int32_t mult[4];
 } nq_params;
 
 /* Alg. 3 with the beta strategy p->strategy (App. F) on each row of x.
@@ -93,7 +100,7 @@ typedef struct {
  *   beta_idx device, nq_beta_words(rows, cols) uint32 (output);
  *   scales   device, rows floats (output).
  * Per row: r = RMS; for every 8-block, for t = 1..k the block y = fl32(x * c_t) with
- * c_t = fl32(1 / fl64(r * fl64(t * base))) is rounded to the nearest E8 point (Alg. 5;
+ * c_t = fl32(1 / fl64(r * beta_t)) is rounded to the nearest E8 point (Alg. 5;
  * ties: exact halves round down, lowest index on argmin/argmax ties, equal D8 / D8+1/2
  * distances pick D8+1/2).  First-beta keeps the first t whose point survives
  * decode(encode(.)) (no overload, Sec. 4.1), else t = k; Opt-beta keeps the t of least
@@ -103,7 +110,7 @@ nq_status nq_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t
                     int64_t cols, int64_t ld_x, uint32_t* codes, uint32_t* beta_idx,
                     float* scales, void* hip_stream);
 
-/* Alg. 2 and the inverse scaling: out[i][8j+l] = r_i * (t_ij * base) * X2_l / 2 where X2
+/* Alg. 2 and the inverse scaling: out[i][8j+l] = r_i * beta_t * X2_l / 2 where X2
  * is the decoded point of block j in 2E8 units (App. E).  out is rows x cols of out_dtype,
  * row i at out + i*ld_out elements, ld_out >= cols.  Each value is the fp64 product rounded
  * once to fp32 (and, for NQ_F16 / NQ_BF16, from there to the 16-bit type). */
@@ -112,11 +119,13 @@ nq_status nq_decode(const nq_params* p, const uint32_t* codes, const uint32_t* b
                     nq_dtype out_dtype, int64_t ld_out, void* hip_stream);
 
 /* C = A_hat * W_hat^T (Alg. 4 for every row pair), fp32 output.
- *   A: M x K coded with parameters pa; W: N x K coded with parameters pw (q, k and base
- *   may differ between the operands; K must be the same);  K % 8 == 0, K <= 65536.
+ *   A: M x K coded with parameters pa; W: N x K coded with parameters pw (q, k, base and
+ *   mult may differ between the operands; K must be the same);  K % 8 == 0, K <= 65536.
  *   c: device, M x N floats, row i at c + i*ldc, ldc >= N.
- * C_ij = r_Ai r_Wj base_A base_W / 4 * sum_blocks <t_A X2_A, t_W X2_W>; the integer tiles
- * t*X2 are exact in bf16 and contracted with fp32 accumulation.
+ * C_ij = r_Ai r_Wj base_A base_W / 4 * sum_blocks <m_A X2_A, m_W X2_W> (m = mult_t of the
+ * block's beta); the integer tiles m*X2 are contracted with fp32 accumulation on bf16
+ * matrix cores, exact in bf16 when 2q * mult_k <= 256 for both operands (always so for the
+ * uniform grid), else on fp16 matrix cores (exact up to 2048, every allowed mult).
  * Every block of both operands is decoded exactly once; the decoded activation (and, for
  * M > 64, the decoded weight) lives in a workspace of nq_matmul_workspace_size(M, N, K)
  * bytes, which nq_matmul takes from the stream-ordered allocator of the current device
@@ -138,15 +147,16 @@ nq_status nq_matmul_ex(const nq_params* pa, const uint32_t* a_codes, const uint3
 /* The two stages of nq_matmul_ex, for callers that time or schedule them separately, and
  * the exact int8 contraction.  stages is a bit mask:
  *   NQ_STAGE_DECODE    decodes the operands into the workspace (every block of A and, for
- *                      M > 64, of W, as t*X2);
+ *                      M > 64, of W, as m*X2);
  *   NQ_STAGE_CONTRACT  computes C from the workspace (for M <= 64 it also decodes W, straight
  *                      into matrix-core operands);
- *   NQ_CONTRACT_INT8   stores t*X2 as int8 and contracts on int8 matrix cores with int32
+ *   NQ_CONTRACT_INT8   stores m*X2 as int8 and contracts on int8 matrix cores with int32
  *                      accumulation instead of bf16 / fp32.  Every inner product
- *                      sum <t_A X2_A, t_W X2_W> (Alg. 4 without its scale) is then exact, and
+ *                      sum <m_A X2_A, m_W X2_W> (Alg. 4 without its scale) is then exact, and
  *                      C = fp32(sum) * r_A * r_W * base_A * base_W / 4.  It requires
- *                      k * q <= 63 for both operands (|t X2| <= 2 k q must fit int8), else
- *                      NQ_ERR_UNSUPPORTED.  Both stages of one product must agree on it.
+ *                      2q * mult_k <= 127 for both operands (with the uniform grid: k * q <= 63;
+ *                      |m X2| <= 2q m must fit int8), else NQ_ERR_UNSUPPORTED.  Both stages
+ *                      of one product must agree on it.
  * A DECODE call followed by a CONTRACT call with the same arguments on the same stream is
  * exactly the call with both bits; DECODE | CONTRACT is nq_matmul_ex.  The workspace must
  * not change in between.  Arguments are validated as in nq_matmul_ex; any other bit, or no

@@ -23,7 +23,8 @@ class NQError(RuntimeError):
 
 class _Params(ctypes.Structure):
     _fields_ = [("q", ctypes.c_int32), ("k", ctypes.c_int32), ("base", ctypes.c_double),
-                ("decoder", ctypes.c_int32), ("strategy", ctypes.c_int32)]
+                ("decoder", ctypes.c_int32), ("strategy", ctypes.c_int32),
+                ("mult", ctypes.c_int32 * 4)]
 
 
 DECODER_FULL = 0   # Alg. 2 with the Gosset oracle of Alg. 5
@@ -86,9 +87,12 @@ def default_base(q, k):
     return 10.0 / (k * q)
 
 
-def _params(q, k, base, decoder=DECODER_FULL, strategy=FIRST_BETA):
+def _params(q, k, base, decoder=DECODER_FULL, strategy=FIRST_BETA, mult=None):
+    m = [0, 0, 0, 0]
+    if mult is not None:
+        m[:len(mult)] = [int(v) for v in mult]
     return _Params(int(q), int(k), float(default_base(q, k) if base is None else base),
-                   int(decoder), int(strategy))
+                   int(decoder), int(strategy), (ctypes.c_int32 * 4)(*m))
 
 
 def _stream(stream):
@@ -112,7 +116,8 @@ def nq_beta_words(rows, cols):
 
 class Coded(NamedTuple):
     """A coded matrix: uint32 code words (stored in an int32 tensor), uint32 beta words,
-    fp32 row scales, and the quantizer parameters."""
+    fp32 row scales, and the quantizer parameters (mult: the integer multiples of base that
+    make the betas, None for 1..k)."""
     codes: "object"
     beta: "object"
     scales: "object"
@@ -122,13 +127,15 @@ class Coded(NamedTuple):
     k: int
     base: float
     decoder: int = DECODER_FULL
+    mult: "object" = None
 
 
 def encode(x, q=14, k=4, base=None, stream=None, out=None, decoder=DECODER_FULL,
-           strategy=FIRST_BETA):
+           strategy=FIRST_BETA, mult=None):
     """nq_encode on a 2-D cuda tensor (fp32 / fp16 / bf16, unit stride along rows).
     ``decoder`` is the decoder the code is defined with (DECODER_FULL or DECODER_M);
-    ``strategy`` picks the beta of each block (FIRST_BETA or OPT_BETA)."""
+    ``strategy`` picks the beta of each block (FIRST_BETA or OPT_BETA); ``mult`` gives the
+    betas as integer multiples of base (k increasing integers in [1, 64]; None: 1..k)."""
     import torch
     if x.dim() != 2 or x.stride(1) != 1 or not x.is_cuda:
         raise ValueError("x must be a 2-D cuda tensor with unit column stride")
@@ -143,12 +150,13 @@ def encode(x, q=14, k=4, base=None, stream=None, out=None, decoder=DECODER_FULL,
         scales = torch.empty(rows, dtype=torch.float32, device=x.device)
     else:
         codes, beta, scales = out
-    p = _params(q, k, base, decoder, strategy)
+    p = _params(q, k, base, decoder, strategy, mult)
     _check(lib.nq_encode(ctypes.byref(p), ctypes.c_void_p(x.data_ptr()), _dtype_code(x.dtype),
                          rows, cols, x.stride(0), ctypes.c_void_p(codes.data_ptr()),
                          ctypes.c_void_p(beta.data_ptr()), ctypes.c_void_p(scales.data_ptr()),
                          _stream(stream)))
-    return Coded(codes, beta, scales, rows, cols, int(q), int(k), p.base, int(decoder))
+    return Coded(codes, beta, scales, rows, cols, int(q), int(k), p.base, int(decoder),
+                 None if mult is None else tuple(int(v) for v in mult))
 
 
 def decode(coded, out_dtype=None, stream=None, out=None):
@@ -157,7 +165,7 @@ def decode(coded, out_dtype=None, stream=None, out=None):
     dt = torch.float32 if out_dtype is None else out_dtype
     if out is None:
         out = torch.empty(coded.rows, coded.cols, dtype=dt, device=coded.codes.device)
-    p = _params(coded.q, coded.k, coded.base, coded.decoder)
+    p = _params(coded.q, coded.k, coded.base, coded.decoder, mult=coded.mult)
     lib = library()
     _check(lib.nq_decode(ctypes.byref(p), ctypes.c_void_p(coded.codes.data_ptr()),
                          ctypes.c_void_p(coded.beta.data_ptr()),
@@ -185,7 +193,8 @@ def matmul(a, w, stream=None, out=None, workspace=None, stages=STAGE_DECODE | ST
         raise ValueError("K mismatch")
     if out is None:
         out = torch.empty(a.rows, w.rows, dtype=torch.float32, device=a.codes.device)
-    pa, pw = _params(a.q, a.k, a.base, a.decoder), _params(w.q, w.k, w.base, w.decoder)
+    pa = _params(a.q, a.k, a.base, a.decoder, mult=a.mult)
+    pw = _params(w.q, w.k, w.base, w.decoder, mult=w.mult)
     lib = library()
     need = lib.nq_matmul_workspace_size(a.rows, w.rows, a.cols)
     if need < 0:

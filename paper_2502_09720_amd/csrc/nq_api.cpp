@@ -39,6 +39,17 @@ nq_status check_params(const nq_params* p, int64_t cols, const char* who) {
     return fail(NQ_ERR_INVALID_ARG, "%s: decoder=%d is not an nq_decoder", who, p->decoder);
   if (p->strategy != NQ_FIRST_BETA && p->strategy != NQ_OPT_BETA)
     return fail(NQ_ERR_INVALID_ARG, "%s: strategy=%d is not an nq_strategy", who, p->strategy);
+  if (p->mult[0] != 0) {
+    for (int t = 0; t < 4; ++t) {
+      const int m = p->mult[t];
+      if (t < p->k ? (m < 1 || m > 64 || (t > 0 && m <= p->mult[t - 1])) : m != 0)
+        return fail(NQ_ERR_INVALID_ARG,
+                    "%s: mult must be all zero, or k increasing integers in [1, 64] followed by "
+                    "zeros", who);
+    }
+  } else if (p->mult[1] != 0 || p->mult[2] != 0 || p->mult[3] != 0) {
+    return fail(NQ_ERR_INVALID_ARG, "%s: mult[0] = 0 needs the whole table zero", who);
+  }
   if (std::sqrt((double)cols) / p->base >= 2097152.0)
     return fail(NQ_ERR_INVALID_ARG, "%s: base too small for cols=%lld (sqrt(cols)/base >= 2^21)",
                 who, (long long)cols);
@@ -53,6 +64,20 @@ nq_status check_cols(int64_t cols, const char* who) {
 }
 
 size_t dtype_size(nq_dtype d) { return d == NQ_F32 ? 4 : 2; }
+
+// The multiple of base for beta index i (0..3): the table, the uniform grid i + 1 when it
+// is zero, and the largest beta for indices past k (never written by the encoder).
+int beta_mult(const nq_params* p, int i) {
+  if (p->mult[0] == 0) return i + 1;
+  return p->mult[i < p->k ? i : p->k - 1];
+}
+uint32_t mult_table(const nq_params* p) {
+  uint32_t t = 0;
+  for (int i = 0; i < 4; ++i) t |= (uint32_t)beta_mult(p, i) << (8 * i);
+  return t;
+}
+// Largest |m X2| of the operand's tiles: 2q times its largest multiple.
+int tile_bound(const nq_params* p) { return 2 * p->q * beta_mult(p, p->k - 1); }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
@@ -87,7 +112,7 @@ const char* nq_status_string(nq_status s) {
 
 const char* nq_last_error(void) { return g_last_error; }
 
-int32_t nq_version(void) { return 300; }
+int32_t nq_version(void) { return 400; }
 
 nq_status nq_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t rows,
                     int64_t cols, int64_t ld_x, uint32_t* codes, uint32_t* beta_idx,
@@ -113,7 +138,7 @@ nq_status nq_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t
   a.mq = nq::magic_q(p->q);
   a.decoder = p->decoder;
   a.strategy = p->strategy;
-  for (int t = 0; t < 4; ++t) a.beta[t] = (double)(t + 1) * p->base;
+  for (int t = 0; t < 4; ++t) a.beta[t] = (double)beta_mult(p, t) * p->base;
   return hip_status(nq::launch_encode(x, (int)x_dtype, rows, (int)cols, ld_x, a, codes, beta_idx,
                                       scales, (hipStream_t)hip_stream),
                     who);
@@ -139,7 +164,7 @@ nq_status nq_decode(const nq_params* p, const uint32_t* codes, const uint32_t* b
   a.q = p->q;
   a.m2q = nq::magic_2q(p->q);
   a.decoder = p->decoder;
-  for (int t = 0; t < 4; ++t) a.half_beta[t] = ((double)(t + 1) * p->base) * 0.5;
+  for (int t = 0; t < 4; ++t) a.half_beta[t] = ((double)beta_mult(p, t) * p->base) * 0.5;
   return hip_status(nq::launch_decode(codes, beta_idx, scales, rows, (int)cols, out,
                                       (int)out_dtype, ld_out, a, (hipStream_t)hip_stream),
                     who);
@@ -216,29 +241,34 @@ static nq_status matmul_stages(int32_t stages, const nq_params* pa, const uint32
                                  w_scales, N, K, c, ldc, who))
     return s;
   const bool i8 = (stages & NQ_CONTRACT_INT8) != 0;
-  if (i8 && (pa->k * pa->q > 63 || pw->k * pw->q > 63))
+  if (i8 && (tile_bound(pa) > 127 || tile_bound(pw) > 127))
     return fail(NQ_ERR_UNSUPPORTED,
-                "%s: the int8 contraction needs k * q <= 63 for both operands (|t X2| <= 2 k q "
-                "must fit int8)", who);
+                "%s: the int8 contraction needs 2q * mult_k <= 127 for both operands (k * q <= "
+                "63 on the uniform grid; |m X2| must fit int8)", who);
+  // bf16 tiles hold every integer up to 256; larger multiples take fp16 (up to 2048)
+  const int et = i8 ? nq::ET_I8
+                    : (tile_bound(pa) <= 256 && tile_bound(pw) <= 256 ? nq::ET_BF16 : nq::ET_F16);
   if (M == 0 || N == 0) return ok();
   const int64_t need = nq_matmul_workspace_size(M, N, K);
   if (workspace_bytes < need || (need > 0 && !workspace))
     return fail(NQ_ERR_INVALID_ARG, "%s: workspace of %lld bytes needed", who, (long long)need);
   if (need > 0 && !aligned16(workspace))
     return fail(NQ_ERR_INVALID_ARG, "%s: workspace must be 16-byte aligned", who);
-  nq::MatmulOperand A{a_codes, a_beta, a_scales, pa->q, nq::magic_2q(pa->q), M, pa->decoder};
-  nq::MatmulOperand W{w_codes, w_beta, w_scales, pw->q, nq::magic_2q(pw->q), N, pw->decoder};
+  nq::MatmulOperand A{a_codes, a_beta, a_scales, pa->q, nq::magic_2q(pa->q), M, pa->decoder,
+                      mult_table(pa)};
+  nq::MatmulOperand W{w_codes, w_beta, w_scales, pw->q, nq::magic_2q(pw->q), N, pw->decoder,
+                      mult_table(pw)};
   const float scale = (float)(pa->base * pw->base * 0.25);
   hipStream_t st = (hipStream_t)hip_stream;
   if (M <= nq::kFusedMaxM)
     return hip_status(
-        nq::launch_matmul_skinny(stages, i8, A, W, K, c, ldc, scale, workspace, st), who);
+        nq::launch_matmul_skinny(stages, et, A, W, K, c, ldc, scale, workspace, st), who);
   static std::once_flag attr_once;
   static hipError_t attr_err = hipSuccess;
   std::call_once(attr_once, [] { attr_err = nq::gemm_set_attributes(); });
   if (attr_err != hipSuccess) return hip_status(attr_err, who);
   return hip_status(
-      nq::launch_matmul_decode_once(stages, i8, A, W, K, c, ldc, scale, workspace, st), who);
+      nq::launch_matmul_decode_once(stages, et, A, W, K, c, ldc, scale, workspace, st), who);
 }
 
 nq_status nq_matmul_ex(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,

@@ -432,22 +432,39 @@ __device__ __forceinline__ GridPos grid_block(int nb, int lg) {
   return g;
 }
 
-// t * X2 of one block as eight bf16 (exact: |t X2| <= 4 * 32 = 128 < 2^8): the upper halves
-// of the fp32 values, coordinates 2i and 2i+1 in word i.
-template <int DV = 0>
-__device__ __forceinline__ u32x4 decode_tile_bf16(uint32_t w, int t, int q, uint32_t m2q) {
+// The multiple m of base for beta index idx (0..3): byte idx of the operand's table.
+__device__ __forceinline__ int beta_mult(uint32_t mtab, uint32_t idx) {
+  return (int)((mtab >> (8u * idx)) & 0xFFu);
+}
+
+// Two integer-valued floats as a 16-bit pair (lo in the low half): bf16 keeps the upper
+// halves of the fp32 values, fp16 converts (toward zero; exact for the integers here).
+template <bool F16>
+__device__ __forceinline__ uint32_t pack16(float lo, float hi) {
+  if constexpr (F16) {
+    return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(lo, hi));
+  } else {
+    return __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
+  }
+}
+
+// m * X2 of one block as eight bf16 or fp16 values, coordinates 2i and 2i+1 in word i.
+// |X2| <= 2q <= 32, so the values are exact integers in bf16 while |m X2| <= 256 (m <= 4
+// for every q, the uniform beta grid) and in fp16 while |m X2| <= 2048 (m <= 64).
+template <int DV = 0, bool F16 = false>
+__device__ __forceinline__ u32x4 decode_tile_16(uint32_t w, int m, int q, uint32_t m2q) {
   if constexpr (DV == 2) {
     uint32_t xa, xb;
     int x0;
     decode_word_m16(w, xa, xb, x0);
-    const float tq = 0.25f * (float)t;    // bytes hold 4 X2 (exact)
+    const float tq = 0.25f * (float)m;    // bytes hold 4 X2 (exact)
     uint32_t o[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const uint32_t x = i < 2 ? xa : xb;
-      const float lo = i == 0 ? (float)(x0 * t) : sbyte_f32(x, 2 * (i & 1)) * tq;
+      const float lo = i == 0 ? (float)(x0 * m) : sbyte_f32(x, 2 * (i & 1)) * tq;
       const float hi = sbyte_f32(x, 2 * (i & 1) + 1) * tq;
-      o[i] = __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
+      o[i] = pack16<F16>(lo, hi);
     }
     return u32x4{o[0], o[1], o[2], o[3]};
   }
@@ -456,23 +473,22 @@ __device__ __forceinline__ u32x4 decode_tile_bf16(uint32_t w, int t, int q, uint
   uint32_t o[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int lo = (int)(short)(X2p[i] & 0xFFFFu) * t;
-    const int hi = ((int)X2p[i] >> 16) * t;
-    o[i] = __builtin_amdgcn_perm(__float_as_uint((float)hi), __float_as_uint((float)lo),
-                                 0x07060302u);
+    const int lo = (int)(short)(X2p[i] & 0xFFFFu) * m;
+    const int hi = ((int)X2p[i] >> 16) * m;
+    o[i] = pack16<F16>((float)lo, (float)hi);
   }
   return u32x4{o[0], o[1], o[2], o[3]};
 }
 
-// t * X2 of one block as eight int8 (exact when 2 k q <= 127: |X2| <= 2q, t <= k), the
+// m * X2 of one block as eight int8 (exact when 2 q m <= 127: |X2| <= 2q), the
 // coordinates in byte order.  The 16-bit products keep their low byte, which is the
 // two's-complement int8 of a value in [-127, 127].
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 template <int DV = 0>
-__device__ __forceinline__ u32x2 decode_tile_i8(uint32_t w, int t, int q, uint32_t m2q) {
+__device__ __forceinline__ u32x2 decode_tile_i8(uint32_t w, int m, int q, uint32_t m2q) {
   uint32_t X2p[4];
   decode_word_pk<DV != 0>(w, q, m2q, X2p);
-  const u16x2 tt = {(unsigned short)t, (unsigned short)t};
+  const u16x2 tt = {(unsigned short)m, (unsigned short)m};
   uint32_t p[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) p[i] = bits32(as_u16x2(X2p[i]) * tt);

@@ -294,8 +294,10 @@ __device__ __forceinline__ void dd_add_square(double& hi, double& lo, float x) {
 }
 
 // BPT > 0: the row's blocks stay in registers (read once).  BPT == 0: long rows are
-// streamed, reading each block once for the scale and once more for the codes.
-template <typename T, int LANES, int BPT>
+// streamed, reading each block once for the scale and once more for the codes.  OPT: the
+// Opt-beta strategy (opt_block) instead of First-beta; a separate instantiation, since its
+// registers would lower the occupancy of the First-beta kernel.
+template <typename T, int LANES, int BPT, bool OPT>
 __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_kernel(
     const T* __restrict__ x, int64_t rows, int cols, int64_t ld_x, EncodeArgs a,
     uint32_t* __restrict__ codes, uint32_t* __restrict__ beta, float* __restrict__ scales) {
@@ -379,7 +381,7 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_kernel(
     uint32_t word = 0;
     int tsel = 0;
     if (mine && coded) {
-      if (a.strategy) {
+      if constexpr (OPT) {
         opt_block(*reinterpret_cast<float(*)[8]>(vb), c, r, a, word, tsel);
       } else {
         encode_block(*reinterpret_cast<float(*)[8]>(vb), c, a, word, tsel);
@@ -413,7 +415,6 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_kernel(
 // the point's exact root bound says it overloads (start again at the next beta) or lies on
 // the cell boundary (the literal test decides).  Those slots (about 12-15% on Gaussian-like and heavy-tailed
 // rows) are queued, and phase 2 finishes them with every lane of the workgroup busy.
-// With Opt-beta, phase 1 evaluates every beta of every slot (opt_block) and queues nothing.
 // Two-bit beta indices are staged in LDS and packed into words at the end.
 // ---------------------------------------------------------------------------------------
 template <int LANES, int BPT>
@@ -650,23 +651,6 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
     const int64_t row = row0 + rw;
     const bool valid = row < rows && j < nb;
     const bool coded = valid && rrow[cw][rw] != 0.0f;
-    if (a.strategy) {
-      // Opt-beta: every beta of every block is evaluated here (nothing is queued)
-      if (valid) {
-        uint32_t word = 0u;
-        int tsel = 0;
-        if (coded) {
-          float v[8], c[4];
-          unpack_raw<T>(rawl[wave][sl], v);
-#pragma unroll
-          for (int t = 0; t < 4; ++t) c[t] = crow[cw][rw][t];
-          opt_block(v, c, rrow[cw][rw], a, word, tsel);
-        }
-        codes_w[rw * nb + j] = word;
-        tsl[wave][sl] = (uint8_t)tsel;
-      }
-      continue;
-    }
     bool queued = false;
     int start = 0, t0 = 0;
     int P[8];
@@ -754,14 +738,14 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
 // ---------------------------------------------------------------------------------------
 // launch
 // ---------------------------------------------------------------------------------------
-template <typename T, int LANES, int BPT>
+template <typename T, int LANES, int BPT, bool OPT = false>
 static hipError_t launch_t(const void* x, int64_t rows, int cols, int64_t ld_x,
                            const EncodeArgs& a, uint32_t* codes, uint32_t* beta, float* scales,
                            hipStream_t st) {
   constexpr int WG = LANES > 64 ? LANES : 256;
   constexpr int RPW = WG / LANES;
   const int64_t grid = (rows + RPW - 1) / RPW;
-  hipLaunchKernelGGL((encode_kernel<T, LANES, BPT>), dim3((unsigned)grid), dim3(WG), 0, st,
+  hipLaunchKernelGGL((encode_kernel<T, LANES, BPT, OPT>), dim3((unsigned)grid), dim3(WG), 0, st,
                      (const T*)x, rows, cols, ld_x, a, codes, beta, scales);
   return hipGetLastError();
 }
@@ -783,6 +767,17 @@ static hipError_t launch_dtype(const void* x, int64_t rows, int cols, int64_t ld
                                const EncodeArgs& a, uint32_t* codes, uint32_t* beta,
                                float* scales, hipStream_t st) {
   const int nb = cols / 8;
+  if (a.strategy) {
+    // Opt-beta: a lane group of up to 64 holds short rows in registers; longer rows stream
+#define NQ_O(L, B) return launch_t<T, L, B, true>(x, rows, cols, ld_x, a, codes, beta, scales, st)
+    if (nb <= 8) NQ_O(8, 1);
+    if (nb <= 16) NQ_O(16, 1);
+    if (nb <= 32) NQ_O(32, 1);
+    if (nb <= 64) NQ_O(64, 1);
+    if (nb <= 2048) NQ_O(256, 0);
+    NQ_O(1024, 0);
+#undef NQ_O
+  }
 #define NQ_W(L, B) return launch_w<T, L, B>(x, rows, cols, ld_x, a, codes, beta, scales, st)
 #define NQ_L(L, B) return launch_t<T, L, B>(x, rows, cols, ld_x, a, codes, beta, scales, st)
   // short rows: several rows per lane group, 512 blocks per wave when there are enough rows

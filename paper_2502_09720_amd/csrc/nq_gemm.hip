@@ -6,9 +6,11 @@
 // vector-ALU work per block than the matrix cores spend on it.  So each block is decoded
 // exactly once:
 //
-//   1. tiles_kernel: Alg. 2 on every code word; writes t * X2 (an integer in [-128, 128],
-//      exact in bf16) as 8 bf16 into a K-contiguous workspace tile, zero-padded to the GEMM
-//      tile grid.  The workspace (a few tens of MB) stays in the 256 MB Infinity Cache.
+//   1. tiles_kernel: Alg. 2 on every code word; writes m * X2 (beta = m * base; with the
+//      uniform grid m = t and |m X2| <= 128, exact in bf16) as 8 bf16 into a K-contiguous
+//      workspace tile, zero-padded to the GEMM tile grid.  Beta sets with larger multiples
+//      use fp16 tiles (exact to 2048) and fp16 matrix cores at the same rate.  The
+//      workspace (a few tens of MB) stays in the 256 MB Infinity Cache.
 //   2. gemm_kernel: bf16 MFMA GEMM (C = T_A T_W^T, fp32 accumulation) with the epilogue
 //      C_ij = acc * r_Ai * r_Wj * base_A * base_W / 4.
 //
@@ -29,6 +31,7 @@
 namespace nq {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x16 __attribute__((ext_vector_type(16)));
@@ -58,15 +61,17 @@ using CfgMid = Cfg<256, 128, 4, 2, 3>;
 using CfgBig = Cfg<256, 256, 4, 2, 2>;
 }  // namespace gemm
 
-// t * X2 of every block of a coded operand into ws[rows_p][nb_p blocks] (zero padding), one
-// thread per block (grid_block): 8 bf16 (16 B) per block, or 8 int8 (8 B) for the int8
-// contraction.
-template <bool I8, int DV>
+// m * X2 of every block of a coded operand into ws[rows_p][nb_p blocks] (zero padding), one
+// thread per block (grid_block): 8 bf16 or fp16 (16 B) per block, or 8 int8 (8 B) for the
+// int8 contraction.
+template <int ET, int DV>
 __global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__ codes,
                                                     const uint32_t* __restrict__ beta,
                                                     int64_t rows, int nb, int64_t rows_p,
-                                                    int nb_p, int q, uint32_t m2q, int lg,
+                                                    int nb_p, int q, uint32_t m2q,
+                                                    uint32_t mtab, int lg,
                                                     void* __restrict__ ws) {
+  constexpr bool I8 = ET == ET_I8;
   const GridPos g = grid_block(nb_p, lg);
   const int64_t row = g.rb + g.lr;
   const int j = g.j;
@@ -77,26 +82,26 @@ __global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__
     const int nbw = (nb + 15) >> 4;
     const uint32_t w = __builtin_nontemporal_load(codes + g.rb * nb + (uint32_t)(g.lr * nb + j));
     const uint32_t bw = beta[g.rb * nbw + (uint32_t)(g.lr * nbw + (j >> 4))];
-    const int t = (int)((bw >> (2 * (j & 15))) & 3u) + 1;
+    const int m = beta_mult(mtab, (bw >> (2 * (j & 15))) & 3u);
     if constexpr (I8) {
-      out = decode_tile_i8<DV>(w, t, q, m2q);
+      out = decode_tile_i8<DV>(w, m, q, m2q);
     } else {
-      out = decode_tile_bf16<DV>(w, t, q, m2q);
+      out = decode_tile_16<DV, ET == ET_F16>(w, m, q, m2q);
     }
   }
   reinterpret_cast<V*>(ws)[g.rb * nb_p + (uint32_t)(g.lr * nb_p + j)] = out;
 }
 
 // Launch tiles_kernel for one operand with its decoder.
-template <bool I8>
+template <int ET>
 void launch_tiles(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void* ws,
                   hipStream_t st) {
   int lg;
   int64_t wgs;
   grid_shape(rows_p, nb_p, lg, wgs);
 #define NQ_TL(DV)                                                                            \
-  hipLaunchKernelGGL((tiles_kernel<I8, DV>), dim3((unsigned)wgs), dim3(256), 0, st, X.codes,    \
-                     X.beta, X.rows, nb, rows_p, nb_p, X.q, X.m2q, lg, ws)
+  hipLaunchKernelGGL((tiles_kernel<ET, DV>), dim3((unsigned)wgs), dim3(256), 0, st, X.codes,    \
+                     X.beta, X.rows, nb, rows_p, nb_p, X.q, X.m2q, X.mtab, lg, ws)
   switch (decoder_variant(X.decoder, X.q)) {
     case 0: NQ_TL(0); break;
     case 1: NQ_TL(1); break;
@@ -104,8 +109,9 @@ void launch_tiles(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void
   }
 #undef NQ_TL
 }
-template void launch_tiles<false>(const MatmulOperand&, int, int64_t, int, void*, hipStream_t);
-template void launch_tiles<true>(const MatmulOperand&, int, int64_t, int, void*, hipStream_t);
+template void launch_tiles<ET_BF16>(const MatmulOperand&, int, int64_t, int, void*, hipStream_t);
+template void launch_tiles<ET_F16>(const MatmulOperand&, int, int64_t, int, void*, hipStream_t);
+template void launch_tiles<ET_I8>(const MatmulOperand&, int, int64_t, int, void*, hipStream_t);
 
 __device__ __forceinline__ void tile_coords(int bid, int tm, int tn, int& pm, int& pn) {
   constexpr int GROUP_M = gemm::GROUP_M;
@@ -131,10 +137,11 @@ typedef __attribute__((address_space(3))) void lds_void;
 // lanes of a 128-bit read per cycle.
 __device__ __forceinline__ int swz(int r) { return (r ^ ((r >> 3) & 3)) & 7; }
 
-// kc: row length of both tiles in 16-byte chunks (a multiple of 8).  I8: int8 tiles and
-// v_mfma_i32_32x32x32_i8 (exact int32 sums); else bf16 tiles and v_mfma_f32_32x32x16_bf16.
-// Both consume 16 B per lane per MFMA, so staging, swizzle and fragment reads are the same.
-template <class C, bool I8>
+// kc: row length of both tiles in 16-byte chunks (a multiple of 8).  ET: int8 tiles and
+// v_mfma_i32_32x32x32_i8 (exact int32 sums), or bf16 / fp16 tiles and
+// v_mfma_f32_32x32x16_bf16 / _f16.  All consume 16 B per lane per MFMA, so staging, swizzle
+// and fragment reads are the same.
+template <class C, int ET>
 __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
     const u32x4* __restrict__ ta, const u32x4* __restrict__ tw, int kc, int tm, int tn,
     const float* __restrict__ ra, const float* __restrict__ rw, int64_t M, int64_t N,
@@ -143,6 +150,7 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
   constexpr int NW = C::NW, TM = C::TM, TN = C::TN, STAGE_BYTES = C::STAGE_BYTES;
   constexpr int GROUPS_PER_WAVE = C::GROUPS_PER_WAVE;
   constexpr int CH = gemm::BKB / 16;  // 16-byte chunks per row per stage
+  constexpr bool I8 = ET == ET_I8;
   extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
 
   int pm, pn;
@@ -258,6 +266,10 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
           acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(
               __builtin_bit_cast(i32x4, af[cur][i]), __builtin_bit_cast(i32x4, bfr[cur][j]),
               acc[i][j], 0, 0, 0);
+        } else if constexpr (ET == ET_F16) {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(
+              __builtin_bit_cast(f16x8, af[cur][i]), __builtin_bit_cast(f16x8, bfr[cur][j]),
+              acc[i][j], 0, 0, 0);
         } else {
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
               __builtin_bit_cast(bf16x8, af[cur][i]), __builtin_bit_cast(bf16x8, bfr[cur][j]),
@@ -310,7 +322,7 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
 }
 
 // Both tile configurations pad M to 256; N is padded to 256 (a multiple of both BN).  Rows
-// are padded to 128 B: 64 bf16, or 128 int8 (never more bytes than the bf16 tiles).
+// are padded to 128 B: 64 bf16 / fp16, or 128 int8 (never more bytes than the 16-bit tiles).
 size_t decode_once_workspace(int64_t M, int64_t N, int64_t K) {
   using namespace gemm;
   const int64_t mp = (M + 255) / 256 * 256;
@@ -319,17 +331,17 @@ size_t decode_once_workspace(int64_t M, int64_t N, int64_t K) {
   return (size_t)((mp + np) * kp * 2);
 }
 
-template <class C, bool I8>
+template <class C, int ET>
 static void launch_gemm(const u32x4* wa, const u32x4* ww, int kc, int64_t mp, int64_t np,
                         const MatmulOperand& A, const MatmulOperand& W, float* c, int64_t ldc,
                         float scale, hipStream_t st) {
   const int tm = (int)(mp / C::BM), tn = (int)(np / C::BN);
-  hipLaunchKernelGGL((gemm_kernel<C, I8>), dim3((unsigned)(tm * tn)), dim3(C::NW * 64),
+  hipLaunchKernelGGL((gemm_kernel<C, ET>), dim3((unsigned)(tm * tn)), dim3(C::NW * 64),
                      (size_t)C::NSTAGE * C::STAGE_BYTES, st, wa, ww, kc, tm, tn, A.scales,
                      W.scales, A.rows, W.rows, c, ldc, scale);
 }
 
-template <bool I8>
+template <int ET>
 static hipError_t decode_once(int stages, const MatmulOperand& A, const MatmulOperand& W,
                               int64_t K, float* c, int64_t ldc, float scale, void* ws,
                               hipStream_t st) {
@@ -337,40 +349,44 @@ static hipError_t decode_once(int stages, const MatmulOperand& A, const MatmulOp
   const int nb = (int)(K / 8);
   const int64_t mp = (A.rows + 255) / 256 * 256;
   const int64_t np = (W.rows + 255) / 256 * 256;
-  constexpr int EB = I8 ? 1 : 2;                       // bytes per element
+  constexpr int EB = ET == ET_I8 ? 1 : 2;              // bytes per element
   const int64_t kp = (K * EB + BKB - 1) / BKB * BKB / EB;
   const int nbp = (int)(kp / 8);
   const int kc = (int)(kp * EB / 16);
   u32x4* wa = reinterpret_cast<u32x4*>(ws);
   u32x4* ww = wa + mp * kc;
   if (stages & 1) {
-    launch_tiles<I8>(A, nb, mp, nbp, (void*)wa, st);
-    launch_tiles<I8>(W, nb, np, nbp, (void*)ww, st);
+    launch_tiles<ET>(A, nb, mp, nbp, (void*)wa, st);
+    launch_tiles<ET>(W, nb, np, nbp, (void*)ww, st);
   }
   if (!(stages & 2)) return hipGetLastError();
   // 256 x 256 tiles once they give every CU a tile, else 256 x 128
   if ((mp / 256) * (np / 256) >= 256) {
-    launch_gemm<CfgBig, I8>(wa, ww, kc, mp, np, A, W, c, ldc, scale, st);
+    launch_gemm<CfgBig, ET>(wa, ww, kc, mp, np, A, W, c, ldc, scale, st);
   } else {
-    launch_gemm<CfgMid, I8>(wa, ww, kc, mp, np, A, W, c, ldc, scale, st);
+    launch_gemm<CfgMid, ET>(wa, ww, kc, mp, np, A, W, c, ldc, scale, st);
   }
   return hipGetLastError();
 }
 
-hipError_t launch_matmul_decode_once(int stages, bool i8, const MatmulOperand& A,
+hipError_t launch_matmul_decode_once(int stages, int et, const MatmulOperand& A,
                                      const MatmulOperand& W, int64_t K, float* c, int64_t ldc,
                                      float scale, void* ws, hipStream_t st) {
-  return i8 ? decode_once<true>(stages, A, W, K, c, ldc, scale, ws, st)
-            : decode_once<false>(stages, A, W, K, c, ldc, scale, ws, st);
+  switch (et) {
+    case ET_I8: return decode_once<ET_I8>(stages, A, W, K, c, ldc, scale, ws, st);
+    case ET_F16: return decode_once<ET_F16>(stages, A, W, K, c, ldc, scale, ws, st);
+    default: return decode_once<ET_BF16>(stages, A, W, K, c, ldc, scale, ws, st);
+  }
 }
 
 hipError_t gemm_set_attributes() {
   using namespace gemm;
-  const void* k[4] = {(const void*)gemm_kernel<CfgMid, false>, (const void*)gemm_kernel<CfgMid, true>,
-                      (const void*)gemm_kernel<CfgBig, false>, (const void*)gemm_kernel<CfgBig, true>};
-  const int bytes[4] = {CfgMid::NSTAGE * CfgMid::STAGE_BYTES, CfgMid::NSTAGE * CfgMid::STAGE_BYTES,
-                        CfgBig::NSTAGE * CfgBig::STAGE_BYTES, CfgBig::NSTAGE * CfgBig::STAGE_BYTES};
-  for (int i = 0; i < 4; ++i) {
+  const void* k[6] = {(const void*)gemm_kernel<CfgMid, ET_BF16>, (const void*)gemm_kernel<CfgMid, ET_F16>,
+                      (const void*)gemm_kernel<CfgMid, ET_I8>, (const void*)gemm_kernel<CfgBig, ET_BF16>,
+                      (const void*)gemm_kernel<CfgBig, ET_F16>, (const void*)gemm_kernel<CfgBig, ET_I8>};
+  constexpr int mid = CfgMid::NSTAGE * CfgMid::STAGE_BYTES, big = CfgBig::NSTAGE * CfgBig::STAGE_BYTES;
+  const int bytes[6] = {mid, mid, mid, big, big, big};
+  for (int i = 0; i < 6; ++i) {
     const hipError_t e = hipFuncSetAttribute(k[i], hipFuncAttributeMaxDynamicSharedMemorySize, bytes[i]);
     if (e != hipSuccess) return e;
   }

@@ -32,7 +32,12 @@ struct MatmulOperand {
   uint32_t m2q;
   int64_t rows;
   int decoder;
+  uint32_t mtab;   // byte i: the multiple m of base for beta index i (beta = m * base)
 };
+
+// Element type of the decoded tiles m * X2 and of the matrix-core instructions: bf16 holds
+// every integer up to 256, fp16 up to 2048, int8 up to 127 (all exact).
+enum ElemType { ET_BF16 = 0, ET_F16 = 1, ET_I8 = 2 };
 
 hipError_t launch_encode(const void* x, int dtype, int64_t rows, int cols, int64_t ld_x,
                          const EncodeArgs& a, uint32_t* codes, uint32_t* beta, float* scales,
@@ -43,16 +48,16 @@ hipError_t launch_decode(const uint32_t* codes, const uint32_t* beta, const floa
                          const DecodeArgs& a, hipStream_t st);
 
 // Small M (skinny): decode A once into a tile, then decode W straight into MFMA operands.
-// stages: bit 0 decodes into the workspace, bit 1 contracts (see nq_matmul_stages); i8:
-// int8 tiles and int8 matrix cores (exact int32 sums) instead of bf16.
+// stages: bit 0 decodes into the workspace, bit 1 contracts (see nq_matmul_stages); et: the
+// ElemType of the tiles and matrix cores (int8: exact int32 sums).
 size_t skinny_workspace(int64_t M, int64_t K);
-hipError_t launch_matmul_skinny(int stages, bool i8, const MatmulOperand& A,
+hipError_t launch_matmul_skinny(int stages, int et, const MatmulOperand& A,
                                 const MatmulOperand& W, int64_t K, float* c, int64_t ldc,
                                 float scale, void* ws, hipStream_t st);
 
 // Decode-once path (large M): workspace bytes, launch (tiles + GEMM), one-time attributes.
 size_t decode_once_workspace(int64_t M, int64_t N, int64_t K);
-hipError_t launch_matmul_decode_once(int stages, bool i8, const MatmulOperand& A,
+hipError_t launch_matmul_decode_once(int stages, int et, const MatmulOperand& A,
                                      const MatmulOperand& W, int64_t K, float* c, int64_t ldc,
                                      float scale, void* ws, hipStream_t st);
 hipError_t gemm_set_attributes();

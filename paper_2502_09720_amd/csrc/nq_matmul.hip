@@ -5,8 +5,9 @@
 // Here the weight decode dominates (the product is a few flops per decoded weight entry),
 // so every block of W is decoded exactly once, straight into a matrix-core operand: for
 // v_mfma_f32_16x16x32_bf16 the B operand of lane l is the 8 K-values of column l % 16 at
-// K offset 8 (l / 16), i.e. exactly one decoded block (t * X2, exact in bf16), so each lane
-// decodes its own block and no LDS staging is needed.  The activation (at most 64 rows) is
+// K offset 8 (l / 16), i.e. exactly one decoded block (m * X2, exact in bf16; fp16 for beta
+// sets whose multiples m exceed what bf16 holds), so each lane decodes its own block and no
+// LDS staging is needed.  The activation (at most 64 rows) is
 // decoded once beforehand into a bf16 tile (tiles_kernel) that stays in cache; its
 // fragments are loaded per step for up to four 16-row M tiles.  A workgroup owns 16
 // columns of C; its four waves split K and combine their partial sums through LDS before
@@ -20,9 +21,10 @@
 namespace nq {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef int i32x4 __attribute__((ext_vector_type(4)));
 
-template <bool I8>
+template <int ET>
 void launch_tiles(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void* ws,
                   hipStream_t st);
 
@@ -39,11 +41,12 @@ void launch_tiles(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void
 // next chunk's words are loaded while the current one is decoded (two register sets in
 // turn).  The host keeps W's code array below
 // 2^31 bytes per launch.
-template <int MT, bool I8, int DVW, int NWV>
+template <int MT, int ET, int DVW, int NWV>
 __global__ __launch_bounds__(NWV * 64) void skinny_kernel(const u32x4* __restrict__ ta, int kcb,
                                                           MatmulOperand A, MatmulOperand W,
                                                           int nb, float* __restrict__ c,
                                                           int64_t ldc, float scale) {
+  constexpr bool I8 = ET == ET_I8;
   using Acc = typename std::conditional<I8, i32x4, f32x4>::type;
   constexpr int BPL = I8 ? 2 : 1;        // blocks per lane per step
   constexpr int PD = MT <= 2 ? 8 : 4;    // steps per chunk
@@ -126,11 +129,14 @@ __global__ __launch_bounds__(NWV * 64) void skinny_kernel(const u32x4* __restric
       const int blk = blk0 + i * BPL;
       u32x4 b;
       if constexpr (I8) {
-        const u32x2 lo = decode_tile_i8<DVW>(x.w[2 * i], (int)((x.b >> (2 * (blk & 15))) & 3u) + 1, W.q, W.m2q);
-        const u32x2 hi = decode_tile_i8<DVW>(x.w[2 * i + 1], (int)((x.b >> (2 * ((blk + 1) & 15))) & 3u) + 1, W.q, W.m2q);
+        const u32x2 lo = decode_tile_i8<DVW>(
+            x.w[2 * i], beta_mult(W.mtab, (x.b >> (2 * (blk & 15))) & 3u), W.q, W.m2q);
+        const u32x2 hi = decode_tile_i8<DVW>(
+            x.w[2 * i + 1], beta_mult(W.mtab, (x.b >> (2 * ((blk + 1) & 15))) & 3u), W.q, W.m2q);
         b = u32x4{lo.x, lo.y, hi.x, hi.y};
       } else {
-        b = decode_tile_bf16<DVW>(x.w[i], (int)((x.b >> (2 * (blk & 15))) & 3u) + 1, W.q, W.m2q);
+        b = decode_tile_16<DVW, ET == ET_F16>(
+            x.w[i], beta_mult(W.mtab, (x.b >> (2 * (blk & 15))) & 3u), W.q, W.m2q);
       }
 #pragma unroll
       for (int m = 0; m < MT; ++m) {
@@ -138,6 +144,10 @@ __global__ __launch_bounds__(NWV * 64) void skinny_kernel(const u32x4* __restric
           acc[m] = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, af[i][m]),
                                                          __builtin_bit_cast(i32x4, b), acc[m], 0,
                                                          0, 0);
+        } else if constexpr (ET == ET_F16) {
+          acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, af[i][m]),
+                                                          __builtin_bit_cast(f16x8, b), acc[m],
+                                                          0, 0, 0);
         } else {
           acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, af[i][m]),
                                                            __builtin_bit_cast(bf16x8, b), acc[m],
@@ -185,21 +195,21 @@ __global__ __launch_bounds__(NWV * 64) void skinny_kernel(const u32x4* __restric
   }
 }
 
-// Rows of the A tile are padded to 128 B (64 bf16 or 128 int8) and to 16 rows.
+// Rows of the A tile are padded to 128 B (64 bf16 / fp16 or 128 int8) and to 16 rows.
 size_t skinny_workspace(int64_t M, int64_t K) {
   const int64_t mp = (M + 15) / 16 * 16;
   const int64_t kp = (K + 63) / 64 * 64;
   return (size_t)(mp * kp * 2);
 }
 
-template <bool I8>
+template <int ET>
 static hipError_t skinny_launch(const MatmulOperand& A, const MatmulOperand& W, const u32x4* ta,
                                 int kcb, int nb, float* c, int64_t ldc, float scale,
                                 hipStream_t st) {
   const int64_t mp = (A.rows + 15) / 16 * 16;
   const unsigned grid = (unsigned)((W.rows + 15) / 16);
 #define NQ_SK(MT, DV)                                                                     \
-  hipLaunchKernelGGL((skinny_kernel<MT, I8, DV, 8>), dim3(grid), dim3(512), 0, st, ta, kcb, A, \
+  hipLaunchKernelGGL((skinny_kernel<MT, ET, DV, 8>), dim3(grid), dim3(512), 0, st, ta, kcb, A, \
                      W, nb, c, ldc, scale)
   const int dvw = decoder_variant(W.decoder, W.q);
 #define NQ_SK2(MT) \
@@ -215,17 +225,17 @@ static hipError_t skinny_launch(const MatmulOperand& A, const MatmulOperand& W, 
   return hipGetLastError();
 }
 
-template <bool I8>
+template <int ET>
 static hipError_t skinny(int stages, const MatmulOperand& A, const MatmulOperand& W, int64_t K,
                          float* c, int64_t ldc, float scale, void* ws, hipStream_t st) {
   const int nb = (int)(K / 8);
   const int64_t mp = (A.rows + 15) / 16 * 16;
-  constexpr int EB = I8 ? 1 : 2;
+  constexpr int EB = ET == ET_I8 ? 1 : 2;
   const int64_t kp = (K * EB + 127) / 128 * 128 / EB;
   const int nbp = (int)(kp / 8);
   const int kcb = (int)(kp * EB / 16);
   u32x4* ta = reinterpret_cast<u32x4*>(ws);
-  if (stages & 1) launch_tiles<I8>(A, nb, mp, nbp, (void*)ta, st);
+  if (stages & 1) launch_tiles<ET>(A, nb, mp, nbp, (void*)ta, st);
   if (!(stages & 2)) return hipGetLastError();
   // W in column ranges whose code words stay below 2^31 bytes (buffer-load offsets)
   const int64_t max_rows = (((int64_t)1 << 31) - 1) / ((int64_t)nb * 4) / 16 * 16;
@@ -236,17 +246,20 @@ static hipError_t skinny(int stages, const MatmulOperand& A, const MatmulOperand
     Wc.beta = W.beta + r0 * ((nb + 15) / 16);
     Wc.scales = W.scales + r0;
     Wc.rows = rows;
-    const hipError_t e = skinny_launch<I8>(A, Wc, ta, kcb, nb, c + r0, ldc, scale, st);
+    const hipError_t e = skinny_launch<ET>(A, Wc, ta, kcb, nb, c + r0, ldc, scale, st);
     if (e != hipSuccess) return e;
   }
   return hipGetLastError();
 }
 
-hipError_t launch_matmul_skinny(int stages, bool i8, const MatmulOperand& A,
+hipError_t launch_matmul_skinny(int stages, int et, const MatmulOperand& A,
                                 const MatmulOperand& W, int64_t K, float* c, int64_t ldc,
                                 float scale, void* ws, hipStream_t st) {
-  return i8 ? skinny<true>(stages, A, W, K, c, ldc, scale, ws, st)
-            : skinny<false>(stages, A, W, K, c, ldc, scale, ws, st);
+  switch (et) {
+    case ET_I8: return skinny<ET_I8>(stages, A, W, K, c, ldc, scale, ws, st);
+    case ET_F16: return skinny<ET_F16>(stages, A, W, K, c, ldc, scale, ws, st);
+    default: return skinny<ET_BF16>(stages, A, W, K, c, ldc, scale, ws, st);
+  }
 }
 
 }  // namespace nq

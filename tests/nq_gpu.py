@@ -28,20 +28,23 @@ def u32(t, shape=None):
     return a if shape is None else a.reshape(shape)
 
 
-def oracle_encode(x32, q, k, base=None, decoder="full", strategy="first"):
+def oracle_encode(x32, q, k, base=None, decoder="full", strategy="first", mult=None):
     """Packed oracle codes (rows, nb), beta words (rows, nbw) and scales (rows,)."""
-    codes, t, r = nestquant.quantize_rows(x32, q, k, base, strategy=strategy, decoder=decoder)
+    codes, t, r = nestquant.quantize_rows(x32, q, k, base, strategy=strategy, decoder=decoder,
+                                          mult=mult)
     return layout.pack_codes(codes), layout.pack_beta(t), r
 
 
-def upload_coded(codes_w, beta_w, scales, rows, cols, q, k, base, decoder=0):
-    """Oracle-packed arrays -> a device Coded operand (decoder: 0 full, 1 NestQuantM)."""
+def upload_coded(codes_w, beta_w, scales, rows, cols, q, k, base, decoder=0, mult=None):
+    """Oracle-packed arrays -> a device Coded operand (decoder: 0 full, 1 NestQuantM; mult:
+    the betas' multiples of base, None for 1..k)."""
     torch = torch_mod()
     from paper_2502_09720_amd import Coded
     c = torch.from_numpy(np.ascontiguousarray(codes_w).reshape(-1).view(np.int32)).cuda()
     b = torch.from_numpy(np.ascontiguousarray(beta_w).reshape(-1).view(np.int32)).cuda()
     s = torch.from_numpy(np.ascontiguousarray(scales, dtype=np.float32)).cuda()
-    return Coded(c, b, s, rows, cols, q, k, base, decoder)
+    return Coded(c, b, s, rows, cols, q, k, base, decoder,
+                 None if mult is None else tuple(int(v) for v in mult))
 
 
 def first_mismatch(a, b):

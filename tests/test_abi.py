@@ -63,8 +63,18 @@ def _pd(decoder, strategy=0):
     return p
 
 
+def _pm(mult, k=4, q=14):
+    p = _p(q=q, k=k)
+    for i, m in enumerate(mult):
+        p.mult[i] = m
+    return p
+
+
 @pytest.mark.parametrize("case", [
     dict(p=_pd(2)), dict(p=_pd(-1)), dict(p=_pd(0, 2)), dict(p=_pd(0, -1)),
+    dict(p=_pm((1, 2, 2, 3))), dict(p=_pm((3, 2, 4, 5))), dict(p=_pm((1, 2, 3, 65))),
+    dict(p=_pm((0, 1, 2, 3))), dict(p=_pm((1, 2, 3, 4), k=3)), dict(p=_pm((2, 3, 0, 0), k=3)),
+    dict(p=_pm((-1, 2, 3, 4))),
     dict(p=None), dict(p=_p(q=1)), dict(p=_p(q=17)), dict(p=_p(k=0)), dict(p=_p(k=5)),
     dict(p=_p(base=0.0)), dict(p=_p(base=-1.0)), dict(p=_p(base=float("nan"))),
     dict(p=_p(base=1e-9)), dict(cols=12), dict(cols=0), dict(cols=65544), dict(rows=-1),
@@ -170,6 +180,18 @@ def test_matmul_int8_needs_small_kq(lib, q, k, ok):
             assert b"int8" in lib.nq_last_error()
 
 
+@pytest.mark.parametrize("q,mult,ok", [(16, (1, 2, 3), True), (16, (1, 2, 4), False),
+                                       (7, (2, 5, 9), True), (7, (2, 5, 10), False),
+                                       (2, (10, 20, 31), True), (2, (10, 20, 32), False)])
+def test_matmul_int8_needs_small_multiples(lib, q, mult, ok):
+    """With a beta table the int8 bound is 2q * mult_k <= 127 (|m X2| <= 2q m)."""
+    good, test = _p(), _pm(mult, k=len(mult), q=q)
+    for pa, pw in ((good, test), (test, good)):
+        st = lib.nq_matmul_stages(7, ctypes.byref(pa), FAKE, FAKE, FAKE, 0, ctypes.byref(pw),
+                                  FAKE, FAKE, FAKE, 200, 64, FAKE, 200, FAKE, 0, S)
+        assert st == (0 if ok else 2)
+
+
 def test_matmul_empty_is_noop(lib):
     p = _p()
     assert lib.nq_matmul(ctypes.byref(p), NULL, NULL, NULL, 0, ctypes.byref(p), NULL, NULL,
@@ -185,12 +207,12 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
 
 
 def test_params_layout():
-    """nq_params is {int32 q, int32 k, double base, int32 decoder, int32 strategy}: 24 bytes,
-    base at offset 8, decoder at 16, strategy at 20."""
+    """nq_params is {int32 q, int32 k, double base, int32 decoder, int32 strategy,
+    int32 mult[4]}: 40 bytes, base at offset 8, decoder at 16, strategy at 20, mult at 24."""
     from paper_2502_09720_amd.binding import _Params
-    assert ctypes.sizeof(_Params) == 24
+    assert ctypes.sizeof(_Params) == 40
     assert _Params.base.offset == 8 and _Params.decoder.offset == 16
-    assert _Params.strategy.offset == 20
+    assert _Params.strategy.offset == 20 and _Params.mult.offset == 24
 
 
 @pytest.mark.parametrize("case", [

@@ -32,7 +32,7 @@ def nq():
 
 
 def check_encode(nq, store, x32, dtype, q, k, base=None, ld_pad=0, decoder="full",
-                 strategy="first"):
+                 strategy="first", mult=None):
     torch = __import__("torch")
     rows, cols = x32.shape
     if ld_pad:
@@ -42,13 +42,13 @@ def check_encode(nq, store, x32, dtype, q, k, base=None, ld_pad=0, decoder="full
     else:
         xd = to_device(store, dtype)
     got = nq.encode(xd, q=q, k=k, base=base, decoder=0 if decoder == "full" else 1,
-                    strategy=nq.FIRST_BETA if strategy == "first" else nq.OPT_BETA)
+                    strategy=nq.FIRST_BETA if strategy == "first" else nq.OPT_BETA, mult=mult)
     torch.cuda.synchronize()
     nb = cols // 8
     gc = u32(got.codes, (rows, nb))
     gb = u32(got.beta, (rows, (nb + 15) // 16))
     gs = got.scales.cpu().numpy()
-    oc, ob, os_ = oracle_encode(x32, q, k, base, decoder, strategy)
+    oc, ob, os_ = oracle_encode(x32, q, k, base, decoder, strategy, mult)
     assert first_mismatch(gs.view(np.uint32), os_.view(np.uint32)) is None, \
         "scales: " + first_mismatch(gs.view(np.uint32), os_.view(np.uint32))
     m = first_mismatch(gc, oc)
@@ -567,3 +567,124 @@ def test_rotate_then_encode_parity(nq):
     _, t_plain, _ = nestquant.quantize_rows(x32[:8], 14, 4)
     _, t_rot, _ = nestquant.quantize_rows(yr[:8], 14, 4)
     assert (t_rot == 4).mean() < (t_plain == 4).mean()
+
+
+# ---------------------------------------------------------------------------------------
+# Beta sets as integer multiples of base (beta_t = m_t base), as the App. F dynamic program
+# chooses them from the grid (1/2){1..50}/q = {1..50} / (2q).  Tiles m * X2 use bf16 while
+# 2q m_k <= 256, fp16 beyond (exact to 2048), int8 while 2q m_k <= 127.
+# ---------------------------------------------------------------------------------------
+MULT_ENCODE_CASES = [
+    # (seed, rows, cols, dtype, dist, q, mult, strategy, decoder)
+    (50, 40, 512, "bf16", "t4", 16, (6, 8, 10, 15), "first", "full"),
+    (51, 30, 1000, "f32", "normal", 14, (3, 5, 9), "first", "full"),
+    (52, 3, 20000, "bf16", "normal", 14, (2, 3, 5, 8), "first", "full"),
+    (53, 40, 256, "bf16", "t4", 16, (6, 8, 10, 15), "opt", "full"),
+    (54, 40, 256, "f16", "normal", 16, (5, 7, 11, 50), "first", "m"),
+    (55, 64, 64, "f32", "normal", 7, (4,), "first", "full"),
+    (56, 9, 4096, "bf16", "t4", 12, (7, 9, 12, 20), "opt", "m"),
+]
+
+
+@pytest.mark.parametrize("case", MULT_ENCODE_CASES,
+                         ids=lambda c: f"s{c[0]}-{c[1]}x{c[2]}-q{c[5]}-{c[7]}-{c[8]}")
+def test_encode_parity_beta_multiples(nq, case):
+    seed, rows, cols, dtype, dist, q, mult, strategy, decoder = case
+    store, x32 = workloads.random_rows(seed, rows, cols, dtype=dtype, dist=dist)
+    check_encode(nq, store, x32, dtype, q, len(mult), base=1.0 / (2 * q), decoder=decoder,
+                 strategy=strategy, mult=mult)
+
+
+@pytest.mark.parametrize("out_dtype", ["f32", "bf16"])
+def test_decode_parity_beta_multiples(nq, out_dtype):
+    torch = __import__("torch")
+    from oracle import layout
+    q, mult = 16, (6, 8, 10, 15)
+    base = 1.0 / (2 * q)
+    _, x32 = workloads.random_rows(57, 45, 520, dtype="f32", dist="t4")
+    oc, ob, os_ = oracle_encode(x32, q, 4, base, mult=mult)
+    coded = upload_coded(oc, ob, os_, 45, 520, q, 4, base, mult=mult)
+    out = nq.decode(coded, out_dtype={"f32": torch.float32, "bf16": torch.bfloat16}[out_dtype])
+    torch.cuda.synchronize()
+    got = decoded_to_f64(out, out_dtype)
+    want = nestquant.decode_rows(layout.unpack_codes(oc), layout.unpack_beta(ob, 65), os_, q,
+                                 base, mult=mult)
+    assert not (np.abs(got - want) > ulp_in(out_dtype, want)).any()
+
+
+def _oracle_product_mult(A32, W32, qa, qw, ma, mw, decoder="full"):
+    from oracle import layout
+    ba, bw = 1.0 / (2 * qa), 1.0 / (2 * qw)
+    ca, ta, ra = nestquant.quantize_rows(A32, qa, len(ma), ba, decoder=decoder, mult=ma)
+    cw, tw, rw = nestquant.quantize_rows(W32, qw, len(mw), bw, decoder=decoder, mult=mw)
+    C = nestquant.coded_matmul(ca, ta, ra, qa, ba, cw, tw, rw, qw, bw, decoder, decoder, ma, mw)
+    A = (layout.pack_codes(ca), layout.pack_beta(ta), ra, ba)
+    W = (layout.pack_codes(cw), layout.pack_beta(tw), rw, bw)
+    return C, A, W, (ta, tw)
+
+
+MULT_MATMUL_CASES = [
+    # (seed, M, N, K, qa, qw, mult_a, mult_w, int8, decoder)
+    (60, 64, 256, 512, 16, 16, (6, 8, 10, 15), (6, 8, 10, 15), False, "full"),     # fp16
+    (61, 257, 129, 1032, 16, 14, (6, 8, 10, 15), (2, 3, 5, 8), False, "full"),     # fp16
+    (62, 130, 70, 72, 14, 14, (2, 3, 5, 8), (1, 2, 4, 7), False, "full"),          # bf16
+    (63, 16, 300, 2048, 14, 14, (2, 3, 5, 8), (1, 2, 3, 4), False, "full"),        # bf16
+    (64, 300, 200, 264, 16, 16, (1, 2, 3), (1, 3), True, "full"),                  # int8
+    (65, 40, 300, 1032, 16, 16, (5, 7, 11, 50), (6, 8, 10, 15), False, "full"),    # fp16
+    (66, 64, 256, 512, 16, 16, (6, 8, 10, 15), (6, 8, 10, 15), False, "m"),        # fp16, bytes
+    (67, 300, 130, 264, 16, 16, (6, 8, 10, 15), (3, 4, 5, 7), False, "m"),         # fp16
+    (68, 33, 100, 1024, 10, 10, (2, 5, 6), (3, 6), True, "m"),                     # int8
+]
+
+
+@pytest.mark.parametrize("case", MULT_MATMUL_CASES,
+                         ids=lambda c: f"{c[1]}x{c[2]}x{c[3]}-q{c[4]}/{c[5]}-{'i8' if c[8] else 'f'}-{c[9]}")
+def test_matmul_parity_beta_multiples(nq, case):
+    torch = __import__("torch")
+    seed, M, N, K, qa, qw, ma, mw, i8, decoder = case
+    _, A32 = workloads.random_rows(seed, M, K, dtype="bf16", dist="t4")
+    _, W32 = workloads.random_rows(seed + 1000, N, K, dtype="bf16", scale=0.02)
+    C, (ac, ab, ar, ba), (wc, wb, wr, bw), _ = _oracle_product_mult(A32, W32, qa, qw, ma, mw,
+                                                                     decoder)
+    dec = 0 if decoder == "full" else 1
+    a = upload_coded(ac, ab, ar, M, K, qa, len(ma), ba, dec, mult=ma)
+    w = upload_coded(wc, wb, wr, N, K, qw, len(mw), bw, dec, mult=mw)
+    got = nq.matmul(a, w, int8=i8)
+    torch.cuda.synchronize()
+    g = got.cpu().numpy().astype(np.float64)
+    rel = np.linalg.norm(g - C) / max(np.linalg.norm(C), 1e-300)
+    assert rel <= (1e-6 if i8 else MATMUL_RTOL), f"relative Frobenius error {rel}"
+    assert np.all(np.abs(g - C) <= 1e-5 * np.abs(C).max() + 1e-30)
+
+
+@pytest.mark.parametrize("M,N,K", [(40, 300, 1032), (300, 200, 264)])
+def test_matmul_fp16_tiles_exact(nq, M, N, K):
+    """With multiples beyond bf16's exact range the decode stage writes m * X2 of every
+    block as exact fp16 integers (the oracle's integer tiles), zero-padded to the grid."""
+    torch = __import__("torch")
+    ma, mw, q = (6, 8, 10, 15), (5, 7, 11, 50), 16
+    _, A32 = workloads.random_rows(76, M, K, dtype="bf16", dist="t4")
+    _, W32 = workloads.random_rows(77, N, K, dtype="bf16", scale=0.02)
+    _, (ac, ab, ar, ba), (wc, wb, wr, bw), (ta, tw) = _oracle_product_mult(A32, W32, q, q, ma, mw)
+    a = upload_coded(ac, ab, ar, M, K, q, 4, ba, mult=ma)
+    w = upload_coded(wc, wb, wr, N, K, q, 4, bw, mult=mw)
+    ws = torch.zeros(nq.matmul_workspace_size(M, N, K), dtype=torch.uint8, device="cuda")
+    out = torch.empty(M, N, device="cuda")
+    nq.matmul(a, w, out=out, workspace=ws, stages=nq.STAGE_DECODE)
+    torch.cuda.synchronize()
+    buf = ws.cpu().numpy().view(np.float16).astype(np.float64)
+    kp = -(-K // 64) * 64
+    from oracle import layout
+    TA = nestquant.integer_tiles(layout.unpack_codes(ac), ta, q, mult=ma)
+    if M <= 64:
+        tiles = [(0, -(-M // 16) * 16, TA)]
+    else:
+        TW = nestquant.integer_tiles(layout.unpack_codes(wc), tw, q, mult=mw)
+        assert np.abs(TW).max() > 256          # beyond bf16's exact integers
+        mp, np_ = -(-M // 256) * 256, -(-N // 256) * 256
+        tiles = [(0, mp, TA), (mp * kp, np_, TW)]
+    for off, rows_p, T in tiles:
+        got = buf[off:off + rows_p * kp].reshape(rows_p, kp)
+        want = np.zeros((rows_p, kp))
+        want[:T.shape[0], :T.shape[1]] = T
+        assert np.array_equal(got, want), first_mismatch(got, want)
