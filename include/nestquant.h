@@ -188,6 +188,41 @@ nq_status nq_rotate(const void* x, nq_dtype x_dtype, int64_t rows, int64_t cols,
  * an invalid K). */
 int64_t nq_matmul_workspace_size(int64_t M, int64_t N, int64_t K);
 
+/* Statistics for choosing the beta set (App. F): for n sample 8-vectors v (normalized as
+ * Alg. 3 normalizes rows, i.e. x / r) and m candidate betas, the squared error of coding
+ * v_p at beta_i and whether that coding overloads.
+ *   q, decoder  the code: 2 <= q <= 16 and an nq_decoder value;
+ *   v        device, n x 8 floats, 16-byte aligned (input);
+ *   betas    host, m doubles, finite, > 0 and strictly increasing, 1 <= m <= 64;
+ *   mse      device, n x m doubles, row p at mse + p*m (output);
+ *   overload device, n x m bytes, 1 where the coding overloads, else 0 (output).
+ * Per pair: y = fl32(v_p * fl32(1 / beta_i)); P = the nearest E8 point (Alg. 5 with
+ * nq_encode's tie rules); X2 = decode(encode(P)) with the decoder (Alg. 1, 2); overload is
+ * X2 != P (Sec. 4.1); mse = sum over l = 0..7, in that order, of d_l^2 with
+ * d_l = fl64(fl64(beta_i * X2_l) / 2 - v_l), every step rounded in fp64.  Samples with
+ * |v| / beta_1 >= 2^21 or non-finite entries give unspecified values.  n = 0 is a no-op;
+ * n < 2^31. */
+nq_status nq_beta_stats(int32_t q, int32_t decoder, const float* v, int64_t n,
+                        const double* betas, int32_t m, double* mse, uint8_t* overload,
+                        void* hip_stream);
+
+/* Alg. 6 (App. F): the k of the m grid betas that minimize the First-beta error of the n
+ * samples under the DP's model, from nq_beta_stats' outputs (device mse and overload, n x m).
+ *   1 <= k <= m <= 64; n < 2^31;
+ *   chosen   device, k int32 (output): the indices into the grid, increasing, or all -1 if
+ *            every grid beta overloads some sample;
+ *   loss     device, one double (output): the minimized total squared error (+inf with -1s).
+ * dp[i][j] is the least total error of the samples that do not overload at beta_i, coded
+ * with beta_i and j - 1 smaller betas under First-beta; the step from the next smaller chosen
+ * beta s adds the errors at beta_i of the samples that overload at beta_s but not at beta_i
+ * (s = 0: a virtual beta at which every sample overloads).  The answer is the least dp[i][k]
+ * over the betas at which no sample overloads.  Every cost is summed over the samples in
+ * index order, one fp64 addition at a time; ties go to the smallest index.  Scratch memory of
+ * (m + 1)^2 doubles comes from the stream-ordered allocator of the current device
+ * (hipMallocAsync / hipFreeAsync on hip_stream). */
+nq_status nq_beta_dp(const double* mse, const uint8_t* overload, int64_t n, int32_t m,
+                     int32_t k, int32_t* chosen, double* loss, void* hip_stream);
+
 /* Sizes of the code and beta-index arrays for a rows x cols matrix (-1 if invalid). */
 int64_t nq_codes_words(int64_t rows, int64_t cols);
 int64_t nq_beta_words(int64_t rows, int64_t cols);

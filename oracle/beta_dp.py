@@ -14,6 +14,8 @@ TEST INFRASTRUCTURE ONLY (see the package docstring).
   The answer is dp[i][k] for an i at which no vector overloads (readings: the least such
   dp[i][k], the smallest i on a tie; a beta set in which nothing fits is not returned).
   Alg. 6's model equals the First-beta error whenever overload is monotone in beta.
+  Reading on the rounding: each cost is summed over the vectors in index order, one fp64
+  addition at a time, and the minima take the first s (and the first i) on exact ties.
 * ``first_beta_loss``: the total First-beta error of a given beta subset (what Alg. 6
   minimizes), for checking the DP against brute force.
 * ``synthetic_frontier``: Sec. 6.1's experiment at a small size: for each (q, k) the DP picks
@@ -71,7 +73,8 @@ def dp_betas(mse, over, k):
     for i in range(1, m + 1):
         for s in range(0, i):
             cond = ov[:, s] & ~ov[:, i]
-            cost[s, i] = float(ms[cond, i].sum())
+            terms = np.where(cond, ms[:, i], 0.0)
+            cost[s, i] = float(np.cumsum(terms)[-1]) if n else 0.0   # sequential order
     dp = np.full((m + 1, k + 1), INF)
     frm = np.full((m + 1, k + 1), -1, dtype=np.int64)
     dp[0, 0] = 0.0

@@ -16,6 +16,8 @@ from .binding import (  # noqa: F401
     STAGE_DECODE,
     Coded,
     NQError,
+    beta_dp,
+    beta_stats,
     decode,
     default_base,
     encode,

@@ -58,6 +58,12 @@ def library():
                                          u32p, f32p, i64, i64, f32p, i64, vp, i64, vp]
         lib.nq_rotate.argtypes = [vp, ctypes.c_int, i64, i64, i64, f32p, i64, vp]
         lib.nq_rotate.restype = ctypes.c_int
+        i32 = ctypes.c_int32
+        lib.nq_beta_stats.argtypes = [i32, i32, vp, i64, ctypes.POINTER(ctypes.c_double), i32,
+                                      vp, vp, vp]
+        lib.nq_beta_stats.restype = ctypes.c_int
+        lib.nq_beta_dp.argtypes = [vp, vp, i64, i32, i32, vp, vp, vp]
+        lib.nq_beta_dp.restype = ctypes.c_int
         lib.nq_matmul_workspace_size.argtypes = [i64, i64, i64]
         lib.nq_matmul_workspace_size.restype = i64
         for f in ("nq_encode", "nq_decode", "nq_matmul", "nq_matmul_ex", "nq_matmul_stages"):
@@ -235,3 +241,33 @@ def rotate(x, out=None, stream=None):
 
 def matmul_workspace_size(M, N, K):
     return library().nq_matmul_workspace_size(M, N, K)
+
+
+def beta_stats(v, betas, q, decoder=DECODER_FULL, stream=None):
+    """nq_beta_stats: for sample 8-vectors v (n x 8 fp32 cuda tensor) and the increasing
+    candidate betas (a sequence of at most 64 floats), the squared coding error mse (n x m
+    fp64) and the overload flags (n x m uint8) of every sample at every beta."""
+    import torch
+    if v.dim() != 2 or v.shape[1] != 8 or v.dtype != torch.float32 or not v.is_contiguous():
+        raise ValueError("v must be a contiguous n x 8 float32 cuda tensor")
+    n, m = v.shape[0], len(betas)
+    mse = torch.empty(n, m, dtype=torch.float64, device=v.device)
+    over = torch.empty(n, m, dtype=torch.uint8, device=v.device)
+    b = (ctypes.c_double * m)(*[float(x) for x in betas])
+    _check(library().nq_beta_stats(int(q), int(decoder), ctypes.c_void_p(v.data_ptr()), n, b,
+                                   m, ctypes.c_void_p(mse.data_ptr()),
+                                   ctypes.c_void_p(over.data_ptr()), _stream(stream)))
+    return mse, over
+
+
+def beta_dp(mse, over, k, stream=None):
+    """nq_beta_dp (Alg. 6): the k grid indices (int32 cuda tensor, increasing; -1 if every
+    beta overloads) minimizing the First-beta error, and that error (fp64 cuda scalar)."""
+    import torch
+    n, m = mse.shape
+    chosen = torch.empty(k, dtype=torch.int32, device=mse.device)
+    loss = torch.empty((), dtype=torch.float64, device=mse.device)
+    _check(library().nq_beta_dp(ctypes.c_void_p(mse.data_ptr()), ctypes.c_void_p(over.data_ptr()),
+                                n, m, int(k), ctypes.c_void_p(chosen.data_ptr()),
+                                ctypes.c_void_p(loss.data_ptr()), _stream(stream)))
+    return chosen, loss

@@ -219,6 +219,51 @@ nq_status nq_rotate(const void* x, nq_dtype x_dtype, int64_t rows, int64_t cols,
                     who);
 }
 
+nq_status nq_beta_stats(int32_t q, int32_t decoder, const float* v, int64_t n,
+                        const double* betas, int32_t m, double* mse, uint8_t* overload,
+                        void* hip_stream) {
+  const char* who = "nq_beta_stats";
+  if (q < 2 || q > 16) return fail(NQ_ERR_INVALID_ARG, "%s: q=%d outside [2,16]", who, q);
+  if (decoder != NQ_DECODER_FULL && decoder != NQ_DECODER_M)
+    return fail(NQ_ERR_INVALID_ARG, "%s: decoder=%d is not an nq_decoder", who, decoder);
+  if (m < 1 || m > 64) return fail(NQ_ERR_INVALID_ARG, "%s: m=%d outside [1,64]", who, m);
+  if (n < 0 || n >= kMaxRows)
+    return fail(NQ_ERR_INVALID_ARG, "%s: n=%lld outside [0, 2^31)", who, (long long)n);
+  if (!betas) return fail(NQ_ERR_INVALID_ARG, "%s: betas is NULL", who);
+  nq::BetaGrid g{};
+  g.m = m;
+  for (int i = 0; i < m; ++i) {
+    if (!std::isfinite(betas[i]) || !(betas[i] > 0.0) || (i > 0 && !(betas[i] > betas[i - 1])))
+      return fail(NQ_ERR_INVALID_ARG, "%s: betas must be finite, > 0 and increasing", who);
+    g.beta[i] = betas[i];
+  }
+  if (n == 0) return ok();
+  if (!v || !mse || !overload) return fail(NQ_ERR_INVALID_ARG, "%s: NULL array pointer", who);
+  if (!aligned16(v)) return fail(NQ_ERR_INVALID_ARG, "%s: v must be 16-byte aligned", who);
+  return hip_status(nq::launch_beta_stats(v, n, g, q, decoder, mse, overload,
+                                          (hipStream_t)hip_stream),
+                    who);
+}
+
+nq_status nq_beta_dp(const double* mse, const uint8_t* overload, int64_t n, int32_t m,
+                     int32_t k, int32_t* chosen, double* loss, void* hip_stream) {
+  const char* who = "nq_beta_dp";
+  if (m < 1 || m > 64) return fail(NQ_ERR_INVALID_ARG, "%s: m=%d outside [1,64]", who, m);
+  if (k < 1 || k > m) return fail(NQ_ERR_INVALID_ARG, "%s: k=%d outside [1, m]", who, k);
+  if (n < 0 || n >= kMaxRows)
+    return fail(NQ_ERR_INVALID_ARG, "%s: n=%lld outside [0, 2^31)", who, (long long)n);
+  if ((n > 0 && (!mse || !overload)) || !chosen || !loss)
+    return fail(NQ_ERR_INVALID_ARG, "%s: NULL array pointer", who);
+  hipStream_t st = (hipStream_t)hip_stream;
+  void* ws = nullptr;
+  hipError_t e = hipMallocAsync(&ws, nq::beta_dp_workspace(m), st);
+  if (e != hipSuccess) return hip_status(e, who);
+  e = nq::launch_beta_dp(mse, overload, n, m, k, chosen, loss, ws, st);
+  const hipError_t f = hipFreeAsync(ws, st);
+  if (e != hipSuccess) return hip_status(e, who);
+  return hip_status(f, who);
+}
+
 int64_t nq_matmul_workspace_size(int64_t M, int64_t N, int64_t K) {
   if (M < 0 || N < 0 || K < 8 || K % 8 || K > kMaxCols) return -1;
   if (M == 0 || N == 0) return 0;

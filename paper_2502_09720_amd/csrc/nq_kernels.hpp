@@ -70,6 +70,17 @@ hipError_t rotate_set_attributes();
 hipError_t launch_rotate(const void* x, int dtype, int64_t rows, int n, int64_t ld_x, float* y,
                          int64_t ld_y, hipStream_t st);
 
+// Beta-set statistics and Alg. 6 (nq_beta): at most 64 candidate betas.
+struct BetaGrid {
+  int m;
+  double beta[64];
+};
+hipError_t launch_beta_stats(const float* v, int64_t n, const BetaGrid& g, int q, int decoder,
+                             double* mse, uint8_t* ov, hipStream_t st);
+size_t beta_dp_workspace(int m);
+hipError_t launch_beta_dp(const double* mse, const uint8_t* ov, int64_t n, int m, int k,
+                          int32_t* chosen, double* loss, void* ws, hipStream_t st);
+
 // M at or below this uses the skinny kernel; above it, decode-once.
 constexpr int64_t kFusedMaxM = 64;
 

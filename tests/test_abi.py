@@ -232,3 +232,40 @@ def test_rotate_rejects(lib, case):
 def test_rotate_zero_rows_is_noop(lib):
     assert lib.nq_rotate(NULL, 0, 0, 4096, 4096, NULL, 4096, S) == 0
     assert lib.nq_rotate(NULL, 0, 0, 14336, 14336, NULL, 14336, S) == 0
+
+
+def _betas(vals):
+    return (ctypes.c_double * len(vals))(*vals)
+
+
+@pytest.mark.parametrize("case", [
+    dict(q=1), dict(q=17), dict(decoder=2), dict(m=0), dict(m=65), dict(n=-1),
+    dict(n=1 << 31), dict(betas=None), dict(vals=(0.1, 0.1)), dict(vals=(0.2, 0.1)),
+    dict(vals=(0.0, 0.1)), dict(vals=(float("inf"),)), dict(vals=(float("nan"), 1.0)),
+    dict(v=NULL), dict(mse=NULL), dict(v=ctypes.c_void_p(0x1004)),
+])
+def test_beta_stats_rejects(lib, case):
+    args = dict(q=16, decoder=0, v=FAKE, n=10, vals=(0.1, 0.2, 0.3), mse=FAKE)
+    args.update(case)
+    vals = args["vals"]
+    m = case.get("m", len(vals))
+    b = None if "betas" in case else _betas(vals + (1.0,) * max(0, m - len(vals)))
+    st = lib.nq_beta_stats(args["q"], args["decoder"], args["v"], args["n"], b, m, args["mse"],
+                           FAKE, S)
+    assert st == 1
+
+
+def test_beta_stats_empty_is_noop(lib):
+    assert lib.nq_beta_stats(16, 0, NULL, 0, _betas((0.1, 0.2)), 2, NULL, NULL, S) == 0
+
+
+@pytest.mark.parametrize("case", [
+    dict(m=0), dict(m=65), dict(k=0), dict(k=5), dict(n=-1), dict(mse=NULL), dict(chosen=NULL),
+    dict(loss=NULL),
+])
+def test_beta_dp_rejects(lib, case):
+    args = dict(mse=FAKE, n=10, m=4, k=2, chosen=FAKE, loss=FAKE)
+    args.update(case)
+    st = lib.nq_beta_dp(args["mse"], FAKE, args["n"], args["m"], args["k"], args["chosen"],
+                        args["loss"], S)
+    assert st == 1
