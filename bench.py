@@ -18,6 +18,8 @@ import os
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -42,6 +44,10 @@ def parse():
     ap.add_argument("--gemv", action="store_true",
                     help="the paper's GEMV: one coded 8192-vector times a coded 8192 x 8192 "
                          "matrix, q=16, k=4, NestQuantM and full decoders, against HBM")
+    ap.add_argument("--frontier", action="store_true",
+                    help="Sec. 6.1 on the GPU: A, B 4096 x 4096 iid N(0,1); for each (q, k) "
+                         "the beta set chosen by Alg. 6 from (1/2){1..50}/q, both coded, "
+                         "multiplied from the codes; rate and RMSE against sqrt(Gamma(R))")
     ap.add_argument("--copy-bytes", type=int, default=0,
                     help="calibration only: time a plain device-to-device copy of this many "
                          "bytes (the reference for the HBM byte counters)")
@@ -100,6 +106,103 @@ def gemv_roofline(args):
                       "config": {"workload": "GEMV a (1x8192) W^T (8192x8192), W N(0,0.02^2)"},
                       "results": res,
                       "paper_context": "NestQuantM 60 us on an NVIDIA A100 (App. E table)"}))
+
+
+def gamma_bound(R):
+    """Gamma(R) (Sec. 2.1): the least inner-product distortion per entry at rate R for iid
+    N(0, 1) vectors: 2 2^-2R - 2^-4R above R*, the tangent line from (0, 1) below it."""
+    phi = lambda x: 2.0 * 2.0 ** (-2 * x) - 2.0 ** (-4 * x)               # noqa: E731
+    dphi = lambda x: np.log(2) * (-4.0 * 2.0 ** (-2 * x) + 4.0 * 2.0 ** (-4 * x))  # noqa: E731
+    lo, hi = 0.1, 3.0
+    for _ in range(100):                       # touching point: (phi(R) - 1) / R = phi'(R)
+        mid = 0.5 * (lo + hi)
+        if ((phi(mid) - 1.0) / mid - dphi(mid)) * ((phi(lo) - 1.0) / lo - dphi(lo)) > 0:
+            lo = mid
+        else:
+            hi = mid
+    rs = 0.5 * (lo + hi)
+    return phi(R) if R >= rs else 1.0 - (1.0 - phi(rs)) * R / rs
+
+
+def frontier(args):
+    """Sec. 6.1 (Fig. 3) at the paper's size on the GPU.  For each (q, k): nq_beta_stats of
+    2^18 N(0, 1) sample 8-vectors at the 50 grid betas {1..50} / (2q), nq_beta_dp for k of
+    them, nq_encode of A and B with those multiples (base 1 / (2q)), nq_matmul, and the
+    normalized RMSE sqrt(mean((A_hat B_hat^T - A B^T)^2) / n) against sqrt(Gamma(R)) at the
+    entropy rate R = log2 q + H(beta usage) / 8.  The same (q, k) with the uniform grid
+    (base 10 / (kq)) is reported beside it.  One JSON line per point, then a summary line."""
+    import torch
+    import paper_2502_09720_amd as nq
+    nq.library()
+    dev = torch.device("cuda")
+    n = 4096
+    g = torch.Generator(device=dev)
+    g.manual_seed(61)
+    A = torch.randn(n, n, generator=g, device=dev, dtype=torch.float32)
+    B = torch.randn(n, n, generator=g, device=dev, dtype=torch.float32)
+    cal = torch.randn(1 << 18, 8, generator=g, device=dev, dtype=torch.float32)
+    exact = A.double() @ B.double().T
+    grid = np.arange(1, 51)
+
+    def usage_bits(c, k):
+        words = c.beta
+        idx = torch.stack([(words >> (2 * j)) & 3 for j in range(16)], 1).reshape(c.rows, -1)
+        idx = idx[:, : c.cols // 8].reshape(-1).long()
+        p = torch.bincount(idx, minlength=4)[:k].double()
+        p = p[p > 0] / p.sum()
+        return float(-(p * torch.log2(p)).sum())
+
+    def point(q, k, base, mult):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev[0].record()
+        a = nq.encode(A, q=q, k=k, base=base, mult=mult)
+        ev[1].record()
+        b = nq.encode(B, q=q, k=k, base=base, mult=mult)
+        ev[2].record()
+        C = nq.matmul(a, b)
+        ev[3].record()
+        torch.cuda.synchronize()
+        err = float(torch.sqrt(((C.double() - exact) ** 2).mean() / n))
+        h = 0.5 * (usage_bits(a, k) + usage_bits(b, k))
+        rate = float(np.log2(q) + h / 8.0)
+        return {"rate_bits": rate, "rate_fixed_bits": float(np.log2(q) + np.log2(k) / 8),
+                "rmse": err, "sqrt_gamma": float(np.sqrt(gamma_bound(rate))),
+                "encode_ms": ev[0].elapsed_time(ev[1]), "matmul_ms": ev[2].elapsed_time(ev[3])}
+
+    pts = []
+    for q in (3, 4, 5, 6, 7, 8, 10, 12, 14, 16):
+        betas = grid / (2.0 * q)
+        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        e0.record()
+        mse, over = nq.beta_stats(cal, betas, q)
+        e1.record()
+        for k in (1, 2, 3, 4):
+            e1b = torch.cuda.Event(enable_timing=True)
+            e1b.record()
+            chosen, loss = nq.beta_dp(mse, over, k)
+            e2.record()
+            torch.cuda.synchronize()
+            idx = chosen.cpu().numpy()
+            if (idx < 0).any():
+                continue
+            mult = tuple(int(i) + 1 for i in idx)
+            row = {"q": q, "k": k, "betas_times_2q": list(mult),
+                   "beta_stats_ms": e0.elapsed_time(e1), "beta_dp_ms": e1b.elapsed_time(e2)}
+            row["dp"] = point(q, k, 1.0 / (2 * q), mult)
+            row["uniform"] = point(q, k, 10.0 / (k * q), None)
+            pts.append(row)
+            print(json.dumps(row), flush=True)
+    # efficient frontier of the DP points: no other point has lower rate and lower error
+    front = []
+    for r in pts:
+        d = r["dp"]
+        if not any(o["dp"]["rate_bits"] <= d["rate_bits"] and o["dp"]["rmse"] < d["rmse"]
+                   and o is not r for o in pts):
+            front.append((r["q"], r["k"], round(d["rate_bits"], 4), round(d["rmse"], 5),
+                          round(d["rmse"] / d["sqrt_gamma"], 3)))
+    print(json.dumps({"frontier": sorted(front, key=lambda t: t[2]),
+                      "columns": ["q", "k", "rate_bits", "rmse", "rmse_over_sqrt_gamma"],
+                      "n": n, "samples": 1 << 18, "data": "synthetic iid N(0,1)"}))
 
 
 def copy_calibration(args):
@@ -257,6 +360,9 @@ def main():
         return
     if args.gemv:
         gemv_roofline(args)
+        return
+    if args.frontier:
+        frontier(args)
         return
 
     import numpy as np

@@ -216,10 +216,11 @@ nq_status nq_beta_stats(int32_t q, int32_t decoder, const float* v, int64_t n,
  * with beta_i and j - 1 smaller betas under First-beta; the step from the next smaller chosen
  * beta s adds the errors at beta_i of the samples that overload at beta_s but not at beta_i
  * (s = 0: a virtual beta at which every sample overloads).  The answer is the least dp[i][k]
- * over the betas at which no sample overloads.  Every cost is summed over the samples in
- * index order, one fp64 addition at a time; ties go to the smallest index.  Scratch memory of
- * (m + 1)^2 doubles comes from the stream-ordered allocator of the current device
- * (hipMallocAsync / hipFreeAsync on hip_stream). */
+ * over the betas at which no sample overloads.  Every cost is an fp64 sum over the samples
+ * in a fixed 64-ary tree (consecutive groups of 64 terms added in order, then groups of 64
+ * of those sums, and so on); ties go to the smallest index.  Scratch memory of about
+ * (n / 4096 + 1) (m (m + 1) / 2 + m) doubles comes from the stream-ordered allocator of the
+ * current device (hipMallocAsync / hipFreeAsync on hip_stream). */
 nq_status nq_beta_dp(const double* mse, const uint8_t* overload, int64_t n, int32_t m,
                      int32_t k, int32_t* chosen, double* loss, void* hip_stream);
 

@@ -14,8 +14,9 @@ TEST INFRASTRUCTURE ONLY (see the package docstring).
   The answer is dp[i][k] for an i at which no vector overloads (readings: the least such
   dp[i][k], the smallest i on a tie; a beta set in which nothing fits is not returned).
   Alg. 6's model equals the First-beta error whenever overload is monotone in beta.
-  Reading on the rounding: each cost is summed over the vectors in index order, one fp64
-  addition at a time, and the minima take the first s (and the first i) on exact ties.
+  Reading on the rounding: each cost is summed over the vectors in a fixed 64-ary tree
+  (``tree_sum``: consecutive groups of 64 terms added in order, then groups of 64 of those
+  sums, and so on), and the minima take the first s (and the first i) on exact ties.
 * ``first_beta_loss``: the total First-beta error of a given beta subset (what Alg. 6
   minimizes), for checking the DP against brute force.
 * ``synthetic_frontier``: Sec. 6.1's experiment at a small size: for each (q, k) the DP picks
@@ -59,6 +60,19 @@ def block_stats(v64, betas, q, decoder="full"):
     return mse, over
 
 
+def tree_sum(terms, fan=64):
+    """Sum of fp64 terms in a fixed fan-ary tree: consecutive groups of ``fan`` values are
+    added in order (one rounding per addition), level by level, until one value is left.
+    A short last group adds only what it has (padding with +0 changes no value)."""
+    t = np.asarray(terms, dtype=np.float64).ravel()
+    if t.size == 0:
+        return 0.0
+    while t.size > 1:
+        t = np.concatenate([t, np.zeros((-t.size) % fan)]).reshape(-1, fan)
+        t = np.cumsum(t, axis=1)[:, -1]                   # sequential within each group
+    return float(t[0])
+
+
 def dp_betas(mse, over, k):
     """Alg. 6: indices (increasing) of the k betas minimizing the First-beta error, and that
     error; (None, inf) when no beta of the grid is overload-free."""
@@ -73,8 +87,7 @@ def dp_betas(mse, over, k):
     for i in range(1, m + 1):
         for s in range(0, i):
             cond = ov[:, s] & ~ov[:, i]
-            terms = np.where(cond, ms[:, i], 0.0)
-            cost[s, i] = float(np.cumsum(terms)[-1]) if n else 0.0   # sequential order
+            cost[s, i] = tree_sum(np.where(cond, ms[:, i], 0.0))
     dp = np.full((m + 1, k + 1), INF)
     frm = np.full((m + 1, k + 1), -1, dtype=np.int64)
     dp[0, 0] = 0.0

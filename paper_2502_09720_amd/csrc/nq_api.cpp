@@ -256,7 +256,7 @@ nq_status nq_beta_dp(const double* mse, const uint8_t* overload, int64_t n, int3
     return fail(NQ_ERR_INVALID_ARG, "%s: NULL array pointer", who);
   hipStream_t st = (hipStream_t)hip_stream;
   void* ws = nullptr;
-  hipError_t e = hipMallocAsync(&ws, nq::beta_dp_workspace(m), st);
+  hipError_t e = hipMallocAsync(&ws, nq::beta_dp_workspace(n, m), st);
   if (e != hipSuccess) return hip_status(e, who);
   e = nq::launch_beta_dp(mse, overload, n, m, k, chosen, loss, ws, st);
   const hipError_t f = hipFreeAsync(ws, st);

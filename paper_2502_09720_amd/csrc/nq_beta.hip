@@ -6,14 +6,16 @@
 //     rules); the code of P is decoded with the chosen decoder (Alg. 2) to X2, overload is
 //     X2 != P (Sec. 4.1), and mse = sum over l = 0..7, in that order, of
 //     (fl64(beta_i X2_l) / 2 - v_l)^2 in fp64 (no contraction).
-//   beta_cost_kernel: cost[s][i] = sum over p, in index order, of mse[p][i] over the vectors
-//     that overload at s but not at i (s = 0 is a virtual beta at which every vector
-//     overloads).  One wave per i, lane s; each lane adds its terms one at a time in vector
-//     order, so the sums are those of a sequential loop.  The wave also records whether any
-//     vector overloads at i.
+//   beta_cost_*_kernel: cost[s][i] = sum over p of mse[p][i] over the vectors that overload
+//     at s but not at i (s = 0 is a virtual beta at which every vector overloads), and the
+//     number of vectors that overload at i, each summed in a fixed 64-ary tree over the
+//     vectors (groups of 64 consecutive terms in order, level by level), so that the sums
+//     are reproducible and the work spreads over the chip.
 //   beta_dp_kernel: Alg. 6 in one workgroup.  dp[i][j] = min over s < i (first s on ties)
 //     of dp[s][j-1] + cost[s][i], dp[0][0] = 0; the answer is the least dp[i][k] (first i)
 //     over the betas at which no vector overloads, and the backtracked indices.
+#include <algorithm>
+
 #include "nq_device.hpp"
 #include "nq_kernels.hpp"
 
@@ -58,54 +60,90 @@ __global__ __launch_bounds__(256) void beta_stats_kernel(const float* __restrict
   ov[idx] = over ? 1 : 0;
 }
 
-// cost[s * (m + 1) + i] for 0 <= s < i <= m, and any[i] = some vector overloads at beta i.
-// Wave i - 1 handles column i; lane s < i accumulates cost[s][i].
-__global__ __launch_bounds__(64) void beta_cost_kernel(const double* __restrict__ mse,
-                                                       const uint8_t* __restrict__ ov,
-                                                       int64_t n, int m,
-                                                       double* __restrict__ cost,
-                                                       uint8_t* __restrict__ any) {
-  const int i = blockIdx.x + 1;
-  const int s = threadIdx.x;
-  const bool live = s < i;
+// The DP's transition costs, one entry per pair 0 <= s < i <= m at index i (i - 1) / 2 + s
+// (P = m (m + 1) / 2 of them), followed by m overload counts (entry P + i - 1: how many
+// samples overload at beta i).  Each entry is a sum over the samples in a fixed 64-ary tree:
+// consecutive groups of 64 terms are added in order, then groups of 64 group sums, and so
+// on; a short last group adds only the terms it has.
+constexpr int kFan = 64;
+
+__device__ __forceinline__ void pair_of(int idx, int P, int& s, int& i) {
+  if (idx >= P) {               // overload count of beta idx - P + 1
+    s = -1;
+    i = idx - P + 1;
+    return;
+  }
+  int r = (int)((1.0f + sqrtf(1.0f + 8.0f * (float)idx)) * 0.5f);
+  while (r * (r - 1) / 2 > idx) --r;
+  while ((r + 1) * r / 2 <= idx) ++r;
+  i = r;
+  s = idx - r * (r - 1) / 2;
+}
+
+// First two tree levels: workgroup x sums samples [4096 x, 4096 x + 4096) for 256 entries
+// (grid y picks which): each group of 64 samples is staged in LDS (coalesced loads of its
+// rows), summed per entry in sample order, and the 64 group sums are added in order.
+__global__ __launch_bounds__(256) void beta_cost_leaf_kernel(const double* __restrict__ mse,
+                                                            const uint8_t* __restrict__ ov,
+                                                            int64_t n, int m, int Q,
+                                                            double* __restrict__ out) {
+  __shared__ double wsh[kFan * 64];
+  __shared__ uint8_t osh[kFan * 64];
+  const int P = m * (m + 1) / 2;
+  const int idx = blockIdx.y * 256 + threadIdx.x;
+  int s = 0, i = 1;
+  if (idx < Q) pair_of(idx, P, s, i);
+  double node = 0.0;
+  const int64_t first = (int64_t)blockIdx.x * kFan * kFan;
+  for (int b = 0; b < kFan; ++b) {
+    const int64_t p0 = first + (int64_t)b * kFan;
+    if (p0 >= n) break;
+    const int rows = (int)(n - p0 < kFan ? n - p0 : kFan);
+    __syncthreads();                       // the previous group's reads are done
+    for (int e = threadIdx.x; e < rows * m; e += 256) {
+      wsh[e] = mse[p0 * m + e];
+      osh[e] = ov[p0 * m + e];
+    }
+    __syncthreads();
+    if (idx < Q) {
+      double leaf = 0.0;
+      if (s < 0) {
+        for (int j = 0; j < rows; ++j) leaf = leaf + (double)osh[j * m + i - 1];
+      } else {
+        for (int j = 0; j < rows; ++j) {
+          const bool os = s == 0 || osh[j * m + s - 1] != 0;
+          if (os && osh[j * m + i - 1] == 0) leaf = leaf + wsh[j * m + i - 1];
+        }
+      }
+      node = node + leaf;
+    }
+  }
+  if (idx < Q) out[(int64_t)blockIdx.x * Q + idx] = node;
+}
+
+// Higher levels: output node x is the in-order sum of input nodes 64 x .. 64 x + 63.
+__global__ __launch_bounds__(256) void beta_cost_node_kernel(const double* __restrict__ in,
+                                                            int64_t cnt, int Q,
+                                                            double* __restrict__ out) {
+  const int idx = blockIdx.y * 256 + threadIdx.x;
+  if (idx >= Q) return;
+  const int64_t c0 = (int64_t)blockIdx.x * kFan;
+  const int kids = (int)(cnt - c0 < kFan ? cnt - c0 : kFan);
   double acc = 0.0;
-  uint32_t seen = 0u;
-  constexpr int U = 8;
-  int64_t p = 0;
-  for (; p + U <= n; p += U) {
-    double w[U];
-    uint32_t oi[U], os[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int64_t row = (p + u) * m;
-      w[u] = mse[row + i - 1];
-      oi[u] = ov[row + i - 1];
-      os[u] = (live && s > 0) ? ov[row + s - 1] : 1u;
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (os[u] && !oi[u]) acc = acc + w[u];
-      seen |= oi[u];
-    }
-  }
-  for (; p < n; ++p) {
-    const int64_t row = p * m;
-    const double w = mse[row + i - 1];
-    const uint32_t oi = ov[row + i - 1];
-    const uint32_t os = (live && s > 0) ? ov[row + s - 1] : 1u;
-    if (os && !oi) acc = acc + w;
-    seen |= oi;
-  }
-  if (live) cost[s * (m + 1) + i] = acc;
-  if (s == 0) any[i] = seen ? 1 : 0;
+  for (int c = 0; c < kids; ++c) acc = acc + in[(c0 + c) * Q + idx];
+  out[(int64_t)blockIdx.x * Q + idx] = acc;
+}
+
+__global__ __launch_bounds__(256) void beta_cost_zero_kernel(int Q, double* __restrict__ out) {
+  for (int e = threadIdx.x; e < Q; e += 256) out[e] = 0.0;
 }
 
 constexpr int kDpMax = 64;
 
-__global__ __launch_bounds__(64) void beta_dp_kernel(const double* __restrict__ cost,
-                                                     const uint8_t* __restrict__ any, int m,
+__global__ __launch_bounds__(64) void beta_dp_kernel(const double* __restrict__ cost, int m,
                                                      int k, int32_t* __restrict__ chosen,
                                                      double* __restrict__ loss) {
+  const int P = m * (m + 1) / 2;   // cost of (s, i) at i (i - 1) / 2 + s; counts after
   __shared__ double dp[kDpMax + 1][kDpMax + 1];
   __shared__ int frm[kDpMax + 1][kDpMax + 1];
   const int tid = threadIdx.x;
@@ -124,7 +162,7 @@ __global__ __launch_bounds__(64) void beta_dp_kernel(const double* __restrict__ 
       for (int s = 0; s < i; ++s) {
         const double prev = dp[s][j - 1];
         if (prev == INFINITY) continue;
-        const double cand = prev + cost[s * (m + 1) + i];
+        const double cand = prev + cost[i * (i - 1) / 2 + s];
         if (best > cand) {
           best = cand;
           arg = s;
@@ -139,7 +177,7 @@ __global__ __launch_bounds__(64) void beta_dp_kernel(const double* __restrict__ 
     double best = INFINITY;
     int pos = -1;
     for (int i = 1; i <= m; ++i)
-      if (!any[i] && dp[i][k] < best) {
+      if (cost[P + i - 1] == 0.0 && dp[i][k] < best) {
         best = dp[i][k];
         pos = i;
       }
@@ -165,15 +203,39 @@ hipError_t launch_beta_stats(const float* v, int64_t n, const BetaGrid& g, int q
   return hipGetLastError();
 }
 
-size_t beta_dp_workspace(int m) { return (size_t)(m + 1) * (m + 1) * 8 + 256; }
+// Tree buffers: level 2 (one node per 4096 samples) and level 3, ping-ponged upward.
+static int64_t cost_entries(int m) { return (int64_t)m * (m + 1) / 2 + m; }
+static int64_t level2_nodes(int64_t n) { return (n + kFan * kFan - 1) / (kFan * kFan); }
+
+size_t beta_dp_workspace(int64_t n, int m) {
+  const int64_t Q = cost_entries(m);
+  const int64_t a = std::max<int64_t>(level2_nodes(n), 1);
+  const int64_t b = (a + kFan - 1) / kFan;
+  return (size_t)((a + b) * Q * 8);
+}
 
 hipError_t launch_beta_dp(const double* mse, const uint8_t* ov, int64_t n, int m, int k,
                           int32_t* chosen, double* loss, void* ws, hipStream_t st) {
-  double* cost = reinterpret_cast<double*>(ws);
-  uint8_t* any = reinterpret_cast<uint8_t*>(cost + (m + 1) * (m + 1));
-  hipLaunchKernelGGL(beta_cost_kernel, dim3((unsigned)m), dim3(64), 0, st, mse, ov, n, m, cost,
-                     any);
-  hipLaunchKernelGGL(beta_dp_kernel, dim3(1), dim3(64), 0, st, cost, any, m, k, chosen, loss);
+  const int Q = (int)cost_entries(m);
+  const unsigned qy = (unsigned)((Q + 255) / 256);
+  double* buf[2] = {reinterpret_cast<double*>(ws), nullptr};
+  int64_t cnt = level2_nodes(n);
+  buf[1] = buf[0] + std::max<int64_t>(cnt, 1) * Q;
+  int cur = 0;
+  if (n == 0) {
+    hipLaunchKernelGGL(beta_cost_zero_kernel, dim3(1), dim3(256), 0, st, Q, buf[0]);
+  } else {
+    hipLaunchKernelGGL(beta_cost_leaf_kernel, dim3((unsigned)cnt, qy), dim3(256), 0, st, mse,
+                       ov, n, m, Q, buf[0]);
+    while (cnt > 1) {
+      const int64_t next = (cnt + kFan - 1) / kFan;
+      hipLaunchKernelGGL(beta_cost_node_kernel, dim3((unsigned)next, qy), dim3(256), 0, st,
+                         buf[cur], cnt, Q, buf[cur ^ 1]);
+      cur ^= 1;
+      cnt = next;
+    }
+  }
+  hipLaunchKernelGGL(beta_dp_kernel, dim3(1), dim3(64), 0, st, buf[cur], m, k, chosen, loss);
   return hipGetLastError();
 }
 

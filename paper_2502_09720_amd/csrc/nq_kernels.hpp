@@ -77,7 +77,7 @@ struct BetaGrid {
 };
 hipError_t launch_beta_stats(const float* v, int64_t n, const BetaGrid& g, int q, int decoder,
                              double* mse, uint8_t* ov, hipStream_t st);
-size_t beta_dp_workspace(int m);
+size_t beta_dp_workspace(int64_t n, int m);
 hipError_t launch_beta_dp(const double* mse, const uint8_t* ov, int64_t n, int m, int k,
                           int32_t* chosen, double* loss, void* ws, hipStream_t st);
 

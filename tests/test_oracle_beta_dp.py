@@ -77,6 +77,30 @@ def test_frontier_respects_the_bound():
         assert by[(16, k)] < by[(8, k)]
 
 
+def test_tree_sum_order():
+    """tree_sum adds groups of 64 in order, level by level: exact on integers, equal to the
+    plain sum for at most 64 terms added left to right, and different from other orders
+    on terms chosen so that rounding depends on the grouping."""
+    rng = np.random.default_rng(3)
+    ints = rng.integers(0, 1000, 10000).astype(np.float64)
+    assert beta_dp.tree_sum(ints) == ints.sum()
+    x = rng.standard_normal(50)
+    acc = 0.0
+    for v in x:
+        acc = acc + v
+    assert beta_dp.tree_sum(x) == acc
+    t = np.array([1.0] + [2.0 ** -53] * 127)               # 1 + 63 tiny, then 64 tiny
+    # grouping matters: the first group rounds each tiny term away, the second keeps them
+    g1 = 1.0
+    for _ in range(63):
+        g1 = g1 + 2.0 ** -53
+    g2 = 0.0
+    for _ in range(64):
+        g2 = g2 + 2.0 ** -53
+    assert beta_dp.tree_sum(t) == g1 + g2 != 1.0
+    assert beta_dp.tree_sum([]) == 0.0
+
+
 def test_entropy_of_usage():
     assert beta_dp.usage_entropy_bits(np.array([1, 2, 3, 4] * 5), 4) == pytest.approx(2.0)
     assert beta_dp.usage_entropy_bits(np.array([3] * 9), 4) == 0.0
