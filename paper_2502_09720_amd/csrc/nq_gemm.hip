@@ -61,47 +61,84 @@ using CfgMid = Cfg<256, 128, 4, 2, 3>;
 using CfgBig = Cfg<256, 256, 4, 2, 2>;
 }  // namespace gemm
 
-// m * X2 of every block of a coded operand into ws[rows_p][nb_p blocks] (zero padding), one
-// thread per block (grid_block): 8 bf16 or fp16 (16 B) per block, or 8 int8 (8 B) for the
-// int8 contraction.
+// m * X2 of every block of a coded operand into ws[rows_p][nb_p blocks] (zero padding): 8
+// bf16 or fp16 (16 B) per block, or 8 int8 (8 B) for the int8 contraction.  The workspace
+// is one flat array of rows_p * nb_p blocks; workgroup w covers TB = 256 * TPB consecutive
+// blocks of it, thread t the blocks w TB + t + 256 i (i < TPB), so each load and store
+// instruction of a wave touches consecutive blocks.  Every thread issues the loads of all
+// its blocks before decoding any, which keeps TPB loads in flight per thread.
+constexpr int kTilesPerThread = 4;
+
 template <int ET, int DV>
 __global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__ codes,
                                                     const uint32_t* __restrict__ beta,
-                                                    int64_t rows, int nb, int64_t rows_p,
-                                                    int nb_p, int q, uint32_t m2q,
-                                                    uint32_t mtab, int lg,
+                                                    int64_t rows, int nb, int64_t total,
+                                                    int nb_p, float inv_nbp, int q,
+                                                    uint32_t m2q, uint32_t mtab,
                                                     void* __restrict__ ws) {
   constexpr bool I8 = ET == ET_I8;
-  const GridPos g = grid_block(nb_p, lg);
-  const int64_t row = g.rb + g.lr;
-  const int j = g.j;
-  if (row >= rows_p || j >= nb_p) return;
+  constexpr int TPB = kTilesPerThread;
+  constexpr uint32_t OOB = 0x80000000u;   // past every buffer range below: reads 0
   using V = typename std::conditional<I8, u32x2, u32x4>::type;
-  V out = {};
-  if (row < rows && j < nb) {
-    const int nbw = (nb + 15) >> 4;
-    const uint32_t w = __builtin_nontemporal_load(codes + g.rb * nb + (uint32_t)(g.lr * nb + j));
-    const uint32_t bw = beta[g.rb * nbw + (uint32_t)(g.lr * nbw + (j >> 4))];
-    const int m = beta_mult(mtab, (bw >> (2 * (j & 15))) & 3u);
-    if constexpr (I8) {
-      out = decode_tile_i8<DV>(w, m, q, m2q);
-    } else {
-      out = decode_tile_16<DV, ET == ET_F16>(w, m, q, m2q);
-    }
+  const int64_t g0 = (int64_t)blockIdx.x * (256 * TPB);
+  // the workgroup's first block as (row0, j0); every other block is an offset
+  // o < nb_p + 256 TPB <= 2^14 past (row0, 0), split by a float division checked once in
+  // each direction.  Code and beta
+  // words are read through buffer resources based at row0 (32-bit offsets; the range check
+  // makes rows past the operand read as zero).
+  const int64_t row0 = g0 / nb_p;
+  const int j0 = (int)(g0 - row0 * nb_p);
+  const int nbw = (nb + 15) >> 4;
+  const int64_t rows_left = rows > row0 ? rows - row0 : 0;
+  const int reach = (j0 + 256 * TPB + nb_p - 1) / nb_p;     // rows this workgroup touches
+  const int64_t span = rows_left < reach ? rows_left : reach;
+  const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(codes + row0 * nb), (short)0, (int)(span * nb * 4), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(beta + row0 * nbw), (short)0, (int)(span * nbw * 4), 0x00020000);
+  uint32_t w[TPB], bw[TPB];
+  int jj[TPB];
+  bool pad[TPB];
+#pragma unroll
+  for (int i = 0; i < TPB; ++i) {
+    const int o = j0 + (int)threadIdx.x + 256 * i;
+    int r = (int)((float)o * inv_nbp);
+    if ((int)__umul24((uint32_t)r, (uint32_t)nb_p) > o) --r;
+    if ((int)__umul24((uint32_t)(r + 1), (uint32_t)nb_p) <= o) ++r;
+    const int j = o - (int)__umul24((uint32_t)r, (uint32_t)nb_p);
+    jj[i] = j;
+    pad[i] = j >= nb || r >= span;
+    const uint32_t co = pad[i] ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nb) + (uint32_t)j);
+    const uint32_t bo = pad[i] ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nbw) + (uint32_t)(j >> 4));
+    w[i] = __builtin_amdgcn_raw_buffer_load_b32(rc, co, 0, 0);
+    bw[i] = __builtin_amdgcn_raw_buffer_load_b32(rb, bo, 0, 0);
   }
-  reinterpret_cast<V*>(ws)[g.rb * nb_p + (uint32_t)(g.lr * nb_p + j)] = out;
+#pragma unroll
+  for (int i = 0; i < TPB; ++i) {
+    const int64_t g = g0 + (int)threadIdx.x + 256 * i;
+    if (g >= total) break;
+    const int m = beta_mult(mtab, (bw[i] >> (2 * (jj[i] & 15))) & 3u);
+    V out;
+    if constexpr (I8) {
+      out = decode_tile_i8<DV>(w[i], m, q, m2q);
+    } else {
+      out = decode_tile_16<DV, ET == ET_F16>(w[i], m, q, m2q);
+    }
+    if (pad[i]) out = V{};                 // padding past the operand's rows or columns
+    reinterpret_cast<V*>(ws)[g] = out;
+  }
 }
 
 // Launch tiles_kernel for one operand with its decoder.
 template <int ET>
 void launch_tiles(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void* ws,
                   hipStream_t st) {
-  int lg;
-  int64_t wgs;
-  grid_shape(rows_p, nb_p, lg, wgs);
+  const int64_t total = rows_p * nb_p;
+  const int64_t wgs = (total + 256 * kTilesPerThread - 1) / (256 * kTilesPerThread);
+  const float inv = 1.0f / (float)nb_p;
 #define NQ_TL(DV)                                                                            \
   hipLaunchKernelGGL((tiles_kernel<ET, DV>), dim3((unsigned)wgs), dim3(256), 0, st, X.codes,    \
-                     X.beta, X.rows, nb, rows_p, nb_p, X.q, X.m2q, X.mtab, lg, ws)
+                     X.beta, X.rows, nb, total, nb_p, inv, X.q, X.m2q, X.mtab, ws)
   switch (decoder_variant(X.decoder, X.q)) {
     case 0: NQ_TL(0); break;
     case 1: NQ_TL(1); break;
