@@ -188,6 +188,25 @@ nq_status nq_rotate(const void* x, nq_dtype x_dtype, int64_t rows, int64_t cols,
  * an invalid K). */
 int64_t nq_matmul_workspace_size(int64_t M, int64_t N, int64_t K);
 
+/* The whole hot path in one call: Alg. 3 on the rows of the activation x (as nq_encode,
+ * writing A's codes, beta indices and scales), then C = A_hat * W_hat^T from the codes (as
+ * nq_matmul_ex).  The encoder also writes A's decoded tiles m * X2 (Alg. 2 of the codes it
+ * has just chosen; the lattice point itself wherever it passed the overload test) straight
+ * into the product's workspace, so A is never decoded in a separate pass; W is decoded as in
+ * nq_matmul_ex.  Results are those of nq_encode followed by nq_matmul_ex (with
+ * NQ_CONTRACT_INT8 in flags, of nq_matmul_stages with that flag).
+ *   flags    0 or NQ_CONTRACT_INT8;
+ *   x, x_dtype, M (rows), K (cols), ld_x, a_codes, a_beta, a_scales: as nq_encode with pa;
+ *   pw, w_codes, w_beta, w_scales, N, c, ldc: as nq_matmul_ex;
+ *   workspace: device, 16-byte aligned, at least nq_matmul_workspace_size(M, N, K) bytes.
+ * Validation as nq_encode and nq_matmul_ex; nothing is launched on error. */
+nq_status nq_encode_matmul(int32_t flags, const nq_params* pa, const void* x, nq_dtype x_dtype,
+                           int64_t M, int64_t K, int64_t ld_x, uint32_t* a_codes,
+                           uint32_t* a_beta, float* a_scales, const nq_params* pw,
+                           const uint32_t* w_codes, const uint32_t* w_beta,
+                           const float* w_scales, int64_t N, float* c, int64_t ldc,
+                           void* workspace, int64_t workspace_bytes, void* hip_stream);
+
 /* Statistics for choosing the beta set (App. F): for n sample 8-vectors v (normalized as
  * Alg. 3 normalizes rows, i.e. x / r) and m candidate betas, the squared error of coding
  * v_p at beta_i and whether that coding overloads.

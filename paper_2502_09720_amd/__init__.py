@@ -21,6 +21,7 @@ from .binding import (  # noqa: F401
     decode,
     default_base,
     encode,
+    encode_matmul,
     library,
     library_path,
     matmul,

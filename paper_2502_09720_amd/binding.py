@@ -56,6 +56,10 @@ def library():
                                      f32p, i64, vp, i64, vp]
         lib.nq_matmul_stages.argtypes = [ctypes.c_int32, pp, u32p, u32p, f32p, i64, pp, u32p,
                                          u32p, f32p, i64, i64, f32p, i64, vp, i64, vp]
+        lib.nq_encode_matmul.argtypes = [ctypes.c_int32, pp, vp, ctypes.c_int, i64, i64, i64,
+                                         u32p, u32p, f32p, pp, u32p, u32p, f32p, i64, f32p, i64,
+                                         vp, i64, vp]
+        lib.nq_encode_matmul.restype = ctypes.c_int
         lib.nq_rotate.argtypes = [vp, ctypes.c_int, i64, i64, i64, f32p, i64, vp]
         lib.nq_rotate.restype = ctypes.c_int
         i32 = ctypes.c_int32
@@ -222,6 +226,48 @@ def matmul(a, w, stream=None, out=None, workspace=None, stages=STAGE_DECODE | ST
     else:
         _check(lib.nq_matmul_stages(stages | (CONTRACT_INT8 if int8 else 0), *args))
     return out
+
+
+def encode_matmul(x, w, q=14, k=4, base=None, decoder=DECODER_FULL, strategy=FIRST_BETA,
+                  mult=None, stream=None, out=None, coded_out=None, workspace=None,
+                  int8=False):
+    """nq_encode_matmul: codes the activation x (2-D cuda tensor, as ``encode``) and returns
+    (its Coded operand, C = A_hat W_hat^T) from one call, the encoder writing A's decoded
+    tiles straight into the product's workspace.  The same results as ``encode`` then
+    ``matmul``."""
+    import torch
+    if x.dim() != 2 or x.stride(1) != 1 or not x.is_cuda:
+        raise ValueError("x must be a 2-D cuda tensor with unit column stride")
+    M, K = x.shape
+    if K != w.cols:
+        raise ValueError("K mismatch")
+    lib = library()
+    if coded_out is None:
+        codes = torch.empty(max(lib.nq_codes_words(M, K), 0), dtype=torch.int32, device=x.device)
+        beta = torch.empty(max(lib.nq_beta_words(M, K), 0), dtype=torch.int32, device=x.device)
+        scales = torch.empty(M, dtype=torch.float32, device=x.device)
+    else:
+        codes, beta, scales = coded_out
+    if out is None:
+        out = torch.empty(M, w.rows, dtype=torch.float32, device=x.device)
+    need = lib.nq_matmul_workspace_size(M, w.rows, K)
+    if need < 0:
+        raise ValueError("invalid matmul shape")
+    if need > 0 and (workspace is None or workspace.numel() * workspace.element_size() < need):
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+    pa = _params(q, k, base, decoder, strategy, mult)
+    pw = _params(w.q, w.k, w.base, w.decoder, mult=w.mult)
+    _check(lib.nq_encode_matmul(
+        CONTRACT_INT8 if int8 else 0, ctypes.byref(pa), ctypes.c_void_p(x.data_ptr()),
+        _dtype_code(x.dtype), M, K, x.stride(0), ctypes.c_void_p(codes.data_ptr()),
+        ctypes.c_void_p(beta.data_ptr()), ctypes.c_void_p(scales.data_ptr()), ctypes.byref(pw),
+        ctypes.c_void_p(w.codes.data_ptr()), ctypes.c_void_p(w.beta.data_ptr()),
+        ctypes.c_void_p(w.scales.data_ptr()), w.rows, ctypes.c_void_p(out.data_ptr()),
+        out.stride(0), ctypes.c_void_p(workspace.data_ptr() if need > 0 else 0), need,
+        _stream(stream)))
+    a = Coded(codes, beta, scales, M, K, int(q), int(k), pa.base, int(decoder),
+              None if mult is None else tuple(int(v) for v in mult))
+    return a, out
 
 
 def rotate(x, out=None, stream=None):

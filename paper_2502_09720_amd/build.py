@@ -34,16 +34,35 @@ def hipcc():
     raise RuntimeError("hipcc not found")
 
 
-def build(verbose=False):
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), *FLAGS, "-I", INCLUDE, "-o", tmp] + [os.path.join(CSRC, s) for s in SOURCES]
+def _run(cmd):
     res = subprocess.run(cmd, capture_output=True, text=True)
     log = "\n".join(l for l in (res.stdout + res.stderr).splitlines()
                     if "packed-fp32-ops" not in l)
     if res.returncode != 0:
         raise RuntimeError("hipcc failed:\n" + " ".join(cmd) + "\n" + log)
-    if verbose and log.strip():
-        print(log)
+    return log
+
+
+def build(verbose=False):
+    """Compile every source to an object in parallel (a temporary directory), then link."""
+    import concurrent.futures
+    import tempfile
+    with tempfile.TemporaryDirectory(prefix="nq_build_") as tmpdir:
+        objs, cmds = [], []
+        for src in SOURCES:
+            obj = os.path.join(tmpdir, src + ".o")
+            objs.append(obj)
+            cmds.append([hipcc(), *[f for f in FLAGS if f != "-shared"], "-c", "-I", INCLUDE,
+                         "-o", obj, os.path.join(CSRC, src)])
+        workers = max(1, min(len(cmds), os.cpu_count() or 1))
+        with concurrent.futures.ThreadPoolExecutor(workers) as ex:
+            logs = list(ex.map(_run, cmds))
+        tmp = LIB + ".tmp"
+        logs.append(_run([hipcc(), *FLAGS, "-o", tmp] + objs))
+    if verbose:
+        for log in logs:
+            if log.strip():
+                print(log)
     os.replace(tmp, LIB)
     return LIB
 

@@ -114,10 +114,9 @@ const char* nq_last_error(void) { return g_last_error; }
 
 int32_t nq_version(void) { return 400; }
 
-nq_status nq_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t rows,
-                    int64_t cols, int64_t ld_x, uint32_t* codes, uint32_t* beta_idx,
-                    float* scales, void* hip_stream) {
-  const char* who = "nq_encode";
+static nq_status check_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t rows,
+                              int64_t cols, int64_t ld_x, uint32_t* codes, uint32_t* beta_idx,
+                              float* scales, const char* who) {
   if (nq_status s = check_cols(cols, who)) return s;
   if (nq_status s = check_params(p, cols, who)) return s;
   if (x_dtype != NQ_F32 && x_dtype != NQ_F16 && x_dtype != NQ_BF16)
@@ -125,12 +124,16 @@ nq_status nq_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t
   if (rows < 0 || rows >= kMaxRows)
     return fail(NQ_ERR_INVALID_ARG, "%s: rows=%lld outside [0, 2^31)", who, (long long)rows);
   if (ld_x < cols) return fail(NQ_ERR_INVALID_ARG, "%s: ld_x < cols", who);
-  if (rows == 0) return ok();
+  if (rows == 0) return NQ_OK;
   if (!x || !codes || !beta_idx || !scales)
     return fail(NQ_ERR_INVALID_ARG, "%s: NULL array pointer", who);
   if (!aligned16(x) || (ld_x * (int64_t)dtype_size(x_dtype)) % 16 != 0)
     return fail(NQ_ERR_INVALID_ARG, "%s: x and its row stride must be 16-byte aligned", who);
-  nq::EncodeArgs a;
+  return NQ_OK;
+}
+
+static nq::EncodeArgs encode_args(const nq_params* p) {
+  nq::EncodeArgs a{};
   a.q = p->q;
   a.k = p->k;
   a.rq = (float)(1.0 / p->q);
@@ -139,6 +142,19 @@ nq_status nq_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t
   a.decoder = p->decoder;
   a.strategy = p->strategy;
   for (int t = 0; t < 4; ++t) a.beta[t] = (double)beta_mult(p, t) * p->base;
+  a.tiles = nullptr;
+  a.mtab = mult_table(p);
+  return a;
+}
+
+nq_status nq_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t rows,
+                    int64_t cols, int64_t ld_x, uint32_t* codes, uint32_t* beta_idx,
+                    float* scales, void* hip_stream) {
+  const char* who = "nq_encode";
+  if (nq_status s = check_encode(p, x, x_dtype, rows, cols, ld_x, codes, beta_idx, scales, who))
+    return s;
+  if (rows == 0) return ok();
+  const nq::EncodeArgs a = encode_args(p);
   return hip_status(nq::launch_encode(x, (int)x_dtype, rows, (int)cols, ld_x, a, codes, beta_idx,
                                       scales, (hipStream_t)hip_stream),
                     who);
@@ -271,6 +287,50 @@ int64_t nq_matmul_workspace_size(int64_t M, int64_t N, int64_t K) {
   return (int64_t)nq::decode_once_workspace(M, N, K);
 }
 
+// Element type of the product's tiles: int8 on request (2q * mult_k <= 127 for both
+// operands), else bf16 while every |m X2| <= 256, else fp16 (exact up to 2048).
+static nq_status elem_type(const nq_params* pa, const nq_params* pw, bool i8, int& et,
+                           const char* who) {
+  if (i8 && (tile_bound(pa) > 127 || tile_bound(pw) > 127))
+    return fail(NQ_ERR_UNSUPPORTED,
+                "%s: the int8 contraction needs 2q * mult_k <= 127 for both operands (k * q <= "
+                "63 on the uniform grid; |m X2| must fit int8)", who);
+  et = i8 ? nq::ET_I8
+          : (tile_bound(pa) <= 256 && tile_bound(pw) <= 256 ? nq::ET_BF16 : nq::ET_F16);
+  return NQ_OK;
+}
+
+static nq_status check_workspace(int64_t M, int64_t N, int64_t K, void* workspace,
+                                 int64_t workspace_bytes, const char* who) {
+  const int64_t need = nq_matmul_workspace_size(M, N, K);
+  if (workspace_bytes < need || (need > 0 && !workspace))
+    return fail(NQ_ERR_INVALID_ARG, "%s: workspace of %lld bytes needed", who, (long long)need);
+  if (need > 0 && !aligned16(workspace))
+    return fail(NQ_ERR_INVALID_ARG, "%s: workspace must be 16-byte aligned", who);
+  return NQ_OK;
+}
+
+// Padded row length, in blocks, of the activation's tile in the workspace (both paths pad K
+// to 128 bytes per row of tiles).
+static int tile_blocks(int64_t K, int et) {
+  const int64_t eb = et == nq::ET_I8 ? 1 : 2;
+  return (int)((K * eb + 127) / 128 * 128 / eb / 8);
+}
+
+static hipError_t launch_product(int stages, int et, const nq_params* pa, const nq_params* pw,
+                                 const nq::MatmulOperand& A, const nq::MatmulOperand& W,
+                                 int64_t K, float* c, int64_t ldc, void* workspace,
+                                 hipStream_t st) {
+  const float scale = (float)(pa->base * pw->base * 0.25);
+  if (A.rows <= nq::kFusedMaxM)
+    return nq::launch_matmul_skinny(stages, et, A, W, K, c, ldc, scale, workspace, st);
+  static std::once_flag attr_once;
+  static hipError_t attr_err = hipSuccess;
+  std::call_once(attr_once, [] { attr_err = nq::gemm_set_attributes(); });
+  if (attr_err != hipSuccess) return attr_err;
+  return nq::launch_matmul_decode_once(stages, et, A, W, K, c, ldc, scale, workspace, st);
+}
+
 static nq_status matmul_stages(int32_t stages, const nq_params* pa, const uint32_t* a_codes,
                                const uint32_t* a_beta, const float* a_scales, int64_t M,
                                const nq_params* pw, const uint32_t* w_codes,
@@ -285,35 +345,17 @@ static nq_status matmul_stages(int32_t stages, const nq_params* pa, const uint32
   if (nq_status s = check_matmul(pa, a_codes, a_beta, a_scales, M, pw, w_codes, w_beta,
                                  w_scales, N, K, c, ldc, who))
     return s;
-  const bool i8 = (stages & NQ_CONTRACT_INT8) != 0;
-  if (i8 && (tile_bound(pa) > 127 || tile_bound(pw) > 127))
-    return fail(NQ_ERR_UNSUPPORTED,
-                "%s: the int8 contraction needs 2q * mult_k <= 127 for both operands (k * q <= "
-                "63 on the uniform grid; |m X2| must fit int8)", who);
-  // bf16 tiles hold every integer up to 256; larger multiples take fp16 (up to 2048)
-  const int et = i8 ? nq::ET_I8
-                    : (tile_bound(pa) <= 256 && tile_bound(pw) <= 256 ? nq::ET_BF16 : nq::ET_F16);
+  int et = 0;
+  if (nq_status s = elem_type(pa, pw, (stages & NQ_CONTRACT_INT8) != 0, et, who)) return s;
   if (M == 0 || N == 0) return ok();
-  const int64_t need = nq_matmul_workspace_size(M, N, K);
-  if (workspace_bytes < need || (need > 0 && !workspace))
-    return fail(NQ_ERR_INVALID_ARG, "%s: workspace of %lld bytes needed", who, (long long)need);
-  if (need > 0 && !aligned16(workspace))
-    return fail(NQ_ERR_INVALID_ARG, "%s: workspace must be 16-byte aligned", who);
+  if (nq_status s = check_workspace(M, N, K, workspace, workspace_bytes, who)) return s;
   nq::MatmulOperand A{a_codes, a_beta, a_scales, pa->q, nq::magic_2q(pa->q), M, pa->decoder,
                       mult_table(pa)};
   nq::MatmulOperand W{w_codes, w_beta, w_scales, pw->q, nq::magic_2q(pw->q), N, pw->decoder,
                       mult_table(pw)};
-  const float scale = (float)(pa->base * pw->base * 0.25);
-  hipStream_t st = (hipStream_t)hip_stream;
-  if (M <= nq::kFusedMaxM)
-    return hip_status(
-        nq::launch_matmul_skinny(stages, et, A, W, K, c, ldc, scale, workspace, st), who);
-  static std::once_flag attr_once;
-  static hipError_t attr_err = hipSuccess;
-  std::call_once(attr_once, [] { attr_err = nq::gemm_set_attributes(); });
-  if (attr_err != hipSuccess) return hip_status(attr_err, who);
-  return hip_status(
-      nq::launch_matmul_decode_once(stages, et, A, W, K, c, ldc, scale, workspace, st), who);
+  return hip_status(launch_product(stages, et, pa, pw, A, W, K, c, ldc, workspace,
+                                   (hipStream_t)hip_stream),
+                    who);
 }
 
 nq_status nq_matmul_ex(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,
@@ -358,6 +400,47 @@ nq_status nq_matmul(const nq_params* pa, const uint32_t* a_codes, const uint32_t
     if (s == NQ_OK && e != hipSuccess) return hip_status(e, who);
   }
   return s;
+}
+
+
+nq_status nq_encode_matmul(int32_t flags, const nq_params* pa, const void* x, nq_dtype x_dtype,
+                           int64_t M, int64_t K, int64_t ld_x, uint32_t* a_codes,
+                           uint32_t* a_beta, float* a_scales, const nq_params* pw,
+                           const uint32_t* w_codes, const uint32_t* w_beta,
+                           const float* w_scales, int64_t N, float* c, int64_t ldc,
+                           void* workspace, int64_t workspace_bytes, void* hip_stream) {
+  const char* who = "nq_encode_matmul";
+  if ((flags & ~NQ_CONTRACT_INT8) != 0)
+    return fail(NQ_ERR_INVALID_ARG, "%s: flags may only hold NQ_CONTRACT_INT8", who);
+  if (nq_status s = check_encode(pa, x, x_dtype, M, K, ld_x, a_codes, a_beta, a_scales, who))
+    return s;
+  if (nq_status s = check_matmul(pa, a_codes, a_beta, a_scales, M, pw, w_codes, w_beta,
+                                 w_scales, N, K, c, ldc, who))
+    return s;
+  int et = 0;
+  if (nq_status s = elem_type(pa, pw, (flags & NQ_CONTRACT_INT8) != 0, et, who)) return s;
+  if (M == 0 || N == 0) return ok();
+  if (nq_status s = check_workspace(M, N, K, workspace, workspace_bytes, who)) return s;
+  hipStream_t st = (hipStream_t)hip_stream;
+  // 1. encode A; the encoder also writes A's decoded tiles into the workspace
+  nq::EncodeArgs a = encode_args(pa);
+  const int nbp = tile_blocks(K, et);
+  const int64_t rows_p = M <= nq::kFusedMaxM ? (M + 15) / 16 * 16 : (M + 255) / 256 * 256;
+  a.tiles = workspace;
+  a.tile_et = et;
+  a.nb_p = nbp;
+  hipError_t e = nq::launch_encode(x, (int)x_dtype, M, (int)K, ld_x, a, a_codes, a_beta,
+                                   a_scales, st);
+  if (e == hipSuccess) e = nq::launch_tiles_pad(et, workspace, M, (int)(K / 8), rows_p, nbp, st);
+  if (e != hipSuccess) return hip_status(e, who);
+  // 2. decode W (decode-once path) and contract
+  nq::MatmulOperand A{a_codes, a_beta, a_scales, pa->q, nq::magic_2q(pa->q), M, pa->decoder,
+                      mult_table(pa)};
+  nq::MatmulOperand W{w_codes, w_beta, w_scales, pw->q, nq::magic_2q(pw->q), N, pw->decoder,
+                      mult_table(pw)};
+  return hip_status(launch_product(nq::kStageDecodeW | NQ_STAGE_CONTRACT, et, pa, pw, A, W, K,
+                                   c, ldc, workspace, st),
+                    who);
 }
 
 }  // extern "C"

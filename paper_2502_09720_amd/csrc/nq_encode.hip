@@ -209,6 +209,56 @@ __device__ __forceinline__ void encode_block(const float (&v)[8], const float (&
   word = encode_codes(P, a.q, a.rq, a.mq);
 }
 
+// Fused encode-and-multiply: the decoded tile m_t * X2 of block j of `row`, stored where
+// the product's decode stage would put it.  X2 is the lattice point P itself when P is known
+// to be reproduced by the decoder (tile_from_x2), else the decode of the code word
+// (tile_decoded); rows that are not coded get zeros.
+__device__ __forceinline__ void tile_from_x2(const EncodeArgs& a, int64_t row, int j,
+                                             const int (&X2)[8], int t) {
+  const int m = (int)((a.mtab >> (8 * t)) & 0xFFu);
+  const int64_t idx = row * a.nb_p + j;
+  if (a.tile_et == ET_I8) {
+    uint32_t lo = 0u, hi = 0u;
+#pragma unroll
+    for (int l = 0; l < 4; ++l) {
+      lo |= ((uint32_t)(m * X2[l]) & 0xFFu) << (8 * l);
+      hi |= ((uint32_t)(m * X2[4 + l]) & 0xFFu) << (8 * l);
+    }
+    reinterpret_cast<u32x2*>(a.tiles)[idx] = u32x2{lo, hi};
+  } else {
+    uint32_t o[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float lo = (float)(m * X2[2 * i]), hi = (float)(m * X2[2 * i + 1]);
+      o[i] = a.tile_et == ET_F16 ? pack16<true>(lo, hi) : pack16<false>(lo, hi);
+    }
+    reinterpret_cast<u32x4*>(a.tiles)[idx] = u32x4{o[0], o[1], o[2], o[3]};
+  }
+}
+
+__device__ __forceinline__ void tile_decoded(const EncodeArgs& a, int64_t row, int j, uint32_t word,
+                                          int t) {
+  uint32_t X2p[4];
+  if (a.decoder) {
+    decode_word_pk<true>(word, a.q, a.m2q, X2p);
+  } else {
+    decode_word_pk<false>(word, a.q, a.m2q, X2p);
+  }
+  int X2[8];
+#pragma unroll
+  for (int l = 0; l < 8; ++l) X2[l] = (int)(short)((X2p[l >> 1] >> (16 * (l & 1))) & 0xFFFFu);
+  tile_from_x2(a, row, j, X2, t);
+}
+
+__device__ __forceinline__ void tile_zero(const EncodeArgs& a, int64_t row, int j) {
+  const int64_t idx = row * a.nb_p + j;
+  if (a.tile_et == ET_I8) {
+    reinterpret_cast<u32x2*>(a.tiles)[idx] = u32x2{0u, 0u};
+  } else {
+    reinterpret_cast<u32x4*>(a.tiles)[idx] = u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
 // Opt-beta for one block (App. F): every beta is tried; the code of the nearest point of
 // y_t = fl32(x c_t) is decoded (Alg. 2 with the code's decoder) to X2_t and compared with
 // the normalized block x / r: err_t = sum over l = 0..7, in that order, of d_l^2 with
@@ -296,8 +346,9 @@ __device__ __forceinline__ void dd_add_square(double& hi, double& lo, float x) {
 // BPT > 0: the row's blocks stay in registers (read once).  BPT == 0: long rows are
 // streamed, reading each block once for the scale and once more for the codes.  OPT: the
 // Opt-beta strategy (opt_block) instead of First-beta; a separate instantiation, since its
-// registers would lower the occupancy of the First-beta kernel.
-template <typename T, int LANES, int BPT, bool OPT>
+// registers would lower the occupancy of the First-beta kernel.  TILES: also write the
+// decoded tiles of the fused encode-and-multiply (likewise a separate instantiation).
+template <typename T, int LANES, int BPT, bool OPT, bool TILES>
 __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_kernel(
     const T* __restrict__ x, int64_t rows, int cols, int64_t ld_x, EncodeArgs a,
     uint32_t* __restrict__ codes, uint32_t* __restrict__ beta, float* __restrict__ scales) {
@@ -388,6 +439,13 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_kernel(
       }
     }
     if (mine) crow[j] = word;
+    if (TILES && mine) {
+      if (coded) {
+        tile_decoded(a, row, j, word, tsel);
+      } else {
+        tile_zero(a, row, j);
+      }
+    }
     // two-bit beta indices: OR over the 16 consecutive blocks of one word
     uint32_t bits = mine ? ((uint32_t)tsel << (2 * (j & 15))) : 0u;
     constexpr int W = LANES < 16 ? LANES : 16;
@@ -445,11 +503,11 @@ struct SlotMap {
 
 // Finish a block from a given first beta: loop until a point survives (or t = k).
 __device__ __forceinline__ void finish_block(const float (&v)[8], const float (&c)[4], int t,
-                                             const EncodeArgs& a, uint32_t& word, int& tsel) {
+                                             const EncodeArgs& a, uint32_t& word, int& tsel,
+                                             int (&P)[8]) {
   const bool m = a.decoder != 0;
   const float mx = m ? 0.0f : root_bound_f(v);
   const float two_q = (float)(2 * a.q);
-  int P[8];
   for (;;) {
     const float ct = pick4(c, t);
     float y[8];
@@ -536,7 +594,7 @@ __device__ __forceinline__ float skip_threshold(float c, int q) {
   return f;
 }
 
-template <typename T, int LANES, int BPT>
+template <typename T, int LANES, int BPT, bool TILES>
 __global__ __launch_bounds__(256) void encode_wave_kernel(
     const T* __restrict__ x, int64_t rows, int cols, int64_t ld_x, EncodeArgs a,
     uint32_t* __restrict__ codes, uint32_t* __restrict__ beta, float* __restrict__ scales) {
@@ -688,8 +746,19 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
       const int pos = qn + __popcll(mask & ((1ull << lane) - 1ull));
       queue[wave][pos] = ((uint32_t)sl << 2) | (uint32_t)start;
     } else if (valid) {
-      codes_w[rw * nb + j] = coded ? encode_codes(P, a.q, a.rq, a.mq) : 0u;
+      const uint32_t word = coded ? encode_codes(P, a.q, a.rq, a.mq) : 0u;
+      codes_w[rw * nb + j] = word;
       tsl[wave][sl] = (uint8_t)t0;
+      if constexpr (TILES) {
+        // a point kept below the last beta passed the overload test: X2 = P
+        if (!coded) {
+          tile_zero(a, row, j);
+        } else if (t0 < a.k - 1) {
+          tile_from_x2(a, row, j, P, t0);
+        } else {
+          tile_decoded(a, row, j, word, t0);
+        }
+      }
     }
     qn += __popcll(mask);
   }
@@ -714,9 +783,17 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
       for (int tt = 0; tt < 4; ++tt) c[tt] = crow[c2][rw][tt];
       uint32_t word;
       int tsel;
-      finish_block(v, c, t, a, word, tsel);
+      int P[8];
+      finish_block(v, c, t, a, word, tsel, P);
       codes[row * nb + j] = word;
       tsl[w][sl] = (uint8_t)tsel;
+      if constexpr (TILES) {
+        if (tsel < a.k - 1) {
+          tile_from_x2(a, row, j, P, tsel);
+        } else {
+          tile_decoded(a, row, j, word, tsel);
+        }
+      }
     }
   }
   __syncthreads();
@@ -738,38 +815,38 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
 // ---------------------------------------------------------------------------------------
 // launch
 // ---------------------------------------------------------------------------------------
-template <typename T, int LANES, int BPT, bool OPT = false>
+template <typename T, int LANES, int BPT, bool OPT, bool TILES>
 static hipError_t launch_t(const void* x, int64_t rows, int cols, int64_t ld_x,
                            const EncodeArgs& a, uint32_t* codes, uint32_t* beta, float* scales,
                            hipStream_t st) {
   constexpr int WG = LANES > 64 ? LANES : 256;
   constexpr int RPW = WG / LANES;
   const int64_t grid = (rows + RPW - 1) / RPW;
-  hipLaunchKernelGGL((encode_kernel<T, LANES, BPT, OPT>), dim3((unsigned)grid), dim3(WG), 0, st,
+  hipLaunchKernelGGL((encode_kernel<T, LANES, BPT, OPT, TILES>), dim3((unsigned)grid), dim3(WG), 0, st,
                      (const T*)x, rows, cols, ld_x, a, codes, beta, scales);
   return hipGetLastError();
 }
 
-template <typename T, int LANES, int BPT>
+template <typename T, int LANES, int BPT, bool TILES>
 static hipError_t launch_w(const void* x, int64_t rows, int cols, int64_t ld_x,
                            const EncodeArgs& a, uint32_t* codes, uint32_t* beta, float* scales,
                            hipStream_t st) {
   using SM = SlotMap<LANES, BPT>;
   const int64_t rows_per_wg = SM::WGROW ? 1 : 4 * SM::ROWS_PER_WAVE;
   const int64_t grid = (rows + rows_per_wg - 1) / rows_per_wg;
-  hipLaunchKernelGGL((encode_wave_kernel<T, LANES, BPT>), dim3((unsigned)grid), dim3(256), 0, st,
+  hipLaunchKernelGGL((encode_wave_kernel<T, LANES, BPT, TILES>), dim3((unsigned)grid), dim3(256), 0, st,
                      (const T*)x, rows, cols, ld_x, a, codes, beta, scales);
   return hipGetLastError();
 }
 
-template <typename T>
+template <typename T, bool TILES>
 static hipError_t launch_dtype(const void* x, int64_t rows, int cols, int64_t ld_x,
                                const EncodeArgs& a, uint32_t* codes, uint32_t* beta,
                                float* scales, hipStream_t st) {
   const int nb = cols / 8;
   if (a.strategy) {
     // Opt-beta: a lane group of up to 64 holds short rows in registers; longer rows stream
-#define NQ_O(L, B) return launch_t<T, L, B, true>(x, rows, cols, ld_x, a, codes, beta, scales, st)
+#define NQ_O(L, B) return launch_t<T, L, B, true, TILES>(x, rows, cols, ld_x, a, codes, beta, scales, st)
     if (nb <= 8) NQ_O(8, 1);
     if (nb <= 16) NQ_O(16, 1);
     if (nb <= 32) NQ_O(32, 1);
@@ -778,8 +855,8 @@ static hipError_t launch_dtype(const void* x, int64_t rows, int cols, int64_t ld
     NQ_O(1024, 0);
 #undef NQ_O
   }
-#define NQ_W(L, B) return launch_w<T, L, B>(x, rows, cols, ld_x, a, codes, beta, scales, st)
-#define NQ_L(L, B) return launch_t<T, L, B>(x, rows, cols, ld_x, a, codes, beta, scales, st)
+#define NQ_W(L, B) return launch_w<T, L, B, TILES>(x, rows, cols, ld_x, a, codes, beta, scales, st)
+#define NQ_L(L, B) return launch_t<T, L, B, false, TILES>(x, rows, cols, ld_x, a, codes, beta, scales, st)
   // short rows: several rows per lane group, 512 blocks per wave when there are enough rows
   if (nb <= 8) { if (rows >= 4096) NQ_W(8, 8); NQ_W(8, 1); }
   if (nb <= 16) { if (rows >= 2048) NQ_W(16, 8); NQ_W(16, 1); }
@@ -799,10 +876,17 @@ static hipError_t launch_dtype(const void* x, int64_t rows, int cols, int64_t ld
 hipError_t launch_encode(const void* x, int dtype, int64_t rows, int cols, int64_t ld_x,
                          const EncodeArgs& a, uint32_t* codes, uint32_t* beta, float* scales,
                          hipStream_t st) {
+  if (a.tiles) {
+    switch (dtype) {
+      case 0: return launch_dtype<float, true>(x, rows, cols, ld_x, a, codes, beta, scales, st);
+      case 1: return launch_dtype<_Float16, true>(x, rows, cols, ld_x, a, codes, beta, scales, st);
+      default: return launch_dtype<uint16_t, true>(x, rows, cols, ld_x, a, codes, beta, scales, st);
+    }
+  }
   switch (dtype) {
-    case 0: return launch_dtype<float>(x, rows, cols, ld_x, a, codes, beta, scales, st);
-    case 1: return launch_dtype<_Float16>(x, rows, cols, ld_x, a, codes, beta, scales, st);
-    default: return launch_dtype<uint16_t>(x, rows, cols, ld_x, a, codes, beta, scales, st);
+    case 0: return launch_dtype<float, false>(x, rows, cols, ld_x, a, codes, beta, scales, st);
+    case 1: return launch_dtype<_Float16, false>(x, rows, cols, ld_x, a, codes, beta, scales, st);
+    default: return launch_dtype<uint16_t, false>(x, rows, cols, ld_x, a, codes, beta, scales, st);
   }
 }
 

@@ -150,6 +150,41 @@ template void launch_tiles<ET_BF16>(const MatmulOperand&, int, int64_t, int, voi
 template void launch_tiles<ET_F16>(const MatmulOperand&, int, int64_t, int, void*, hipStream_t);
 template void launch_tiles<ET_I8>(const MatmulOperand&, int, int64_t, int, void*, hipStream_t);
 
+// Zero blocks of a tile: the flat range [first, first + count) when cols == 0, else the
+// blocks nb..nb_p-1 of rows 0..rows-1 (cols = nb_p - nb of them per row).
+__global__ __launch_bounds__(256) void tiles_pad_kernel(void* __restrict__ ws, int eb,
+                                                        int64_t first, int64_t count, int nb,
+                                                        int nb_p, int cols) {
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= count) return;
+  int64_t g = first + t;
+  if (cols > 0) {
+    const int64_t r = t / cols;
+    g = r * nb_p + nb + (t - r * cols);
+  }
+  if (eb == 16) {
+    reinterpret_cast<u32x4*>(ws)[g] = u32x4{0u, 0u, 0u, 0u};
+  } else {
+    reinterpret_cast<u32x2*>(ws)[g] = u32x2{0u, 0u};
+  }
+}
+
+hipError_t launch_tiles_pad(int et, void* ws, int64_t rows, int nb, int64_t rows_p, int nb_p,
+                            hipStream_t st) {
+  const int eb = et == ET_I8 ? 8 : 16;
+  if (rows_p > rows) {
+    const int64_t count = (rows_p - rows) * nb_p;
+    hipLaunchKernelGGL(tiles_pad_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, st,
+                       ws, eb, rows * nb_p, count, nb, nb_p, 0);
+  }
+  if (nb_p > nb && rows > 0) {
+    const int64_t count = rows * (nb_p - nb);
+    hipLaunchKernelGGL(tiles_pad_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, st,
+                       ws, eb, (int64_t)0, count, nb, nb_p, nb_p - nb);
+  }
+  return hipGetLastError();
+}
+
 __device__ __forceinline__ void tile_coords(int bid, int tm, int tn, int& pm, int& pn) {
   constexpr int GROUP_M = gemm::GROUP_M;
   // XCD-contiguous numbering: workgroups bid, bid+8, ... run on one XCD
@@ -392,10 +427,8 @@ static hipError_t decode_once(int stages, const MatmulOperand& A, const MatmulOp
   const int kc = (int)(kp * EB / 16);
   u32x4* wa = reinterpret_cast<u32x4*>(ws);
   u32x4* ww = wa + mp * kc;
-  if (stages & 1) {
-    launch_tiles<ET>(A, nb, mp, nbp, (void*)wa, st);
-    launch_tiles<ET>(W, nb, np, nbp, (void*)ww, st);
-  }
+  if (stages & 1) launch_tiles<ET>(A, nb, mp, nbp, (void*)wa, st);
+  if (stages & (1 | kStageDecodeW)) launch_tiles<ET>(W, nb, np, nbp, (void*)ww, st);
   if (!(stages & 2)) return hipGetLastError();
   // 256 x 256 tiles once they give every CU a tile, else 256 x 128
   if ((mp / 256) * (np / 256) >= 256) {

@@ -14,7 +14,14 @@ struct EncodeArgs {
   uint32_t mq;     // ceil(2^20 / q): floor(u / q) = (u * mq) >> 20 for 0 <= u < 2048 q
   int decoder;     // 0: Alg. 2 / Alg. 5, 1: NestQuantM (App. D)
   int strategy;    // 0: First-beta, 1: Opt-beta (App. F)
-  double beta[4];  // fl64(t * base), t = 1..4
+  double beta[4];  // fl64(m_t * base), t = 1..4
+  // Fused encode-and-multiply: when tiles is set, the decoded tile m_t * X2 of every block
+  // is also written to tiles[row * nb_p + j] as the product's decode stage would (ElemType
+  // tile_et: 16 B per block for bf16 / fp16, 8 B for int8; mtab as in MatmulOperand).
+  void* tiles;
+  int tile_et;
+  int nb_p;
+  uint32_t mtab;
 };
 
 struct DecodeArgs {
@@ -46,6 +53,16 @@ hipError_t launch_encode(const void* x, int dtype, int64_t rows, int cols, int64
 hipError_t launch_decode(const uint32_t* codes, const uint32_t* beta, const float* scales,
                          int64_t rows, int cols, void* out, int out_dtype, int64_t ld_out,
                          const DecodeArgs& a, hipStream_t st);
+
+// Stage bits of the launchers: 1 decodes both operands (A's tile and, on the decode-once
+// path, W's), 2 contracts; kStageDecodeW decodes only W (A's tile was written by the
+// fused encoder).
+constexpr int kStageDecodeW = 8;
+
+// Zero the padding of an operand tile written by the fused encoder: rows rows..rows_p-1 and,
+// in the first `rows` rows, blocks nb..nb_p-1.
+hipError_t launch_tiles_pad(int et, void* ws, int64_t rows, int nb, int64_t rows_p, int nb_p,
+                            hipStream_t st);
 
 // Small M (skinny): decode A once into a tile, then decode W straight into MFMA operands.
 // stages: bit 0 decodes into the workspace, bit 1 contracts (see nq_matmul_stages); et: the

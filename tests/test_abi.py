@@ -269,3 +269,27 @@ def test_beta_dp_rejects(lib, case):
     st = lib.nq_beta_dp(args["mse"], FAKE, args["n"], args["m"], args["k"], args["chosen"],
                         args["loss"], S)
     assert st == 1
+
+
+@pytest.mark.parametrize("case", [
+    dict(flags=1), dict(flags=2), dict(flags=8), dict(pa=None), dict(x=NULL), dict(K=12),
+    dict(dtype=9), dict(c=NULL), dict(ldc=10), dict(ws_bytes=0),
+    dict(pa=_p(q=16)),                              # int8 needs k q <= 63
+])
+def test_encode_matmul_rejects(lib, case):
+    p = _p()
+    args = dict(flags=0, pa=p, x=FAKE, dtype=0, M=300, K=64, c=FAKE, ldc=200, ws_bytes=1 << 30)
+    args.update(case)
+    if "pa" in case and case["pa"] is not None and case["pa"].q == 16:
+        args["flags"] = 4
+    pa = None if args["pa"] is None else ctypes.byref(args["pa"])
+    st = lib.nq_encode_matmul(args["flags"], pa, args["x"], args["dtype"], args["M"], args["K"],
+                              args["K"], FAKE, FAKE, FAKE, ctypes.byref(p), FAKE, FAKE, FAKE,
+                              200, args["c"], args["ldc"], FAKE, args["ws_bytes"], S)
+    assert st in (1, 2)
+
+
+def test_encode_matmul_empty_is_noop(lib):
+    p = _p()
+    assert lib.nq_encode_matmul(0, ctypes.byref(p), NULL, 0, 0, 64, 64, NULL, NULL, NULL,
+                                ctypes.byref(p), NULL, NULL, NULL, 0, NULL, 0, NULL, 0, S) == 0

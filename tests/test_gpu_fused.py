@@ -1,0 +1,106 @@
+"""GPU tests of nq_encode_matmul, the whole hot path in one call (the encoder writes the
+activation's decoded tiles into the product's workspace).
+
+Bar: it must equal nq_encode followed by nq_matmul_ex (or nq_matmul_stages with
+NQ_CONTRACT_INT8) bit for bit, codes, beta words, scales and C, since both contract the same
+exact integer tiles with the same kernel; and the product must meet the usual oracle bar
+(relative Frobenius error <= 1e-3).  Cases cover both product paths (M <= 64 and above),
+padding of M and K, fp32 / fp16 / bf16 inputs, both decoders, beta multiples on fp16 tiles,
+Opt-beta, the int8 contraction, streamed long rows and zero rows.
+"""
+
+import numpy as np
+import pytest
+
+import workloads
+from oracle import layout, nestquant
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def nq():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2502_09720_amd as nq
+    nq.library()
+    return nq
+
+
+def _dev(store, dtype):
+    import torch
+    if dtype == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(store).view(np.int16)).cuda().view(torch.bfloat16)
+    return torch.from_numpy(np.ascontiguousarray(store)).cuda()
+
+
+FUSED_CASES = [
+    # (seed, M, N, K, dtype, dist, q, k, mult, decoder, strategy, int8)
+    (1, 300, 200, 264, "bf16", "t4", 14, 4, None, 0, 0, False),
+    (2, 40, 300, 1032, "f16", "normal", 14, 4, None, 0, 0, False),
+    (3, 256, 256, 512, "f32", "normal", 16, 4, None, 1, 0, False),
+    (4, 130, 70, 72, "bf16", "t4", 16, 4, (6, 8, 10, 15), 0, 0, False),
+    (5, 257, 129, 1024, "bf16", "t4", 14, 4, None, 0, 1, False),
+    (6, 100, 64, 264, "bf16", "normal", 15, 4, None, 0, 0, True),
+    (7, 70, 50, 20000, "bf16", "normal", 14, 4, None, 0, 0, False),
+    (8, 16, 100, 4096, "bf16", "t4", 7, 4, None, 1, 0, True),
+    (9, 2, 33, 8, "f32", "normal", 14, 4, None, 0, 0, False),
+    (10, 64, 128, 128, "bf16", "normal", 12, 3, (2, 5, 9), 1, 1, False),
+]
+
+
+@pytest.mark.parametrize("case", FUSED_CASES,
+                         ids=lambda c: f"s{c[0]}-{c[1]}x{c[2]}x{c[3]}-{c[4]}-q{c[6]}")
+def test_encode_matmul_equals_encode_then_matmul(nq, case):
+    import torch
+    seed, M, N, K, dtype, dist, q, k, mult, dec, strat, i8 = case
+    store, x32 = workloads.random_rows(seed, M, K, dtype=dtype, dist=dist)
+    if M > 3:
+        store = store.copy()
+        store[M // 2] = 0                       # a zero row: r = 0, codes 0, tile 0
+        x32 = x32.copy()
+        x32[M // 2] = 0
+    wstore, w32 = workloads.random_rows(seed + 500, N, K, dtype="bf16", scale=0.02)
+    base = None if mult is None else 1.0 / (2 * q)
+    w = nq.encode(_dev(wstore, "bf16"), q=q, k=k, decoder=dec)
+    x = _dev(store, dtype)
+    a1 = nq.encode(x, q=q, k=k, base=base, decoder=dec, strategy=strat, mult=mult)
+    c1 = nq.matmul(a1, w, int8=i8)
+    a2, c2 = nq.encode_matmul(x, w, q=q, k=k, base=base, decoder=dec, strategy=strat,
+                              mult=mult, int8=i8)
+    torch.cuda.synchronize()
+    assert torch.equal(a1.codes, a2.codes)
+    assert torch.equal(a1.beta, a2.beta)
+    assert torch.equal(a1.scales, a2.scales)
+    assert torch.equal(c1, c2), f"max diff {(c1 - c2).abs().max().item()}"
+    # and the oracle's product of the same codes (A from the oracle, W from its own codes)
+    dname = "full" if dec == 0 else "m"
+    sname = "first" if strat == 0 else "opt"
+    bb = nestquant.default_base(q, k) if base is None else base
+    ca, ta, ra = nestquant.quantize_rows(x32, q, k, bb, strategy=sname, decoder=dname, mult=mult)
+    nbk = K // 8
+    wc = layout.unpack_codes(w.codes.cpu().numpy().view(np.uint32).reshape(N, nbk))
+    wt = layout.unpack_beta(w.beta.cpu().numpy().view(np.uint32).reshape(N, -1), nbk)
+    C = nestquant.coded_matmul(ca, ta, ra, q, bb, wc, wt, w.scales.cpu().numpy(), q, w.base,
+                               dname, dname, mult, None)
+    g = c2.cpu().numpy().astype(np.float64)
+    rel = np.linalg.norm(g - C) / max(np.linalg.norm(C), 1e-300)
+    assert rel <= 1e-3, rel
+
+
+def test_encode_matmul_reuses_its_workspace(nq):
+    """Two calls in a row on one workspace (a larger product, then a smaller one with more
+    padding) give the separate path's results: the padding is cleared on every call."""
+    import torch
+    wstore, _ = workloads.random_rows(600, 300, 1024, dtype="bf16", scale=0.02)
+    w = nq.encode(_dev(wstore, "bf16"), 14, 4)
+    ws = torch.full((nq.matmul_workspace_size(300, 300, 1024),), 255, dtype=torch.uint8,
+                    device="cuda")
+    for M, K in ((300, 1024), (70, 1024)):
+        store, _ = workloads.random_rows(601 + M, M, K, dtype="bf16")
+        x = _dev(store, "bf16")
+        _, c2 = nq.encode_matmul(x, w, 14, 4, workspace=ws)
+        c1 = nq.matmul(nq.encode(x, 14, 4), w)
+        torch.cuda.synchronize()
+        assert torch.equal(c1, c2)
