@@ -81,39 +81,80 @@ __device__ __forceinline__ void pair_of(int idx, int P, int& s, int& i) {
 }
 
 // First two tree levels: workgroup x sums samples [4096 x, 4096 x + 4096) for 256 entries
-// (grid y picks which): each group of 64 samples is staged in LDS (coalesced loads of its
-// rows), summed per entry in sample order, and the 64 group sums are added in order.
+// (grid y picks which): each group of 64 samples is staged in LDS (two buffers; the next
+// group's rows are loaded into registers while the current one is summed), summed per entry
+// in sample order, and the 64 group sums are added in order.
 __global__ __launch_bounds__(256) void beta_cost_leaf_kernel(const double* __restrict__ mse,
                                                             const uint8_t* __restrict__ ov,
                                                             int64_t n, int m, int Q,
                                                             double* __restrict__ out) {
-  __shared__ double wsh[kFan * 64];
-  __shared__ uint8_t osh[kFan * 64];
+  constexpr int PER = kFan * 64 / 256;       // staged elements per thread (64 rows, m <= 64)
+  __shared__ double wsh[2][kFan * 64];
+  __shared__ uint8_t osh[2][kFan * 64];
   const int P = m * (m + 1) / 2;
   const int idx = blockIdx.y * 256 + threadIdx.x;
   int s = 0, i = 1;
   if (idx < Q) pair_of(idx, P, s, i);
-  double node = 0.0;
+  const int cs = s > 0 ? s - 1 : i - 1;      // column of the smaller beta (s = 0: none)
   const int64_t first = (int64_t)blockIdx.x * kFan * kFan;
-  for (int b = 0; b < kFan; ++b) {
-    const int64_t p0 = first + (int64_t)b * kFan;
-    if (p0 >= n) break;
-    const int rows = (int)(n - p0 < kFan ? n - p0 : kFan);
-    __syncthreads();                       // the previous group's reads are done
-    for (int e = threadIdx.x; e < rows * m; e += 256) {
-      wsh[e] = mse[p0 * m + e];
-      osh[e] = ov[p0 * m + e];
+  const int groups = (int)(n - first < (int64_t)kFan * kFan ? (n - first + kFan - 1) / kFan : kFan);
+  // buffer resources over this workgroup's samples (at most 4096 m entries, 32-bit offsets);
+  // offsets past a group's rows carry the top bit, outside every range, and read 0
+  constexpr uint32_t OOB = 0x80000000u;
+  const int64_t nsamp = n - first < (int64_t)kFan * kFan ? n - first : (int64_t)kFan * kFan;
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(mse + first * m), (short)0, (int)(nsamp * m * 8), 0x00020000);
+  const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(ov + first * m), (short)0, (int)(nsamp * m), 0x00020000);
+  double wr[PER];
+  uint32_t orr[PER];
+  auto fetch = [&](int b) {
+    const int base = b * kFan * m;
+    const int len = (int)(nsamp - (int64_t)b * kFan < kFan ? nsamp - (int64_t)b * kFan : kFan) * m;
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = (int)threadIdx.x + 256 * u;
+      const uint32_t ok = e < len ? 0u : OOB;
+      const uint2 pair = __builtin_bit_cast(
+          uint2, __builtin_amdgcn_raw_buffer_load_b64(rw, (uint32_t)(base + e) * 8u | ok, 0, 0));
+      wr[u] = __builtin_bit_cast(double, pair);
+      orr[u] = __builtin_amdgcn_raw_buffer_load_b8(ro, (uint32_t)(base + e) | ok, 0, 0);
+    }
+  };
+  double node = 0.0;
+  fetch(0);
+  for (int b = 0; b < groups; ++b) {
+    const int buf = b & 1;
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      wsh[buf][threadIdx.x + 256 * u] = wr[u];
+      osh[buf][threadIdx.x + 256 * u] = (uint8_t)orr[u];
     }
     __syncthreads();
+    if (b + 1 < groups) fetch(b + 1);      // in flight while this group is summed
+    const int64_t p0 = first + (int64_t)b * kFan;
+    const int rows = (int)(n - p0 < kFan ? n - p0 : kFan);
     if (idx < Q) {
+      // terms of the samples this entry skips are +0, which leaves every partial sum as it
+      // is; the LDS reads of eight samples are issued before their additions
+      const double* wb = wsh[buf];
+      const uint8_t* ob = osh[buf];
       double leaf = 0.0;
-      if (s < 0) {
-        for (int j = 0; j < rows; ++j) leaf = leaf + (double)osh[j * m + i - 1];
-      } else {
-        for (int j = 0; j < rows; ++j) {
-          const bool os = s == 0 || osh[j * m + s - 1] != 0;
-          if (os && osh[j * m + i - 1] == 0) leaf = leaf + wsh[j * m + i - 1];
+      for (int j0 = 0; j0 < rows; j0 += 8) {
+        double t[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          // every value is read unconditionally and the term selected by a multiply by 0 or
+          // 1 (exact: errors are finite and >= 0), so that no read sits behind a branch
+          const int j = j0 + u < rows ? j0 + u : rows - 1;
+          const uint32_t oi = ob[j * m + i - 1];
+          const uint32_t os = (uint32_t)ob[j * m + cs] | (uint32_t)(s == 0);
+          const double wv = wb[j * m + i - 1];
+          const uint32_t keep = (j0 + u < rows) ? ((s < 0 ? oi : (os & (oi ^ 1u))) & 1u) : 0u;
+          t[u] = (s < 0 ? 1.0 : wv) * (double)keep;
         }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) leaf = leaf + t[u];
       }
       node = node + leaf;
     }
