@@ -2,79 +2,126 @@
 // NestQuantM's of App. D) followed by the inverse scaling x_hat = r * beta_t * p (Alg. 3's
 // normalization undone).
 //
-// One lane per 8-entry block: read one code word, the row's beta word and scale, decode in
-// exact integer arithmetic, and write the 8 values (32 B fp32 or 16 B fp16/bf16) with one
-// or two vector stores; consecutive lanes handle consecutive blocks of a row.
+// Each block: read its code word, the row's beta word and scale, decode in exact integer
+// arithmetic, and write the 8 values (32 B fp32 or 16 B fp16/bf16) with one or two vector
+// stores; consecutive lanes handle consecutive blocks.
 #include "nq_device.hpp"
 #include "nq_kernels.hpp"
 
 namespace nq {
 
+constexpr int kDecodePerThread = 4;
+
+// One select chain instead of an indexed read of the argument block (which would be a
+// dependent memory load after the beta word arrives).
+__device__ __forceinline__ double pick_half_beta(const DecodeArgs& a, uint32_t t) {
+  return t == 0 ? a.half_beta[0] : (t == 1 ? a.half_beta[1] : (t == 2 ? a.half_beta[2] : a.half_beta[3]));
+}
+
+// The blocks of the rows x nb matrix, in row-major order, are dealt to workgroups in runs
+// of 256 * kDecodePerThread; thread t of a workgroup takes blocks t + 256 i of its run, so
+// every load and store instruction of a wave touches consecutive blocks.  A thread issues
+// the loads of all its blocks (code word, beta word, row scale: buffer loads based at the
+// run's first row, out-of-range offsets reading 0) before decoding any.
 template <int OUT, int DV>  // OUT: 0 = fp32, 1 = fp16, 2 = bf16; DV: decoder_variant
 __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict__ codes,
                                                      const uint32_t* __restrict__ beta,
                                                      const float* __restrict__ scales,
-                                                     int64_t rows, int nb, int lg,
+                                                     int64_t rows, int nb, float inv_nb,
                                                      void* __restrict__ out, int64_t ld_out,
                                                      DecodeArgs a) {
-  const GridPos g = grid_block(nb, lg);
-  if (g.rb + g.lr >= rows || g.j >= nb) return;
-  const int j = g.j;
+  constexpr int TPB = kDecodePerThread;
+  constexpr uint32_t OOB = 0x80000000u;
+  const int64_t total = rows * nb;
+  const int64_t g0 = (int64_t)blockIdx.x * (256 * TPB);
+  const int64_t row0 = g0 / nb;
+  const int j0 = (int)(g0 - row0 * nb);
   const int nbw = (nb + 15) >> 4;
-  const uint32_t w = __builtin_nontemporal_load(codes + g.rb * nb + (uint32_t)(g.lr * nb + j));
-  const uint32_t bw = beta[g.rb * nbw + (uint32_t)(g.lr * nbw + (j >> 4))];
-  const int t = (int)((bw >> (2 * (j & 15))) & 3u);
-  const double sc = (double)scales[g.rb + g.lr] * a.half_beta[t];
-  uint32_t X2p[4];
-  if constexpr (DV == 2) {
-    // byte-SIMD NestQuantM at q = 16: repack the signed bytes as int16 pairs
-    uint32_t xa, xb;
-    int x0;
-    decode_word_m16(w, xa, xb, x0);
+  const int reach = (j0 + 256 * TPB + nb - 1) / nb;           // rows this workgroup touches
+  const int span = (int)(rows - row0 < reach ? rows - row0 : reach);
+  const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(codes + row0 * nb), (short)0, span * nb * 4, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(beta + row0 * nbw), (short)0, span * nbw * 4, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(scales + row0), (short)0, span * 4, 0x00020000);
+  uint32_t w[TPB], bw[TPB];
+  float sr[TPB];
+  int rr[TPB], jj[TPB];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const uint32_t x = i < 2 ? xa : xb;
-      const int lo = i == 0 ? x0 : ((int)(int8_t)(uint8_t)(x >> (16 * (i & 1))) >> 2);
-      const int hi = (int)(int8_t)(uint8_t)(x >> (16 * (i & 1) + 8)) >> 2;
-      X2p[i] = ((uint32_t)lo & 0xFFFFu) | ((uint32_t)hi << 16);
-    }
-  } else {
-    decode_word_pk<DV == 1>(w, a.q, a.m2q, X2p);
+  for (int i = 0; i < TPB; ++i) {
+    const int o = j0 + (int)threadIdx.x + 256 * i;     // < nb + 256 TPB <= 2^14
+    int r = (int)((float)o * inv_nb);
+    if ((int)__umul24((uint32_t)r, (uint32_t)nb) > o) --r;
+    if ((int)__umul24((uint32_t)(r + 1), (uint32_t)nb) <= o) ++r;
+    const int j = o - (int)__umul24((uint32_t)r, (uint32_t)nb);
+    rr[i] = r;
+    jj[i] = j;
+    const uint32_t ok = g0 + (int)threadIdx.x + 256 * i < total ? 0u : OOB;
+    w[i] = __builtin_amdgcn_raw_buffer_load_b32(
+        rc, (4u * (__umul24((uint32_t)r, (uint32_t)nb) + (uint32_t)j)) | ok, 0, 0);
+    bw[i] = __builtin_amdgcn_raw_buffer_load_b32(
+        rb, (4u * (__umul24((uint32_t)r, (uint32_t)nbw) + (uint32_t)(j >> 4))) | ok, 0, 0);
+    sr[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (4u * (uint32_t)r) | ok, 0, 0));
   }
-  if constexpr (OUT == 0) {
-    // fp32: each value rounded once from its fp64 product
-    float v[8];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      v[2 * i] = (float)(sc * (double)(int)(short)(X2p[i] & 0xFFFFu));
-      v[2 * i + 1] = (float)(sc * (double)((int)X2p[i] >> 16));
-    }
-    f32x4* o = reinterpret_cast<f32x4*>((float*)out + (g.rb + g.lr) * ld_out + 8 * j);
-    const f32x4 lo = {v[0], v[1], v[2], v[3]};
-    const f32x4 hi = {v[4], v[5], v[6], v[7]};
-    __builtin_nontemporal_store(lo, o);
-    __builtin_nontemporal_store(hi, o + 1);
-  } else {
-    // 16-bit outputs: X2 (|X2| <= 32) times the fp32-rounded scale is within two fp32
-    // roundings (relative 2^-23) of the exact value, far below half an fp16 / bf16 ulp,
-    // so the final rounding lands on the nearest or the adjacent 16-bit value
-    const float s32 = (float)sc;
-    uint32_t pk[4];
+  for (int i = 0; i < TPB; ++i) {
+    if (g0 + (int)threadIdx.x + 256 * i >= total) break;
+    const int j = jj[i];
+    const uint32_t t = (bw[i] >> (2 * (j & 15))) & 3u;
+    const double sc = (double)sr[i] * pick_half_beta(a, t);
+    uint32_t X2p[4];
+    if constexpr (DV == 2) {
+      // byte-SIMD NestQuantM at q = 16: repack the signed bytes as int16 pairs
+      uint32_t xa, xb;
+      int x0;
+      decode_word_m16(w[i], xa, xb, x0);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float lo = (float)(int)(short)(X2p[i] & 0xFFFFu) * s32;
-      const float hi = (float)((int)X2p[i] >> 16) * s32;
-      if constexpr (OUT == 1) {
-        pk[i] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)lo) |
-                ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)hi) << 16);
-      } else {
-        pk[i] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)lo) |
-                ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)hi) << 16);
+      for (int u = 0; u < 4; ++u) {
+        const uint32_t x = u < 2 ? xa : xb;
+        const int lo = u == 0 ? x0 : ((int)(int8_t)(uint8_t)(x >> (16 * (u & 1))) >> 2);
+        const int hi = (int)(int8_t)(uint8_t)(x >> (16 * (u & 1) + 8)) >> 2;
+        X2p[u] = ((uint32_t)lo & 0xFFFFu) | ((uint32_t)hi << 16);
       }
+    } else {
+      decode_word_pk<DV == 1>(w[i], a.q, a.m2q, X2p);
     }
-    const u32x4 v = {pk[0], pk[1], pk[2], pk[3]};
-    __builtin_nontemporal_store(
-        v, reinterpret_cast<u32x4*>((uint16_t*)out + (g.rb + g.lr) * ld_out + 8 * j));
+    const int64_t orow = row0 + rr[i];
+    if constexpr (OUT == 0) {
+      // fp32: each value rounded once from its fp64 product
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        v[2 * u] = (float)(sc * (double)(int)(short)(X2p[u] & 0xFFFFu));
+        v[2 * u + 1] = (float)(sc * (double)((int)X2p[u] >> 16));
+      }
+      f32x4* o = reinterpret_cast<f32x4*>((float*)out + orow * ld_out + 8 * j);
+      const f32x4 lo = {v[0], v[1], v[2], v[3]};
+      const f32x4 hi = {v[4], v[5], v[6], v[7]};
+      __builtin_nontemporal_store(lo, o);
+      __builtin_nontemporal_store(hi, o + 1);
+    } else {
+      // 16-bit outputs: X2 (|X2| <= 32) times the fp32-rounded scale is within two fp32
+      // roundings (relative 2^-23) of the exact value, far below half an fp16 / bf16 ulp,
+      // so the final rounding lands on the nearest or the adjacent 16-bit value
+      const float s32 = (float)sc;
+      uint32_t pk[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float lo = (float)(int)(short)(X2p[u] & 0xFFFFu) * s32;
+        const float hi = (float)((int)X2p[u] >> 16) * s32;
+        if constexpr (OUT == 1) {
+          pk[u] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)lo) |
+                  ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)hi) << 16);
+        } else {
+          pk[u] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)lo) |
+                  ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)hi) << 16);
+        }
+      }
+      const u32x4 v = {pk[0], pk[1], pk[2], pk[3]};
+      __builtin_nontemporal_store(
+          v, reinterpret_cast<u32x4*>((uint16_t*)out + orow * ld_out + 8 * j));
+    }
   }
 }
 
@@ -82,13 +129,12 @@ hipError_t launch_decode(const uint32_t* codes, const uint32_t* beta, const floa
                          int64_t rows, int cols, void* out, int out_dtype, int64_t ld_out,
                          const DecodeArgs& a, hipStream_t st) {
   const int nb = cols / 8;
-  int lg;
-  int64_t wgs;
-  grid_shape(rows, nb, lg, wgs);
-  const unsigned grid = (unsigned)wgs;
+  const int64_t total = rows * nb;
+  const unsigned grid = (unsigned)((total + 256 * kDecodePerThread - 1) / (256 * kDecodePerThread));
+  const float inv = 1.0f / (float)nb;
 #define NQ_DEC(O, DV)                                                                       \
   hipLaunchKernelGGL((decode_kernel<O, DV>), dim3(grid), dim3(256), 0, st, codes, beta,     \
-                     scales, rows, nb, lg, out, ld_out, a)
+                     scales, rows, nb, inv, out, ld_out, a)
 #define NQ_DEC3(O) \
   if (dv == 0) NQ_DEC(O, 0); else if (dv == 1) NQ_DEC(O, 1); else NQ_DEC(O, 2)
   const int dv = decoder_variant(a.decoder, a.q);
