@@ -688,3 +688,39 @@ def test_matmul_fp16_tiles_exact(nq, M, N, K):
         want = np.zeros((rows_p, kp))
         want[:T.shape[0], :T.shape[1]] = T
         assert np.array_equal(got, want), first_mismatch(got, want)
+
+
+# ---------------------------------------------------------------------------------------
+# Maximum row length (K = 65536 = 8192 blocks, the largest the boundary accepts): the
+# streamed encoder, the decoder, both product paths and the fused call.
+# ---------------------------------------------------------------------------------------
+def test_max_cols_encode_decode(nq):
+    torch = __import__("torch")
+    store, x32 = workloads.random_rows(90, 3, 65536, dtype="bf16", dist="t4")
+    got = check_encode(nq, store, x32, "bf16", 14, 4)
+    dec = nq.decode(got)
+    torch.cuda.synchronize()
+    from oracle import layout
+    oc, ob, os_ = oracle_encode(x32, 14, 4)
+    want = nestquant.decode_rows(layout.unpack_codes(oc), layout.unpack_beta(ob, 8192), os_, 14,
+                                 nestquant.default_base(14, 4))
+    g = dec.cpu().numpy().astype(np.float64)
+    assert not (np.abs(g - want) > ulp_in("f32", want)).any()
+
+
+@pytest.mark.parametrize("M,N", [(3, 40), (70, 66)])
+def test_max_cols_matmul_and_fused(nq, M, N):
+    torch = __import__("torch")
+    K = 65536
+    sa, A32 = workloads.random_rows(91, M, K, dtype="bf16", dist="t4")
+    _, W32 = workloads.random_rows(92, N, K, dtype="bf16", scale=0.02)
+    C, (ac, ab, ar, ba), (wc, wb, wr, bw) = _oracle_product(A32, W32, 14, 14, 4)
+    a = upload_coded(ac, ab, ar, M, K, 14, 4, ba)
+    w = upload_coded(wc, wb, wr, N, K, 14, 4, bw)
+    got = nq.matmul(a, w)
+    _, fused = nq.encode_matmul(to_device(sa, "bf16"), w, 14, 4)
+    torch.cuda.synchronize()
+    for out in (got, fused):
+        g = out.cpu().numpy().astype(np.float64)
+        assert np.linalg.norm(g - C) / np.linalg.norm(C) <= MATMUL_RTOL
+        assert np.all(np.abs(g - C) <= 1e-5 * np.abs(C).max())
