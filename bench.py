@@ -38,6 +38,9 @@ def parse():
     ap.add_argument("--workload", type=int, default=3, help="workload id (see workloads.py)")
     ap.add_argument("--q", type=int, default=None, help="override q (workload 4 has q=7 too)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay a captured HIP graph of the step instead of launching its "
+                         "kernels directly (slower on these boxes: about 141 against 135 us)")
     ap.add_argument("--kv", action="store_true",
                     help="standalone nq_encode / nq_decode of the 2^28-entry fp16 KV-like "
                          "matrix (2^21 rows of 128) against the HBM roofline")
@@ -412,9 +415,32 @@ def main():
         if ev is not None:
             ev[1].record()
 
-    for i in range(args.warmup):
+    for i in range(max(args.warmup, 1)):
         step(i)
     torch.cuda.synchronize()
+    use_graph = args.graph
+    if use_graph:
+        # one captured graph of the step per activation buffer: a replay launches the
+        # encoder, W's decode and the contraction with no host work between them
+        graphs = []
+        for b in range(nbuf):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                nq.encode_matmul(As[b], wc, q=q, k=k, out=C, coded_out=(codes, beta, scales),
+                                 workspace=ws)
+            graphs.append(g)
+        torch.cuda.synchronize()
+
+        def step(i, ev=None):
+            if ev is not None:
+                ev[0].record()
+            graphs[i % nbuf].replay()
+            if ev is not None:
+                ev[1].record()
+
+        for i in range(args.warmup):
+            step(i)
+        torch.cuda.synchronize()
     sev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -540,6 +566,7 @@ def main():
         "config": {
             "workload": c["name"], "M": M, "N": N, "K": K, "q": q, "k": k,
             "A": f"{dta} {'Student-t(4)' if cfg == 3 else 'synthetic'}", "W": f"{dtw} coded once",
+            "launch": "HIP graph replay of the step" if use_graph else "direct launches",
             "parallelism": "single GPU",
         },
         "components": {

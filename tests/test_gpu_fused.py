@@ -104,3 +104,36 @@ def test_encode_matmul_reuses_its_workspace(nq):
         c1 = nq.matmul(nq.encode(x, 14, 4), w)
         torch.cuda.synchronize()
         assert torch.equal(c1, c2)
+
+
+def test_encode_matmul_graph_replays(nq):
+    """nq_encode_matmul captured in a HIP graph (through torch.cuda.graph) and replayed
+    several times, with eager work that changes the input in place between replays: every
+    replay equals the eager call on the same input."""
+    import torch
+    store, _ = workloads.random_rows(610, 300, 1024, dtype="bf16", dist="t4")
+    wstore, _ = workloads.random_rows(611, 260, 1024, dtype="bf16", scale=0.02)
+    w = nq.encode(_dev(wstore, "bf16"), 14, 4)
+    x = _dev(store, "bf16").clone()
+    ws = torch.empty(nq.matmul_workspace_size(300, 260, 1024), dtype=torch.uint8, device="cuda")
+    codes = torch.empty(300 * 128, dtype=torch.int32, device="cuda")
+    beta = torch.empty(300 * 8, dtype=torch.int32, device="cuda")
+    scales = torch.empty(300, dtype=torch.float32, device="cuda")
+    out = torch.empty(300, 260, device="cuda")
+    args = dict(q=14, k=4, out=out, coded_out=(codes, beta, scales), workspace=ws)
+    nq.encode_matmul(x, w, **args)                 # warm-up outside the capture
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        nq.encode_matmul(x, w, **args)
+    for rep in range(4):
+        x.mul_(1.5 if rep % 2 else -0.75)          # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = (out.clone(), codes.clone(), beta.clone(), scales.clone())
+        a_ref, c_ref = nq.encode_matmul(x, w, q=14, k=4)
+        torch.cuda.synchronize()
+        assert torch.equal(got[0], c_ref)
+        assert torch.equal(got[1], a_ref.codes) and torch.equal(got[2], a_ref.beta)
+        assert torch.equal(got[3], a_ref.scales)
