@@ -430,8 +430,10 @@ static hipError_t decode_once(int stages, const MatmulOperand& A, const MatmulOp
   if (stages & 1) launch_tiles<ET>(A, nb, mp, nbp, (void*)wa, st);
   if (stages & (1 | kStageDecodeW)) launch_tiles<ET>(W, nb, np, nbp, (void*)ww, st);
   if (!(stages & 2)) return hipGetLastError();
-  // 256 x 256 tiles once they give every CU a tile, else 256 x 128
-  if ((mp / 256) * (np / 256) >= 256) {
+  // 256 x 256 tiles (half the global->LDS traffic per flop) unless they leave a partly
+  // empty last round over the 256 CUs that 256 x 128 tiles (half the work each) avoid
+  const int64_t big = (mp / 256) * (np / 256), mid = (mp / 256) * (np / 128);
+  if (big >= 256 && 2 * ((big + 255) / 256) <= (mid + 255) / 256) {
     launch_gemm<CfgBig, ET>(wa, ww, kc, mp, np, A, W, c, ldc, scale, st);
   } else {
     launch_gemm<CfgMid, ET>(wa, ww, kc, mp, np, A, W, c, ldc, scale, st);
