@@ -287,7 +287,8 @@ __device__ __forceinline__ void opt_block(const float (&v)[8], const float (&c)[
     } else {
       decode_word_pk<false>(w, a.q, a.m2q, X2);
     }
-    const double bt = a.beta[t];
+    // a select chain, not an indexed read of the argument block (a memory load)
+    const double bt = t == 0 ? a.beta[0] : (t == 1 ? a.beta[1] : (t == 2 ? a.beta[2] : a.beta[3]));
     double err = 0.0;
 #pragma unroll
     for (int l = 0; l < 8; ++l) {
