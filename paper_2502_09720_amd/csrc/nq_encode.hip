@@ -472,8 +472,10 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_kernel(
 // every slot at the first beta the root bound of x does not rule out, with the fp32
 // nearest-point decision, and finishes it unless that decision was too close to call, or
 // the point's exact root bound says it overloads (start again at the next beta) or lies on
-// the cell boundary (the literal test decides).  Those slots (about 12-15% on Gaussian-like and heavy-tailed
-// rows) are queued, and phase 2 finishes them with every lane of the workgroup busy.
+// the cell boundary (the literal test decides).  Those slots (about 12-19% on Gaussian-like
+// and heavy-tailed rows) are queued, and phase 2 finishes them with every lane of the
+// workgroup busy.  With tiles, slots at the last beta whose point is not strictly inside
+// the cell are queued too, so that phase 1 never runs the decoder (full decoder only).
 // Two-bit beta indices are staged in LDS and packed into words at the end.
 // ---------------------------------------------------------------------------------------
 template <int LANES, int BPT>
@@ -712,7 +714,7 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
     const bool coded = valid && rrow[cw][rw] != 0.0f;
     bool queued = false;
     int start = 0, t0 = 0;
-    int P[8];
+    int P[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     if (coded) {
       float v[8];
       unpack_raw<T>(rawl[wave][sl], v);
@@ -740,6 +742,11 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
             start = M > 2 * a.q ? t0 + 1 : t0;
           }
         }
+      } else if (TILES && !a.decoder && e8_root_bound(P) >= 2 * a.q) {
+        // the last beta, where a point may overload: only a point strictly inside the cell
+        // is its own decode; the others take the decoder's tile in phase 2
+        queued = true;
+        start = t0;
       }
     }
     const uint64_t mask = __ballot(queued);
@@ -751,13 +758,13 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
       codes_w[rw * nb + j] = word;
       tsl[wave][sl] = (uint8_t)t0;
       if constexpr (TILES) {
-        // a point kept below the last beta passed the overload test: X2 = P
-        if (!coded) {
-          tile_zero(a, row, j);
-        } else if (t0 < a.k - 1) {
-          tile_from_x2(a, row, j, P, t0);
-        } else {
+        // a point kept here passed the overload test or lies strictly inside the cell, so
+        // X2 = P (zero for rows that are not coded); the NestQuantM decoder has no such
+        // bound at the last beta, where its tile is decoded
+        if (coded && a.decoder && t0 == a.k - 1) {
           tile_decoded(a, row, j, word, t0);
+        } else {
+          tile_from_x2(a, row, j, P, t0);
         }
       }
     }
