@@ -422,25 +422,34 @@ nq_status nq_encode_matmul(int32_t flags, const nq_params* pa, const void* x, nq
   if (M == 0 || N == 0) return ok();
   if (nq_status s = check_workspace(M, N, K, workspace, workspace_bytes, who)) return s;
   hipStream_t st = (hipStream_t)hip_stream;
-  // 1. encode A; the encoder also writes A's decoded tiles into the workspace
+  nq::MatmulOperand A{a_codes, a_beta, a_scales, pa->q, nq::magic_2q(pa->q), M, pa->decoder,
+                      mult_table(pa)};
+  nq::MatmulOperand W{w_codes, w_beta, w_scales, pw->q, nq::magic_2q(pw->q), N, pw->decoder,
+                      mult_table(pw)};
+  // 1. encode A; the encoder also writes A's decoded tiles into the workspace and, on the
+  //    decode-once path where its instantiation allows, W's tile decode rides in the same
+  //    launch (workgroups after the encoder's, which fill the encoder's tail)
   nq::EncodeArgs a = encode_args(pa);
   const int nbp = tile_blocks(K, et);
   const int64_t rows_p = M <= nq::kFusedMaxM ? (M + 15) / 16 * 16 : (M + 255) / 256 * 256;
   a.tiles = workspace;
   a.tile_et = et;
   a.nb_p = nbp;
+  int stages = nq::kStageDecodeW | NQ_STAGE_CONTRACT;
+  if (M > nq::kFusedMaxM && nq::encode_carries_task((int)K, pa->strategy)) {
+    int64_t w_offset, np;
+    int wnbp;
+    nq::decode_once_layout(et, M, N, K, w_offset, np, wnbp);
+    a.task = nq::tile_task(W, (int)(K / 8), np, wnbp,
+                           static_cast<unsigned char*>(workspace) + w_offset);
+    stages = NQ_STAGE_CONTRACT;
+  }
   hipError_t e = nq::launch_encode(x, (int)x_dtype, M, (int)K, ld_x, a, a_codes, a_beta,
                                    a_scales, st);
   if (e == hipSuccess) e = nq::launch_tiles_pad(et, workspace, M, (int)(K / 8), rows_p, nbp, st);
   if (e != hipSuccess) return hip_status(e, who);
-  // 2. decode W (decode-once path) and contract
-  nq::MatmulOperand A{a_codes, a_beta, a_scales, pa->q, nq::magic_2q(pa->q), M, pa->decoder,
-                      mult_table(pa)};
-  nq::MatmulOperand W{w_codes, w_beta, w_scales, pw->q, nq::magic_2q(pw->q), N, pw->decoder,
-                      mult_table(pw)};
-  return hip_status(launch_product(nq::kStageDecodeW | NQ_STAGE_CONTRACT, et, pa, pw, A, W, K,
-                                   c, ldc, workspace, st),
-                    who);
+  // 2. decode W (unless the encoder's launch did) and contract
+  return hip_status(launch_product(stages, et, pa, pw, A, W, K, c, ldc, workspace, st), who);
 }
 
 }  // extern "C"

@@ -13,6 +13,7 @@
 // boundary comparison is made exactly.
 #include "nq_device.hpp"
 #include "nq_kernels.hpp"
+#include "nq_tiles.hpp"
 
 namespace nq {
 
@@ -614,12 +615,23 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
   __shared__ double rsum[4][RW];
   __shared__ int qlen[4];
 
+  // A TileTask's a.task.wgs workgroups come last in the grid: dispatched once every row has
+  // started, they fill the CUs that the encoder's last rows leave idle (spreading them
+  // among the encoder's workgroups was slower than a separate launch).
+  const int64_t bid = blockIdx.x;
+  if constexpr (TILES && SM::WGROW) {
+    const int64_t first = (int64_t)gridDim.x - a.task.wgs;
+    if (bid >= first) {
+      run_tile_task(a.task, a.tile_et, bid - first);
+      return;
+    }
+  }
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int cw = SM::WGROW ? 0 : wave;
   const int nb = cols >> 3;
   const int nbw = (nb + 15) >> 4;
   auto row_base = [&](int w) -> int64_t {
-    return SM::WGROW ? (int64_t)blockIdx.x : ((int64_t)blockIdx.x * 4 + w) * RW;
+    return SM::WGROW ? bid : (bid * 4 + w) * RW;
   };
   const int64_t row0 = row_base(wave);
   const double n = (double)cols;
@@ -841,7 +853,8 @@ static hipError_t launch_w(const void* x, int64_t rows, int cols, int64_t ld_x,
                            hipStream_t st) {
   using SM = SlotMap<LANES, BPT>;
   const int64_t rows_per_wg = SM::WGROW ? 1 : 4 * SM::ROWS_PER_WAVE;
-  const int64_t grid = (rows + rows_per_wg - 1) / rows_per_wg;
+  int64_t grid = (rows + rows_per_wg - 1) / rows_per_wg;
+  if (TILES && SM::WGROW) grid += a.task.wgs;
   hipLaunchKernelGGL((encode_wave_kernel<T, LANES, BPT, TILES>), dim3((unsigned)grid), dim3(256), 0, st,
                      (const T*)x, rows, cols, ld_x, a, codes, beta, scales);
   return hipGetLastError();
@@ -881,9 +894,18 @@ static hipError_t launch_dtype(const void* x, int64_t rows, int cols, int64_t ld
 #undef NQ_L
 }
 
+// The encoder instantiations that carry a TileTask: First-beta rows of 257 to 2048 blocks
+// (one row per workgroup; every prefill shape of a Llama layer has K in 2056..16384).
+bool encode_carries_task(int cols, int strategy) {
+  const int nb = cols / 8;
+  return strategy == 0 && nb > 256 && nb <= 2048;
+}
+
 hipError_t launch_encode(const void* x, int dtype, int64_t rows, int cols, int64_t ld_x,
                          const EncodeArgs& a, uint32_t* codes, uint32_t* beta, float* scales,
                          hipStream_t st) {
+  if (a.task.wgs > 0 && !(a.tiles && encode_carries_task(cols, a.strategy)))
+    return hipErrorInvalidValue;
   if (a.tiles) {
     switch (dtype) {
       case 0: return launch_dtype<float, true>(x, rows, cols, ld_x, a, codes, beta, scales, st);

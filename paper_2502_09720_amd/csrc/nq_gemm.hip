@@ -27,6 +27,7 @@
 
 #include "nq_device.hpp"
 #include "nq_kernels.hpp"
+#include "nq_tiles.hpp"
 
 namespace nq {
 
@@ -61,14 +62,7 @@ using CfgMid = Cfg<256, 128, 4, 2, 3>;
 using CfgBig = Cfg<256, 256, 4, 2, 2>;
 }  // namespace gemm
 
-// m * X2 of every block of a coded operand into ws[rows_p][nb_p blocks] (zero padding): 8
-// bf16 or fp16 (16 B) per block, or 8 int8 (8 B) for the int8 contraction.  The workspace
-// is one flat array of rows_p * nb_p blocks; workgroup w covers TB = 256 * TPB consecutive
-// blocks of it, thread t the blocks w TB + t + 256 i (i < TPB), so each load and store
-// instruction of a wave touches consecutive blocks.  Every thread issues the loads of all
-// its blocks before decoding any, which keeps TPB loads in flight per thread.
-constexpr int kTilesPerThread = 4;
-
+// One workgroup per 256 * kTilesPerThread blocks of the tile (tiles_block).
 template <int ET, int DV>
 __global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__ codes,
                                                     const uint32_t* __restrict__ beta,
@@ -76,57 +70,8 @@ __global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__
                                                     int nb_p, float inv_nbp, int q,
                                                     uint32_t m2q, uint32_t mtab,
                                                     void* __restrict__ ws) {
-  constexpr bool I8 = ET == ET_I8;
-  constexpr int TPB = kTilesPerThread;
-  constexpr uint32_t OOB = 0x80000000u;   // past every buffer range below: reads 0
-  using V = typename std::conditional<I8, u32x2, u32x4>::type;
-  const int64_t g0 = (int64_t)blockIdx.x * (256 * TPB);
-  // the workgroup's first block as (row0, j0); every other block is an offset
-  // o < nb_p + 256 TPB <= 2^14 past (row0, 0), split by a float division checked once in
-  // each direction.  Code and beta
-  // words are read through buffer resources based at row0 (32-bit offsets; the range check
-  // makes rows past the operand read as zero).
-  const int64_t row0 = g0 / nb_p;
-  const int j0 = (int)(g0 - row0 * nb_p);
-  const int nbw = (nb + 15) >> 4;
-  const int64_t rows_left = rows > row0 ? rows - row0 : 0;
-  const int reach = (j0 + 256 * TPB + nb_p - 1) / nb_p;     // rows this workgroup touches
-  const int64_t span = rows_left < reach ? rows_left : reach;
-  const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(codes + row0 * nb), (short)0, (int)(span * nb * 4), 0x00020000);
-  const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(beta + row0 * nbw), (short)0, (int)(span * nbw * 4), 0x00020000);
-  uint32_t w[TPB], bw[TPB];
-  int jj[TPB];
-  bool pad[TPB];
-#pragma unroll
-  for (int i = 0; i < TPB; ++i) {
-    const int o = j0 + (int)threadIdx.x + 256 * i;
-    int r = (int)((float)o * inv_nbp);
-    if ((int)__umul24((uint32_t)r, (uint32_t)nb_p) > o) --r;
-    if ((int)__umul24((uint32_t)(r + 1), (uint32_t)nb_p) <= o) ++r;
-    const int j = o - (int)__umul24((uint32_t)r, (uint32_t)nb_p);
-    jj[i] = j;
-    pad[i] = j >= nb || r >= span;
-    const uint32_t co = pad[i] ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nb) + (uint32_t)j);
-    const uint32_t bo = pad[i] ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nbw) + (uint32_t)(j >> 4));
-    w[i] = __builtin_amdgcn_raw_buffer_load_b32(rc, co, 0, 0);
-    bw[i] = __builtin_amdgcn_raw_buffer_load_b32(rb, bo, 0, 0);
-  }
-#pragma unroll
-  for (int i = 0; i < TPB; ++i) {
-    const int64_t g = g0 + (int)threadIdx.x + 256 * i;
-    if (g >= total) break;
-    const int m = beta_mult(mtab, (bw[i] >> (2 * (jj[i] & 15))) & 3u);
-    V out;
-    if constexpr (I8) {
-      out = decode_tile_i8<DV>(w[i], m, q, m2q);
-    } else {
-      out = decode_tile_16<DV, ET == ET_F16>(w[i], m, q, m2q);
-    }
-    if (pad[i]) out = V{};                 // padding past the operand's rows or columns
-    reinterpret_cast<V*>(ws)[g] = out;
-  }
+  tiles_block<ET, DV>(codes, beta, rows, nb, total, nb_p, inv_nbp, q, m2q, mtab, ws,
+                      (int64_t)blockIdx.x);
 }
 
 // Launch tiles_kernel for one operand with its decoder.
@@ -134,7 +79,7 @@ template <int ET>
 void launch_tiles(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void* ws,
                   hipStream_t st) {
   const int64_t total = rows_p * nb_p;
-  const int64_t wgs = (total + 256 * kTilesPerThread - 1) / (256 * kTilesPerThread);
+  const int64_t wgs = tile_workgroups(total);
   const float inv = 1.0f / (float)nb_p;
 #define NQ_TL(DV)                                                                            \
   hipLaunchKernelGGL((tiles_kernel<ET, DV>), dim3((unsigned)wgs), dim3(256), 0, st, X.codes,    \
@@ -413,6 +358,37 @@ static void launch_gemm(const u32x4* wa, const u32x4* ww, int kc, int64_t mp, in
                      W.scales, A.rows, W.rows, c, ldc, scale);
 }
 
+// Workspace layout of the decode-once path: A's tile (mp x nb_p blocks) then W's (np x nb_p),
+// rows padded to whole 128-byte stages.
+void decode_once_layout(int et, int64_t M, int64_t N, int64_t K, int64_t& w_offset,
+                        int64_t& rows_p, int& nb_p) {
+  using namespace gemm;
+  const int eb = et == ET_I8 ? 1 : 2;                 // bytes per element
+  const int64_t mp = (M + 255) / 256 * 256;
+  const int64_t kp = (K * eb + BKB - 1) / BKB * BKB / eb;
+  w_offset = mp * kp * eb;
+  rows_p = (N + 255) / 256 * 256;
+  nb_p = (int)(kp / 8);
+}
+
+TileTask tile_task(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void* ws) {
+  TileTask t;
+  t.codes = X.codes;
+  t.beta = X.beta;
+  t.rows = X.rows;
+  t.total = rows_p * nb_p;
+  t.ws = ws;
+  t.nb = nb;
+  t.nb_p = nb_p;
+  t.inv_nbp = 1.0f / (float)nb_p;
+  t.q = X.q;
+  t.m2q = X.m2q;
+  t.mtab = X.mtab;
+  t.dv = decoder_variant(X.decoder, X.q);
+  t.wgs = (int)tile_workgroups(t.total);
+  return t;
+}
+
 template <int ET>
 static hipError_t decode_once(int stages, const MatmulOperand& A, const MatmulOperand& W,
                               int64_t K, float* c, int64_t ldc, float scale, void* ws,
@@ -420,13 +396,13 @@ static hipError_t decode_once(int stages, const MatmulOperand& A, const MatmulOp
   using namespace gemm;
   const int nb = (int)(K / 8);
   const int64_t mp = (A.rows + 255) / 256 * 256;
-  const int64_t np = (W.rows + 255) / 256 * 256;
+  int64_t w_offset, np;
+  int nbp;
+  decode_once_layout(ET, A.rows, W.rows, K, w_offset, np, nbp);
   constexpr int EB = ET == ET_I8 ? 1 : 2;              // bytes per element
-  const int64_t kp = (K * EB + BKB - 1) / BKB * BKB / EB;
-  const int nbp = (int)(kp / 8);
-  const int kc = (int)(kp * EB / 16);
+  const int kc = nbp * 8 * EB / 16;
   u32x4* wa = reinterpret_cast<u32x4*>(ws);
-  u32x4* ww = wa + mp * kc;
+  u32x4* ww = reinterpret_cast<u32x4*>(static_cast<unsigned char*>(ws) + w_offset);
   if (stages & 1) launch_tiles<ET>(A, nb, mp, nbp, (void*)wa, st);
   if (stages & (1 | kStageDecodeW)) launch_tiles<ET>(W, nb, np, nbp, (void*)ww, st);
   if (!(stages & 2)) return hipGetLastError();

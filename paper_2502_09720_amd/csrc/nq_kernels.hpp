@@ -6,6 +6,24 @@
 
 namespace nq {
 
+// The tile decode of one coded operand (tiles_block) carried by wgs extra workgroups of
+// another launch; dv is decoder_variant of the operand.  wgs == 0: no task.
+struct TileTask {
+  const uint32_t* codes;
+  const uint32_t* beta;
+  int64_t rows;
+  int64_t total;   // rows_p * nb_p blocks of the tile
+  void* ws;        // the tile
+  int nb;
+  int nb_p;
+  float inv_nbp;   // fl32(1 / nb_p)
+  int q;
+  uint32_t m2q;
+  uint32_t mtab;
+  int dv;
+  int wgs;
+};
+
 struct EncodeArgs {
   int q;           // nesting ratio
   int k;           // number of betas
@@ -22,6 +40,9 @@ struct EncodeArgs {
   int tile_et;
   int nb_p;
   uint32_t mtab;
+  // With tiles set, the launch of the slot-compacted encoder may also carry W's tile
+  // decode, as task.wgs workgroups after the encoder's.
+  TileTask task;
 };
 
 struct DecodeArgs {
@@ -58,6 +79,15 @@ hipError_t launch_decode(const uint32_t* codes, const uint32_t* beta, const floa
 // path, W's), 2 contracts; kStageDecodeW decodes only W (A's tile was written by the
 // fused encoder).
 constexpr int kStageDecodeW = 8;
+
+// The TileTask that decodes operand X into its tile ws (rows_p x nb_p blocks, element type
+// et), for a launch of the fused encoder.
+TileTask tile_task(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void* ws);
+// Whether the encoder of rows of `cols` entries (First-beta) can carry a TileTask.
+bool encode_carries_task(int cols, int strategy);
+// Where W's tile starts in a decode-once workspace, and its padded shape.
+void decode_once_layout(int et, int64_t M, int64_t N, int64_t K, int64_t& w_offset,
+                        int64_t& rows_p, int& nb_p);
 
 // Zero the padding of an operand tile written by the fused encoder: rows rows..rows_p-1 and,
 // in the first `rows` rows, blocks nb..nb_p-1.

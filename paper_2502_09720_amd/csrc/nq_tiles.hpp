@@ -1,0 +1,104 @@
+// Decode of a coded operand into the product's integer tiles (m * X2 per block, Alg. 2 +
+// Alg. 5 on every code word), one workgroup's share at a time.  tiles_kernel runs it as a
+// launch of its own; the fused encode-and-multiply runs W's share as the last workgroups of
+// the encoder's grid (TileTask), where they fill the CUs the encoder's last rows leave idle
+// and save a launch.
+#pragma once
+
+#include <type_traits>
+
+#include "nq_device.hpp"
+#include "nq_kernels.hpp"
+
+namespace nq {
+
+// m * X2 of every block of a coded operand into ws[rows_p][nb_p blocks] (zero padding): 8
+// bf16 or fp16 (16 B) per block, or 8 int8 (8 B) for the int8 contraction.  The workspace
+// is one flat array of rows_p * nb_p blocks; workgroup w covers TB = 256 * TPB consecutive
+// blocks of it, thread t the blocks w TB + t + 256 i (i < TPB), so each load and store
+// instruction of a wave touches consecutive blocks.  Every thread issues the loads of all
+// its blocks before decoding any, which keeps TPB loads in flight per thread.
+constexpr int kTilesPerThread = 4;
+
+inline int64_t tile_workgroups(int64_t total) {
+  return (total + 256 * kTilesPerThread - 1) / (256 * kTilesPerThread);
+}
+
+template <int ET, int DV>
+__device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
+                                            const uint32_t* __restrict__ beta, int64_t rows,
+                                            int nb, int64_t total, int nb_p, float inv_nbp,
+                                            int q, uint32_t m2q, uint32_t mtab,
+                                            void* __restrict__ ws, int64_t wg) {
+  constexpr bool I8 = ET == ET_I8;
+  constexpr int TPB = kTilesPerThread;
+  constexpr uint32_t OOB = 0x80000000u;   // past every buffer range below: reads 0
+  using V = typename std::conditional<I8, u32x2, u32x4>::type;
+  const int64_t g0 = wg * (256 * TPB);
+  // the workgroup's first block as (row0, j0); every other block is an offset
+  // o < nb_p + 256 TPB <= 2^14 past (row0, 0), split by a float division checked once in
+  // each direction.  Code and beta words are read through buffer resources based at row0
+  // (32-bit offsets; the range check makes rows past the operand read as zero).
+  const int64_t row0 = g0 / nb_p;
+  const int j0 = (int)(g0 - row0 * nb_p);
+  const int nbw = (nb + 15) >> 4;
+  const int64_t rows_left = rows > row0 ? rows - row0 : 0;
+  const int reach = (j0 + 256 * TPB + nb_p - 1) / nb_p;     // rows this workgroup touches
+  const int64_t span = rows_left < reach ? rows_left : reach;
+  const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(codes + row0 * nb), (short)0, (int)(span * nb * 4), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(beta + row0 * nbw), (short)0, (int)(span * nbw * 4), 0x00020000);
+  uint32_t w[TPB], bw[TPB];
+  int jj[TPB];
+  bool pad[TPB];
+#pragma unroll
+  for (int i = 0; i < TPB; ++i) {
+    const int o = j0 + (int)threadIdx.x + 256 * i;
+    int r = (int)((float)o * inv_nbp);
+    if ((int)__umul24((uint32_t)r, (uint32_t)nb_p) > o) --r;
+    if ((int)__umul24((uint32_t)(r + 1), (uint32_t)nb_p) <= o) ++r;
+    const int j = o - (int)__umul24((uint32_t)r, (uint32_t)nb_p);
+    jj[i] = j;
+    pad[i] = j >= nb || r >= span;
+    const uint32_t co = pad[i] ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nb) + (uint32_t)j);
+    const uint32_t bo = pad[i] ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nbw) + (uint32_t)(j >> 4));
+    w[i] = __builtin_amdgcn_raw_buffer_load_b32(rc, co, 0, 0);
+    bw[i] = __builtin_amdgcn_raw_buffer_load_b32(rb, bo, 0, 0);
+  }
+#pragma unroll
+  for (int i = 0; i < TPB; ++i) {
+    const int64_t g = g0 + (int)threadIdx.x + 256 * i;
+    if (g >= total) break;
+    const int m = beta_mult(mtab, (bw[i] >> (2 * (jj[i] & 15))) & 3u);
+    V out;
+    if constexpr (I8) {
+      out = decode_tile_i8<DV>(w[i], m, q, m2q);
+    } else {
+      out = decode_tile_16<DV, ET == ET_F16>(w[i], m, q, m2q);
+    }
+    if (pad[i]) out = V{};                 // padding past the operand's rows or columns
+    reinterpret_cast<V*>(ws)[g] = out;
+  }
+}
+
+// Workgroup wg of a TileTask, with the element type and decoder chosen at run time (uniform
+// over the workgroup).
+__device__ __forceinline__ void run_tile_task(const TileTask& t, int et, int64_t wg) {
+#define NQ_TB(ET, DV) \
+  tiles_block<ET, DV>(t.codes, t.beta, t.rows, t.nb, t.total, t.nb_p, t.inv_nbp, t.q, t.m2q, t.mtab, t.ws, wg)
+  switch (et * 3 + t.dv) {
+    case 0: NQ_TB(ET_BF16, 0); break;
+    case 1: NQ_TB(ET_BF16, 1); break;
+    case 2: NQ_TB(ET_BF16, 2); break;
+    case 3: NQ_TB(ET_F16, 0); break;
+    case 4: NQ_TB(ET_F16, 1); break;
+    case 5: NQ_TB(ET_F16, 2); break;
+    case 6: NQ_TB(ET_I8, 0); break;
+    case 7: NQ_TB(ET_I8, 1); break;
+    default: NQ_TB(ET_I8, 2); break;
+  }
+#undef NQ_TB
+}
+
+}  // namespace nq

@@ -6,7 +6,8 @@ NQ_CONTRACT_INT8) bit for bit, codes, beta words, scales and C, since both contr
 exact integer tiles with the same kernel; and the product must meet the usual oracle bar
 (relative Frobenius error <= 1e-3).  Cases cover both product paths (M <= 64 and above),
 padding of M and K, fp32 / fp16 / bf16 inputs, both decoders, beta multiples on fp16 tiles,
-Opt-beta, the int8 contraction, streamed long rows and zero rows.
+Opt-beta, the int8 contraction, streamed long rows, zero rows, and the launch that also
+carries W's tile decode (rows of 257..2048 blocks, M > 64) with every tile type and decoder.
 """
 
 import numpy as np
@@ -47,6 +48,16 @@ FUSED_CASES = [
     (8, 16, 100, 4096, "bf16", "t4", 7, 4, None, 1, 0, True),
     (9, 2, 33, 8, "f32", "normal", 14, 4, None, 0, 0, False),
     (10, 64, 128, 128, "bf16", "normal", 12, 3, (2, 5, 9), 1, 1, False),
+    # rows of 257..2048 blocks with M > 64: W's tile decode rides in the encoder's launch,
+    # for every tile type and decoder variant
+    (11, 300, 200, 2056, "bf16", "t4", 14, 4, None, 0, 0, False),
+    (12, 130, 77, 4104, "f16", "normal", 16, 4, None, 1, 0, False),
+    (13, 96, 300, 3000, "bf16", "t4", 16, 4, (6, 8, 10, 15), 0, 0, False),
+    (14, 200, 129, 2304, "bf16", "normal", 15, 4, None, 0, 0, True),
+    (15, 65, 64, 16384, "f32", "normal", 7, 4, None, 1, 0, False),
+    (16, 80, 50, 8192, "bf16", "t4", 7, 3, (1, 2, 4), 1, 0, True),
+    (17, 100, 90, 2560, "bf16", "normal", 16, 3, None, 1, 0, True),
+    (18, 70, 40, 4096, "f16", "t4", 16, 4, (5, 9, 20, 40), 1, 0, False),
 ]
 
 
@@ -89,15 +100,17 @@ def test_encode_matmul_equals_encode_then_matmul(nq, case):
     assert rel <= 1e-3, rel
 
 
-def test_encode_matmul_reuses_its_workspace(nq):
+@pytest.mark.parametrize("K", [1024, 2112])
+def test_encode_matmul_reuses_its_workspace(nq, K):
     """Two calls in a row on one workspace (a larger product, then a smaller one with more
-    padding) give the separate path's results: the padding is cleared on every call."""
+    padding) give the separate path's results: the padding is cleared on every call (K =
+    2112: W's tile decoded inside the encoder's launch)."""
     import torch
-    wstore, _ = workloads.random_rows(600, 300, 1024, dtype="bf16", scale=0.02)
+    wstore, _ = workloads.random_rows(600, 300, K, dtype="bf16", scale=0.02)
     w = nq.encode(_dev(wstore, "bf16"), 14, 4)
-    ws = torch.full((nq.matmul_workspace_size(300, 300, 1024),), 255, dtype=torch.uint8,
+    ws = torch.full((nq.matmul_workspace_size(300, 300, K),), 255, dtype=torch.uint8,
                     device="cuda")
-    for M, K in ((300, 1024), (70, 1024)):
+    for M in (300, 70):
         store, _ = workloads.random_rows(601 + M, M, K, dtype="bf16")
         x = _dev(store, "bf16")
         _, c2 = nq.encode_matmul(x, w, 14, 4, workspace=ws)
@@ -106,18 +119,19 @@ def test_encode_matmul_reuses_its_workspace(nq):
         assert torch.equal(c1, c2)
 
 
-def test_encode_matmul_graph_replays(nq):
+@pytest.mark.parametrize("K", [1024, 2112])
+def test_encode_matmul_graph_replays(nq, K):
     """nq_encode_matmul captured in a HIP graph (through torch.cuda.graph) and replayed
     several times, with eager work that changes the input in place between replays: every
     replay equals the eager call on the same input."""
     import torch
-    store, _ = workloads.random_rows(610, 300, 1024, dtype="bf16", dist="t4")
-    wstore, _ = workloads.random_rows(611, 260, 1024, dtype="bf16", scale=0.02)
+    store, _ = workloads.random_rows(610, 300, K, dtype="bf16", dist="t4")
+    wstore, _ = workloads.random_rows(611, 260, K, dtype="bf16", scale=0.02)
     w = nq.encode(_dev(wstore, "bf16"), 14, 4)
     x = _dev(store, "bf16").clone()
-    ws = torch.empty(nq.matmul_workspace_size(300, 260, 1024), dtype=torch.uint8, device="cuda")
-    codes = torch.empty(300 * 128, dtype=torch.int32, device="cuda")
-    beta = torch.empty(300 * 8, dtype=torch.int32, device="cuda")
+    ws = torch.empty(nq.matmul_workspace_size(300, 260, K), dtype=torch.uint8, device="cuda")
+    codes = torch.empty(300 * (K // 8), dtype=torch.int32, device="cuda")
+    beta = torch.empty(300 * ((K // 8 + 15) // 16), dtype=torch.int32, device="cuda")
     scales = torch.empty(300, dtype=torch.float32, device="cuda")
     out = torch.empty(300, 260, device="cuda")
     args = dict(q=14, k=4, out=out, coded_out=(codes, beta, scales), workspace=ws)
