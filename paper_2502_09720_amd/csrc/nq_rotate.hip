@@ -80,6 +80,13 @@ __device__ __forceinline__ void load8<_Float16>(const _Float16* __restrict__ p, 
   }
 }
 
+// LDS position of entry e: bits 3..5 of e XOR bits 7..9.  The first four-stage pass (stride
+// 8 entries) has the 64 lanes of a wave on 8 consecutive entries times 8 groups 128 entries
+// apart, which would be 8 banks; the swizzle spreads them over all 64.  It permutes entries
+// only within aligned runs of 64, keeps runs of 8 contiguous (the 8-entry loads and stores
+// stay vector accesses) and leaves the other passes conflict-free.
+__device__ __forceinline__ int lds_pos(int e) { return e ^ (((e >> 7) & 7) << 3); }
+
 // Stages h = 2^b0 .. 2^(b0 + NB - 1) of every length-2^lp segment of buf (total entries):
 // each thread takes groups of 2^NB entries whose indices differ only in bits b0 .. b0+NB-1.
 template <int NB>
@@ -91,7 +98,7 @@ __device__ __forceinline__ void fwht_pass(float* buf, int total, int lp, int b0)
     const int base = (seg << lp) | ((lg >> b0) << (b0 + NB)) | (lg & ((1 << b0) - 1));
     float v[G];
 #pragma unroll
-    for (int r = 0; r < G; ++r) v[r] = buf[base + (r << b0)];
+    for (int r = 0; r < G; ++r) v[r] = buf[lds_pos(base + (r << b0))];
 #pragma unroll
     for (int h = 1; h < G; h <<= 1) {
 #pragma unroll
@@ -104,7 +111,7 @@ __device__ __forceinline__ void fwht_pass(float* buf, int total, int lp, int b0)
       }
     }
 #pragma unroll
-    for (int r = 0; r < G; ++r) buf[base + (r << b0)] = v[r];
+    for (int r = 0; r < G; ++r) buf[lds_pos(base + (r << b0))] = v[r];
   }
 }
 
@@ -137,8 +144,9 @@ __global__ __launch_bounds__(256) void rotate_kernel(const T* __restrict__ x, in
         }
       }
     }
+    float* d = buf + lds_pos(e);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) buf[e + i] = v[i];
+    for (int i = 0; i < 8; ++i) d[i] = v[i];
   }
   // stages h = 8 .. p / 2 along each segment of length p, four at a time
   for (int b0 = 3; b0 < lp; b0 += 4) {
@@ -155,17 +163,17 @@ __global__ __launch_bounds__(256) void rotate_kernel(const T* __restrict__ x, in
     // mix the 28 segments of each row column by column, sums in index order
     for (int q = tid; q < rr * p; q += 256) {
       const int r = q / p, b = q - r * p;
-      float* col = buf + r * n + b;
+      const int col = r * n + b;
       float xi[28];
 #pragma unroll
-      for (int i = 0; i < 28; ++i) xi[i] = col[i * p];
+      for (int i = 0; i < 28; ++i) xi[i] = buf[lds_pos(col + i * p)];
 #pragma unroll
       for (int a = 0; a < 28; ++a) {
         float acc = ((kH28.neg[a] & 1u) != 0) ? -xi[0] : xi[0];
 #pragma unroll
         for (int i = 1; i < 28; ++i)
           acc = (((kH28.neg[a] >> i) & 1u) != 0) ? acc - xi[i] : acc + xi[i];
-        col[a * p] = acc;
+        buf[lds_pos(col + a * p)] = acc;
       }
     }
     __syncthreads();
@@ -173,8 +181,9 @@ __global__ __launch_bounds__(256) void rotate_kernel(const T* __restrict__ x, in
   for (int g = tid; g < total / 8; g += 256) {
     const int e = 8 * g;
     const int r = e / n, c = e - r * n;
-    f32x4 lo = {buf[e] * s, buf[e + 1] * s, buf[e + 2] * s, buf[e + 3] * s};
-    f32x4 hi = {buf[e + 4] * s, buf[e + 5] * s, buf[e + 6] * s, buf[e + 7] * s};
+    const float* d = buf + lds_pos(e);
+    f32x4 lo = {d[0] * s, d[1] * s, d[2] * s, d[3] * s};
+    f32x4 hi = {d[4] * s, d[5] * s, d[6] * s, d[7] * s};
     f32x4* o = reinterpret_cast<f32x4*>(y + (row0 + r) * ld_y + c);
     __builtin_nontemporal_store(lo, o);
     __builtin_nontemporal_store(hi, o + 1);
