@@ -6,9 +6,10 @@
 // vector-ALU work per block than the matrix cores spend on it.  So each block is decoded
 // exactly once:
 //
-//   1. tiles_kernel: Alg. 2 on every code word; writes m * X2 (beta = m * base; with the
-//      uniform grid m = t and |m X2| <= 128, exact in bf16) as 8 bf16 into a K-contiguous
-//      workspace tile, zero-padded to the GEMM tile grid.  Beta sets with larger multiples
+//   1. tiles_pair_kernel (both operands in one launch; tiles_kernel for one): Alg. 2 on
+//      every code word; writes m * X2 (beta = m * base; with the uniform grid m = t and
+//      |m X2| <= 128, exact in bf16) as 8 bf16 into a K-contiguous workspace tile,
+//      zero-padded to the GEMM tile grid.  Beta sets with larger multiples
 //      use fp16 tiles (exact to 2048) and fp16 matrix cores at the same rate.  The
 //      workspace (a few tens of MB) stays in the 256 MB Infinity Cache.
 //   2. gemm_kernel: bf16 MFMA GEMM (C = T_A T_W^T, fp32 accumulation) with the epilogue
@@ -94,6 +95,17 @@ void launch_tiles(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void
 template void launch_tiles<ET_BF16>(const MatmulOperand&, int, int64_t, int, void*, hipStream_t);
 template void launch_tiles<ET_F16>(const MatmulOperand&, int, int64_t, int, void*, hipStream_t);
 template void launch_tiles<ET_I8>(const MatmulOperand&, int, int64_t, int, void*, hipStream_t);
+
+// Both operands' tiles in one launch: workgroups below a.wgs decode A, the rest W (one
+// launch boundary and one tail fewer than two launches).
+__global__ __launch_bounds__(256) void tiles_pair_kernel(TileTask a, TileTask w, int et) {
+  const int64_t b = blockIdx.x;
+  if (b < a.wgs) {
+    run_tile_task(a, et, b);
+  } else {
+    run_tile_task(w, et, b - a.wgs);
+  }
+}
 
 // Zero blocks of a tile: the flat range [first, first + count) when cols == 0, else the
 // blocks nb..nb_p-1 of rows 0..rows-1 (cols = nb_p - nb of them per row).
@@ -403,8 +415,14 @@ static hipError_t decode_once(int stages, const MatmulOperand& A, const MatmulOp
   const int kc = nbp * 8 * EB / 16;
   u32x4* wa = reinterpret_cast<u32x4*>(ws);
   u32x4* ww = reinterpret_cast<u32x4*>(static_cast<unsigned char*>(ws) + w_offset);
-  if (stages & 1) launch_tiles<ET>(A, nb, mp, nbp, (void*)wa, st);
-  if (stages & (1 | kStageDecodeW)) launch_tiles<ET>(W, nb, np, nbp, (void*)ww, st);
+  if (stages & 1) {
+    const TileTask ta = tile_task(A, nb, mp, nbp, (void*)wa);
+    const TileTask tw = tile_task(W, nb, np, nbp, (void*)ww);
+    hipLaunchKernelGGL(tiles_pair_kernel, dim3((unsigned)(ta.wgs + tw.wgs)), dim3(256), 0, st,
+                       ta, tw, ET);
+  } else if (stages & kStageDecodeW) {
+    launch_tiles<ET>(W, nb, np, nbp, (void*)ww, st);
+  }
   if (!(stages & 2)) return hipGetLastError();
   // 256 x 256 tiles (half the global->LDS traffic per flop) unless they leave a partly
   // empty last round over the 256 CUs that 256 x 128 tiles (half the work each) avoid
