@@ -33,14 +33,16 @@ METRIC = "nq_matmul TFLOP/s + nq_encode GB/s (q=14,k=4) at Llama-3-8B prefill sh
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=100,
+                    help="untimed steps first (the first ~10 ms of back-to-back steps run "
+                         "slower, about 120 against 104 us per q_proj step)")
     ap.add_argument("--workload", type=int, default=3, help="workload id (see workloads.py)")
     ap.add_argument("--q", type=int, default=None, help="override q (workload 4 has q=7 too)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--graph", action="store_true",
                     help="replay a captured HIP graph of the step instead of launching its "
-                         "kernels directly (slower on these boxes: about 141 against 135 us)")
+                         "kernels directly (slower on these boxes)")
     ap.add_argument("--kv", action="store_true",
                     help="standalone nq_encode / nq_decode of the 2^28-entry fp16 KV-like "
                          "matrix (2^21 rows of 128) against the HBM roofline")
@@ -441,13 +443,19 @@ def main():
         for i in range(args.warmup):
             step(i)
         torch.cuda.synchronize()
-    sev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    # the timed region: K steps back to back (no event markers between them, which would
+    # hold up the stream), then the same K steps again with an event pair around each one
+    # for the per-step device time
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(i, sev[i])
+        step(i)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    sev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+    for i in range(args.steps):
+        step(i, sev[i])
+    torch.cuda.synchronize()
     step_ev_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in sev]))
 
     # the same work as separate calls, with events between them on the kernels' stream:
