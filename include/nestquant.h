@@ -192,8 +192,10 @@ int64_t nq_matmul_workspace_size(int64_t M, int64_t N, int64_t K);
  * writing A's codes, beta indices and scales), then C = A_hat * W_hat^T from the codes (as
  * nq_matmul_ex).  The encoder also writes A's decoded tiles m * X2 (Alg. 2 of the codes it
  * has just chosen; the lattice point itself wherever it passed the overload test) straight
- * into the product's workspace, so A is never decoded in a separate pass; W is decoded as in
- * nq_matmul_ex.  Results are those of nq_encode followed by nq_matmul_ex (with
+ * into the product's workspace, so A is never decoded in a separate pass.  W is decoded as in
+ * nq_matmul_ex; for M > 64 and First-beta rows of 2056..16384 entries that decode runs in
+ * the encoder's launch, after its workgroups.  Results are those of nq_encode followed by
+ * nq_matmul_ex (with
  * NQ_CONTRACT_INT8 in flags, of nq_matmul_stages with that flag).
  *   flags    0 or NQ_CONTRACT_INT8;
  *   x, x_dtype, M (rows), K (cols), ld_x, a_codes, a_beta, a_scales: as nq_encode with pa;
