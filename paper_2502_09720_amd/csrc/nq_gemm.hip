@@ -16,9 +16,10 @@
 //      C_ij = acc * r_Ai * r_Wj * base_A * base_W / 4.
 //
 // GEMM tiling (gfx950): a workgroup of NW = WM x WN waves owns a BM x BN tile of C; each
-// wave owns (BM/WM) x (BN/WN) as v_mfma_f32_32x32x16_bf16 tiles.  K advances 64 bf16
-// (128 B per row) per stage through NSTAGE LDS buffers filled by global_load_lds_dwordx4:
-// each wave instruction moves 8 rows x 128 B straight into LDS (no register staging).  The
+// wave owns (BM/WM) x (BN/WN) as v_mfma_f32_32x32x16_bf16 tiles.  K advances 64 or 32 bf16
+// (SB = 128 or 64 B per row) per stage through NSTAGE LDS buffers filled by
+// global_load_lds_dwordx4: each wave instruction moves 1 KiB of rows straight into LDS (no
+// register staging).  The
 // 16-byte chunk c of row r is stored at chunk c ^ swz(r) (see swz), so that the fragment
 // reads (32 rows, one chunk) hit distinct LDS banks.  Stage k+NSTAGE-1 is loaded while stage k is
 // multiplied.  Workgroups are mapped so that the tiles resident on one XCD (workgroup id
@@ -39,28 +40,37 @@ typedef int i32x4 __attribute__((ext_vector_type(4)));
 typedef int i32x16 __attribute__((ext_vector_type(16)));
 
 namespace gemm {
-constexpr int BK = 64;     // bf16 per stage: 128 B per row (128 int8 for the int8 variant)
-constexpr int BKB = 128;   // bytes per row per stage
+constexpr int BK = 64;     // workspace rows are padded to 64 bf16 / 128 int8 ...
+constexpr int BKB = 128;   // ... i.e. to whole 128-byte runs (the largest stage row)
 constexpr int GROUP_M = 4;
 
-// A tile configuration: BM x BN tile, WM x WN waves, NSTAGE LDS buffers.
-template <int BM_, int BN_, int WM_, int WN_, int NSTAGE_>
+// A tile configuration: BM x BN tile, WM x WN waves, NSTAGE LDS buffers of SB bytes of K per
+// row (128: 64 bf16; 64: 32 bf16, twice the stages in the same LDS).
+template <int BM_, int BN_, int WM_, int WN_, int NSTAGE_, int SB_ = BKB>
 struct Cfg {
-  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, NSTAGE = NSTAGE_;
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, NSTAGE = NSTAGE_, SB = SB_;
   static constexpr int NW = WM * WN;
   static constexpr int TM = BM / WM / 32;  // 32x32 MFMA tiles per wave along M
   static constexpr int TN = BN / WN / 32;
-  static constexpr int STAGE_BYTES = (BM + BN) * BKB;
-  static constexpr int GROUPS = (BM + BN) / 8;  // 8-row groups per stage
+  static constexpr int CH = SB / 16;       // 16-byte chunks per row per stage
+  static constexpr int STAGE_BYTES = (BM + BN) * SB;
+  static constexpr int GROUP_ROWS = 1024 / SB;  // rows moved by one wave load instruction
+  static constexpr int GROUPS = (BM + BN) / GROUP_ROWS;
   static constexpr int GROUPS_PER_WAVE = GROUPS / NW;
+  static_assert(SB == 128 || SB == 64, "stage rows of 128 or 64 bytes");
   static_assert(GROUPS % NW == 0, "row groups must split evenly over the waves");
   static_assert(NSTAGE * STAGE_BYTES <= 160 * 1024, "LDS is 160 KB");
 };
 
 // 256 x 128 tiles (one per CU for the 8B prefill shapes) and 256 x 256 tiles (half the
-// global->LDS traffic per flop, for products with at least one tile per CU).
+// global->LDS traffic per flop, for products with at least one tile per CU).  LDS holds two
+// stages of the big tile with 128 bytes of K per row, or four with 64 bytes; the deeper
+// prefetch of the latter is faster (with two, waves waited on their loads 45% of the time).
+// The int8 contraction (half the MFMA time per byte) keeps the two 128-byte stages, which
+// measured faster for it.
 using CfgMid = Cfg<256, 128, 4, 2, 3>;
-using CfgBig = Cfg<256, 256, 4, 2, 2>;
+using CfgBig = Cfg<256, 256, 4, 2, 4, 64>;
+using CfgBigI8 = Cfg<256, 256, 4, 2, 2>;
 }  // namespace gemm
 
 // One workgroup per 256 * kTilesPerThread blocks of the tile (tiles_block).
@@ -159,12 +169,20 @@ __device__ __forceinline__ void tile_coords(int bid, int tm, int tn, int& pm, in
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// LDS swizzle: chunk c of row r lives at chunk c ^ swz(r), with
+// LDS swizzle: chunk c of row r lives at chunk c ^ swz(r).  128-byte rows (8 chunks):
 // swz(r) = (r mod 8) ^ ((r / 8) mod 4), a function of r mod 32 only (every 32-row MFMA tile
-// starts at a multiple of 32).  The 16-byte fragment reads of 32 consecutive rows at one
-// logical chunk then fall in distinct bank groups whether the LDS serves 8, 16 or 32
-// lanes of a 128-bit read per cycle.
-__device__ __forceinline__ int swz(int r) { return (r ^ ((r >> 3) & 3)) & 7; }
+// starts at a multiple of 32); the 16-byte fragment reads of 32 consecutive rows at one
+// logical chunk then fall in distinct bank groups whether the LDS serves 8, 16 or 32 lanes
+// of a 128-bit read per cycle.  64-byte rows (4 chunks, four rows per 256-byte bank period):
+// swz(r) = (r / 4) mod 4, so that any 16 consecutive rows cover all 64 banks.
+template <int CH>
+__device__ __forceinline__ int swz(int r) {
+  if constexpr (CH == 8) {
+    return (r ^ ((r >> 3) & 3)) & 7;
+  } else {
+    return (r >> 2) & 3;
+  }
+}
 
 // kc: row length of both tiles in 16-byte chunks (a multiple of 8).  ET: int8 tiles and
 // v_mfma_i32_32x32x32_i8 (exact int32 sums), or bf16 / fp16 tiles and
@@ -178,7 +196,7 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
   constexpr int BM = C::BM, BN = C::BN, WM = C::WM, WN = C::WN, NSTAGE = C::NSTAGE;
   constexpr int NW = C::NW, TM = C::TM, TN = C::TN, STAGE_BYTES = C::STAGE_BYTES;
   constexpr int GROUPS_PER_WAVE = C::GROUPS_PER_WAVE;
-  constexpr int CH = gemm::BKB / 16;  // 16-byte chunks per row per stage
+  constexpr int CH = C::CH, SB = C::SB, GR = C::GROUP_ROWS;
   constexpr bool I8 = ET == ET_I8;
   extern __shared__ __attribute__((aligned(1024))) unsigned char lds[];
 
@@ -188,22 +206,22 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
   const int wave = tid >> 6, lane = tid & 63;
   const int wm = wave / WN, wn = wave % WN;
 
-  // This lane's source for each of the wave's row groups: row (lane >> 3) of the group,
-  // stored at physical chunk lane & 7, i.e. logical chunk (lane & 7) ^ swz(row).
-  const int lrow = lane >> 3;
+  // This lane's source for each of the wave's row groups: row lane / CH of the group,
+  // stored at physical chunk lane % CH, i.e. logical chunk (lane % CH) ^ swz(row).
+  const int lrow = lane / CH;
   const u32x4* src[GROUPS_PER_WAVE];
   int dst[GROUPS_PER_WAVE];
 #pragma unroll
   for (int i = 0; i < GROUPS_PER_WAVE; ++i) {
     const int grp = wave + i * NW;              // 0 .. GROUPS-1; A groups first
-    const int row = grp * 8 + lrow;             // row within the stage (A rows, then W rows)
-    const int lchunk = (lane & 7) ^ swz(row);
-    if (grp < BM / 8) {
+    const int row = grp * GR + lrow;            // row within the stage (A rows, then W rows)
+    const int lchunk = (lane % CH) ^ swz<CH>(row);
+    if (grp < BM / GR) {
       src[i] = ta + ((int64_t)pm * BM + row) * kc + lchunk;
     } else {
       src[i] = tw + ((int64_t)pn * BN + (row - BM)) * kc + lchunk;
     }
-    dst[i] = grp * 1024;                        // 8 rows x 128 B
+    dst[i] = grp * 1024;                        // GR rows x SB bytes
   }
   auto load_stage = [&](int ks) {
     unsigned char* base = lds + (ks % NSTAGE) * STAGE_BYTES;
@@ -224,11 +242,11 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
   // swizzle depends only on the row modulo 32, and every 32-row tile starts at a multiple
   // of 32, so one offset per kk serves all of this lane's A and W tiles.
   const int frow = lane & 31;
-  const int abase = (wm * (BM / WM) + frow) * 128;
-  const int wbase = BM * 128 + (wn * (BN / WN) + frow) * 128;
+  const int abase = (wm * (BM / WM) + frow) * SB;
+  const int wbase = BM * SB + (wn * (BN / WN) + frow) * SB;
   int coff[CH / 2];
 #pragma unroll
-  for (int kk = 0; kk < CH / 2; ++kk) coff[kk] = ((2 * kk + (lane >> 5)) ^ swz(frow)) * 16;
+  for (int kk = 0; kk < CH / 2; ++kk) coff[kk] = ((2 * kk + (lane >> 5)) ^ swz<CH>(frow)) * 16;
 
   const int nks = kc / CH;
 #pragma unroll
@@ -279,10 +297,10 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
     u32x4 af[2][TM], bfr[2][TN];
 #pragma unroll
     for (int i = 0; i < TM; ++i)
-      af[0][i] = *reinterpret_cast<const u32x4*>(sb + abase + i * 32 * 128 + coff[0]);
+      af[0][i] = *reinterpret_cast<const u32x4*>(sb + abase + i * 32 * SB + coff[0]);
 #pragma unroll
     for (int j = 0; j < TN; ++j)
-      bfr[0][j] = *reinterpret_cast<const u32x4*>(sb + wbase + j * 32 * 128 + coff[0]);
+      bfr[0][j] = *reinterpret_cast<const u32x4*>(sb + wbase + j * 32 * SB + coff[0]);
     constexpr int KSTEPS = CH / 2;  // MFMAs per (i, j) per stage: 32 B of K each
     constexpr int LOADS_PER_STEP = (GROUPS_PER_WAVE + KSTEPS - 1) / KSTEPS;
 #pragma unroll
@@ -306,9 +324,9 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
         }
         if (kk + 1 < KSTEPS) {
           if (m < TM) {
-            af[cur ^ 1][m] = *reinterpret_cast<const u32x4*>(sb + abase + m * 32 * 128 + coff[kk + 1]);
+            af[cur ^ 1][m] = *reinterpret_cast<const u32x4*>(sb + abase + m * 32 * SB + coff[kk + 1]);
           } else if (m < TM + TN) {
-            bfr[cur ^ 1][m - TM] = *reinterpret_cast<const u32x4*>(sb + wbase + (m - TM) * 32 * 128 + coff[kk + 1]);
+            bfr[cur ^ 1][m - TM] = *reinterpret_cast<const u32x4*>(sb + wbase + (m - TM) * 32 * SB + coff[kk + 1]);
           }
         }
         const int g = kk * LOADS_PER_STEP + m;
@@ -322,9 +340,9 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
       for (int m = TM * TN; m < TM + TN || m < LOADS_PER_STEP; ++m) {
         if (kk + 1 < KSTEPS) {
           if (m < TM) {
-            af[cur ^ 1][m] = *reinterpret_cast<const u32x4*>(sb + abase + m * 32 * 128 + coff[kk + 1]);
+            af[cur ^ 1][m] = *reinterpret_cast<const u32x4*>(sb + abase + m * 32 * SB + coff[kk + 1]);
           } else if (m < TM + TN) {
-            bfr[cur ^ 1][m - TM] = *reinterpret_cast<const u32x4*>(sb + wbase + (m - TM) * 32 * 128 + coff[kk + 1]);
+            bfr[cur ^ 1][m - TM] = *reinterpret_cast<const u32x4*>(sb + wbase + (m - TM) * 32 * SB + coff[kk + 1]);
           }
         }
         const int g = kk * LOADS_PER_STEP + m;
@@ -428,7 +446,8 @@ static hipError_t decode_once(int stages, const MatmulOperand& A, const MatmulOp
   // empty last round over the 256 CUs that 256 x 128 tiles (half the work each) avoid
   const int64_t big = (mp / 256) * (np / 256), mid = (mp / 256) * (np / 128);
   if (big >= 256 && 2 * ((big + 255) / 256) <= (mid + 255) / 256) {
-    launch_gemm<CfgBig, ET>(wa, ww, kc, mp, np, A, W, c, ldc, scale, st);
+    using Big = typename std::conditional<ET == ET_I8, CfgBigI8, CfgBig>::type;
+    launch_gemm<Big, ET>(wa, ww, kc, mp, np, A, W, c, ldc, scale, st);
   } else {
     launch_gemm<CfgMid, ET>(wa, ww, kc, mp, np, A, W, c, ldc, scale, st);
   }
@@ -449,9 +468,10 @@ hipError_t gemm_set_attributes() {
   using namespace gemm;
   const void* k[6] = {(const void*)gemm_kernel<CfgMid, ET_BF16>, (const void*)gemm_kernel<CfgMid, ET_F16>,
                       (const void*)gemm_kernel<CfgMid, ET_I8>, (const void*)gemm_kernel<CfgBig, ET_BF16>,
-                      (const void*)gemm_kernel<CfgBig, ET_F16>, (const void*)gemm_kernel<CfgBig, ET_I8>};
+                      (const void*)gemm_kernel<CfgBig, ET_F16>, (const void*)gemm_kernel<CfgBigI8, ET_I8>};
   constexpr int mid = CfgMid::NSTAGE * CfgMid::STAGE_BYTES, big = CfgBig::NSTAGE * CfgBig::STAGE_BYTES;
-  const int bytes[6] = {mid, mid, mid, big, big, big};
+  constexpr int big8 = CfgBigI8::NSTAGE * CfgBigI8::STAGE_BYTES;
+  const int bytes[6] = {mid, mid, mid, big, big, big8};
   for (int i = 0; i < 6; ++i) {
     const hipError_t e = hipFuncSetAttribute(k[i], hipFuncAttributeMaxDynamicSharedMemorySize, bytes[i]);
     if (e != hipSuccess) return e;
