@@ -80,8 +80,8 @@ hipError_t launch_decode(const uint32_t* codes, const uint32_t* beta, const floa
 // fused encoder).
 constexpr int kStageDecodeW = 8;
 
-// The TileTask that decodes operand X into its tile ws (rows_p x nb_p blocks, element type
-// et), for a launch of the fused encoder.
+// The TileTask that decodes operand X into its tile ws (rows_p x nb_p blocks; the element
+// type comes with the launch that runs it).
 TileTask tile_task(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void* ws);
 // Whether the encoder of rows of `cols` entries (First-beta) can carry a TileTask.
 bool encode_carries_task(int cols, int strategy);
