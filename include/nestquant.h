@@ -163,6 +163,11 @@ nq_status nq_matmul_ex(const nq_params* pa, const uint32_t* a_codes, const uint3
  * stage bit, is NQ_ERR_INVALID_ARG.  The workspace size is nq_matmul_workspace_size either
  * way. */
 enum { NQ_STAGE_DECODE = 1, NQ_STAGE_CONTRACT = 2, NQ_CONTRACT_INT8 = 4 };
+
+/* Flag of nq_encode_matmul: rotate the activation's rows before coding them (as
+ * nq_rotate_encode; W must then have been coded from rotated rows, W U, so that
+ * (A U)(W U)^T = A W^T). */
+enum { NQ_ROTATE_A = 8 };
 nq_status nq_matmul_stages(int32_t stages, const nq_params* pa, const uint32_t* a_codes,
                            const uint32_t* a_beta, const float* a_scales, int64_t M,
                            const nq_params* pw, const uint32_t* w_codes, const uint32_t* w_beta,
@@ -184,6 +189,18 @@ nq_status nq_matmul_stages(int32_t stages, const nq_params* pa, const uint32_t* 
 nq_status nq_rotate(const void* x, nq_dtype x_dtype, int64_t rows, int64_t cols, int64_t ld_x,
                     float* y, int64_t ld_y, void* hip_stream);
 
+/* nq_rotate followed by nq_encode in one pass (Sec. 5: the rotation in front of the
+ * quantizer): every row of x is rotated in on-chip memory with nq_rotate's arithmetic and
+ * coded from there, so the fp32 rotated rows never go to memory.  Codes, beta indices and
+ * scales equal those of nq_encode on nq_rotate's output, bit for bit.
+ *   p, x, x_dtype, rows, cols, ld_x, codes, beta_idx, scales: as nq_encode.
+ * Supported: First-beta, and cols = 3584, 4096, 7168, 8192, 14336 or 16384 (widths nq_rotate
+ * supports with 257..2048 blocks per row); else NQ_ERR_UNSUPPORTED (call nq_rotate, then
+ * nq_encode).  Validation as nq_encode; rows == 0 is a no-op. */
+nq_status nq_rotate_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t rows,
+                           int64_t cols, int64_t ld_x, uint32_t* codes, uint32_t* beta_idx,
+                           float* scales, void* hip_stream);
+
 /* Workspace bytes nq_matmul_ex needs for an M x N x K product (0 when M or N is 0; -1 for
  * an invalid K). */
 int64_t nq_matmul_workspace_size(int64_t M, int64_t N, int64_t K);
@@ -196,8 +213,10 @@ int64_t nq_matmul_workspace_size(int64_t M, int64_t N, int64_t K);
  * nq_matmul_ex; for M > 64 and First-beta rows of 2056..16384 entries that decode runs in
  * the encoder's launch, after its workgroups.  Results are those of nq_encode followed by
  * nq_matmul_ex (with
- * NQ_CONTRACT_INT8 in flags, of nq_matmul_stages with that flag).
- *   flags    0 or NQ_CONTRACT_INT8;
+ * NQ_CONTRACT_INT8 in flags, of nq_matmul_stages with that flag; with NQ_ROTATE_A, of
+ * nq_rotate_encode in place of nq_encode).
+ *   flags    0, or NQ_CONTRACT_INT8 and / or NQ_ROTATE_A (the widths and strategy of
+ *            nq_rotate_encode, else NQ_ERR_UNSUPPORTED);
  *   x, x_dtype, M (rows), K (cols), ld_x, a_codes, a_beta, a_scales: as nq_encode with pa;
  *   pw, w_codes, w_beta, w_scales, N, c, ldc: as nq_matmul_ex;
  *   workspace: device, 16-byte aligned, at least nq_matmul_workspace_size(M, N, K) bytes.

@@ -12,6 +12,7 @@ from .binding import (  # noqa: F401
     DECODER_M,
     FIRST_BETA,
     OPT_BETA,
+    ROTATE_A,
     STAGE_CONTRACT,
     STAGE_DECODE,
     Coded,

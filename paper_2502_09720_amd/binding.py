@@ -49,6 +49,8 @@ def library():
         vp, i64, u32p, f32p = ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p
         pp = ctypes.POINTER(_Params)
         lib.nq_encode.argtypes = [pp, vp, ctypes.c_int, i64, i64, i64, u32p, u32p, f32p, vp]
+        lib.nq_rotate_encode.argtypes = lib.nq_encode.argtypes
+        lib.nq_rotate_encode.restype = ctypes.c_int
         lib.nq_decode.argtypes = [pp, u32p, u32p, f32p, i64, i64, vp, ctypes.c_int, i64, vp]
         lib.nq_matmul.argtypes = [pp, u32p, u32p, f32p, i64, pp, u32p, u32p, f32p, i64, i64,
                                   f32p, i64, vp]
@@ -141,11 +143,13 @@ class Coded(NamedTuple):
 
 
 def encode(x, q=14, k=4, base=None, stream=None, out=None, decoder=DECODER_FULL,
-           strategy=FIRST_BETA, mult=None):
+           strategy=FIRST_BETA, mult=None, rotate=False):
     """nq_encode on a 2-D cuda tensor (fp32 / fp16 / bf16, unit stride along rows).
     ``decoder`` is the decoder the code is defined with (DECODER_FULL or DECODER_M);
     ``strategy`` picks the beta of each block (FIRST_BETA or OPT_BETA); ``mult`` gives the
-    betas as integer multiples of base (k increasing integers in [1, 64]; None: 1..k)."""
+    betas as integer multiples of base (k increasing integers in [1, 64]; None: 1..k).
+    ``rotate``: nq_rotate_encode, the rows Hadamard-rotated (as ``rotate``) while they are
+    coded (First-beta; cols in 3584, 4096, 7168, 8192, 14336, 16384)."""
     import torch
     if x.dim() != 2 or x.stride(1) != 1 or not x.is_cuda:
         raise ValueError("x must be a 2-D cuda tensor with unit column stride")
@@ -161,10 +165,10 @@ def encode(x, q=14, k=4, base=None, stream=None, out=None, decoder=DECODER_FULL,
     else:
         codes, beta, scales = out
     p = _params(q, k, base, decoder, strategy, mult)
-    _check(lib.nq_encode(ctypes.byref(p), ctypes.c_void_p(x.data_ptr()), _dtype_code(x.dtype),
-                         rows, cols, x.stride(0), ctypes.c_void_p(codes.data_ptr()),
-                         ctypes.c_void_p(beta.data_ptr()), ctypes.c_void_p(scales.data_ptr()),
-                         _stream(stream)))
+    fn = lib.nq_rotate_encode if rotate else lib.nq_encode
+    _check(fn(ctypes.byref(p), ctypes.c_void_p(x.data_ptr()), _dtype_code(x.dtype), rows, cols,
+              x.stride(0), ctypes.c_void_p(codes.data_ptr()), ctypes.c_void_p(beta.data_ptr()),
+              ctypes.c_void_p(scales.data_ptr()), _stream(stream)))
     return Coded(codes, beta, scales, rows, cols, int(q), int(k), p.base, int(decoder),
                  None if mult is None else tuple(int(v) for v in mult))
 
@@ -188,6 +192,7 @@ def decode(coded, out_dtype=None, stream=None, out=None):
 STAGE_DECODE = 1
 STAGE_CONTRACT = 2
 CONTRACT_INT8 = 4
+ROTATE_A = 8
 
 
 def matmul(a, w, stream=None, out=None, workspace=None, stages=STAGE_DECODE | STAGE_CONTRACT,
@@ -230,11 +235,12 @@ def matmul(a, w, stream=None, out=None, workspace=None, stages=STAGE_DECODE | ST
 
 def encode_matmul(x, w, q=14, k=4, base=None, decoder=DECODER_FULL, strategy=FIRST_BETA,
                   mult=None, stream=None, out=None, coded_out=None, workspace=None,
-                  int8=False):
+                  int8=False, rotate=False):
     """nq_encode_matmul: codes the activation x (2-D cuda tensor, as ``encode``) and returns
     (its Coded operand, C = A_hat W_hat^T) from one call, the encoder writing A's decoded
     tiles straight into the product's workspace.  The same results as ``encode`` then
-    ``matmul``."""
+    ``matmul``.  ``rotate``: x's rows are Hadamard-rotated while coded (NQ_ROTATE_A; w must
+    hold the codes of rotated weight rows)."""
     import torch
     if x.dim() != 2 or x.stride(1) != 1 or not x.is_cuda:
         raise ValueError("x must be a 2-D cuda tensor with unit column stride")
@@ -257,8 +263,9 @@ def encode_matmul(x, w, q=14, k=4, base=None, decoder=DECODER_FULL, strategy=FIR
         workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
     pa = _params(q, k, base, decoder, strategy, mult)
     pw = _params(w.q, w.k, w.base, w.decoder, mult=w.mult)
+    flags = (CONTRACT_INT8 if int8 else 0) | (ROTATE_A if rotate else 0)
     _check(lib.nq_encode_matmul(
-        CONTRACT_INT8 if int8 else 0, ctypes.byref(pa), ctypes.c_void_p(x.data_ptr()),
+        flags, ctypes.byref(pa), ctypes.c_void_p(x.data_ptr()),
         _dtype_code(x.dtype), M, K, x.stride(0), ctypes.c_void_p(codes.data_ptr()),
         ctypes.c_void_p(beta.data_ptr()), ctypes.c_void_p(scales.data_ptr()), ctypes.byref(pw),
         ctypes.c_void_p(w.codes.data_ptr()), ctypes.c_void_p(w.beta.data_ptr()),

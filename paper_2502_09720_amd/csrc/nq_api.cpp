@@ -112,7 +112,7 @@ const char* nq_status_string(nq_status s) {
 
 const char* nq_last_error(void) { return g_last_error; }
 
-int32_t nq_version(void) { return 400; }
+int32_t nq_version(void) { return 410; }
 
 static nq_status check_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t rows,
                               int64_t cols, int64_t ld_x, uint32_t* codes, uint32_t* beta_idx,
@@ -201,6 +201,39 @@ static nq_status check_matmul(const nq_params* pa, const uint32_t* a_codes,
   if (!a_codes || !a_beta || !a_scales || !w_codes || !w_beta || !w_scales || !c)
     return fail(NQ_ERR_INVALID_ARG, "%s: NULL array pointer", who);
   return NQ_OK;
+}
+
+// The rotation of rows of `cols` entries inside the encoder: NQ_ERR_UNSUPPORTED unless the
+// encoder's one-row-per-workgroup instantiations can hold and rotate them.
+static nq_status rotation_args(const nq_params* p, int64_t cols, nq::EncodeArgs& a,
+                               const char* who) {
+  if (!nq::encode_rotates((int)cols, p->strategy))
+    return fail(NQ_ERR_UNSUPPORTED,
+                "%s: rotating while coding needs First-beta and cols in {3584, 4096, 7168, 8192, "
+                "14336, 16384} (got cols=%lld, strategy=%d); call nq_rotate, then nq_encode",
+                who, (long long)cols, p->strategy);
+  int pp = 0;
+  nq::rotation_split(cols, pp);
+  int lp = 0;
+  while ((1 << lp) < pp) ++lp;
+  a.rot_p = pp;
+  a.rot_lp = lp;
+  a.rot_s = (float)(1.0 / std::sqrt((double)cols));   // as nq_rotate's scaling
+  return NQ_OK;
+}
+
+nq_status nq_rotate_encode(const nq_params* p, const void* x, nq_dtype x_dtype, int64_t rows,
+                           int64_t cols, int64_t ld_x, uint32_t* codes, uint32_t* beta_idx,
+                           float* scales, void* hip_stream) {
+  const char* who = "nq_rotate_encode";
+  if (nq_status s = check_encode(p, x, x_dtype, rows, cols, ld_x, codes, beta_idx, scales, who))
+    return s;
+  nq::EncodeArgs a = encode_args(p);
+  if (nq_status s = rotation_args(p, cols, a, who)) return s;
+  if (rows == 0) return ok();
+  return hip_status(nq::launch_encode(x, (int)x_dtype, rows, (int)cols, ld_x, a, codes, beta_idx,
+                                      scales, (hipStream_t)hip_stream),
+                    who);
 }
 
 nq_status nq_rotate(const void* x, nq_dtype x_dtype, int64_t rows, int64_t cols, int64_t ld_x,
@@ -410,10 +443,13 @@ nq_status nq_encode_matmul(int32_t flags, const nq_params* pa, const void* x, nq
                            const float* w_scales, int64_t N, float* c, int64_t ldc,
                            void* workspace, int64_t workspace_bytes, void* hip_stream) {
   const char* who = "nq_encode_matmul";
-  if ((flags & ~NQ_CONTRACT_INT8) != 0)
-    return fail(NQ_ERR_INVALID_ARG, "%s: flags may only hold NQ_CONTRACT_INT8", who);
+  if ((flags & ~(NQ_CONTRACT_INT8 | NQ_ROTATE_A)) != 0)
+    return fail(NQ_ERR_INVALID_ARG, "%s: flags may only hold NQ_CONTRACT_INT8, NQ_ROTATE_A", who);
   if (nq_status s = check_encode(pa, x, x_dtype, M, K, ld_x, a_codes, a_beta, a_scales, who))
     return s;
+  nq::EncodeArgs a = encode_args(pa);
+  if (flags & NQ_ROTATE_A)
+    if (nq_status s = rotation_args(pa, K, a, who)) return s;
   if (nq_status s = check_matmul(pa, a_codes, a_beta, a_scales, M, pw, w_codes, w_beta,
                                  w_scales, N, K, c, ldc, who))
     return s;
@@ -429,7 +465,6 @@ nq_status nq_encode_matmul(int32_t flags, const nq_params* pa, const void* x, nq
   // 1. encode A; the encoder also writes A's decoded tiles into the workspace and, on the
   //    decode-once path where its instantiation allows, W's tile decode rides in the same
   //    launch (workgroups after the encoder's, which fill the encoder's tail)
-  nq::EncodeArgs a = encode_args(pa);
   const int nbp = tile_blocks(K, et);
   const int64_t rows_p = M <= nq::kFusedMaxM ? (M + 15) / 16 * 16 : (M + 255) / 256 * 256;
   a.tiles = workspace;

@@ -13,6 +13,7 @@
 // boundary comparison is made exactly.
 #include "nq_device.hpp"
 #include "nq_kernels.hpp"
+#include "nq_rotate.hpp"
 #include "nq_tiles.hpp"
 
 namespace nq {
@@ -598,7 +599,9 @@ __device__ __forceinline__ float skip_threshold(float c, int q) {
   return f;
 }
 
-template <typename T, int LANES, int BPT, bool TILES>
+// ROT (one row per workgroup only): the row is first rotated in LDS (rotate_rows_lds, the
+// arithmetic of nq_rotate) and the encoder reads its blocks from there, times a.rot_s.
+template <typename T, int LANES, int BPT, bool TILES, bool ROT>
 __global__ __launch_bounds__(256) void encode_wave_kernel(
     const T* __restrict__ x, int64_t rows, int cols, int64_t ld_x, EncodeArgs a,
     uint32_t* __restrict__ codes, uint32_t* __restrict__ beta, float* __restrict__ scales) {
@@ -606,7 +609,9 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
   constexpr int SLOTS = SM::SLOTS;
   constexpr int RW = SM::ROWS_PER_WAVE;
   constexpr int CW = SM::WGROW ? 1 : 4;          // row tables: per wave, or one per workgroup
-  __shared__ RawBlock<T> rawl[4][SLOTS];
+  static_assert(!ROT || SM::WGROW, "rotation in LDS needs one row per workgroup");
+  __shared__ RawBlock<T> rawl[4][ROT ? 1 : SLOTS];
+  __shared__ __attribute__((aligned(16))) float rbuf[ROT ? 8 * 4 * SLOTS : 1];
   __shared__ uint32_t queue[4][SLOTS];
   __shared__ uint8_t tsl[4][SLOTS];
   __shared__ float crow[CW][RW][4];
@@ -635,9 +640,38 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
   };
   const int64_t row0 = row_base(wave);
   const double n = (double)cols;
+  // block of slot sl of wave w, as fp32
+  auto slot_block = [&](int w, int sl, float (&v)[8]) {
+    if constexpr (ROT) {
+      const float* d = rbuf + lds_pos(8 * SM::j(sl >> 6, sl & 63, w));
+#pragma unroll
+      for (int l = 0; l < 8; ++l) v[l] = d[l] * a.rot_s;
+    } else {
+      unpack_raw<T>(rawl[w][sl], v);
+    }
+  };
 
   // ---- phase 0: stage the slots in LDS, row sums of squares ----
-  {
+  if constexpr (ROT) {
+    // the whole workgroup rotates its row (uniform: one row per workgroup)
+    if (row0 < rows) rotate_rows_lds<T>(x + row0 * ld_x, ld_x, 1, cols, a.rot_p, a.rot_lp, rbuf);
+    double part = 0.0;
+#pragma unroll
+    for (int i = 0; i < BPT; ++i) {
+      const int j = SM::j(i, lane, wave);
+      if (row0 < rows && j < nb) {
+        float v[8];
+        slot_block(wave, i * 64 + lane, v);
+        double s = 0.0;
+#pragma unroll
+        for (int l = 0; l < 8; ++l) s = __builtin_fma((double)v[l], (double)v[l], s);
+        part += s;
+      }
+    }
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) part += __shfl_xor(part, m, 64);
+    if (lane == 0) rsum[wave][0] = part;
+  } else {
     RawBlock<T> raw[BPT];
 #pragma unroll
     for (int i = 0; i < BPT; ++i) {
@@ -691,7 +725,7 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
           int w, sl;
           SM::slot_of(rw, j, wave, w, sl);
           float v[8];
-          unpack_raw<T>(rawl[w][sl], v);
+          slot_block(w, sl, v);
 #pragma unroll
           for (int l = 0; l < 8; ++l) dd_add_square(hi, lo, v[l]);
         }
@@ -729,7 +763,7 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
     int P[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     if (coded) {
       float v[8];
-      unpack_raw<T>(rawl[wave][sl], v);
+      slot_block(wave, sl, v);
       // first beta whose point is not surely overloaded: one threshold test per beta
       const float mx = a.decoder ? m_stat(v) : root_bound_f(v);
       const f32x4 hi = *reinterpret_cast<const f32x4*>(chi[cw][rw]);
@@ -798,7 +832,7 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
       const int64_t row = row_base(w) + rw;
       const int c2 = SM::WGROW ? 0 : w;
       float v[8], c[4];
-      unpack_raw<T>(rawl[w][sl], v);
+      slot_block(w, sl, v);
 #pragma unroll
       for (int tt = 0; tt < 4; ++tt) c[tt] = crow[c2][rw][tt];
       uint32_t word;
@@ -847,7 +881,7 @@ static hipError_t launch_t(const void* x, int64_t rows, int cols, int64_t ld_x,
   return hipGetLastError();
 }
 
-template <typename T, int LANES, int BPT, bool TILES>
+template <typename T, int LANES, int BPT, bool TILES, bool ROT = false>
 static hipError_t launch_w(const void* x, int64_t rows, int cols, int64_t ld_x,
                            const EncodeArgs& a, uint32_t* codes, uint32_t* beta, float* scales,
                            hipStream_t st) {
@@ -855,7 +889,7 @@ static hipError_t launch_w(const void* x, int64_t rows, int cols, int64_t ld_x,
   const int64_t rows_per_wg = SM::WGROW ? 1 : 4 * SM::ROWS_PER_WAVE;
   int64_t grid = (rows + rows_per_wg - 1) / rows_per_wg;
   if (TILES && SM::WGROW) grid += a.task.wgs;
-  hipLaunchKernelGGL((encode_wave_kernel<T, LANES, BPT, TILES>), dim3((unsigned)grid), dim3(256), 0, st,
+  hipLaunchKernelGGL((encode_wave_kernel<T, LANES, BPT, TILES, ROT>), dim3((unsigned)grid), dim3(256), 0, st,
                      (const T*)x, rows, cols, ld_x, a, codes, beta, scales);
   return hipGetLastError();
 }
@@ -865,6 +899,15 @@ static hipError_t launch_dtype(const void* x, int64_t rows, int cols, int64_t ld
                                const EncodeArgs& a, uint32_t* codes, uint32_t* beta,
                                float* scales, hipStream_t st) {
   const int nb = cols / 8;
+  if (a.rot_p) {
+    // rows rotated in LDS first: one row per workgroup
+#define NQ_R(B) return launch_w<T, 256, B, TILES, true>(x, rows, cols, ld_x, a, codes, beta, scales, st)
+    if (!encode_rotates(cols, a.strategy)) return hipErrorInvalidValue;
+    if (nb <= 512) NQ_R(2);
+    if (nb <= 1024) NQ_R(4);
+    NQ_R(8);
+#undef NQ_R
+  }
   if (a.strategy) {
     // Opt-beta: a lane group of up to 64 holds short rows in registers; longer rows stream
 #define NQ_O(L, B) return launch_t<T, L, B, true, TILES>(x, rows, cols, ld_x, a, codes, beta, scales, st)
@@ -899,6 +942,13 @@ static hipError_t launch_dtype(const void* x, int64_t rows, int cols, int64_t ld
 bool encode_carries_task(int cols, int strategy) {
   const int nb = cols / 8;
   return strategy == 0 && nb > 256 && nb <= 2048;
+}
+
+// The same instantiations rotate their row in LDS, for widths nq_rotate supports:
+// 4096, 8192, 16384 and 28 * 2^k = 3584, 7168, 14336.
+bool encode_rotates(int cols, int strategy) {
+  int p = 0;
+  return encode_carries_task(cols, strategy) && rotation_split(cols, p) != 0;
 }
 
 hipError_t launch_encode(const void* x, int dtype, int64_t rows, int cols, int64_t ld_x,

@@ -43,6 +43,11 @@ struct EncodeArgs {
   // With tiles set, the launch of the slot-compacted encoder may also carry W's tile
   // decode, as task.wgs workgroups after the encoder's.
   TileTask task;
+  // Rows rotated in LDS before coding (nq_rotate_encode): rot_p = cols / m (m = 1 or 28,
+  // 2^rot_lp), rot_s = fl32(1 / sqrt(cols)); rot_p == 0: no rotation.
+  int rot_p;
+  int rot_lp;
+  float rot_s;
 };
 
 struct DecodeArgs {
@@ -83,8 +88,10 @@ constexpr int kStageDecodeW = 8;
 // The TileTask that decodes operand X into its tile ws (rows_p x nb_p blocks; the element
 // type comes with the launch that runs it).
 TileTask tile_task(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void* ws);
-// Whether the encoder of rows of `cols` entries (First-beta) can carry a TileTask.
+// Whether the encoder of rows of `cols` entries (First-beta) can carry a TileTask, and
+// whether it can rotate its rows in LDS (also needs a width nq_rotate supports).
 bool encode_carries_task(int cols, int strategy);
+bool encode_rotates(int cols, int strategy);
 // Where W's tile starts in a decode-once workspace, and its padded shape.
 void decode_once_layout(int et, int64_t M, int64_t N, int64_t K, int64_t& w_offset,
                         int64_t& rows_p, int& nb_p);

@@ -272,7 +272,8 @@ def test_beta_dp_rejects(lib, case):
 
 
 @pytest.mark.parametrize("case", [
-    dict(flags=1), dict(flags=2), dict(flags=8), dict(pa=None), dict(x=NULL), dict(K=12),
+    dict(flags=1), dict(flags=2), dict(flags=16), dict(flags=8), dict(pa=None), dict(x=NULL),
+    dict(K=12),
     dict(dtype=9), dict(c=NULL), dict(ldc=10), dict(ws_bytes=0),
     dict(pa=_p(q=16)),                              # int8 needs k q <= 63
 ])
@@ -293,3 +294,28 @@ def test_encode_matmul_empty_is_noop(lib):
     p = _p()
     assert lib.nq_encode_matmul(0, ctypes.byref(p), NULL, 0, 0, 64, 64, NULL, NULL, NULL,
                                 ctypes.byref(p), NULL, NULL, NULL, 0, NULL, 0, NULL, 0, S) == 0
+
+
+@pytest.mark.parametrize("case,status", [
+    (dict(cols=2048), 2), (dict(cols=4104), 2), (dict(cols=32768), 2), (dict(cols=28672), 2),
+    (dict(strategy=1), 2), (dict(q=1), 1), (dict(x=NULL), 1), (dict(ld=100), 1),
+    (dict(dtype=7), 2), (dict(x=ctypes.c_void_p(0x1004)), 1),
+])
+def test_rotate_encode_rejects(lib, case, status):
+    """Widths the in-LDS rotation does not hold, Opt-beta, and the checks of nq_encode."""
+    args = dict(cols=4096, strategy=0, q=14, x=FAKE, ld=None, dtype=2)
+    args.update(case)
+    p = _pd(0, args["strategy"])
+    p.q = args["q"]
+    ld = args["ld"] if args["ld"] is not None else args["cols"]
+    st = lib.nq_rotate_encode(ctypes.byref(p), args["x"], args["dtype"], 4, args["cols"], ld,
+                              FAKE, FAKE, FAKE, S)
+    assert st == status
+    assert lib.nq_last_error()
+
+
+def test_rotate_encode_zero_rows_is_noop(lib):
+    p = _p()
+    for cols in (3584, 4096, 7168, 8192, 14336, 16384):
+        assert lib.nq_rotate_encode(ctypes.byref(p), NULL, 2, 0, cols, cols, NULL, NULL, NULL,
+                                    S) == 0

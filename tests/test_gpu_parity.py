@@ -569,6 +569,71 @@ def test_rotate_then_encode_parity(nq):
     assert (t_rot == 4).mean() < (t_plain == 4).mean()
 
 
+ROTATE_ENCODE_CASES = [
+    # (seed, rows, cols, dtype, dist, q, k, decoder, mult): every width the in-LDS rotation
+    # holds (4096, 8192, 16384: Sylvester; 3584, 7168, 14336: H_28 mix), 2 / 4 / 8 blocks
+    # per lane, all input types, both decoders, beta multiples
+    (80, 101, 4096, "bf16", "t4", 14, 4, 0, None),
+    (81, 37, 3584, "f16", "normal", 16, 4, 1, None),
+    (82, 20, 14336, "bf16", "normal", 7, 4, 0, None),
+    (83, 9, 8192, "f32", "t4", 14, 4, 0, (6, 8, 10, 16)),
+    (84, 5, 16384, "bf16", "normal", 12, 3, 1, None),
+    (85, 3, 7168, "f16", "t4", 15, 2, 0, None),
+]
+
+
+@pytest.mark.parametrize("case", ROTATE_ENCODE_CASES,
+                         ids=lambda c: f"s{c[0]}-{c[1]}x{c[2]}-{c[3]}-q{c[5]}")
+def test_rotate_encode_equals_rotate_then_encode(nq, case):
+    """nq_rotate_encode (rows rotated in LDS, then coded) gives nq_encode(nq_rotate(x))
+    bit for bit: codes, beta words and scales, including a zero row."""
+    torch = __import__("torch")
+    seed, rows, cols, dtype, dist, q, k, dec, mult = case
+    store, _ = workloads.random_rows(seed, rows, cols, dtype=dtype, dist=dist)
+    store = store.copy()
+    store[rows // 2] = 0
+    x = to_device(store, dtype)
+    base = None if mult is None else 1.0 / (2 * q)
+    a1 = nq.encode(nq.rotate(x), q=q, k=k, base=base, decoder=dec, mult=mult)
+    a2 = nq.encode(x, q=q, k=k, base=base, decoder=dec, mult=mult, rotate=True)
+    torch.cuda.synchronize()
+    assert torch.equal(a1.codes, a2.codes)
+    assert torch.equal(a1.beta, a2.beta)
+    assert torch.equal(a1.scales, a2.scales)
+    assert float(a2.scales[rows // 2]) == 0.0
+
+
+def test_rotate_encode_against_oracle(nq):
+    """The fused rotation and coding against the oracle's rotation followed by its encoder."""
+    torch = __import__("torch")
+    from oracle import rotation
+    store, x32 = workloads.random_rows(86, 12, 4096, dtype="bf16", dist="t4")
+    got = nq.encode(to_device(store, "bf16"), q=14, k=4, rotate=True)
+    torch.cuda.synchronize()
+    oc, ob, os_ = oracle_encode(rotation.rotate_rows(x32), 14, 4)
+    assert first_mismatch(u32(got.codes, oc.shape), oc) is None
+    assert first_mismatch(u32(got.beta, ob.shape), ob) is None
+    assert np.array_equal(got.scales.cpu().numpy().view(np.uint32), os_.view(np.uint32))
+
+
+@pytest.mark.parametrize("int8", [False, True])
+def test_encode_matmul_rotated(nq, int8):
+    """nq_encode_matmul with NQ_ROTATE_A equals it on the rotated activation, with W coded
+    from its rotated rows (A W^T = (A U)(W U)^T)."""
+    torch = __import__("torch")
+    store, _ = workloads.random_rows(87, 300, 3584, dtype="bf16", dist="t4")
+    wstore, _ = workloads.random_rows(88, 200, 3584, dtype="bf16", scale=0.02)
+    x = to_device(store, "bf16")
+    q = 15 if int8 else 14
+    wc = nq.encode(nq.rotate(to_device(wstore, "bf16")), q=q, k=4)
+    a1, c1 = nq.encode_matmul(nq.rotate(x), wc, q=q, k=4, int8=int8)
+    a2, c2 = nq.encode_matmul(x, wc, q=q, k=4, int8=int8, rotate=True)
+    torch.cuda.synchronize()
+    assert torch.equal(a1.codes, a2.codes) and torch.equal(a1.beta, a2.beta)
+    assert torch.equal(a1.scales, a2.scales)
+    assert torch.equal(c1, c2)
+
+
 # ---------------------------------------------------------------------------------------
 # Beta sets as integer multiples of base (beta_t = m_t base), as the App. F dynamic program
 # chooses them from the grid (1/2){1..50}/q = {1..50} / (2q).  Tiles m * X2 use bf16 while
