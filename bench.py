@@ -494,7 +494,36 @@ def main():
         rbytes = M * K * (in_bytes + 4)
         rot = {"ms": rms, "GBps": rbytes / (rms * 1e-3) / 1e9,
                "hbm_frac": rbytes / (rms * 1e-3) / 1e9 / HBM_PEAK_GBPS, "bytes": rbytes}
+
+        def timed(fn):
+            for i in range(args.warmup):
+                fn(i)
+            torch.cuda.synchronize()
+            ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)]
+                  for _ in range(args.steps)]
+            for i in range(args.steps):
+                ev[i][0].record()
+                fn(i)
+                ev[i][1].record()
+            torch.cuda.synchronize()
+            return float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+
+        # rotation and coding of A in two passes (nq_rotate, then nq_encode of its fp32
+        # rows), and in one (nq_rotate_encode: the rows rotated in LDS); then the whole step
+        # on rotated operands (W coded once from its rotated rows)
+        rot["rotate_then_encode_ms"] = timed(lambda i: (
+            nq.rotate(As[i % nbuf], out=Y), nq.encode(Y, q=q, k=k, out=(codes, beta, scales))))
         del Y
+        try:
+            rot["rotate_encode_ms"] = timed(lambda i: nq.encode(
+                As[i % nbuf], q=q, k=k, out=(codes, beta, scales), rotate=True))
+            wc_rot = nq.encode(nq.rotate(W), q=q, k=k)
+            rot["nq_encode_matmul_rotated_ms"] = timed(lambda i: nq.encode_matmul(
+                As[i % nbuf], wc_rot, q=q, k=k, out=C, coded_out=(codes, beta, scales),
+                workspace=ws, rotate=True))
+            del wc_rot
+        except nq.NQError:
+            pass                              # a width the in-LDS rotation does not hold
     except nq.NQError:
         pass                                  # K not 2^k or 28 * 2^k
 
