@@ -184,8 +184,11 @@ nq_status nq_matmul_stages(int32_t stages, const nq_params* pa, const uint32_t* 
  *        overlap x.
  * Supported: cols = 2^k or 28 * 2^k with 2^k >= 8 and cols <= 32768, else
  * NQ_ERR_UNSUPPORTED.  Arithmetic: fp32 fast Walsh-Hadamard transform (stages h = 1, 2, 4, ...
- * along each length-2^k segment), then for 28 * 2^k the H_28 sums in index order, then one
- * multiplication by fl32(1 / sqrt(n)).  rows == 0 is a no-op. */
+ * along each length-2^k segment); then for 28 * 2^k, with segments i = 2b + r,
+ * u_2b = X_2b + X_2b+1 and u_2b+1 = X_2b - X_2b+1 (H_2), and segment 2c + s of the output is
+ * the sum over b != c, in increasing b, of C[b][c] u_2b+s followed by + u_2c+1 (s = 0) or
+ * - u_2c (s = 1), C the conference matrix of the construction (H_28 = C kron H_2 + I_14 kron
+ * K_2); then one multiplication by fl32(1 / sqrt(n)).  rows == 0 is a no-op. */
 nq_status nq_rotate(const void* x, nq_dtype x_dtype, int64_t rows, int64_t cols, int64_t ld_x,
                     float* y, int64_t ld_y, void* hip_stream);
 

@@ -6,7 +6,9 @@
 // Arithmetic (the paper leaves it open; fixed here so that results are reproducible):
 //   1. the fast Walsh-Hadamard transform along j in fp32: for h = 1, 2, 4, ..., every pair
 //      (i, i + h) with i & h = 0 becomes (a + b, a - b);
-//   2. for m = 28: output a = sum over i = 0..27, in that order, of H_28[i, a] X[i, :];
+//   2. for m = 28, H_28 = C kron H_2 + I_14 kron K_2 applied through that structure (rows
+//      i = 2b + r): u_2b = X_2b + X_2b+1, u_2b+1 = X_2b - X_2b+1; output 2c + s = sum over
+//      b != c, in increasing b, of C[b][c] u_2b+s, then + u_2c+1 (s = 0) or - u_2c (s = 1);
 //   3. every entry times fl32(1 / sqrt(n)).
 // Within a stage the butterflies are independent, so any parallel order gives the same
 // numbers.
@@ -15,8 +17,8 @@
 // consecutive entries into registers and does the stages h = 1, 2, 4 there; the later stages
 // run four at a time: a thread takes 16 entries whose indices differ in four consecutive
 // bits, does those four stages in registers and writes them back (a barrier per four
-// stages).  The H_28 signs are compile-time constants, so each term of the mix is one add or
-// subtract.
+// stages).  The signs of the conference matrix behind H_28 are compile-time constants, so
+// each term of the mix is one add or subtract.
 #pragma once
 
 #include "nq_device.hpp"
@@ -24,30 +26,23 @@
 namespace nq {
 
 // Paley's second construction at q = 13 (q = 1 mod 4): chi the quadratic character mod 13,
-// C = [[0, 1^T], [1, Q]] with Q[i][j] = chi(j - i) (14 x 14, symmetric), and
-// H_28 = C kron [[1, 1], [1, -1]] + I_14 kron [[1, -1], [-1, -1]].  neg[a] has bit i set
-// where H_28[i][a] = -1.
-struct H28Table {
-  uint32_t neg[28];
+// the symmetric conference matrix C = [[0, 1^T], [1, Q]] with Q[i][j] = chi(j - i) (14 x 14,
+// zero diagonal), and H_28 = C kron [[1, 1], [1, -1]] + I_14 kron [[1, -1], [-1, -1]].
+// neg[c] has bit b set where C[b][c] = -1.
+struct C14Table {
+  uint32_t neg[14];
 };
-constexpr H28Table make_h28() {
-  H28Table s{};
+constexpr C14Table make_c14() {
+  C14Table t{};
   int chi[13] = {};
   for (int a = 1; a < 13; ++a) chi[a] = -1;
   for (int v = 1; v < 13; ++v) chi[(v * v) % 13] = 1;
-  for (int i = 0; i < 28; ++i)
-    for (int a = 0; a < 28; ++a) {
-      const int bi = i / 2, ri = i % 2, ba = a / 2, ra = a % 2;
-      const int c = (bi == 0 && ba == 0) ? 0
-                    : (bi == 0 || ba == 0) ? 1
-                    : chi[((ba - 1) - (bi - 1) + 13) % 13];
-      const int k2 = (ri == 1 && ra == 1) ? -1 : 1;
-      const int d2 = bi == ba ? ((ri == 0 && ra == 0) ? 1 : -1) : 0;
-      if (c * k2 + d2 < 0) s.neg[a] |= 1u << i;
-    }
-  return s;
+  for (int b = 1; b < 14; ++b)
+    for (int c = 1; c < 14; ++c)
+      if (b != c && chi[((c - 1) - (b - 1) + 13) % 13] < 0) t.neg[c] |= 1u << b;
+  return t;
 }
-constexpr H28Table kH28 = make_h28();
+constexpr C14Table kC14 = make_c14();
 
 template <typename T>
 __device__ __forceinline__ void load8(const T* __restrict__ p, float (&v)[8]);
@@ -157,20 +152,33 @@ __device__ __forceinline__ void rotate_rows_lds(const T* __restrict__ x, int64_t
   }
   __syncthreads();
   if (m == 28) {
-    // mix the 28 segments of each row column by column, sums in index order
+    // the H_28 factor through its construction, for each column of the 28 segments: H_2 on
+    // each segment pair (u_2b = X_2b + X_2b+1, u_2b+1 = X_2b - X_2b+1), then output 2c + s
+    // is the sum over b != c, in increasing b, of C[b][c] u_2b+s, plus u_2c+1 (s = 0) or
+    // minus u_2c (s = 1): 13 additions per output
     for (int q = tid; q < rr * p; q += 256) {
       const int r = q / p, b = q - r * p;
       const int col = r * n + b;
-      float xi[28];
+      float u[28];
 #pragma unroll
-      for (int i = 0; i < 28; ++i) xi[i] = buf[lds_pos(col + i * p)];
+      for (int i = 0; i < 14; ++i) {
+        const float x0 = buf[lds_pos(col + 2 * i * p)], x1 = buf[lds_pos(col + (2 * i + 1) * p)];
+        u[2 * i] = x0 + x1;
+        u[2 * i + 1] = x0 - x1;
+      }
 #pragma unroll
-      for (int a = 0; a < 28; ++a) {
-        float acc = ((kH28.neg[a] & 1u) != 0) ? -xi[0] : xi[0];
+      for (int c = 0; c < 14; ++c) {
 #pragma unroll
-        for (int i = 1; i < 28; ++i)
-          acc = (((kH28.neg[a] >> i) & 1u) != 0) ? acc - xi[i] : acc + xi[i];
-        buf[lds_pos(col + a * p)] = acc;
+        for (int s = 0; s < 2; ++s) {
+          const int b0 = c == 0 ? 1 : 0;
+          float acc = ((kC14.neg[c] >> b0) & 1u) != 0 ? -u[2 * b0 + s] : u[2 * b0 + s];
+#pragma unroll
+          for (int bb = b0 + 1; bb < 14; ++bb) {
+            if (bb == c) continue;
+            acc = ((kC14.neg[c] >> bb) & 1u) != 0 ? acc - u[2 * bb + s] : acc + u[2 * bb + s];
+          }
+          buf[lds_pos(col + (2 * c + s) * p)] = s == 0 ? acc + u[2 * c + 1] : acc - u[2 * c];
+        }
       }
     }
     __syncthreads();

@@ -70,3 +70,29 @@ def test_unsupported_sizes():
     assert rotation.split(24) is None
     assert rotation.split(11008) is None
     assert rotation.split(28672) == (28, 1024)
+
+
+def test_conference14():
+    """C of Paley's second construction: symmetric (q = 13 = 1 mod 4), zero diagonal,
+    +-1 elsewhere and C C^T = 13 I, which makes C kron H_2 + I kron K_2 a Hadamard matrix."""
+    C = rotation.conference14()
+    assert np.array_equal(C, C.T)
+    assert np.all(np.diag(C) == 0)
+    assert set(np.unique(C[~np.eye(14, dtype=bool)])) == {-1, 1}
+    assert np.array_equal(C @ C.T, 13 * np.eye(14, dtype=np.int64))
+
+
+@pytest.mark.parametrize("p", [8, 64])
+def test_structured_mix_is_exact_on_integers(p):
+    """Small integer rows keep every fp32 sum exact, so the fast transform (with the H_28
+    mix through its Kronecker structure) must equal the integer product x (H_28 kron H_p)
+    before the final scaling: any wrong sign or index in the mix shows."""
+    n = 28 * p
+    rng = np.random.default_rng(p)
+    x = rng.integers(-8, 9, size=(5, n)).astype(np.float32)
+    y = rotation.rotate_rows(x)
+    H = np.kron(rotation.paley28(), scipy.linalg.hadamard(p)).astype(np.int64)
+    S = x.astype(np.int64) @ H
+    assert np.all(np.abs(S) < 2 ** 24)
+    want = (S.astype(np.float32) * rotation.scale32(n)).astype(np.float32)
+    assert np.array_equal(y, want)
