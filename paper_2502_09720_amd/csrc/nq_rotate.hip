@@ -1,6 +1,8 @@
-// Online Hadamard rotation of rows, nq_rotate (Sec. 5 of the NestQuant paper): one workgroup
-// of 256 threads holds R rows (R n <= 2048 elements, or one row of up to 32768) in LDS as
-// fp32, rotates them (nq_rotate.hpp) and writes y = (rotated entries) * fl32(1 / sqrt(n)).
+// Online Hadamard rotation of rows, nq_rotate (Sec. 5 of the NestQuant paper): a workgroup
+// holds R rows in LDS as fp32 (R n <= 2048 elements, or one row, with 256 threads; rows of
+// more than 12288 entries with 1024 threads, whose extra waves keep more of the row's loads
+// and stores in flight: at 56 to 128 KiB of LDS per row only one or two rows fit a CU),
+// rotates them (nq_rotate.hpp) and writes y = (rotated entries) * fl32(1 / sqrt(n)).
 #include <algorithm>
 #include <cmath>
 
@@ -10,18 +12,21 @@
 
 namespace nq {
 
-template <typename T>
-__global__ __launch_bounds__(256) void rotate_kernel(const T* __restrict__ x, int64_t rows,
-                                                     int n, int64_t ld_x, int p, int lp,
-                                                     int rpw, float s, float* __restrict__ y,
-                                                     int64_t ld_y) {
+// Rows at least this long get a workgroup of 1024 threads.
+constexpr int kRotateWideCols = 12288;
+
+template <typename T, int NT>
+__global__ __launch_bounds__(NT) void rotate_kernel(const T* __restrict__ x, int64_t rows,
+                                                    int n, int64_t ld_x, int p, int lp,
+                                                    int rpw, float s, float* __restrict__ y,
+                                                    int64_t ld_y) {
   extern __shared__ float buf[];
   const int tid = threadIdx.x;
   const int64_t row0 = (int64_t)blockIdx.x * rpw;
   const int rr = (int)std::min<int64_t>(rpw, rows - row0);   // rows in this workgroup
   const int total = rr * n;                                  // elements held
-  rotate_rows_lds<T>(x + row0 * ld_x, ld_x, rr, n, p, lp, buf);
-  for (int g = tid; g < total / 8; g += 256) {
+  rotate_rows_lds<T, NT>(x + row0 * ld_x, ld_x, rr, n, p, lp, buf);
+  for (int g = tid; g < total / 8; g += NT) {
     const int e = 8 * g;
     const int r = e / n, c = e - r * n;
     const float* d = buf + lds_pos(e);
@@ -56,15 +61,21 @@ static hipError_t launch_t(const void* x, int64_t rows, int n, int64_t ld_x, flo
   const size_t lds = (size_t)rpw * n * sizeof(float);
   const float s = (float)(1.0 / std::sqrt((double)n));
   const int64_t grid = (rows + rpw - 1) / rpw;
-  hipLaunchKernelGGL((rotate_kernel<T>), dim3((unsigned)grid), dim3(256), lds, st, (const T*)x,
-                     rows, n, ld_x, p, lp, rpw, s, y, ld_y);
+  if (n >= kRotateWideCols) {
+    hipLaunchKernelGGL((rotate_kernel<T, 1024>), dim3((unsigned)grid), dim3(1024), lds, st,
+                       (const T*)x, rows, n, ld_x, p, lp, rpw, s, y, ld_y);
+  } else {
+    hipLaunchKernelGGL((rotate_kernel<T, 256>), dim3((unsigned)grid), dim3(256), lds, st,
+                       (const T*)x, rows, n, ld_x, p, lp, rpw, s, y, ld_y);
+  }
   return hipGetLastError();
 }
 
 hipError_t rotate_set_attributes() {
-  const void* k[3] = {(const void*)rotate_kernel<float>, (const void*)rotate_kernel<_Float16>,
-                      (const void*)rotate_kernel<uint16_t>};
-  for (int i = 0; i < 3; ++i) {
+  const void* k[6] = {(const void*)rotate_kernel<float, 256>, (const void*)rotate_kernel<_Float16, 256>,
+                      (const void*)rotate_kernel<uint16_t, 256>, (const void*)rotate_kernel<float, 1024>,
+                      (const void*)rotate_kernel<_Float16, 1024>, (const void*)rotate_kernel<uint16_t, 1024>};
+  for (int i = 0; i < 6; ++i) {
     const hipError_t e = hipFuncSetAttribute(k[i], hipFuncAttributeMaxDynamicSharedMemorySize,
                                              kRotateMaxCols * (int)sizeof(float));
     if (e != hipSuccess) return e;

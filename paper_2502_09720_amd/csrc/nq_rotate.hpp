@@ -13,7 +13,7 @@
 // Within a stage the butterflies are independent, so any parallel order gives the same
 // numbers.
 //
-// A workgroup of 256 threads holds its rows in LDS as fp32.  Each thread first takes 8
+// A workgroup of NT threads holds its rows in LDS as fp32.  Each thread first takes 8
 // consecutive entries into registers and does the stages h = 1, 2, 4 there; the later stages
 // run four at a time: a thread takes 16 entries whose indices differ in four consecutive
 // bits, does those four stages in registers and writes them back (a barrier per four
@@ -83,11 +83,11 @@ __device__ __forceinline__ int lds_pos(int e) { return e ^ (((e >> 7) & 7) << 3)
 
 // Stages h = 2^b0 .. 2^(b0 + NB - 1) of every length-2^lp segment of buf (total entries):
 // each thread takes groups of 2^NB entries whose indices differ only in bits b0 .. b0+NB-1.
-template <int NB>
+template <int NB, int NT>
 __device__ __forceinline__ void fwht_pass(float* buf, int total, int lp, int b0) {
   constexpr int G = 1 << NB;
   const int per_seg = 1 << (lp - NB);
-  for (int g = threadIdx.x; g < (total >> NB); g += 256) {
+  for (int g = threadIdx.x; g < (total >> NB); g += NT) {
     const int seg = g >> (lp - NB), lg = g & (per_seg - 1);
     const int base = (seg << lp) | ((lg >> b0) << (b0 + NB)) | (lg & ((1 << b0) - 1));
     float v[G];
@@ -111,16 +111,16 @@ __device__ __forceinline__ void fwht_pass(float* buf, int total, int lp, int b0)
 
 // Steps 1 and 2 for the rr consecutive rows at x (n entries each, row stride ld_x), held in
 // buf: entry e (row e / n) ends at buf[lds_pos(e)], and its rotated value is that times
-// fl32(1 / sqrt(n)).  p = n / m = 2^lp >= 8.  Every thread of the workgroup (256) must call
+// fl32(1 / sqrt(n)).  p = n / m = 2^lp >= 8.  Every thread of the workgroup (NT) must call
 // it; it ends with a barrier.
-template <typename T>
+template <typename T, int NT = 256>
 __device__ __forceinline__ void rotate_rows_lds(const T* __restrict__ x, int64_t ld_x, int rr,
                                                 int n, int p, int lp, float* buf) {
   const int tid = threadIdx.x;
   const int total = rr * n;   // elements held
   const int m = n / p;
   // load 8 entries at a time, stages h = 1, 2, 4 in registers (p >= 8)
-  for (int g = tid; g < total / 8; g += 256) {
+  for (int g = tid; g < total / 8; g += NT) {
     const int e = 8 * g;
     const int r = e / n, c = e - r * n;
     float v[8];
@@ -144,10 +144,10 @@ __device__ __forceinline__ void rotate_rows_lds(const T* __restrict__ x, int64_t
   for (int b0 = 3; b0 < lp; b0 += 4) {
     __syncthreads();
     switch (lp - b0 < 4 ? lp - b0 : 4) {
-      case 1: fwht_pass<1>(buf, total, lp, b0); break;
-      case 2: fwht_pass<2>(buf, total, lp, b0); break;
-      case 3: fwht_pass<3>(buf, total, lp, b0); break;
-      default: fwht_pass<4>(buf, total, lp, b0); break;
+      case 1: fwht_pass<1, NT>(buf, total, lp, b0); break;
+      case 2: fwht_pass<2, NT>(buf, total, lp, b0); break;
+      case 3: fwht_pass<3, NT>(buf, total, lp, b0); break;
+      default: fwht_pass<4, NT>(buf, total, lp, b0); break;
     }
   }
   __syncthreads();
@@ -156,7 +156,7 @@ __device__ __forceinline__ void rotate_rows_lds(const T* __restrict__ x, int64_t
     // each segment pair (u_2b = X_2b + X_2b+1, u_2b+1 = X_2b - X_2b+1), then output 2c + s
     // is the sum over b != c, in increasing b, of C[b][c] u_2b+s, plus u_2c+1 (s = 0) or
     // minus u_2c (s = 1): 13 additions per output
-    for (int q = tid; q < rr * p; q += 256) {
+    for (int q = tid; q < rr * p; q += NT) {
       const int r = q / p, b = q - r * p;
       const int col = r * n + b;
       float u[28];
