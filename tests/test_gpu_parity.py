@@ -616,12 +616,12 @@ def test_rotate_encode_against_oracle(nq):
     assert np.array_equal(got.scales.cpu().numpy().view(np.uint32), os_.view(np.uint32))
 
 
-@pytest.mark.parametrize("int8", [False, True])
-def test_encode_matmul_rotated(nq, int8):
+@pytest.mark.parametrize("M,int8", [(300, False), (300, True), (16, False), (65, True)])
+def test_encode_matmul_rotated(nq, M, int8):
     """nq_encode_matmul with NQ_ROTATE_A equals it on the rotated activation, with W coded
-    from its rotated rows (A W^T = (A U)(W U)^T)."""
+    from its rotated rows (A W^T = (A U)(W U)^T), on both product paths."""
     torch = __import__("torch")
-    store, _ = workloads.random_rows(87, 300, 3584, dtype="bf16", dist="t4")
+    store, _ = workloads.random_rows(87, M, 3584, dtype="bf16", dist="t4")
     wstore, _ = workloads.random_rows(88, 200, 3584, dtype="bf16", scale=0.02)
     x = to_device(store, "bf16")
     q = 15 if int8 else 14
