@@ -148,8 +148,10 @@ def encode(x, q=14, k=4, base=None, stream=None, out=None, decoder=DECODER_FULL,
     ``decoder`` is the decoder the code is defined with (DECODER_FULL or DECODER_M);
     ``strategy`` picks the beta of each block (FIRST_BETA or OPT_BETA); ``mult`` gives the
     betas as integer multiples of base (k increasing integers in [1, 64]; None: 1..k).
-    ``rotate``: nq_rotate_encode, the rows Hadamard-rotated (as ``rotate``) while they are
-    coded (First-beta; cols in 3584, 4096, 7168, 8192, 14336, 16384)."""
+    ``rotate``: the rows are Hadamard-rotated (as ``rotate``) before they are coded: in one
+    pass (nq_rotate_encode) where the library supports it (First-beta; cols in 3584, 4096,
+    7168, 8192, 14336, 16384), else as nq_rotate into a temporary fp32 matrix followed by
+    nq_encode (same results)."""
     import torch
     if x.dim() != 2 or x.stride(1) != 1 or not x.is_cuda:
         raise ValueError("x must be a 2-D cuda tensor with unit column stride")
@@ -165,10 +167,16 @@ def encode(x, q=14, k=4, base=None, stream=None, out=None, decoder=DECODER_FULL,
     else:
         codes, beta, scales = out
     p = _params(q, k, base, decoder, strategy, mult)
-    fn = lib.nq_rotate_encode if rotate else lib.nq_encode
-    _check(fn(ctypes.byref(p), ctypes.c_void_p(x.data_ptr()), _dtype_code(x.dtype), rows, cols,
-              x.stride(0), ctypes.c_void_p(codes.data_ptr()), ctypes.c_void_p(beta.data_ptr()),
-              ctypes.c_void_p(scales.data_ptr()), _stream(stream)))
+
+    def call(fn, src):
+        return fn(ctypes.byref(p), ctypes.c_void_p(src.data_ptr()), _dtype_code(src.dtype), rows,
+                  cols, src.stride(0), ctypes.c_void_p(codes.data_ptr()),
+                  ctypes.c_void_p(beta.data_ptr()), ctypes.c_void_p(scales.data_ptr()),
+                  _stream(stream))
+    st = call(lib.nq_rotate_encode if rotate else lib.nq_encode, x)
+    if rotate and st == NQ_ERR_UNSUPPORTED:
+        st = call(lib.nq_encode, _rotated(x, stream))                     # two passes
+    _check(st)
     return Coded(codes, beta, scales, rows, cols, int(q), int(k), p.base, int(decoder),
                  None if mult is None else tuple(int(v) for v in mult))
 
@@ -239,8 +247,9 @@ def encode_matmul(x, w, q=14, k=4, base=None, decoder=DECODER_FULL, strategy=FIR
     """nq_encode_matmul: codes the activation x (2-D cuda tensor, as ``encode``) and returns
     (its Coded operand, C = A_hat W_hat^T) from one call, the encoder writing A's decoded
     tiles straight into the product's workspace.  The same results as ``encode`` then
-    ``matmul``.  ``rotate``: x's rows are Hadamard-rotated while coded (NQ_ROTATE_A; w must
-    hold the codes of rotated weight rows)."""
+    ``matmul``.  ``rotate``: x's rows are Hadamard-rotated before they are coded (w must hold
+    the codes of rotated weight rows): NQ_ROTATE_A where the library supports it (as for
+    ``encode``), else nq_rotate into a temporary fp32 matrix first (same results)."""
     import torch
     if x.dim() != 2 or x.stride(1) != 1 or not x.is_cuda:
         raise ValueError("x must be a 2-D cuda tensor with unit column stride")
@@ -263,15 +272,21 @@ def encode_matmul(x, w, q=14, k=4, base=None, decoder=DECODER_FULL, strategy=FIR
         workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
     pa = _params(q, k, base, decoder, strategy, mult)
     pw = _params(w.q, w.k, w.base, w.decoder, mult=w.mult)
-    flags = (CONTRACT_INT8 if int8 else 0) | (ROTATE_A if rotate else 0)
-    _check(lib.nq_encode_matmul(
-        flags, ctypes.byref(pa), ctypes.c_void_p(x.data_ptr()),
-        _dtype_code(x.dtype), M, K, x.stride(0), ctypes.c_void_p(codes.data_ptr()),
-        ctypes.c_void_p(beta.data_ptr()), ctypes.c_void_p(scales.data_ptr()), ctypes.byref(pw),
-        ctypes.c_void_p(w.codes.data_ptr()), ctypes.c_void_p(w.beta.data_ptr()),
-        ctypes.c_void_p(w.scales.data_ptr()), w.rows, ctypes.c_void_p(out.data_ptr()),
-        out.stride(0), ctypes.c_void_p(workspace.data_ptr() if need > 0 else 0), need,
-        _stream(stream)))
+
+    def call(flags, src):
+        return lib.nq_encode_matmul(
+            flags, ctypes.byref(pa), ctypes.c_void_p(src.data_ptr()), _dtype_code(src.dtype), M,
+            K, src.stride(0), ctypes.c_void_p(codes.data_ptr()),
+            ctypes.c_void_p(beta.data_ptr()), ctypes.c_void_p(scales.data_ptr()),
+            ctypes.byref(pw), ctypes.c_void_p(w.codes.data_ptr()),
+            ctypes.c_void_p(w.beta.data_ptr()), ctypes.c_void_p(w.scales.data_ptr()), w.rows,
+            ctypes.c_void_p(out.data_ptr()), out.stride(0),
+            ctypes.c_void_p(workspace.data_ptr() if need > 0 else 0), need, _stream(stream))
+    flags = CONTRACT_INT8 if int8 else 0
+    st = call(flags | (ROTATE_A if rotate else 0), x)
+    if rotate and st == NQ_ERR_UNSUPPORTED:
+        st = call(flags, _rotated(x, stream))                                # two passes
+    _check(st)
     a = Coded(codes, beta, scales, M, K, int(q), int(k), pa.base, int(decoder),
               None if mult is None else tuple(int(v) for v in mult))
     return a, out
@@ -290,6 +305,11 @@ def rotate(x, out=None, stream=None):
                                x.stride(0), ctypes.c_void_p(out.data_ptr()), out.stride(0),
                                _stream(stream)))
     return out
+
+
+def _rotated(x, stream):
+    """nq_rotate of x into a new fp32 matrix (the two-pass form of the rotating calls)."""
+    return rotate(x, stream=stream)
 
 
 def matmul_workspace_size(M, N, K):

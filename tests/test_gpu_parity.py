@@ -603,6 +603,29 @@ def test_rotate_encode_equals_rotate_then_encode(nq, case):
     assert float(a2.scales[rows // 2]) == 0.0
 
 
+@pytest.mark.parametrize("cols,strategy", [(2048, "first"), (4096, "opt"), (28672, "first")])
+def test_rotate_option_falls_back_to_two_passes(nq, cols, strategy):
+    """encode(rotate=True) and encode_matmul(rotate=True) where the rotation cannot run in
+    the encoder (row widths outside 257..2048 blocks, Opt-beta): nq_rotate, then the plain
+    call, with the same results as doing both by hand."""
+    torch = __import__("torch")
+    from paper_2502_09720_amd import OPT_BETA, FIRST_BETA
+    strat = OPT_BETA if strategy == "opt" else FIRST_BETA
+    store, _ = workloads.random_rows(89, 7, cols, dtype="bf16", dist="t4")
+    x = to_device(store, "bf16")
+    y = nq.rotate(x)
+    a1 = nq.encode(y, q=14, k=4, strategy=strat)
+    a2 = nq.encode(x, q=14, k=4, strategy=strat, rotate=True)
+    wstore, _ = workloads.random_rows(90, 70, cols, dtype="bf16")
+    wc = nq.encode(nq.rotate(to_device(wstore, "bf16")), q=14, k=4)
+    b1, c1 = nq.encode_matmul(y, wc, q=14, k=4, strategy=strat)
+    b2, c2 = nq.encode_matmul(x, wc, q=14, k=4, strategy=strat, rotate=True)
+    torch.cuda.synchronize()
+    assert torch.equal(a1.codes, a2.codes) and torch.equal(a1.beta, a2.beta)
+    assert torch.equal(a1.scales, a2.scales)
+    assert torch.equal(b1.codes, b2.codes) and torch.equal(c1, c2)
+
+
 def test_rotate_encode_against_oracle(nq):
     """The fused rotation and coding against the oracle's rotation followed by its encoder."""
     torch = __import__("torch")
