@@ -227,6 +227,8 @@ def matmul(a, w, stream=None, out=None, workspace=None, stages=STAGE_DECODE | ST
         if not whole:
             raise ValueError("a staged matmul needs a workspace of matmul_workspace_size bytes")
         workspace = torch.empty(need, dtype=torch.uint8, device=a.codes.device)
+        if stream is not None:
+            workspace.record_stream(stream)       # freed on return, in use on `stream`
     ws_ptr = workspace.data_ptr() if need > 0 else 0
     args = (ctypes.byref(pa), ctypes.c_void_p(a.codes.data_ptr()),
             ctypes.c_void_p(a.beta.data_ptr()), ctypes.c_void_p(a.scales.data_ptr()), a.rows,
@@ -270,6 +272,8 @@ def encode_matmul(x, w, q=14, k=4, base=None, decoder=DECODER_FULL, strategy=FIR
         raise ValueError("invalid matmul shape")
     if need > 0 and (workspace is None or workspace.numel() * workspace.element_size() < need):
         workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+        if stream is not None:
+            workspace.record_stream(stream)       # freed on return, in use on `stream`
     pa = _params(q, k, base, decoder, strategy, mult)
     pw = _params(w.q, w.k, w.base, w.decoder, mult=w.mult)
 
@@ -308,8 +312,13 @@ def rotate(x, out=None, stream=None):
 
 
 def _rotated(x, stream):
-    """nq_rotate of x into a new fp32 matrix (the two-pass form of the rotating calls)."""
-    return rotate(x, stream=stream)
+    """nq_rotate of x into a new fp32 matrix (the two-pass form of the rotating calls).  The
+    temporary is freed when the caller returns, so it is marked as in use on `stream` until
+    the work queued there is done."""
+    y = rotate(x, stream=stream)
+    if stream is not None:
+        y.record_stream(stream)
+    return y
 
 
 def matmul_workspace_size(M, N, K):

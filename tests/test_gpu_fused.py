@@ -151,3 +151,26 @@ def test_encode_matmul_graph_replays(nq, K):
         assert torch.equal(got[0], c_ref)
         assert torch.equal(got[1], a_ref.codes) and torch.equal(got[2], a_ref.beta)
         assert torch.equal(got[3], a_ref.scales)
+
+
+def test_calls_on_a_side_stream(nq):
+    """matmul and encode_matmul queued on a stream other than the current one, with the
+    workspace taken from torch's allocator inside the call (and rotate=True's temporary):
+    the same results as on the current stream."""
+    import torch
+    store, _ = workloads.random_rows(620, 300, 2048, dtype="bf16", dist="t4")
+    wstore, _ = workloads.random_rows(621, 130, 2048, dtype="bf16", scale=0.02)
+    x = _dev(store, "bf16")
+    w = nq.encode(_dev(wstore, "bf16"), 14, 4)
+    a0, c0 = nq.encode_matmul(x, w, 14, 4)
+    m0 = nq.matmul(a0, w)
+    r0 = nq.encode(x, 14, 4, rotate=True)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    a1, c1 = nq.encode_matmul(x, w, 14, 4, stream=side)
+    m1 = nq.matmul(a1, w, stream=side)
+    r1 = nq.encode(x, 14, 4, rotate=True, stream=side)
+    side.synchronize()
+    assert torch.equal(c0, c1) and torch.equal(m0, m1)
+    assert torch.equal(a0.codes, a1.codes) and torch.equal(r0.codes, r1.codes)
