@@ -4,6 +4,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <atomic>
 #include <mutex>
 
 #include "nestquant.h"
@@ -25,6 +26,36 @@ nq_status ok() {
   g_last_error[0] = '\0';
   return NQ_OK;
 }
+
+// Kernel attributes (the dynamic LDS limit) belong to each device: set them once on every
+// device that a call's stream runs on, before its first launch there.
+class PerDevice {
+ public:
+  explicit PerDevice(hipError_t (*fn)()) : fn_(fn) {}
+  hipError_t ensure(hipStream_t st) {
+    hipDevice_t dev = 0;
+    hipError_t e = hipStreamGetDevice(st, &dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kDevices) return hipErrorInvalidDevice;
+    if (done_[dev].load(std::memory_order_acquire)) return hipSuccess;
+    std::lock_guard<std::mutex> g(mu_);
+    if (done_[dev].load(std::memory_order_relaxed)) return hipSuccess;
+    int cur = 0;
+    e = hipGetDevice(&cur);
+    if (e != hipSuccess) return e;
+    if (cur != dev && (e = hipSetDevice(dev)) != hipSuccess) return e;
+    const hipError_t r = fn_();
+    if (cur != dev && (e = hipSetDevice(cur)) != hipSuccess) return e;
+    if (r == hipSuccess) done_[dev].store(true, std::memory_order_release);
+    return r;
+  }
+
+ private:
+  static constexpr int kDevices = 64;
+  hipError_t (*fn_)();
+  std::mutex mu_;
+  std::atomic<bool> done_[kDevices] = {};
+};
 
 constexpr int64_t kMaxCols = 65536;
 constexpr int64_t kMaxRows = (int64_t)1 << 31;
@@ -259,9 +290,8 @@ nq_status nq_rotate(const void* x, nq_dtype x_dtype, int64_t rows, int64_t cols,
   const int64_t ybytes = ((rows - 1) * ld_y + cols) * 4;
   if (xb < yb + ybytes && yb < xb + xbytes)
     return fail(NQ_ERR_INVALID_ARG, "%s: x and y overlap", who);
-  static std::once_flag attr_once;
-  static hipError_t attr_err = hipSuccess;
-  std::call_once(attr_once, [] { attr_err = nq::rotate_set_attributes(); });
+  static PerDevice attrs(nq::rotate_set_attributes);
+  const hipError_t attr_err = attrs.ensure((hipStream_t)hip_stream);
   if (attr_err != hipSuccess) return hip_status(attr_err, who);
   return hip_status(nq::launch_rotate(x, (int)x_dtype, rows, (int)cols, ld_x, y, ld_y,
                                       (hipStream_t)hip_stream),
@@ -357,9 +387,8 @@ static hipError_t launch_product(int stages, int et, const nq_params* pa, const 
   const float scale = (float)(pa->base * pw->base * 0.25);
   if (A.rows <= nq::kFusedMaxM)
     return nq::launch_matmul_skinny(stages, et, A, W, K, c, ldc, scale, workspace, st);
-  static std::once_flag attr_once;
-  static hipError_t attr_err = hipSuccess;
-  std::call_once(attr_once, [] { attr_err = nq::gemm_set_attributes(); });
+  static PerDevice attrs(nq::gemm_set_attributes);
+  const hipError_t attr_err = attrs.ensure(st);
   if (attr_err != hipSuccess) return attr_err;
   return nq::launch_matmul_decode_once(stages, et, A, W, K, c, ldc, scale, workspace, st);
 }

@@ -643,9 +643,9 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
   // block of slot sl of wave w, as fp32
   auto slot_block = [&](int w, int sl, float (&v)[8]) {
     if constexpr (ROT) {
-      const float* d = rbuf + lds_pos(8 * SM::j(sl >> 6, sl & 63, w));
+      const int pe = lds_pos(8 * SM::j(sl >> 6, sl & 63, w));
 #pragma unroll
-      for (int l = 0; l < 8; ++l) v[l] = d[l] * a.rot_s;
+      for (int l = 0; l < 8; ++l) v[l] = rbuf[pe ^ l] * a.rot_s;
     } else {
       unpack_raw<T>(rawl[w][sl], v);
     }

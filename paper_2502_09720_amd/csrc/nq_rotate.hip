@@ -26,15 +26,21 @@ __global__ __launch_bounds__(NT) void rotate_kernel(const T* __restrict__ x, int
   const int rr = (int)std::min<int64_t>(rpw, rows - row0);   // rows in this workgroup
   const int total = rr * n;                                  // elements held
   rotate_rows_lds<T, NT>(x + row0 * ld_x, ld_x, rr, n, p, lp, buf);
-  for (int g = tid; g < total / 8; g += NT) {
-    const int e = 8 * g;
-    const int r = e / n, c = e - r * n;
-    const float* d = buf + lds_pos(e);
-    f32x4 lo = {d[0] * s, d[1] * s, d[2] * s, d[3] * s};
-    f32x4 hi = {d[4] * s, d[5] * s, d[6] * s, d[7] * s};
+  auto out = [&](int e, int r, int c) {
+    const int pe = lds_pos(e);
+    f32x4 lo = {buf[pe] * s, buf[pe ^ 1] * s, buf[pe ^ 2] * s, buf[pe ^ 3] * s};
+    f32x4 hi = {buf[pe ^ 4] * s, buf[pe ^ 5] * s, buf[pe ^ 6] * s, buf[pe ^ 7] * s};
     f32x4* o = reinterpret_cast<f32x4*>(y + (row0 + r) * ld_y + c);
     __builtin_nontemporal_store(lo, o);
     __builtin_nontemporal_store(hi, o + 1);
+  };
+  if (rr == 1) {
+    for (int e = 8 * tid; e < n; e += 8 * NT) out(e, 0, e);
+  } else {
+    for (int e = 8 * tid; e < total; e += 8 * NT) {
+      const int r = e / n;
+      out(e, r, e - r * n);
+    }
   }
 }
 

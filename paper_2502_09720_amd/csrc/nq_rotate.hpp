@@ -74,25 +74,35 @@ __device__ __forceinline__ void load8<_Float16>(const _Float16* __restrict__ p, 
   }
 }
 
-// LDS position of entry e: bits 3..5 of e XOR bits 7..9.  The first four-stage pass (stride
-// 8 entries) has the 64 lanes of a wave on 8 consecutive entries times 8 groups 128 entries
-// apart, which would be 8 banks; the swizzle spreads them over all 64.  It permutes entries
-// only within aligned runs of 64, keeps runs of 8 contiguous (the 8-entry loads and stores
-// stay vector accesses) and leaves the other passes conflict-free.
-__device__ __forceinline__ int lds_pos(int e) { return e ^ (((e >> 7) & 7) << 3); }
+// LDS position of entry e: bits 3..5 of e XOR bits 7..9, and bits 0..2 XOR (bit 5 ^ bit 8,
+// bit 6, bit 7).  It permutes entries only within aligned runs of 64, and an aligned run of 8
+// within itself (lds_pos(e + l) = lds_pos(e) ^ l for e a multiple of 8, l < 8).  Each access
+// pattern below then puts the 64 lanes of a wave on 64 distinct banks, and each half-wave on
+// 32 distinct banks modulo 32: a lane per 8-entry block, every lane on the same entry of its
+// block (bits 3..8 from the lane; unswizzled, 8 lanes per bank); the first four-stage pass
+// (bits 0..2 and 7..9 from the lane); the later passes and the H_28 mix (bits 0..5 from the
+// lane).
+__device__ __forceinline__ int lds_pos(int e) {
+  return e ^ (((e >> 7) & 7) << 3) ^ (((e >> 5) ^ (e >> 8)) & 1) ^ (((e >> 6) & 3) << 1);
+}
 
-// Stages h = 2^b0 .. 2^(b0 + NB - 1) of every length-2^lp segment of buf (total entries):
-// each thread takes groups of 2^NB entries whose indices differ only in bits b0 .. b0+NB-1.
-template <int NB, int NT>
-__device__ __forceinline__ void fwht_pass(float* buf, int total, int lp, int b0) {
+// lds_pos is linear over XOR: lds_pos(a ^ b) = lds_pos(a) ^ lds_pos(b).  So where an index is
+// a base plus bits the base does not use, its position is the base's position XOR a
+// constant, one instruction per access.
+
+// Stages h = 2^B0 .. 2^(B0 + NB - 1) of every length-2^lp segment of buf (total entries):
+// each thread takes groups of 2^NB entries whose indices differ only in bits B0 .. B0+NB-1.
+template <int NB, int B0, int NT>
+__device__ __forceinline__ void fwht_pass(float* buf, int total, int lp) {
   constexpr int G = 1 << NB;
   const int per_seg = 1 << (lp - NB);
   for (int g = threadIdx.x; g < (total >> NB); g += NT) {
     const int seg = g >> (lp - NB), lg = g & (per_seg - 1);
-    const int base = (seg << lp) | ((lg >> b0) << (b0 + NB)) | (lg & ((1 << b0) - 1));
+    const int base = (seg << lp) | ((lg >> B0) << (B0 + NB)) | (lg & ((1 << B0) - 1));
+    const int pb = lds_pos(base);
     float v[G];
 #pragma unroll
-    for (int r = 0; r < G; ++r) v[r] = buf[lds_pos(base + (r << b0))];
+    for (int r = 0; r < G; ++r) v[r] = buf[pb ^ lds_pos(r << B0)];
 #pragma unroll
     for (int h = 1; h < G; h <<= 1) {
 #pragma unroll
@@ -105,7 +115,50 @@ __device__ __forceinline__ void fwht_pass(float* buf, int total, int lp, int b0)
       }
     }
 #pragma unroll
-    for (int r = 0; r < G; ++r) buf[lds_pos(base + (r << b0))] = v[r];
+    for (int r = 0; r < G; ++r) buf[pb ^ lds_pos(r << B0)] = v[r];
+  }
+}
+
+// The pass over bits B0 .. min(B0 + 3, lp - 1), after a barrier, if lp > B0.
+template <int B0, int NT>
+__device__ __forceinline__ void fwht_pass_at(float* buf, int total, int lp) {
+  if (lp <= B0) return;
+  __syncthreads();
+  switch (lp - B0 < 4 ? lp - B0 : 4) {
+    case 1: fwht_pass<1, B0, NT>(buf, total, lp); break;
+    case 2: fwht_pass<2, B0, NT>(buf, total, lp); break;
+    case 3: fwht_pass<3, B0, NT>(buf, total, lp); break;
+    default: fwht_pass<4, B0, NT>(buf, total, lp); break;
+  }
+}
+
+// The H_28 factor for column b (< p) of row r of buf, through its construction: H_2 on each
+// segment pair (u_2b = X_2b + X_2b+1, u_2b+1 = X_2b - X_2b+1), then output 2c + s is the sum
+// over b' != c, in increasing b', of C[b'][c] u_2b'+s, plus u_2c+1 (s = 0) or minus u_2c
+// (s = 1): 13 additions per output.  Entry k of the column is r n + k p + b = (28 r + k) p | b.
+__device__ __forceinline__ void mix28_column(float* buf, int b, int r, int p) {
+  const int pb = lds_pos(b);
+  auto at = [&](int k) -> float& { return buf[pb ^ lds_pos((28 * r + k) * p)]; };
+  float u[28];
+#pragma unroll
+  for (int i = 0; i < 14; ++i) {
+    const float x0 = at(2 * i), x1 = at(2 * i + 1);
+    u[2 * i] = x0 + x1;
+    u[2 * i + 1] = x0 - x1;
+  }
+#pragma unroll
+  for (int c = 0; c < 14; ++c) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int b0 = c == 0 ? 1 : 0;
+      float acc = ((kC14.neg[c] >> b0) & 1u) != 0 ? -u[2 * b0 + s] : u[2 * b0 + s];
+#pragma unroll
+      for (int bb = b0 + 1; bb < 14; ++bb) {
+        if (bb == c) continue;
+        acc = ((kC14.neg[c] >> bb) & 1u) != 0 ? acc - u[2 * bb + s] : acc + u[2 * bb + s];
+      }
+      at(2 * c + s) = s == 0 ? acc + u[2 * c + 1] : acc - u[2 * c];
+    }
   }
 }
 
@@ -120,9 +173,7 @@ __device__ __forceinline__ void rotate_rows_lds(const T* __restrict__ x, int64_t
   const int total = rr * n;   // elements held
   const int m = n / p;
   // load 8 entries at a time, stages h = 1, 2, 4 in registers (p >= 8)
-  for (int g = tid; g < total / 8; g += NT) {
-    const int e = 8 * g;
-    const int r = e / n, c = e - r * n;
+  auto first = [&](int e, int r, int c) {
     float v[8];
     load8<T>(x + r * ld_x + c, v);
 #pragma unroll
@@ -136,49 +187,31 @@ __device__ __forceinline__ void rotate_rows_lds(const T* __restrict__ x, int64_t
         }
       }
     }
-    float* d = buf + lds_pos(e);
+    const int pe = lds_pos(e);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) d[i] = v[i];
-  }
-  // stages h = 8 .. p / 2 along each segment of length p, four at a time
-  for (int b0 = 3; b0 < lp; b0 += 4) {
-    __syncthreads();
-    switch (lp - b0 < 4 ? lp - b0 : 4) {
-      case 1: fwht_pass<1, NT>(buf, total, lp, b0); break;
-      case 2: fwht_pass<2, NT>(buf, total, lp, b0); break;
-      case 3: fwht_pass<3, NT>(buf, total, lp, b0); break;
-      default: fwht_pass<4, NT>(buf, total, lp, b0); break;
+    for (int i = 0; i < 8; ++i) buf[pe ^ i] = v[i];
+  };
+  if (rr == 1) {
+    for (int e = 8 * tid; e < n; e += 8 * NT) first(e, 0, e);
+  } else {
+    for (int e = 8 * tid; e < total; e += 8 * NT) {
+      const int r = e / n;
+      first(e, r, e - r * n);
     }
   }
+  // stages h = 8 .. p / 2 along each segment of length p, four at a time (p <= 2^15)
+  fwht_pass_at<3, NT>(buf, total, lp);
+  fwht_pass_at<7, NT>(buf, total, lp);
+  fwht_pass_at<11, NT>(buf, total, lp);
   __syncthreads();
   if (m == 28) {
-    // the H_28 factor through its construction, for each column of the 28 segments: H_2 on
-    // each segment pair (u_2b = X_2b + X_2b+1, u_2b+1 = X_2b - X_2b+1), then output 2c + s
-    // is the sum over b != c, in increasing b, of C[b][c] u_2b+s, plus u_2c+1 (s = 0) or
-    // minus u_2c (s = 1): 13 additions per output
-    for (int q = tid; q < rr * p; q += NT) {
-      const int r = q / p, b = q - r * p;
-      const int col = r * n + b;
-      float u[28];
-#pragma unroll
-      for (int i = 0; i < 14; ++i) {
-        const float x0 = buf[lds_pos(col + 2 * i * p)], x1 = buf[lds_pos(col + (2 * i + 1) * p)];
-        u[2 * i] = x0 + x1;
-        u[2 * i + 1] = x0 - x1;
-      }
-#pragma unroll
-      for (int c = 0; c < 14; ++c) {
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          const int b0 = c == 0 ? 1 : 0;
-          float acc = ((kC14.neg[c] >> b0) & 1u) != 0 ? -u[2 * b0 + s] : u[2 * b0 + s];
-#pragma unroll
-          for (int bb = b0 + 1; bb < 14; ++bb) {
-            if (bb == c) continue;
-            acc = ((kC14.neg[c] >> bb) & 1u) != 0 ? acc - u[2 * bb + s] : acc + u[2 * bb + s];
-          }
-          buf[lds_pos(col + (2 * c + s) * p)] = s == 0 ? acc + u[2 * c + 1] : acc - u[2 * c];
-        }
+    // the H_28 factor, column by column
+    if (rr == 1) {
+      for (int b = tid; b < p; b += NT) mix28_column(buf, b, 0, p);
+    } else {
+      for (int q = tid; q < rr * p; q += NT) {
+        const int r = q / p;
+        mix28_column(buf, q - r * p, r, p);
       }
     }
     __syncthreads();
