@@ -25,7 +25,30 @@ __global__ __launch_bounds__(NT) void rotate_kernel(const T* __restrict__ x, int
   const int64_t row0 = (int64_t)blockIdx.x * rpw;
   const int rr = (int)std::min<int64_t>(rpw, rows - row0);   // rows in this workgroup
   const int total = rr * n;                                  // elements held
-  rotate_rows_lds<T, NT>(x + row0 * ld_x, ld_x, rr, n, p, lp, buf);
+  const int half = rotate_rows_lds<T, NT, true>(x + row0 * ld_x, ld_x, rr, n, p, lp, buf);
+  if (half > 0) {
+    // the last stage, h = half (a power of two >= 8), fused with the output: entries e and
+    // e + half of each group of 8 become (a + b, a - b), then times s
+    for (int g = 8 * tid; g < total / 2; g += 8 * NT) {
+      const int e = ((g & -half) << 1) | (g & (half - 1));
+      const int r = rr == 1 ? 0 : e / n, c = e - r * n;
+      const int pa = lds_pos(e), pb = lds_pos(e + half);
+      float lo[8], hi[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const float a = buf[pa ^ i], b = buf[pb ^ i];
+        lo[i] = (a + b) * s;
+        hi[i] = (a - b) * s;
+      }
+      f32x4* o = reinterpret_cast<f32x4*>(y + (row0 + r) * ld_y + c);
+      __builtin_nontemporal_store((f32x4){lo[0], lo[1], lo[2], lo[3]}, o);
+      __builtin_nontemporal_store((f32x4){lo[4], lo[5], lo[6], lo[7]}, o + 1);
+      o = reinterpret_cast<f32x4*>(y + (row0 + r) * ld_y + c + half);
+      __builtin_nontemporal_store((f32x4){hi[0], hi[1], hi[2], hi[3]}, o);
+      __builtin_nontemporal_store((f32x4){hi[4], hi[5], hi[6], hi[7]}, o + 1);
+    }
+    return;
+  }
   auto out = [&](int e, int r, int c) {
     const int pe = lds_pos(e);
     f32x4 lo = {buf[pe] * s, buf[pe ^ 1] * s, buf[pe ^ 2] * s, buf[pe ^ 3] * s};

@@ -119,12 +119,13 @@ __device__ __forceinline__ void fwht_pass(float* buf, int total, int lp) {
   }
 }
 
-// The pass over bits B0 .. min(B0 + 3, lp - 1), after a barrier, if lp > B0.
+// The pass over bits B0 .. min(B0 + 3, top - 1) of segments of length 2^lp, after a
+// barrier, if top > B0.
 template <int B0, int NT>
-__device__ __forceinline__ void fwht_pass_at(float* buf, int total, int lp) {
-  if (lp <= B0) return;
+__device__ __forceinline__ void fwht_pass_at(float* buf, int total, int lp, int top) {
+  if (top <= B0) return;
   __syncthreads();
-  switch (lp - B0 < 4 ? lp - B0 : 4) {
+  switch (top - B0 < 4 ? top - B0 : 4) {
     case 1: fwht_pass<1, B0, NT>(buf, total, lp); break;
     case 2: fwht_pass<2, B0, NT>(buf, total, lp); break;
     case 3: fwht_pass<3, B0, NT>(buf, total, lp); break;
@@ -166,9 +167,13 @@ __device__ __forceinline__ void mix28_column(float* buf, int b, int r, int p) {
 // buf: entry e (row e / n) ends at buf[lds_pos(e)], and its rotated value is that times
 // fl32(1 / sqrt(n)).  p = n / m = 2^lp >= 8.  Every thread of the workgroup (NT) must call
 // it; it ends with a barrier.
-template <typename T, int NT = 256>
-__device__ __forceinline__ void rotate_rows_lds(const T* __restrict__ x, int64_t ld_x, int rr,
-                                                int n, int p, int lp, float* buf) {
+//
+// LAST_OUT (n = p = 2^lp with lp = 4, 8 or 12, where the last pass would hold a single
+// stage): that stage, h = p / 2, is left to the caller, which applies it as it reads the
+// entries out (rotate_last_stage); the function returns h then, else 0.
+template <typename T, int NT = 256, bool LAST_OUT = false>
+__device__ __forceinline__ int rotate_rows_lds(const T* __restrict__ x, int64_t ld_x, int rr,
+                                               int n, int p, int lp, float* buf) {
   const int tid = threadIdx.x;
   const int total = rr * n;   // elements held
   const int m = n / p;
@@ -200,10 +205,13 @@ __device__ __forceinline__ void rotate_rows_lds(const T* __restrict__ x, int64_t
     }
   }
   // stages h = 8 .. p / 2 along each segment of length p, four at a time (p <= 2^15)
-  fwht_pass_at<3, NT>(buf, total, lp);
-  fwht_pass_at<7, NT>(buf, total, lp);
-  fwht_pass_at<11, NT>(buf, total, lp);
+  const bool defer = LAST_OUT && m == 1 && (lp == 4 || lp == 8 || lp == 12);
+  const int top = defer ? lp - 1 : lp;   // stages below 2^top here
+  fwht_pass_at<3, NT>(buf, total, lp, top);
+  fwht_pass_at<7, NT>(buf, total, lp, top);
+  fwht_pass_at<11, NT>(buf, total, lp, top);
   __syncthreads();
+  if (defer) return p / 2;
   if (m == 28) {
     // the H_28 factor, column by column
     if (rr == 1) {
@@ -216,6 +224,7 @@ __device__ __forceinline__ void rotate_rows_lds(const T* __restrict__ x, int64_t
     }
     __syncthreads();
   }
+  return 0;
 }
 
 }  // namespace nq
