@@ -203,7 +203,8 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
   int pm, pn;
   tile_coords(blockIdx.x, tm, tn, pm, pn);
   const int tid = threadIdx.x;
-  const int wave = tid >> 6, lane = tid & 63;
+  // the wave index as a uniform (scalar) value, so that LDS destinations stay scalar
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int wm = wave / WN, wn = wave % WN;
 
   // This lane's source for each of the wave's row groups: row lane / CH of the group,
@@ -272,9 +273,12 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
     cs[j] = rw[col < N ? col : N - 1] * scale;
   }
 
-  for (int ks = 0; ks < nks; ++ks) {
+  // One stage; PF: the loads of stage ks + NSTAGE - 1 are issued (every stage but the last
+  // NSTAGE - 1), a compile-time flag so that the steady-state loop has no branches.
+  auto stage = [&](int ks, auto pf) {
+    constexpr bool PF = decltype(pf)::value;
     // stage ks has landed when at most the later stages' loads are outstanding
-    if (ks + NSTAGE - 2 < nks) {
+    if (PF || ks + NSTAGE - 2 < nks) {
       __builtin_amdgcn_s_waitcnt((GROUPS_PER_WAVE * (NSTAGE - 2)) | (0x7 << 4) | (0xF << 8));
     } else {
       __builtin_amdgcn_s_waitcnt(0 | (0x7 << 4) | (0xF << 8));
@@ -287,7 +291,7 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     __builtin_amdgcn_s_barrier();
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    const bool prefetch = ks + NSTAGE - 1 < nks;
+    constexpr bool prefetch = PF;
     unsigned char* nb = lds + ((ks + NSTAGE - 1) % NSTAGE) * STAGE_BYTES;
     const unsigned char* sb = lds + (ks % NSTAGE) * STAGE_BYTES;
     // Fragments are double-buffered in registers.  Within a step the MFMAs are interleaved
@@ -351,7 +355,10 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
                                            (lds_void*)(nb + dst[g]), 16, 0, 0);
       }
     }
-  }
+  };
+  int ks = 0;
+  for (; ks < nks - (NSTAGE - 1); ++ks) stage(ks, std::true_type{});
+  for (; ks < nks; ++ks) stage(ks, std::false_type{});
 
   // Epilogue: C = acc * r_A * (r_W * scale); whole tiles skip the bounds tests.
   float* cp = c + m0 * ldc + n0;
