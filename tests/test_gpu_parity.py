@@ -525,6 +525,15 @@ ROTATE_CASES = [
     (66, 7, 1792, "bf16", "normal"),
     (67, 4, 14336, "bf16", "normal"),
     (68, 3, 28672, "f16", "normal"),
+    # several rows per workgroup with a ragged last group, the single last stage applied on
+    # the way out (16, 256, 4096), and the other pass splits
+    (69, 300, 16, "bf16", "normal"),
+    (70, 37, 256, "f16", "t4"),
+    (71, 13, 512, "f32", "normal"),
+    (72, 6, 2048, "bf16", "t4"),
+    (73, 5, 8192, "bf16", "normal"),
+    (74, 9, 3584, "f16", "normal"),
+    (75, 5, 7168, "bf16", "t4"),
 ]
 
 
