@@ -237,7 +237,7 @@ def kv_roofline(args):
     import workloads
     import paper_2502_09720_amd as nq
 
-    c = workloads.CONFIGS[5]
+    c = workloads.WORKLOADS[5]
     rows, cols = c["X_rows"], c["X_cols"]
     dev = torch.device("cuda:0")
     X = torch.empty(rows, cols, dtype=torch.float16, device=dev)
@@ -321,7 +321,7 @@ def cpu_baseline(cfg, q, k, flops_full, min_seconds=10.0, max_reps=5):
         blas_threads = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
     except Exception:  # pragma: no cover
         blas_threads = 1
-    c = workloads.CONFIGS[cfg]
+    c = workloads.WORKLOADS[cfg]
     M, N, K = c["M"], c["N"], c["K"]
     _, A32, _ = workloads.operand(cfg, "A")
     _, W32, _ = workloads.operand(cfg, "W")
@@ -376,7 +376,7 @@ def main():
     import paper_2502_09720_amd as nq
 
     cfg = args.workload
-    c = workloads.CONFIGS[cfg]
+    c = workloads.WORKLOADS[cfg]
     M, N, K = c["M"], c["N"], c["K"]
     q = args.q or c["qs"][0]
     k = c["k"]

@@ -65,14 +65,14 @@ def _check_rows(coded, x32, rows, q, k, decoder="full"):
     return c, t, r
 
 
-WORKLOADS = [(2, 14), (3, 14), (4, 14), (4, 7), (5, 14)]
+CASES = [(2, 14), (3, 14), (4, 14), (4, 7), (5, 14)]
 
 
-@pytest.mark.parametrize("cfg,q", WORKLOADS, ids=lambda v: str(v))
+@pytest.mark.parametrize("cfg,q", CASES, ids=lambda v: str(v))
 def test_workload_full_size_sampled(nq, cfg, q):
     """The bench step (nq_encode_matmul with W coded once by nq_encode) at full size."""
     import torch
-    c = workloads.CONFIGS[cfg]
+    c = workloads.WORKLOADS[cfg]
     M, N, K, k = c["M"], c["N"], c["K"], c["k"]
     sa, A32, dt = workloads.operand(cfg, "A")
     sw, W32, _ = workloads.operand(cfg, "W")

@@ -7,16 +7,16 @@ their inputs from here, so every side sees identical bytes.
 The paper evaluates on Llama-3-8B / 70B weights and WikiText2 activations (Sec. 5), which
 are not available; these draws stand in for them with the same shapes:
 
-  cfg 1  A 64x512, W 256x512, fp32 iid N(0,1)                               (small case)
-  cfg 2  A 16x4096 bf16 N(0,1); W 14336x4096 bf16 N(0,0.02^2)               (decode-shaped)
-  cfg 3  A 2048x4096 bf16 Student-t(4); W 4096x4096 bf16 N(0,0.02^2)        (8B q_proj)
-  cfg 4  A 4096x14336 bf16 N(0,1) with 143 columns (1%) scaled by 20;
+  workload 1  A 64x512, W 256x512, fp32 iid N(0,1)                               (small case)
+  workload 2  A 16x4096 bf16 N(0,1); W 14336x4096 bf16 N(0,0.02^2)               (decode-shaped)
+  workload 3  A 2048x4096 bf16 Student-t(4); W 4096x4096 bf16 N(0,0.02^2)        (8B q_proj)
+  workload 4  A 4096x14336 bf16 N(0,1) with 143 columns (1%) scaled by 20;
          W 4096x14336 bf16 N(0,0.02^2)                                      (8B down_proj)
-  cfg 5  A 2048x8192 bf16 N(0,1); W 28672x8192 bf16 N(0,0.015^2);
+  workload 5  A 2048x8192 bf16 N(0,1); W 28672x8192 bf16 N(0,0.015^2);
          X 2^21 x 128 fp16 N(0,1) (2^28 entries, KV-cache-like rows)         (70B MLP)
 
-Recipe: each operand has its own stream ``numpy.random.default_rng([cfg, j])`` with j = 0
-for A, 1 for W, 2 for X; values are drawn in float64 (in row chunks, so a row range can be
+Recipe: each operand has its own stream ``numpy.random.default_rng([w, j])``, w the
+workload number and j = 0 for A, 1 for W, 2 for X; values are drawn in float64 (in row chunks, so a row range can be
 generated alone), scaled, and rounded once to the stored dtype (round to nearest even).
 """
 
@@ -24,7 +24,7 @@ import numpy as np
 
 CHUNK_ROWS = 1 << 14
 
-CONFIGS = {
+WORKLOADS = {
     1: dict(name="coded GEMM 64x256x512 fp32 N(0,1)", M=64, N=256, K=512, dtype="f32",
             qs=(14,), k=4),
     2: dict(name="decode-shaped linear 16x14336x4096 bf16", M=16, N=14336, K=4096, dtype="bf16",
@@ -119,7 +119,7 @@ def operand(cfg, which, row_range=None):
     storage is uint16 bf16 bits, float16 or float32; the fp32 view holds the same values.
     row_range=(lo, hi) returns only those rows, identical to the full draw's rows.
     """
-    c = CONFIGS[cfg]
+    c = WORKLOADS[cfg]
     if which == "A":
         rows, cols, dt = c["M"], c["K"], c["dtype"]
     elif which == "W":
@@ -134,7 +134,7 @@ def operand(cfg, which, row_range=None):
 
 
 def outlier_columns(cfg=4):
-    c = CONFIGS[cfg]
+    c = WORKLOADS[cfg]
     rng = np.random.default_rng([cfg, 0])
     return np.sort(rng.choice(c["K"], size=c["K"] // 100, replace=False))
 
