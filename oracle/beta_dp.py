@@ -14,11 +14,14 @@ TEST INFRASTRUCTURE ONLY (see the package docstring).
   The answer is dp[i][k] for an i at which no vector overloads (readings: the least such
   dp[i][k], the smallest i on a tie; a beta set in which nothing fits is not returned).
   Alg. 6's model equals the First-beta error whenever overload is monotone in beta.
-  Reading on the rounding: each cost is summed over the vectors in a fixed 64-ary tree
-  (``tree_sum``: consecutive groups of 64 terms added in order, then groups of 64 of those
-  sums, and so on), and the minima take the first s (and the first i) on exact ties.
-* ``first_beta_loss``: the total First-beta error of a given beta subset (what Alg. 6
-  minimizes), for checking the DP against brute force.
+  Reading on the rounding: each cost is the exact sum of its terms over the vectors,
+  rounded once to fp64 (no summation order is involved); the recurrence adds costs in
+  fp64 as Alg. 6 writes it, and the minima take the first s (and the first i) on exact ties.
+* ``dp_model_loss``: the total that Alg. 6's recurrence assigns to a given beta subset (every
+  transition's charge, summed exactly), for checking the DP against brute force on any
+  statistics.
+* ``first_beta_loss``: the total First-beta error of a given beta subset (summed exactly);
+  it equals ``dp_model_loss`` when overload is monotone in beta.
 * ``synthetic_frontier``: Sec. 6.1's experiment at a small size: for each (q, k) the DP picks
   k betas from the grid {1/2, 1, ..., 25} / q on sample vectors, both matrices are coded with
   them (Alg. 3, First-beta) and multiplied from the codes (Alg. 4); the rate is
@@ -60,17 +63,9 @@ def block_stats(v64, betas, q, decoder="full"):
     return mse, over
 
 
-def tree_sum(terms, fan=64):
-    """Sum of fp64 terms in a fixed fan-ary tree: consecutive groups of ``fan`` values are
-    added in order (one rounding per addition), level by level, until one value is left.
-    A short last group adds only what it has (padding with +0 changes no value)."""
-    t = np.asarray(terms, dtype=np.float64).ravel()
-    if t.size == 0:
-        return 0.0
-    while t.size > 1:
-        t = np.concatenate([t, np.zeros((-t.size) % fan)]).reshape(-1, fan)
-        t = np.cumsum(t, axis=1)[:, -1]                   # sequential within each group
-    return float(t[0])
+def exact_sum(terms):
+    """The exact sum of fp64 terms, rounded once to fp64 (math.fsum)."""
+    return math.fsum(np.asarray(terms, dtype=np.float64).ravel().tolist())
 
 
 def dp_betas(mse, over, k):
@@ -87,7 +82,7 @@ def dp_betas(mse, over, k):
     for i in range(1, m + 1):
         for s in range(0, i):
             cond = ov[:, s] & ~ov[:, i]
-            cost[s, i] = tree_sum(np.where(cond, ms[:, i], 0.0))
+            cost[s, i] = exact_sum(ms[cond, i])
     dp = np.full((m + 1, k + 1), INF)
     frm = np.full((m + 1, k + 1), -1, dtype=np.int64)
     dp[0, 0] = 0.0
@@ -115,23 +110,43 @@ def dp_betas(mse, over, k):
 def first_beta_loss(mse, over, subset):
     """Total error of First-beta with the betas `subset` (indices): each vector takes the
     first beta of the subset at which it does not overload, the last one if it overloads at
-    all of them."""
+    all of them (summed exactly)."""
     sub = list(subset)
     ok = ~over[:, sub]
     pick = np.where(ok.any(axis=1), np.argmax(ok, axis=1), len(sub) - 1)
-    return float(mse[np.arange(mse.shape[0]), np.asarray(sub)[pick]].sum())
+    return exact_sum(mse[np.arange(mse.shape[0]), np.asarray(sub)[pick]])
 
 
-def brute_force_betas(mse, over, k):
-    """The best k-subset under Alg. 6's model, by enumeration (small grids only)."""
+def dp_model_loss(mse, over, subset):
+    """What Alg. 6's recurrence charges for the increasing betas `subset` (s_1 < ... < s_k):
+    for each j, the errors at beta_{s_j} of the vectors that overload at s_{j-1} but not at
+    s_j (s_0 the virtual beta at which every vector overloads), summed exactly.  inf if the
+    largest beta overloads some vector (the DP never returns such a set)."""
+    sub = list(subset)
+    if over[:, sub[-1]].any():
+        return math.inf
+    terms = []
+    prev = np.ones(mse.shape[0], dtype=bool)
+    for s in sub:
+        cond = prev & ~over[:, s]
+        terms.append(mse[cond, s])
+        prev = over[:, s]
+    return exact_sum(np.concatenate(terms)) if terms else 0.0
+
+
+def brute_force_betas(mse, over, k, loss=None):
+    """The best k-subset under ``loss`` (default: the First-beta error) among those whose
+    largest beta overloads nothing, by enumeration (small grids only); first subset in
+    lexicographic order on ties."""
+    loss = first_beta_loss if loss is None else loss
     m = mse.shape[1]
     best, arg = math.inf, None
     for sub in itertools.combinations(range(m), k):
         if over[:, sub[-1]].any():
             continue
-        loss = first_beta_loss(mse, over, sub)
-        if loss < best:
-            best, arg = loss, list(sub)
+        val = loss(mse, over, sub)
+        if val < best:
+            best, arg = val, list(sub)
     return arg, best
 
 

@@ -272,8 +272,17 @@ def coded_matmul(a_codes, a_t, a_r, qa, base_a, w_codes, w_t, w_r, qw, base_w,
     sums are formed with an fp64 matrix product, which is exact because every partial sum
     is an integer below 2^53.  Returns fp64 (M, N).
     """
-    TA = integer_tiles(a_codes, a_t, qa, decoder_a, mult_a).astype(np.float64)
-    TW = integer_tiles(w_codes, w_t, qw, decoder_w, mult_w).astype(np.float64)
+    TA = integer_tiles(a_codes, a_t, qa, decoder_a, mult_a)
+    TW = integer_tiles(w_codes, w_t, qw, decoder_w, mult_w)
+    return product_from_tiles(TA, a_r, base_a, TW, w_r, base_w)
+
+
+def product_from_tiles(TA, a_r, base_a, TW, w_r, base_w):
+    """C_ij = r_Ai r_Wj base_A base_W / 4 * sum_l TA_il TW_jl for integer tiles T = m X2
+    (``integer_tiles``) and fp32 row scales: the exact integer sums (an fp64 matrix product,
+    exact while every partial sum is an integer below 2^53), then the scaling.  fp64 (M, N)."""
+    TA = np.asarray(TA).astype(np.float64)
+    TW = np.asarray(TW).astype(np.float64)
     bound = float(np.abs(TA).max(initial=0)) * float(np.abs(TW).max(initial=0)) * TA.shape[1]
     assert bound < 2.0 ** 53, "integer sums would not be exact in fp64"
     S = TA @ TW.T

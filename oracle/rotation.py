@@ -15,13 +15,10 @@ only "hardcoded Hadamard"):
 * y = x U is computed in fp32 as a fast Walsh-Hadamard transform: for h = 1, 2, 4, ...,
   2^(k-1), every pair (i, i + h) with i & h = 0 becomes (a + b, a - b), one fp32 rounding
   per sum; the row is read as X[i, j] = x[i 2^k + j], i < m, and the transform runs along j.
-* For m = 28 the H_1 factor is applied through its construction, H_28 = C kron H_2 +
-  I_14 kron K_2 (below; H_28 is symmetric, so y_a = sum_i H_28[i, a] X_i = (H_28 X)_a).
-  With rows i = 2b + r: first u_{2b} = X_{2b} + X_{2b+1} and u_{2b+1} = X_{2b} - X_{2b+1}
-  (the H_2 factor, one fp32 rounding each); then output a = 2c + s is the sum over b = 0..13,
-  b != c (C has a zero diagonal), in increasing b, of C[b, c] u_{2b+s}, starting from the
-  first term, followed by the K_2 term: + u_{2c+1} for s = 0, - u_{2c} for s = 1 (fp32, one
-  rounding per step).  That is 13 additions per output instead of 27.
+* For m = 28, output segment a of the H_1 factor is the plain matrix product written out:
+  the sum over i = 0..27, in increasing i, of H_28[i, a] X_i (X_i the i-th length-2^k
+  segment after the transform), starting from H_28[0, a] X_0, fp32 with one rounding per
+  addition (each term is an exact +-X_i).
 * Finally every entry is multiplied once by fl32(1 / sqrt(n)) (fl64 square root and
   division first; a power of two when n is a power of four).
 * H_28 (Paley II, q = 13 = 1 mod 4): with chi the quadratic character mod 13 and the
@@ -104,20 +101,12 @@ def rotate_rows(x32):
         X = Y.reshape(rows, m, p)
         h *= 2
     if m == 28:
-        C = conference14()
-        u = np.empty_like(X)
-        u[:, 0::2, :] = X[:, 0::2, :] + X[:, 1::2, :]            # H_2 on each row pair
-        u[:, 1::2, :] = X[:, 0::2, :] - X[:, 1::2, :]
+        H1 = paley28()
         out = np.empty_like(X)
-        for c in range(14):
-            for s_ in (0, 1):
-                acc = None
-                for b in range(14):
-                    if b == c:
-                        continue
-                    t = u[:, 2 * b + s_, :] * np.float32(C[b, c])   # exact +-u
-                    acc = t if acc is None else acc + t            # one rounding per sum
-                k2 = u[:, 2 * c + 1, :] if s_ == 0 else -u[:, 2 * c, :]
-                out[:, 2 * c + s_, :] = acc + k2
+        for a in range(28):
+            acc = X[:, 0, :] * np.float32(H1[0, a])                # exact +-X_0
+            for i in range(1, 28):
+                acc = acc + X[:, i, :] * np.float32(H1[i, a])     # one rounding per sum
+            out[:, a, :] = acc
         X = out
     return (X.reshape(rows, n) * scale32(n)).astype(np.float32)

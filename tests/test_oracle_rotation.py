@@ -83,10 +83,10 @@ def test_conference14():
 
 
 @pytest.mark.parametrize("p", [8, 64])
-def test_structured_mix_is_exact_on_integers(p):
-    """Small integer rows keep every fp32 sum exact, so the fast transform (with the H_28
-    mix through its Kronecker structure) must equal the integer product x (H_28 kron H_p)
-    before the final scaling: any wrong sign or index in the mix shows."""
+def test_mix_is_exact_on_integers(p):
+    """Small integer rows keep every fp32 sum exact, so the fast transform followed by the
+    H_28 sums must equal the integer product x (H_28 kron H_p) before the final scaling: any
+    wrong sign or index in the transform or the mix shows."""
     n = 28 * p
     rng = np.random.default_rng(p)
     x = rng.integers(-8, 9, size=(5, n)).astype(np.float32)
