@@ -26,7 +26,8 @@
  *
  * Conventions for every call:
  *   - all array pointers are device pointers, owned by the caller; the library keeps no
- *     per-call state, and allocates nothing except nq_matmul's stream-ordered workspace;
+ *     per-call state and allocates no memory: calls that need scratch memory take a
+ *     caller-owned workspace and have a size query (nq_matmul_ex, nq_beta_dp);
  *   - calls are asynchronous on `hip_stream` (a hipStream_t; NULL = the null stream) and
  *     may be issued from several host threads;
  *   - arguments are checked on the host before anything is launched: on any error the
@@ -47,17 +48,20 @@ typedef enum {
   NQ_OK = 0,
   NQ_ERR_INVALID_ARG = 1,  /* a size, stride, pointer or parameter is out of range   */
   NQ_ERR_UNSUPPORTED = 2,  /* valid in principle but not implemented (e.g. dtype)    */
-  NQ_ERR_HIP = 3           /* the HIP runtime reported an error at launch            */
+  NQ_ERR_HIP = 3,          /* the HIP runtime reported an error at launch            */
+  NQ_STATUS_MAX_ENUM = 0x7FFFFFFF
 } nq_status;
 
-typedef enum { NQ_F32 = 0, NQ_F16 = 1, NQ_BF16 = 2 } nq_dtype;
+/* Every enum of this ABI has a MAX_ENUM member, so that it is 32 bits wide and any int32
+ * value a caller passes is a value of the type (invalid ones are then rejected by value). */
+typedef enum { NQ_F32 = 0, NQ_F16 = 1, NQ_BF16 = 2, NQ_DTYPE_MAX_ENUM = 0x7FFFFFFF } nq_dtype;
 
 /* Decoder of the code (part of its definition: the encoder's overload test uses it).
  *   NQ_DECODER_FULL  Alg. 2 with the Gosset oracle of Alg. 5 (App. C);
  *   NQ_DECODER_M     NestQuantM (App. D): the oracle's parity fixes at the first coordinate
  *                    (no argmin / argmax); the encoder is unchanged except that a point
  *                    counts as overloaded when this decoder does not reproduce it. */
-typedef enum { NQ_DECODER_FULL = 0, NQ_DECODER_M = 1 } nq_decoder;
+typedef enum { NQ_DECODER_FULL = 0, NQ_DECODER_M = 1, NQ_DECODER_MAX_ENUM = 0x7FFFFFFF } nq_decoder;
 
 /* How the encoder picks one of the k betas for a block (App. F).  Both give the same code
  * format; decoding and the matrix product do not look at it.
@@ -67,7 +71,7 @@ typedef enum { NQ_DECODER_FULL = 0, NQ_DECODER_M = 1 } nq_decoder;
  *                  error is sum over l = 0..7, in that order, of d_l^2 with
  *                  d_l = fl64(fl64(beta_t * X2_t,l) / 2 - fl64(x_l / r)), every step
  *                  rounded in fp64, and the first t with the least error wins. */
-typedef enum { NQ_FIRST_BETA = 0, NQ_OPT_BETA = 1 } nq_strategy;
+typedef enum { NQ_FIRST_BETA = 0, NQ_OPT_BETA = 1, NQ_STRATEGY_MAX_ENUM = 0x7FFFFFFF } nq_strategy;
 
 /* Quantizer parameters (Sec. 4.2, App. F):
  *   q        nesting ratio, 2 <= q <= 16 (codes are nibbles);
@@ -118,7 +122,7 @@ nq_status nq_decode(const nq_params* p, const uint32_t* codes, const uint32_t* b
                     const float* scales, int64_t rows, int64_t cols, void* out,
                     nq_dtype out_dtype, int64_t ld_out, void* hip_stream);
 
-/* C = A_hat * W_hat^T (Alg. 4 for every row pair), fp32 output.
+/* C = A_hat * W_hat^T (Alg. 4 for every row pair), fp32 output, with no workspace.
  *   A: M x K coded with parameters pa; W: N x K coded with parameters pw (q, k, base and
  *   mult may differ between the operands; K must be the same);  K % 8 == 0, K <= 65536.
  *   c: device, M x N floats, row i at c + i*ldc, ldc >= N.
@@ -126,18 +130,23 @@ nq_status nq_decode(const nq_params* p, const uint32_t* codes, const uint32_t* b
  * block's beta); the integer tiles m*X2 are contracted with fp32 accumulation on bf16
  * matrix cores, exact in bf16 when 2q * mult_k <= 256 for both operands (always so for the
  * uniform grid), else on fp16 matrix cores (exact up to 2048, every allowed mult).
- * Every block of both operands is decoded exactly once; the decoded activation (and, for
- * M > 64, the decoded weight) lives in a workspace of nq_matmul_workspace_size(M, N, K)
- * bytes, which nq_matmul takes from the stream-ordered allocator of the current device
- * (hipMallocAsync / hipFreeAsync on hip_stream); use nq_matmul_ex to pass a workspace. */
+ * Each workgroup decodes (Alg. 2) the code words of its own rows of A and W into on-chip
+ * memory and contracts them there, so the call needs and allocates no memory; a block of A is
+ * decoded once per 128 columns of C (64 for M <= 64) and a block of W once per 256 rows of C
+ * (64 for M <= 64).  nq_matmul_ex computes the same product decoding every block exactly
+ * once into a caller's workspace, which is faster once M is in the hundreds; for M > 64 the
+ * two sum in the same order and agree bit for bit. */
 nq_status nq_matmul(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,
                     const float* a_scales, int64_t M, const nq_params* pw,
                     const uint32_t* w_codes, const uint32_t* w_beta, const float* w_scales,
                     int64_t N, int64_t K, float* c, int64_t ldc, void* hip_stream);
 
 /* nq_matmul with a caller-owned device workspace (16-byte aligned, at least
- * nq_matmul_workspace_size(M, N, K) bytes).  The workspace is used as scratch until the
- * call's kernels finish on hip_stream. */
+ * nq_matmul_workspace_size(M, N, K) bytes): every block of both operands is decoded exactly
+ * once (Alg. 2) into integer tiles m*X2 in the workspace (for M <= 64 only A's; W is then
+ * decoded straight into matrix-core operands), then contracted.  Same product as nq_matmul
+ * (for M <= 64 the fp32 sums are taken in another order).  The workspace is used as scratch
+ * until the call's kernels finish on hip_stream. */
 nq_status nq_matmul_ex(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,
                        const float* a_scales, int64_t M, const nq_params* pw,
                        const uint32_t* w_codes, const uint32_t* w_beta, const float* w_scales,
@@ -184,11 +193,10 @@ nq_status nq_matmul_stages(int32_t stages, const nq_params* pa, const uint32_t* 
  *        overlap x.
  * Supported: cols = 2^k or 28 * 2^k with 2^k >= 8 and cols <= 32768, else
  * NQ_ERR_UNSUPPORTED.  Arithmetic: fp32 fast Walsh-Hadamard transform (stages h = 1, 2, 4, ...
- * along each length-2^k segment); then for 28 * 2^k, with segments i = 2b + r,
- * u_2b = X_2b + X_2b+1 and u_2b+1 = X_2b - X_2b+1 (H_2), and segment 2c + s of the output is
- * the sum over b != c, in increasing b, of C[b][c] u_2b+s followed by + u_2c+1 (s = 0) or
- * - u_2c (s = 1), C the conference matrix of the construction (H_28 = C kron H_2 + I_14 kron
- * K_2); then one multiplication by fl32(1 / sqrt(n)).  rows == 0 is a no-op. */
+ * along each length-2^k segment); then for 28 * 2^k, output segment a is the sum over
+ * i = 0..27, in increasing i, of H_28[i][a] X_i (X_i the i-th segment, each term an exact
+ * +-X_i, one fp32 rounding per addition); then one multiplication by fl32(1 / sqrt(n)).
+ * rows == 0 is a no-op. */
 nq_status nq_rotate(const void* x, nq_dtype x_dtype, int64_t rows, int64_t cols, int64_t ld_x,
                     float* y, int64_t ld_y, void* hip_stream);
 
@@ -252,26 +260,36 @@ nq_status nq_beta_stats(int32_t q, int32_t decoder, const float* v, int64_t n,
 /* Alg. 6 (App. F): the k of the m grid betas that minimize the First-beta error of the n
  * samples under the DP's model, from nq_beta_stats' outputs (device mse and overload, n x m).
  *   1 <= k <= m <= 64; n < 2^31;
- *   chosen   device, k int32 (output): the indices into the grid, increasing, or all -1 if
- *            every grid beta overloads some sample;
- *   loss     device, one double (output): the minimized total squared error (+inf with -1s).
+ *   chosen    device, k int32 (output): the indices into the grid, increasing, or all -1 if
+ *             every grid beta overloads some sample;
+ *   loss      device, one double (output): the minimized total squared error (+inf with -1s);
+ *   workspace device, 8-byte aligned, at least nq_beta_dp_workspace_size(n, m) bytes of
+ *             scratch, used until the call's kernels finish on hip_stream.
  * dp[i][j] is the least total error of the samples that do not overload at beta_i, coded
  * with beta_i and j - 1 smaller betas under First-beta; the step from the next smaller chosen
  * beta s adds the errors at beta_i of the samples that overload at beta_s but not at beta_i
  * (s = 0: a virtual beta at which every sample overloads).  The answer is the least dp[i][k]
  * over the betas at which no sample overloads.  Every cost is an fp64 sum over the samples
  * in a fixed 64-ary tree (consecutive groups of 64 terms added in order, then groups of 64
- * of those sums, and so on); ties go to the smallest index.  Scratch memory of about
- * (n / 4096 + 1) (m (m + 1) / 2 + m) doubles comes from the stream-ordered allocator of the
- * current device (hipMallocAsync / hipFreeAsync on hip_stream). */
+ * of those sums, and so on), so each computed cost and dp value is within (63 d + k) 2^-53
+ * of its exact value, relatively (d = ceil(log64 n)); ties go to the smallest index. */
 nq_status nq_beta_dp(const double* mse, const uint8_t* overload, int64_t n, int32_t m,
-                     int32_t k, int32_t* chosen, double* loss, void* hip_stream);
+                     int32_t k, int32_t* chosen, double* loss, void* workspace,
+                     int64_t workspace_bytes, void* hip_stream);
 
-/* Sizes of the code and beta-index arrays for a rows x cols matrix (-1 if invalid). */
+/* Scratch bytes nq_beta_dp needs for n samples and m betas (about (n / 4096 + 1)
+ * (m (m + 1) / 2 + m) doubles; -1 for an invalid n or m). */
+int64_t nq_beta_dp_workspace_size(int64_t n, int32_t m);
+
+/* Sizes, in 32-bit words, of the code and beta-index arrays of a rows x cols coded matrix
+ * (-1 if rows < 0 or cols is not a positive multiple of 8): one word per 8-block, the eight
+ * 4-bit codes of App. E's packing (rows * cols / 8), and one word per 16 blocks of 2-bit
+ * beta indices (App. E indexes a dictionary of at most four betas; rows * ceil(cols / 128)).
+ * Every coded matrix of the library is stored in arrays of exactly these sizes. */
 int64_t nq_codes_words(int64_t rows, int64_t cols);
 int64_t nq_beta_words(int64_t rows, int64_t cols);
 
-/* Static description of a status code. */
+/* Static description of a status code (the error reporting of this ABI; no paper passage). */
 const char* nq_status_string(nq_status s);
 
 /* Message describing the last failed call on this host thread ("" if none). */

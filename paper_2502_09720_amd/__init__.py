@@ -26,6 +26,7 @@ from .binding import (  # noqa: F401
     library,
     library_path,
     matmul,
+    matmul_direct,
     matmul_workspace_size,
     nq_beta_words,
     nq_codes_words,

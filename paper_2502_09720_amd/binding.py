@@ -68,8 +68,10 @@ def library():
         lib.nq_beta_stats.argtypes = [i32, i32, vp, i64, ctypes.POINTER(ctypes.c_double), i32,
                                       vp, vp, vp]
         lib.nq_beta_stats.restype = ctypes.c_int
-        lib.nq_beta_dp.argtypes = [vp, vp, i64, i32, i32, vp, vp, vp]
+        lib.nq_beta_dp.argtypes = [vp, vp, i64, i32, i32, vp, vp, vp, i64, vp]
         lib.nq_beta_dp.restype = ctypes.c_int
+        lib.nq_beta_dp_workspace_size.argtypes = [i64, i32]
+        lib.nq_beta_dp_workspace_size.restype = i64
         lib.nq_matmul_workspace_size.argtypes = [i64, i64, i64]
         lib.nq_matmul_workspace_size.restype = i64
         for f in ("nq_encode", "nq_decode", "nq_matmul", "nq_matmul_ex", "nq_matmul_stages"):
@@ -243,6 +245,25 @@ def matmul(a, w, stream=None, out=None, workspace=None, stages=STAGE_DECODE | ST
     return out
 
 
+def matmul_direct(a, w, stream=None, out=None):
+    """nq_matmul: C = A_hat W_hat^T with no workspace (each workgroup decodes the code words
+    of its own rows into on-chip memory); the same product as ``matmul``."""
+    import torch
+    if a.cols != w.cols:
+        raise ValueError("K mismatch")
+    if out is None:
+        out = torch.empty(a.rows, w.rows, dtype=torch.float32, device=a.codes.device)
+    pa = _params(a.q, a.k, a.base, a.decoder, mult=a.mult)
+    pw = _params(w.q, w.k, w.base, w.decoder, mult=w.mult)
+    _check(library().nq_matmul(
+        ctypes.byref(pa), ctypes.c_void_p(a.codes.data_ptr()), ctypes.c_void_p(a.beta.data_ptr()),
+        ctypes.c_void_p(a.scales.data_ptr()), a.rows, ctypes.byref(pw),
+        ctypes.c_void_p(w.codes.data_ptr()), ctypes.c_void_p(w.beta.data_ptr()),
+        ctypes.c_void_p(w.scales.data_ptr()), w.rows, a.cols, ctypes.c_void_p(out.data_ptr()),
+        out.stride(0), _stream(stream)))
+    return out
+
+
 def encode_matmul(x, w, q=14, k=4, base=None, decoder=DECODER_FULL, strategy=FIRST_BETA,
                   mult=None, stream=None, out=None, coded_out=None, workspace=None,
                   int8=False, rotate=False):
@@ -342,14 +363,25 @@ def beta_stats(v, betas, q, decoder=DECODER_FULL, stream=None):
     return mse, over
 
 
-def beta_dp(mse, over, k, stream=None):
+def beta_dp(mse, over, k, stream=None, workspace=None):
     """nq_beta_dp (Alg. 6): the k grid indices (int32 cuda tensor, increasing; -1 if every
-    beta overloads) minimizing the First-beta error, and that error (fp64 cuda scalar)."""
+    beta overloads) minimizing the First-beta error, and that error (fp64 cuda scalar).  The
+    scratch memory (nq_beta_dp_workspace_size bytes) comes from torch's allocator unless
+    given."""
     import torch
     n, m = mse.shape
+    lib = library()
     chosen = torch.empty(k, dtype=torch.int32, device=mse.device)
     loss = torch.empty((), dtype=torch.float64, device=mse.device)
-    _check(library().nq_beta_dp(ctypes.c_void_p(mse.data_ptr()), ctypes.c_void_p(over.data_ptr()),
-                                n, m, int(k), ctypes.c_void_p(chosen.data_ptr()),
-                                ctypes.c_void_p(loss.data_ptr()), _stream(stream)))
+    need = lib.nq_beta_dp_workspace_size(n, m)
+    if need < 0:
+        raise ValueError("invalid beta_dp shape")
+    if workspace is None or workspace.numel() * workspace.element_size() < need:
+        workspace = torch.empty(max(need, 8), dtype=torch.uint8, device=mse.device)
+        if stream is not None:
+            workspace.record_stream(stream)       # freed on return, in use on `stream`
+    _check(lib.nq_beta_dp(ctypes.c_void_p(mse.data_ptr()), ctypes.c_void_p(over.data_ptr()),
+                          n, m, int(k), ctypes.c_void_p(chosen.data_ptr()),
+                          ctypes.c_void_p(loss.data_ptr()), ctypes.c_void_p(workspace.data_ptr()),
+                          workspace.numel() * workspace.element_size(), _stream(stream)))
     return chosen, loss

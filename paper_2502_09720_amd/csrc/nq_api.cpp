@@ -137,6 +137,7 @@ const char* nq_status_string(nq_status s) {
     case NQ_ERR_INVALID_ARG: return "NQ_ERR_INVALID_ARG: invalid argument";
     case NQ_ERR_UNSUPPORTED: return "NQ_ERR_UNSUPPORTED: unsupported configuration";
     case NQ_ERR_HIP: return "NQ_ERR_HIP: HIP runtime error";
+    default: break;
   }
   return "unknown nq_status";
 }
@@ -324,8 +325,14 @@ nq_status nq_beta_stats(int32_t q, int32_t decoder, const float* v, int64_t n,
                     who);
 }
 
+int64_t nq_beta_dp_workspace_size(int64_t n, int32_t m) {
+  if (n < 0 || n >= kMaxRows || m < 1 || m > 64) return -1;
+  return (int64_t)nq::beta_dp_workspace(n, m);
+}
+
 nq_status nq_beta_dp(const double* mse, const uint8_t* overload, int64_t n, int32_t m,
-                     int32_t k, int32_t* chosen, double* loss, void* hip_stream) {
+                     int32_t k, int32_t* chosen, double* loss, void* workspace,
+                     int64_t workspace_bytes, void* hip_stream) {
   const char* who = "nq_beta_dp";
   if (m < 1 || m > 64) return fail(NQ_ERR_INVALID_ARG, "%s: m=%d outside [1,64]", who, m);
   if (k < 1 || k > m) return fail(NQ_ERR_INVALID_ARG, "%s: k=%d outside [1, m]", who, k);
@@ -333,14 +340,14 @@ nq_status nq_beta_dp(const double* mse, const uint8_t* overload, int64_t n, int3
     return fail(NQ_ERR_INVALID_ARG, "%s: n=%lld outside [0, 2^31)", who, (long long)n);
   if ((n > 0 && (!mse || !overload)) || !chosen || !loss)
     return fail(NQ_ERR_INVALID_ARG, "%s: NULL array pointer", who);
-  hipStream_t st = (hipStream_t)hip_stream;
-  void* ws = nullptr;
-  hipError_t e = hipMallocAsync(&ws, nq::beta_dp_workspace(n, m), st);
-  if (e != hipSuccess) return hip_status(e, who);
-  e = nq::launch_beta_dp(mse, overload, n, m, k, chosen, loss, ws, st);
-  const hipError_t f = hipFreeAsync(ws, st);
-  if (e != hipSuccess) return hip_status(e, who);
-  return hip_status(f, who);
+  const int64_t need = nq_beta_dp_workspace_size(n, m);
+  if (!workspace || workspace_bytes < need)
+    return fail(NQ_ERR_INVALID_ARG, "%s: workspace of %lld bytes needed", who, (long long)need);
+  if (((uintptr_t)workspace & 7u) != 0)
+    return fail(NQ_ERR_INVALID_ARG, "%s: workspace must be 8-byte aligned", who);
+  return hip_status(nq::launch_beta_dp(mse, overload, n, m, k, chosen, loss, workspace,
+                                       (hipStream_t)hip_stream),
+                    who);
 }
 
 int64_t nq_matmul_workspace_size(int64_t M, int64_t N, int64_t K) {
@@ -447,21 +454,19 @@ nq_status nq_matmul(const nq_params* pa, const uint32_t* a_codes, const uint32_t
   if (nq_status s = check_matmul(pa, a_codes, a_beta, a_scales, M, pw, w_codes, w_beta,
                                  w_scales, N, K, c, ldc, who))
     return s;
+  int et = 0;
+  if (nq_status s = elem_type(pa, pw, false, et, who)) return s;
   if (M == 0 || N == 0) return ok();
-  const int64_t need = nq_matmul_workspace_size(M, N, K);
-  void* ws = nullptr;
   hipStream_t st = (hipStream_t)hip_stream;
-  if (need > 0) {
-    const hipError_t e = hipMallocAsync(&ws, (size_t)need, st);
-    if (e != hipSuccess) return hip_status(e, who);
-  }
-  const nq_status s = nq_matmul_ex(pa, a_codes, a_beta, a_scales, M, pw, w_codes, w_beta,
-                                   w_scales, N, K, c, ldc, ws, need, hip_stream);
-  if (ws) {
-    const hipError_t e = hipFreeAsync(ws, st);
-    if (s == NQ_OK && e != hipSuccess) return hip_status(e, who);
-  }
-  return s;
+  static PerDevice attrs(nq::fused_set_attributes);
+  const hipError_t attr_err = attrs.ensure(st);
+  if (attr_err != hipSuccess) return hip_status(attr_err, who);
+  nq::MatmulOperand A{a_codes, a_beta, a_scales, pa->q, nq::magic_2q(pa->q), M, pa->decoder,
+                      mult_table(pa)};
+  nq::MatmulOperand W{w_codes, w_beta, w_scales, pw->q, nq::magic_2q(pw->q), N, pw->decoder,
+                      mult_table(pw)};
+  const float scale = (float)(pa->base * pw->base * 0.25);
+  return hip_status(nq::launch_matmul_fused(et, A, W, K, c, ldc, scale, st), who);
 }
 
 

@@ -65,7 +65,7 @@ __global__ __launch_bounds__(256) void beta_stats_kernel(const float* __restrict
 // samples overload at beta i).  Each entry is a sum over the samples in a fixed 64-ary tree:
 // consecutive groups of 64 terms are added in order, then groups of 64 group sums, and so
 // on; a short last group adds only the terms it has.
-constexpr int kFan = 64;
+constexpr int kFan = kBetaFan;
 
 __device__ __forceinline__ void pair_of(int idx, int P, int& s, int& i) {
   if (idx >= P) {               // overload count of beta idx - P + 1
@@ -244,23 +244,12 @@ hipError_t launch_beta_stats(const float* v, int64_t n, const BetaGrid& g, int q
   return hipGetLastError();
 }
 
-// Tree buffers: level 2 (one node per 4096 samples) and level 3, ping-ponged upward.
-static int64_t cost_entries(int m) { return (int64_t)m * (m + 1) / 2 + m; }
-static int64_t level2_nodes(int64_t n) { return (n + kFan * kFan - 1) / (kFan * kFan); }
-
-size_t beta_dp_workspace(int64_t n, int m) {
-  const int64_t Q = cost_entries(m);
-  const int64_t a = std::max<int64_t>(level2_nodes(n), 1);
-  const int64_t b = (a + kFan - 1) / kFan;
-  return (size_t)((a + b) * Q * 8);
-}
-
 hipError_t launch_beta_dp(const double* mse, const uint8_t* ov, int64_t n, int m, int k,
                           int32_t* chosen, double* loss, void* ws, hipStream_t st) {
-  const int Q = (int)cost_entries(m);
+  const int Q = (int)beta_cost_entries(m);
   const unsigned qy = (unsigned)((Q + 255) / 256);
   double* buf[2] = {reinterpret_cast<double*>(ws), nullptr};
-  int64_t cnt = level2_nodes(n);
+  int64_t cnt = beta_level2_nodes(n);
   buf[1] = buf[0] + std::max<int64_t>(cnt, 1) * Q;
   int cur = 0;
   if (n == 0) {

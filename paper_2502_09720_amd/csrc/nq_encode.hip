@@ -937,20 +937,6 @@ static hipError_t launch_dtype(const void* x, int64_t rows, int cols, int64_t ld
 #undef NQ_L
 }
 
-// The encoder instantiations that carry a TileTask: First-beta rows of 257 to 2048 blocks
-// (one row per workgroup; every prefill shape of a Llama layer has K in 2056..16384).
-bool encode_carries_task(int cols, int strategy) {
-  const int nb = cols / 8;
-  return strategy == 0 && nb > 256 && nb <= 2048;
-}
-
-// The same instantiations rotate their row in LDS, for widths nq_rotate supports:
-// 4096, 8192, 16384 and 28 * 2^k = 3584, 7168, 14336.
-bool encode_rotates(int cols, int strategy) {
-  int p = 0;
-  return encode_carries_task(cols, strategy) && rotation_split(cols, p) != 0;
-}
-
 hipError_t launch_encode(const void* x, int dtype, int64_t rows, int cols, int64_t ld_x,
                          const EncodeArgs& a, uint32_t* codes, uint32_t* beta, float* scales,
                          hipStream_t st) {

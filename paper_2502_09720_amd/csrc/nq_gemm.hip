@@ -28,21 +28,15 @@
 #include <type_traits>
 
 #include "nq_device.hpp"
+#include "nq_gemm_common.hpp"
 #include "nq_kernels.hpp"
 #include "nq_tiles.hpp"
 
 namespace nq {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef int i32x4 __attribute__((ext_vector_type(4)));
-typedef int i32x16 __attribute__((ext_vector_type(16)));
-
 namespace gemm {
 constexpr int BK = 64;     // workspace rows are padded to 64 bf16 / 128 int8 ...
-constexpr int BKB = 128;   // ... i.e. to whole 128-byte runs (the largest stage row)
-constexpr int GROUP_M = 4;
+constexpr int BKB = kTileRowBytes;   // ... i.e. to whole 128-byte runs (the largest stage row)
 
 // A tile configuration: BM x BN tile, WM x WN waves, NSTAGE LDS buffers of SB bytes of K per
 // row (128: 64 bf16; 64: 32 bf16, twice the stages in the same LDS).
@@ -150,38 +144,6 @@ hipError_t launch_tiles_pad(int et, void* ws, int64_t rows, int nb, int64_t rows
                        ws, eb, (int64_t)0, count, nb, nb_p, nb_p - nb);
   }
   return hipGetLastError();
-}
-
-__device__ __forceinline__ void tile_coords(int bid, int tm, int tn, int& pm, int& pn) {
-  constexpr int GROUP_M = gemm::GROUP_M;
-  // XCD-contiguous numbering: workgroups bid, bid+8, ... run on one XCD
-  const int total = tm * tn;
-  int t = bid;
-  if ((total & 7) == 0) t = (bid & 7) * (total >> 3) + (bid >> 3);
-  const int width = GROUP_M * tn;
-  const int g = t / width;
-  const int first = g * GROUP_M;
-  const int gm = min(tm - first, GROUP_M);
-  const int r = t - g * width;
-  pm = first + r % gm;
-  pn = r / gm;
-}
-
-typedef __attribute__((address_space(3))) void lds_void;
-
-// LDS swizzle: chunk c of row r lives at chunk c ^ swz(r).  128-byte rows (8 chunks):
-// swz(r) = (r mod 8) ^ ((r / 8) mod 4), a function of r mod 32 only (every 32-row MFMA tile
-// starts at a multiple of 32); the 16-byte fragment reads of 32 consecutive rows at one
-// logical chunk then fall in distinct bank groups whether the LDS serves 8, 16 or 32 lanes
-// of a 128-bit read per cycle.  64-byte rows (4 chunks, four rows per 256-byte bank period):
-// swz(r) = (r / 4) mod 4, so that any 16 consecutive rows cover all 64 banks.
-template <int CH>
-__device__ __forceinline__ int swz(int r) {
-  if constexpr (CH == 8) {
-    return (r ^ ((r >> 3) & 3)) & 7;
-  } else {
-    return (r >> 2) & 3;
-  }
 }
 
 // kc: row length of both tiles in 16-byte chunks (a multiple of 8).  ET: int8 tiles and
@@ -378,16 +340,6 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
       }
 }
 
-// Both tile configurations pad M to 256; N is padded to 256 (a multiple of both BN).  Rows
-// are padded to 128 B: 64 bf16 / fp16, or 128 int8 (never more bytes than the 16-bit tiles).
-size_t decode_once_workspace(int64_t M, int64_t N, int64_t K) {
-  using namespace gemm;
-  const int64_t mp = (M + 255) / 256 * 256;
-  const int64_t np = (N + 255) / 256 * 256;
-  const int64_t kp = (K + BK - 1) / BK * BK;
-  return (size_t)((mp + np) * kp * 2);
-}
-
 template <class C, int ET>
 static void launch_gemm(const u32x4* wa, const u32x4* ww, int kc, int64_t mp, int64_t np,
                         const MatmulOperand& A, const MatmulOperand& W, float* c, int64_t ldc,
@@ -396,37 +348,6 @@ static void launch_gemm(const u32x4* wa, const u32x4* ww, int kc, int64_t mp, in
   hipLaunchKernelGGL((gemm_kernel<C, ET>), dim3((unsigned)(tm * tn)), dim3(C::NW * 64),
                      (size_t)C::NSTAGE * C::STAGE_BYTES, st, wa, ww, kc, tm, tn, A.scales,
                      W.scales, A.rows, W.rows, c, ldc, scale);
-}
-
-// Workspace layout of the decode-once path: A's tile (mp x nb_p blocks) then W's (np x nb_p),
-// rows padded to whole 128-byte stages.
-void decode_once_layout(int et, int64_t M, int64_t N, int64_t K, int64_t& w_offset,
-                        int64_t& rows_p, int& nb_p) {
-  using namespace gemm;
-  const int eb = et == ET_I8 ? 1 : 2;                 // bytes per element
-  const int64_t mp = (M + 255) / 256 * 256;
-  const int64_t kp = (K * eb + BKB - 1) / BKB * BKB / eb;
-  w_offset = mp * kp * eb;
-  rows_p = (N + 255) / 256 * 256;
-  nb_p = (int)(kp / 8);
-}
-
-TileTask tile_task(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void* ws) {
-  TileTask t;
-  t.codes = X.codes;
-  t.beta = X.beta;
-  t.rows = X.rows;
-  t.total = rows_p * nb_p;
-  t.ws = ws;
-  t.nb = nb;
-  t.nb_p = nb_p;
-  t.inv_nbp = 1.0f / (float)nb_p;
-  t.q = X.q;
-  t.m2q = X.m2q;
-  t.mtab = X.mtab;
-  t.dv = decoder_variant(X.decoder, X.q);
-  t.wgs = (int)tile_workgroups(t.total);
-  return t;
 }
 
 template <int ET>

@@ -116,6 +116,12 @@ hipError_t launch_matmul_decode_once(int stages, int et, const MatmulOperand& A,
                                      float scale, void* ws, hipStream_t st);
 hipError_t gemm_set_attributes();
 
+// No workspace (nq_matmul): each workgroup decodes its own rows' code words into LDS and
+// contracts them there (bf16 or fp16 tiles).
+hipError_t launch_matmul_fused(int et, const MatmulOperand& A, const MatmulOperand& W,
+                               int64_t K, float* c, int64_t ldc, float scale, hipStream_t st);
+hipError_t fused_set_attributes();
+
 // Hadamard rotation of rows (nq_rotate): columns 2^k or 28 * 2^k (2^k >= 8), at most this.
 constexpr int kRotateMaxCols = 32768;
 // m (1 or 28, 0 if unsupported) and p = n / m
@@ -137,6 +143,25 @@ hipError_t launch_beta_dp(const double* mse, const uint8_t* ov, int64_t n, int m
 
 // M at or below this uses the skinny kernel; above it, decode-once.
 constexpr int64_t kFusedMaxM = 64;
+
+// Rows of the product's decoded tiles are padded to whole runs of this many bytes (the
+// longest stage row of the decode-once GEMM): 64 bf16 / fp16 values or 128 int8.
+constexpr int kTileRowBytes = 128;
+
+// The tile decode (tiles_block) gives each thread this many blocks: one workgroup of 256
+// threads per 256 * kTilesPerThread blocks.
+constexpr int kTilesPerThread = 4;
+inline int64_t tile_workgroups(int64_t total) {
+  return (total + 256 * kTilesPerThread - 1) / (256 * kTilesPerThread);
+}
+
+// The beta DP's cost sums: a 64-ary tree over the samples; m (m + 1) / 2 transition costs
+// and m overload counts per tree node.
+constexpr int kBetaFan = 64;
+inline int64_t beta_cost_entries(int m) { return (int64_t)m * (m + 1) / 2 + m; }
+inline int64_t beta_level2_nodes(int64_t n) {
+  return (n + kBetaFan * kBetaFan - 1) / (kBetaFan * kBetaFan);
+}
 
 // Launch shape for grid_block: log2 of the lanes per row (-1: 256-block segments) and the
 // number of workgroups.

@@ -195,13 +195,6 @@ __global__ __launch_bounds__(NWV * 64) void skinny_kernel(const u32x4* __restric
   }
 }
 
-// Rows of the A tile are padded to 128 B (64 bf16 / fp16 or 128 int8) and to 16 rows.
-size_t skinny_workspace(int64_t M, int64_t K) {
-  const int64_t mp = (M + 15) / 16 * 16;
-  const int64_t kp = (K + 63) / 64 * 64;
-  return (size_t)(mp * kp * 2);
-}
-
 template <int ET>
 static hipError_t skinny_launch(const MatmulOperand& A, const MatmulOperand& W, const u32x4* ta,
                                 int kcb, int nb, float* c, int64_t ldc, float scale,

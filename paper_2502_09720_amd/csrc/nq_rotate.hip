@@ -67,18 +67,6 @@ __global__ __launch_bounds__(NT) void rotate_kernel(const T* __restrict__ x, int
   }
 }
 
-int rotation_split(int64_t n, int& p) {
-  for (int m : {1, 28}) {
-    if (n % m) continue;
-    const int64_t pp = n / m;
-    if (pp >= 8 && (pp & (pp - 1)) == 0 && n <= kRotateMaxCols) {
-      p = (int)pp;
-      return m;
-    }
-  }
-  return 0;
-}
-
 template <typename T>
 static hipError_t launch_t(const void* x, int64_t rows, int n, int64_t ld_x, float* y,
                            int64_t ld_y, hipStream_t st) {

@@ -6,9 +6,9 @@
 // Arithmetic (the paper leaves it open; fixed here so that results are reproducible):
 //   1. the fast Walsh-Hadamard transform along j in fp32: for h = 1, 2, 4, ..., every pair
 //      (i, i + h) with i & h = 0 becomes (a + b, a - b);
-//   2. for m = 28, H_28 = C kron H_2 + I_14 kron K_2 applied through that structure (rows
-//      i = 2b + r): u_2b = X_2b + X_2b+1, u_2b+1 = X_2b - X_2b+1; output 2c + s = sum over
-//      b != c, in increasing b, of C[b][c] u_2b+s, then + u_2c+1 (s = 0) or - u_2c (s = 1);
+//   2. for m = 28, output segment a = the sum over i = 0..27, in increasing i, of
+//      H_28[i][a] X_i (the plain product with the order-28 factor, one rounding per
+//      addition, starting from H_28[0][a] X_0);
 //   3. every entry times fl32(1 / sqrt(n)).
 // Within a stage the butterflies are independent, so any parallel order gives the same
 // numbers.
@@ -17,8 +17,8 @@
 // consecutive entries into registers and does the stages h = 1, 2, 4 there; the later stages
 // run four at a time: a thread takes 16 entries whose indices differ in four consecutive
 // bits, does those four stages in registers and writes them back (a barrier per four
-// stages).  The signs of the conference matrix behind H_28 are compile-time constants, so
-// each term of the mix is one add or subtract.
+// stages).  The signs of H_28 are compile-time constants, so each term of the mix is one
+// add or subtract.
 #pragma once
 
 #include "nq_device.hpp"
@@ -28,21 +28,29 @@ namespace nq {
 // Paley's second construction at q = 13 (q = 1 mod 4): chi the quadratic character mod 13,
 // the symmetric conference matrix C = [[0, 1^T], [1, Q]] with Q[i][j] = chi(j - i) (14 x 14,
 // zero diagonal), and H_28 = C kron [[1, 1], [1, -1]] + I_14 kron [[1, -1], [-1, -1]].
-// neg[c] has bit b set where C[b][c] = -1.
-struct C14Table {
-  uint32_t neg[14];
+// neg[a] has bit i set where H_28[i][a] = -1.
+struct H28Table {
+  uint32_t neg[28];
 };
-constexpr C14Table make_c14() {
-  C14Table t{};
+constexpr H28Table make_h28() {
+  H28Table t{};
   int chi[13] = {};
   for (int a = 1; a < 13; ++a) chi[a] = -1;
   for (int v = 1; v < 13; ++v) chi[(v * v) % 13] = 1;
-  for (int b = 1; b < 14; ++b)
-    for (int c = 1; c < 14; ++c)
-      if (b != c && chi[((c - 1) - (b - 1) + 13) % 13] < 0) t.neg[c] |= 1u << b;
+  int C[14][14] = {};
+  for (int b = 0; b < 14; ++b)
+    for (int c = 0; c < 14; ++c)
+      C[b][c] = b == c ? 0 : (b == 0 || c == 0) ? 1 : chi[((c - 1) - (b - 1) + 13) % 13];
+  const int H2[2][2] = {{1, 1}, {1, -1}}, K2[2][2] = {{1, -1}, {-1, -1}};
+  for (int i = 0; i < 28; ++i)
+    for (int a = 0; a < 28; ++a) {
+      const int b = i / 2, r = i % 2, c = a / 2, s = a % 2;
+      const int v = C[b][c] * H2[r][s] + (b == c ? K2[r][s] : 0);
+      if (v < 0) t.neg[a] |= 1u << i;
+    }
   return t;
 }
-constexpr C14Table kC14 = make_c14();
+constexpr H28Table kH28 = make_h28();
 
 template <typename T>
 __device__ __forceinline__ void load8(const T* __restrict__ p, float (&v)[8]);
@@ -133,33 +141,21 @@ __device__ __forceinline__ void fwht_pass_at(float* buf, int total, int lp, int 
   }
 }
 
-// The H_28 factor for column b (< p) of row r of buf, through its construction: H_2 on each
-// segment pair (u_2b = X_2b + X_2b+1, u_2b+1 = X_2b - X_2b+1), then output 2c + s is the sum
-// over b' != c, in increasing b', of C[b'][c] u_2b'+s, plus u_2c+1 (s = 0) or minus u_2c
-// (s = 1): 13 additions per output.  Entry k of the column is r n + k p + b = (28 r + k) p | b.
+// The H_28 factor for column b (< p) of row r of buf: output segment a is the sum over
+// i = 0..27, in increasing i, of H_28[i][a] X_i (27 additions per output).  Entry k of the
+// column is r n + k p + b = (28 r + k) p | b.
 __device__ __forceinline__ void mix28_column(float* buf, int b, int r, int p) {
   const int pb = lds_pos(b);
   auto at = [&](int k) -> float& { return buf[pb ^ lds_pos((28 * r + k) * p)]; };
-  float u[28];
+  float x[28];
 #pragma unroll
-  for (int i = 0; i < 14; ++i) {
-    const float x0 = at(2 * i), x1 = at(2 * i + 1);
-    u[2 * i] = x0 + x1;
-    u[2 * i + 1] = x0 - x1;
-  }
+  for (int i = 0; i < 28; ++i) x[i] = at(i);
 #pragma unroll
-  for (int c = 0; c < 14; ++c) {
+  for (int a = 0; a < 28; ++a) {
+    float acc = (kH28.neg[a] & 1u) != 0 ? -x[0] : x[0];
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      const int b0 = c == 0 ? 1 : 0;
-      float acc = ((kC14.neg[c] >> b0) & 1u) != 0 ? -u[2 * b0 + s] : u[2 * b0 + s];
-#pragma unroll
-      for (int bb = b0 + 1; bb < 14; ++bb) {
-        if (bb == c) continue;
-        acc = ((kC14.neg[c] >> bb) & 1u) != 0 ? acc - u[2 * bb + s] : acc + u[2 * bb + s];
-      }
-      at(2 * c + s) = s == 0 ? acc + u[2 * c + 1] : acc - u[2 * c];
-    }
+    for (int i = 1; i < 28; ++i) acc = ((kH28.neg[a] >> i) & 1u) != 0 ? acc - x[i] : acc + x[i];
+    at(a) = acc;
   }
 }
 

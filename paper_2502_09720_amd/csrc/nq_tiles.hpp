@@ -18,12 +18,6 @@ namespace nq {
 // blocks of it, thread t the blocks w TB + t + 256 i (i < TPB), so each load and store
 // instruction of a wave touches consecutive blocks.  Every thread issues the loads of all
 // its blocks before decoding any, which keeps TPB loads in flight per thread.
-constexpr int kTilesPerThread = 4;
-
-inline int64_t tile_workgroups(int64_t total) {
-  return (total + 256 * kTilesPerThread - 1) / (256 * kTilesPerThread);
-}
-
 template <int ET, int DV>
 __device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
                                             const uint32_t* __restrict__ beta, int64_t rows,

@@ -261,14 +261,45 @@ def test_beta_stats_empty_is_noop(lib):
 
 @pytest.mark.parametrize("case", [
     dict(m=0), dict(m=65), dict(k=0), dict(k=5), dict(n=-1), dict(mse=NULL), dict(chosen=NULL),
-    dict(loss=NULL),
+    dict(loss=NULL), dict(ws=NULL), dict(ws_bytes=8), dict(ws=ctypes.c_void_p(0x1004)),
 ])
 def test_beta_dp_rejects(lib, case):
-    args = dict(mse=FAKE, n=10, m=4, k=2, chosen=FAKE, loss=FAKE)
+    args = dict(mse=FAKE, n=10, m=4, k=2, chosen=FAKE, loss=FAKE, ws=FAKE, ws_bytes=1 << 20)
     args.update(case)
     st = lib.nq_beta_dp(args["mse"], FAKE, args["n"], args["m"], args["k"], args["chosen"],
-                        args["loss"], S)
+                        args["loss"], args["ws"], args["ws_bytes"], S)
     assert st == 1
+
+
+def test_beta_dp_workspace_size(lib):
+    f = lib.nq_beta_dp_workspace_size
+    f.argtypes = [ctypes.c_int64, ctypes.c_int32]
+    f.restype = ctypes.c_int64
+    q = lambda m: m * (m + 1) // 2 + m             # transition costs and overload counts
+    assert f(0, 4) == 2 * q(4) * 8                 # one level-2 node and one level-3 node
+    assert f(1 << 18, 50) == (64 + 1) * q(50) * 8  # 2^18 samples: 64 nodes of 4096
+    assert f(-1, 4) == -1 and f(10, 0) == -1 and f(10, 65) == -1
+
+
+# Every entry point that takes no workspace must not allocate: the library imports no
+# allocation routine from the HIP runtime at all.
+ALLOCATORS = re.compile(r"^(hip(Ext)?Malloc\w*|hipFree\w*|hipHostMalloc|hipHostAlloc|"
+                        r"hipMallocAsync|hipMallocFromPoolAsync|hipMemPool\w*|hipArrayCreate|"
+                        r"hipMalloc3D\w*)$")
+
+
+def test_library_imports_no_allocator(lib):
+    import shutil
+    import subprocess
+    import paper_2502_09720_amd as nq
+    nm = shutil.which("nm")
+    if nm is None:
+        pytest.skip("nm not available")
+    out = subprocess.run([nm, "-D", "--undefined-only", nq.library_path()], capture_output=True,
+                         text=True, check=True).stdout
+    imported = {line.split()[-1].split("@")[0] for line in out.splitlines() if line.strip()}
+    assert "hipLaunchKernel" in imported                       # the listing is the real one
+    assert not {name for name in imported if ALLOCATORS.match(name)}
 
 
 @pytest.mark.parametrize("case", [

@@ -1,10 +1,19 @@
 """GPU parity of the beta-set statistics and of Alg. 6 (App. F) against the oracle.
 
 Bar: the statistics are bit-exact (the overload flags are integers; each error is the same
-eight fp64 operations in the same order), and the dynamic program's chosen indices and its
-loss are bit-exact (its costs are summed in vector order on both sides, so every decision
-is taken on identical fp64 values).
+eight fp64 operations in the same order).  The dynamic program's costs are sums over the
+samples, which the oracle takes exactly (rounded once) and the kernel in a 64-ary tree of
+fp64 additions, so near-ties between beta sets may be broken differently.  The kernel's
+answer is therefore judged by what it must satisfy: the same solvability; a valid set
+(k increasing grid indices whose largest beta overloads no sample); its loss under Alg. 6's
+model, summed exactly by the oracle, equal to the oracle's optimum within the summation
+bound; and the loss it reports equal to that exact loss within the same bound.  The bound:
+in a 64-ary tree of depth d = ceil(log64 n) every non-negative term passes through at most
+63 d roundings, and the recurrence adds k costs, so every computed value is within
+(63 d + k) 2^-53 of the exact one, relatively; the test allows twice that.
 """
+
+import math
 
 import numpy as np
 import pytest
@@ -68,13 +77,39 @@ def test_beta_stats_parity(nq, case):
         assert got_over.any() and (~got_over).any()
 
 
+def _sum_bound(n, k):
+    d = 1
+    while 64 ** d < max(n, 1):
+        d += 1
+    return 2.0 * (63 * d + k) * 2.0 ** -53
+
+
+def _check_dp(chosen, loss, mse, over, k):
+    """The kernel's (chosen, loss) against the oracle's exact optimum (module docstring)."""
+    n, m = mse.shape
+    idx, best = beta_dp.dp_betas(mse, over, k)
+    got = chosen.cpu().numpy().tolist()
+    got_loss = float(loss.cpu())
+    if idx is None:
+        assert got == [-1] * k and got_loss == math.inf
+        return True
+    assert len(got) == k and all(0 <= i < m for i in got) and got == sorted(set(got)), got
+    assert not over[:, got[-1]].any(), "the largest chosen beta overloads a sample"
+    exact = beta_dp.dp_model_loss(mse, over, got)
+    eps = _sum_bound(n, k)
+    assert exact <= best * (1 + eps), (got, idx, exact, best)
+    assert abs(got_loss - exact) <= eps * exact, (got_loss, exact)
+    return got == idx
+
+
 @pytest.mark.parametrize("q,decoder,kind,solvable", [(16, "full", "normal", True),
                                                      (14, "m", "normal", True),
                                                      (7, "full", "grid", True),
                                                      (12, "full", "t4", False)])
 def test_beta_dp_parity(nq, q, decoder, kind, solvable):
-    """The chosen indices and the loss agree with the oracle; heavy-tailed samples overload
-    even at the largest grid beta, and then both report that no set exists."""
+    """The kernel's set is optimal under Alg. 6's model within the summation bound, and so
+    is its loss; heavy-tailed samples overload even at the largest grid beta, and then both
+    report that no set exists."""
     import torch
     v = _samples(10 + q, 4000, kind)
     betas = _grid(q)
@@ -83,17 +118,15 @@ def test_beta_dp_parity(nq, q, decoder, kind, solvable):
     for k in (1, 2, 4, 8):
         chosen, loss = nq.beta_dp(mse, over, k)
         torch.cuda.synchronize()
-        idx, val = beta_dp.dp_betas(want_mse, want_over, k)
-        assert (idx is not None) == solvable
-        want = idx if idx is not None else [-1] * k
-        assert chosen.cpu().numpy().tolist() == want, (k, chosen.cpu().numpy(), idx)
-        assert float(loss.cpu()) == val
+        assert (beta_dp.dp_betas(want_mse, want_over, k)[0] is not None) == solvable
+        _check_dp(chosen, loss, want_mse, want_over, k)
 
 
 def test_beta_dp_on_monotone_instances(nq):
-    """Synthetic statistics with monotone overload: the kernel's choice equals the oracle's
-    (and so, by the oracle's pin, the brute-force optimum)."""
+    """Synthetic statistics with monotone overload (where Alg. 6's model is the First-beta
+    error): the kernel's set is optimal within the summation bound."""
     import torch
+    same = total = 0
     for seed in range(5):
         rng = np.random.default_rng(100 + seed)
         n, m = int(rng.integers(50, 300)), int(rng.integers(5, 64))
@@ -104,9 +137,25 @@ def test_beta_dp_on_monotone_instances(nq):
         for k in sorted({1, 2, min(4, m), min(7, m)}):
             chosen, loss = nq.beta_dp(md, od, k)
             torch.cuda.synchronize()
-            idx, val = beta_dp.dp_betas(mse, over, k)
-            assert chosen.cpu().numpy().tolist() == idx
-            assert float(loss.cpu()) == val
+            same += _check_dp(chosen, loss, mse, over, k)
+            total += 1
+    print(f"kernel's set equal to the oracle's on {same} of {total} instances")
+
+
+def test_beta_dp_large_sample(nq):
+    """2^16 Gaussian samples, 50 grid betas: trees of depth 3 on the kernel's side (the
+    frontier's 2^18 calibration samples also take depth 3)."""
+    import torch
+    q = 14
+    v = _samples(77, 1 << 16, "normal")
+    betas = _grid(q)
+    mse, over = nq.beta_stats(torch.from_numpy(v).cuda(), betas, q)
+    want_mse, want_over = beta_dp.block_stats(v.astype(np.float64), betas, q)
+    assert np.array_equal(over.cpu().numpy().astype(bool), want_over)
+    for k in (2, 4):
+        chosen, loss = nq.beta_dp(mse, over, k)
+        torch.cuda.synchronize()
+        _check_dp(chosen, loss, want_mse, want_over, k)
 
 
 def test_beta_dp_every_beta_overloads(nq):
