@@ -153,6 +153,25 @@ nq_status nq_matmul_ex(const nq_params* pa, const uint32_t* a_codes, const uint3
                        int64_t N, int64_t K, float* c, int64_t ldc, void* workspace,
                        int64_t workspace_bytes, void* hip_stream);
 
+/* Bytes of the library's static device scratch used by nq_matmul_static (64 MiB per device). */
+#define NQ_STATIC_SCRATCH_BYTES (64u << 20)
+
+/* nq_matmul_ex for callers that cannot allocate device memory: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc.  The workspace is the library's own
+ * static device array of NQ_STATIC_SCRATCH_BYTES, which every device the library runs on holds
+ * until the process ends; the call allocates nothing (no hipMalloc, no allocating library
+ * routine).  Same arguments, checks and results (bit for bit) as nq_matmul_ex without the
+ * workspace arguments.  A product whose nq_matmul_workspace_size(M, N, K) exceeds
+ * NQ_STATIC_SCRATCH_BYTES is rejected with NQ_ERR_UNSUPPORTED before anything is launched
+ * (every product with M <= 64 fits, and so does 2048 x 4096 x 4096).  All calls on one device
+ * share its array: calls whose kernels overlap on a device (other streams, other host threads)
+ * race and must be serialized by the caller; consecutive calls on one stream are safe. */
+nq_status nq_matmul_static(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,
+                           const float* a_scales, int64_t M, const nq_params* pw,
+                           const uint32_t* w_codes, const uint32_t* w_beta,
+                           const float* w_scales, int64_t N, int64_t K, float* c, int64_t ldc,
+                           void* hip_stream);
+
 /* The two stages of nq_matmul_ex, for callers that time or schedule them separately, and
  * the exact int8 contraction.  stages is a bit mask:
  *   NQ_STAGE_DECODE    decodes the operands into the workspace (every block of A and, for

@@ -15,7 +15,8 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libnestquant.so")
 
 SOURCES = ["nq_api.cpp", "nq_encode.hip", "nq_decode.hip", "nq_matmul.hip", "nq_gemm.hip",
-           "nq_fused.hip", "nq_rotate.hip", "nq_beta.hip", "nq_host.cpp"]
+           "nq_fused.hip", "nq_rotate.hip", "nq_beta.hip", "nq_host.cpp",
+           "nq_static.hip"]
 
 # -ffp-contract=off: the exact-sign logic needs every product and sum rounded separately.
 # -packed-fp32-ops off: no v_pk_*_f32 in the generated code.

@@ -119,6 +119,16 @@ nq_status hip_status(hipError_t e, const char* who) {
 
 }  // namespace
 
+namespace nq {
+nq_status set_error(nq_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return s;
+}
+}  // namespace nq
+
 extern "C" {
 
 int64_t nq_codes_words(int64_t rows, int64_t cols) {
@@ -400,12 +410,14 @@ static hipError_t launch_product(int stages, int et, const nq_params* pa, const 
   return nq::launch_matmul_decode_once(stages, et, A, W, K, c, ldc, scale, workspace, st);
 }
 
-static nq_status matmul_stages(int32_t stages, const nq_params* pa, const uint32_t* a_codes,
-                               const uint32_t* a_beta, const float* a_scales, int64_t M,
-                               const nq_params* pw, const uint32_t* w_codes,
-                               const uint32_t* w_beta, const float* w_scales, int64_t N,
-                               int64_t K, float* c, int64_t ldc, void* workspace,
-                               int64_t workspace_bytes, void* hip_stream, const char* who) {
+}  // extern "C"
+
+nq_status nq::matmul_stages(int32_t stages, const nq_params* pa, const uint32_t* a_codes,
+                            const uint32_t* a_beta, const float* a_scales, int64_t M,
+                            const nq_params* pw, const uint32_t* w_codes,
+                            const uint32_t* w_beta, const float* w_scales, int64_t N, int64_t K,
+                            float* c, int64_t ldc, void* workspace, int64_t workspace_bytes,
+                            void* hip_stream, const char* who) {
   if ((stages & ~(NQ_STAGE_DECODE | NQ_STAGE_CONTRACT | NQ_CONTRACT_INT8)) != 0 ||
       (stages & (NQ_STAGE_DECODE | NQ_STAGE_CONTRACT)) == 0)
     return fail(NQ_ERR_INVALID_ARG,
@@ -427,12 +439,14 @@ static nq_status matmul_stages(int32_t stages, const nq_params* pa, const uint32
                     who);
 }
 
+extern "C" {
+
 nq_status nq_matmul_ex(const nq_params* pa, const uint32_t* a_codes, const uint32_t* a_beta,
                        const float* a_scales, int64_t M, const nq_params* pw,
                        const uint32_t* w_codes, const uint32_t* w_beta, const float* w_scales,
                        int64_t N, int64_t K, float* c, int64_t ldc, void* workspace,
                        int64_t workspace_bytes, void* hip_stream) {
-  return matmul_stages(NQ_STAGE_DECODE | NQ_STAGE_CONTRACT, pa, a_codes, a_beta, a_scales, M,
+  return nq::matmul_stages(NQ_STAGE_DECODE | NQ_STAGE_CONTRACT, pa, a_codes, a_beta, a_scales, M,
                        pw, w_codes, w_beta, w_scales, N, K, c, ldc, workspace, workspace_bytes,
                        hip_stream, "nq_matmul_ex");
 }
@@ -442,7 +456,7 @@ nq_status nq_matmul_stages(int32_t stages, const nq_params* pa, const uint32_t* 
                            const nq_params* pw, const uint32_t* w_codes, const uint32_t* w_beta,
                            const float* w_scales, int64_t N, int64_t K, float* c, int64_t ldc,
                            void* workspace, int64_t workspace_bytes, void* hip_stream) {
-  return matmul_stages(stages, pa, a_codes, a_beta, a_scales, M, pw, w_codes, w_beta, w_scales,
+  return nq::matmul_stages(stages, pa, a_codes, a_beta, a_scales, M, pw, w_codes, w_beta, w_scales,
                        N, K, c, ldc, workspace, workspace_bytes, hip_stream, "nq_matmul_stages");
 }
 

@@ -4,7 +4,19 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "nestquant.h"
+
 namespace nq {
+
+// The ABI layer's error reporting (nq_last_error) and its product with a workspace, for the
+// entry points defined outside nq_api.cpp.
+nq_status set_error(nq_status s, const char* fmt, ...);
+nq_status matmul_stages(int32_t stages, const nq_params* pa, const uint32_t* a_codes,
+                        const uint32_t* a_beta, const float* a_scales, int64_t M,
+                        const nq_params* pw, const uint32_t* w_codes, const uint32_t* w_beta,
+                        const float* w_scales, int64_t N, int64_t K, float* c, int64_t ldc,
+                        void* workspace, int64_t workspace_bytes, void* hip_stream,
+                        const char* who);
 
 // The tile decode of one coded operand (tiles_block) carried by wgs extra workgroups of
 // another launch; dv is decoder_variant of the operand.  wgs == 0: no task.
