@@ -30,6 +30,12 @@ INT8_PEAK_TOPS = 5000.0    # MI355X dense int8 MFMA
 METRIC = "nq_matmul TFLOP/s + nq_encode GB/s (q=14,k=4) at Llama-3-8B prefill shapes"
 
 
+def stats(ms):
+    """mean, median and min of per-call event times (ms)."""
+    a = np.asarray(ms, dtype=np.float64)
+    return {"mean_ms": float(a.mean()), "median_ms": float(np.median(a)), "min_ms": float(a.min())}
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -40,6 +46,8 @@ def parse():
     ap.add_argument("--workload", type=int, default=3, help="workload id (see workloads.py)")
     ap.add_argument("--q", type=int, default=None, help="override q (workload 4 has q=7 too)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kv", action="store_true",
+                    help="leave out the standalone encode / decode of the 2^28-entry KV matrix")
     ap.add_argument("--graph", action="store_true",
                     help="replay a captured HIP graph of the step instead of launching its "
                          "kernels directly (slower on these boxes)")
@@ -230,9 +238,10 @@ def copy_calibration(args):
                       "GBps": 2 * n / (ms * 1e-3) / 1e9}))
 
 
-def kv_roofline(args):
-    """nq_encode and nq_decode of X (2^21 x 128 fp16 N(0,1)) against 8 TB/s."""
-    import numpy as np
+def kv_measure(steps, warmup):
+    """nq_encode and nq_decode of X (2^21 x 128 fp16 N(0,1)) against 8 TB/s: per call the
+    algorithmic bytes (fp16 in or out, codes, beta words, scales) over its event time.  X is
+    512 MiB, twice the Infinity Cache, so every call streams it from HBM."""
     import torch
     import workloads
     import paper_2502_09720_amd as nq
@@ -255,19 +264,24 @@ def kv_roofline(args):
     for name, fn in (("nq_encode", lambda: nq.encode(X, q=q, k=k, out=(coded.codes, coded.beta,
                                                                         coded.scales))),
                      ("nq_decode", lambda: nq.decode(coded, torch.float16, out=out))):
-        for _ in range(args.warmup):
+        for _ in range(warmup):
             fn()
         torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(args.steps):
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+        for i in range(steps):
+            ev[i][0].record()
             fn()
-        e1.record()
+            ev[i][1].record()
         torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / args.steps
-        gbps = (io + coded_bytes) / (ms * 1e-3) / 1e9
-        res[name] = {"ms": ms, "GBps": gbps, "hbm_frac": gbps / HBM_PEAK_GBPS,
-                     "bytes": io + coded_bytes}
+        t = stats([e[0].elapsed_time(e[1]) for e in ev])
+        gbps = (io + coded_bytes) / (t["median_ms"] * 1e-3) / 1e9
+        res[name] = dict(t, GBps=gbps, hbm_frac=gbps / HBM_PEAK_GBPS, bytes=io + coded_bytes)
+    del X, out, coded
+    return res
+
+
+def kv_roofline(args):
+    res = kv_measure(args.steps, args.warmup)
     print(json.dumps({"metric": "nq_encode / nq_decode GB/s, 2^28 fp16 entries in rows of 128",
                       "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
                       "dtype": "f16", "data": "synthetic",
@@ -327,10 +341,11 @@ def cpu_baseline(cfg, q, k, flops_full, min_seconds=10.0, max_reps=5):
     _, W32, _ = workloads.operand(cfg, "W")
     base = nestquant.default_base(q, k)
     cw, tw, rw = nestquant.quantize_rows(W32, q, k)
-    times = []
+    times, enc_times = [], []
     while len(times) < max_reps and (len(times) < 2 or sum(times) < min_seconds):
         t0 = time.perf_counter()
         ca, ta, ra = nestquant.quantize_rows(A32, q, k)
+        enc_times.append(time.perf_counter() - t0)
         TA = nestquant.integer_tiles(ca, ta, q).astype(np.float64)
         TW = nestquant.integer_tiles(cw, tw, q).astype(np.float64)
         S = TA @ TW.T
@@ -338,17 +353,30 @@ def cpu_baseline(cfg, q, k, flops_full, min_seconds=10.0, max_reps=5):
         times.append(time.perf_counter() - t0)
         del TA, TW, S
     step = float(np.mean(times))
+    enc = float(np.mean(enc_times))
     return {
         "value": flops_full / step / 1e12,
         "unit": "TFLOP/s",
         "cores": int(blas_threads),
+        "os_cpu_count": os.cpu_count(),
+        "blas_threads": int(blas_threads),
+        "elementwise_threads": 1,
         "kind": "oracle",
         "sample": (f"the whole step of {M}x{N}x{K} (oracle encode of all {M} A rows, decode of "
                    f"A and of the {N} coded W rows, exact fp64 product), W coding excluded as "
                    f"on the GPU; {len(times)} repetitions, {sum(times):.1f} s measured; numpy "
                    f"elementwise on 1 thread, BLAS on {blas_threads}"),
         "seconds_per_step": step,
+        "seconds_per_step_min": float(np.min(times)),
+        "encode_A_seconds": enc,
+        "encode_A_GBps": enc_bytes_of(cfg) / enc / 1e9,
     }
+
+
+def enc_bytes_of(cfg):
+    import workloads
+    c = workloads.WORKLOADS[cfg]
+    return algorithmic(c["M"], c["N"], c["K"], 4 if c["dtype"] == "f32" else 2)[0]
 
 
 def main():
@@ -399,8 +427,15 @@ def main():
     nbuf = max(1, -(-512 * 2**20 // (M * K * in_bytes)) + 1)
     As = [A0] + [A0.clone() for _ in range(nbuf - 1)]
 
-    wc = nq.encode(W, q=q, k=k)
+    # W is coded once (a weight) and kept in enough copies (at least 16, over 512 MiB in all)
+    # that each step's read of the coded W comes from HBM, as for the layers of a model
+    wc0 = nq.encode(W, q=q, k=k)
+    del W
     nb, nbw = K // 8, (K // 8 + 15) // 16
+    coded_w_bytes = N * nb * 4 + N * nbw * 4 + N * 4
+    nw = max(16, -(-512 * 2**20 // coded_w_bytes))
+    wcs = [wc0] + [wc0._replace(codes=wc0.codes.clone(), beta=wc0.beta.clone(),
+                                scales=wc0.scales.clone()) for _ in range(nw - 1)]
     codes = torch.empty(M * nb, dtype=torch.int32, device=dev)
     beta = torch.empty(M * nbw, dtype=torch.int32, device=dev)
     scales = torch.empty(M, dtype=torch.float32, device=dev)
@@ -412,8 +447,8 @@ def main():
     def step(i, ev=None):
         if ev is not None:
             ev[0].record()
-        nq.encode_matmul(As[i % nbuf], wc, q=q, k=k, out=C, coded_out=(codes, beta, scales),
-                         workspace=ws)
+        nq.encode_matmul(As[i % nbuf], wcs[i % nw], q=q, k=k, out=C,
+                         coded_out=(codes, beta, scales), workspace=ws)
         if ev is not None:
             ev[1].record()
 
@@ -428,15 +463,15 @@ def main():
         for b in range(nbuf):
             g = torch.cuda.CUDAGraph()
             with torch.cuda.graph(g):
-                nq.encode_matmul(As[b], wc, q=q, k=k, out=C, coded_out=(codes, beta, scales),
-                                 workspace=ws)
+                nq.encode_matmul(As[b], wcs[b % nw], q=q, k=k, out=C,
+                                 coded_out=(codes, beta, scales), workspace=ws)
             graphs.append(g)
         torch.cuda.synchronize()
 
         def step(i, ev=None):
             if ev is not None:
                 ev[0].record()
-            graphs[i % nbuf].replay()
+            graphs[i % nbuf].replay()   # buffer b pairs with W copy b % nw
             if ev is not None:
                 ev[1].record()
 
@@ -456,7 +491,8 @@ def main():
     for i in range(args.steps):
         step(i, sev[i])
     torch.cuda.synchronize()
-    step_ev_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in sev]))
+    step_t = stats([e[0].elapsed_time(e[1]) for e in sev])
+    step_ev_ms = step_t["mean_ms"]
 
     # the same work as separate calls, with events between them on the kernels' stream:
     # nq_encode of A, then nq_matmul as its two stages (operand decode, contraction)
@@ -464,9 +500,9 @@ def main():
         ev[0].record()
         ac = nq.encode(As[i % nbuf], q=q, k=k, out=(codes, beta, scales))
         ev[1].record()
-        nq.matmul(ac, wc, out=C, workspace=ws, stages=nq.STAGE_DECODE)
+        nq.matmul(ac, wcs[i % nw], out=C, workspace=ws, stages=nq.STAGE_DECODE)
         ev[2].record()
-        nq.matmul(ac, wc, out=C, workspace=ws, stages=nq.STAGE_CONTRACT)
+        nq.matmul(ac, wcs[i % nw], out=C, workspace=ws, stages=nq.STAGE_CONTRACT)
         ev[3].record()
 
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
@@ -517,7 +553,7 @@ def main():
         try:
             rot["rotate_encode_ms"] = timed(lambda i: nq.encode(
                 As[i % nbuf], q=q, k=k, out=(codes, beta, scales), rotate=True))
-            wc_rot = nq.encode(nq.rotate(W), q=q, k=k)
+            wc_rot = nq.encode(nq.rotate(up(workloads.operand(cfg, "W")[0], dtw)), q=q, k=k)
             rot["nq_encode_matmul_rotated_ms"] = timed(lambda i: nq.encode_matmul(
                 As[i % nbuf], wc_rot, q=q, k=k, out=C, coded_out=(codes, beta, scales),
                 workspace=ws, rotate=True))
@@ -546,12 +582,12 @@ def main():
         ev8 = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
         ac = nq.encode(As[0], q=q, k=k, out=(codes, beta, scales))
         for i in range(args.warmup):
-            nq.matmul(ac, wc, out=C, workspace=ws, int8=True)
+            nq.matmul(ac, wcs[i % nw], out=C, workspace=ws, int8=True)
         for i in range(args.steps):
             ev8[i][0].record()
-            nq.matmul(ac, wc, out=C, workspace=ws, stages=nq.STAGE_DECODE, int8=True)
+            nq.matmul(ac, wcs[i % nw], out=C, workspace=ws, stages=nq.STAGE_DECODE, int8=True)
             ev8[i][1].record()
-            nq.matmul(ac, wc, out=C, workspace=ws, stages=nq.STAGE_CONTRACT, int8=True)
+            nq.matmul(ac, wcs[i % nw], out=C, workspace=ws, stages=nq.STAGE_CONTRACT, int8=True)
             ev8[i][2].record()
         torch.cuda.synchronize()
         d8 = float(np.mean([e[0].elapsed_time(e[1]) for e in ev8]))
@@ -561,9 +597,11 @@ def main():
               "contract_int8_frac": flops / (c8 * 1e-3) / 1e12 / INT8_PEAK_TOPS,
               "matmul_TOPs": flops / ((d8 + c8) * 1e-3) / 1e12}
 
-    enc_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
-    dec_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
-    con_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    enc_t = stats([e[0].elapsed_time(e[1]) for e in evs])
+    dec_t = stats([e[1].elapsed_time(e[2]) for e in evs])
+    con_t = stats([e[2].elapsed_time(e[3]) for e in evs])
+    mm_t = stats([e[1].elapsed_time(e[3]) for e in evs])
+    enc_ms, dec_ms, con_ms = enc_t["mean_ms"], dec_t["mean_ms"], con_t["mean_ms"]
     mm_ms = dec_ms + con_ms
     ms_per_step = wall * 1e3 / args.steps
 
@@ -586,6 +624,14 @@ def main():
                     "unit": "TFLOP/s", "frac": con_tflops / BF16_PEAK_TFLOPS,
                     "traffic": gemm_traffic(cfg, q),
                     "per_launch": f"2*M*N*K = {flops:.4g} flops"}
+    # the product from the codes as a whole (decode of both operands + contraction), the
+    # quantity the decode-GEMM target is stated for
+    decode_gemm = {"kernels": "operand decode + contraction (nq_matmul_stages)",
+                   "bound": "mfma", "achieved": mm_tflops, "peak": BF16_PEAK_TFLOPS,
+                   "unit": "TFLOP/s", "frac": mm_tflops / BF16_PEAK_TFLOPS,
+                   "median_frac": flops / (mm_t["median_ms"] * 1e-3) / 1e12 / BF16_PEAK_TFLOPS,
+                   "per_call": f"2*M*N*K = {flops:.4g} flops"}
+    kv = None if args.no_kv else kv_measure(min(args.steps, 50), min(args.warmup, 20))
 
     out = {
         "metric": METRIC,
@@ -608,23 +654,38 @@ def main():
         },
         "components": {
             "nq_encode_matmul_ms": step_ev_ms,
+            "nq_encode_matmul_stats": step_t,
             "nq_encode_ms": enc_ms,
+            "nq_encode_stats": enc_t,
             "nq_encode_GBps": enc_gbps,
             "nq_encode_hbm_frac": enc_gbps / HBM_PEAK_GBPS,
             "nq_encode_bytes": enc_bytes,
             "nq_matmul_ms": mm_ms,
+            "nq_matmul_stats": mm_t,
             "nq_matmul_decode_stage_ms": dec_ms,
+            "nq_matmul_decode_stage_stats": dec_t,
             "nq_matmul_contract_stage_ms": con_ms,
+            "nq_matmul_contract_stage_stats": con_t,
             "nq_matmul_TFLOPs": mm_tflops,
             "nq_matmul_mfma_frac": mm_tflops / BF16_PEAK_TFLOPS,
             "nq_matmul_bytes": mm_bytes,
             "a_rotation_buffers": nbuf,
+            "w_coded_copies": nw,
+            "kv_2e21x128_fp16": kv,
             "rate_bits_per_entry": float(np.log2(q) + np.log2(k) / 8),
             "nq_matmul_int8_variant": i8,
             "nq_rotate_A": rot,
             "nq_encode_A_opt_beta": opt,
         },
         "roofline": roofline,
+        "decode_gemm": decode_gemm,
+        "targets": {
+            "encode_hbm_frac": enc_gbps / HBM_PEAK_GBPS,
+            "decode_gemm_mfma_frac": mm_tflops / BF16_PEAK_TFLOPS,
+            "kv_encode_hbm_frac": kv["nq_encode"]["hbm_frac"] if kv else None,
+            "kv_decode_hbm_frac": kv["nq_decode"]["hbm_frac"] if kv else None,
+            "stated": "encode >= 0.60 of 8 TB/s; decode-GEMM >= 0.50 of 2.5 PFLOP/s",
+        },
         "cpu_baseline": None,
     }
     if not args.no_cpu_baseline:
