@@ -70,31 +70,29 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict_
     const int j = jj[i];
     const uint32_t t = (bw[i] >> (2 * (j & 15))) & 3u;
     const double sc = (double)sr[i] * pick_half_beta(a, t);
-    uint32_t X2p[4];
+    // X2 of the block: xs holds coordinates 0-3 and 4-7 as signed bytes (decode_word_b8),
+    // or as four times X2 for NestQuantM at q = 16 (decode_word_m16, coordinate 0 apart)
+    uint32_t xs[2];
+    int x0 = 0;
     if constexpr (DV == 2) {
-      // byte-SIMD NestQuantM at q = 16: repack the signed bytes as int16 pairs
-      uint32_t xa, xb;
-      int x0;
-      decode_word_m16(w[i], xa, xb, x0);
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const uint32_t x = u < 2 ? xa : xb;
-        const int lo = u == 0 ? x0 : ((int)(int8_t)(uint8_t)(x >> (16 * (u & 1))) >> 2);
-        const int hi = (int)(int8_t)(uint8_t)(x >> (16 * (u & 1) + 8)) >> 2;
-        X2p[u] = ((uint32_t)lo & 0xFFFFu) | ((uint32_t)hi << 16);
-      }
+      decode_word_m16(w[i], xs[0], xs[1], x0);
     } else {
-      decode_word_pk<DV == 1>(w[i], a.q, a.m2q, X2p);
+      uint32_t xa, xb;
+      decode_word_b8<DV == 1>(w[i], a.q, a.m2q, xa, xb);
+      xs[0] = xa ^ 0x80808080u;
+      xs[1] = xb ^ 0x80808080u;
     }
+    auto x2 = [&](int l) {
+      const int b = (int)(int8_t)(uint8_t)(xs[l >> 2] >> (8 * (l & 3)));
+      if constexpr (DV == 2) return l == 0 ? x0 : b >> 2;
+      return b;
+    };
     const int64_t orow = row0 + rr[i];
     if constexpr (OUT == 0) {
       // fp32: each value rounded once from its fp64 product
       float v[8];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        v[2 * u] = (float)(sc * (double)(int)(short)(X2p[u] & 0xFFFFu));
-        v[2 * u + 1] = (float)(sc * (double)((int)X2p[u] >> 16));
-      }
+      for (int l = 0; l < 8; ++l) v[l] = (float)(sc * (double)x2(l));
       f32x4* o = reinterpret_cast<f32x4*>((float*)out + orow * ld_out + 8 * j);
       const f32x4 lo = {v[0], v[1], v[2], v[3]};
       const f32x4 hi = {v[4], v[5], v[6], v[7]};
@@ -108,8 +106,8 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict_
       uint32_t pk[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const float lo = (float)(int)(short)(X2p[u] & 0xFFFFu) * s32;
-        const float hi = (float)((int)X2p[u] >> 16) * s32;
+        const float lo = (float)x2(2 * u) * s32;
+        const float hi = (float)x2(2 * u + 1) * s32;
         if constexpr (OUT == 1) {
           pk[u] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)lo) |
                   ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)hi) << 16);

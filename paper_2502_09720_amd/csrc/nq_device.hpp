@@ -254,6 +254,8 @@ __device__ __forceinline__ i16x2 as_i16x2(uint32_t v) { return __builtin_bit_cas
 __device__ __forceinline__ uint32_t bits32(u16x2 v) { return __builtin_bit_cast(uint32_t, v); }
 __device__ __forceinline__ uint32_t bits32(i16x2 v) { return __builtin_bit_cast(uint32_t, v); }
 
+#include "nq_b8.hpp"
+
 template <bool M = false>
 __device__ __forceinline__ void decode_word_pk(uint32_t w, int q, uint32_t m2q,
                                                uint32_t (&X2)[4]) {
@@ -450,7 +452,9 @@ __device__ __forceinline__ uint32_t pack16(float lo, float hi) {
 
 // m * X2 of one block as eight bf16 or fp16 values, coordinates 2i and 2i+1 in word i.
 // |X2| <= 2q <= 32, so the values are exact integers in bf16 while |m X2| <= 256 (m <= 4
-// for every q, the uniform beta grid) and in fp16 while |m X2| <= 2048 (m <= 64).
+// for every q, the uniform beta grid) and in fp16 while |m X2| <= 2048 (m <= 64).  DV 0 and 1
+// decode with decode_word_b8 (bytes biased by 128: value = m byte - 128 m, one exact fma);
+// DV 2 (NestQuantM at q = 16) with decode_word_m16.
 template <int DV = 0, bool F16 = false>
 __device__ __forceinline__ u32x4 decode_tile_16(uint32_t w, int m, int q, uint32_t m2q) {
   if constexpr (DV == 2) {
@@ -468,33 +472,33 @@ __device__ __forceinline__ u32x4 decode_tile_16(uint32_t w, int m, int q, uint32
     }
     return u32x4{o[0], o[1], o[2], o[3]};
   }
-  uint32_t X2p[4];
-  decode_word_pk<DV == 1>(w, q, m2q, X2p);
-  uint32_t o[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int lo = (int)(short)(X2p[i] & 0xFFFFu) * m;
-    const int hi = ((int)X2p[i] >> 16) * m;
-    o[i] = pack16<F16>((float)lo, (float)hi);
-  }
-  return u32x4{o[0], o[1], o[2], o[3]};
+  uint32_t xa, xb;
+  decode_word_b8<DV == 1>(w, q, m2q, xa, xb);
+  const float fm = (float)m, off = -128.0f * fm;
+  auto val = [&](uint32_t x, int b) {
+    return __builtin_fmaf((float)((x >> (8 * b)) & 0xFFu), fm, off);   // m (byte - 128), exact
+  };
+  return u32x4{pack16<F16>(val(xa, 0), val(xa, 1)), pack16<F16>(val(xa, 2), val(xa, 3)),
+               pack16<F16>(val(xb, 0), val(xb, 1)), pack16<F16>(val(xb, 2), val(xb, 3))};
 }
 
 // m * X2 of one block as eight int8 (exact when 2 q m <= 127: |X2| <= 2q), the
-// coordinates in byte order.  The 16-bit products keep their low byte, which is the
-// two's-complement int8 of a value in [-127, 127].
+// coordinates in byte order.  The signed bytes X2 are multiplied in 16-bit lanes (even and
+// odd bytes apart); each product keeps its low byte, the two's-complement int8 of a value
+// in [-127, 127].
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 template <int DV = 0>
 __device__ __forceinline__ u32x2 decode_tile_i8(uint32_t w, int m, int q, uint32_t m2q) {
-  uint32_t X2p[4];
-  decode_word_pk<DV != 0>(w, q, m2q, X2p);
-  const u16x2 tt = {(unsigned short)m, (unsigned short)m};
-  uint32_t p[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) p[i] = bits32(as_u16x2(X2p[i]) * tt);
-  // bytes 0 and 2 of two words: coordinates 4 i .. 4 i + 3
-  return u32x2{__builtin_amdgcn_perm(p[1], p[0], 0x06040200u),
-               __builtin_amdgcn_perm(p[3], p[2], 0x06040200u)};
+  uint32_t xa, xb;
+  decode_word_b8<DV != 0>(w, q, m2q, xa, xb);
+  const u16x2 mm = {(unsigned short)m, (unsigned short)m};
+  auto mul8 = [&](uint32_t x) {
+    const uint32_t s = x ^ 0x80808080u;                  // X2 as signed bytes
+    const uint32_t lo = bits32(as_u16x2(s & 0x00FF00FFu) * mm);
+    const uint32_t hi = bits32(as_u16x2((s >> 8) & 0x00FF00FFu) * mm);
+    return (lo & 0x00FF00FFu) | ((hi & 0x00FF00FFu) << 8);
+  };
+  return u32x2{mul8(xa), mul8(xb)};
 }
 
 // The decoder's residual X - q * 2 Q(X / 2q) for integer X >= 0 (< 2^11), Q = Alg. 5 or

@@ -240,16 +240,23 @@ __device__ __forceinline__ void tile_from_x2(const EncodeArgs& a, int64_t row, i
 
 __device__ __forceinline__ void tile_decoded(const EncodeArgs& a, int64_t row, int j, uint32_t word,
                                           int t) {
-  uint32_t X2p[4];
-  if (a.decoder) {
-    decode_word_pk<true>(word, a.q, a.m2q, X2p);
+  const int m = (int)((a.mtab >> (8 * t)) & 0xFFu);
+  const int64_t idx = row * a.nb_p + j;
+  const int dv = decoder_variant(a.decoder, a.q);
+  if (a.tile_et == ET_I8) {
+    reinterpret_cast<u32x2*>(a.tiles)[idx] =
+        dv == 0 ? decode_tile_i8<0>(word, m, a.q, a.m2q) : decode_tile_i8<1>(word, m, a.q, a.m2q);
+  } else if (a.tile_et == ET_F16) {
+    reinterpret_cast<u32x4*>(a.tiles)[idx] =
+        dv == 0 ? decode_tile_16<0, true>(word, m, a.q, a.m2q)
+                : (dv == 1 ? decode_tile_16<1, true>(word, m, a.q, a.m2q)
+                           : decode_tile_16<2, true>(word, m, a.q, a.m2q));
   } else {
-    decode_word_pk<false>(word, a.q, a.m2q, X2p);
+    reinterpret_cast<u32x4*>(a.tiles)[idx] =
+        dv == 0 ? decode_tile_16<0, false>(word, m, a.q, a.m2q)
+                : (dv == 1 ? decode_tile_16<1, false>(word, m, a.q, a.m2q)
+                           : decode_tile_16<2, false>(word, m, a.q, a.m2q));
   }
-  int X2[8];
-#pragma unroll
-  for (int l = 0; l < 8; ++l) X2[l] = (int)(short)((X2p[l >> 1] >> (16 * (l & 1))) & 0xFFFFu);
-  tile_from_x2(a, row, j, X2, t);
 }
 
 __device__ __forceinline__ void tile_zero(const EncodeArgs& a, int64_t row, int j) {

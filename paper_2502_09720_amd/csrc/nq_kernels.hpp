@@ -191,7 +191,7 @@ inline void grid_shape(int64_t rows, int nb, int& lg, int64_t& wgs) {
 
 // Decoder kernels by variant: 0 Alg. 2 / Alg. 5, 1 NestQuantM (packed 16-bit), 2 NestQuantM
 // at q = 16 (byte SIMD).
-inline int decoder_variant(int decoder, int q) { return decoder == 0 ? 0 : (q == 16 ? 2 : 1); }
+__host__ __device__ inline int decoder_variant(int decoder, int q) { return decoder == 0 ? 0 : (q == 16 ? 2 : 1); }
 
 inline uint32_t magic_2q(int q) { return (uint32_t)((65536 + 2 * q - 1) / (2 * q)); }
 inline uint32_t magic_q(int q) { return (uint32_t)(((1u << 20) + q - 1) / q); }

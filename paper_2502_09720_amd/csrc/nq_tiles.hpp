@@ -45,7 +45,6 @@ __device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
       (void*)(beta + row0 * nbw), (short)0, (int)(span * nbw * 4), 0x00020000);
   uint32_t w[TPB], bw[TPB];
   int jj[TPB];
-  bool pad[TPB];
 #pragma unroll
   for (int i = 0; i < TPB; ++i) {
     const int o = j0 + (int)threadIdx.x + 256 * i;
@@ -54,9 +53,9 @@ __device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
     if ((int)__umul24((uint32_t)(r + 1), (uint32_t)nb_p) <= o) ++r;
     const int j = o - (int)__umul24((uint32_t)r, (uint32_t)nb_p);
     jj[i] = j;
-    pad[i] = j >= nb || r >= span;
-    const uint32_t co = pad[i] ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nb) + (uint32_t)j);
-    const uint32_t bo = pad[i] ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nbw) + (uint32_t)(j >> 4));
+    const bool pad = j >= nb || r >= span;
+    const uint32_t co = pad ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nb) + (uint32_t)j);
+    const uint32_t bo = pad ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nbw) + (uint32_t)(j >> 4));
     w[i] = __builtin_amdgcn_raw_buffer_load_b32(rc, co, 0, 0);
     bw[i] = __builtin_amdgcn_raw_buffer_load_b32(rb, bo, 0, 0);
   }
@@ -71,7 +70,8 @@ __device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
     } else {
       out = decode_tile_16<DV, ET == ET_F16>(w[i], m, q, m2q);
     }
-    if (pad[i]) out = V{};                 // padding past the operand's rows or columns
+    // padding past the operand's rows or columns read the word 0 (out of range), which
+    // decodes to the zero point: its tile is zero
     reinterpret_cast<V*>(ws)[g] = out;
   }
 }
