@@ -19,10 +19,11 @@ __device__ __forceinline__ double pick_half_beta(const DecodeArgs& a, uint32_t t
 }
 
 // The blocks of the rows x nb matrix, in row-major order, are dealt to workgroups in runs
-// of 256 * kDecodePerThread; thread t of a workgroup takes blocks t + 256 i of its run, so
-// every load and store instruction of a wave touches consecutive blocks.  A thread issues
-// the loads of all its blocks (code word, beta word, row scale: buffer loads based at the
-// run's first row, out-of-range offsets reading 0) before decoding any.
+// of 256 * kDecodePerThread; thread t takes blocks t + 256 i of its run, so that every load
+// and store instruction of a wave touches consecutive blocks.  A thread splits its first
+// block's position into (row, column) once and steps it by 256 blocks for the next ones.
+// It issues the loads of all its blocks (code word, beta word, row scale: buffer loads based
+// at the run's first row, out-of-range offsets reading 0) before decoding any.
 template <int OUT, int DV>  // OUT: 0 = fp32, 1 = fp16, 2 = bf16; DV: decoder_variant
 __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict__ codes,
                                                      const uint32_t* __restrict__ beta,
@@ -45,16 +46,27 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict_
       (void*)(beta + row0 * nbw), (short)0, span * nbw * 4, 0x00020000);
   const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(scales + row0), (short)0, span * 4, 0x00020000);
+  // the first block's (row, column) from o < nb + 256 TPB <= 2^14 by a float division checked
+  // once in each direction; each further block is dr rows and dj columns on, with one carry
+  const int o = j0 + (int)threadIdx.x;
+  int r = (int)((float)o * inv_nb);
+  if ((int)__umul24((uint32_t)r, (uint32_t)nb) > o) --r;
+  if ((int)__umul24((uint32_t)(r + 1), (uint32_t)nb) <= o) ++r;
+  int j = o - (int)__umul24((uint32_t)r, (uint32_t)nb);
+  const int dr = 256 / nb, dj = 256 - dr * nb;
   uint32_t w[TPB], bw[TPB];
   float sr[TPB];
   int rr[TPB], jj[TPB];
 #pragma unroll
   for (int i = 0; i < TPB; ++i) {
-    const int o = j0 + (int)threadIdx.x + 256 * i;     // < nb + 256 TPB <= 2^14
-    int r = (int)((float)o * inv_nb);
-    if ((int)__umul24((uint32_t)r, (uint32_t)nb) > o) --r;
-    if ((int)__umul24((uint32_t)(r + 1), (uint32_t)nb) <= o) ++r;
-    const int j = o - (int)__umul24((uint32_t)r, (uint32_t)nb);
+    if (i > 0) {
+      j += dj;
+      r += dr;
+      if (j >= nb) {
+        j -= nb;
+        ++r;
+      }
+    }
     rr[i] = r;
     jj[i] = j;
     const uint32_t ok = g0 + (int)threadIdx.x + 256 * i < total ? 0u : OOB;

@@ -16,8 +16,10 @@ namespace nq {
 // bf16 or fp16 (16 B) per block, or 8 int8 (8 B) for the int8 contraction.  The workspace
 // is one flat array of rows_p * nb_p blocks; workgroup w covers TB = 256 * TPB consecutive
 // blocks of it, thread t the blocks w TB + t + 256 i (i < TPB), so each load and store
-// instruction of a wave touches consecutive blocks.  Every thread issues the loads of all
-// its blocks before decoding any, which keeps TPB loads in flight per thread.
+// instruction of a wave touches consecutive blocks.  A thread splits its first block's
+// position into (row, column) once and steps the split by 256 blocks for the next ones.
+// Every thread issues the loads of all its blocks before decoding any, which keeps TPB
+// loads in flight per thread.
 template <int ET, int DV>
 __device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
                                             const uint32_t* __restrict__ beta, int64_t rows,
@@ -30,9 +32,9 @@ __device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
   using V = typename std::conditional<I8, u32x2, u32x4>::type;
   const int64_t g0 = wg * (256 * TPB);
   // the workgroup's first block as (row0, j0); every other block is an offset
-  // o < nb_p + 256 TPB <= 2^14 past (row0, 0), split by a float division checked once in
-  // each direction.  Code and beta words are read through buffer resources based at row0
-  // (32-bit offsets; the range check makes rows past the operand read as zero).
+  // o < nb_p + 256 TPB <= 2^14 past (row0, 0).  Code and beta words are read through buffer
+  // resources based at row0 (32-bit offsets; the range check makes rows past the operand
+  // read as zero).
   const int64_t row0 = g0 / nb_p;
   const int j0 = (int)(g0 - row0 * nb_p);
   const int nbw = (nb + 15) >> 4;
@@ -43,15 +45,26 @@ __device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
       (void*)(codes + row0 * nb), (short)0, (int)(span * nb * 4), 0x00020000);
   const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(beta + row0 * nbw), (short)0, (int)(span * nbw * 4), 0x00020000);
+  // the first block's (row, column) by a float division checked once in each direction;
+  // each further block is 256 blocks on: dr rows and dj columns more, with one carry
+  const int o = j0 + (int)threadIdx.x;
+  int r = (int)((float)o * inv_nbp);
+  if ((int)__umul24((uint32_t)r, (uint32_t)nb_p) > o) --r;
+  if ((int)__umul24((uint32_t)(r + 1), (uint32_t)nb_p) <= o) ++r;
+  int j = o - (int)__umul24((uint32_t)r, (uint32_t)nb_p);
+  const int dr = 256 / nb_p, dj = 256 - dr * nb_p;
   uint32_t w[TPB], bw[TPB];
   int jj[TPB];
 #pragma unroll
   for (int i = 0; i < TPB; ++i) {
-    const int o = j0 + (int)threadIdx.x + 256 * i;
-    int r = (int)((float)o * inv_nbp);
-    if ((int)__umul24((uint32_t)r, (uint32_t)nb_p) > o) --r;
-    if ((int)__umul24((uint32_t)(r + 1), (uint32_t)nb_p) <= o) ++r;
-    const int j = o - (int)__umul24((uint32_t)r, (uint32_t)nb_p);
+    if (i > 0) {
+      j += dj;
+      r += dr;
+      if (j >= nb_p) {
+        j -= nb_p;
+        ++r;
+      }
+    }
     jj[i] = j;
     const bool pad = j >= nb || r >= span;
     const uint32_t co = pad ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nb) + (uint32_t)j);
