@@ -133,7 +133,8 @@ __device__ __forceinline__ void e8_point(const E8Cand& k, bool d8, int (&P)[8]) 
 __device__ __forceinline__ void nearest_e8(const float (&y)[8], int (&P)[8]) {
   E8Cand k;
   e8_candidates(y, k);
-  const bool d8 = fabsf(k.gap) >= 1.0e-5f ? k.gap < 0.0f : e8_gap_negative_exact(k);
+  bool d8 = k.gap < 0.0f;
+  if (__builtin_expect(fabsf(k.gap) < 1.0e-5f, 0)) d8 = e8_gap_negative_exact(k);
   e8_point(k, d8, P);
 }
 

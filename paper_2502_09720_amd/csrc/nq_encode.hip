@@ -482,8 +482,8 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_kernel(
 // nearest-point decision, and finishes it unless that decision was too close to call, or
 // the point's exact root bound says it overloads (start again at the next beta) or lies on
 // the cell boundary (the literal test decides).  Those slots (about 12-19% on Gaussian-like
-// and heavy-tailed rows) are queued, and phase 2 finishes them with every lane of the
-// workgroup busy.  With tiles, slots at the last beta whose point is not strictly inside
+// and heavy-tailed rows) are queued, and phase 2 finishes them in rounds of one beta each,
+// the slots still searching compacted after every round so that the lanes stay busy.  With tiles, slots at the last beta whose point is not strictly inside
 // the cell are queued too, so that phase 1 never runs the decoder (full decoder only).
 // Two-bit beta indices are staged in LDS and packed into words at the end.
 // ---------------------------------------------------------------------------------------
@@ -513,31 +513,19 @@ struct SlotMap {
   }
 };
 
-// Finish a block from a given first beta: loop until a point survives (or t = k).
-__device__ __forceinline__ void finish_block(const float (&v)[8], const float (&c)[4], int t,
-                                             const EncodeArgs& a, uint32_t& word, int& tsel,
-                                             int (&P)[8]) {
-  const bool m = a.decoder != 0;
-  const float mx = m ? 0.0f : root_bound_f(v);
-  const float two_q = (float)(2 * a.q);
-  for (;;) {
-    const float ct = pick4(c, t);
-    float y[8];
+// One evaluation of a queued block at beta t: its exact nearest point P, and whether the
+// search stops there (the last beta, or a point that does not overload).  The root bound of
+// x is not consulted: the integer root bound of P settles every point off the cell
+// boundary, and a point it cannot settle is decided by the literal test.
+__device__ __forceinline__ bool eval_block(const float (&v)[8], float ct, int t,
+                                           const EncodeArgs& a, int (&P)[8]) {
+  float y[8];
 #pragma unroll
-    for (int l = 0; l < 8; ++l) y[l] = v[l] * ct;
-    nearest_e8(y, P);
-    if (t == a.k - 1) break;
-    if (m) {
-      if (!overloaded_m(P, a.q, a.mq, a.m2q)) break;
-    } else {
-      const float u = 2.0f * ct * mx;
-      const bool sure = u + kRootMargin + u * 0x1p-12f < two_q;
-      if (sure || !overloaded(P, a.q, a.rq, a.mq, a.m2q)) break;
-    }
-    ++t;
-  }
-  tsel = t;
-  word = encode_codes(P, a.q, a.rq, a.mq);
+  for (int l = 0; l < 8; ++l) y[l] = v[l] * ct;
+  nearest_e8(y, P);
+  if (t == a.k - 1) return true;
+  return a.decoder ? !overloaded_m(P, a.q, a.mq, a.m2q)
+                   : !overloaded(P, a.q, a.rq, a.mq, a.m2q);
 }
 
 // Raw input of one block: 16 B for 16-bit types, 32 B for fp32.
@@ -619,7 +607,9 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
   static_assert(!ROT || SM::WGROW, "rotation in LDS needs one row per workgroup");
   __shared__ RawBlock<T> rawl[4][ROT ? 1 : SLOTS];
   __shared__ __attribute__((aligned(16))) float rbuf[ROT ? 8 * 4 * SLOTS : 1];
-  __shared__ uint32_t queue[4][SLOTS];
+  __shared__ uint16_t queue[4][SLOTS];
+  __shared__ uint16_t qnext[4 * SLOTS];
+  __shared__ int qcnt[4];
   __shared__ uint8_t tsl[4][SLOTS];
   __shared__ float crow[CW][RW][4];
   __shared__ __attribute__((aligned(16))) float chi[CW][RW][4];
@@ -657,6 +647,8 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
       unpack_raw<T>(rawl[w][sl], v);
     }
   };
+
+  if (threadIdx.x < 4) qcnt[threadIdx.x] = 0;   // phase 2's list lengths, one per round
 
   // ---- phase 0: stage the slots in LDS, row sums of squares ----
   if constexpr (ROT) {
@@ -805,7 +797,7 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
     const uint64_t mask = __ballot(queued);
     if (queued) {
       const int pos = qn + __popcll(mask & ((1ull << lane) - 1ull));
-      queue[wave][pos] = ((uint32_t)sl << 2) | (uint32_t)start;
+      queue[wave][pos] = (uint16_t)((sl << 2) | start);
     } else if (valid) {
       const uint32_t word = coded ? encode_codes(P, a.q, a.rq, a.mq) : 0u;
       codes_w[rw * nb + j] = word;
@@ -826,38 +818,74 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
   if (lane == 0) qlen[wave] = qn;
   __syncthreads();
 
-  // ---- phase 2: the queued slots of the whole workgroup, every lane busy ----
+  // ---- phase 2: the queued slots of the whole workgroup, one beta per round ----
+  // Round 0 takes the four wave queues; a slot whose point overloads goes on to the next
+  // beta in the next round, through a compacted list (entries w << 11 | sl << 2 | t), so
+  // that every round keeps its lanes busy instead of each wave looping until its slowest
+  // lane is done.  There are at most k rounds (t grows by one per round, and t = k - 1
+  // always stops).
   {
-    const int q0 = qlen[0], q1 = q0 + qlen[1], q2 = q1 + qlen[2], total = q2 + qlen[3];
-    for (int idx = threadIdx.x; idx < total; idx += 256) {
-      const int w = (idx >= q0) + (idx >= q1) + (idx >= q2);
-      const int off = w == 0 ? 0 : (w == 1 ? q0 : (w == 2 ? q1 : q2));
-      const uint32_t e = queue[w][idx - off];
-      const int sl = (int)(e >> 2), t = (int)(e & 3u);
-      const int i = sl >> 6, l = sl & 63;
-      const int rw = SM::row_w(i, l), j = SM::j(i, l, w);
-      const int64_t row = row_base(w) + rw;
-      const int c2 = SM::WGROW ? 0 : w;
-      float v[8], c[4];
-      slot_block(w, sl, v);
-#pragma unroll
-      for (int tt = 0; tt < 4; ++tt) c[tt] = crow[c2][rw][tt];
-      uint32_t word;
-      int tsel;
-      int P[8];
-      finish_block(v, c, t, a, word, tsel, P);
-      codes[row * nb + j] = word;
-      tsl[w][sl] = (uint8_t)tsel;
-      if constexpr (TILES) {
-        if (tsel < a.k - 1) {
-          tile_from_x2(a, row, j, P, tsel);
-        } else {
-          tile_decoded(a, row, j, word, tsel);
+    const int q0 = qlen[0], q1 = q0 + qlen[1], q2 = q1 + qlen[2];
+    int n = q2 + qlen[3];
+#pragma unroll 1
+    for (int rd = 0; n > 0; ++rd) {
+      uint16_t* __restrict__ out_q = (rd & 1) ? &queue[0][0] : qnext;
+      const uint16_t* __restrict__ in_q = (rd & 1) ? qnext : &queue[0][0];
+#pragma unroll 1
+      for (int base = 0; base < n; base += 256) {
+        const int idx = base + (int)threadIdx.x;
+        bool more = false;
+        uint32_t next = 0;
+        if (idx < n) {
+          int w, sl, t;
+          if (rd == 0) {
+            w = (idx >= q0) + (idx >= q1) + (idx >= q2);
+            const int off = w == 0 ? 0 : (w == 1 ? q0 : (w == 2 ? q1 : q2));
+            const uint32_t e = queue[w][idx - off];
+            sl = (int)(e >> 2);
+            t = (int)(e & 3u);
+          } else {
+            const uint32_t e = in_q[idx];
+            w = (int)(e >> 11);
+            sl = (int)((e >> 2) & 511u);
+            t = (int)(e & 3u);
+          }
+          const int i = sl >> 6, l = sl & 63;
+          const int rw = SM::row_w(i, l), j = SM::j(i, l, w);
+          const int64_t row = row_base(w) + rw;
+          const int c2 = SM::WGROW ? 0 : w;
+          float v[8];
+          slot_block(w, sl, v);
+          int P[8];
+          if (eval_block(v, crow[c2][rw][t], t, a, P)) {
+            const uint32_t word = encode_codes(P, a.q, a.rq, a.mq);
+            codes[row * nb + j] = word;
+            tsl[w][sl] = (uint8_t)t;
+            if constexpr (TILES) {
+              if (t < a.k - 1) {
+                tile_from_x2(a, row, j, P, t);
+              } else {
+                tile_decoded(a, row, j, word, t);
+              }
+            }
+          } else {
+            more = true;
+            next = ((uint32_t)w << 11) | ((uint32_t)sl << 2) | (uint32_t)(t + 1);
+          }
+        }
+        // wave-aggregated append to the next round's list
+        const uint64_t mask = __ballot(more);
+        if (mask != 0) {
+          int pos0 = 0;
+          if (lane == 0) pos0 = atomicAdd(&qcnt[rd], __popcll(mask));
+          pos0 = __shfl(pos0, 0, 64);
+          if (more) out_q[pos0 + __popcll(mask & ((1ull << lane) - 1ull))] = (uint16_t)next;
         }
       }
+      __syncthreads();
+      n = qcnt[rd];
     }
   }
-  __syncthreads();
 
   // ---- beta words: 16 two-bit indices of consecutive blocks (consecutive lanes) ----
 #pragma unroll
