@@ -476,15 +476,18 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_kernel(
 //   LANES == 64: row_w = 0, j = l + 64 i                              (one row per wave)
 //   LANES == 256: row_w = 0, j = 64 w + l + 256 i                     (one row per workgroup)
 // Phase 0 reads every slot from HBM once (all of a lane's loads in flight together), stages
-// it in LDS and forms the row sums of squares; then one lane per row turns its sum into the
-// scale r, the four multipliers c_t and the thresholds of skip_threshold.  Phase 1 evaluates
-// every slot at the first beta the root bound of x does not rule out, with the fp32
-// nearest-point decision, and finishes it unless that decision was too close to call, or
-// the point's exact root bound says it overloads (start again at the next beta) or lies on
-// the cell boundary (the literal test decides).  Those slots (about 12-19% on Gaussian-like
-// and heavy-tailed rows) are queued, and phase 2 finishes them in rounds of one beta each,
-// the slots still searching compacted after every round so that the lanes stay busy.  With tiles, slots at the last beta whose point is not strictly inside
-// the cell are queued too, so that phase 1 never runs the decoder (full decoder only).
+// it in LDS and forms the row sums of squares; then one lane per row (one per beta, with one
+// row per workgroup) turns its sum into the scale r, the multipliers c_t and the thresholds
+// of skip_threshold.  Phase 1 evaluates every slot at the first beta the root bound of x
+// does not rule out, with the fp32 nearest-point decision, and finishes it unless that
+// decision was too close to call or the point's exact root bound says it overloads (both
+// queued, at the same and at the next beta), or the point lies on the cell boundary (kept
+// with its point in a boundary list).  Phase 2a runs the literal test on the boundary list;
+// phase 2 then finishes the queued slots (about 8-10% on Gaussian-like and heavy-tailed
+// rows, plus the boundary points that overload) in rounds of one beta each, the slots still
+// searching compacted after every round so that the lanes stay busy.  With tiles, slots at
+// the last beta whose point is not strictly inside the cell are queued too, so that phase 1
+// never runs the decoder (full decoder only).
 // Two-bit beta indices are staged in LDS and packed into words at the end.
 // ---------------------------------------------------------------------------------------
 template <int LANES, int BPT>
@@ -578,20 +581,24 @@ __device__ __forceinline__ void unpack_raw<_Float16>(const RawBlock<_Float16>& r
 // nearest point P of y = fl32(c x), M(P) >= 2 M(y) - 2 sqrt(2) (covering radius 1, roots of
 // norm sqrt(2)) and M(y) = c M(x) up to relative rounding errors below 2^-19 (y, and the
 // fp32 evaluation of M), so M(x) > (2q + 2 sqrt(2) + 0.02) / (2 c (1 - 2^-12)) implies
-// M(P) > 2q.  Rounded up.
-// The NestQuantM counterpart for the statistic m_stat: (q + 2)(1 + 2^-12) / c, rounded up.
-__device__ __forceinline__ float skip_threshold_m(float c, int q) {
-  const double v = (double)(q + 2) * (1.0 + 0x1p-12) / (double)c;
+// M(P) > 2q.  With rb = fl64(r beta_t) and c = fl32(fl64(1 / rb)), 1 / c <= rb (1 + 2^-23),
+// so the threshold is evaluated from rb with products only (no division), inflated by 2^-20
+// to cover their roundings, and rounded up.  A threshold a little above the exact one only
+// lets a block try a beta that overloads; the search still ends at the same beta.
+// The NestQuantM counterpart for the statistic m_stat: (q + 2)(1 + 2^-12) / c.
+__device__ __forceinline__ float round_up_f32(double v) {
   float f = (float)v;
   if ((double)f < v) f = next_up(f);
   return f;
 }
 
-__device__ __forceinline__ float skip_threshold(float c, int q) {
-  const double v = (2.0 * q + (double)kRootMargin) / (2.0 * (double)c * (1.0 - 0x1p-12));
-  float f = (float)v;
-  if ((double)f < v) f = next_up(f);
-  return f;
+__device__ __forceinline__ float skip_threshold_m(double rb, int q) {
+  return round_up_f32((double)(q + 2) * (1.0 + 0x1p-12) * rb * (1.0 + 0x1p-20));
+}
+
+__device__ __forceinline__ float skip_threshold(double rb, int q) {
+  return round_up_f32((2.0 * q + (double)kRootMargin) * (0.5 / (1.0 - 0x1p-12)) * rb *
+                      (1.0 + 0x1p-20));
 }
 
 // ROT (one row per workgroup only): the row is first rotated in LDS (rotate_rows_lds, the
@@ -607,9 +614,13 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
   static_assert(!ROT || SM::WGROW, "rotation in LDS needs one row per workgroup");
   __shared__ RawBlock<T> rawl[4][ROT ? 1 : SLOTS];
   __shared__ __attribute__((aligned(16))) float rbuf[ROT ? 8 * 4 * SLOTS : 1];
+  constexpr int BQ = SLOTS < 256 ? SLOTS : 256;   // room in the boundary list
   __shared__ uint16_t queue[4][SLOTS];
   __shared__ uint16_t qnext[4 * SLOTS];
   __shared__ int qcnt[4];
+  __shared__ uint16_t bq[BQ];                      // boundary slots: w << 11 | sl << 2 | t
+  __shared__ uint2 bp[BQ];                         // and their points, as signed bytes
+  __shared__ int bcnt;
   __shared__ uint8_t tsl[4][SLOTS];
   __shared__ float crow[CW][RW][4];
   __shared__ __attribute__((aligned(16))) float chi[CW][RW][4];
@@ -649,6 +660,7 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
   };
 
   if (threadIdx.x < 4) qcnt[threadIdx.x] = 0;   // phase 2's list lengths, one per round
+  if (threadIdx.x == 0) bcnt = 0;
 
   // ---- phase 0: stage the slots in LDS, row sums of squares ----
   if constexpr (ROT) {
@@ -707,9 +719,12 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
   }
   __syncthreads();
 
-  // ---- row scales and multipliers: one lane per row ----
+  // ---- row scales and multipliers ----
+  // One lane per row; with one row per workgroup, lanes 0-3 of wave 0 all find the scale
+  // (the same instructions) and then each the multiplier and threshold of its own beta.
   {
-    const bool mine = SM::WGROW ? threadIdx.x == 0 : lane < RW;
+    constexpr int TL = SM::WGROW ? 4 : 1;   // lanes per row
+    const bool mine = SM::WGROW ? threadIdx.x < TL : lane < RW;
     const int rw = SM::WGROW ? 0 : lane;
     const int64_t row = row0 + rw;
     if (mine && row < rows) {
@@ -733,16 +748,23 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
         r = exact_rms(t, e, n, r);
       }
       const bool coded = (r > 0.0f) && isfinite(r);
-      rrow[cw][rw] = coded ? r : 0.0f;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const float c = coded ? (float)(1.0 / ((double)r * a.beta[t])) : 0.0f;
-        crow[cw][rw][t] = c;
+      auto set_beta = [&](int t) {
+        const double rb = (double)r * a.beta[t];
+        crow[cw][rw][t] = coded ? (float)(1.0 / rb) : 0.0f;
         chi[cw][rw][t] = (coded && t < a.k - 1)
-                             ? (a.decoder ? skip_threshold_m(c, a.q) : skip_threshold(c, a.q))
+                             ? (a.decoder ? skip_threshold_m(rb, a.q) : skip_threshold(rb, a.q))
                              : INFINITY;
+      };
+      if constexpr (SM::WGROW) {
+        set_beta((int)threadIdx.x);
+      } else {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) set_beta(t);
       }
-      scales[row] = r;
+      if (SM::WGROW ? threadIdx.x == 0 : true) {
+        rrow[cw][rw] = coded ? r : 0.0f;
+        scales[row] = r;
+      }
     }
   }
   __syncthreads();
@@ -757,7 +779,7 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
     const int64_t row = row0 + rw;
     const bool valid = row < rows && j < nb;
     const bool coded = valid && rrow[cw][rw] != 0.0f;
-    bool queued = false;
+    bool queued = false, bnd = false;
     int start = 0, t0 = 0;
     int P[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     if (coded) {
@@ -782,9 +804,11 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
           }
         } else {
           const int M = e8_root_bound(P);
-          if (M >= 2 * a.q) {          // overloads (>), or on the boundary (=): decide later
+          if (M > 2 * a.q) {           // overloads: the next beta, later
             queued = true;
-            start = M > 2 * a.q ? t0 + 1 : t0;
+            start = t0 + 1;
+          } else if (M == 2 * a.q) {   // on the boundary: the literal test decides, later
+            bnd = true;
           }
         }
       } else if (TILES && !a.decoder && e8_root_bound(P) >= 2 * a.q) {
@@ -794,11 +818,38 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
         start = t0;
       }
     }
+    // boundary points go to the boundary list with P (|P_l| <= 2q), while it has room, and
+    // to the queue at the same beta otherwise
+    const uint64_t lanes_below = (1ull << lane) - 1ull;
+    bool listed = false;
+    const uint64_t bmask = __ballot(bnd);
+    if (bmask != 0) {
+      int b0 = 0;
+      if (lane == 0) b0 = atomicAdd(&bcnt, __popcll(bmask));
+      b0 = __shfl(b0, 0, 64);
+      if (bnd) {
+        const int bi = b0 + __popcll(bmask & lanes_below);
+        if (bi < BQ) {
+          listed = true;
+          bq[bi] = (uint16_t)((wave << 11) | (sl << 2) | t0);
+          uint32_t lo = 0, hi = 0;
+#pragma unroll
+          for (int l = 0; l < 4; ++l) {
+            lo |= ((uint32_t)P[l] & 0xFFu) << (8 * l);
+            hi |= ((uint32_t)P[4 + l] & 0xFFu) << (8 * l);
+          }
+          bp[bi] = uint2{lo, hi};
+        } else {
+          queued = true;
+          start = t0;
+        }
+      }
+    }
     const uint64_t mask = __ballot(queued);
     if (queued) {
-      const int pos = qn + __popcll(mask & ((1ull << lane) - 1ull));
+      const int pos = qn + __popcll(mask & lanes_below);
       queue[wave][pos] = (uint16_t)((sl << 2) | start);
-    } else if (valid) {
+    } else if (valid && !listed) {
       const uint32_t word = coded ? encode_codes(P, a.q, a.rq, a.mq) : 0u;
       codes_w[rw * nb + j] = word;
       tsl[wave][sl] = (uint8_t)t0;
@@ -817,6 +868,39 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
   }
   if (lane == 0) qlen[wave] = qn;
   __syncthreads();
+
+  // ---- phase 2a: the boundary list, where P is known: the literal test alone ----
+  // A point that passes is coded at its beta; the others join their wave's queue at the
+  // next beta (each slot is in one list only, so the queues have room).
+  {
+    const int nbq = min(bcnt, BQ);
+    if (nbq > 0) {
+      for (int idx = threadIdx.x; idx < nbq; idx += 256) {
+        const uint32_t e = bq[idx];
+        const int w = (int)(e >> 11), sl = (int)((e >> 2) & 511u), t = (int)(e & 3u);
+        const uint2 pb = bp[idx];
+        int P[8];
+#pragma unroll
+        for (int l = 0; l < 4; ++l) {
+          P[l] = (int)(int8_t)(uint8_t)(pb.x >> (8 * l));
+          P[4 + l] = (int)(int8_t)(uint8_t)(pb.y >> (8 * l));
+        }
+        if (!boundary_overloaded(P, a.q, a.mq, a.m2q)) {
+          const int i = sl >> 6, l = sl & 63;
+          const int rw = SM::row_w(i, l), j = SM::j(i, l, w);
+          const int64_t row = row_base(w) + rw;
+          const uint32_t word = encode_codes(P, a.q, a.rq, a.mq);
+          codes[row * nb + j] = word;
+          tsl[w][sl] = (uint8_t)t;
+          if constexpr (TILES) tile_from_x2(a, row, j, P, t);
+        } else {
+          const int pos = atomicAdd(&qlen[w], 1);
+          queue[w][pos] = (uint16_t)((sl << 2) | (t + 1));
+        }
+      }
+      __syncthreads();
+    }
+  }
 
   // ---- phase 2: the queued slots of the whole workgroup, one beta per round ----
   // Round 0 takes the four wave queues; a slot whose point overloads goes on to the next
