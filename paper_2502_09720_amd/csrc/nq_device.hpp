@@ -66,7 +66,7 @@ __device__ __forceinline__ int exact_sign_sum(const double (&t)[N]) {
 struct E8Cand {
   int d[8], g[8];
   float e[8];
-  int p, r, odd1, odd2;
+  int odd1, odd2;
   float ep, er, gap;
 };
 
@@ -80,29 +80,20 @@ __device__ __forceinline__ void e8_candidates(const float (&y)[8], E8Cand& k) {
   }
   const int sum_d = ((k.d[0] + k.d[1]) + (k.d[2] + k.d[3])) + ((k.d[4] + k.d[5]) + (k.d[6] + k.d[7]));
   const int sum_g = ((k.g[0] + k.g[1]) + (k.g[2] + k.g[3])) + ((k.g[4] + k.g[5]) + (k.g[6] + k.g[7]));
-  int p = 0, r = 0;
-  float ep = k.e[0], er = k.e[0];
-#pragma unroll
-  for (int l = 1; l < 8; ++l) {
-    const bool up = k.e[l] > ep;    // strict: the lowest index wins ties
-    const bool dn = k.e[l] < er;
-    p = up ? l : p;
-    ep = up ? k.e[l] : ep;
-    r = dn ? l : r;
-    er = dn ? k.e[l] : er;
-  }
-  k.p = p;
-  k.r = r;
-  k.ep = ep;
-  k.er = er;
+  // max e and min e (the coordinates that hold them are found in e8_point, for the one
+  // candidate that is kept)
+  k.ep = fmaxf(fmaxf(fmaxf(k.e[0], k.e[1]), fmaxf(k.e[2], k.e[3])),
+               fmaxf(fmaxf(k.e[4], k.e[5]), fmaxf(k.e[6], k.e[7])));
+  k.er = fminf(fminf(fminf(k.e[0], k.e[1]), fminf(k.e[2], k.e[3])),
+               fminf(fminf(k.e[4], k.e[5]), fminf(k.e[6], k.e[7])));
   k.odd1 = (sum_d + sum_g) & 1;
   k.odd2 = sum_d & 1;
   float se = k.e[0];
 #pragma unroll
   for (int l = 1; l < 8; ++l) se = se + k.e[l];
   float gap = se - 2.0f;
-  if (k.odd1) gap = gap + (1.0f - 2.0f * ep);
-  if (k.odd2) gap = gap - 2.0f * er;
+  if (k.odd1) gap = gap + (1.0f - 2.0f * k.ep);
+  if (k.odd2) gap = gap - 2.0f * k.er;
   k.gap = gap;
 }
 
@@ -122,7 +113,13 @@ __device__ __forceinline__ void e8_point(const E8Cand& k, bool d8, int (&P)[8]) 
   // delta for g = 0 / g = 1, off and on the fixed coordinate
   const int a_g0 = d8 ? 0 : 1, a_g1 = d8 ? 2 : 1;
   const int b_g0 = d8 ? 2 : -1, b_g1 = d8 ? 0 : 3;
-  const int fix = d8 ? (k.odd1 ? k.p : 8) : (k.odd2 ? k.r : 8);
+  // the fixed coordinate: the lowest index holding max e (D8) or min e (D8+1/2), if that
+  // candidate's parity needs a fix
+  const float target = d8 ? k.ep : k.er;
+  int idx = 7;
+#pragma unroll
+  for (int l = 6; l >= 0; --l) idx = (k.e[l] == target) ? l : idx;
+  const int fix = (d8 ? k.odd1 : k.odd2) ? idx : 8;
 #pragma unroll
   for (int l = 0; l < 8; ++l) {
     const int delta = (l == fix) ? (k.g[l] ? b_g1 : b_g0) : (k.g[l] ? a_g1 : a_g0);
@@ -150,8 +147,8 @@ __device__ __forceinline__ bool nearest_e8_fast(const float (&y)[8], int (&P)[8]
 // max over the 240 roots lambda of E8 of <P, lambda> for P in 2E8 units:
 // max( |P|_(1) + |P|_(2),  (sum |P_i| - 2 [odd number of negative P_i] min |P_i|) / 2 ).
 // P lies strictly inside the cell q V of q 2E8 iff the bound is < 2q, strictly outside iff
-// it is > 2q; equality is the cell boundary.
-__device__ __forceinline__ int e8_root_bound(const int (&P)[8]) {
+// it is > 2q; equality is the cell boundary.  amax = |P|_(1) comes with it.
+__device__ __forceinline__ int e8_root_bound(const int (&P)[8], int& amax) {
   int a[8];
 #pragma unroll
   for (int l = 0; l < 8; ++l) a[l] = abs(P[l]);
@@ -164,7 +161,13 @@ __device__ __forceinline__ int e8_root_bound(const int (&P)[8]) {
   const int sa = ((a[0] + a[1]) + (a[2] + a[3])) + ((a[4] + a[5]) + (a[6] + a[7]));
   const int mn = min(min(min(a[0], a[1]), min(a[2], a[3])), min(min(a[4], a[5]), min(a[6], a[7])));
   const int neg = (int)(((uint32_t)(P[0] ^ P[1] ^ P[2] ^ P[3] ^ P[4] ^ P[5] ^ P[6] ^ P[7])) >> 31);
+  amax = m1;
   return max(m1 + m2, (sa - 2 * neg * mn) >> 1);
+}
+
+__device__ __forceinline__ int e8_root_bound(const int (&P)[8]) {
+  int amax;
+  return e8_root_bound(P, amax);
 }
 
 // Root bound of a real 8-vector: max over the 240 roots lambda of <x, lambda>.  For the
@@ -202,7 +205,9 @@ __device__ __forceinline__ int mod_q_general(int v, int q, float rq) {
 // Fast path (|P_i| < 512, always true for points that do not overload, |P_i| <= 2q): add a
 // bias of 1024 q to make v non-negative and divide with a 24-bit multiply,
 // floor(u / q) = (u * mq) >> 20 with mq = ceil(2^20 / q), exact for u < 2^20 / q.
-__device__ __forceinline__ uint32_t encode_codes(const int (&P)[8], int q, float rq, uint32_t mq) {
+// encode_codes_amax takes max |P_i| when the caller already has it.
+__device__ __forceinline__ uint32_t encode_codes_amax(const int (&P)[8], int q, float rq,
+                                                      uint32_t mq, int amax) {
   int v[8];
   v[0] = P[0];
   v[2] = (P[1] - P[0]) >> 1;
@@ -212,11 +217,8 @@ __device__ __forceinline__ uint32_t encode_codes(const int (&P)[8], int q, float
   v[5] = (P[6] - P[0]) >> 1;
   v[7] = (P[7] - P[0]) >> 1;
   v[1] = (5 * P[0] - P[1] - P[2] - P[3] + P[4] - P[5] - P[6] - P[7]) >> 2;
-  int big = 0;
-#pragma unroll
-  for (int l = 0; l < 8; ++l) big |= abs(P[l]);
   uint32_t w = 0;
-  if (big < 512) {
+  if (amax < 512) {
     // |v| <= 3 * 511 < 1024 q, so u = v + 1024 q lies in [0, 2048 q) and 2048 q < 2^20 / q
     const int bias = q << 10;
 #pragma unroll
@@ -230,6 +232,13 @@ __device__ __forceinline__ uint32_t encode_codes(const int (&P)[8], int q, float
     for (int l = 0; l < 8; ++l) w |= (uint32_t)mod_q_general(v[l], q, rq) << (4 * l);
   }
   return w;
+}
+
+__device__ __forceinline__ uint32_t encode_codes(const int (&P)[8], int q, float rq, uint32_t mq) {
+  int big = 0;
+#pragma unroll
+  for (int l = 0; l < 8; ++l) big |= abs(P[l]);
+  return encode_codes_amax(P, q, rq, mq, big);
 }
 
 // ---------------------------------------------------------------------------------------

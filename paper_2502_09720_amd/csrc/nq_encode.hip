@@ -780,7 +780,7 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
     const bool valid = row < rows && j < nb;
     const bool coded = valid && rrow[cw][rw] != 0.0f;
     bool queued = false, bnd = false;
-    int start = 0, t0 = 0;
+    int start = 0, t0 = 0, amax = 0;
     int P[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     if (coded) {
       float v[8];
@@ -796,26 +796,27 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
       if (!nearest_e8_fast(y, P)) {
         queued = true;                 // decision too close for fp32: redo exactly
         start = t0;
-      } else if (t0 < a.k - 1) {
-        if (a.decoder) {
-          if (overloaded_m(P, a.q, a.mq, a.m2q)) {   // NestQuantM: its decoder decides
-            queued = true;
-            start = t0 + 1;
-          }
-        } else {
-          const int M = e8_root_bound(P);
+      } else if (a.decoder) {
+        amax = 1 << 30;                // not known: encode_codes finds it
+        if (t0 < a.k - 1 && overloaded_m(P, a.q, a.mq, a.m2q)) {   // its decoder decides
+          queued = true;
+          start = t0 + 1;
+        }
+      } else {
+        const int M = e8_root_bound(P, amax);
+        if (t0 < a.k - 1) {
           if (M > 2 * a.q) {           // overloads: the next beta, later
             queued = true;
             start = t0 + 1;
           } else if (M == 2 * a.q) {   // on the boundary: the literal test decides, later
             bnd = true;
           }
+        } else if (TILES && M >= 2 * a.q) {
+          // the last beta, where a point may overload: only a point strictly inside the
+          // cell is its own decode; the others take the decoder's tile in phase 2
+          queued = true;
+          start = t0;
         }
-      } else if (TILES && !a.decoder && e8_root_bound(P) >= 2 * a.q) {
-        // the last beta, where a point may overload: only a point strictly inside the cell
-        // is its own decode; the others take the decoder's tile in phase 2
-        queued = true;
-        start = t0;
       }
     }
     // boundary points go to the boundary list with P (|P_l| <= 2q), while it has room, and
@@ -850,7 +851,11 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
       const int pos = qn + __popcll(mask & lanes_below);
       queue[wave][pos] = (uint16_t)((sl << 2) | start);
     } else if (valid && !listed) {
-      const uint32_t word = coded ? encode_codes(P, a.q, a.rq, a.mq) : 0u;
+      uint32_t word = 0u;
+      if (coded) {
+        word = amax < (1 << 30) ? encode_codes_amax(P, a.q, a.rq, a.mq, amax)
+                                : encode_codes(P, a.q, a.rq, a.mq);
+      }
       codes_w[rw * nb + j] = word;
       tsl[wave][sl] = (uint8_t)t0;
       if constexpr (TILES) {
@@ -889,7 +894,7 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
           const int i = sl >> 6, l = sl & 63;
           const int rw = SM::row_w(i, l), j = SM::j(i, l, w);
           const int64_t row = row_base(w) + rw;
-          const uint32_t word = encode_codes(P, a.q, a.rq, a.mq);
+          const uint32_t word = encode_codes_amax(P, a.q, a.rq, a.mq, 2 * a.q);  // |P_l| <= 2q
           codes[row * nb + j] = word;
           tsl[w][sl] = (uint8_t)t;
           if constexpr (TILES) tile_from_x2(a, row, j, P, t);
