@@ -833,13 +833,12 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
         if (bi < BQ) {
           listed = true;
           bq[bi] = (uint16_t)((wave << 11) | (sl << 2) | t0);
-          uint32_t lo = 0, hi = 0;
-#pragma unroll
-          for (int l = 0; l < 4; ++l) {
-            lo |= ((uint32_t)P[l] & 0xFFu) << (8 * l);
-            hi |= ((uint32_t)P[4 + l] & 0xFFu) << (8 * l);
-          }
-          bp[bi] = uint2{lo, hi};
+          // low bytes of P_0..P_3 and P_4..P_7 (byte selects 0 and 4 of each pair; 12 = zero)
+          auto pack4 = [](int p0, int p1, int p2, int p3) {
+            return __builtin_amdgcn_perm((uint32_t)p1, (uint32_t)p0, 0x0C0C0400u) |
+                   __builtin_amdgcn_perm((uint32_t)p3, (uint32_t)p2, 0x04000C0Cu);
+          };
+          bp[bi] = uint2{pack4(P[0], P[1], P[2], P[3]), pack4(P[4], P[5], P[6], P[7])};
         } else {
           queued = true;
           start = t0;
