@@ -469,12 +469,14 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_kernel(
 // ---------------------------------------------------------------------------------------
 // Slot-compacted encoder (rows of up to 2048 blocks).
 //
-// A workgroup of four waves owns 256 * BPT blocks ("slots"): slot s = 64 i + l of wave w is
+// A workgroup of four waves (two with LANES = 128) owns 64 * BPT blocks per wave ("slots"):
+// slot s = 64 i + l of wave w is
 // block j of row row_w, with
 //   LANES <  64: row_w = i * (64 / LANES) + l / LANES, j = l % LANES  (a row per lane group
 //                and pass; 64 / LANES * BPT rows per wave)
 //   LANES == 64: row_w = 0, j = l + 64 i                              (one row per wave)
-//   LANES == 256: row_w = 0, j = 64 w + l + 256 i                     (one row per workgroup)
+//   LANES >  64: row_w = 0, j = 64 w + l + LANES i                   (one row per workgroup
+//                of LANES / 64 waves)
 // Phase 0 reads every slot from HBM once (all of a lane's loads in flight together), stages
 // it in LDS and forms the row sums of squares; then one lane per row (one per beta, with one
 // row per workgroup) turns its sum into the scale r, the multipliers c_t and the thresholds
@@ -604,29 +606,31 @@ __device__ __forceinline__ float skip_threshold(double rb, int q) {
 // ROT (one row per workgroup only): the row is first rotated in LDS (rotate_rows_lds, the
 // arithmetic of nq_rotate) and the encoder reads its blocks from there, times a.rot_s.
 template <typename T, int LANES, int BPT, bool TILES, bool ROT>
-__global__ __launch_bounds__(256) void encode_wave_kernel(
+__global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_wave_kernel(
     const T* __restrict__ x, int64_t rows, int cols, int64_t ld_x, EncodeArgs a,
     uint32_t* __restrict__ codes, uint32_t* __restrict__ beta, float* __restrict__ scales) {
   using SM = SlotMap<LANES, BPT>;
   constexpr int SLOTS = SM::SLOTS;
   constexpr int RW = SM::ROWS_PER_WAVE;
   constexpr int CW = SM::WGROW ? 1 : 4;          // row tables: per wave, or one per workgroup
-  static_assert(!ROT || SM::WGROW, "rotation in LDS needs one row per workgroup");
-  __shared__ RawBlock<T> rawl[4][ROT ? 1 : SLOTS];
+  constexpr int NW = (LANES > 64 ? LANES : 256) / 64;   // waves per workgroup: 4, or 2
+  static_assert(NW == 4 || NW == 2, "four or two waves per workgroup");
+  static_assert(!ROT || LANES == 256, "rotation in LDS needs one row per 256-lane workgroup");
+  __shared__ RawBlock<T> rawl[NW][ROT ? 1 : SLOTS];
   __shared__ __attribute__((aligned(16))) float rbuf[ROT ? 8 * 4 * SLOTS : 1];
   constexpr int BQ = SLOTS < 256 ? SLOTS : 256;   // room in the boundary list
-  __shared__ uint16_t queue[4][SLOTS];
-  __shared__ uint16_t qnext[4 * SLOTS];
+  __shared__ uint16_t queue[NW][SLOTS];
+  __shared__ uint16_t qnext[NW * SLOTS];
   __shared__ int qcnt[4];
   __shared__ uint16_t bq[BQ];                      // boundary slots: w << 11 | sl << 2 | t
   __shared__ uint2 bp[BQ];                         // and their points, as signed bytes
   __shared__ int bcnt;
-  __shared__ uint8_t tsl[4][SLOTS];
+  __shared__ uint8_t tsl[NW][SLOTS];
   __shared__ float crow[CW][RW][4];
   __shared__ __attribute__((aligned(16))) float chi[CW][RW][4];
   __shared__ float rrow[CW][RW];
-  __shared__ double rsum[4][RW];
-  __shared__ int qlen[4];
+  __shared__ double rsum[NW][RW];
+  __shared__ int qlen[NW];
 
   // A TileTask's a.task.wgs workgroups come last in the grid: dispatched once every row has
   // started, they fill the CUs that the encoder's last rows leave idle (spreading them
@@ -635,7 +639,7 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
   if constexpr (TILES && SM::WGROW) {
     const int64_t first = (int64_t)gridDim.x - a.task.wgs;
     if (bid >= first) {
-      run_tile_task(a.task, a.tile_et, bid - first);
+      run_tile_task<NW * 64>(a.task, a.tile_et, bid - first);
       return;
     }
   }
@@ -729,7 +733,11 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
     const int64_t row = row0 + rw;
     if (mine && row < rows) {
       double s = rsum[wave][rw];
-      if constexpr (SM::WGROW) s = ((rsum[0][0] + rsum[1][0]) + rsum[2][0]) + rsum[3][0];
+      if constexpr (SM::WGROW) {
+        s = rsum[0][0];
+#pragma unroll
+        for (int w = 1; w < NW; ++w) s += rsum[w][0];
+      }
       bool sure;
       float r = rms_candidate(s, n, sure);
       if (!sure) {
@@ -879,7 +887,7 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
   {
     const int nbq = min(bcnt, BQ);
     if (nbq > 0) {
-      for (int idx = threadIdx.x; idx < nbq; idx += 256) {
+      for (int idx = threadIdx.x; idx < nbq; idx += NW * 64) {
         const uint32_t e = bq[idx];
         const int w = (int)(e >> 11), sl = (int)((e >> 2) & 511u), t = (int)(e & 3u);
         const uint2 pb = bp[idx];
@@ -913,22 +921,31 @@ __global__ __launch_bounds__(256) void encode_wave_kernel(
   // lane is done.  There are at most k rounds (t grows by one per round, and t = k - 1
   // always stops).
   {
-    const int q0 = qlen[0], q1 = q0 + qlen[1], q2 = q1 + qlen[2];
-    int n = q2 + qlen[3];
+    int qs[NW + 1];   // starts of the wave queues in round 0's index space
+    qs[0] = 0;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) qs[w + 1] = qs[w] + qlen[w];
+    int n = qs[NW];
 #pragma unroll 1
     for (int rd = 0; n > 0; ++rd) {
       uint16_t* __restrict__ out_q = (rd & 1) ? &queue[0][0] : qnext;
       const uint16_t* __restrict__ in_q = (rd & 1) ? qnext : &queue[0][0];
 #pragma unroll 1
-      for (int base = 0; base < n; base += 256) {
+      for (int base = 0; base < n; base += NW * 64) {
         const int idx = base + (int)threadIdx.x;
         bool more = false;
         uint32_t next = 0;
         if (idx < n) {
           int w, sl, t;
           if (rd == 0) {
-            w = (idx >= q0) + (idx >= q1) + (idx >= q2);
-            const int off = w == 0 ? 0 : (w == 1 ? q0 : (w == 2 ? q1 : q2));
+            int off;
+            if constexpr (NW == 4) {
+              w = (idx >= qs[1]) + (idx >= qs[2]) + (idx >= qs[3]);
+              off = w == 0 ? 0 : (w == 1 ? qs[1] : (w == 2 ? qs[2] : qs[3]));
+            } else {
+              w = idx >= qs[1];
+              off = w ? qs[1] : 0;
+            }
             const uint32_t e = queue[w][idx - off];
             sl = (int)(e >> 2);
             t = (int)(e & 3u);
@@ -1009,10 +1026,11 @@ static hipError_t launch_w(const void* x, int64_t rows, int cols, int64_t ld_x,
                            const EncodeArgs& a, uint32_t* codes, uint32_t* beta, float* scales,
                            hipStream_t st) {
   using SM = SlotMap<LANES, BPT>;
+  constexpr int WG = LANES > 64 ? LANES : 256;
   const int64_t rows_per_wg = SM::WGROW ? 1 : 4 * SM::ROWS_PER_WAVE;
   int64_t grid = (rows + rows_per_wg - 1) / rows_per_wg;
   if (TILES && SM::WGROW) grid += a.task.wgs;
-  hipLaunchKernelGGL((encode_wave_kernel<T, LANES, BPT, TILES, ROT>), dim3((unsigned)grid), dim3(256), 0, st,
+  hipLaunchKernelGGL((encode_wave_kernel<T, LANES, BPT, TILES, ROT>), dim3((unsigned)grid), dim3(WG), 0, st,
                      (const T*)x, rows, cols, ld_x, a, codes, beta, scales);
   return hipGetLastError();
 }
@@ -1051,7 +1069,7 @@ static hipError_t launch_dtype(const void* x, int64_t rows, int cols, int64_t ld
   if (nb <= 64) { if (rows >= 512) NQ_W(64, 8); NQ_W(64, 1); }
   if (nb <= 128) NQ_W(64, 2);
   if (nb <= 256) NQ_W(64, 4);
-  if (nb <= 512) NQ_W(256, 2);
+  if (nb <= 512) NQ_W(128, 4);   // one row per two waves: a single wave of workgroups
   if (nb <= 1024) NQ_W(256, 4);
   if (nb <= 2048) NQ_W(256, 8);
   if (nb <= 4096) NQ_L(512, 8);

@@ -14,45 +14,47 @@ namespace nq {
 
 // m * X2 of every block of a coded operand into ws[rows_p][nb_p blocks] (zero padding): 8
 // bf16 or fp16 (16 B) per block, or 8 int8 (8 B) for the int8 contraction.  The workspace
-// is one flat array of rows_p * nb_p blocks; workgroup w covers TB = 256 * TPB consecutive
-// blocks of it, thread t the blocks w TB + t + 256 i (i < TPB), so each load and store
-// instruction of a wave touches consecutive blocks.  A thread splits its first block's
-// position into (row, column) once and steps the split by 256 blocks for the next ones.
-// Every thread issues the loads of all its blocks before decoding any, which keeps TPB
-// loads in flight per thread.
-template <int ET, int DV>
+// is one flat array of rows_p * nb_p blocks; workgroup w covers TB = 256 * kTilesPerThread
+// consecutive blocks of it with NT threads, thread t the blocks w TB + t + NT i (i < TPB =
+// TB / NT), so each load and store instruction of a wave touches consecutive blocks.  A
+// thread splits its first block's position into (row, column) once and steps the split by
+// NT blocks for the next ones.  Every thread issues the loads of all its blocks before
+// decoding any, which keeps TPB loads in flight per thread.
+template <int ET, int DV, int NT = 256>
 __device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
                                             const uint32_t* __restrict__ beta, int64_t rows,
                                             int nb, int64_t total, int nb_p, float inv_nbp,
                                             int q, uint32_t m2q, uint32_t mtab,
                                             void* __restrict__ ws, int64_t wg) {
   constexpr bool I8 = ET == ET_I8;
-  constexpr int TPB = kTilesPerThread;
+  constexpr int TB = 256 * kTilesPerThread;   // blocks per workgroup
+  constexpr int TPB = TB / NT;                // blocks per thread
+  static_assert(TPB * NT == TB, "NT divides the workgroup's blocks");
   constexpr uint32_t OOB = 0x80000000u;   // past every buffer range below: reads 0
   using V = typename std::conditional<I8, u32x2, u32x4>::type;
-  const int64_t g0 = wg * (256 * TPB);
+  const int64_t g0 = wg * TB;
   // the workgroup's first block as (row0, j0); every other block is an offset
-  // o < nb_p + 256 TPB <= 2^14 past (row0, 0).  Code and beta words are read through buffer
+  // o < nb_p + TB <= 2^14 past (row0, 0).  Code and beta words are read through buffer
   // resources based at row0 (32-bit offsets; the range check makes rows past the operand
   // read as zero).
   const int64_t row0 = g0 / nb_p;
   const int j0 = (int)(g0 - row0 * nb_p);
   const int nbw = (nb + 15) >> 4;
   const int64_t rows_left = rows > row0 ? rows - row0 : 0;
-  const int reach = (j0 + 256 * TPB + nb_p - 1) / nb_p;     // rows this workgroup touches
+  const int reach = (j0 + TB + nb_p - 1) / nb_p;            // rows this workgroup touches
   const int64_t span = rows_left < reach ? rows_left : reach;
   const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(codes + row0 * nb), (short)0, (int)(span * nb * 4), 0x00020000);
   const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(beta + row0 * nbw), (short)0, (int)(span * nbw * 4), 0x00020000);
   // the first block's (row, column) by a float division checked once in each direction;
-  // each further block is 256 blocks on: dr rows and dj columns more, with one carry
+  // each further block is NT blocks on: dr rows and dj columns more, with one carry
   const int o = j0 + (int)threadIdx.x;
   int r = (int)((float)o * inv_nbp);
   if ((int)__umul24((uint32_t)r, (uint32_t)nb_p) > o) --r;
   if ((int)__umul24((uint32_t)(r + 1), (uint32_t)nb_p) <= o) ++r;
   int j = o - (int)__umul24((uint32_t)r, (uint32_t)nb_p);
-  const int dr = 256 / nb_p, dj = 256 - dr * nb_p;
+  const int dr = NT / nb_p, dj = NT - dr * nb_p;
   uint32_t w[TPB], bw[TPB];
   int jj[TPB];
 #pragma unroll
@@ -74,7 +76,7 @@ __device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
   }
 #pragma unroll
   for (int i = 0; i < TPB; ++i) {
-    const int64_t g = g0 + (int)threadIdx.x + 256 * i;
+    const int64_t g = g0 + (int)threadIdx.x + NT * i;
     if (g >= total) break;
     const int m = beta_mult(mtab, (bw[i] >> (2 * (jj[i] & 15))) & 3u);
     V out;
@@ -89,11 +91,12 @@ __device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
   }
 }
 
-// Workgroup wg of a TileTask, with the element type and decoder chosen at run time (uniform
-// over the workgroup).
+// Workgroup wg of a TileTask (NT threads), with the element type and decoder chosen at run
+// time (uniform over the workgroup).
+template <int NT = 256>
 __device__ __forceinline__ void run_tile_task(const TileTask& t, int et, int64_t wg) {
 #define NQ_TB(ET, DV) \
-  tiles_block<ET, DV>(t.codes, t.beta, t.rows, t.nb, t.total, t.nb_p, t.inv_nbp, t.q, t.m2q, t.mtab, t.ws, wg)
+  tiles_block<ET, DV, NT>(t.codes, t.beta, t.rows, t.nb, t.total, t.nb_p, t.inv_nbp, t.q, t.m2q, t.mtab, t.ws, wg)
   switch (et * 3 + t.dv) {
     case 0: NQ_TB(ET_BF16, 0); break;
     case 1: NQ_TB(ET_BF16, 1); break;
