@@ -1069,7 +1069,9 @@ static hipError_t launch_dtype(const void* x, int64_t rows, int cols, int64_t ld
   if (nb <= 64) { if (rows >= 512) NQ_W(64, 8); NQ_W(64, 1); }
   if (nb <= 128) NQ_W(64, 2);
   if (nb <= 256) NQ_W(64, 4);
-  if (nb <= 512) NQ_W(128, 4);   // one row per two waves: a single wave of workgroups
+  // 257..512 blocks: with many rows, one row per two waves keeps the launch to a single wave
+  // of workgroups over the CUs; with few rows, four waves per row finish each row sooner
+  if (nb <= 512) { if (rows > 1024) NQ_W(128, 4); NQ_W(256, 2); }
   if (nb <= 1024) NQ_W(256, 4);
   if (nb <= 2048) NQ_W(256, 8);
   if (nb <= 4096) NQ_L(512, 8);
