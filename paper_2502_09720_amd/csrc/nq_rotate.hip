@@ -15,11 +15,12 @@ namespace nq {
 // Rows at least this long get a workgroup of 1024 threads.
 constexpr int kRotateWideCols = 12288;
 
+// With 1024 threads, at most 64 VGPRs, so that two rows (two workgroups) fit a CU while
+// their LDS does (n <= 14336): one row's loads and stores then overlap the other's transform.
 template <typename T, int NT>
-__global__ __launch_bounds__(NT) void rotate_kernel(const T* __restrict__ x, int64_t rows,
-                                                    int n, int64_t ld_x, int p, int lp,
-                                                    int rpw, float s, float* __restrict__ y,
-                                                    int64_t ld_y) {
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(NT == 1024 ? 8 : 1)))
+void rotate_kernel(const T* __restrict__ x, int64_t rows, int n, int64_t ld_x, int p, int lp,
+                   int rpw, float s, float* __restrict__ y, int64_t ld_y) {
   extern __shared__ float buf[];
   const int tid = threadIdx.x;
   const int64_t row0 = (int64_t)blockIdx.x * rpw;
