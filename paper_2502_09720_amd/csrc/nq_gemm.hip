@@ -216,24 +216,31 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
   for (int s = 0; s < NSTAGE - 1; ++s)
     if (s < nks) load_stage(s);
 
-  // Row and column scales of this lane's outputs, fetched now so that the epilogue issues
-  // only stores.  32x32 accumulator layout: lane l holds column l % 32; register e holds
-  // row 8 (e / 4) + 4 (l / 32) + (e % 4).  Indices are clamped into range (M, N >= 1).
+  // Row and column scales of this lane's outputs.  32x32 accumulator layout: lane l holds
+  // column l % 32; register e holds row 8 (e / 4) + 4 (l / 32) + (e % 4).  Indices are
+  // clamped into range (M, N >= 1).  The 256 x 128 tile fetches them before the main loop,
+  // so that the epilogue issues only stores; the 256 x 256 tile's accumulators and
+  // fragments leave no room to hold them through the loop (they were spilled to scratch and
+  // reloaded in every stage), so it fetches them after the loop.
+  constexpr bool EARLY_SCALES = BN <= 128;
   const int64_t m0 = (int64_t)pm * BM + wm * (BM / WM) + 4 * (lane >> 5);
   const int64_t n0 = (int64_t)pn * BN + wn * (BN / WN) + (lane & 31);
   float rs[TM][16], cs[TN];
+  auto fetch_scales = [&]() {
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int64_t row = m0 + i * 32 + 8 * (e >> 2) + (e & 3);
-      rs[i][e] = ra[row < M ? row : M - 1];
+      for (int e = 0; e < 16; ++e) {
+        const int64_t row = m0 + i * 32 + 8 * (e >> 2) + (e & 3);
+        rs[i][e] = ra[row < M ? row : M - 1];
+      }
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int64_t col = n0 + j * 32;
+      cs[j] = rw[col < N ? col : N - 1] * scale;
     }
-#pragma unroll
-  for (int j = 0; j < TN; ++j) {
-    const int64_t col = n0 + j * 32;
-    cs[j] = rw[col < N ? col : N - 1] * scale;
-  }
+  };
+  if constexpr (EARLY_SCALES) fetch_scales();
 
   // One stage; PF: the loads of stage ks + NSTAGE - 1 are issued (every stage but the last
   // NSTAGE - 1), a compile-time flag so that the steady-state loop has no branches.
@@ -321,6 +328,8 @@ __global__ __launch_bounds__(C::NW * 64, 1) void gemm_kernel(
   int ks = 0;
   for (; ks < nks - (NSTAGE - 1); ++ks) stage(ks, std::true_type{});
   for (; ks < nks; ++ks) stage(ks, std::false_type{});
+
+  if constexpr (!EARLY_SCALES) fetch_scales();
 
   // Epilogue: C = acc * r_A * (r_W * scale); whole tiles skip the bounds tests.  C is
   // written once and not read here, so its stores are nontemporal (streamed past the
