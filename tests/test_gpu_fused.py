@@ -58,6 +58,10 @@ FUSED_CASES = [
     (16, 80, 50, 8192, "bf16", "t4", 7, 3, (1, 2, 4), 1, 0, True),
     (17, 100, 90, 2560, "bf16", "normal", 16, 3, None, 1, 0, True),
     (18, 70, 40, 4096, "f16", "t4", 16, 4, (5, 9, 20, 40), 1, 0, False),
+    # rows of 1025..2048 blocks: W's tile decode workgroups come first in the grid
+    (19, 129, 100, 14336, "bf16", "t4", 14, 4, None, 0, 0, True),
+    # more than 1024 rows of 257..512 blocks: two-wave encoder workgroups carry W's decode
+    (20, 1100, 96, 4096, "bf16", "t4", 14, 4, None, 0, 0, False),
 ]
 
 
