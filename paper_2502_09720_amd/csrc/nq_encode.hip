@@ -485,11 +485,11 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_kernel(
 // decision was too close to call or the point's exact root bound says it overloads (both
 // queued, at the same and at the next beta), or the point lies on the cell boundary (kept
 // with its point in a boundary list).  Phase 2a runs the literal test on the boundary list;
-// phase 2 then finishes the queued slots (about 8-10% on Gaussian-like and heavy-tailed
-// rows, plus the boundary points that overload) in rounds of one beta each, the slots still
-// searching compacted after every round so that the lanes stay busy.  With tiles, slots at
-// the last beta whose point is not strictly inside the cell are queued too, so that phase 1
-// never runs the decoder (full decoder only).
+// phase 2 then finishes the queued slots (8.6% of the blocks on heavy-tailed Student-t rows,
+// fewer on Gaussian ones, plus the boundary points that overload) in rounds of one beta
+// each, the slots still searching compacted after every round so that the lanes stay busy.
+// With tiles, slots at the last beta whose point is not strictly inside the cell are queued
+// too, so that phase 1 never runs the decoder (full decoder only).
 // Two-bit beta indices are staged in LDS and packed into words at the end.
 // ---------------------------------------------------------------------------------------
 template <int LANES, int BPT>
