@@ -1005,16 +1005,19 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_wave_kernel(
   }
 
   // ---- beta words: 16 two-bit indices of consecutive blocks (consecutive lanes) ----
+  // Block j sits in lane j mod 16 of its group of 16 lanes (j mod 8 of 8 when rows have 8
+  // blocks): each lane shifts its own index into place and an OR across the group forms the
+  // word, which the group's first lane stores.
+  constexpr int G = LANES < 16 ? LANES : 16;
 #pragma unroll
   for (int i = 0; i < BPT; ++i) {
     const int rw = SM::row_w(i, lane), j = SM::j(i, lane, wave);
     const int64_t row = row0 + rw;
-    if (row < rows && j < nb && (j & 15) == 0) {
-      uint32_t bits = 0;
-      const int cnt = min(min(16, nb - j), LANES < 16 ? LANES : 16);
-      for (int m = 0; m < cnt; ++m) bits |= (uint32_t)tsl[wave][i * 64 + lane + m] << (2 * m);
-      beta[row * nbw + (j >> 4)] = bits;
-    }
+    const bool ok = row < rows && j < nb;
+    uint32_t bits = ok ? (uint32_t)tsl[wave][i * 64 + lane] << (2 * (j & 15)) : 0u;
+#pragma unroll
+    for (int m = 1; m < G; m <<= 1) bits |= (uint32_t)__shfl_xor((int)bits, m, 64);
+    if (ok && (j & 15) == 0) beta[row * nbw + (j >> 4)] = bits;
   }
 }
 
