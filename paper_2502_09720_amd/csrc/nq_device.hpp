@@ -162,7 +162,7 @@ __device__ __forceinline__ int e8_root_bound(const int (&P)[8], int& amax) {
   const int mn = min(min(min(a[0], a[1]), min(a[2], a[3])), min(min(a[4], a[5]), min(a[6], a[7])));
   const int neg = (int)(((uint32_t)(P[0] ^ P[1] ^ P[2] ^ P[3] ^ P[4] ^ P[5] ^ P[6] ^ P[7])) >> 31);
   amax = m1;
-  return max(m1 + m2, (sa - 2 * neg * mn) >> 1);
+  return max(m1 + m2, (sa - ((0 - neg) & (mn << 1))) >> 1);   // a select, not a multiply
 }
 
 __device__ __forceinline__ int e8_root_bound(const int (&P)[8]) {
@@ -206,6 +206,24 @@ __device__ __forceinline__ int mod_q_general(int v, int q, float rq) {
 // bias of 1024 q to make v non-negative and divide with a 24-bit multiply,
 // floor(u / q) = (u * mq) >> 20 with mq = ceil(2^20 / q), exact for u < 2^20 / q.
 // encode_codes_amax takes max |P_i| when the caller already has it.
+//
+// umul24_v is the full-rate 24-bit multiply (low 32 bits of the product of the operands'
+// low 24 bits), the same as __umul24; written out because the compiler turns some
+// __umul24 of values it has range facts about into a quarter-rate 32-bit multiply.
+__device__ __forceinline__ uint32_t umul24_v(uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_mul_u32_u24 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
+// Low 16 bits of the products of the two 16-bit halves (full rate); a multiply of 16-bit
+// vectors in C is split by the compiler into quarter-rate 32-bit multiplies.
+__device__ __forceinline__ uint32_t pk_mul_lo_u16(uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_pk_mul_lo_u16 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
 __device__ __forceinline__ uint32_t encode_codes_amax(const int (&P)[8], int q, float rq,
                                                       uint32_t mq, int amax) {
   int v[8];
@@ -216,18 +234,22 @@ __device__ __forceinline__ uint32_t encode_codes_amax(const int (&P)[8], int q, 
   v[3] = (P[5] - P[0]) >> 1;
   v[5] = (P[6] - P[0]) >> 1;
   v[7] = (P[7] - P[0]) >> 1;
-  v[1] = (5 * P[0] - P[1] - P[2] - P[3] + P[4] - P[5] - P[6] - P[7]) >> 2;
+  const int rest = -P[1] - P[2] - P[3] + P[4] - P[5] - P[6] - P[7];
   uint32_t w = 0;
   if (amax < 512) {
-    // |v| <= 3 * 511 < 1024 q, so u = v + 1024 q lies in [0, 2048 q) and 2048 q < 2^20 / q
+    // |v| <= 3 * 511 < 1024 q, so u = v + 1024 q lies in [0, 2048 q) and 2048 q < 2^20 / q.
+    // Every product is a full-rate 24-bit multiply (u < 2^15, mq < 2^20, |P_0| < 512).
+    v[1] = (__mul24(P[0], 5) + rest) >> 2;
+    const uint32_t qq = (uint32_t)q, mm = mq;
     const int bias = q << 10;
 #pragma unroll
     for (int l = 0; l < 8; ++l) {
       const uint32_t u = (uint32_t)(v[l] + bias);
-      const uint32_t n = __umul24(u, mq) >> 20;
-      w |= (u - __umul24(n, (uint32_t)q)) << (4 * l);
+      const uint32_t n = umul24_v(u, mm) >> 20;
+      w |= (u - umul24_v(n, qq)) << (4 * l);
     }
   } else {
+    v[1] = (5 * P[0] + rest) >> 2;
 #pragma unroll
     for (int l = 0; l < 8; ++l) w |= (uint32_t)mod_q_general(v[l], q, rq) << (4 * l);
   }
@@ -501,11 +523,11 @@ template <int DV = 0>
 __device__ __forceinline__ u32x2 decode_tile_i8(uint32_t w, int m, int q, uint32_t m2q) {
   uint32_t xa, xb;
   decode_word_b8<DV != 0>(w, q, m2q, xa, xb);
-  const u16x2 mm = {(unsigned short)m, (unsigned short)m};
+  const uint32_t mm = (uint32_t)m | ((uint32_t)m << 16);   // m in both halves
   auto mul8 = [&](uint32_t x) {
     const uint32_t s = x ^ 0x80808080u;                  // X2 as signed bytes
-    const uint32_t lo = bits32(as_u16x2(s & 0x00FF00FFu) * mm);
-    const uint32_t hi = bits32(as_u16x2((s >> 8) & 0x00FF00FFu) * mm);
+    const uint32_t lo = pk_mul_lo_u16(s & 0x00FF00FFu, mm);
+    const uint32_t hi = pk_mul_lo_u16((s >> 8) & 0x00FF00FFu, mm);
     return (lo & 0x00FF00FFu) | ((hi & 0x00FF00FFu) << 8);
   };
   return u32x2{mul8(xa), mul8(xb)};

@@ -214,7 +214,8 @@ __device__ __forceinline__ void encode_block(const float (&v)[8], const float (&
 // Fused encode-and-multiply: the decoded tile m_t * X2 of block j of `row`, stored where
 // the product's decode stage would put it.  X2 is the lattice point P itself when P is known
 // to be reproduced by the decoder (tile_from_x2), else the decode of the code word
-// (tile_decoded); rows that are not coded get zeros.
+// (tile_decoded); rows that are not coded get zeros.  |X2_l| <= 2q for a point that is
+// kept, so m X2 is a full-rate 24-bit product.
 __device__ __forceinline__ void tile_from_x2(const EncodeArgs& a, int64_t row, int j,
                                              const int (&X2)[8], int t) {
   const int m = (int)((a.mtab >> (8 * t)) & 0xFFu);
@@ -223,15 +224,16 @@ __device__ __forceinline__ void tile_from_x2(const EncodeArgs& a, int64_t row, i
     uint32_t lo = 0u, hi = 0u;
 #pragma unroll
     for (int l = 0; l < 4; ++l) {
-      lo |= ((uint32_t)(m * X2[l]) & 0xFFu) << (8 * l);
-      hi |= ((uint32_t)(m * X2[4 + l]) & 0xFFu) << (8 * l);
+      // the low byte of m X2 from the operands' low 24 bits
+      lo |= (umul24_v((uint32_t)m, (uint32_t)X2[l]) & 0xFFu) << (8 * l);
+      hi |= (umul24_v((uint32_t)m, (uint32_t)X2[4 + l]) & 0xFFu) << (8 * l);
     }
     reinterpret_cast<u32x2*>(a.tiles)[idx] = u32x2{lo, hi};
   } else {
     uint32_t o[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float lo = (float)(m * X2[2 * i]), hi = (float)(m * X2[2 * i + 1]);
+      const float lo = (float)__mul24(m, X2[2 * i]), hi = (float)__mul24(m, X2[2 * i + 1]);
       o[i] = a.tile_et == ET_F16 ? pack16<true>(lo, hi) : pack16<false>(lo, hi);
     }
     reinterpret_cast<u32x4*>(a.tiles)[idx] = u32x4{o[0], o[1], o[2], o[3]};
@@ -499,6 +501,8 @@ struct SlotMap {
   static constexpr int ROWS_PER_WAVE = LANES < 64 ? RPP * BPT : 1;
   static constexpr int SLOTS = 64 * BPT;
   __device__ static int row_w(int i, int l) { return LANES < 64 ? i * RPP + l / LANES : 0; }
+  // row_w(i, l) = row_step(i) + row_w(0, l), the first term the same for every lane
+  __device__ static constexpr int row_step(int i) { return LANES < 64 ? i * RPP : 0; }
   __device__ static int j(int i, int l, int wave) {
     return LANES < 64 ? l % LANES : (LANES == 64 ? l + 64 * i : 64 * wave + l + LANES * i);
   }
@@ -655,7 +659,10 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_wave_kernel(
       }
     }
   }
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  // the wave index is uniform over the wave: held in a scalar register, so that row offsets
+  // derived from it are scalar arithmetic
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int lane = threadIdx.x & 63;
   const int cw = SM::WGROW ? 0 : wave;
   const int nb = cols >> 3;
   const int nbw = (nb + 15) >> 4;
@@ -664,6 +671,12 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_wave_kernel(
   };
   const int64_t row0 = row_base(wave);
   const double n = (double)cols;
+  // index of block j of row row_base(w) + rw in the code words: rows of more than 64 blocks
+  // have rw = 0, shorter rows w RW + rw < 2^12 and nb <= 64, a 24-bit product
+  auto code_at = [&](int w, int rw, int j) -> int64_t {
+    if constexpr (SM::WGROW) return row_base(w) * nb + j;
+    return (bid * 4 * RW) * (int64_t)nb + __mul24(w * RW + rw, nb) + j;
+  };
   // block of slot sl of wave w, as fp32
   auto slot_block = [&](int w, int sl, float (&v)[8]) {
     if constexpr (ROT) {
@@ -700,12 +713,14 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_wave_kernel(
     if (lane == 0) rsum[wave][0] = part;
   } else {
     RawBlock<T> raw[BPT];
+    // one 64-bit row offset per lane; the rest of each block's address is uniform
+    const T* __restrict__ x_lane = x + (row0 + SM::row_w(0, lane)) * ld_x;
 #pragma unroll
     for (int i = 0; i < BPT; ++i) {
       const int rw = SM::row_w(i, lane), j = SM::j(i, lane, wave);
       const int64_t row = row0 + rw;
       if (row < rows && j < nb) {
-        load_raw<T>(x + row * ld_x + 8 * j, raw[i]);
+        load_raw<T>(x_lane + SM::row_step(i) * ld_x + 8 * j, raw[i]);
       } else {
         zero_raw<T>(raw[i]);
       }
@@ -875,7 +890,7 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_wave_kernel(
         word = amax < (1 << 30) ? encode_codes_amax(P, a.q, a.rq, a.mq, amax)
                                 : encode_codes(P, a.q, a.rq, a.mq);
       }
-      codes_w[rw * nb + j] = word;
+      codes_w[__mul24(rw, nb) + j] = word;   // rw = 0 or nb <= 64
       tsl[wave][sl] = (uint8_t)t0;
       if constexpr (TILES) {
         // a point kept here passed the overload test or lies strictly inside the cell, so
@@ -914,7 +929,7 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_wave_kernel(
           const int rw = SM::row_w(i, l), j = SM::j(i, l, w);
           const int64_t row = row_base(w) + rw;
           const uint32_t word = encode_codes_amax(P, a.q, a.rq, a.mq, 2 * a.q);  // |P_l| <= 2q
-          codes[row * nb + j] = word;
+          codes[code_at(w, rw, j)] = word;
           tsl[w][sl] = (uint8_t)t;
           if constexpr (TILES) tile_from_x2(a, row, j, P, t);
         } else {
@@ -976,7 +991,7 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_wave_kernel(
           int P[8];
           if (eval_block(v, crow[c2][rw][t], t, a, P)) {
             const uint32_t word = encode_codes(P, a.q, a.rq, a.mq);
-            codes[row * nb + j] = word;
+            codes[code_at(w, rw, j)] = word;
             tsl[w][sl] = (uint8_t)t;
             if constexpr (TILES) {
               if (t < a.k - 1) {
@@ -1009,6 +1024,7 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_wave_kernel(
   // blocks): each lane shifts its own index into place and an OR across the group forms the
   // word, which the group's first lane stores.
   constexpr int G = LANES < 16 ? LANES : 16;
+  uint32_t* __restrict__ beta_w = beta + row0 * nbw;   // this wave's rows
 #pragma unroll
   for (int i = 0; i < BPT; ++i) {
     const int rw = SM::row_w(i, lane), j = SM::j(i, lane, wave);
@@ -1017,7 +1033,7 @@ __global__ __launch_bounds__(LANES > 64 ? LANES : 256) void encode_wave_kernel(
     uint32_t bits = ok ? (uint32_t)tsl[wave][i * 64 + lane] << (2 * (j & 15)) : 0u;
 #pragma unroll
     for (int m = 1; m < G; m <<= 1) bits |= (uint32_t)__shfl_xor((int)bits, m, 64);
-    if (ok && (j & 15) == 0) beta[row * nbw + (j >> 4)] = bits;
+    if (ok && (j & 15) == 0) beta_w[__mul24(rw, nbw) + (j >> 4)] = bits;   // rw = 0 or nbw <= 4
   }
 }
 
