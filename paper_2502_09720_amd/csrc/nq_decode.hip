@@ -54,21 +54,28 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict_
   if ((int)__umul24((uint32_t)(r + 1), (uint32_t)nb) <= o) ++r;
   int j = o - (int)__umul24((uint32_t)r, (uint32_t)nb);
   const int dr = 256 / nb, dj = 256 - dr * nb;
+  // offset of the block's first output value from the run's first row, stepped with (r, j)
+  // (one 64-bit multiply per thread; the steps are uniform)
+  int64_t oo = (int64_t)r * ld_out + 8 * j;
+  const int64_t ostep = (int64_t)dr * ld_out + 8 * dj, owrap = ld_out - 8 * (int64_t)nb;
   uint32_t w[TPB], bw[TPB];
   float sr[TPB];
-  int rr[TPB], jj[TPB];
+  int jj[TPB];
+  int64_t ooff[TPB];
 #pragma unroll
   for (int i = 0; i < TPB; ++i) {
     if (i > 0) {
       j += dj;
       r += dr;
+      oo += ostep;
       if (j >= nb) {
         j -= nb;
         ++r;
+        oo += owrap;
       }
     }
-    rr[i] = r;
     jj[i] = j;
+    ooff[i] = oo;
     const uint32_t ok = g0 + (int)threadIdx.x + 256 * i < total ? 0u : OOB;
     w[i] = __builtin_amdgcn_raw_buffer_load_b32(
         rc, (4u * (__umul24((uint32_t)r, (uint32_t)nb) + (uint32_t)j)) | ok, 0, 0);
@@ -99,13 +106,12 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict_
       if constexpr (DV == 2) return l == 0 ? x0 : b >> 2;
       return b;
     };
-    const int64_t orow = row0 + rr[i];
     if constexpr (OUT == 0) {
       // fp32: each value rounded once from its fp64 product
       float v[8];
 #pragma unroll
       for (int l = 0; l < 8; ++l) v[l] = (float)(sc * (double)x2(l));
-      f32x4* o = reinterpret_cast<f32x4*>((float*)out + orow * ld_out + 8 * j);
+      f32x4* o = reinterpret_cast<f32x4*>((float*)out + row0 * ld_out + ooff[i]);
       const f32x4 lo = {v[0], v[1], v[2], v[3]};
       const f32x4 hi = {v[4], v[5], v[6], v[7]};
       __builtin_nontemporal_store(lo, o);
@@ -130,7 +136,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict_
       }
       const u32x4 v = {pk[0], pk[1], pk[2], pk[3]};
       __builtin_nontemporal_store(
-          v, reinterpret_cast<u32x4*>((uint16_t*)out + orow * ld_out + 8 * j));
+          v, reinterpret_cast<u32x4*>((uint16_t*)out + row0 * ld_out + ooff[i]));
     }
   }
 }
