@@ -58,6 +58,13 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict_
   // (one 64-bit multiply per thread; the steps are uniform)
   int64_t oo = (int64_t)r * ld_out + 8 * j;
   const int64_t ostep = (int64_t)dr * ld_out + 8 * dj, owrap = ld_out - 8 * (int64_t)nb;
+  // blocks of this thread still inside the matrix: block i exists iff 256 i < left
+  const int64_t left64 = total - g0 - (int64_t)threadIdx.x;
+  const int left = left64 > 256 * TPB ? 256 * TPB : (int)left64;
+  // the four half-betas in LDS, read by index (a select chain over kernel arguments
+  // compiles to branches that every wave with mixed beta indices runs in full)
+  __shared__ double hbt[4];
+  if (threadIdx.x < 4) hbt[threadIdx.x] = pick_half_beta(a, threadIdx.x);
   uint32_t w[TPB], bw[TPB];
   float sr[TPB];
   int jj[TPB];
@@ -76,35 +83,36 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict_
     }
     jj[i] = j;
     ooff[i] = oo;
-    const uint32_t ok = g0 + (int)threadIdx.x + 256 * i < total ? 0u : OOB;
-    w[i] = __builtin_amdgcn_raw_buffer_load_b32(
-        rc, (4u * (__umul24((uint32_t)r, (uint32_t)nb) + (uint32_t)j)) | ok, 0, 0);
+    const uint32_t ok = 256 * i < left ? 0u : OOB;
+    // the code words of a run are consecutive: block i of this thread is word o + 256 i
+    // (ok sets bit 31 only, above every in-range offset, so the constant can follow it)
+    w[i] = __builtin_amdgcn_raw_buffer_load_b32(rc, ((4u * (uint32_t)o) | ok) + 1024u * i, 0, 0);
     bw[i] = __builtin_amdgcn_raw_buffer_load_b32(
         rb, (4u * (__umul24((uint32_t)r, (uint32_t)nbw) + (uint32_t)(j >> 4))) | ok, 0, 0);
     sr[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (4u * (uint32_t)r) | ok, 0, 0));
   }
+  __syncthreads();   // hbt
 #pragma unroll
   for (int i = 0; i < TPB; ++i) {
-    if (g0 + (int)threadIdx.x + 256 * i >= total) break;
+    if (256 * i >= left) break;
     const int j = jj[i];
     const uint32_t t = (bw[i] >> (2 * (j & 15))) & 3u;
-    const double sc = (double)sr[i] * pick_half_beta(a, t);
-    // X2 of the block: xs holds coordinates 0-3 and 4-7 as signed bytes (decode_word_b8),
-    // or as four times X2 for NestQuantM at q = 16 (decode_word_m16, coordinate 0 apart)
+    const double sc = (double)sr[i] * hbt[t];
+    // X2 of the block: xs holds coordinates 0-3 and 4-7 as bytes X2 + 128 (decode_word_b8),
+    // or as four times X2, signed, for NestQuantM at q = 16 (decode_word_m16, coordinate 0
+    // apart)
     uint32_t xs[2];
     int x0 = 0;
     if constexpr (DV == 2) {
       decode_word_m16(w[i], xs[0], xs[1], x0);
     } else {
-      uint32_t xa, xb;
-      decode_word_b8<DV == 1>(w[i], a.q, a.m2q, xa, xb);
-      xs[0] = xa ^ 0x80808080u;
-      xs[1] = xb ^ 0x80808080u;
+      decode_word_b8<DV == 1>(w[i], a.q, a.m2q, xs[0], xs[1]);
     }
     auto x2 = [&](int l) {
-      const int b = (int)(int8_t)(uint8_t)(xs[l >> 2] >> (8 * (l & 3)));
-      if constexpr (DV == 2) return l == 0 ? x0 : b >> 2;
-      return b;
+      if constexpr (DV == 2) {
+        return l == 0 ? x0 : (int)(int8_t)(uint8_t)(xs[l >> 2] >> (8 * (l & 3))) >> 2;
+      }
+      return (int)((xs[l >> 2] >> (8 * (l & 3))) & 0xFFu) - 128;
     };
     if constexpr (OUT == 0) {
       // fp32: each value rounded once from its fp64 product
@@ -119,19 +127,33 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict_
     } else {
       // 16-bit outputs: X2 (|X2| <= 32) times the fp32-rounded scale is within two fp32
       // roundings (relative 2^-23) of the exact value, far below half an fp16 / bf16 ulp,
-      // so the final rounding lands on the nearest or the adjacent 16-bit value
-      const float s32 = (float)sc;
+      // so the final rounding lands on the nearest or the adjacent 16-bit value.  From the
+      // biased byte b = X2 + 128 the fp32 product is one fma, b s - 128 s (128 s is exact),
+      // the same rounding of the same exact value X2 s.
+      const float s32 = (float)sc, off = -128.0f * s32;
+      auto val = [&](int l) {
+        if constexpr (DV == 2) return (float)x2(l) * s32;
+        return __builtin_fmaf((float)((xs[l >> 2] >> (8 * (l & 3))) & 0xFFu), s32, off);
+      };
       uint32_t pk[4];
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
-        const float lo = (float)x2(2 * u) * s32;
-        const float hi = (float)x2(2 * u + 1) * s32;
         if constexpr (OUT == 1) {
-          pk[u] = (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)lo) |
-                  ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)hi) << 16);
+          // the fma and its rounding to fp16 in one mixed-precision instruction per half
+          if constexpr (DV == 2) {
+            pk[u] = fma_mix_pk_f16((float)x2(2 * u), (float)x2(2 * u + 1), s32, 0.0f);
+          } else {
+            const uint32_t x = xs[u >> 1];
+            const float b0 = (float)((x >> (16 * (u & 1))) & 0xFFu);
+            const float b1 = (float)((x >> (16 * (u & 1) + 8)) & 0xFFu);
+            pk[u] = fma_mix_pk_f16(b0, b1, s32, off);
+          }
         } else {
-          pk[u] = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)lo) |
-                  ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)hi) << 16);
+          // one two-value conversion (round to nearest even) per word
+          typedef float f32x2 __attribute__((ext_vector_type(2)));
+          typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+          pk[u] = __builtin_bit_cast(
+              uint32_t, __builtin_convertvector((f32x2){val(2 * u), val(2 * u + 1)}, bf16x2));
         }
       }
       const u32x4 v = {pk[0], pk[1], pk[2], pk[3]};

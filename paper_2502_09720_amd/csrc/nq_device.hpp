@@ -216,6 +216,16 @@ __device__ __forceinline__ uint32_t umul24_v(uint32_t a, uint32_t b) {
   return r;
 }
 
+// fp16(fp32 fma(a0, b, c)) in the low and fp16(fp32 fma(a1, b, c)) in the high half: the
+// mixed-precision fma with fp32 sources rounds its fp32 result to fp16 (the compiler selects
+// the low-half form for fp16(a * b) itself; the high-half form saves the shift and OR).
+__device__ __forceinline__ uint32_t fma_mix_pk_f16(float a0, float a1, float b, float c) {
+  uint32_t d;
+  asm("v_fma_mixlo_f16 %0, %1, %2, %3 op_sel_hi:[0,0,0]" : "=v"(d) : "v"(a0), "v"(b), "v"(c));
+  asm("v_fma_mixhi_f16 %0, %1, %2, %3 op_sel_hi:[0,0,0]" : "+v"(d) : "v"(a1), "v"(b), "v"(c));
+  return d;
+}
+
 // Low 16 bits of the products of the two 16-bit halves (full rate); a multiply of 16-bit
 // vectors in C is split by the compiler into quarter-rate 32-bit multiplies.
 __device__ __forceinline__ uint32_t pk_mul_lo_u16(uint32_t a, uint32_t b) {
