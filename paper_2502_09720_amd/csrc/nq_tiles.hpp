@@ -57,27 +57,46 @@ __device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
   const int dr = NT / nb_p, dj = NT - dr * nb_p;
   uint32_t w[TPB], bw[TPB];
   int jj[TPB];
+  // Without padding columns (nb_p == nb) the code words of the workgroup's blocks are
+  // consecutive (block i of this thread is word o + NT i) and a block past the operand's
+  // rows lies past the end of both buffer ranges, so no offset needs a select.
+  auto load = [&](auto dense) {
 #pragma unroll
-  for (int i = 0; i < TPB; ++i) {
-    if (i > 0) {
-      j += dj;
-      r += dr;
-      if (j >= nb_p) {
-        j -= nb_p;
-        ++r;
+    for (int i = 0; i < TPB; ++i) {
+      if (i > 0) {
+        j += dj;
+        r += dr;
+        if (j >= nb_p) {
+          j -= nb_p;
+          ++r;
+        }
       }
+      jj[i] = j;
+      uint32_t co, bo;
+      if constexpr (decltype(dense)::value) {
+        co = 4u * (uint32_t)o + 4u * NT * i;
+        bo = 4u * (__umul24((uint32_t)r, (uint32_t)nbw) + (uint32_t)(j >> 4));
+      } else {
+        const bool pad = j >= nb || r >= span;
+        co = pad ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nb) + (uint32_t)j);
+        bo = pad ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nbw) + (uint32_t)(j >> 4));
+      }
+      w[i] = __builtin_amdgcn_raw_buffer_load_b32(rc, co, 0, 0);
+      bw[i] = __builtin_amdgcn_raw_buffer_load_b32(rb, bo, 0, 0);
     }
-    jj[i] = j;
-    const bool pad = j >= nb || r >= span;
-    const uint32_t co = pad ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nb) + (uint32_t)j);
-    const uint32_t bo = pad ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nbw) + (uint32_t)(j >> 4));
-    w[i] = __builtin_amdgcn_raw_buffer_load_b32(rc, co, 0, 0);
-    bw[i] = __builtin_amdgcn_raw_buffer_load_b32(rb, bo, 0, 0);
+  };
+  if (nb_p == nb) {
+    load(std::true_type{});
+  } else {
+    load(std::false_type{});
   }
+  // blocks of this thread inside the workspace: block i exists iff NT i < left
+  const int64_t left64 = total - g0 - (int64_t)threadIdx.x;
+  const int left = left64 > TB ? TB : (int)left64;
+  V* __restrict__ dst = reinterpret_cast<V*>(ws) + g0 + (int)threadIdx.x;
 #pragma unroll
   for (int i = 0; i < TPB; ++i) {
-    const int64_t g = g0 + (int)threadIdx.x + NT * i;
-    if (g >= total) break;
+    if (NT * i >= left) break;
     const int m = beta_mult(mtab, (bw[i] >> (2 * (jj[i] & 15))) & 3u);
     V out;
     if constexpr (I8) {
@@ -87,7 +106,7 @@ __device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
     }
     // padding past the operand's rows or columns read the word 0 (out of range), which
     // decodes to the zero point: its tile is zero
-    reinterpret_cast<V*>(ws)[g] = out;
+    dst[NT * i] = out;
   }
 }
 
