@@ -5,6 +5,8 @@
 // Each block: read its code word, the row's beta word and scale, decode in exact integer
 // arithmetic, and write the 8 values (32 B fp32 or 16 B fp16/bf16) with one or two vector
 // stores; consecutive lanes handle consecutive blocks.
+#include <type_traits>
+
 #include "nq_device.hpp"
 #include "nq_kernels.hpp"
 
@@ -67,36 +69,58 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict_
   if (threadIdx.x < 4) hbt[threadIdx.x] = pick_half_beta(a, threadIdx.x);
   uint32_t w[TPB], bw[TPB];
   float sr[TPB];
-  int jj[TPB];
+  int sh[TPB];        // bit position of the block's beta index in its beta word
   int64_t ooff[TPB];
+  // Rows of a multiple of 16 blocks written without a gap (ld_out = cols): block i of this
+  // thread is block o + 256 i of the run, its beta word o / 16 + 16 i at bits 2 (o mod 16)
+  // and its output 8 (o + 256 i) values on; only the row, for the scale, is stepped (with no
+  // carry when nb divides 256).
+  auto load = [&](auto flat, auto carry) {
+    constexpr bool FLAT = decltype(flat)::value;
 #pragma unroll
-  for (int i = 0; i < TPB; ++i) {
-    if (i > 0) {
-      j += dj;
-      r += dr;
-      oo += ostep;
-      if (j >= nb) {
-        j -= nb;
-        ++r;
-        oo += owrap;
+    for (int i = 0; i < TPB; ++i) {
+      if (i > 0) {
+        j += dj;
+        r += dr;
+        if constexpr (!FLAT) oo += ostep;
+        if (decltype(carry)::value && j >= nb) {
+          j -= nb;
+          ++r;
+          if constexpr (!FLAT) oo += owrap;
+        }
       }
+      const uint32_t ok = 256 * i < left ? 0u : OOB;
+      // the code words of a run are consecutive: block i of this thread is word o + 256 i
+      // (ok sets bit 31 only, above every in-range offset, so the constant can follow it)
+      w[i] = __builtin_amdgcn_raw_buffer_load_b32(rc, ((4u * (uint32_t)o) | ok) + 1024u * i, 0, 0);
+      uint32_t bo;
+      if constexpr (FLAT) {
+        sh[i] = 2 * (o & 15);
+        bo = ((4u * (uint32_t)(o >> 4)) | ok) + 64u * i;
+        ooff[i] = 8 * (int64_t)o + 2048 * i;
+      } else {
+        sh[i] = 2 * (j & 15);
+        bo = (4u * (__umul24((uint32_t)r, (uint32_t)nbw) + (uint32_t)(j >> 4))) | ok;
+        ooff[i] = oo;
+      }
+      bw[i] = __builtin_amdgcn_raw_buffer_load_b32(rb, bo, 0, 0);
+      sr[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (4u * (uint32_t)r) | ok, 0, 0));
     }
-    jj[i] = j;
-    ooff[i] = oo;
-    const uint32_t ok = 256 * i < left ? 0u : OOB;
-    // the code words of a run are consecutive: block i of this thread is word o + 256 i
-    // (ok sets bit 31 only, above every in-range offset, so the constant can follow it)
-    w[i] = __builtin_amdgcn_raw_buffer_load_b32(rc, ((4u * (uint32_t)o) | ok) + 1024u * i, 0, 0);
-    bw[i] = __builtin_amdgcn_raw_buffer_load_b32(
-        rb, (4u * (__umul24((uint32_t)r, (uint32_t)nbw) + (uint32_t)(j >> 4))) | ok, 0, 0);
-    sr[i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, (4u * (uint32_t)r) | ok, 0, 0));
+  };
+  if ((nb & 15) == 0 && ld_out == 8 * (int64_t)nb) {
+    if (dj == 0) {
+      load(std::true_type{}, std::false_type{});
+    } else {
+      load(std::true_type{}, std::true_type{});
+    }
+  } else {
+    load(std::false_type{}, std::true_type{});
   }
   __syncthreads();   // hbt
 #pragma unroll
   for (int i = 0; i < TPB; ++i) {
     if (256 * i >= left) break;
-    const int j = jj[i];
-    const uint32_t t = (bw[i] >> (2 * (j & 15))) & 3u;
+    const uint32_t t = (bw[i] >> sh[i]) & 3u;
     const double sc = (double)sr[i] * hbt[t];
     // X2 of the block: xs holds coordinates 0-3 and 4-7 as bytes X2 + 128 (decode_word_b8),
     // or as four times X2, signed, for NestQuantM at q = 16 (decode_word_m16, coordinate 0

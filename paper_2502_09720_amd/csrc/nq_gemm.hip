@@ -68,15 +68,15 @@ using CfgBigI8 = Cfg<256, 256, 4, 2, 2>;
 }  // namespace gemm
 
 // One workgroup per 256 * kTilesPerThread blocks of the tile (tiles_block).
-template <int ET, int DV>
+template <int ET, int DV, bool FLAT>
 __global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__ codes,
                                                     const uint32_t* __restrict__ beta,
                                                     int64_t rows, int nb, int64_t total,
                                                     int nb_p, float inv_nbp, int q,
                                                     uint32_t m2q, uint32_t mtab,
                                                     void* __restrict__ ws) {
-  tiles_block<ET, DV>(codes, beta, rows, nb, total, nb_p, inv_nbp, q, m2q, mtab, ws,
-                      (int64_t)blockIdx.x);
+  tiles_block<ET, DV, 256, FLAT>(codes, beta, rows, nb, total, nb_p, inv_nbp, q, m2q, mtab,
+                                 ws, (int64_t)blockIdx.x);
 }
 
 // Launch tiles_kernel for one operand with its decoder.
@@ -86,9 +86,14 @@ void launch_tiles(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void
   const int64_t total = rows_p * nb_p;
   const int64_t wgs = tile_workgroups(total);
   const float inv = 1.0f / (float)nb_p;
+  const bool flat = nb_p == nb && (nb & 15) == 0;
 #define NQ_TL(DV)                                                                            \
-  hipLaunchKernelGGL((tiles_kernel<ET, DV>), dim3((unsigned)wgs), dim3(256), 0, st, X.codes,    \
-                     X.beta, X.rows, nb, total, nb_p, inv, X.q, X.m2q, X.mtab, ws)
+  if (flat)                                                                                  \
+    hipLaunchKernelGGL((tiles_kernel<ET, DV, true>), dim3((unsigned)wgs), dim3(256), 0, st,    \
+                       X.codes, X.beta, X.rows, nb, total, nb_p, inv, X.q, X.m2q, X.mtab, ws); \
+  else                                                                                       \
+    hipLaunchKernelGGL((tiles_kernel<ET, DV, false>), dim3((unsigned)wgs), dim3(256), 0, st,   \
+                       X.codes, X.beta, X.rows, nb, total, nb_p, inv, X.q, X.m2q, X.mtab, ws)
   switch (decoder_variant(X.decoder, X.q)) {
     case 0: NQ_TL(0); break;
     case 1: NQ_TL(1); break;

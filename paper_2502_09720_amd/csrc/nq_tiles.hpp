@@ -20,7 +20,10 @@ namespace nq {
 // thread splits its first block's position into (row, column) once and steps the split by
 // NT blocks for the next ones.  Every thread issues the loads of all its blocks before
 // decoding any, which keeps TPB loads in flight per thread.
-template <int ET, int DV, int NT = 256>
+// FLAT: no padding columns (nb_p == nb) and nb a multiple of 16, so that the code words
+// and beta words of a workgroup's blocks are consecutive and no block needs its (row,
+// column); run_tile_task picks it at run time.
+template <int ET, int DV, int NT = 256, bool FLAT = false>
 __device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
                                             const uint32_t* __restrict__ beta, int64_t rows,
                                             int nb, int64_t total, int nb_p, float inv_nbp,
@@ -56,39 +59,51 @@ __device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
   int j = o - (int)__umul24((uint32_t)r, (uint32_t)nb_p);
   const int dr = NT / nb_p, dj = NT - dr * nb_p;
   uint32_t w[TPB], bw[TPB];
-  int jj[TPB];
-  // Without padding columns (nb_p == nb) the code words of the workgroup's blocks are
-  // consecutive (block i of this thread is word o + NT i) and a block past the operand's
-  // rows lies past the end of both buffer ranges, so no offset needs a select.
-  auto load = [&](auto dense) {
+  int sh[TPB];   // bit position of the block's beta index in its beta word
+  if constexpr (FLAT) {
+    // block i of this thread is code word o + NT i and beta word o / 16 + NT i / 16, at
+    // bits 2 (o mod 16); blocks past the operand's rows lie past both buffer ranges
 #pragma unroll
     for (int i = 0; i < TPB; ++i) {
-      if (i > 0) {
-        j += dj;
-        r += dr;
-        if (j >= nb_p) {
-          j -= nb_p;
-          ++r;
-        }
-      }
-      jj[i] = j;
-      uint32_t co, bo;
-      if constexpr (decltype(dense)::value) {
-        co = 4u * (uint32_t)o + 4u * NT * i;
-        bo = 4u * (__umul24((uint32_t)r, (uint32_t)nbw) + (uint32_t)(j >> 4));
-      } else {
-        const bool pad = j >= nb || r >= span;
-        co = pad ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nb) + (uint32_t)j);
-        bo = pad ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nbw) + (uint32_t)(j >> 4));
-      }
-      w[i] = __builtin_amdgcn_raw_buffer_load_b32(rc, co, 0, 0);
-      bw[i] = __builtin_amdgcn_raw_buffer_load_b32(rb, bo, 0, 0);
+      sh[i] = 2 * (o & 15);
+      w[i] = __builtin_amdgcn_raw_buffer_load_b32(rc, 4u * (uint32_t)o + 4u * NT * i, 0, 0);
+      bw[i] = __builtin_amdgcn_raw_buffer_load_b32(
+          rb, 4u * (uint32_t)(o >> 4) + 4u * (NT / 16) * i, 0, 0);
     }
-  };
-  if (nb_p == nb) {
-    load(std::true_type{});
   } else {
-    load(std::false_type{});
+    // Without padding columns (nb_p == nb) the code words are still consecutive (block i
+    // of this thread is word o + NT i) and a block past the operand's rows lies past the
+    // end of both buffer ranges, so no offset needs a select.
+    auto load = [&](auto dense) {
+#pragma unroll
+      for (int i = 0; i < TPB; ++i) {
+        if (i > 0) {
+          j += dj;
+          r += dr;
+          if (j >= nb_p) {
+            j -= nb_p;
+            ++r;
+          }
+        }
+        sh[i] = 2 * (j & 15);
+        uint32_t co, bo;
+        if constexpr (decltype(dense)::value) {
+          co = 4u * (uint32_t)o + 4u * NT * i;
+          bo = 4u * (__umul24((uint32_t)r, (uint32_t)nbw) + (uint32_t)(j >> 4));
+        } else {
+          const bool pad = j >= nb || r >= span;
+          co = pad ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nb) + (uint32_t)j);
+          bo = pad ? OOB : 4u * (__umul24((uint32_t)r, (uint32_t)nbw) + (uint32_t)(j >> 4));
+        }
+        w[i] = __builtin_amdgcn_raw_buffer_load_b32(rc, co, 0, 0);
+        bw[i] = __builtin_amdgcn_raw_buffer_load_b32(rb, bo, 0, 0);
+      }
+    };
+    if (nb_p == nb) {
+      load(std::true_type{});
+    } else {
+      load(std::false_type{});
+    }
   }
   // blocks of this thread inside the workspace: block i exists iff NT i < left
   const int64_t left64 = total - g0 - (int64_t)threadIdx.x;
@@ -97,7 +112,7 @@ __device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
 #pragma unroll
   for (int i = 0; i < TPB; ++i) {
     if (NT * i >= left) break;
-    const int m = beta_mult(mtab, (bw[i] >> (2 * (jj[i] & 15))) & 3u);
+    const int m = beta_mult(mtab, (bw[i] >> sh[i]) & 3u);
     V out;
     if constexpr (I8) {
       out = decode_tile_i8<DV>(w[i], m, q, m2q);
@@ -114,8 +129,17 @@ __device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
 // time (uniform over the workgroup).
 template <int NT = 256>
 __device__ __forceinline__ void run_tile_task(const TileTask& t, int et, int64_t wg) {
-#define NQ_TB(ET, DV) \
-  tiles_block<ET, DV, NT>(t.codes, t.beta, t.rows, t.nb, t.total, t.nb_p, t.inv_nbp, t.q, t.m2q, t.mtab, t.ws, wg)
+  // the flat instantiation for the tile kernels' 256-thread workgroups only: in the
+  // encoder's two-wave workgroups the general one measured faster (q_proj step 95.0-95.7
+  // against 97.6-98.3 us on one box), and the encoder kernel keeps one instance per type
+  const bool flat = NT == 256 && t.nb_p == t.nb && (t.nb & 15) == 0;
+#define NQ_TB(ET, DV)                                                                     \
+  if (flat)                                                                               \
+    tiles_block<ET, DV, NT, NT == 256>(t.codes, t.beta, t.rows, t.nb, t.total, t.nb_p,    \
+                                       t.inv_nbp, t.q, t.m2q, t.mtab, t.ws, wg);          \
+  else                                                                                    \
+    tiles_block<ET, DV, NT, false>(t.codes, t.beta, t.rows, t.nb, t.total, t.nb_p,        \
+                                   t.inv_nbp, t.q, t.m2q, t.mtab, t.ws, wg)
   switch (et * 3 + t.dv) {
     case 0: NQ_TB(ET_BF16, 0); break;
     case 1: NQ_TB(ET_BF16, 1); break;
