@@ -123,8 +123,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict_
     const uint32_t t = (bw[i] >> sh[i]) & 3u;
     const double sc = (double)sr[i] * hbt[t];
     // X2 of the block: xs holds coordinates 0-3 and 4-7 as bytes X2 + 128 (decode_word_b8),
-    // or as four times X2, signed, for NestQuantM at q = 16 (decode_word_m16, coordinate 0
-    // apart)
+    // or X2 + 32 for NestQuantM at q = 16 (decode_word_m16, coordinate 0 apart)
     uint32_t xs[2];
     int x0 = 0;
     if constexpr (DV == 2) {
@@ -134,7 +133,7 @@ __global__ __launch_bounds__(256) void decode_kernel(const uint32_t* __restrict_
     }
     auto x2 = [&](int l) {
       if constexpr (DV == 2) {
-        return l == 0 ? x0 : (int)(int8_t)(uint8_t)(xs[l >> 2] >> (8 * (l & 3))) >> 2;
+        return l == 0 ? x0 : (int)((xs[l >> 2] >> (8 * (l & 3))) & 0xFFu) - 32;
       }
       return (int)((xs[l >> 2] >> (8 * (l & 3))) & 0xFFu) - 128;
     };

@@ -406,10 +406,10 @@ __device__ __forceinline__ void decode_word_pk(uint32_t w, int q, uint32_t m2q,
 // arithmetic and tie rules as decode_word_pk<true> at q = 16.
 //
 // Outputs: x0 = X2_0 (the flipped coordinate, |x0| <= 32) and, in xa (coordinates 0-3) and
-// xb (4-7), every coordinate before the flip as a 6-bit two's-complement field shifted to
-// the top of its byte, so that the signed byte is 4 X2_l (|X2_l| <= 16 there): the D8
-// residual f - 32 g is f | (g << 5) in 6 bits, the D8+1/2 residual f - 16 is
-// f ^ 0x30 ^ ((f & 0x10) << 1).  Only OR / XOR / shifts, no carries between bytes.
+// xb (4-7), every coordinate before the flip as the unsigned byte X2_l + 32 (|X2_l| <= 16
+// there): the D8 residual f - 32 g is f | (g << 5) as a 6-bit two's-complement field, the
+// D8+1/2 residual f - 16 is f ^ 0x30 ^ ((f & 0x10) << 1), and flipping bit 5 of such a field
+// adds 32.  Only OR / XOR / shifts, no carries between bytes.
 // ---------------------------------------------------------------------------------------
 __device__ __forceinline__ void decode_word_m16(uint32_t w, uint32_t& xa, uint32_t& xb, int& x0) {
   const uint32_t E = w & 0x0F0F0F0Fu;           // bytes c0 c2 c4 c6
@@ -437,18 +437,13 @@ __device__ __forceinline__ void decode_word_m16(uint32_t w, uint32_t& xa, uint32
   const uint32_t m = 0u - (uint32_t)d8;                       // all ones for D8
   const uint32_t ra = Fa ^ 0x30303030u ^ ((Fa & 0x10101010u) << 1);
   const uint32_t rb = Fb ^ 0x30303030u ^ ((Fb & 0x10101010u) << 1);
-  xa = (ra ^ (((Fa | (Ga << 5)) ^ ra) & m)) << 2;
-  xb = (rb ^ (((Fb | (Gb << 5)) ^ rb) & m)) << 2;
+  xa = (ra ^ (((Fa | (Ga << 5)) ^ ra) & m)) ^ 0x20202020u;
+  xb = (rb ^ (((Fb | (Gb << 5)) ^ rb) & m)) ^ 0x20202020u;
   // coordinate 0 moves by +32 s (D8) or -32 s (D8+1/2), s = 2 g0 - 1
   const bool g0 = (Ga & 1u) != 0;
   const int r0 = d8 ? (g0 ? f0 - 32 : f0) : f0 - 16;
   const bool fix = d8 ? (odd1 != 0) : (pi != 0);
   x0 = r0 + (fix ? ((g0 == d8) ? 32 : -32) : 0);
-}
-
-// Signed byte b of x as a float.
-__device__ __forceinline__ float sbyte_f32(uint32_t x, int b) {
-  return (float)(int)(int8_t)(uint8_t)(x >> (8 * b));
 }
 
 // One thread per block of a rows x nb grid of blocks, 256 threads per workgroup: rows
@@ -503,16 +498,14 @@ __device__ __forceinline__ u32x4 decode_tile_16(uint32_t w, int m, int q, uint32
     uint32_t xa, xb;
     int x0;
     decode_word_m16(w, xa, xb, x0);
-    const float tq = 0.25f * (float)m;    // bytes hold 4 X2 (exact)
-    uint32_t o[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const uint32_t x = i < 2 ? xa : xb;
-      const float lo = i == 0 ? (float)(x0 * m) : sbyte_f32(x, 2 * (i & 1)) * tq;
-      const float hi = sbyte_f32(x, 2 * (i & 1) + 1) * tq;
-      o[i] = pack16<F16>(lo, hi);
-    }
-    return u32x4{o[0], o[1], o[2], o[3]};
+    // bytes hold X2 + 32: m X2 = b m - 32 m is one fma (both terms exact, the result an
+    // integer of at most 11 bits)
+    const float fm = (float)m, off = -32.0f * fm;
+    auto val = [&](uint32_t x, int b) {
+      return __builtin_fmaf((float)((x >> (8 * b)) & 0xFFu), fm, off);
+    };
+    return u32x4{pack16<F16>((float)(x0 * m), val(xa, 1)), pack16<F16>(val(xa, 2), val(xa, 3)),
+                 pack16<F16>(val(xb, 0), val(xb, 1)), pack16<F16>(val(xb, 2), val(xb, 3))};
   }
   uint32_t xa, xb;
   decode_word_b8<DV == 1>(w, q, m2q, xa, xb);

@@ -67,16 +67,16 @@ using CfgBig = Cfg<256, 256, 4, 2, 4, 64>;
 using CfgBigI8 = Cfg<256, 256, 4, 2, 2>;
 }  // namespace gemm
 
-// One workgroup per 256 * kTilesPerThread blocks of the tile (tiles_block).
-template <int ET, int DV, bool FLAT>
+// One workgroup per TB blocks of the tile (tiles_block).
+template <int ET, int DV, bool FLAT, int TB>
 __global__ __launch_bounds__(256) void tiles_kernel(const uint32_t* __restrict__ codes,
                                                     const uint32_t* __restrict__ beta,
                                                     int64_t rows, int nb, int64_t total,
                                                     int nb_p, float inv_nbp, int q,
                                                     uint32_t m2q, uint32_t mtab,
                                                     void* __restrict__ ws) {
-  tiles_block<ET, DV, 256, FLAT>(codes, beta, rows, nb, total, nb_p, inv_nbp, q, m2q, mtab,
-                                 ws, (int64_t)blockIdx.x);
+  tiles_block<ET, DV, 256, FLAT, TB>(codes, beta, rows, nb, total, nb_p, inv_nbp, q, m2q,
+                                     mtab, ws, (int64_t)blockIdx.x);
 }
 
 // Launch tiles_kernel for one operand with its decoder.
@@ -84,22 +84,29 @@ template <int ET>
 void launch_tiles(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void* ws,
                   hipStream_t st) {
   const int64_t total = rows_p * nb_p;
-  const int64_t wgs = tile_workgroups(total);
   const float inv = 1.0f / (float)nb_p;
   const bool flat = nb_p == nb && (nb & 15) == 0;
+  // operands too small to fill the CUs at kTilesPerThread blocks per thread (the decode of a
+  // decode-shaped activation) take one block per thread
+  const bool small = total < (int64_t)256 * 256 * kTilesPerThread;
+  const int64_t wgs = small ? (total + 255) / 256 : tile_workgroups(total);
+#define NQ_TL1(DV, F, TB)                                                                    \
+  hipLaunchKernelGGL((tiles_kernel<ET, DV, F, TB>), dim3((unsigned)wgs), dim3(256), 0, st,     \
+                     X.codes, X.beta, X.rows, nb, total, nb_p, inv, X.q, X.m2q, X.mtab, ws)
 #define NQ_TL(DV)                                                                            \
-  if (flat)                                                                                  \
-    hipLaunchKernelGGL((tiles_kernel<ET, DV, true>), dim3((unsigned)wgs), dim3(256), 0, st,    \
-                       X.codes, X.beta, X.rows, nb, total, nb_p, inv, X.q, X.m2q, X.mtab, ws); \
-  else                                                                                       \
-    hipLaunchKernelGGL((tiles_kernel<ET, DV, false>), dim3((unsigned)wgs), dim3(256), 0, st,   \
-                       X.codes, X.beta, X.rows, nb, total, nb_p, inv, X.q, X.m2q, X.mtab, ws)
+  if (small) {                                                                               \
+    if (flat) NQ_TL1(DV, true, 256); else NQ_TL1(DV, false, 256);                            \
+  } else {                                                                                   \
+    if (flat) NQ_TL1(DV, true, 256 * kTilesPerThread);                                       \
+    else NQ_TL1(DV, false, 256 * kTilesPerThread);                                           \
+  }
   switch (decoder_variant(X.decoder, X.q)) {
     case 0: NQ_TL(0); break;
     case 1: NQ_TL(1); break;
     default: NQ_TL(2); break;
   }
 #undef NQ_TL
+#undef NQ_TL1
 }
 template void launch_tiles<ET_BF16>(const MatmulOperand&, int, int64_t, int, void*, hipStream_t);
 template void launch_tiles<ET_F16>(const MatmulOperand&, int, int64_t, int, void*, hipStream_t);

@@ -41,7 +41,12 @@ void launch_tiles(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void
 // next chunk's words are loaded while the current one is decoded (two register sets in
 // turn).  The host keeps W's code array below
 // 2^31 bytes per launch.
-template <int MT, int ET, int DVW, int NWV>
+//
+// ADEC (one or two activation rows, the GEMV): each workgroup first decodes A's rows itself
+// into LDS (the same tile layout, kcb chunks per row) and reads its fragments there, so the
+// product is one launch instead of two; the extra decodes are A.rows * nbp per workgroup
+// against 16 * nb of W's.
+template <int MT, int ET, int DVW, int NWV, bool ADEC = false>
 __global__ __launch_bounds__(NWV * 64) void skinny_kernel(const u32x4* __restrict__ ta, int kcb,
                                                           MatmulOperand A, MatmulOperand W,
                                                           int nb, float* __restrict__ c,
@@ -71,6 +76,36 @@ __global__ __launch_bounds__(NWV * 64) void skinny_kernel(const u32x4* __restric
 
   // chunks of CB blocks; wave w takes a contiguous share of them
   const int nbp = kcb * 16 / (I8 ? 8 : 16);            // padded blocks per row of the A tile
+  extern __shared__ __attribute__((aligned(16))) unsigned char alds[];   // ADEC: A's tile
+  if constexpr (ADEC) {
+    // A's blocks (padding columns read as the zero word, which decodes to zero)
+    const int nbwa = (nb + 15) >> 4;
+    const int na = (int)A.rows * nbp;
+    const int dva = decoder_variant(A.decoder, A.q);
+    for (int b = threadIdx.x; b < na; b += NWV * 64) {
+      const int r = b >= nbp ? 1 : 0;                   // A.rows <= 2
+      const int j = b - r * nbp;
+      uint32_t wd = 0u, bw = 0u;
+      if (j < nb) {
+        wd = A.codes[(int64_t)r * nb + j];
+        bw = A.beta[(int64_t)r * nbwa + (j >> 4)];
+      }
+      const int ma = beta_mult(A.mtab, (bw >> (2 * (j & 15))) & 3u);
+      if constexpr (I8) {
+        const u32x2 v = dva == 0 ? decode_tile_i8<0>(wd, ma, A.q, A.m2q)
+                                 : (dva == 1 ? decode_tile_i8<1>(wd, ma, A.q, A.m2q)
+                                             : decode_tile_i8<2>(wd, ma, A.q, A.m2q));
+        *reinterpret_cast<u32x2*>(alds + r * kcb * 16 + j * 8) = v;
+      } else {
+        constexpr bool F16 = ET == ET_F16;
+        const u32x4 v = dva == 0 ? decode_tile_16<0, F16>(wd, ma, A.q, A.m2q)
+                                 : (dva == 1 ? decode_tile_16<1, F16>(wd, ma, A.q, A.m2q)
+                                             : decode_tile_16<2, F16>(wd, ma, A.q, A.m2q));
+        *reinterpret_cast<u32x4*>(alds + (r * kcb + j) * 16) = v;
+      }
+    }
+    __syncthreads();
+  }
   const int nch = (nbp + CB - 1) / CB;
   const int c0 = (int)((int64_t)nch * wave / NWV), c1 = (int)((int64_t)nch * (wave + 1) / NWV);
 
@@ -116,9 +151,14 @@ __global__ __launch_bounds__(NWV * 64) void skinny_kernel(const u32x4* __restric
       for (int i = 0; i < PD; ++i) {
         const int blk = blk0 + i * BPL;
         const uint32_t off = (uint32_t)((16 * m + col) * kcb + blk / BPL) * 16u;
-        af[i][m] = row_ok && blk < nbp
-                       ? __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, off, 0, 0))
-                       : u32x4{0u, 0u, 0u, 0u};
+        if constexpr (ADEC) {
+          af[i][m] = row_ok && blk < nbp ? *reinterpret_cast<const u32x4*>(alds + off)
+                                         : u32x4{0u, 0u, 0u, 0u};
+        } else {
+          af[i][m] = row_ok && blk < nbp
+                         ? __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(ra, off, 0, 0))
+                         : u32x4{0u, 0u, 0u, 0u};
+        }
       }
     }
   };
@@ -198,9 +238,19 @@ __global__ __launch_bounds__(NWV * 64) void skinny_kernel(const u32x4* __restric
 template <int ET>
 static hipError_t skinny_launch(const MatmulOperand& A, const MatmulOperand& W, const u32x4* ta,
                                 int kcb, int nb, float* c, int64_t ldc, float scale,
-                                hipStream_t st) {
+                                bool adec, hipStream_t st) {
   const int64_t mp = (A.rows + 15) / 16 * 16;
   const unsigned grid = (unsigned)((W.rows + 15) / 16);
+  if (adec) {
+    const size_t lds = (size_t)A.rows * kcb * 16;
+#define NQ_SKA(DV)                                                                             \
+  hipLaunchKernelGGL((skinny_kernel<1, ET, DV, 8, true>), dim3(grid), dim3(512), lds, st, ta,  \
+                     kcb, A, W, nb, c, ldc, scale)
+    const int dv = decoder_variant(W.decoder, W.q);
+    if (dv == 0) NQ_SKA(0); else if (dv == 1) NQ_SKA(1); else NQ_SKA(2);
+#undef NQ_SKA
+    return hipGetLastError();
+  }
 #define NQ_SK(MT, DV)                                                                     \
   hipLaunchKernelGGL((skinny_kernel<MT, ET, DV, 8>), dim3(grid), dim3(512), 0, st, ta, kcb, A, \
                      W, nb, c, ldc, scale)
@@ -228,7 +278,10 @@ static hipError_t skinny(int stages, const MatmulOperand& A, const MatmulOperand
   const int nbp = (int)(kp / 8);
   const int kcb = (int)(kp * EB / 16);
   u32x4* ta = reinterpret_cast<u32x4*>(ws);
-  if (stages & 1) launch_tiles<ET>(A, nb, mp, nbp, (void*)ta, st);
+  // one or two activation rows whose tile fits 48 KiB of LDS: the product kernel decodes
+  // them itself (no decode stage of its own)
+  const bool adec = A.rows <= 2 && A.rows * (int64_t)kcb * 16 <= 49152;
+  if ((stages & 1) && !adec) launch_tiles<ET>(A, nb, mp, nbp, (void*)ta, st);
   if (!(stages & 2)) return hipGetLastError();
   // W in column ranges whose code words stay below 2^31 bytes (buffer-load offsets)
   const int64_t max_rows = (((int64_t)1 << 31) - 1) / ((int64_t)nb * 4) / 16 * 16;
@@ -239,7 +292,7 @@ static hipError_t skinny(int stages, const MatmulOperand& A, const MatmulOperand
     Wc.beta = W.beta + r0 * ((nb + 15) / 16);
     Wc.scales = W.scales + r0;
     Wc.rows = rows;
-    const hipError_t e = skinny_launch<ET>(A, Wc, ta, kcb, nb, c + r0, ldc, scale, st);
+    const hipError_t e = skinny_launch<ET>(A, Wc, ta, kcb, nb, c + r0, ldc, scale, adec, st);
     if (e != hipSuccess) return e;
   }
   return hipGetLastError();

@@ -22,20 +22,30 @@ namespace nq {
 // decoding any, which keeps TPB loads in flight per thread.
 // FLAT: no padding columns (nb_p == nb) and nb a multiple of 16, so that the code words
 // and beta words of a workgroup's blocks are consecutive and no block needs its (row,
-// column); run_tile_task picks it at run time.
-template <int ET, int DV, int NT = 256, bool FLAT = false>
+// column); run_tile_task picks it at run time.  TB: blocks per workgroup (256 per thread
+// group of NT; a small operand takes one block per thread, in more workgroups, since its
+// launch is bound by the latency of one thread's chain of decodes).
+template <int ET, int DV, int NT = 256, bool FLAT = false, int TB = 256 * kTilesPerThread>
 __device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
                                             const uint32_t* __restrict__ beta, int64_t rows,
                                             int nb, int64_t total, int nb_p, float inv_nbp,
                                             int q, uint32_t m2q, uint32_t mtab,
                                             void* __restrict__ ws, int64_t wg) {
   constexpr bool I8 = ET == ET_I8;
-  constexpr int TB = 256 * kTilesPerThread;   // blocks per workgroup
   constexpr int TPB = TB / NT;                // blocks per thread
   static_assert(TPB * NT == TB, "NT divides the workgroup's blocks");
   constexpr uint32_t OOB = 0x80000000u;   // past every buffer range below: reads 0
   using V = typename std::conditional<I8, u32x2, u32x4>::type;
   const int64_t g0 = wg * TB;
+  if (g0 >= rows * (int64_t)nb_p) {
+    // a workgroup of padding rows only (past the operand): zero tiles, nothing to read
+#pragma unroll
+    for (int i = 0; i < TPB; ++i) {
+      const int64_t g = g0 + (int)threadIdx.x + NT * i;
+      if (g < total) reinterpret_cast<V*>(ws)[g] = V{};
+    }
+    return;
+  }
   // the workgroup's first block as (row0, j0); every other block is an offset
   // o < nb_p + TB <= 2^14 past (row0, 0).  Code and beta words are read through buffer
   // resources based at row0 (32-bit offsets; the range check makes rows past the operand

@@ -233,6 +233,10 @@ MATMUL_CASES = [
     (7, 33, 65, 64, 14, 14, 1),
     (8, 20, 50, 264, 14, 16, 3),
     (9, 48, 1000, 4096, 14, 14, 4),
+    # one or two activation rows: the product kernel decodes A into LDS itself
+    (10, 1, 300, 1032, 14, 14, 4),
+    (11, 2, 129, 4096, 16, 7, 4),
+    (12, 2, 64, 264, 7, 14, 2),
 ]
 
 
@@ -478,6 +482,8 @@ M_MATMUL_CASES = [
     (52, 200, 130, 520, 16, 4, False),
     (53, 130, 70, 264, 14, 4, True),
     (54, 40, 500, 1032, 15, 4, True),
+    (55, 2, 260, 2048, 16, 4, False),
+    (56, 1, 100, 1032, 14, 4, True),
 ]
 
 
@@ -722,6 +728,8 @@ MULT_MATMUL_CASES = [
     (66, 64, 256, 512, 16, 16, (6, 8, 10, 15), (6, 8, 10, 15), False, "m"),        # fp16, bytes
     (67, 300, 130, 264, 16, 16, (6, 8, 10, 15), (3, 4, 5, 7), False, "m"),         # fp16
     (68, 33, 100, 1024, 10, 10, (2, 5, 6), (3, 6), True, "m"),                     # int8
+    (69, 1, 200, 1032, 16, 16, (5, 7, 11, 50), (6, 8, 10, 15), False, "full"),     # fp16, M = 1
+    (70, 2, 70, 264, 16, 16, (6, 8, 10, 15), (3, 4, 5, 7), False, "m"),            # fp16, M = 2
 ]
 
 
