@@ -62,6 +62,10 @@ FUSED_CASES = [
     (19, 129, 100, 14336, "bf16", "t4", 14, 4, None, 0, 0, True),
     # more than 1024 rows of 257..512 blocks: two-wave encoder workgroups carry W's decode
     (20, 1100, 96, 4096, "bf16", "t4", 14, 4, None, 0, 0, False),
+    # one or two activation rows: the product kernel decodes A's codes into LDS itself
+    (21, 1, 300, 4104, "bf16", "t4", 16, 4, None, 1, 0, False),
+    (22, 2, 130, 2048, "bf16", "normal", 14, 4, None, 0, 0, True),
+    (23, 1, 64, 1032, "bf16", "t4", 16, 4, (6, 8, 10, 15), 0, 0, False),
 ]
 
 
