@@ -12,7 +12,7 @@
 
 namespace nq {
 
-constexpr int kDecodePerThread = 4;
+constexpr int kDecodePerThread = 8;
 
 // One select chain instead of an indexed read of the argument block (which would be a
 // dependent memory load after the beta word arrives).
