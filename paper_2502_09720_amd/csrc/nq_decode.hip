@@ -14,8 +14,8 @@ namespace nq {
 
 constexpr int kDecodePerThread = 8;
 
-// One select chain instead of an indexed read of the argument block (which would be a
-// dependent memory load after the beta word arrives).
+// The half-beta of index t from the kernel arguments (threads 0-3 copy the four into LDS,
+// which the blocks then index).
 __device__ __forceinline__ double pick_half_beta(const DecodeArgs& a, uint32_t t) {
   return t == 0 ? a.half_beta[0] : (t == 1 ? a.half_beta[1] : (t == 2 ? a.half_beta[2] : a.half_beta[3]));
 }

@@ -14,17 +14,16 @@ namespace nq {
 
 // m * X2 of every block of a coded operand into ws[rows_p][nb_p blocks] (zero padding): 8
 // bf16 or fp16 (16 B) per block, or 8 int8 (8 B) for the int8 contraction.  The workspace
-// is one flat array of rows_p * nb_p blocks; workgroup w covers TB = 256 * kTilesPerThread
-// consecutive blocks of it with NT threads, thread t the blocks w TB + t + NT i (i < TPB =
-// TB / NT), so each load and store instruction of a wave touches consecutive blocks.  A
-// thread splits its first block's position into (row, column) once and steps the split by
-// NT blocks for the next ones.  Every thread issues the loads of all its blocks before
-// decoding any, which keeps TPB loads in flight per thread.
+// is one flat array of rows_p * nb_p blocks; workgroup w covers TB consecutive blocks of it
+// with NT threads, thread t the blocks w TB + t + NT i (i < TPB = TB / NT), so each load
+// and store instruction of a wave touches consecutive blocks.  A thread splits its first
+// block's position into (row, column) once and steps the split by NT blocks for the next
+// ones.  Every thread issues the loads of all its blocks before decoding any, which keeps
+// TPB loads in flight per thread.  TB is 256 * kTilesPerThread, or 256 for an operand too
+// small to fill the CUs (its launch is bound by the latency of one thread's decodes).
 // FLAT: no padding columns (nb_p == nb) and nb a multiple of 16, so that the code words
 // and beta words of a workgroup's blocks are consecutive and no block needs its (row,
-// column); run_tile_task picks it at run time.  TB: blocks per workgroup (256 per thread
-// group of NT; a small operand takes one block per thread, in more workgroups, since its
-// launch is bound by the latency of one thread's chain of decodes).
+// column); the callers pick it at run time.
 template <int ET, int DV, int NT = 256, bool FLAT = false, int TB = 256 * kTilesPerThread>
 __device__ __forceinline__ void tiles_block(const uint32_t* __restrict__ codes,
                                             const uint32_t* __restrict__ beta, int64_t rows,
