@@ -2,8 +2,8 @@
 // code word, four coordinates per 32-bit register (byte SIMD), for every q <= 16.  Included
 // by nq_device.hpp inside namespace nq (it needs u16x2 and the amdgcn byte builtins).
 //
-// Same arithmetic and tie rules as decode_word_pk: X = G c, then X - q * 2 Q(X / 2q) in exact
-// integers, every distance times 2q.  Why bytes suffice:
+// The arithmetic and tie rules of Alg. 5 (nq_device.hpp): X = G c, then X - q * 2 Q(X / 2q)
+// in exact integers, every distance times 2q.  Why bytes suffice:
 //   * every X = G c fits a byte: X4 = c0 + 4 c1 + 2 (c2 + ... + c7) <= 255 and the others
 //     are below 3q <= 48;
 //   * f = X mod 2q and d = floor(X / 2q) (in {0, 1} except for X4): with 128 - 2q added to

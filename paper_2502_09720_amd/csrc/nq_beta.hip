@@ -41,17 +41,18 @@ __global__ __launch_bounds__(256) void beta_stats_kernel(const float* __restrict
   int P[8];
   nearest_e8(y, P);
   const uint32_t w = encode_codes(P, q, rq, mq);
-  uint32_t X2p[4];
+  // the byte decoder: X2_l + 128 in byte l of xs (every X2 of a code word fits a byte)
+  uint32_t xs[2];
   if (decoder) {
-    decode_word_pk<true>(w, q, m2q, X2p);
+    decode_word_b8<true>(w, q, m2q, xs[0], xs[1]);
   } else {
-    decode_word_pk<false>(w, q, m2q, X2p);
+    decode_word_b8<false>(w, q, m2q, xs[0], xs[1]);
   }
   bool over = false;
   double err = 0.0;
 #pragma unroll
   for (int l = 0; l < 8; ++l) {
-    const int x2 = (int)(short)((X2p[l >> 1] >> (16 * (l & 1))) & 0xFFFFu);
+    const int x2 = (int)((xs[l >> 2] >> (8 * (l & 3))) & 0xFFu) - 128;
     over |= x2 != P[l];
     const double d = beta * (double)x2 / 2.0 - (double)x[l];
     err = err + d * d;

@@ -274,12 +274,11 @@ __device__ __forceinline__ uint32_t encode_codes(const int (&P)[8], int q, float
 }
 
 // ---------------------------------------------------------------------------------------
-// Alg. 2 on one code word with two coordinates per 32-bit register (packed 16-bit integer
-// instructions): X = G c, then X - q * 2 Q(X / 2q) in exact integers (all distances times
-// 2q), Q = Alg. 5 with the tie rules of nearest_e8, or (M) the NestQuantM oracle of App. D,
-// whose parity fixes are at the first coordinate (no argmin / argmax).  Output X2 as four
-// packed int16 pairs (coordinates 2i, 2i+1 in the low and high halves of word i).
-// m2q = ceil(2^16 / (2q)) gives floor(X / 2q) = (X * m2q) >> 16 exactly for 0 <= X < 2^11.
+// Alg. 2 on one code word, four coordinates per 32-bit register (byte SIMD, nq_b8.hpp):
+// X = G c, then X - q * 2 Q(X / 2q) in exact integers (all distances times 2q), Q = Alg. 5
+// with the tie rules of nearest_e8, or (M) the NestQuantM oracle of App. D, whose parity
+// fixes are at the first coordinate (no argmin / argmax).  m2q = ceil(2^16 / (2q)) gives
+// floor(X / 2q) = (X * m2q) >> 16 exactly for 0 <= X < 2^11.
 //
 // Shifting X by 2q * v with v in D8 leaves the decode unchanged (Alg. 5 commutes with D8
 // shifts), so only f = X mod 2q per coordinate and the parity pi of sum floor(X / 2q)
@@ -289,121 +288,15 @@ __device__ __forceinline__ uint32_t encode_codes(const int (&P)[8], int q, float
 //   4q - sum |h| + odd1 * 2 min|h| - pi * (2q - 2 max|h|),   odd1 = (pi + #[h > 0]) mod 2.
 // ---------------------------------------------------------------------------------------
 typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
-typedef short i16x2 __attribute__((ext_vector_type(2)));
-
-__device__ __forceinline__ u16x2 as_u16x2(uint32_t v) { return __builtin_bit_cast(u16x2, v); }
-__device__ __forceinline__ i16x2 as_i16x2(uint32_t v) { return __builtin_bit_cast(i16x2, v); }
-__device__ __forceinline__ uint32_t bits32(u16x2 v) { return __builtin_bit_cast(uint32_t, v); }
-__device__ __forceinline__ uint32_t bits32(i16x2 v) { return __builtin_bit_cast(uint32_t, v); }
 
 #include "nq_b8.hpp"
-
-template <bool M = false>
-__device__ __forceinline__ void decode_word_pk(uint32_t w, int q, uint32_t m2q,
-                                               uint32_t (&X2)[4]) {
-  const uint32_t E = w & 0x0F0F0F0Fu;         // bytes c0 c2 c4 c6
-  const uint32_t O = (w >> 4) & 0x0F0F0F0Fu;  // bytes c1 c3 c5 c7
-  // v_perm_b32 selectors (byte 0x0c reads as zero): pairs as 16-bit lanes
-  const u16x2 cc = as_u16x2(__builtin_amdgcn_perm(0u, E, 0x0C000C00u));   // (c0, c0)
-  const u16x2 p02 = as_u16x2(__builtin_amdgcn_perm(0u, E, 0x0C010C0Cu));  // (0, c2)
-  const u16x2 p46 = as_u16x2(__builtin_amdgcn_perm(0u, E, 0x0C030C02u));  // (c4, c6)
-  const u16x2 p13 = as_u16x2(__builtin_amdgcn_perm(0u, O, 0x0C010C00u));  // (c1, c3)
-  const u16x2 p57 = as_u16x2(__builtin_amdgcn_perm(0u, O, 0x0C030C02u));  // (c5, c7)
-  const u16x2 two = {2, 2};
-  const uint32_t sum_c = __builtin_amdgcn_sad_u8(E, 0u, __builtin_amdgcn_sad_u8(O, 0u, 0u));
-  const uint32_t c0 = E & 0xFFu;
-  // X = G c: X1 = c0 + 2 c2, X2/X3 = c0 + 2 (c4, c6), X5 = c0 + 2 c3, X6/X7 = c0 + 2 (c5, c7),
-  // X4 = c0 + 4 c1 + 2 (c2 + ... + c7) = (c0 + 2 c1) + 2 (sum c - c0)
-  uint32_t R[4];
-  R[0] = bits32(cc + p02 * two);
-  R[1] = bits32(cc + p46 * two);
-  R[2] = bits32(cc + p13 * two) + 2u * (sum_c - c0);  // low half stays below 2^16
-  R[3] = bits32(cc + p57 * two);
-  const uint32_t den = 2u * (uint32_t)q;
-  const u16x2 den2 = {(unsigned short)den, (unsigned short)den};
-  const u16x2 qq = {(unsigned short)q, (unsigned short)q};
-  // f = X mod 2q: X < 3q for every coordinate but X4, so one conditional subtraction
-  uint32_t m[4], f[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const u16x2 x = as_u16x2(R[i]);
-    const u16x2 xm = x - den2;                  // wraps when X < 2q
-    m[i] = bits32(xm);
-    f[i] = bits32(__builtin_elementwise_min(x, xm));
-  }
-  const uint32_t X4 = R[2] & 0xFFFFu;
-  const uint32_t d4 = __umul24(X4, m2q) >> 16;
-  const uint32_t f4 = X4 - __umul24(d4, den);
-  f[2] = (f[2] & 0xFFFF0000u) | f4;
-  // parity of sum floor(X / 2q): bit 15 of each (X - 2q) lane is set iff X < 2q
-  const uint32_t lt = (m[0] & 0x80008000u) | ((m[1] & 0x80008000u) >> 1) |
-                      ((m[2] & 0x80000000u) >> 2) | ((m[3] & 0x80008000u) >> 3);
-  const uint32_t pi = (1u + __builtin_popcount(lt) + d4) & 1u;   // (7 - #lt + d4) mod 2
-  // h = f - q, |h|, g = [h > 0] (sign bit of -h)
-  uint32_t h[4], neg[4], ah[4];
-  uint32_t sum_ah = 0;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const i16x2 hh = as_i16x2(bits32(as_u16x2(f[i]) - qq));
-    const i16x2 nn = -hh;
-    h[i] = bits32(hh);
-    neg[i] = bits32(nn);
-    ah[i] = bits32(__builtin_elementwise_max(hh, nn));
-    sum_ah = __builtin_amdgcn_sad_u16(f[i], bits32(qq), sum_ah);
-  }
-  const uint32_t gb = (neg[0] & 0x80008000u) | ((neg[1] & 0x80008000u) >> 1) |
-                      ((neg[2] & 0x80008000u) >> 2) | ((neg[3] & 0x80008000u) >> 3);
-  const uint32_t odd1 = (pi + __builtin_popcount(gb)) & 1u;
-  int p = 0, r = 0, minh, maxh;
-  if constexpr (M) {
-    minh = maxh = (int)(short)(ah[0] & 0xFFFFu);       // both fixes at coordinate 0
-  } else {
-    // keys |h| * 8 + index (min: argmin |h|, lowest index) and |h| * 8 + 7 - index (max)
-    const uint32_t kidx_min[4] = {0x00010000u, 0x00030002u, 0x00050004u, 0x00070006u};
-    const uint32_t kidx_max[4] = {0x00060007u, 0x00040005u, 0x00020003u, 0x00000001u};
-    const u16x2 eight = {8, 8};
-    u16x2 kmin2 = as_u16x2(ah[0]) * eight + as_u16x2(kidx_min[0]);
-    u16x2 kmax2 = as_u16x2(ah[0]) * eight + as_u16x2(kidx_max[0]);
-#pragma unroll
-    for (int i = 1; i < 4; ++i) {
-      kmin2 = __builtin_elementwise_min(kmin2, as_u16x2(ah[i]) * eight + as_u16x2(kidx_min[i]));
-      kmax2 = __builtin_elementwise_max(kmax2, as_u16x2(ah[i]) * eight + as_u16x2(kidx_max[i]));
-    }
-    const uint32_t kmin = min((uint32_t)kmin2.x, (uint32_t)kmin2.y);
-    const uint32_t kmax = max((uint32_t)kmax2.x, (uint32_t)kmax2.y);
-    p = (int)(kmin & 7u);
-    r = 7 - (int)(kmax & 7u);
-    minh = (int)(kmin >> 3);
-    maxh = (int)(kmax >> 3);
-  }
-  const int gap = 4 * q - (int)sum_ah + (odd1 ? 2 * minh : 0) - (pi ? 2 * q - 2 * maxh : 0);
-  const bool d8 = gap < 0;
-  // residuals: D8 c = f - 2q g, D8+1/2 h
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const u16x2 g2 = as_u16x2(neg[i]) >> (u16x2){15, 15};
-    const uint32_t c = bits32(as_u16x2(f[i]) - g2 * den2);
-    X2[i] = d8 ? c : h[i];
-  }
-  // the fixed coordinate moves by +-2q: D8 by +2q s, D8+1/2 by -2q s, s = 2 g - 1
-  const int idx = d8 ? p : r;
-  const bool fix = d8 ? (odd1 != 0) : (pi != 0);
-  const int pos = (idx & 1) ? 31 - (idx >> 1) : 15 - (idx >> 1);
-  const bool gi = ((gb >> pos) & 1u) != 0;
-  const int delta = fix ? ((gi == d8) ? (int)den : -(int)den) : 0;
-  const uint32_t dl = ((uint32_t)delta & 0xFFFFu) << (16 * (idx & 1));
-  const int word = idx >> 1;
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-    X2[i] = bits32(as_u16x2(X2[i]) + as_u16x2(word == i ? dl : 0u));
-}
 
 // ---------------------------------------------------------------------------------------
 // NestQuantM decode at q = 16 with four coordinates per register (byte SIMD).  With 2q = 32
 // every X = G c fits a byte (X4 <= 15 + 2 * 120 = 255, the others <= 45), floor(X / 32) and
 // X mod 32 are a shift and a mask per byte, sum |X mod 32 - 16| is one v_sad_u8 per four
 // coordinates, and without argmin / argmax only coordinate 0 is ever flipped.  Same
-// arithmetic and tie rules as decode_word_pk<true> at q = 16.
+// arithmetic and tie rules as decode_word_b8<true> at q = 16.
 //
 // Outputs: x0 = X2_0 (the flipped coordinate, |x0| <= 32) and, in xa (coordinates 0-3) and
 // xb (4-7), every coordinate before the flip as the unsigned byte X2_l + 32 (|X2_l| <= 16
@@ -537,7 +430,7 @@ __device__ __forceinline__ u32x2 decode_tile_i8(uint32_t w, int m, int q, uint32
 }
 
 // The decoder's residual X - q * 2 Q(X / 2q) for integer X >= 0 (< 2^11), Q = Alg. 5 or
-// (M) the NestQuantM oracle: the scalar form of decode_word_pk without the generator step.
+// (M) the NestQuantM oracle: the scalar form of decode_word_b8 without the generator step.
 // Rounding half down, round(X / 2q) = floor((X + q - 1) / 2q).
 template <bool M = false>
 __device__ __forceinline__ void residual_from_X(const int (&X)[8], int q, uint32_t m2q,

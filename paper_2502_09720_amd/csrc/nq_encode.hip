@@ -292,18 +292,19 @@ __device__ __forceinline__ void opt_block(const float (&v)[8], const float (&c)[
     int P[8];
     nearest_e8(y, P);
     const uint32_t w = encode_codes(P, a.q, a.rq, a.mq);
-    uint32_t X2[4];
+    // the byte decoder: X2_l + 128 in byte l of xs (bit-exact with the 16-bit-pair one)
+    uint32_t xs[2];
     if (a.decoder) {
-      decode_word_pk<true>(w, a.q, a.m2q, X2);
+      decode_word_b8<true>(w, a.q, a.m2q, xs[0], xs[1]);
     } else {
-      decode_word_pk<false>(w, a.q, a.m2q, X2);
+      decode_word_b8<false>(w, a.q, a.m2q, xs[0], xs[1]);
     }
     // a select chain, not an indexed read of the argument block (a memory load)
     const double bt = t == 0 ? a.beta[0] : (t == 1 ? a.beta[1] : (t == 2 ? a.beta[2] : a.beta[3]));
     double err = 0.0;
 #pragma unroll
     for (int l = 0; l < 8; ++l) {
-      const int x2 = (int)(short)((X2[l >> 1] >> (16 * (l & 1))) & 0xFFFFu);
+      const int x2 = (int)((xs[l >> 2] >> (8 * (l & 3))) & 0xFFu) - 128;
       const double d = bt * (double)x2 / 2.0 - xn[l];
       err = err + d * d;
     }
