@@ -1098,11 +1098,14 @@ static hipError_t launch_dtype(const void* x, int64_t rows, int cols, int64_t ld
   }
 #define NQ_W(L, B) return launch_w<T, L, B, TILES>(x, rows, cols, ld_x, a, codes, beta, scales, st)
 #define NQ_L(L, B) return launch_t<T, L, B, false, TILES>(x, rows, cols, ld_x, a, codes, beta, scales, st)
-  // short rows: several rows per lane group, 512 blocks per wave when there are enough rows
-  if (nb <= 8) { if (rows >= 4096) NQ_W(8, 8); NQ_W(8, 1); }
-  if (nb <= 16) { if (rows >= 2048) NQ_W(16, 8); NQ_W(16, 1); }
-  if (nb <= 32) { if (rows >= 1024) NQ_W(32, 8); NQ_W(32, 1); }
-  if (nb <= 64) { if (rows >= 512) NQ_W(64, 8); NQ_W(64, 1); }
+  // short rows: several rows per lane group, 256 blocks per wave when there are enough rows
+  // (with 512 the staged blocks took 51 KB of LDS per workgroup of fp16 rows, three
+  // workgroups per CU: the 2^21 x 128 fp16 matrix 555 against 509-511 us); rows of 33-64
+  // blocks have one row per wave, one block per lane
+  if (nb <= 8) { if (rows >= 2048) NQ_W(8, 4); NQ_W(8, 1); }
+  if (nb <= 16) { if (rows >= 1024) NQ_W(16, 4); NQ_W(16, 1); }
+  if (nb <= 32) { if (rows >= 512) NQ_W(32, 4); NQ_W(32, 1); }
+  if (nb <= 64) NQ_W(64, 1);
   if (nb <= 128) NQ_W(64, 2);
   if (nb <= 256) NQ_W(64, 4);
   // 257..512 blocks: with many rows, one row per two waves keeps the launch to a single wave

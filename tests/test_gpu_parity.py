@@ -78,6 +78,12 @@ ENCODE_CASES = [
     (16, 50, 96, "bf16", "normal", 1.0, 5, 3),
     (17, 30, 256, "f32", "normal", 1e-30, 14, 4),
     (18, 30, 256, "f32", "normal", 1e30, 12, 4),
+    # many short rows: lane groups of 8, 16 and 32 with four blocks per lane (256-block
+    # waves), and 33-64-block rows at one row per wave
+    (19, 2100, 64, "bf16", "t4", 1.0, 14, 4),
+    (20, 1030, 128, "f16", "normal", 1.0, 14, 4),
+    (21, 520, 256, "f32", "t4", 1.0, 7, 4),
+    (22, 600, 320, "bf16", "normal", 1.0, 16, 4),
 ]
 
 
