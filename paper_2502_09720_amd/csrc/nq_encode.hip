@@ -611,11 +611,12 @@ __device__ __forceinline__ float skip_threshold(double rb, int q) {
 // ROT (one row per workgroup only): the row is first rotated in LDS (rotate_rows_lds, the
 // arithmetic of nq_rotate) and the encoder reads its blocks from there, times a.rot_s.
 template <typename T, int LANES, int BPT, bool TILES, bool ROT>
-// Two-wave workgroups (LANES 128) are held to 96 VGPRs, five waves per SIMD: the fused
-// launch (W's tile decode beside the coding of A) measured 94.9-95.1 against 96.2-96.4 us
-// per q_proj step at 97 VGPRs (four waves), with no spills.
+// Workgroups of a row (LANES 128 and 256) are held to 96 VGPRs, five waves per SIMD: the
+// fused launch (W's tile decode beside the coding of A) measured 94.9-95.1 against
+// 96.2-96.4 us per q_proj step at 97 VGPRs (four waves, no spills), and the 70B MLP step
+// 976-982 against 991-997 us (two dwords of scratch in its fused instantiation).
 __global__ __launch_bounds__(LANES > 64 ? LANES : 256)
-__attribute__((amdgpu_waves_per_eu(LANES == 128 ? 5 : 1))) void encode_wave_kernel(
+__attribute__((amdgpu_waves_per_eu(LANES >= 128 ? 5 : 1))) void encode_wave_kernel(
     const T* __restrict__ x, int64_t rows, int cols, int64_t ld_x, EncodeArgs a,
     uint32_t* __restrict__ codes, uint32_t* __restrict__ beta, float* __restrict__ scales) {
   using SM = SlotMap<LANES, BPT>;
