@@ -217,6 +217,26 @@ def test_decode_parity(nq, out_dtype, q, k):
     assert not bad.any(), f"{bad.sum()} values beyond 1 ulp; worst {err.max()}"
 
 
+# Rows of a multiple of 16 blocks written without a gap take the decoder's flat addressing
+# (beta words and outputs at per-thread constant offsets): 16 blocks (rows stepped with no
+# carry), 48 and 512 blocks (with a carry), next to 33 blocks (the general path).
+@pytest.mark.parametrize("out_dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("rows,cols", [(1000, 128), (300, 384), (70, 4096), (90, 264)])
+def test_decode_parity_row_shapes(nq, out_dtype, rows, cols):
+    torch = __import__("torch")
+    from oracle import layout
+    q, k = 14, 4
+    store, x32 = workloads.random_rows(rows + cols, rows, cols, dtype="f16", dist="t4")
+    base = nestquant.default_base(q, k)
+    oc, ob, os_ = oracle_encode(x32, q, k)
+    coded = upload_coded(oc, ob, os_, rows, cols, q, k, base)
+    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[out_dtype]
+    got = decoded_to_f64(nq.decode(coded, tdt), out_dtype)
+    want = nestquant.decode_rows(layout.unpack_codes(oc), layout.unpack_beta(ob, cols // 8),
+                                 os_, q, base)
+    assert np.all(np.abs(got - want) <= ulp_in(out_dtype, want))
+
+
 def _oracle_product(A32, W32, qa, qw, k):
     ba, bw = nestquant.default_base(qa, k), nestquant.default_base(qw, k)
     ca, ta, ra = nestquant.quantize_rows(A32, qa, k)
