@@ -1,6 +1,6 @@
 // Alg. 2 (Voronoi decode, with the Gosset oracle of Alg. 5 or NestQuantM's of App. D) on one
 // code word, four coordinates per 32-bit register (byte SIMD), for every q <= 16.  Included
-// by nq_device.hpp inside namespace nq (it needs u16x2 and the amdgcn byte builtins).
+// by nq_device.hpp inside namespace nq (it needs u16x2, bcnt_add and the amdgcn byte builtins).
 //
 // The arithmetic and tie rules of Alg. 5 (nq_device.hpp): X = G c, then X - q * 2 Q(X / 2q)
 // in exact integers, every distance times 2q.  Why bytes suffice:
@@ -12,8 +12,8 @@
 //   * g = [f > q] (an exact half rounds down) is bit 7 of f + 127 - q;
 //   * the distance to the nearest integer, times 2q, is E = min(f, 2q - f) = g ? 2q - f : f
 //     (2q - f never borrows since f < 2q).  Alg. 5's D8 fix goes to argmax E and its D8+1/2
-//     fix to argmin E, lowest index on ties: keys 8 E + 7 - l (max) and 8 E + l (min) fit a
-//     byte (E <= q <= 16) and are reduced in 16-bit lanes;
+//     fix to argmin E, lowest index on ties: the keys 256 E + 7 - l (max) and 256 E + l (min)
+//     are reduced in 16-bit lanes;
 //   * the gap of Alg. 5 times 2q is sum E - 4q + odd1 (2q - 2 E_p) - odd2 2 E_r, with
 //     odd2 = sum d mod 2 (popcounts of the bit-7 masks plus floor(X4 / 2q)) and
 //     odd1 = (odd2 + #g) mod 2; D8 iff it is negative;
@@ -33,7 +33,7 @@ __device__ __forceinline__ void decode_word_b8(uint32_t w, int q, uint32_t m2q, 
   const uint32_t q2 = __builtin_amdgcn_perm(0u, den, 0x00000000u);            // 2q
   const uint32_t c1 = __builtin_amdgcn_perm(0u, 128u - den, 0x00000000u);     // 128 - 2q
   const uint32_t c2 = __builtin_amdgcn_perm(0u, 127u - (uint32_t)q, 0x00000000u);  // 127 - q
-  const uint32_t c3 = __builtin_amdgcn_perm(0u, 128u - (uint32_t)q, 0x00000000u);  // 128 - q
+  const uint32_t qb = __builtin_amdgcn_perm(0u, (uint32_t)q, 0x00000000u);         // q
 
   // X = G c: (X0..X3) = c0 + 2 (0, c2, c4, c6); (X4..X7) = c0 + 2 (c1 + sum c - c0, c3, c5, c7)
   const uint32_t E = w & 0x0F0F0F0Fu;           // bytes c0 c2 c4 c6
@@ -57,35 +57,36 @@ __device__ __forceinline__ void decode_word_b8(uint32_t w, int q, uint32_t m2q, 
   const uint32_t d4 = __umul24(X4, m2q) >> 16;         // floor(X4 / 2q), X4 < 2^11
   const uint32_t f4 = X4 - __umul24(d4, den);
   const uint32_t fB = ((kB & tB) | (~kB & Xb0)) | f4;
-  const uint32_t pis = (uint32_t)__builtin_popcount(mA) + (uint32_t)__builtin_popcount(mB) + d4;
+  const uint32_t pis = bcnt_add(mB, bcnt_add(mA, d4));
 
-  // g = [f > q]; E = g ? 2q - f : f
-  const uint32_t gA = (fA + c2) & 0x80808080u, gB = (fB + c2) & 0x80808080u;
-  const uint32_t gkA = gA - (gA >> 7), gkB = gB - (gB >> 7);
+  // g = [f > q]; E = g ? 2q - f : f.  gf is 0xFF in the bytes with g: v_perm's selectors 8-11
+  // repeat bit 7 of bytes 1 and 3 of either source, so with the sources (t, t << 8) every
+  // byte of t has its bit 7 spread over its own byte.  popcount(gf) = 8 #g.
+  const uint32_t tgA = fA + c2, tgB = fB + c2;
+  const uint32_t gfA = __builtin_amdgcn_perm(tgA, tgA << 8, 0x0B090A08u);
+  const uint32_t gfB = __builtin_amdgcn_perm(tgB, tgB << 8, 0x0B090A08u);
   const uint32_t nA = q2 - fA, nB = q2 - fB;
-  const uint32_t EA = (gkA & nA) | (~gkA & fA);
-  const uint32_t EB = (gkB & nB) | (~gkB & fB);
+  const uint32_t EA = (gfA & nA) | (~gfA & fA);
+  const uint32_t EB = (gfB & nB) | (~gfB & fB);
   const uint32_t pi = pis & 1u;
-  const uint32_t odd1 =
-      (pis + (uint32_t)__builtin_popcount(gA) + (uint32_t)__builtin_popcount(gB)) & 1u;
+  const uint32_t odd1 = (bcnt_add(gfB, bcnt_add(gfA, pis << 3)) >> 3) & 1u;
   const int sumE = (int)__builtin_amdgcn_sad_u8(EA, 0u, __builtin_amdgcn_sad_u8(EB, 0u, 0u));
 
-  int p = 0, r = 0, Ep, Er;
+  int p = 0, r = 0, Ep2, Er2;   // 2 E_p, 2 E_r
   if constexpr (M) {
-    Ep = Er = (int)(EA & 0xFFu);
+    Ep2 = Er2 = (int)((EA & 0xFFu) << 1);
   } else {
-    // byte l of a word: coordinate l (A) or 4 + l (B)
-    const uint32_t xA = (EA << 3) | 0x04050607u, xB = (EB << 3) | 0x00010203u;  // 8E + 7 - l
-    const uint32_t nA8 = (EA << 3) | 0x03020100u, nB8 = (EB << 3) | 0x07060504u;  // 8E + l
-    // 16-bit lanes (byte i of A, byte i of B) for i = 0..3
-    const u16x2 a0 = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(xB, xA, 0x0C040C00u));
-    const u16x2 a1 = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(xB, xA, 0x0C050C01u));
-    const u16x2 a2 = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(xB, xA, 0x0C060C02u));
-    const u16x2 a3 = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(xB, xA, 0x0C070C03u));
-    const u16x2 b0 = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(nB8, nA8, 0x0C040C00u));
-    const u16x2 b1 = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(nB8, nA8, 0x0C050C01u));
-    const u16x2 b2 = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(nB8, nA8, 0x0C060C02u));
-    const u16x2 b3 = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(nB8, nA8, 0x0C070C03u));
+    // 16-bit keys 256 E + 7 - l (max) and 256 E + l (min): E_l is the high byte of a lane,
+    // the index tag the low byte, taken from a constant word (tag byte i belongs to byte i)
+    const uint32_t s01 = 0x05010400u, s23 = 0x07030602u;   // lanes (byte 0, 1), (byte 2, 3)
+    const u16x2 a0 = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(EA, 0x04050607u, s01));
+    const u16x2 a1 = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(EA, 0x04050607u, s23));
+    const u16x2 a2 = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(EB, 0x00010203u, s01));
+    const u16x2 a3 = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(EB, 0x00010203u, s23));
+    const u16x2 b0 = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(EA, 0x03020100u, s01));
+    const u16x2 b1 = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(EA, 0x03020100u, s23));
+    const u16x2 b2 = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(EB, 0x07060504u, s01));
+    const u16x2 b3 = __builtin_bit_cast(u16x2, __builtin_amdgcn_perm(EB, 0x07060504u, s23));
     const u16x2 mx = __builtin_elementwise_max(__builtin_elementwise_max(a0, a1),
                                                __builtin_elementwise_max(a2, a3));
     const u16x2 mn = __builtin_elementwise_min(__builtin_elementwise_min(b0, b1),
@@ -93,30 +94,26 @@ __device__ __forceinline__ void decode_word_b8(uint32_t w, int q, uint32_t m2q, 
     const uint32_t kmax = mx.x > mx.y ? (uint32_t)mx.x : (uint32_t)mx.y;
     const uint32_t kmin = mn.x < mn.y ? (uint32_t)mn.x : (uint32_t)mn.y;
     p = 7 - (int)(kmax & 7u);
-    Ep = (int)(kmax >> 3);
+    Ep2 = (int)(kmax >> 7);   // the tag is below 128
     r = (int)(kmin & 7u);
-    Er = (int)(kmin >> 3);
+    Er2 = (int)(kmin >> 7);
   }
-  const int gap = sumE - 2 * (int)den + (odd1 ? (int)den - 2 * Ep : 0) - (pi ? 2 * Er : 0);
+  const int gap = sumE - 2 * (int)den + (odd1 ? (int)den - Ep2 : 0) - (pi ? Er2 : 0);
   const bool d8 = gap < 0;
 
-  // residuals biased by 128: D8 f - 2q g (g ? 128 - (2q - f) : 128 + f); D8+1/2 f - q + 128;
-  // chosen with a mask (both are cheap, and a branch would diverge)
+  // residuals biased by 128: D8 f - 2q g, D8+1/2 f - q, i.e. (f | 128) minus 2q in the bytes
+  // with g (D8) or minus q in every byte (D8+1/2), chosen with a mask (a branch would diverge)
   const uint32_t dm = 0u - (uint32_t)d8;               // all ones for D8
-  const uint32_t gfA = gkA + gA, gfB = gkB + gB;       // 0xFF in the bytes with g
-  const uint32_t dA = (gfA & (0x80808080u - nA)) | (~gfA & (fA | 0x80808080u));
-  const uint32_t dB = (gfB & (0x80808080u - nB)) | (~gfB & (fB | 0x80808080u));
-  const uint32_t rA = (dm & dA) | (~dm & (fA + c3));
-  const uint32_t rB = (dm & dB) | (~dm & (fB + c3));
-  // the fixed coordinate moves by +2q s (D8) or -2q s (D8+1/2), s = 2 g - 1
-  const int idx = d8 ? p : r;
-  const uint32_t fix = d8 ? odd1 : pi;
-  const int sh = 8 * (idx & 3);
-  const uint32_t gw = idx < 4 ? gA : gB;
-  const uint32_t gi = (gw >> (sh + 7)) & 1u;
-  const uint32_t dl = (0u - fix) & (den << sh);
-  const uint32_t sdl = (gi ^ (uint32_t)d8) ? 0u - dl : dl;   // +dl when g_idx == d8
-  const uint32_t lo = idx < 4 ? 0xFFFFFFFFu : 0u;
-  xa = rA + (lo & sdl);
-  xb = rB + (~lo & sdl);
+  const uint32_t rA = (fA | 0x80808080u) - (d8 ? (gfA & q2) : qb);
+  const uint32_t rB = (fB | 0x80808080u) - (d8 ? (gfB & q2) : qb);
+  // the fixed coordinate moves by 2q towards the other rounding: +2q where [g] == d8 (a D8
+  // coordinate rounded up, a D8+1/2 coordinate below its half-integer), else -2q.  With dl the
+  // move's size at its byte of the pair (xa, xb), the fixed pair is (rA, rB) - dl + 2 (dl
+  // where [g] == d8); (rA, rB) - dl stays at least 80 in every byte, so nothing borrows.
+  const uint32_t idx = (uint32_t)(d8 ? p : r);
+  const uint32_t fd = __umul24(d8 ? odd1 : pi, den);
+  const uint64_t dl = (uint64_t)fd << (8u * idx);
+  const uint32_t dlA = (uint32_t)dl, dlB = (uint32_t)(dl >> 32);
+  xa = rA - dlA + 2u * (dlA & ~(gfA ^ dm));
+  xb = rB - dlB + 2u * (dlB & ~(gfB ^ dm));
 }

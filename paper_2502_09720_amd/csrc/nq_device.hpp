@@ -234,6 +234,13 @@ __device__ __forceinline__ uint32_t pk_mul_lo_u16(uint32_t a, uint32_t b) {
   return r;
 }
 
+// popcount(x) + acc in one instruction (the compiler adds a separate popcount to acc).
+__device__ __forceinline__ uint32_t bcnt_add(uint32_t x, uint32_t acc) {
+  uint32_t r;
+  asm("v_bcnt_u32_b32 %0, %1, %2" : "=v"(r) : "v"(x), "v"(acc));
+  return r;
+}
+
 __device__ __forceinline__ uint32_t encode_codes_amax(const int (&P)[8], int q, float rq,
                                                       uint32_t mq, int amax) {
   int v[8];

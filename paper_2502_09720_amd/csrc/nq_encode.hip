@@ -614,9 +614,11 @@ template <typename T, int LANES, int BPT, bool TILES, bool ROT>
 // Workgroups of a row (LANES 128 and 256) are held to 96 VGPRs, five waves per SIMD: the
 // fused launch (W's tile decode beside the coding of A) measured 94.9-95.1 against
 // 96.2-96.4 us per q_proj step at 97 VGPRs (four waves, no spills), and the 70B MLP step
-// 976-982 against 991-997 us (two dwords of scratch in its fused instantiation).
+// 976-982 against 991-997 us (two dwords of scratch in its fused instantiation).  The
+// 64-lane instantiation with one block per thread (rows of at most 64 blocks) gets the same
+// bound: its fused instantiation fits it without scratch.
 __global__ __launch_bounds__(LANES > 64 ? LANES : 256)
-__attribute__((amdgpu_waves_per_eu(LANES >= 128 ? 5 : 1))) void encode_wave_kernel(
+__attribute__((amdgpu_waves_per_eu(LANES >= 128 || (LANES == 64 && BPT == 1) ? 5 : 1))) void encode_wave_kernel(
     const T* __restrict__ x, int64_t rows, int cols, int64_t ld_x, EncodeArgs a,
     uint32_t* __restrict__ codes, uint32_t* __restrict__ beta, float* __restrict__ scales) {
   using SM = SlotMap<LANES, BPT>;
