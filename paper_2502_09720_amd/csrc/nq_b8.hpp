@@ -29,20 +29,22 @@ template <bool M = false>
 __device__ __forceinline__ void decode_word_b8(uint32_t w, int q, uint32_t m2q, uint32_t& xa,
                                                uint32_t& xb) {
   const uint32_t den = 2u * (uint32_t)q;
-  // per-byte constants (q is uniform, so the compiler keeps them out of the block loops)
-  const uint32_t q2 = __builtin_amdgcn_perm(0u, den, 0x00000000u);            // 2q
-  const uint32_t c1 = __builtin_amdgcn_perm(0u, 128u - den, 0x00000000u);     // 128 - 2q
-  const uint32_t c2 = __builtin_amdgcn_perm(0u, 127u - (uint32_t)q, 0x00000000u);  // 127 - q
-  const uint32_t qb = __builtin_amdgcn_perm(0u, (uint32_t)q, 0x00000000u);         // q
+  // per-byte constants (q is uniform): scalar multiplies, except qb, a select operand (which
+  // must be a vector register) broadcast once by v_perm
+  const uint32_t q2 = den * 0x01010101u;                      // 2q
+  const uint32_t c1 = (128u - den) * 0x01010101u;             // 128 - 2q
+  const uint32_t c2 = (127u - (uint32_t)q) * 0x01010101u;     // 127 - q
+  const uint32_t qb = __builtin_amdgcn_perm(0u, (uint32_t)q, 0x00000000u);   // q
 
   // X = G c: (X0..X3) = c0 + 2 (0, c2, c4, c6); (X4..X7) = c0 + 2 (c1 + sum c - c0, c3, c5, c7)
   const uint32_t E = w & 0x0F0F0F0Fu;           // bytes c0 c2 c4 c6
   const uint32_t O = (w >> 4) & 0x0F0F0F0Fu;    // bytes c1 c3 c5 c7
   const uint32_t c0 = E & 0xFFu;
-  const uint32_t sum_c = __builtin_amdgcn_sad_u8(E, 0u, __builtin_amdgcn_sad_u8(O, 0u, 0u));
+  // c1 + sum c - c0, with c1 - c0 as the sums' accumulator (modulo 2^32)
+  const uint32_t x4h = __builtin_amdgcn_sad_u8(E, 0u, __builtin_amdgcn_sad_u8(O, 0u, (O & 0xFFu) - c0));
   const uint32_t c0x4 = __builtin_amdgcn_perm(0u, E, 0x00000000u);     // c0 in every byte
-  const uint32_t Xa = c0x4 + ((E & 0xFFFFFF00u) << 1);
-  const uint32_t Xb = c0x4 + (((O & 0xFFFFFF00u) | ((O & 0xFFu) + sum_c - c0)) << 1);
+  const uint32_t Xa = c0x4 + ((E ^ c0) << 1);                          // E ^ c0: byte 0 cleared
+  const uint32_t Xb = c0x4 + (((O & 0xFFFFFF00u) | x4h) << 1);
 
   // f = X mod 2q; bit 7 of (X + 128 - 2q) is [X >= 2q], and then f is its low seven bits
   const uint32_t tA = Xa + c1;
@@ -68,9 +70,11 @@ __device__ __forceinline__ void decode_word_b8(uint32_t w, int q, uint32_t m2q, 
   const uint32_t nA = q2 - fA, nB = q2 - fB;
   const uint32_t EA = (gfA & nA) | (~gfA & fA);
   const uint32_t EB = (gfB & nB) | (~gfB & fB);
-  const uint32_t pi = pis & 1u;
-  const uint32_t odd1 = (bcnt_add(gfB, bcnt_add(gfA, pis << 3)) >> 3) & 1u;
-  const int sumE = (int)__builtin_amdgcn_sad_u8(EA, 0u, __builtin_amdgcn_sad_u8(EB, 0u, 0u));
+  // parity masks (all ones when odd): odd2 = sum d mod 2, odd1 = (odd2 + #g) mod 2
+  const uint32_t pim = 0u - (pis & 1u);
+  const uint32_t o1m = 0u - ((bcnt_add(gfB, bcnt_add(gfA, pis << 3)) >> 3) & 1u);
+  // sum E - 4q (the sums' accumulator starts at -4q, modulo 2^32)
+  const int sumE4 = (int)__builtin_amdgcn_sad_u8(EA, 0u, __builtin_amdgcn_sad_u8(EB, 0u, 0u - 2u * den));
 
   int p = 0, r = 0, Ep2, Er2;   // 2 E_p, 2 E_r
   if constexpr (M) {
@@ -98,7 +102,7 @@ __device__ __forceinline__ void decode_word_b8(uint32_t w, int q, uint32_t m2q, 
     r = (int)(kmin & 7u);
     Er2 = (int)(kmin >> 7);
   }
-  const int gap = sumE - 2 * (int)den + (odd1 ? (int)den - Ep2 : 0) - (pi ? Er2 : 0);
+  const int gap = sumE4 + (int)(o1m & (den - (uint32_t)Ep2)) - (int)(pim & (uint32_t)Er2);
   const bool d8 = gap < 0;
 
   // residuals biased by 128: D8 f - 2q g, D8+1/2 f - q, i.e. (f | 128) minus 2q in the bytes
@@ -111,7 +115,7 @@ __device__ __forceinline__ void decode_word_b8(uint32_t w, int q, uint32_t m2q, 
   // move's size at its byte of the pair (xa, xb), the fixed pair is (rA, rB) - dl + 2 (dl
   // where [g] == d8); (rA, rB) - dl stays at least 80 in every byte, so nothing borrows.
   const uint32_t idx = (uint32_t)(d8 ? p : r);
-  const uint32_t fd = __umul24(d8 ? odd1 : pi, den);
+  const uint32_t fd = (d8 ? o1m : pim) & den;
   const uint64_t dl = (uint64_t)fd << (8u * idx);
   const uint32_t dlA = (uint32_t)dl, dlB = (uint32_t)(dl >> 32);
   xa = rA - dlA + 2u * (dlA & ~(gfA ^ dm));
