@@ -436,6 +436,25 @@ __device__ __forceinline__ u32x2 decode_tile_i8(uint32_t w, int m, int q, uint32
   return u32x2{mul8(xa), mul8(xb)};
 }
 
+// X2 of one block as eight int8 (|X2| <= 2q <= 32), the coordinates in byte order, with no
+// multiple applied.  The byte decoder's X2 + 128 is int8 X2 after flipping bit 7 of each
+// byte; NestQuantM's X2 + 32 (coordinate 0 put back from x0 first) becomes int8 X2 as
+// ((b | 128) - 32) ^ 128 per byte, which never borrows between bytes (b | 128 >= 128).
+template <int DV = 0>
+__device__ __forceinline__ u32x2 decode_x2_i8(uint32_t w, int q, uint32_t m2q) {
+  uint32_t xa, xb;
+  if constexpr (DV == 2) {
+    int x0;
+    decode_word_m16(w, xa, xb, x0);
+    xa = (xa & 0xFFFFFF00u) | (uint32_t)(x0 + 32);
+    return u32x2{((xa | 0x80808080u) - 0x20202020u) ^ 0x80808080u,
+                 ((xb | 0x80808080u) - 0x20202020u) ^ 0x80808080u};
+  } else {
+    decode_word_b8<DV == 1>(w, q, m2q, xa, xb);
+    return u32x2{xa ^ 0x80808080u, xb ^ 0x80808080u};
+  }
+}
+
 // The decoder's residual X - q * 2 Q(X / 2q) for integer X >= 0 (< 2^11), Q = Alg. 5 or
 // (M) the NestQuantM oracle: the scalar form of decode_word_b8 without the generator step.
 // Rounding half down, round(X / 2q) = floor((X + q - 1) / 2q).

@@ -46,7 +46,13 @@ void launch_tiles(const MatmulOperand& X, int nb, int64_t rows_p, int nb_p, void
 // into LDS (the same tile layout, kcb chunks per row) and reads its fragments there, so the
 // product is one launch instead of two; the extra decodes are A.rows * nbp per workgroup
 // against 16 * nb of W's.
-template <int MT, int ET, int DVW, int NWV, bool ADEC = false>
+//
+// DOT (with ADEC, when the sums fit 32 bits): no matrix cores.  A's rows go to LDS as int8
+// X2 with their blocks' multiples m_A beside them; a lane decodes each of its W blocks to
+// int8 X2, forms sum_l X2_W,l X2_A,l with two v_dot4_i32_i8 and adds m_W m_A times it to an
+// exact int32 sum (Alg. 4's inner product of the lattice points, times the two multiples).
+// The column's sum is the lanes' sum over the four K quarters and the waves.
+template <int MT, int ET, int DVW, int NWV, bool ADEC = false, bool DOT = false>
 __global__ __launch_bounds__(NWV * 64) void skinny_kernel(const u32x4* __restrict__ ta, int kcb,
                                                           MatmulOperand A, MatmulOperand W,
                                                           int nb, float* __restrict__ c,
@@ -91,7 +97,13 @@ __global__ __launch_bounds__(NWV * 64) void skinny_kernel(const u32x4* __restric
         bw = A.beta[(int64_t)r * nbwa + (j >> 4)];
       }
       const int ma = beta_mult(A.mtab, (bw >> (2 * (j & 15))) & 3u);
-      if constexpr (I8) {
+      if constexpr (DOT) {
+        const u32x2 v = dva == 0 ? decode_x2_i8<0>(wd, A.q, A.m2q)
+                                 : (dva == 1 ? decode_x2_i8<1>(wd, A.q, A.m2q)
+                                             : decode_x2_i8<2>(wd, A.q, A.m2q));
+        *reinterpret_cast<u32x2*>(alds + (r * nbp + j) * 8) = v;
+        alds[(int)A.rows * nbp * 8 + r * nbp + j] = (unsigned char)ma;
+      } else if constexpr (I8) {
         const u32x2 v = dva == 0 ? decode_tile_i8<0>(wd, ma, A.q, A.m2q)
                                  : (dva == 1 ? decode_tile_i8<1>(wd, ma, A.q, A.m2q)
                                              : decode_tile_i8<2>(wd, ma, A.q, A.m2q));
@@ -162,8 +174,31 @@ __global__ __launch_bounds__(NWV * 64) void skinny_kernel(const u32x4* __restric
       }
     }
   };
+  int isum[2] = {0, 0};   // DOT: the exact sums of A's rows 0 and 1
   auto compute = [&](int ch, Words& x) {
     const int blk0 = ch * CB + kg * WPL;
+    if constexpr (DOT) {
+      const int ar = (int)A.rows;
+      const unsigned char* mas = alds + ar * nbp * 8;   // m_A of each block
+#pragma unroll
+      for (int i = 0; i < PD; ++i) {
+        const int blk = blk0 + i;
+        const u32x2 xw = decode_x2_i8<DVW>(x.w[i], W.q, W.m2q);
+        const int mw = beta_mult(W.mtab, (x.b >> (2 * (blk & 15))) & 3u);
+        if (blk < nbp) {     // past the padded row: W's words read as 0, nothing to add
+#pragma unroll
+          for (int r = 0; r < 2; ++r) {
+            if (r < ar) {
+              const u32x2 xa = *reinterpret_cast<const u32x2*>(alds + (r * nbp + blk) * 8);
+              int d = __builtin_amdgcn_sdot4((int)xa.x, (int)xw.x, 0, false);
+              d = __builtin_amdgcn_sdot4((int)xa.y, (int)xw.y, d, false);
+              isum[r] += __mul24(d, __mul24(mw, (int)mas[r * nbp + blk]));
+            }
+          }
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < PD; ++i) {
       const int blk = blk0 + i * BPL;
@@ -200,15 +235,36 @@ __global__ __launch_bounds__(NWV * 64) void skinny_kernel(const u32x4* __restric
   Words x0, x1;
   load_w(c0, x0);
   for (int ch = c0; ch < c1; ch += 2) {
-    load_a(ch);                  // before the next W words: loads complete in order
+    if constexpr (!DOT) load_a(ch);   // before the next W words: loads complete in order
     load_w(ch + 1, x1);
     compute(ch, x0);
     if (ch + 1 >= c1) break;
-    load_a(ch + 1);
+    if constexpr (!DOT) load_a(ch + 1);
     load_w(ch + 2, x0);
     compute(ch + 1, x1);
   }
 
+  if constexpr (DOT) {
+    // every lane's two sums through LDS; wave 0 adds the waves', then the four K quarters
+    // (lanes col, col + 16, col + 32, col + 48), and scales once
+    __shared__ int dpart[NWV][2][64];
+    dpart[wave][0][lane] = isum[0];
+    dpart[wave][1][lane] = isum[1];
+    __syncthreads();
+    if (wave == 0) {
+      const float sw = nok ? W.scales[n] * scale : 0.0f;
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        int v = 0;
+#pragma unroll
+        for (int w = 0; w < NWV; ++w) v += dpart[w][r][lane];
+        v += __shfl_xor(v, 16);
+        v += __shfl_xor(v, 32);
+        if (kg == 0 && nok && r < A.rows) c[r * ldc + n] = (float)v * (A.scales[r] * sw);
+      }
+    }
+    return;
+  }
   if (wave > 0) {
 #pragma unroll
     for (int m = 0; m < MT; ++m) part[wave - 1][m][lane] = acc[m];
@@ -235,12 +291,33 @@ __global__ __launch_bounds__(NWV * 64) void skinny_kernel(const u32x4* __restric
   }
 }
 
+// The largest multiple m in an operand's table (its four bytes).
+static uint32_t max_mult(uint32_t t) {
+  return std::max(std::max(t & 0xFFu, (t >> 8) & 0xFFu), std::max((t >> 16) & 0xFFu, t >> 24));
+}
+
 template <int ET>
 static hipError_t skinny_launch(const MatmulOperand& A, const MatmulOperand& W, const u32x4* ta,
                                 int kcb, int nb, float* c, int64_t ldc, float scale,
                                 bool adec, hipStream_t st) {
   const int64_t mp = (A.rows + 15) / 16 * 16;
   const unsigned grid = (unsigned)((W.rows + 15) / 16);
+  // the integer-dot GEMV when a row's exact sum fits 32 bits: |X2| <= 2q per coordinate, so
+  // |sum| <= nbp * 8 * (2 q_A)(2 q_W) * max m_A * max m_W
+  const int nbp = kcb * 16 / (ET == ET_I8 ? 8 : 16);
+  const bool dot = adec && ET != ET_I8 &&
+                   (double)nbp * 8.0 * (2.0 * A.q) * (2.0 * W.q) * (double)max_mult(A.mtab) *
+                           (double)max_mult(W.mtab) < 2147483647.0;
+  if (dot) {
+    const size_t lds = (size_t)A.rows * nbp * 9;      // int8 X2 (8 bytes) + m_A per block
+#define NQ_SKD(DV)                                                                           \
+  hipLaunchKernelGGL((skinny_kernel<1, ET, DV, 8, true, true>), dim3(grid), dim3(512), lds,  \
+                     st, ta, kcb, A, W, nb, c, ldc, scale)
+    const int dv = decoder_variant(W.decoder, W.q);
+    if (dv == 0) NQ_SKD(0); else if (dv == 1) NQ_SKD(1); else NQ_SKD(2);
+#undef NQ_SKD
+    return hipGetLastError();
+  }
   if (adec) {
     const size_t lds = (size_t)A.rows * kcb * 16;
 #define NQ_SKA(DV)                                                                             \
