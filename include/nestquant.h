@@ -148,8 +148,7 @@ nq_status nq_matmul(const nq_params* pa, const uint32_t* a_codes, const uint32_t
  * (for M <= 64 the fp32 sums are taken in another order).  With M <= 2 (and A's tile within
  * 48 KiB) the product kernel decodes A itself and the workspace is unused; there, when
  * every sum fits 32 bits (8 * ceil(K / 64) * 8 * (2 q_A)(2 q_W) * max mult_A * max mult_W
- * < 2^31, e.g.
- * K <= 2^17 at q = 16 with multiples up to 4), each output's sum of
+ * < 2^31: always at q = 16 with multiples up to 4), each output's sum of
  * <m_A X2_A, m_W X2_W> is exact in int32 (int8 dot products, no matrix cores) and rounded
  * once to fp32.  The workspace is used as scratch until the call's kernels finish on
  * hip_stream. */
