@@ -437,22 +437,15 @@ __device__ __forceinline__ u32x2 decode_tile_i8(uint32_t w, int m, int q, uint32
 }
 
 // X2 of one block as eight int8 (|X2| <= 2q <= 32), the coordinates in byte order, with no
-// multiple applied.  The byte decoder's X2 + 128 is int8 X2 after flipping bit 7 of each
-// byte; NestQuantM's X2 + 32 (coordinate 0 put back from x0 first) becomes int8 X2 as
-// ((b | 128) - 32) ^ 128 per byte, which never borrows between bytes (b | 128 >= 128).
+// multiple applied: the byte decoder's X2 + 128 with bit 7 of each byte flipped.  DV 0 is
+// the full decoder, DV 1 NestQuantM (at q = 16 too: decode_word_m16's X2 + 32 would take
+// three instructions a word to int8 instead of one).
 template <int DV = 0>
 __device__ __forceinline__ u32x2 decode_x2_i8(uint32_t w, int q, uint32_t m2q) {
+  static_assert(DV == 0 || DV == 1, "the byte decoder's variants");
   uint32_t xa, xb;
-  if constexpr (DV == 2) {
-    int x0;
-    decode_word_m16(w, xa, xb, x0);
-    xa = (xa & 0xFFFFFF00u) | (uint32_t)(x0 + 32);
-    return u32x2{((xa | 0x80808080u) - 0x20202020u) ^ 0x80808080u,
-                 ((xb | 0x80808080u) - 0x20202020u) ^ 0x80808080u};
-  } else {
-    decode_word_b8<DV == 1>(w, q, m2q, xa, xb);
-    return u32x2{xa ^ 0x80808080u, xb ^ 0x80808080u};
-  }
+  decode_word_b8<DV == 1>(w, q, m2q, xa, xb);
+  return u32x2{xa ^ 0x80808080u, xb ^ 0x80808080u};
 }
 
 // The decoder's residual X - q * 2 Q(X / 2q) for integer X >= 0 (< 2^11), Q = Alg. 5 or

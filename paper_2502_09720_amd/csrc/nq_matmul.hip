@@ -98,9 +98,9 @@ __global__ __launch_bounds__(NWV * 64) void skinny_kernel(const u32x4* __restric
       }
       const int ma = beta_mult(A.mtab, (bw >> (2 * (j & 15))) & 3u);
       if constexpr (DOT) {
+        // NestQuantM at q = 16 through the byte decoder too: its int8 form is one XOR a word
         const u32x2 v = dva == 0 ? decode_x2_i8<0>(wd, A.q, A.m2q)
-                                 : (dva == 1 ? decode_x2_i8<1>(wd, A.q, A.m2q)
-                                             : decode_x2_i8<2>(wd, A.q, A.m2q));
+                                 : decode_x2_i8<1>(wd, A.q, A.m2q);
         *reinterpret_cast<u32x2*>(alds + (r * nbp + j) * 8) = v;
         alds[(int)A.rows * nbp * 8 + r * nbp + j] = (unsigned char)ma;
       } else if constexpr (I8) {
@@ -313,8 +313,10 @@ static hipError_t skinny_launch(const MatmulOperand& A, const MatmulOperand& W, 
 #define NQ_SKD(DV)                                                                           \
   hipLaunchKernelGGL((skinny_kernel<1, ET, DV, 8, true, true>), dim3(grid), dim3(512), lds,  \
                      st, ta, kcb, A, W, nb, c, ldc, scale)
+    // NestQuantM (variants 1 and 2) on the byte decoder: cheaper than decode_word_m16 here,
+    // where the int8 form costs one XOR a word against three
     const int dv = decoder_variant(W.decoder, W.q);
-    if (dv == 0) NQ_SKD(0); else if (dv == 1) NQ_SKD(1); else NQ_SKD(2);
+    if (dv == 0) NQ_SKD(0); else NQ_SKD(1);
 #undef NQ_SKD
     return hipGetLastError();
   }
