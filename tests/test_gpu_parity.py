@@ -533,6 +533,43 @@ def test_matmul_parity_nestquantm(nq, case):
     assert rel <= (1e-6 if i8 else MATMUL_RTOL), f"relative Frobenius error {rel}"
 
 
+GEMV_EXACT_CASES = [
+    # (seed, M, N, K, qa, qw, decoder): one or two activation rows, whose sums are exact int32
+    (90, 1, 300, 8192, 16, 16, "full"),
+    (91, 2, 129, 4096, 16, 7, "full"),
+    (92, 1, 200, 1032, 16, 16, "m"),
+    (93, 2, 70, 2056, 14, 14, "m"),
+]
+
+
+@pytest.mark.parametrize("case", GEMV_EXACT_CASES, ids=lambda c: f"{c[1]}x{c[2]}x{c[3]}-q{c[4]}/{c[5]}-{c[6]}")
+def test_gemv_exact_integer_sums(nq, case):
+    """With one or two activation rows each output is Alg. 4's exact integer sum, rounded
+    once to fp32 and scaled by r_A r_W base_A base_W / 4 in fp32 (the scale base_A base_W / 4,
+    r_W times it, r_A times that, and the sum times the result: five fp32 roundings in all),
+    so every element is within 6 * 2^-24 of the oracle's exact value relatively, however
+    much its sum cancels."""
+    torch = __import__("torch")
+    from oracle import layout
+    seed, M, N, K, qa, qw, dec = case
+    k = 4
+    _, A32 = workloads.random_rows(seed, M, K, dtype="bf16", dist="t4")
+    _, W32 = workloads.random_rows(seed + 1000, N, K, dtype="bf16", scale=0.02)
+    ba, bw = nestquant.default_base(qa, k), nestquant.default_base(qw, k)
+    ca, ta, ra = nestquant.quantize_rows(A32, qa, k, decoder=dec)
+    cw, tw, rw = nestquant.quantize_rows(W32, qw, k, decoder=dec)
+    C = nestquant.coded_matmul(ca, ta, ra, qa, ba, cw, tw, rw, qw, bw, dec, dec)
+    flag = 1 if dec == "m" else 0
+    a = upload_coded(layout.pack_codes(ca), layout.pack_beta(ta), ra, M, K, qa, k, ba, flag)
+    w = upload_coded(layout.pack_codes(cw), layout.pack_beta(tw), rw, N, K, qw, k, bw, flag)
+    got = nq.matmul(a, w)
+    torch.cuda.synchronize()
+    g = got.cpu().numpy().astype(np.float64)
+    err = np.abs(g - C)
+    tol = 6 * 2.0 ** -24 * np.abs(C) + 1e-38
+    assert np.all(err <= tol), f"worst relative {np.max(err / np.maximum(np.abs(C), 1e-38))}"
+
+
 # ------------------------------------------------------------------------------------------
 # Hadamard rotation (Sec. 5) and rotate-then-encode
 # ------------------------------------------------------------------------------------------
