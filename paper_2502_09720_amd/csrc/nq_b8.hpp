@@ -41,7 +41,8 @@ __device__ __forceinline__ void decode_word_b8(uint32_t w, int q, uint32_t m2q, 
   const uint32_t O = (w >> 4) & 0x0F0F0F0Fu;    // bytes c1 c3 c5 c7
   const uint32_t c0 = E & 0xFFu;
   // c1 + sum c - c0, with c1 - c0 as the sums' accumulator (modulo 2^32)
-  const uint32_t x4h = __builtin_amdgcn_sad_u8(E, 0u, __builtin_amdgcn_sad_u8(O, 0u, (O & 0xFFu) - c0));
+  const uint32_t x4h =
+      __builtin_amdgcn_sad_u8(E, 0u, __builtin_amdgcn_sad_u8(O, 0u, (O & 0xFFu) - c0));
   const uint32_t c0x4 = __builtin_amdgcn_perm(0u, E, 0x00000000u);     // c0 in every byte
   const uint32_t Xa = c0x4 + ((E ^ c0) << 1);                          // E ^ c0: byte 0 cleared
   const uint32_t Xb = c0x4 + (((O & 0xFFFFFF00u) | x4h) << 1);
@@ -74,7 +75,8 @@ __device__ __forceinline__ void decode_word_b8(uint32_t w, int q, uint32_t m2q, 
   const uint32_t pim = 0u - (pis & 1u);
   const uint32_t o1m = 0u - ((bcnt_add(gfB, bcnt_add(gfA, pis << 3)) >> 3) & 1u);
   // sum E - 4q (the sums' accumulator starts at -4q, modulo 2^32)
-  const int sumE4 = (int)__builtin_amdgcn_sad_u8(EA, 0u, __builtin_amdgcn_sad_u8(EB, 0u, 0u - 2u * den));
+  const int sumE4 =
+      (int)__builtin_amdgcn_sad_u8(EA, 0u, __builtin_amdgcn_sad_u8(EB, 0u, 0u - 2u * den));
 
   int p = 0, r = 0, Ep2, Er2;   // 2 E_p, 2 E_r
   if constexpr (M) {
